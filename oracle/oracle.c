@@ -1,0 +1,221 @@
+/*
+ * CPU ORACLE for ROI-aware multi-sweep voxelisation -- TEST INFRASTRUCTURE.
+ * Plain, single-threaded, deliberately unoptimised.  See oracle.h for the
+ * definition this file follows step by step and for who may call it.
+ */
+#include "oracle.h"
+
+#include <math.h>
+#include <stdlib.h>
+#include <string.h>
+
+void oracle_make_roi(double cx, double cy, double length, double width, double yaw, double margin,
+                     oracle_roi* out) {
+  out->cx = (float)cx;
+  out->cy = (float)cy;
+  out->cos_yaw = (float)cos(yaw);
+  out->sin_yaw = (float)sin(yaw);
+  out->ext_x = (float)(0.5 * length + margin);
+  out->ext_y = (float)(0.5 * width + margin);
+  out->unused0 = 0.0f;
+  out->unused1 = 0.0f;
+}
+
+/* Sec. IV-D, Eq. 6: p' = R p + T, one fused chain per output row. */
+void oracle_compensate(const float* P, float x, float y, float z, float* o) {
+  o[0] = fmaf(P[0], x, fmaf(P[1], y, fmaf(P[2], z, P[3])));
+  o[1] = fmaf(P[4], x, fmaf(P[5], y, fmaf(P[6], z, P[7])));
+  o[2] = fmaf(P[8], x, fmaf(P[9], y, fmaf(P[10], z, P[11])));
+}
+
+/* Alg. 1 keep test against one box of ROI_L (Eq. 1), bird's-eye view only:
+ * rotate the offset from the centre into the box frame, compare with the
+ * half extents (edges inclusive). */
+int32_t oracle_inside(const oracle_roi* r, float x, float y) {
+  float dx = x - r->cx;
+  float dy = y - r->cy;
+  float s_dy = r->sin_yaw * dy;
+  float s_dx = r->sin_yaw * dx;
+  float lx = fmaf(r->cos_yaw, dx, s_dy);
+  float ly = fmaf(r->cos_yaw, dy, -s_dx);
+  return fabsf(lx) <= r->ext_x && fabsf(ly) <= r->ext_y;
+}
+
+/* Alg. 1 "Voxelize": grid coordinate of p' on each axis. */
+int32_t oracle_quantize(const oracle_grid* g, const float* p, int32_t* ijk) {
+  for (int d = 0; d < 3; ++d) {
+    float f = (p[d] - g->range_min[d]) / g->voxel_size[d];
+    if (!(f >= 0.0f && f < (float)g->dims[d])) return 0;
+    ijk[d] = (int32_t)f;
+  }
+  return 1;
+}
+
+static int bad_args(int32_t C, int64_t N, const oracle_grid* g) {
+  if (C < 3 || N < 0 || !g) return 1;
+  if (g->num_frames < 1 || g->num_sweeps < 1 || g->max_points < 1 || g->max_voxels < 1) return 1;
+  for (int d = 0; d < 3; ++d)
+    if (g->dims[d] < 1) return 1;
+  return 0;
+}
+
+/* Steps 1-4 of oracle.h for frame b, appended to (keys, idx). */
+static int64_t keep_frame(int32_t b, const float* feat, int64_t stride, const int64_t* frame_offsets,
+                          const uint8_t* sweep_ids, const float* poses, const oracle_roi* rois,
+                          const int32_t* roi_offsets, const uint8_t* budgets, const oracle_grid* g,
+                          uint64_t* keys, int64_t* idx, int64_t k) {
+  const int S = g->num_sweeps;
+  const uint64_t Dx = (uint64_t)g->dims[0], Dy = (uint64_t)g->dims[1], Dz = (uint64_t)g->dims[2];
+  for (int64_t i = frame_offsets[b]; i < frame_offsets[b + 1]; ++i) {
+    int s = sweep_ids[i];
+    if (s >= S) continue;
+    float p[3];
+    oracle_compensate(poses + ((int64_t)b * S + s) * 12, feat[i], feat[stride + i], feat[2 * stride + i], p);
+    int keep = 0;
+    for (int32_t j = roi_offsets[b]; j < roi_offsets[b + 1] && !keep; ++j)
+      if (s < budgets[j] && oracle_inside(&rois[j], p[0], p[1])) keep = 1;
+    if (!keep) continue;
+    int32_t ijk[3];
+    if (!oracle_quantize(g, p, ijk)) continue;
+    keys[k] = (((uint64_t)b * Dz + (uint64_t)ijk[2]) * Dy + (uint64_t)ijk[1]) * Dx + (uint64_t)ijk[0];
+    idx[k] = i;
+    ++k;
+  }
+  return k;
+}
+
+int64_t oracle_keep(const float* feat, int64_t stride, int32_t num_features, int64_t num_points,
+                    const int64_t* frame_offsets, const uint8_t* sweep_ids, const float* poses,
+                    const oracle_roi* rois, const int32_t* roi_offsets, const uint8_t* budgets,
+                    const oracle_grid* g, uint64_t* keys, int64_t* idx) {
+  if (bad_args(num_features, num_points, g)) return -1;
+  int64_t k = 0;
+  for (int32_t b = 0; b < g->num_frames; ++b)
+    k = keep_frame(b, feat, stride, frame_offsets, sweep_ids, poses, rois, roi_offsets, budgets, g, keys, idx,
+                   k);
+  return k;
+}
+
+typedef struct {
+  uint64_t key;
+  int64_t idx;
+} pair_t;
+
+static int cmp_pair(const void* a, const void* b) {
+  const pair_t* x = (const pair_t*)a;
+  const pair_t* y = (const pair_t*)b;
+  if (x->key != y->key) return x->key < y->key ? -1 : 1;
+  if (x->idx != y->idx) return x->idx < y->idx ? -1 : 1;
+  return 0;
+}
+
+typedef struct {
+  int64_t start; /* first pair of the voxel in sorted order */
+  int64_t run;   /* number of kept points that fell in it */
+  int64_t first; /* smallest point index in it */
+  int64_t pos;   /* position in key order */
+} voxel_t;
+
+static int cmp_first(const void* a, const void* b) {
+  const voxel_t* x = (const voxel_t*)a;
+  const voxel_t* y = (const voxel_t*)b;
+  return x->first < y->first ? -1 : (x->first > y->first ? 1 : 0);
+}
+
+static int cmp_pos(const void* a, const void* b) {
+  const voxel_t* x = (const voxel_t*)a;
+  const voxel_t* y = (const voxel_t*)b;
+  return x->pos < y->pos ? -1 : (x->pos > y->pos ? 1 : 0);
+}
+
+int64_t oracle_roi_voxelize(const float* feat, int64_t stride, int32_t C, int64_t N,
+                            const int64_t* frame_offsets, const uint8_t* sweep_ids, const float* poses,
+                            const oracle_roi* rois, const int32_t* roi_offsets, const uint8_t* budgets,
+                            const oracle_grid* g, int32_t* out_coords, int32_t* out_counts,
+                            float* out_feats, int32_t* out_point_idx, int64_t* out_voxel_offsets) {
+  if (bad_args(C, N, g)) return -1;
+  const int S = g->num_sweeps;
+  const int M = g->max_points;
+  const int64_t cap = g->max_voxels;
+  const uint64_t Dx = (uint64_t)g->dims[0], Dy = (uint64_t)g->dims[1], Dz = (uint64_t)g->dims[2];
+  int64_t total = 0;
+  out_voxel_offsets[0] = 0;
+  for (int32_t b = 0; b < g->num_frames; ++b) {
+    int64_t n_b = frame_offsets[b + 1] - frame_offsets[b];
+    uint64_t* keys = (uint64_t*)malloc(sizeof(uint64_t) * (size_t)(n_b > 0 ? n_b : 1));
+    int64_t* idx = (int64_t*)malloc(sizeof(int64_t) * (size_t)(n_b > 0 ? n_b : 1));
+    /* steps 1-4 */
+    int64_t K = keep_frame(b, feat, stride, frame_offsets, sweep_ids, poses, rois, roi_offsets, budgets, g,
+                           keys, idx, 0);
+    /* step 5: sort (key, index) */
+    pair_t* pairs = (pair_t*)malloc(sizeof(pair_t) * (size_t)(K > 0 ? K : 1));
+    for (int64_t k = 0; k < K; ++k) {
+      pairs[k].key = keys[k];
+      pairs[k].idx = idx[k];
+    }
+    qsort(pairs, (size_t)K, sizeof(pair_t), cmp_pair);
+    /* equal keys form a voxel */
+    voxel_t* vox = (voxel_t*)malloc(sizeof(voxel_t) * (size_t)(K > 0 ? K : 1));
+    int64_t V = 0;
+    for (int64_t k = 0; k < K; ++k) {
+      if (k == 0 || pairs[k].key != pairs[k - 1].key) {
+        vox[V].start = k;
+        vox[V].run = 0;
+        vox[V].first = pairs[k].idx;
+        vox[V].pos = V;
+        ++V;
+      }
+      vox[V - 1].run += 1;
+    }
+    /* step 6: per-frame voxel cap by first appearance */
+    int64_t Vout = V;
+    if (V > cap) {
+      qsort(vox, (size_t)V, sizeof(voxel_t), cmp_first);
+      Vout = cap;
+      qsort(vox, (size_t)Vout, sizeof(voxel_t), cmp_pos);
+    }
+    /* step 7: outputs and means */
+    for (int64_t v = 0; v < Vout; ++v) {
+      int64_t row = total + v;
+      const voxel_t* vx = &vox[v];
+      uint64_t key = pairs[vx->start].key;
+      uint64_t ix = key % Dx, rest = key / Dx;
+      uint64_t iy = rest % Dy;
+      rest /= Dy;
+      uint64_t iz = rest % Dz;
+      out_coords[row * 4 + 0] = b;
+      out_coords[row * 4 + 1] = (int32_t)iz;
+      out_coords[row * 4 + 2] = (int32_t)iy;
+      out_coords[row * 4 + 3] = (int32_t)ix;
+      int64_t cnt = vx->run < M ? vx->run : M;
+      out_counts[row] = (int32_t)cnt;
+      for (int m = 0; m < M; ++m)
+        out_point_idx[row * M + m] = m < cnt ? (int32_t)pairs[vx->start + m].idx : -1;
+      for (int c = 0; c < C; ++c) {
+        double sum = 0.0;
+        for (int64_t m = 0; m < cnt; ++m) {
+          int64_t i = pairs[vx->start + m].idx;
+          float val;
+          if (c < 3) {
+            float p[3];
+            int s = sweep_ids[i];
+            oracle_compensate(poses + ((int64_t)b * S + s) * 12, feat[i], feat[stride + i],
+                              feat[2 * stride + i], p);
+            val = p[c];
+          } else {
+            val = feat[(int64_t)c * stride + i];
+          }
+          sum += (double)val;
+        }
+        out_feats[row * C + c] = (float)(sum / (double)cnt);
+      }
+    }
+    total += Vout;
+    out_voxel_offsets[b + 1] = total;
+    free(vox);
+    free(pairs);
+    free(idx);
+    free(keys);
+  }
+  return total;
+}

@@ -1,0 +1,94 @@
+/*
+ * CPU ORACLE for ROI-aware multi-sweep voxelisation -- TEST INFRASTRUCTURE.
+ *
+ * Only the test-suite, the smoke check and the benchmark's CPU-baseline leg
+ * call this code.  The product path (the HIP library) never links, loads or
+ * calls it, and it shares no code, header or constant with that library.
+ *
+ * What it computes (paper: Sec. IV-D Eq. 6-7, Sec. IV-C Eq. 1, Sec. IV-F
+ * Alg. 1 with the out-of-ROI keep rate set to zero), for every frame b:
+ *   1. a point of sweep s >= num_sweeps is dropped;
+ *   2. it is moved into the current frame, p' = R_{b,s} p + T_{b,s}
+ *      (Eq. 6/7), in fp32 as the fused chain
+ *        x' = fma(R00, x, fma(R01, y, fma(R02, z, T0)))   (rows 1, 2 alike);
+ *   3. it is kept iff some ROI j of frame b admits its sweep (s < budget_j)
+ *      and contains it in bird's-eye view (Alg. 1 keep test; ROI_L of Eq. 1
+ *      read as a union of oriented boxes):
+ *        dx = x' - cx, dy = y' - cy,
+ *        lx = fma(cos, dx, sin*dy), ly = fma(cos, dy, -(sin*dx)),
+ *        |lx| <= ext_x  and  |ly| <= ext_y;
+ *   4. it is quantised (Alg. 1 "Voxelize"): f_d = (p'_d - min_d) / v_d in
+ *      fp32 (correctly rounded), kept iff 0 <= f_d < D_d on all three axes,
+ *      i_d = trunc(f_d), key = ((b*Dz + iz)*Dy + iy)*Dx + ix;
+ *   5. the kept (key, index) pairs are sorted; equal keys form a voxel, which
+ *      keeps its max_points lowest point indices;
+ *   6. a frame with more than max_voxels voxels keeps the max_voxels voxels
+ *      whose lowest point index is smallest, still listed in key order;
+ *   7. each voxel's feature c is the mean over its kept points of p'_c
+ *      (c < 3) or of the raw column c (c >= 3), summed in double in
+ *      ascending point order and rounded once to fp32 (Alg. 1 "VoxelFeature-
+ *      Encoder" read as mean pooling).
+ *
+ * Build: plain C, -O2 -ffp-contract=off, no fast-math.
+ */
+#ifndef MMBEV_ORACLE_H
+#define MMBEV_ORACLE_H
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* Oriented BEV box in the current frame: 32 bytes. */
+typedef struct {
+  float cx, cy;           /* centre [m] */
+  float cos_yaw, sin_yaw; /* rounded once from double */
+  float ext_x, ext_y;     /* half length + margin, half width + margin [m] */
+  float unused0, unused1;
+} oracle_roi;
+
+typedef struct {
+  float range_min[3];
+  float voxel_size[3];
+  int32_t dims[3]; /* Dx, Dy, Dz */
+  int32_t max_points;
+  int32_t max_voxels; /* per frame */
+  int32_t num_sweeps;
+  int32_t num_frames;
+} oracle_grid;
+
+/* ROI record from a descriptor: centre, full length and width, yaw, margin
+ * (Eq. 1 buffer r added to each half extent), all rounded once to fp32. */
+void oracle_make_roi(double cx, double cy, double length, double width, double yaw, double margin,
+                     oracle_roi* out);
+
+/* Step 2 alone: p' for one point under one 3x4 pose. */
+void oracle_compensate(const float* pose12, float x, float y, float z, float* out3);
+
+/* Step 3 alone: 1 if (x', y') lies in the ROI. */
+int32_t oracle_inside(const oracle_roi* roi, float x, float y);
+
+/* Step 4 alone: 1 and the three indices if p' lies in the grid. */
+int32_t oracle_quantize(const oracle_grid* g, const float* p3, int32_t* ijk);
+
+/* Steps 1-4 for all points: kept (key, index) pairs in index order.
+ * Returns K, or -1 on a bad argument. keys/idx must hold N entries. */
+int64_t oracle_keep(const float* feat, int64_t stride, int32_t num_features, int64_t num_points,
+                    const int64_t* frame_offsets, const uint8_t* sweep_ids, const float* poses,
+                    const oracle_roi* rois, const int32_t* roi_offsets, const uint8_t* budgets,
+                    const oracle_grid* g, uint64_t* keys, int64_t* idx);
+
+/* The whole path.  Outputs sized for num_frames * max_voxels rows:
+ * coords int32 [.][4] = (b, iz, iy, ix); counts int32 [.]; feats fp32 [.][C];
+ * point_idx int32 [.][max_points] padded with -1; voxel_offsets int64 [B+1].
+ * Returns the total number of voxels written, or -1 on a bad argument. */
+int64_t oracle_roi_voxelize(const float* feat, int64_t stride, int32_t num_features, int64_t num_points,
+                            const int64_t* frame_offsets, const uint8_t* sweep_ids, const float* poses,
+                            const oracle_roi* rois, const int32_t* roi_offsets, const uint8_t* budgets,
+                            const oracle_grid* g, int32_t* out_coords, int32_t* out_counts,
+                            float* out_feats, int32_t* out_point_idx, int64_t* out_voxel_offsets);
+
+#ifdef __cplusplus
+}
+#endif
+#endif

@@ -1,0 +1,204 @@
+/*
+ * mmbev -- ROI-aware multi-sweep LiDAR voxelisation on AMD Instinct MI355X
+ * (gfx950).  C ABI of libmmbev.so.
+ *
+ * The library implements the LiDAR half of the paper's sparse ROI-aware
+ * feature extraction (Sec. IV-F, Alg. 1 "ROIAwareVoxelization", invoked as
+ * "ROIVoxelize(ROI_L, n sweeps)" in the coordination loop of Alg. 2): every
+ * point of a multi-sweep cloud is moved into the current frame by its sweep's
+ * ego pose (Sec. IV-D, Eq. 6/7), kept only if it lies inside one of the
+ * frame's temporal ROIs (Sec. IV-C, Eq. 1, read as oriented bird's-eye-view
+ * boxes) whose sweep budget admits its sweep (Sec. IV-G budget management,
+ * read per ROI), quantised to a voxel grid, grouped by voxel, capped at
+ * max_points points per voxel and max_voxels voxels per frame ("hard
+ * voxelisation", Sec. IV-F), and mean-pooled into a sparse voxel tensor
+ * (the Voxel Feature Encoder of Alg. 1, read as mean pooling).  Points
+ * outside every ROI are dropped (Alg. 1's out-of-ROI keep rate set to zero).
+ *
+ * Exact semantics (every decision is taken in fp32 in this operation order;
+ * the library is bit-exact against this definition):
+ *   frame b of the batch holds points [points.frame_offsets[b],
+ *   points.frame_offsets[b+1]) and ROIs [rois.frame_offsets[b],
+ *   rois.frame_offsets[b+1]).  For point i of frame b with sweep s =
+ *   sweep_ids[i]:
+ *   1. s >= grid.num_sweeps: dropped.
+ *   2. P = sweep_poses + (b*num_sweeps + s)*12 (row-major [R | T]);
+ *        x' = fma(P0, x, fma(P1, y, fma(P2,  z, P3)))
+ *        y' = fma(P4, x, fma(P5, y, fma(P6,  z, P7)))
+ *        z' = fma(P8, x, fma(P9, y, fma(P10, z, P11)))
+ *   3. kept iff for some ROI j of frame b: s < roi_sweep_budget[j] and
+ *        dx = x' - cx; dy = y' - cy;
+ *        lx = fma(cos_yaw, dx, sin_yaw*dy); ly = fma(cos_yaw, dy, -(sin_yaw*dx));
+ *        |lx| <= ext_x and |ly| <= ext_y            (products rounded to fp32)
+ *   4. f_d = (p'_d - range_min[d]) / voxel_size[d]  (IEEE fp32, correctly rounded);
+ *      kept iff 0 <= f_d < dims[d] for d = x, y, z (NaN fails); i_d = trunc(f_d).
+ *      Voxel key = (b, iz, iy, ix) in lexicographic order.
+ *   5. Voxels are the distinct keys of frame b.  A voxel keeps its max_points
+ *      lowest point indices.  A frame with more than max_voxels voxels keeps
+ *      the max_voxels voxels whose lowest point index is smallest.
+ *   6. Output, per frame in ascending key order: coords (b, iz, iy, ix), the
+ *      kept count, the kept point indices ascending (padded with -1), and the
+ *      mean of each feature over the kept points -- x', y', z' for features
+ *      0..2, the raw column for features 3.. -- summed in double in ascending
+ *      point order and rounded once to fp32.
+ */
+#ifndef MMBEV_H
+#define MMBEV_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define MMBEV_ABI_VERSION 1
+
+/* ------------------------------------------------------------- status */
+typedef int32_t mmbev_status_t;
+#define MMBEV_OK 0
+#define MMBEV_ERR_INVALID_ARG (-1) /* null pointer, bad size or range */
+#define MMBEV_ERR_WORKSPACE (-2)   /* workspace missing, too small or misaligned */
+#define MMBEV_ERR_UNSUPPORTED (-3) /* sizes beyond the documented limits */
+#define MMBEV_ERR_HIP (-4)         /* a HIP call failed; no partial results */
+
+/* Device-side data faults.  The kernels never read or write out of bounds,
+ * whatever the data; when the content of a device array breaks the contract
+ * they OR one of these bits into the int32 at byte 0 of the workspace and the
+ * output is unspecified.  Read it after the stream has completed. */
+#define MMBEV_FAULT_POINT_OFFSETS 1 /* point frame offsets not 0 .. num_points, non-decreasing */
+#define MMBEV_FAULT_ROI_OFFSETS 2   /* ROI frame offsets not 0 .. num_rois, non-decreasing,
+                                       or a frame with more than max_rois_per_frame ROIs */
+#define MMBEV_FAULT_WAIT 4          /* an inter-workgroup wait exceeded its bound */
+
+/* ------------------------------------------------------------- inputs */
+
+/* Points, structure of arrays in device memory: feature c of point i is
+ * feat[c*stride + i].  Features 0..2 are x, y, z in the frame of the point's
+ * sweep [m]; features 3.. (e.g. intensity, sweep time offset) are passed
+ * through to the mean.  Frames are contiguous point ranges. */
+typedef struct {
+  const float* feat;            /* device, [num_features][stride] */
+  int64_t stride;               /* >= num_points */
+  int32_t num_features;         /* C, 3..8 */
+  int32_t reserved;             /* 0 */
+  int64_t num_points;           /* N, 0 .. 2^30-1 over all frames */
+  const int64_t* frame_offsets; /* device, [num_frames+1], 0 = off[0] <= ... <= off[B] = N */
+} mmbev_points_t;
+
+/* One temporal ROI (Eq. 1 footprint buffered by the margin r): an oriented
+ * bird's-eye-view box in the current frame, 32 bytes.  Build with
+ * mmbev_make_rois; the kernels never recompute cos/sin. */
+typedef struct {
+  float cx, cy;           /* centre [m] */
+  float cos_yaw, sin_yaw; /* box x axis = (cos_yaw, sin_yaw) */
+  float ext_x, ext_y;     /* half length + margin, half width + margin [m] */
+  float reserved[2];
+} mmbev_roi_t;
+
+/* ROIs of all frames, grouped by frame.  The order inside a frame (e.g. a
+ * criticality ranking) does not change the result. */
+typedef struct {
+  const mmbev_roi_t* boxes;     /* device, [num_rois] */
+  const int32_t* frame_offsets; /* device, [num_frames+1] */
+  int32_t num_rois;             /* >= 0 */
+  int32_t max_rois_per_frame;   /* upper bound on any frame's count, 0..1024 */
+} mmbev_rois_t;
+
+typedef struct {
+  float range_min[3];  /* grid origin x, y, z [m] */
+  float voxel_size[3]; /* > 0 [m] */
+  int32_t dims[3];     /* Dx, Dy, Dz >= 1, Dx*Dy*Dz <= 2^32 */
+  int32_t max_points;  /* M, 1..64 points kept per voxel */
+  int32_t max_voxels;  /* voxels kept per frame, >= 1 */
+  int32_t num_sweeps;  /* S, 1..255 */
+  int32_t num_frames;  /* B, 1..65535 */
+} mmbev_grid_t;
+
+/* ------------------------------------------------------------ queries */
+int32_t mmbev_abi_version(void);
+const char* mmbev_status_string(mmbev_status_t status);
+
+/* Workspace bytes mmbev_roi_voxelize needs for these sizes (0 if they are
+ * invalid).  The workspace depends only on the grid, num_points and
+ * max_rois_per_frame. */
+size_t mmbev_roi_voxelize_workspace_bytes(const mmbev_grid_t* grid, int64_t num_points,
+                                          int32_t max_rois_per_frame);
+
+/* Zero-fill a workspace on `stream` (a hipStream_t; NULL = default stream).
+ * A workspace must be initialised once before its first use; after that it
+ * is reused across calls as is. */
+mmbev_status_t mmbev_workspace_init(void* workspace, size_t workspace_bytes, void* stream);
+
+/* ------------------------------------------------------------ helpers */
+
+/* Host helper: ROI records from descriptor rows of 6 doubles (cx, cy,
+ * length, width, yaw, margin).  cos/sin are taken in double and rounded once;
+ * ext = size/2 + margin rounded once.  desc and out are host memory. */
+mmbev_status_t mmbev_make_rois(const double* desc, int64_t count, mmbev_roi_t* out);
+
+/* ------------------------------------------------------------ the path */
+
+/*
+ * Voxelise a batch of frames (semantics at the top of this file).
+ *
+ * All array arguments are device pointers; the structs themselves are host
+ * memory read during the call.  Outputs have room for
+ * num_frames * max_voxels rows:
+ *   out_coords        int32 [rows][4]   (b, iz, iy, ix)
+ *   out_counts        int32 [rows]      kept points per voxel, 1..max_points
+ *   out_feats         fp32  [rows][num_features]
+ *   out_point_idx     int32 [rows][max_points], -1 padded
+ *   out_voxel_offsets int64 [num_frames+1]; frame b's voxels are rows
+ *                     [off[b], off[b+1]) in ascending key order
+ * Rows past off[num_frames] are left untouched.
+ *
+ * sweep_ids          uint8 [num_points], 0 = the current (newest) sweep
+ * sweep_poses        fp32  [num_frames][num_sweeps][12], row-major [R | T]
+ *                    taking sweep-s coordinates into the current frame
+ * roi_sweep_budget   uint8 [num_rois]: ROI j admits sweeps s < budget[j]
+ *                    (0 disables the ROI)
+ *
+ * Ownership: the caller owns every buffer; the library allocates nothing and
+ * keeps no state between calls.  Work is enqueued on `stream` (a
+ * hipStream_t; NULL = default stream) and the call returns without waiting;
+ * results are valid once the stream has reached this point.  The workspace
+ * (size from mmbev_roi_voxelize_workspace_bytes, 256-byte aligned,
+ * initialised once by mmbev_workspace_init) must not be used by two calls
+ * that can run at the same time.
+ *
+ * Errors: argument errors are detected on the host before anything is
+ * enqueued and returned as MMBEV_ERR_*; a failed launch returns
+ * MMBEV_ERR_HIP.  Problems in the content of device arrays are reported
+ * through the fault word (MMBEV_FAULT_*).
+ */
+mmbev_status_t mmbev_roi_voxelize(const mmbev_points_t* points, const uint8_t* sweep_ids,
+                                  const float* sweep_poses, const mmbev_rois_t* rois,
+                                  const uint8_t* roi_sweep_budget, const mmbev_grid_t* grid_params,
+                                  int32_t* out_coords, int32_t* out_counts, float* out_feats,
+                                  int32_t* out_point_idx, int64_t* out_voxel_offsets, void* workspace,
+                                  size_t workspace_bytes, void* stream);
+
+/*
+ * Same call as mmbev_roi_voxelize, for measurement: before each of its
+ * kernel launches, and once after the last, it records the next of the
+ * caller's events (hipEvent_t, created with timing enabled) on `stream`, as
+ * long as events remain.  The launch order is: 0 ROI staging, 1 point filter,
+ * then one radix pass per key digit, head scan, per-frame finalisation,
+ * first-appearance preparation, one radix pass per digit of the point index,
+ * mean pooling.  Returns the number of events recorded through
+ * *events_recorded (host int32, may be NULL).  Elapsed time between events k
+ * and k+1 is the duration of launch k.
+ */
+mmbev_status_t mmbev_roi_voxelize_profiled(const mmbev_points_t* points, const uint8_t* sweep_ids,
+                                           const float* sweep_poses, const mmbev_rois_t* rois,
+                                           const uint8_t* roi_sweep_budget, const mmbev_grid_t* grid_params,
+                                           int32_t* out_coords, int32_t* out_counts, float* out_feats,
+                                           int32_t* out_point_idx, int64_t* out_voxel_offsets, void* workspace,
+                                           size_t workspace_bytes, void* stream, void* const* events,
+                                           int32_t num_events, int32_t* events_recorded);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* MMBEV_H */

@@ -1,0 +1,322 @@
+// C ABI of libmmbev: argument validation, launch configuration, workspace
+// carve-up and the stream-ordered launch sequence of one call.  No
+// allocation, no host synchronisation, no state kept between calls.
+#include <algorithm>
+#include <cmath>
+#include <cstring>
+
+#include "launch.hpp"
+
+using namespace mmbev;
+
+namespace {
+
+int bits_for(uint64_t maxval) {
+  int b = 0;
+  while (b < 64 && (maxval >> b) != 0) ++b;
+  return b;
+}
+
+size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
+
+struct Plan {
+  int64_t N;
+  int32_t B, S, C, M, cap, max_rois, W;
+  int32_t cell_shift, ncx, ncy, ncells;
+  int32_t kb, fb, key_has_frame, passes, dbits, cap_passes, cap_dbits;
+  int64_t filter_tiles, sort_tiles, scan_tiles, mean_tiles;
+  size_t off_hdr, off_cellmask, off_budgetmask, off_filter_status, off_sort_status, off_scan_status,
+      off_mean_status, off_keys0, off_vals0, off_keys1, off_vals1, off_ckeys, off_cvals, off_seg, off_voxoff,
+      off_capoff, off_keep, total;
+};
+
+mmbev_status_t make_plan(const mmbev_grid_t* g, int64_t N, int32_t max_rois, int32_t C, Plan* p) {
+  if (!g) return MMBEV_ERR_INVALID_ARG;
+  if (N < 0 || max_rois < 0) return MMBEV_ERR_INVALID_ARG;
+  if (C < 3 || C > 8) return MMBEV_ERR_INVALID_ARG;
+  for (int d = 0; d < 3; ++d) {
+    if (!std::isfinite(g->range_min[d]) || !std::isfinite(g->voxel_size[d]) || !(g->voxel_size[d] > 0.0f))
+      return MMBEV_ERR_INVALID_ARG;
+    if (g->dims[d] < 1 || g->dims[d] >= (1 << 24)) return MMBEV_ERR_INVALID_ARG;
+  }
+  if (g->max_points < 1 || g->max_points > 64) return MMBEV_ERR_INVALID_ARG;
+  if (g->max_voxels < 1) return MMBEV_ERR_INVALID_ARG;
+  if (g->num_sweeps < 1 || g->num_sweeps > 255) return MMBEV_ERR_INVALID_ARG;
+  if (g->num_frames < 1 || g->num_frames > 65535) return MMBEV_ERR_INVALID_ARG;
+  if (N >= (int64_t)1 << 30) return MMBEV_ERR_UNSUPPORTED;
+  if (max_rois > 1024) return MMBEV_ERR_UNSUPPORTED;
+  const uint64_t cells = (uint64_t)g->dims[0] * (uint64_t)g->dims[1] * (uint64_t)g->dims[2];
+  if (cells > ((uint64_t)1 << 32)) return MMBEV_ERR_UNSUPPORTED;
+  if ((uint64_t)g->num_frames * (uint64_t)g->max_voxels > (uint64_t)INT32_MAX) return MMBEV_ERR_UNSUPPORTED;
+
+  p->N = N;
+  p->B = g->num_frames;
+  p->S = g->num_sweeps;
+  p->C = C;
+  p->M = g->max_points;
+  p->cap = g->max_voxels;
+  p->max_rois = max_rois;
+  p->W = std::max(1, (max_rois + 31) / 32);
+  int cs = 0;
+  while ((((int64_t)g->dims[0] + (1 << cs) - 1) >> cs) > 128 || (((int64_t)g->dims[1] + (1 << cs) - 1) >> cs) > 128)
+    ++cs;
+  p->cell_shift = cs;
+  p->ncx = (int32_t)(((int64_t)g->dims[0] + (1 << cs) - 1) >> cs);
+  p->ncy = (int32_t)(((int64_t)g->dims[1] + (1 << cs) - 1) >> cs);
+  p->ncells = p->ncx * p->ncy;
+  p->kb = std::max(1, bits_for(cells - 1));
+  p->fb = bits_for((uint64_t)(p->B - 1));
+  const int total_bits = p->kb + p->fb;
+  p->key_has_frame = total_bits <= 32 ? 1 : 0;
+  p->passes = (total_bits + 7) / 8;
+  p->dbits = (total_bits + p->passes - 1) / p->passes;
+  const int cap_bits = std::max(1, bits_for((uint64_t)std::max<int64_t>(N - 1, 0)));
+  p->cap_passes = (cap_bits + 7) / 8;
+  p->cap_dbits = (cap_bits + p->cap_passes - 1) / p->cap_passes;
+
+  const int64_t n1 = std::max<int64_t>(N, 1);
+  p->filter_tiles = (N + kFilterTile - 1) / kFilterTile;
+  p->sort_tiles = (n1 + kSortTile - 1) / kSortTile;
+  p->scan_tiles = (n1 + kScanTile - 1) / kScanTile;
+  p->mean_tiles = (n1 + kMeanTile - 1) / kMeanTile;
+
+  size_t o = 0;
+  auto take = [&](size_t bytes) {
+    size_t at = o;
+    o = align256(o + bytes);
+    return at;
+  };
+  p->off_hdr = take(sizeof(WsHeader));
+  p->off_cellmask = take((size_t)p->B * p->ncells * p->W * 4);
+  p->off_budgetmask = take((size_t)p->B * p->S * p->W * 4);
+  p->off_filter_status = take((size_t)std::max<int64_t>(p->filter_tiles, 1) * 8);
+  p->off_sort_status = take((size_t)p->sort_tiles * kSortBins * 8);
+  p->off_scan_status = take((size_t)p->scan_tiles * 8);
+  p->off_mean_status = take((size_t)p->mean_tiles * 8);
+  p->off_keys0 = take((size_t)n1 * 4);
+  p->off_vals0 = take((size_t)n1 * 4);
+  p->off_keys1 = take((size_t)n1 * 4);
+  p->off_vals1 = take((size_t)n1 * 4);
+  p->off_ckeys = take((size_t)n1 * 4);
+  p->off_cvals = take((size_t)n1 * 4);
+  p->off_seg = take((size_t)(N + 1) * 4);
+  p->off_voxoff = take((size_t)(p->B + 1) * 4);
+  p->off_capoff = take((size_t)(p->B + 1) * 4);
+  p->off_keep = take((size_t)n1);
+  p->total = o;
+  return MMBEV_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int32_t mmbev_abi_version(void) { return MMBEV_ABI_VERSION; }
+
+const char* mmbev_status_string(mmbev_status_t s) {
+  switch (s) {
+    case MMBEV_OK: return "ok";
+    case MMBEV_ERR_INVALID_ARG: return "invalid argument";
+    case MMBEV_ERR_WORKSPACE: return "workspace missing, too small or misaligned";
+    case MMBEV_ERR_UNSUPPORTED: return "size beyond the supported limits";
+    case MMBEV_ERR_HIP: return "HIP launch failed";
+    default: return "unknown status";
+  }
+}
+
+size_t mmbev_roi_voxelize_workspace_bytes(const mmbev_grid_t* grid, int64_t num_points, int32_t max_rois_per_frame) {
+  Plan p;
+  if (make_plan(grid, num_points, max_rois_per_frame, 3, &p) != MMBEV_OK) return 0;
+  return p.total;
+}
+
+mmbev_status_t mmbev_workspace_init(void* workspace, size_t workspace_bytes, void* stream) {
+  if (!workspace || ((uintptr_t)workspace & 255)) return MMBEV_ERR_WORKSPACE;
+  if (workspace_bytes == 0) return MMBEV_OK;
+  return launch_fill_zero(workspace, workspace_bytes, (hipStream_t)stream) == hipSuccess ? MMBEV_OK
+                                                                                           : MMBEV_ERR_HIP;
+}
+
+mmbev_status_t mmbev_make_rois(const double* desc, int64_t count, mmbev_roi_t* out) {
+  if (count < 0 || (count > 0 && (!desc || !out))) return MMBEV_ERR_INVALID_ARG;
+  for (int64_t k = 0; k < count; ++k) {
+    const double* d = desc + 6 * k;
+    mmbev_roi_t r;
+    r.cx = (float)d[0];
+    r.cy = (float)d[1];
+    r.cos_yaw = (float)std::cos(d[4]);
+    r.sin_yaw = (float)std::sin(d[4]);
+    r.ext_x = (float)(0.5 * d[2] + d[5]);
+    r.ext_y = (float)(0.5 * d[3] + d[5]);
+    r.reserved[0] = 0.0f;
+    r.reserved[1] = 0.0f;
+    out[k] = r;
+  }
+  return MMBEV_OK;
+}
+
+}  // extern "C"
+
+namespace {
+
+// Records the caller's profiling events between launches (none when absent).
+struct EventTrail {
+  void* const* events = nullptr;
+  int32_t n = 0, used = 0;
+  hipError_t mark(hipStream_t s) {
+    if (used >= n) return hipSuccess;
+    return hipEventRecord((hipEvent_t)events[used++], s);
+  }
+};
+
+mmbev_status_t voxelize(const mmbev_points_t* points, const uint8_t* sweep_ids, const float* sweep_poses,
+                        const mmbev_rois_t* rois, const uint8_t* roi_sweep_budget, const mmbev_grid_t* grid,
+                        int32_t* out_coords, int32_t* out_counts, float* out_feats, int32_t* out_point_idx,
+                        int64_t* out_voxel_offsets, void* workspace, size_t workspace_bytes, void* stream,
+                        EventTrail& ev) {
+  if (!points || !rois || !grid) return MMBEV_ERR_INVALID_ARG;
+  const int64_t N = points->num_points;
+  Plan p;
+  mmbev_status_t st = make_plan(grid, N, rois->max_rois_per_frame, points->num_features, &p);
+  if (st != MMBEV_OK) return st;
+  if (points->stride < N || points->stride >= ((int64_t)1 << 40)) return MMBEV_ERR_INVALID_ARG;
+  if (N > 0 && (!points->feat || !sweep_ids)) return MMBEV_ERR_INVALID_ARG;
+  if (!points->frame_offsets || !sweep_poses || !rois->frame_offsets) return MMBEV_ERR_INVALID_ARG;
+  if (rois->num_rois < 0) return MMBEV_ERR_INVALID_ARG;
+  if (rois->num_rois > 0 && (!rois->boxes || !roi_sweep_budget)) return MMBEV_ERR_INVALID_ARG;
+  if (!out_coords || !out_counts || !out_feats || !out_point_idx || !out_voxel_offsets)
+    return MMBEV_ERR_INVALID_ARG;
+  if (!workspace || ((uintptr_t)workspace & 255) || workspace_bytes < p.total) return MMBEV_ERR_WORKSPACE;
+
+  Config c;
+  std::memset(&c, 0, sizeof(c));
+  c.feat = points->feat;
+  c.sweep = sweep_ids;
+  c.poses = sweep_poses;
+  c.frame_off = points->frame_offsets;
+  c.rois = rois->boxes;
+  c.roi_off = rois->frame_offsets;
+  c.budget = roi_sweep_budget;
+  c.stride = points->stride;
+  c.N = (int32_t)N;
+  c.C = p.C;
+  c.B = p.B;
+  c.S = p.S;
+  c.M = p.M;
+  c.cap = p.cap;
+  c.R = rois->num_rois;
+  c.max_rois = p.max_rois;
+  c.W = p.W;
+  for (int d = 0; d < 3; ++d) {
+    c.mn[d] = grid->range_min[d];
+    c.vs[d] = grid->voxel_size[d];
+    c.Df[d] = (float)grid->dims[d];
+  }
+  c.Dx = (uint32_t)grid->dims[0];
+  c.Dy = (uint32_t)grid->dims[1];
+  c.Dz = (uint32_t)grid->dims[2];
+  c.cell_shift = p.cell_shift;
+  c.ncx = p.ncx;
+  c.ncy = p.ncy;
+  c.ncells = p.ncells;
+  c.kb = p.kb;
+  c.fb = p.fb;
+  c.key_has_frame = p.key_has_frame;
+  c.passes = p.passes;
+  c.dbits = p.dbits;
+  c.cap_passes = p.cap_passes;
+  c.cap_dbits = p.cap_dbits;
+  c.vec = (((uintptr_t)points->feat & 15) == 0 && (points->stride & 3) == 0 && ((uintptr_t)sweep_ids & 3) == 0) ? 1
+                                                                                                                : 0;
+  c.out_coords = out_coords;
+  c.out_counts = out_counts;
+  c.out_feats = out_feats;
+  c.out_point_idx = out_point_idx;
+  c.out_voxel_offsets = out_voxel_offsets;
+  char* ws = (char*)workspace;
+  c.hdr = (WsHeader*)(ws + p.off_hdr);
+  c.cellmask = (uint32_t*)(ws + p.off_cellmask);
+  c.budgetmask = (uint32_t*)(ws + p.off_budgetmask);
+  c.filter_status = (uint64_t*)(ws + p.off_filter_status);
+  c.sort_status = (uint64_t*)(ws + p.off_sort_status);
+  c.scan_status = (uint64_t*)(ws + p.off_scan_status);
+  c.mean_status = (uint64_t*)(ws + p.off_mean_status);
+  c.keys[0] = (uint32_t*)(ws + p.off_keys0);
+  c.vals[0] = (uint32_t*)(ws + p.off_vals0);
+  c.keys[1] = (uint32_t*)(ws + p.off_keys1);
+  c.vals[1] = (uint32_t*)(ws + p.off_vals1);
+  c.ckeys = (uint32_t*)(ws + p.off_ckeys);
+  c.cvals = (uint32_t*)(ws + p.off_cvals);
+  c.seg_start = (uint32_t*)(ws + p.off_seg);
+  c.vox_off = (uint32_t*)(ws + p.off_voxoff);
+  c.cap_off = (uint32_t*)(ws + p.off_capoff);
+  c.keepflag = (uint8_t*)(ws + p.off_keep);
+  c.filter_tiles = (int32_t)p.filter_tiles;
+  c.sort_grid = (int32_t)std::min<int64_t>(p.sort_tiles, 1024);
+  c.scan_grid = (int32_t)std::min<int64_t>(p.scan_tiles, 1024);
+  c.mean_grid = (int32_t)std::min<int64_t>(p.mean_tiles, 2048);
+
+  hipStream_t s = (hipStream_t)stream;
+#define MMBEV_TRY(call)                                                   \
+  do {                                                                    \
+    if (ev.mark(s) != hipSuccess || (call) != hipSuccess) return MMBEV_ERR_HIP; \
+  } while (0)
+
+  MMBEV_TRY(launch_stage(c, s));
+  MMBEV_TRY(launch_filter(c, s));
+  int cur = 0;
+  for (int pass = 0; pass < c.passes; ++pass) {
+    MMBEV_TRY(launch_radix_pass(c, 0, pass, c.keys[cur], c.vals[cur], c.keys[1 - cur], c.vals[1 - cur], false, s));
+    cur = 1 - cur;
+  }
+  const uint32_t* keys = c.keys[cur];
+  const uint32_t* vals = c.vals[cur];
+  MMBEV_TRY(launch_unique(c, keys, vals, s));
+  MMBEV_TRY(launch_finalize(c, keys, vals, s));
+  // first-appearance sort of the voxels of over-cap frames (kernels exit at once when none is)
+  uint32_t* ck[2] = {c.keys[1 - cur], c.ckeys};
+  uint32_t* cv[2] = {c.vals[1 - cur], c.cvals};
+  MMBEV_TRY(launch_cap_prep(c, vals, ck[0], cv[0], s));
+  for (int pass = 0; pass < c.cap_passes; ++pass) {
+    const bool mark = pass == c.cap_passes - 1;
+    MMBEV_TRY(launch_radix_pass(c, 1, pass, ck[pass & 1], cv[pass & 1], ck[1 - (pass & 1)], cv[1 - (pass & 1)],
+                                mark, s));
+  }
+  MMBEV_TRY(launch_mean(c, keys, vals, s));
+#undef MMBEV_TRY
+  if (ev.mark(s) != hipSuccess) return MMBEV_ERR_HIP;
+  return MMBEV_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+mmbev_status_t mmbev_roi_voxelize(const mmbev_points_t* points, const uint8_t* sweep_ids, const float* sweep_poses,
+                                  const mmbev_rois_t* rois, const uint8_t* roi_sweep_budget,
+                                  const mmbev_grid_t* grid, int32_t* out_coords, int32_t* out_counts,
+                                  float* out_feats, int32_t* out_point_idx, int64_t* out_voxel_offsets,
+                                  void* workspace, size_t workspace_bytes, void* stream) {
+  EventTrail ev;
+  return voxelize(points, sweep_ids, sweep_poses, rois, roi_sweep_budget, grid, out_coords, out_counts, out_feats,
+                  out_point_idx, out_voxel_offsets, workspace, workspace_bytes, stream, ev);
+}
+
+mmbev_status_t mmbev_roi_voxelize_profiled(const mmbev_points_t* points, const uint8_t* sweep_ids,
+                                           const float* sweep_poses, const mmbev_rois_t* rois,
+                                           const uint8_t* roi_sweep_budget, const mmbev_grid_t* grid,
+                                           int32_t* out_coords, int32_t* out_counts, float* out_feats,
+                                           int32_t* out_point_idx, int64_t* out_voxel_offsets, void* workspace,
+                                           size_t workspace_bytes, void* stream, void* const* events,
+                                           int32_t num_events, int32_t* events_recorded) {
+  EventTrail ev;
+  ev.events = events;
+  ev.n = (events && num_events > 0) ? num_events : 0;
+  mmbev_status_t st = voxelize(points, sweep_ids, sweep_poses, rois, roi_sweep_budget, grid, out_coords,
+                               out_counts, out_feats, out_point_idx, out_voxel_offsets, workspace, workspace_bytes,
+                               stream, ev);
+  if (events_recorded) *events_recorded = ev.used;
+  return st;
+}
+
+}  // extern "C"

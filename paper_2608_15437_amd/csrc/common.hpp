@@ -1,0 +1,226 @@
+// Shared definitions of the gfx950 voxelisation path: the launch
+// configuration computed on the host, the workspace layout, and the pinned
+// per-point arithmetic (Eq. 6 compensation, the Alg. 1 ROI keep test, grid
+// quantisation) that the filter and the mean kernels must evaluate
+// identically.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "mmbev.h"
+
+namespace mmbev {
+
+constexpr int kBlock = 256;           // threads per workgroup (4 wave64)
+constexpr int kWaves = kBlock / 64;
+constexpr int kFilterGroups = 4;      // float4 groups per thread in the filter
+constexpr int kFilterTile = kBlock * 4 * kFilterGroups;  // 4096 points
+constexpr int kSortItems = 8;         // items per thread in a radix pass
+constexpr int kSortTile = kBlock * kSortItems;           // 2048 pairs
+constexpr int kSortBins = 256;        // max radix digit width 8 bits
+constexpr int kMaxPasses = 6;         // 48 key bits
+constexpr int kScanItems = 16;        // items per thread in the head scan
+constexpr int kScanTile = kBlock * kScanItems;           // 4096 pairs
+constexpr int kMeanTile = kBlock;                        // one voxel per thread
+constexpr int kMaxPoseLds = 64;       // (frame, sweep) poses staged in LDS per tile
+constexpr uint32_t kSpinLimit = 1u << 20;
+
+// Look-back status word: [63:32] tag, [31:30] flag, [29:0] value.
+constexpr uint32_t kFlagAgg = 1u << 30;
+constexpr uint32_t kFlagIncl = 2u << 30;
+constexpr uint32_t kValueMask = (1u << 30) - 1u;
+
+// Tag slots of the look-back launches of one call.
+enum Slot : uint32_t {
+  kSlotFilter = 0,
+  kSlotSort0 = 1,        // .. kSlotSort0 + kMaxPasses - 1
+  kSlotCapSort0 = 7,     // .. + kMaxPasses - 1
+  kSlotUnique = 13,
+  kSlotMean = 14,
+  kNumSlots = 16,
+};
+
+// Workspace header: per-call counters, rewritten by the first kernel of a call.
+struct alignas(256) WsHeader {
+  int32_t fault;              // byte 0: MMBEV_FAULT_* bits of the last call
+  uint32_t epoch;             // call counter; tags look-back words
+  uint32_t kept;              // K, kept points
+  uint32_t voxels;            // V, distinct voxels over all frames
+  uint32_t capped_voxels;     // voxels of frames over the cap
+  uint32_t any_capped;        // 1 if some frame exceeds max_voxels
+  uint32_t pad[2];
+  uint32_t tickets[kNumSlots];               // dynamic tile ids per launch
+  uint32_t hist[2][kMaxPasses][kSortBins];   // digit histograms: main sort, cap sort
+};
+
+// Everything a kernel needs, computed once on the host and passed by value.
+struct Config {
+  // inputs
+  const float* feat;
+  const uint8_t* sweep;
+  const float* poses;
+  const int64_t* frame_off;
+  const mmbev_roi_t* rois;
+  const int32_t* roi_off;
+  const uint8_t* budget;
+  int64_t stride;
+  int32_t N;  // < 2^30
+  int32_t C, B, S, M, cap;
+  int32_t R, max_rois, W;  // W: 32-bit mask words per cell
+  float mn[3], vs[3], Df[3];
+  uint32_t Dx, Dy, Dz;
+  int32_t cell_shift, ncx, ncy, ncells;
+  // keys: key_local = (iz*Dy + iy)*Dx + ix < 2^kb; frame b above it
+  int32_t kb, fb, key_has_frame;  // key_has_frame: kb + fb <= 32, key = b << kb | key_local
+  int32_t passes, dbits;
+  int32_t cap_passes, cap_dbits;
+  int32_t vec;  // 16-byte vector loads allowed
+  // outputs
+  int32_t* out_coords;
+  int32_t* out_counts;
+  float* out_feats;
+  int32_t* out_point_idx;
+  int64_t* out_voxel_offsets;
+  // workspace
+  WsHeader* hdr;
+  uint32_t* cellmask;      // [B][ncells][W]
+  uint32_t* budgetmask;    // [B][S][W]
+  uint64_t* filter_status; // [filter tiles]
+  uint64_t* sort_status;   // [sort tiles][256]
+  uint64_t* scan_status;   // [scan tiles]
+  uint64_t* mean_status;   // [mean tiles]
+  uint32_t* keys[2];
+  uint32_t* vals[2];
+  uint32_t* ckeys;         // cap sort scratch (with keys/vals of the other parity)
+  uint32_t* cvals;
+  uint32_t* seg_start;     // [N+1] first sorted position of voxel v
+  uint32_t* vox_off;       // [B+1] first voxel of frame b
+  uint32_t* cap_off;       // [B+1] position of frame b among capped-frame voxels
+  uint8_t* keepflag;       // [N] per capped-frame voxel (key order)
+  int32_t filter_tiles, sort_grid, scan_grid, mean_grid;
+};
+
+// ------------------------------------------------------------------ helpers
+__device__ __forceinline__ uint32_t lane_id() { return __lane_id(); }
+
+__device__ __forceinline__ uint64_t lanemask_lt() {
+  uint32_t l = __lane_id();
+  return l == 0 ? 0ull : (~0ull >> (64 - l));
+}
+
+__device__ __forceinline__ uint32_t tag_of(uint32_t epoch, uint32_t slot) { return epoch * kNumSlots + slot; }
+
+__device__ __forceinline__ uint64_t status_word(uint32_t tag, uint32_t flag, uint32_t value) {
+  return ((uint64_t)tag << 32) | (uint64_t)(flag | (value & kValueMask));
+}
+
+__device__ __forceinline__ void status_store(uint64_t* p, uint64_t w) {
+  __hip_atomic_store(p, w, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+__device__ __forceinline__ uint64_t status_load(const uint64_t* p) {
+  return __hip_atomic_load(const_cast<uint64_t*>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+__device__ __forceinline__ void raise_fault(WsHeader* h, int32_t bits) {
+  __hip_atomic_fetch_or(&h->fault, bits, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// Exclusive prefix of the tiles before `tile` for one look-back lane.
+// Walks back over aggregates until an inclusive prefix is found.  Waits are
+// bounded: on expiry the fault bit is raised and the partial sum returned.
+__device__ __forceinline__ uint32_t look_back(const uint64_t* status, int64_t tile, int64_t step, uint32_t tag,
+                                              WsHeader* h) {
+  uint32_t prefix = 0;
+  int64_t j = tile - 1;
+  while (j >= 0) {
+    uint64_t w;
+    uint32_t spins = 0;
+    for (;;) {
+      w = status_load(status + j * step);
+      if ((uint32_t)(w >> 32) == tag && ((uint32_t)w & (kFlagAgg | kFlagIncl))) break;
+      if (++spins >= kSpinLimit) {
+        raise_fault(h, MMBEV_FAULT_WAIT);
+        return prefix;
+      }
+      __builtin_amdgcn_s_sleep(1);
+    }
+    prefix += (uint32_t)w & kValueMask;
+    if ((uint32_t)w & kFlagIncl) break;
+    --j;
+  }
+  return prefix;
+}
+
+// Exclusive prefix over the workgroup (kBlock threads, all must call);
+// s_tmp holds kWaves words of LDS.  Returns the prefix, sets total.
+__device__ __forceinline__ uint32_t block_exclusive_scan(uint32_t v, uint32_t* s_tmp, uint32_t& total) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  uint32_t x = v;
+#pragma unroll
+  for (int d = 1; d < 64; d <<= 1) {
+    uint32_t y = __shfl_up(x, d, 64);
+    if (lane >= d) x += y;
+  }
+  if (lane == 63) s_tmp[wave] = x;
+  __syncthreads();
+  uint32_t wpre = 0, tot = 0;
+#pragma unroll
+  for (int w = 0; w < kWaves; ++w) {
+    uint32_t t = s_tmp[w];
+    wpre += (w < wave) ? t : 0u;
+    tot += t;
+  }
+  __syncthreads();
+  total = tot;
+  return wpre + x - v;
+}
+
+// Frame of point index i: largest b with off[b] <= i, clamped to [0, B-1].
+__device__ __forceinline__ int32_t frame_of_point(const int64_t* off, int32_t B, int64_t i) {
+  int32_t lo = 0, hi = B - 1;
+  while (lo < hi) {
+    int32_t mid = (lo + hi + 1) >> 1;
+    if (off[mid] <= i)
+      lo = mid;
+    else
+      hi = mid - 1;
+  }
+  return lo;
+}
+
+// ------------------------------------------------ pinned point arithmetic
+// The library is compiled with -ffp-contract=off and correctly rounded fp32
+// division, so each operator below is one IEEE operation; fused
+// multiply-adds are written out where the definition has them.
+__device__ __forceinline__ float fma_rn(float a, float b, float c) { return __builtin_fmaf(a, b, c); }
+
+// Eq. 6: p' = R p + T as one fused chain per row.
+__device__ __forceinline__ void compensate(const float* P, float x, float y, float z, float& ox, float& oy,
+                                           float& oz) {
+  ox = fma_rn(P[0], x, fma_rn(P[1], y, fma_rn(P[2], z, P[3])));
+  oy = fma_rn(P[4], x, fma_rn(P[5], y, fma_rn(P[6], z, P[7])));
+  oz = fma_rn(P[8], x, fma_rn(P[9], y, fma_rn(P[10], z, P[11])));
+}
+
+// Alg. 1 keep test against one oriented box of ROI_L (edges inclusive).
+__device__ __forceinline__ bool inside_roi(const mmbev_roi_t& r, float x, float y) {
+  float dx = x - r.cx;
+  float dy = y - r.cy;
+  float s_dy = r.sin_yaw * dy;
+  float s_dx = r.sin_yaw * dx;
+  float lx = fma_rn(r.cos_yaw, dx, s_dy);
+  float ly = fma_rn(r.cos_yaw, dy, -s_dx);
+  return fabsf(lx) <= r.ext_x && fabsf(ly) <= r.ext_y;
+}
+
+// Grid coordinate on one axis; false when outside [0, D) or not a number.
+__device__ __forceinline__ bool quantize_axis(float p, float mn, float vs, float Df, int32_t& i) {
+  float f = (p - mn) / vs;
+  bool ok = (f >= 0.0f) && (f < Df);
+  i = ok ? (int32_t)f : 0;
+  return ok;
+}
+
+}  // namespace mmbev

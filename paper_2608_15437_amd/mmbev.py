@@ -1,0 +1,242 @@
+"""Python binding of libmmbev (ctypes): argument marshalling only.
+
+The names mirror include/mmbev.h.  PyTorch supplies device memory and the
+current stream; every step of the voxelisation runs in the HIP kernels of
+libmmbev.so.  There is no fallback: if the library or a GPU is missing, the
+calls raise.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libmmbev.so")
+
+OK, ERR_INVALID_ARG, ERR_WORKSPACE, ERR_UNSUPPORTED, ERR_HIP = 0, -1, -2, -3, -4
+FAULT_POINT_OFFSETS, FAULT_ROI_OFFSETS, FAULT_WAIT = 1, 2, 4
+
+ROI_DTYPE = np.dtype([("cx", "<f4"), ("cy", "<f4"), ("cos_yaw", "<f4"), ("sin_yaw", "<f4"),
+                      ("ext_x", "<f4"), ("ext_y", "<f4"), ("reserved0", "<f4"), ("reserved1", "<f4")])
+
+
+class mmbev_points_t(ctypes.Structure):
+    _fields_ = [("feat", ctypes.c_void_p), ("stride", ctypes.c_int64), ("num_features", ctypes.c_int32),
+                ("reserved", ctypes.c_int32), ("num_points", ctypes.c_int64), ("frame_offsets", ctypes.c_void_p)]
+
+
+class mmbev_rois_t(ctypes.Structure):
+    _fields_ = [("boxes", ctypes.c_void_p), ("frame_offsets", ctypes.c_void_p), ("num_rois", ctypes.c_int32),
+                ("max_rois_per_frame", ctypes.c_int32)]
+
+
+class mmbev_grid_t(ctypes.Structure):
+    _fields_ = [("range_min", ctypes.c_float * 3), ("voxel_size", ctypes.c_float * 3),
+                ("dims", ctypes.c_int32 * 3), ("max_points", ctypes.c_int32), ("max_voxels", ctypes.c_int32),
+                ("num_sweeps", ctypes.c_int32), ("num_frames", ctypes.c_int32)]
+
+
+class MmbevError(RuntimeError):
+    pass
+
+
+_lib = None
+
+
+def load() -> ctypes.CDLL:
+    """Load libmmbev.so (built in-tree by build.py); raise if absent."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise MmbevError(f"{LIB_PATH} is missing: build it with paper_2608_15437_amd.build.build()")
+        L = ctypes.CDLL(LIB_PATH)
+        p = ctypes.c_void_p
+        L.mmbev_abi_version.argtypes = []
+        L.mmbev_abi_version.restype = ctypes.c_int32
+        L.mmbev_status_string.argtypes = [ctypes.c_int32]
+        L.mmbev_status_string.restype = ctypes.c_char_p
+        L.mmbev_roi_voxelize_workspace_bytes.argtypes = [ctypes.POINTER(mmbev_grid_t), ctypes.c_int64,
+                                                         ctypes.c_int32]
+        L.mmbev_roi_voxelize_workspace_bytes.restype = ctypes.c_size_t
+        L.mmbev_workspace_init.argtypes = [p, ctypes.c_size_t, p]
+        L.mmbev_workspace_init.restype = ctypes.c_int32
+        L.mmbev_make_rois.argtypes = [p, ctypes.c_int64, p]
+        L.mmbev_make_rois.restype = ctypes.c_int32
+        L.mmbev_roi_voxelize.argtypes = [ctypes.POINTER(mmbev_points_t), p, p, ctypes.POINTER(mmbev_rois_t), p,
+                                         ctypes.POINTER(mmbev_grid_t), p, p, p, p, p, p, ctypes.c_size_t, p]
+        L.mmbev_roi_voxelize.restype = ctypes.c_int32
+        L.mmbev_roi_voxelize_profiled.argtypes = L.mmbev_roi_voxelize.argtypes + [p, ctypes.c_int32, p]
+        L.mmbev_roi_voxelize_profiled.restype = ctypes.c_int32
+        _lib = L
+    return _lib
+
+
+def _check(status: int, what: str) -> None:
+    if status != OK:
+        msg = load().mmbev_status_string(status).decode()
+        raise MmbevError(f"{what}: {msg} ({status})")
+
+
+def abi_version() -> int:
+    return int(load().mmbev_abi_version())
+
+
+def grid_params(range_min, voxel_size, dims, max_points, max_voxels, num_sweeps, num_frames) -> mmbev_grid_t:
+    g = mmbev_grid_t()
+    for d in range(3):
+        g.range_min[d] = float(range_min[d])
+        g.voxel_size[d] = float(voxel_size[d])
+        g.dims[d] = int(dims[d])
+    g.max_points, g.max_voxels = int(max_points), int(max_voxels)
+    g.num_sweeps, g.num_frames = int(num_sweeps), int(num_frames)
+    return g
+
+
+def roi_voxelize_workspace_bytes(grid: mmbev_grid_t, num_points: int, max_rois_per_frame: int) -> int:
+    return int(load().mmbev_roi_voxelize_workspace_bytes(ctypes.byref(grid), int(num_points),
+                                                         int(max_rois_per_frame)))
+
+
+def _ptr(t) -> int | None:
+    if t is None:
+        return None
+    return int(t.data_ptr()) if t.numel() > 0 else None
+
+
+def _stream(stream) -> int | None:
+    import torch
+
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return int(stream.cuda_stream) or None
+
+
+def workspace_init(workspace, stream=None) -> None:
+    _check(load().mmbev_workspace_init(_ptr(workspace), workspace.numel() * workspace.element_size(),
+                                       _stream(stream)), "mmbev_workspace_init")
+
+
+def make_rois(desc) -> np.ndarray:
+    """ROI records (host) from descriptor rows (cx, cy, length, width, yaw, margin)."""
+    desc = np.ascontiguousarray(desc, dtype=np.float64).reshape(-1, 6)
+    out = np.zeros(len(desc), dtype=ROI_DTYPE)
+    _check(load().mmbev_make_rois(desc.ctypes.data if len(desc) else None, len(desc),
+                                  out.ctypes.data if len(desc) else None), "mmbev_make_rois")
+    return out
+
+
+def roi_voxelize(feat, frame_offsets, sweep_ids, sweep_poses, rois, roi_frame_offsets, roi_sweep_budget,
+                 grid: mmbev_grid_t, out_coords, out_counts, out_feats, out_point_idx, out_voxel_offsets,
+                 workspace, max_rois_per_frame: int, stream=None, events=None) -> int:
+    """Enqueue one call of mmbev_roi_voxelize on `stream` (torch tensors on the GPU).
+
+    feat: float32 [C][stride] (SoA); frame_offsets: int64 [B+1]; sweep_ids: uint8 [N];
+    sweep_poses: float32 [B][S][12]; rois: float32 [R][8] (mmbev_roi_t records);
+    roi_frame_offsets: int32 [B+1]; roi_sweep_budget: uint8 [R]; outputs as in mmbev.h.
+    """
+    C = int(feat.shape[0])
+    N = int(sweep_ids.numel())
+    pts = mmbev_points_t(feat=_ptr(feat), stride=int(feat.stride(0)) if feat.dim() == 2 else N,
+                         num_features=C, reserved=0, num_points=N, frame_offsets=_ptr(frame_offsets))
+    if N > 0 and feat.dim() == 2 and feat.stride(1) != 1:
+        raise MmbevError("feat rows must be contiguous")
+    R = int(rois.shape[0])
+    rr = mmbev_rois_t(boxes=_ptr(rois), frame_offsets=_ptr(roi_frame_offsets), num_rois=R,
+                      max_rois_per_frame=int(max_rois_per_frame))
+    args = [ctypes.byref(pts), _ptr(sweep_ids), _ptr(sweep_poses), ctypes.byref(rr), _ptr(roi_sweep_budget),
+            ctypes.byref(grid), _ptr(out_coords), _ptr(out_counts), _ptr(out_feats), _ptr(out_point_idx),
+            _ptr(out_voxel_offsets), _ptr(workspace), workspace.numel() * workspace.element_size(),
+            _stream(stream)]
+    if events is None:
+        _check(load().mmbev_roi_voxelize(*args), "mmbev_roi_voxelize")
+        return 0
+    # events: torch.cuda.Event objects (timing enabled) that have been recorded once
+    handles = (ctypes.c_void_p * len(events))(*[int(e.cuda_event) for e in events])
+    used = ctypes.c_int32(0)
+    _check(load().mmbev_roi_voxelize_profiled(*args, handles, len(events), ctypes.byref(used)),
+           "mmbev_roi_voxelize_profiled")
+    return int(used.value)
+
+
+class Voxelizer:
+    """Owns device inputs, outputs and workspace for repeated calls on one batch shape.
+
+    All buffers are torch tensors on `device`; `run()` enqueues one call on the
+    current stream and returns without waiting.
+    """
+
+    def __init__(self, feat, frame_offsets, sweep_ids, sweep_poses, rois, roi_frame_offsets, roi_sweep_budget,
+                 grid: mmbev_grid_t, max_rois_per_frame: int, device):
+        import torch
+
+        self.device = torch.device(device)
+        dev = self.device
+
+        def up(a, dtype):
+            return torch.as_tensor(np.ascontiguousarray(a)).to(dtype).to(dev)
+
+        self.feat = up(feat, torch.float32)
+        self.frame_offsets = up(frame_offsets, torch.int64)
+        self.sweep_ids = up(sweep_ids, torch.uint8)
+        self.sweep_poses = up(sweep_poses, torch.float32)
+        rois = np.ascontiguousarray(rois)
+        rec = rois.view(np.float32).reshape(-1, 8) if rois.dtype.fields else np.asarray(rois, np.float32)
+        self.rois = up(rec.reshape(-1, 8), torch.float32)
+        self.roi_frame_offsets = up(roi_frame_offsets, torch.int32)
+        self.roi_sweep_budget = up(roi_sweep_budget, torch.uint8)
+        self.grid = grid
+        self.max_rois = int(max_rois_per_frame)
+        B, cap, M, C = grid.num_frames, grid.max_voxels, grid.max_points, int(self.feat.shape[0])
+        rows = B * cap
+        self.out_coords = torch.full((rows, 4), -7, dtype=torch.int32, device=dev)
+        self.out_counts = torch.full((rows,), -7, dtype=torch.int32, device=dev)
+        self.out_feats = torch.full((rows, C), -7.0, dtype=torch.float32, device=dev)
+        self.out_point_idx = torch.full((rows, M), -7, dtype=torch.int32, device=dev)
+        self.out_voxel_offsets = torch.zeros(B + 1, dtype=torch.int64, device=dev)
+        nbytes = roi_voxelize_workspace_bytes(grid, int(self.sweep_ids.numel()), self.max_rois)
+        if nbytes == 0:
+            raise MmbevError("invalid sizes for mmbev_roi_voxelize_workspace_bytes")
+        self.workspace = torch.empty(nbytes, dtype=torch.uint8, device=dev)
+        workspace_init(self.workspace)
+
+    def run(self, stream=None, events=None) -> int:
+        return roi_voxelize(self.feat, self.frame_offsets, self.sweep_ids, self.sweep_poses, self.rois,
+                            self.roi_frame_offsets, self.roi_sweep_budget, self.grid, self.out_coords,
+                            self.out_counts, self.out_feats, self.out_point_idx, self.out_voxel_offsets,
+                            self.workspace, self.max_rois, stream, events)
+
+    def fault(self) -> int:
+        """Device fault word of the last completed call (synchronises)."""
+        return int(self.workspace[:4].cpu().numpy().view(np.int32)[0])
+
+    def header(self) -> dict:
+        """Per-call counters of the last completed call (synchronises)."""
+        h = self.workspace[:32].cpu().numpy().view(np.uint32)
+        return {"fault": int(h[0]), "epoch": int(h[1]), "kept": int(h[2]), "voxels": int(h[3]),
+                "capped_voxels": int(h[4]), "any_capped": int(h[5])}
+
+    def result(self) -> dict:
+        """Outputs of the last completed call as numpy arrays trimmed to V rows (synchronises)."""
+        off = self.out_voxel_offsets.cpu().numpy()
+        V = int(off[-1])
+        return {"coords": self.out_coords[:V].cpu().numpy(), "counts": self.out_counts[:V].cpu().numpy(),
+                "feats": self.out_feats[:V].cpu().numpy(), "point_idx": self.out_point_idx[:V].cpu().numpy(),
+                "voxel_offsets": off}
+
+
+def voxelizer_for_workload(wl, device, rois=None) -> Voxelizer:
+    """A Voxelizer for a synth workload; ROI records from the library's mmbev_make_rois."""
+    gr = wl.grid
+    g = grid_params(gr.range_min, gr.voxel_size, gr.dims, gr.max_points, gr.max_voxels, gr.num_sweeps,
+                    gr.num_frames)
+    recs = make_rois(wl.roi_desc) if rois is None else rois
+    return Voxelizer(wl.feat, wl.frame_offsets, wl.sweep_ids, wl.poses, recs, wl.roi_offsets, wl.budgets, g,
+                     max(wl.max_rois_per_frame, 1), device)
+
+
+def roi_voxelize_workload(wl, device) -> dict:
+    vz = voxelizer_for_workload(wl, device)
+    vz.run()
+    return vz.result()

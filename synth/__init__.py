@@ -19,6 +19,7 @@ from __future__ import annotations
 
 import ctypes
 import os
+from concurrent.futures import ThreadPoolExecutor
 from dataclasses import dataclass, field
 
 import numpy as np
@@ -176,8 +177,11 @@ def _build(name: str, scene: SceneT, recipe: RoiRecipeT | None, seeds, grid: Gri
     feat = np.zeros((C, N), dtype=np.float32)
     sweep_ids = np.zeros(N, dtype=np.uint8)
     poses = np.zeros((B, S, 12), dtype=np.float32)
-    descs, budgets, roi_off, obstacles = [], [], [0], []
-    for f, seed in enumerate(seeds):
+    descs, budgets, roi_off = [], [], [0]
+
+    def one_frame(f):
+        # ctypes releases the GIL: frames are generated in parallel into disjoint ranges
+        seed = seeds[f]
         obs = np.zeros((max(scene.num_obstacles, 1), 7), dtype=np.float64)
         nobs = L.synth_obstacles(ctypes.byref(scene), seed, obs.ctypes.data)
         obs = np.ascontiguousarray(obs[:nobs])
@@ -187,7 +191,14 @@ def _build(name: str, scene: SceneT, recipe: RoiRecipeT | None, seeds, grid: Gri
         if n != per_frame:
             raise RuntimeError("synth_frame failed")
         poses[f] = pose_f
-        obstacles.append(obs)
+        return obs
+
+    workers = min(B, max(1, min(os.cpu_count() or 1, 16)))
+    with ThreadPoolExecutor(max_workers=workers) as ex:
+        obstacles = list(ex.map(one_frame, range(B)))
+    for f, seed in enumerate(seeds):
+        obs = obstacles[f]
+        nobs = len(obs)
         if fixed_rois is not None:
             d, bud = fixed_rois
             d = np.asarray(d, dtype=np.float64).reshape(-1, 6)

@@ -35,6 +35,8 @@
 
 #include "gen.h"
 
+static const double kPi = 3.14159265358979323846;
+
 /* ---------------------------------------------------------------- RNG */
 typedef struct {
   uint64_t s[4];
@@ -81,11 +83,11 @@ static int rng_int(rng_t* r, int lo, int hi) {
 static double rng_normal(rng_t* r) {
   double u1 = 1.0 - rng_u01(r); /* (0, 1] */
   double u2 = rng_u01(r);
-  return sqrt(-2.0 * log(u1)) * cos(2.0 * M_PI * u2);
+  return sqrt(-2.0 * log(u1)) * cos(2.0 * kPi * u2);
 }
 
 /* ------------------------------------------------------------ helpers */
-static const double kDeg = M_PI / 180.0;
+static const double kDeg = kPi / 180.0;
 
 /* Ego pose of the sweep taken tau seconds before now (tau <= 0 passed as
  * its value), constant speed v and yaw rate w: heading psi and planar
@@ -139,8 +141,8 @@ int64_t synth_obstacles(const synth_scene_t* sc, uint64_t seed, double* obs) {
     double wid = sc->obs_wid * rng_uniform(&r, 1.0 - jit, 1.0 + jit);
     double hgt = sc->obs_hgt * rng_uniform(&r, 1.0 - jit, 1.0 + jit);
     double rad = sqrt(rng_uniform(&r, sc->obs_r_lo * sc->obs_r_lo, sc->obs_r_hi * sc->obs_r_hi));
-    double az = rng_uniform(&r, 0.0, 2.0 * M_PI);
-    double yaw = sc->axis_aligned ? 0.0 : rng_uniform(&r, 0.0, 2.0 * M_PI);
+    double az = rng_uniform(&r, 0.0, 2.0 * kPi);
+    double yaw = sc->axis_aligned ? 0.0 : rng_uniform(&r, 0.0, 2.0 * kPi);
     double cx = rad * cos(az), cy = rad * sin(az);
     double br = 0.5 * sqrt(len * len + wid * wid);
     int clash = 0;
@@ -214,13 +216,13 @@ int64_t synth_frame(const synth_scene_t* sc, uint64_t seed, const double* obs, i
       lc[k][3] = sin(-ys);
     }
 
-    double phase = rng_uniform(&r, 0.0, 2.0 * M_PI / na);
+    double phase = rng_uniform(&r, 0.0, 2.0 * kPi / na);
     for (int b = 0; b < nb; ++b) {
       double el = (nb == 1) ? sc->elev_lo_deg * kDeg
                             : (sc->elev_lo_deg + (sc->elev_hi_deg - sc->elev_lo_deg) * b / (nb - 1)) * kDeg;
       double ce = cos(el), se = sin(el);
       for (int a = 0; a < na; ++a) {
-        double az = phase + 2.0 * M_PI * a / na;
+        double az = phase + 2.0 * kPi * a / na;
         double d[3] = {ce * cos(az), ce * sin(az), se};
         double t = INFINITY;
         if (d[2] < -1e-12) t = -sc->sensor_h / d[2];
@@ -297,7 +299,7 @@ int64_t synth_rois(const synth_roi_recipe_t* rc, uint64_t seed, const double* ob
     double* d = desc + 6 * n;
     double len = rc->rand_len * rng_uniform(&r, 0.9, 1.1);
     double wid = rc->rand_wid * rng_uniform(&r, 0.9, 1.1);
-    double yaw = rng_uniform(&r, 0.0, 2.0 * M_PI);
+    double yaw = rng_uniform(&r, 0.0, 2.0 * kPi);
     double cx, cy;
     if (k >= rc->num_random - rc->num_overlapping && n > 0) {
       int64_t j = rng_int(&r, 0, (int)(n - 1));

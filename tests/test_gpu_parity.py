@@ -1,0 +1,173 @@
+"""Parity of the HIP path (through the C ABI) with the CPU oracle.
+
+Structure (voxel coordinates, order, counts, kept point indices, frame
+offsets) must match bit for bit; mean features within 1e-5 absolute, the
+stated tolerance for the fp32 means (both sides sum the same fp32 values in
+double in the same order, so in practice they agree exactly).
+"""
+import numpy as np
+import pytest
+
+import oracle
+import synth
+from common import Case, assert_same_voxels, case_from_workload, load_golden, records
+
+pytestmark = pytest.mark.gpu
+FEAT_TOL = 1e-5
+
+
+def run_gpu(mb, case: Case, device="cuda:0", gpu_rois=None):
+    """Run the HIP path; ROI records are the case's own (hand-made) or gpu_rois
+    (built by the library's mmbev_make_rois from the same descriptors)."""
+    g = case.grid
+    grid = mb.grid_params(g["range_min"], g["voxel_size"], g["dims"], g["max_points"], g["max_voxels"],
+                          g["num_sweeps"], g["num_frames"])
+    mr = int(np.max(np.diff(case.roi_offsets))) if len(case.roi_offsets) > 1 else 0
+    rois = case.rois if gpu_rois is None else gpu_rois
+    vz = mb.Voxelizer(case.feat, case.frame_offsets, case.sweep_ids, case.poses, rois, case.roi_offsets,
+                      case.budgets, grid, max(mr, 1), device)
+    vz.run()
+    return vz
+
+
+def check(mb, case: Case, label="", desc=None):
+    """Oracle vs GPU.  With `desc` (ROI descriptors) each side builds its own records."""
+    exp = case.run_oracle()
+    vz = run_gpu(mb, case, gpu_rois=None if desc is None else mb.make_rois(desc))
+    got = vz.result()
+    assert vz.fault() == 0, f"{label}: device fault {vz.fault()}"
+    assert_same_voxels(got, exp, feat_atol=FEAT_TOL, label=label)
+    # rows past V untouched (canary -7 written at allocation)
+    V = int(exp["voxel_offsets"][-1])
+    rest = vz.out_counts[V:].cpu().numpy()
+    assert np.all(rest == -7), f"{label}: rows past V were written"
+    return vz, exp
+
+
+def test_golden_hand_two_frames(gpu_lib):
+    case, exp = load_golden("hand_two_frames.json")
+    vz = run_gpu(gpu_lib, case)
+    assert vz.fault() == 0
+    assert_same_voxels(vz.result(), exp, feat_atol=0.0, label="golden")
+
+
+@pytest.mark.parametrize("name", ["c1", "c2", "c3", "c4", "c5"])
+def test_configs_match_oracle(gpu_lib, name):
+    wl = synth.CONFIGS[name]()
+    case = case_from_workload(wl)
+    vz, exp = check(gpu_lib, case, label=name, desc=wl.roi_desc)
+    h = vz.header()
+    keys, _ = case.oracle_keep()
+    assert h["kept"] == len(keys), "kept-point count differs from the oracle's"
+
+
+@pytest.mark.parametrize("seed,frames,cap,M,budget", [
+    (1, 1, 1000, 4, (1, 3)), (2, 2, 25, 2, (1, 3)), (3, 3, 7, 1, (0, 3)), (4, 4, 1, 3, (1, 3)),
+    (5, 5, 50, 8, (2, 3)), (6, 2, 3, 64, (1, 3)), (7, 7, 400, 5, (1, 2))])
+def test_small_scenes_match_oracle(gpu_lib, seed, frames, cap, M, budget):
+    wl = synth.small(seed, frames=frames, max_voxels=cap, max_points=M, budget=budget)
+    check(gpu_lib, case_from_workload(wl), label=f"small{seed}", desc=wl.roi_desc)
+
+
+def test_ragged_tail_and_scalar_loads(gpu_lib):
+    """N not a multiple of 4 and a row stride that forbids 16-byte loads."""
+    wl = synth.small(21, frames=1, beams=7, azimuths=61, sweeps=3)
+    case = case_from_workload(wl)
+    N = case.feat.shape[1]
+    assert N % 4 != 0
+    check(gpu_lib, case, label="ragged", desc=wl.roi_desc)
+    # stride N+1 (scalar path): embed the SoA rows in a wider array
+    import torch
+    wide = np.zeros((case.feat.shape[0], N + 1), dtype=np.float32)
+    wide[:, :N] = case.feat
+    g = case.grid
+    grid = gpu_lib.grid_params(g["range_min"], g["voxel_size"], g["dims"], g["max_points"], g["max_voxels"],
+                               g["num_sweeps"], g["num_frames"])
+    vz = gpu_lib.Voxelizer(case.feat, case.frame_offsets, case.sweep_ids, case.poses, gpu_lib.make_rois(wl.roi_desc),
+                           case.roi_offsets, case.budgets, grid, int(np.max(np.diff(case.roi_offsets))), "cuda:0")
+    vz.feat = torch.as_tensor(wide).cuda()[:, :N]
+    vz.run()
+    assert_same_voxels(vz.result(), case.run_oracle(), feat_atol=FEAT_TOL, label="stride")
+
+
+def test_wide_keys_need_frame_lookup(gpu_lib):
+    """Key bits + frame bits > 32: the frame comes from the point index."""
+    wl = synth.small(31, frames=33, beams=4, azimuths=32, sweeps=2, dims=(2048, 2048, 64), voxel=0.02,
+                     max_voxels=60)
+    case = case_from_workload(wl)
+    check(gpu_lib, case, label="wide", desc=wl.roi_desc)
+
+
+def test_edge_cases(gpu_lib):
+    case, _ = load_golden("hand_two_frames.json")
+    # every budget 0: nothing kept
+    check(gpu_lib, Case(**{**case.__dict__, "budgets": np.zeros_like(case.budgets)}), label="budget0")
+    # one frame with no ROI
+    check(gpu_lib, Case(**{**case.__dict__, "rois": case.rois[:2], "budgets": case.budgets[:2],
+                           "roi_offsets": np.array([0, 2, 2], dtype=np.int32)}), label="no-roi frame")
+    # sweep ids past num_sweeps
+    check(gpu_lib, Case(**{**case.__dict__, "sweep_ids": np.full_like(case.sweep_ids, 9)}), label="sweep>=S")
+    # non-finite coordinates
+    feat = case.feat.copy()
+    feat[0, 0], feat[1, 5], feat[2, 12] = np.nan, np.inf, -np.inf
+    check(gpu_lib, Case(**{**case.__dict__, "feat": feat}), label="nonfinite")
+    # a single point, and an empty frame in the middle
+    one = Case(feat=case.feat[:, :1].copy(), sweep_ids=case.sweep_ids[:1], frame_offsets=np.array([0, 1]),
+               poses=case.poses[:1], rois=case.rois[:2], roi_offsets=np.array([0, 2], dtype=np.int32),
+               budgets=case.budgets[:2], grid=dict(case.grid, num_frames=1))
+    check(gpu_lib, one, label="one point")
+    wl = synth.small(41, frames=3)
+    c3 = case_from_workload(wl)
+    fo = c3.frame_offsets.copy()
+    keep = np.r_[0:fo[1], fo[2]:fo[3]]
+    empty_mid = Case(feat=np.ascontiguousarray(c3.feat[:, keep]), sweep_ids=c3.sweep_ids[keep],
+                     frame_offsets=np.array([0, fo[1], fo[1], fo[1] + fo[3] - fo[2]]), poses=c3.poses, rois=c3.rois,
+                     roi_offsets=c3.roi_offsets, budgets=c3.budgets, grid=c3.grid)
+    check(gpu_lib, empty_mid, label="empty middle frame", desc=wl.roi_desc)
+
+
+def test_zero_points(gpu_lib):
+    case, _ = load_golden("hand_two_frames.json")
+    z = Case(feat=np.zeros((4, 0), np.float32), sweep_ids=np.zeros(0, np.uint8), frame_offsets=np.array([0, 0, 0]),
+             poses=case.poses, rois=case.rois, roi_offsets=case.roi_offsets, budgets=case.budgets, grid=case.grid)
+    vz = run_gpu(gpu_lib, z)
+    assert vz.result()["voxel_offsets"].tolist() == [0, 0, 0]
+    assert vz.fault() == 0
+
+
+def test_repeat_calls_are_bit_identical_and_workspace_reusable(gpu_lib):
+    import torch
+
+    wl = synth.c2()
+    vz = gpu_lib.voxelizer_for_workload(wl, "cuda:0")
+    vz.run()
+    a = vz.result()
+    for _ in range(3):
+        vz.run()
+    torch.cuda.synchronize()
+    b = vz.result()
+    for k in a:
+        assert np.array_equal(a[k], b[k]), k
+    assert vz.header()["epoch"] == 4
+
+
+def test_device_fault_word_reports_bad_offsets(gpu_lib):
+    import torch
+
+    case, _ = load_golden("hand_two_frames.json")
+    vz = run_gpu(gpu_lib, case)
+    vz.frame_offsets = torch.tensor([0, 12, 18], dtype=torch.int64, device="cuda:0")  # off[B] != N
+    vz.run()
+    torch.cuda.synchronize()
+    assert vz.fault() & gpu_lib.FAULT_POINT_OFFSETS
+    vz.frame_offsets = torch.tensor([0, 12, 19], dtype=torch.int64, device="cuda:0")
+    vz.roi_frame_offsets = torch.tensor([0, 3, 4], dtype=torch.int32, device="cuda:0")  # 3 > max_rois_per_frame
+    vz.run()
+    torch.cuda.synchronize()
+    assert vz.fault() & gpu_lib.FAULT_ROI_OFFSETS
+
+
+def test_throughput_batch_full_size(gpu_lib):
+    """The benchmark's batched workload, every frame checked against the oracle."""
+    wl = synth.throughput(16)
+    check(gpu_lib, case_from_workload(wl), label="c2x16", desc=wl.roi_desc)

@@ -45,18 +45,12 @@ def source_sha(paths) -> str:
 
 
 def launch_names(vz) -> list:
-    import math
-
     g = vz.grid
     cells = g.dims[0] * g.dims[1] * g.dims[2]
     kb = max(1, (cells - 1).bit_length())
     fb = (g.num_frames - 1).bit_length()
     passes = (kb + fb + 7) // 8
-    N = int(vz.sweep_ids.numel())
-    cap_bits = max(1, max(N - 1, 0).bit_length())
-    cap_passes = (cap_bits + 7) // 8
-    return (["stage", "filter"] + [f"sort{p}" for p in range(passes)] + ["unique", "finalize", "cap_prep"]
-            + [f"capsort{p}" for p in range(cap_passes)] + ["mean"])
+    return ["stage", "filter"] + [f"sort{p}" for p in range(passes)] + ["unique", "finalize", "cap", "mean"]
 
 
 def time_calls(vz, steps: int, warmup: int) -> float:

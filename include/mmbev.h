@@ -185,8 +185,7 @@ mmbev_status_t mmbev_roi_voxelize(const mmbev_points_t* points, const uint8_t* s
  * caller's events (hipEvent_t, created with timing enabled) on `stream`, as
  * long as events remain.  The launch order is: 0 ROI staging, 1 point filter,
  * then one radix pass per key digit, head scan, per-frame finalisation,
- * first-appearance preparation, one radix pass per digit of the point index,
- * mean pooling.  Returns the number of events recorded through
+ * per-frame voxel cap, mean pooling.  Returns the number of events recorded through
  * *events_recorded (host int32, may be NULL).  Elapsed time between events k
  * and k+1 is the duration of launch k.
  */

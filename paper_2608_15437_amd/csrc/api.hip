@@ -23,11 +23,11 @@ struct Plan {
   int64_t N;
   int32_t B, S, C, M, cap, max_rois, W;
   int32_t cell_shift, ncx, ncy, ncells;
-  int32_t kb, fb, key_has_frame, passes, dbits, cap_passes, cap_dbits;
-  int64_t filter_tiles, sort_tiles, scan_tiles, mean_tiles;
-  size_t off_hdr, off_cellmask, off_budgetmask, off_filter_status, off_sort_status, off_scan_status,
-      off_mean_status, off_keys0, off_vals0, off_keys1, off_vals1, off_ckeys, off_cvals, off_seg, off_voxoff,
-      off_capoff, off_keep, total;
+  int32_t kb, fb, key_has_frame, passes, dbits;
+  int64_t filter_tiles, sort_tiles, mean_tiles;
+  int32_t filter_groups;
+  size_t off_hdr, off_cellmask, off_cellany, off_budgetmask, off_tinfo, off_fcount, off_cnt, off_tot, off_hcount,
+      off_keys0, off_vals0, off_keys1, off_vals1, off_capkey, off_rank, off_seg, off_voxoff, total;
 };
 
 mmbev_status_t make_plan(const mmbev_grid_t* g, int64_t N, int32_t max_rois, int32_t C, Plan* p) {
@@ -70,16 +70,13 @@ mmbev_status_t make_plan(const mmbev_grid_t* g, int64_t N, int32_t max_rois, int
   p->key_has_frame = total_bits <= 32 ? 1 : 0;
   p->passes = (total_bits + 7) / 8;
   p->dbits = (total_bits + p->passes - 1) / p->passes;
-  const int cap_bits = std::max(1, bits_for((uint64_t)std::max<int64_t>(N - 1, 0)));
-  p->cap_passes = (cap_bits + 7) / 8;
-  p->cap_dbits = (cap_bits + p->cap_passes - 1) / p->cap_passes;
 
   const int64_t n1 = std::max<int64_t>(N, 1);
-  p->filter_tiles = (N + kFilterTile - 1) / kFilterTile;
-  p->sort_tiles = (n1 + kSortTile - 1) / kSortTile;
-  p->scan_tiles = (n1 + kScanTile - 1) / kScanTile;
-  p->mean_tiles = (n1 + kMeanTile - 1) / kMeanTile;
-
+  // filter tile: 1024 points per group of the 256 threads (two groups for
+  // large inputs: more bytes in flight per workgroup)
+  p->filter_groups = N >= ((int64_t)1 << 21) ? 2 : 1;
+  p->filter_tiles = (N + 1024 * p->filter_groups - 1) / (1024 * p->filter_groups);
+  p->sort_tiles = std::min<int64_t>(kMaxSortChunks, (n1 + kSortTile - 1) / kSortTile);
   size_t o = 0;
   auto take = [&](size_t bytes) {
     size_t at = o;
@@ -88,21 +85,21 @@ mmbev_status_t make_plan(const mmbev_grid_t* g, int64_t N, int32_t max_rois, int
   };
   p->off_hdr = take(sizeof(WsHeader));
   p->off_cellmask = take((size_t)p->B * p->ncells * p->W * 4);
+  p->off_cellany = p->W > 1 ? take((size_t)p->B * p->ncells * 4) : p->off_cellmask;
   p->off_budgetmask = take((size_t)p->B * p->S * p->W * 4);
-  p->off_filter_status = take((size_t)std::max<int64_t>(p->filter_tiles, 1) * 8);
-  p->off_sort_status = take((size_t)p->sort_tiles * kSortBins * 8);
-  p->off_scan_status = take((size_t)p->scan_tiles * 8);
-  p->off_mean_status = take((size_t)p->mean_tiles * 8);
+  p->off_tinfo = take((size_t)std::max<int64_t>(p->filter_tiles, 1) * sizeof(TileInfo));
+  p->off_fcount = take((size_t)kMaxFilterGrid * 4);
+  p->off_cnt = take((size_t)kSortBins * std::max(kMaxFilterGrid, kMaxSortChunks) * 4);
+  p->off_tot = take((size_t)kSortBins * 4);
+  p->off_hcount = take((size_t)kMaxSortChunks * 4);
   p->off_keys0 = take((size_t)n1 * 4);
   p->off_vals0 = take((size_t)n1 * 4);
   p->off_keys1 = take((size_t)n1 * 4);
   p->off_vals1 = take((size_t)n1 * 4);
-  p->off_ckeys = take((size_t)n1 * 4);
-  p->off_cvals = take((size_t)n1 * 4);
+  p->off_capkey = take((size_t)n1 * 4);
+  p->off_rank = take((size_t)n1 * 4);
   p->off_seg = take((size_t)(N + 1) * 4);
   p->off_voxoff = take((size_t)(p->B + 1) * 4);
-  p->off_capoff = take((size_t)(p->B + 1) * 4);
-  p->off_keep = take((size_t)n1);
   p->total = o;
   return MMBEV_OK;
 }
@@ -211,7 +208,11 @@ mmbev_status_t voxelize(const mmbev_points_t* points, const uint8_t* sweep_ids, 
     c.mn[d] = grid->range_min[d];
     c.vs[d] = grid->voxel_size[d];
     c.Df[d] = (float)grid->dims[d];
+    c.inv_vs[d] = (float)(1.0 / (double)grid->voxel_size[d]);
   }
+  // the approximate cell lookup is off by less than one voxel while
+  // 3 * 2^-24 * D < 1; two voxels of padding keep it conservative
+  c.cell_pad = 2 + (std::max(grid->dims[0], grid->dims[1]) >> 21);
   c.Dx = (uint32_t)grid->dims[0];
   c.Dy = (uint32_t)grid->dims[1];
   c.Dz = (uint32_t)grid->dims[2];
@@ -224,8 +225,6 @@ mmbev_status_t voxelize(const mmbev_points_t* points, const uint8_t* sweep_ids, 
   c.key_has_frame = p.key_has_frame;
   c.passes = p.passes;
   c.dbits = p.dbits;
-  c.cap_passes = p.cap_passes;
-  c.cap_dbits = p.cap_dbits;
   c.vec = (((uintptr_t)points->feat & 15) == 0 && (points->stride & 3) == 0 && ((uintptr_t)sweep_ids & 3) == 0) ? 1
                                                                                                                 : 0;
   c.out_coords = out_coords;
@@ -236,24 +235,41 @@ mmbev_status_t voxelize(const mmbev_points_t* points, const uint8_t* sweep_ids, 
   char* ws = (char*)workspace;
   c.hdr = (WsHeader*)(ws + p.off_hdr);
   c.cellmask = (uint32_t*)(ws + p.off_cellmask);
+  c.cellany = (uint32_t*)(ws + p.off_cellany);
   c.budgetmask = (uint32_t*)(ws + p.off_budgetmask);
-  c.filter_status = (uint64_t*)(ws + p.off_filter_status);
-  c.sort_status = (uint64_t*)(ws + p.off_sort_status);
-  c.scan_status = (uint64_t*)(ws + p.off_scan_status);
-  c.mean_status = (uint64_t*)(ws + p.off_mean_status);
+  c.tinfo = (TileInfo*)(ws + p.off_tinfo);
+  c.fcount = (uint32_t*)(ws + p.off_fcount);
+  c.cnt = (uint32_t*)(ws + p.off_cnt);
+  c.tot = (uint32_t*)(ws + p.off_tot);
+  c.hcount = (uint32_t*)(ws + p.off_hcount);
   c.keys[0] = (uint32_t*)(ws + p.off_keys0);
   c.vals[0] = (uint32_t*)(ws + p.off_vals0);
   c.keys[1] = (uint32_t*)(ws + p.off_keys1);
   c.vals[1] = (uint32_t*)(ws + p.off_vals1);
-  c.ckeys = (uint32_t*)(ws + p.off_ckeys);
-  c.cvals = (uint32_t*)(ws + p.off_cvals);
+  c.capkey = (uint32_t*)(ws + p.off_capkey);
+  c.out_rank = (uint32_t*)(ws + p.off_rank);
   c.seg_start = (uint32_t*)(ws + p.off_seg);
   c.vox_off = (uint32_t*)(ws + p.off_voxoff);
-  c.cap_off = (uint32_t*)(ws + p.off_capoff);
-  c.keepflag = (uint8_t*)(ws + p.off_keep);
   c.filter_tiles = (int32_t)p.filter_tiles;
-  c.sort_grid = (int32_t)std::min<int64_t>(p.sort_tiles, 1024);
-  c.scan_grid = (int32_t)std::min<int64_t>(p.scan_tiles, 1024);
+  c.filter_groups = p.filter_groups;
+  c.filter_tile_points = 1024 * p.filter_groups;
+  {
+    // persistent filter: as many workgroups as fit on the device at once,
+    // each owning a contiguous chunk of tiles
+    int dev = 0, cus = 0, per_cu = 0;
+    if (hipGetDevice(&dev) != hipSuccess ||
+        hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+        filter_occupancy(p.filter_groups, c.vec, &per_cu) != hipSuccess)
+      return MMBEV_ERR_HIP;
+    int64_t grid = std::max<int64_t>(1, (int64_t)std::max(per_cu, 1) * cus);
+    grid = std::min<int64_t>(grid, kMaxFilterGrid);
+    grid = std::max<int64_t>(1, std::min<int64_t>(grid, p.filter_tiles));
+    const int64_t chunk = std::max<int64_t>(1, (p.filter_tiles + grid - 1) / grid);
+    c.filter_chunk_tiles = (int32_t)chunk;
+    c.filter_grid = (int32_t)std::max<int64_t>(1, (p.filter_tiles + chunk - 1) / chunk);
+    c.filter_chunk_points = (int32_t)(chunk * c.filter_tile_points);
+  }
+  c.sort_chunks = (int32_t)std::max<int64_t>(1, p.sort_tiles);
   c.mean_grid = (int32_t)std::min<int64_t>(p.mean_tiles, 2048);
 
   hipStream_t s = (hipStream_t)stream;
@@ -266,22 +282,14 @@ mmbev_status_t voxelize(const mmbev_points_t* points, const uint8_t* sweep_ids, 
   MMBEV_TRY(launch_filter(c, s));
   int cur = 0;
   for (int pass = 0; pass < c.passes; ++pass) {
-    MMBEV_TRY(launch_radix_pass(c, 0, pass, c.keys[cur], c.vals[cur], c.keys[1 - cur], c.vals[1 - cur], false, s));
+    MMBEV_TRY(launch_radix_pass(c, pass, c.keys[cur], c.vals[cur], c.keys[1 - cur], c.vals[1 - cur], s));
     cur = 1 - cur;
   }
   const uint32_t* keys = c.keys[cur];
   const uint32_t* vals = c.vals[cur];
   MMBEV_TRY(launch_unique(c, keys, vals, s));
   MMBEV_TRY(launch_finalize(c, keys, vals, s));
-  // first-appearance sort of the voxels of over-cap frames (kernels exit at once when none is)
-  uint32_t* ck[2] = {c.keys[1 - cur], c.ckeys};
-  uint32_t* cv[2] = {c.vals[1 - cur], c.cvals};
-  MMBEV_TRY(launch_cap_prep(c, vals, ck[0], cv[0], s));
-  for (int pass = 0; pass < c.cap_passes; ++pass) {
-    const bool mark = pass == c.cap_passes - 1;
-    MMBEV_TRY(launch_radix_pass(c, 1, pass, ck[pass & 1], cv[pass & 1], ck[1 - (pass & 1)], cv[1 - (pass & 1)],
-                                mark, s));
-  }
+  MMBEV_TRY(launch_cap(c, vals, s));
   MMBEV_TRY(launch_mean(c, keys, vals, s));
 #undef MMBEV_TRY
   if (ev.mark(s) != hipSuccess) return MMBEV_ERR_HIP;

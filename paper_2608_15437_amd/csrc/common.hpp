@@ -14,8 +14,14 @@ namespace mmbev {
 
 constexpr int kBlock = 256;           // threads per workgroup (4 wave64)
 constexpr int kWaves = kBlock / 64;
-constexpr int kFilterGroups = 4;      // float4 groups per thread in the filter
-constexpr int kFilterTile = kBlock * 4 * kFilterGroups;  // 4096 points
+constexpr int kFilterGroups = 4;      // max float4 groups per thread in the filter
+constexpr int kFilterTile = kBlock * 4 * kFilterGroups;  // 4096 points (largest filter tile)
+constexpr int kMaxLdsFrames = 64;     // frames of one filter tile whose offsets are staged in LDS
+constexpr int kMaxLdsRois = 512;      // ROI records of one filter tile staged in LDS
+constexpr int kMaxLdsBudgetWords = 1024;
+constexpr int kMaxSortLdsFrames = 4096;  // frame offsets staged in LDS by the sort and scan kernels
+constexpr int kMaxFilterGrid = 4096;     // persistent filter workgroups
+constexpr int kMaxSortChunks = 1024;     // chunks of a radix pass and of the head scan
 constexpr int kSortItems = 8;         // items per thread in a radix pass
 constexpr int kSortTile = kBlock * kSortItems;           // 2048 pairs
 constexpr int kSortBins = 256;        // max radix digit width 8 bits
@@ -35,9 +41,7 @@ constexpr uint32_t kValueMask = (1u << 30) - 1u;
 enum Slot : uint32_t {
   kSlotFilter = 0,
   kSlotSort0 = 1,        // .. kSlotSort0 + kMaxPasses - 1
-  kSlotCapSort0 = 7,     // .. + kMaxPasses - 1
-  kSlotUnique = 13,
-  kSlotMean = 14,
+  kSlotUnique = 7,
   kNumSlots = 16,
 };
 
@@ -49,9 +53,14 @@ struct alignas(256) WsHeader {
   uint32_t voxels;            // V, distinct voxels over all frames
   uint32_t capped_voxels;     // voxels of frames over the cap
   uint32_t any_capped;        // 1 if some frame exceeds max_voxels
-  uint32_t pad[2];
-  uint32_t tickets[kNumSlots];               // dynamic tile ids per launch
-  uint32_t hist[2][kMaxPasses][kSortBins];   // digit histograms: main sort, cap sort
+  uint32_t pad[10];
+  uint32_t hist[kMaxPasses][kSortBins];      // digit histograms of the radix passes
+};
+
+// Frame and ROI range of one filter tile, precomputed by the staging kernel.
+struct TileInfo {
+  int32_t f0, f1;      // frames of the tile's first and last point
+  int32_t r_lo, r_hi;  // ROIs of frames f0..f1 (clamped to [0, R])
 };
 
 // Everything a kernel needs, computed once on the host and passed by value.
@@ -69,12 +78,13 @@ struct Config {
   int32_t C, B, S, M, cap;
   int32_t R, max_rois, W;  // W: 32-bit mask words per cell
   float mn[3], vs[3], Df[3];
+  float inv_vs[3];         // 1/voxel_size, for the conservative cell lookup only
+  int32_t cell_pad;        // voxels added around each ROI's cell rectangle
   uint32_t Dx, Dy, Dz;
   int32_t cell_shift, ncx, ncy, ncells;
   // keys: key_local = (iz*Dy + iy)*Dx + ix < 2^kb; frame b above it
   int32_t kb, fb, key_has_frame;  // key_has_frame: kb + fb <= 32, key = b << kb | key_local
   int32_t passes, dbits;
-  int32_t cap_passes, cap_dbits;
   int32_t vec;  // 16-byte vector loads allowed
   // outputs
   int32_t* out_coords;
@@ -85,20 +95,22 @@ struct Config {
   // workspace
   WsHeader* hdr;
   uint32_t* cellmask;      // [B][ncells][W]
+  uint32_t* cellany;       // [B][ncells], OR of a cell's W words (== cellmask when W == 1)
   uint32_t* budgetmask;    // [B][S][W]
-  uint64_t* filter_status; // [filter tiles]
-  uint64_t* sort_status;   // [sort tiles][256]
-  uint64_t* scan_status;   // [scan tiles]
-  uint64_t* mean_status;   // [mean tiles]
+  TileInfo* tinfo;         // [filter tiles]
+  uint32_t* fcount;        // [filter_grid] kept pairs per filter workgroup
+  uint32_t* cnt;           // [256][max(filter_grid, sort_chunks)] digit counts -> offsets
+  uint32_t* tot;           // [256] digit totals of a radix pass
+  uint32_t* hcount;        // [sort_chunks] voxel heads per chunk
   uint32_t* keys[2];
   uint32_t* vals[2];
-  uint32_t* ckeys;         // cap sort scratch (with keys/vals of the other parity)
-  uint32_t* cvals;
+  uint32_t* capkey;        // [N] first point index of each voxel of a capped frame
+  uint32_t* out_rank;      // [N] row of a capped frame's voxel inside its frame, or ~0u
   uint32_t* seg_start;     // [N+1] first sorted position of voxel v
   uint32_t* vox_off;       // [B+1] first voxel of frame b
-  uint32_t* cap_off;       // [B+1] position of frame b among capped-frame voxels
-  uint8_t* keepflag;       // [N] per capped-frame voxel (key order)
-  int32_t filter_tiles, sort_grid, scan_grid, mean_grid;
+  int32_t filter_tiles, filter_groups, filter_tile_points;
+  int32_t filter_grid, filter_chunk_tiles, filter_chunk_points;  // persistent filter chunks
+  int32_t sort_chunks, mean_grid;
 };
 
 // ------------------------------------------------------------------ helpers
@@ -127,28 +139,68 @@ __device__ __forceinline__ void raise_fault(WsHeader* h, int32_t bits) {
   __hip_atomic_fetch_or(&h->fault, bits, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
-// Exclusive prefix of the tiles before `tile` for one look-back lane.
-// Walks back over aggregates until an inclusive prefix is found.  Waits are
-// bounded: on expiry the fault bit is raised and the partial sum returned.
-__device__ __forceinline__ uint32_t look_back(const uint64_t* status, int64_t tile, int64_t step, uint32_t tag,
-                                              WsHeader* h) {
-  uint32_t prefix = 0;
-  int64_t j = tile - 1;
-  while (j >= 0) {
-    uint64_t w;
-    uint32_t spins = 0;
-    for (;;) {
-      w = status_load(status + j * step);
-      if ((uint32_t)(w >> 32) == tag && ((uint32_t)w & (kFlagAgg | kFlagIncl))) break;
-      if (++spins >= kSpinLimit) {
-        raise_fault(h, MMBEV_FAULT_WAIT);
-        return prefix;
-      }
-      __builtin_amdgcn_s_sleep(1);
+// Wait until a look-back status word carries this launch's tag and a flag.
+// Bounded: on expiry the fault bit is raised and an inclusive zero returned.
+__device__ __forceinline__ uint64_t status_wait(const uint64_t* p, uint32_t tag, WsHeader* h) {
+  uint32_t spins = 0;
+  for (;;) {
+    const uint64_t w = status_load(p);
+    if ((uint32_t)(w >> 32) == tag && ((uint32_t)w & (kFlagAgg | kFlagIncl))) return w;
+    if (++spins >= kSpinLimit) {
+      raise_fault(h, MMBEV_FAULT_WAIT);
+      return status_word(tag, kFlagIncl, 0);
     }
-    prefix += (uint32_t)w & kValueMask;
-    if ((uint32_t)w & kFlagIncl) break;
-    --j;
+    __builtin_amdgcn_s_sleep(1);
+  }
+}
+
+// Exclusive prefix of the tiles before `tile` (one value per tile), computed
+// by one whole wave: each step reads 64 predecessors at once and stops at
+// the nearest one that already holds an inclusive prefix.  When many tiles
+// publish together, a lane-by-lane walk would cost one memory round trip per
+// predecessor; this costs one per 64.  Every lane returns the same value.
+__device__ __forceinline__ uint32_t look_back_wave(const uint64_t* status, int64_t tile, uint32_t tag, WsHeader* h) {
+  const int lane = threadIdx.x & 63;
+  uint32_t prefix = 0;
+  for (int64_t hi = tile - 1; hi >= 0; hi -= 64) {
+    const int64_t j = hi - lane;  // lane 0: nearest predecessor
+    uint32_t flag = kFlagIncl, val = 0;
+    if (j >= 0) {
+      const uint64_t w = status_wait(status + j, tag, h);
+      flag = (uint32_t)w & (kFlagAgg | kFlagIncl);
+      val = (uint32_t)w & kValueMask;
+    }
+    const uint64_t incl = __ballot(flag == kFlagIncl);
+    const int first = incl ? __builtin_ctzll(incl) : 64;
+    uint32_t x = lane <= first ? val : 0u;
+#pragma unroll
+    for (int d = 32; d >= 1; d >>= 1) x += __shfl_xor(x, d, 64);
+    prefix += x;
+    if (incl) break;
+  }
+  return prefix;
+}
+
+// Exclusive prefix of one digit over the tiles before `tile` (one thread per
+// digit; status words of tile j for this digit at status[j * step]).  Reads
+// kLookWindow predecessors per step with independent loads.
+constexpr int kLookWindow = 8;
+__device__ __forceinline__ uint32_t look_back_window(const uint64_t* status, int64_t tile, int64_t step,
+                                                     uint32_t tag, WsHeader* h) {
+  uint32_t prefix = 0;
+  for (int64_t hi = tile - 1; hi >= 0; hi -= kLookWindow) {
+    uint64_t w[kLookWindow];
+#pragma unroll
+    for (int k = 0; k < kLookWindow; ++k) w[k] = hi - k >= 0 ? status_load(status + (hi - k) * step) : 0ull;
+#pragma unroll
+    for (int k = 0; k < kLookWindow; ++k) {
+      if (hi - k < 0) return prefix;
+      uint64_t x = w[k];
+      if (!((uint32_t)(x >> 32) == tag && ((uint32_t)x & (kFlagAgg | kFlagIncl))))
+        x = status_wait(status + (hi - k) * step, tag, h);
+      prefix += (uint32_t)x & kValueMask;
+      if ((uint32_t)x & kFlagIncl) return prefix;
+    }
   }
   return prefix;
 }
@@ -175,6 +227,16 @@ __device__ __forceinline__ uint32_t block_exclusive_scan(uint32_t v, uint32_t* s
   __syncthreads();
   total = tot;
   return wpre + x - v;
+}
+
+// Chunk w of a compact array [0, K): kSortTile-aligned, at most G chunks,
+// visited in order (radix passes and the voxel head scan).
+__device__ __forceinline__ void chunk_range(uint32_t K, uint32_t w, uint32_t G, uint32_t& lo, uint32_t& hi) {
+  uint32_t cs = (K + G - 1) / G;
+  cs = (cs + kSortTile - 1) / kSortTile * kSortTile;
+  const uint64_t l = (uint64_t)w * cs;
+  lo = (uint32_t)min(l, (uint64_t)K);
+  hi = (uint32_t)min(l + cs, (uint64_t)K);
 }
 
 // Frame of point index i: largest b with off[b] <= i, clamped to [0, B-1].

@@ -11,7 +11,9 @@
 //
 // Block (0, 0) also opens the call: it bumps the epoch that tags look-back
 // words, clears the per-call counters and digit histograms, and checks the
-// frame offsets of points and ROIs.
+// frame offsets of points and ROIs.  The blocks of frame 0 also record, for
+// every tile of the point filter, its frame range and ROI range, so a filter
+// workgroup starts with one load instead of two binary searches.
 #include "launch.hpp"
 
 namespace mmbev {
@@ -43,8 +45,8 @@ __device__ void roi_cell_rect(const Config& c, const mmbev_roi_t& r, int16_t* ou
         double lo = (ctr[d] - half[d] - pad - (double)c.mn[d]) / (double)c.vs[d];
         double hi = (ctr[d] + half[d] + pad - (double)c.mn[d]) / (double)c.vs[d];
         double D = (double)c.Df[d];
-        lo = fmin(fmax(floor(lo) - 1.0, -1.0), D);
-        hi = fmin(fmax(floor(hi) + 1.0, -1.0), D);
+        lo = fmin(fmax(floor(lo) - (double)c.cell_pad, -1.0), D);
+        hi = fmin(fmax(floor(hi) + (double)c.cell_pad, -1.0), D);
         int32_t ilo = (int32_t)lo, ihi = (int32_t)hi;
         if (ihi < 0 || ilo >= (int32_t)D) {
           lim[d][0] = 1;
@@ -83,9 +85,8 @@ __global__ __launch_bounds__(kBlock) void stage_kernel(Config c) {
       h->capped_voxels = 0;
       h->any_capped = 0;
     }
-    for (int e = tid; e < kNumSlots; e += kBlock) h->tickets[e] = 0;
-    uint32_t* hist = &h->hist[0][0][0];
-    for (int e = tid; e < 2 * kMaxPasses * kSortBins; e += kBlock) hist[e] = 0;
+    uint32_t* hist = &h->hist[0][0];
+    for (int e = tid; e < kMaxPasses * kSortBins; e += kBlock) hist[e] = 0;
     __syncthreads();
     int32_t bad = 0;
     for (int f = tid; f <= c.B; f += kBlock) {
@@ -104,6 +105,19 @@ __global__ __launch_bounds__(kBlock) void stage_kernel(Config c) {
     if (bad) raise_fault(h, bad);
   }
 
+  // frame and ROI range of every filter tile (rows of frame 0 only)
+  if (b == 0)
+    for (int64_t t = (int64_t)blockIdx.x * kBlock + tid; t < c.filter_tiles; t += (int64_t)gridDim.x * kBlock) {
+      const int64_t first = t * c.filter_tile_points;
+      const int64_t last = min(first + c.filter_tile_points, (int64_t)c.N) - 1;
+      TileInfo ti;
+      ti.f0 = c.B == 1 ? 0 : frame_of_point(c.frame_off, c.B, first);
+      ti.f1 = c.B == 1 ? 0 : max(frame_of_point(c.frame_off, c.B, last), ti.f0);
+      ti.r_lo = min(max(c.roi_off[ti.f0], 0), c.R);
+      ti.r_hi = min(max(c.roi_off[ti.f1 + 1], ti.r_lo), c.R);
+      c.tinfo[t] = ti;
+    }
+
   // ROIs of frame b (offsets clamped into [0, R], count into [0, max_rois])
   int32_t r0 = min(max(c.roi_off[b], 0), c.R);
   int32_t r1 = min(max(c.roi_off[b + 1], r0), c.R);
@@ -111,22 +125,29 @@ __global__ __launch_bounds__(kBlock) void stage_kernel(Config c) {
   for (int j = tid; j < n; j += kBlock) roi_cell_rect(c, c.rois[r0 + j], s_rect[j]);
   __syncthreads();
 
+  // one thread per cell (all W words of it) or per (sweep, word) of the budget masks
   const int64_t cell_words = (int64_t)c.ncells * c.W;
-  const int64_t total = cell_words + (int64_t)c.S * c.W;
+  const int64_t total = (int64_t)c.ncells + (int64_t)c.S * c.W;
   for (int64_t e = (int64_t)blockIdx.x * kBlock + tid; e < total; e += (int64_t)gridDim.x * kBlock) {
-    uint32_t word = 0;
-    if (e < cell_words) {
-      int32_t cell = (int32_t)(e / c.W), w = (int32_t)(e % c.W);
-      int32_t cx = cell % c.ncx, cy = cell / c.ncx;
-      for (int k = 0; k < 32; ++k) {
-        int j = w * 32 + k;
-        if (j < n && cx >= s_rect[j][0] && cx <= s_rect[j][1] && cy >= s_rect[j][2] && cy <= s_rect[j][3])
-          word |= 1u << k;
+    if (e < c.ncells) {
+      const int32_t cell = (int32_t)e;
+      const int32_t cx = cell % c.ncx, cy = cell / c.ncx;
+      uint32_t any = 0;
+      for (int w = 0; w < c.W; ++w) {
+        uint32_t word = 0;
+        for (int k = 0; k < 32; ++k) {
+          int j = w * 32 + k;
+          if (j < n && cx >= s_rect[j][0] && cx <= s_rect[j][1] && cy >= s_rect[j][2] && cy <= s_rect[j][3])
+            word |= 1u << k;
+        }
+        c.cellmask[(int64_t)b * cell_words + (int64_t)cell * c.W + w] = word;
+        any |= word;
       }
-      c.cellmask[(int64_t)b * cell_words + e] = word;
+      if (c.W > 1) c.cellany[(int64_t)b * c.ncells + cell] = any;
     } else {
-      int64_t e2 = e - cell_words;
+      int64_t e2 = e - c.ncells;
       int32_t s = (int32_t)(e2 / c.W), w = (int32_t)(e2 % c.W);
+      uint32_t word = 0;
       for (int k = 0; k < 32; ++k) {
         int j = w * 32 + k;
         if (j < n && (int32_t)c.budget[r0 + j] > s) word |= 1u << k;
@@ -146,7 +167,7 @@ __global__ __launch_bounds__(kBlock) void fill_zero_kernel(uint4* p, size_t n16,
 }  // namespace
 
 hipError_t launch_stage(const Config& c, hipStream_t st) {
-  int64_t total = (int64_t)c.ncells * c.W + (int64_t)c.S * c.W;
+  int64_t total = std::max<int64_t>((int64_t)c.ncells + (int64_t)c.S * c.W, c.filter_tiles);
   int gx = (int)std::min<int64_t>((total + kBlock - 1) / kBlock, 128);
   hipLaunchKernelGGL(stage_kernel, dim3(gx, c.B), dim3(kBlock), 0, st, c);
   return hipGetLastError();

@@ -74,7 +74,7 @@ mmbev_status_t make_plan(const mmbev_grid_t* g, int64_t N, int32_t max_rois, int
   const int64_t n1 = std::max<int64_t>(N, 1);
   // filter tile: 1024 points per group of the 256 threads (two groups for
   // large inputs: more bytes in flight per workgroup)
-  p->filter_groups = N >= ((int64_t)1 << 21) ? 2 : 1;
+  p->filter_groups = 1;  // one float4 group per thread: the lowest register count
   p->filter_tiles = (N + 1024 * p->filter_groups - 1) / (1024 * p->filter_groups);
   p->sort_tiles = std::min<int64_t>(kMaxSortChunks, (n1 + kSortTile - 1) / kSortTile);
   size_t o = 0;
@@ -209,10 +209,18 @@ mmbev_status_t voxelize(const mmbev_points_t* points, const uint8_t* sweep_ids, 
     c.vs[d] = grid->voxel_size[d];
     c.Df[d] = (float)grid->dims[d];
     c.inv_vs[d] = (float)(1.0 / (double)grid->voxel_size[d]);
+    c.nmin_v[d] = (float)(-(double)grid->range_min[d] / (double)grid->voxel_size[d]);
   }
-  // the approximate cell lookup is off by less than one voxel while
-  // 3 * 2^-24 * D < 1; two voxels of padding keep it conservative
-  c.cell_pad = 2 + (std::max(grid->dims[0], grid->dims[1]) >> 21);
+  {
+    // the approximate cell lookup x'*(1/v) - min/v is off from the exact
+    // (x' - min)/v by at most (2|min/v| + D) * 2^-22 voxels for points that
+    // can be kept; pad every ROI's cell rectangle by one voxel more than that
+    double err = 0.0;
+    for (int d = 0; d < 2; ++d)
+      err = std::max(err, (2.0 * std::fabs((double)grid->range_min[d] / (double)grid->voxel_size[d]) +
+                           (double)grid->dims[d]) * std::ldexp(1.0, -22));
+    c.cell_pad = 2 + (int32_t)std::ceil(err);
+  }
   c.Dx = (uint32_t)grid->dims[0];
   c.Dy = (uint32_t)grid->dims[1];
   c.Dz = (uint32_t)grid->dims[2];

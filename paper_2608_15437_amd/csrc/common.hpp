@@ -14,11 +14,11 @@ namespace mmbev {
 
 constexpr int kBlock = 256;           // threads per workgroup (4 wave64)
 constexpr int kWaves = kBlock / 64;
-constexpr int kFilterGroups = 4;      // max float4 groups per thread in the filter
-constexpr int kFilterTile = kBlock * 4 * kFilterGroups;  // 4096 points (largest filter tile)
+constexpr int kFilterGroups = 2;      // max float4 groups per thread in the filter
+constexpr int kFilterQueue = 512;     // candidate points of a filter tile handled per segment
 constexpr int kMaxLdsFrames = 64;     // frames of one filter tile whose offsets are staged in LDS
-constexpr int kMaxLdsRois = 512;      // ROI records of one filter tile staged in LDS
-constexpr int kMaxLdsBudgetWords = 1024;
+constexpr int kMaxLdsRois = 256;      // ROI records of one filter chunk staged in LDS
+constexpr int kMaxLdsBudgetWords = 256;
 constexpr int kMaxSortLdsFrames = 4096;  // frame offsets staged in LDS by the sort and scan kernels
 constexpr int kMaxFilterGrid = 4096;     // persistent filter workgroups
 constexpr int kMaxSortChunks = 1024;     // chunks of a radix pass and of the head scan
@@ -79,6 +79,7 @@ struct Config {
   int32_t R, max_rois, W;  // W: 32-bit mask words per cell
   float mn[3], vs[3], Df[3];
   float inv_vs[3];         // 1/voxel_size, for the conservative cell lookup only
+  float nmin_v[3];         // -range_min/voxel_size, same use
   int32_t cell_pad;        // voxels added around each ROI's cell rectangle
   uint32_t Dx, Dy, Dz;
   int32_t cell_shift, ncx, ncy, ncells;

@@ -171,3 +171,42 @@ def test_throughput_batch_full_size(gpu_lib):
     """The benchmark's batched workload, every frame checked against the oracle."""
     wl = synth.throughput(16)
     check(gpu_lib, case_from_workload(wl), label="c2x16", desc=wl.roi_desc)
+
+
+def _face_lattice_case(pose_rows, voxel=(0.1, 0.15, 0.3), mn=(-3.7, -2.9, -1.3), dims=(60, 40, 10)):
+    """Points on voxel faces (and one ulp either side) of a non-dyadic grid,
+    all inside one ROI covering the grid: the voxel index of every point is
+    decided by the rounding of (p - min) / v, and every tile queues far more
+    candidates than one segment holds."""
+    f32 = np.float32
+    faces = []
+    for d in range(3):
+        k = np.arange(-1, dims[d] + 2, dtype=np.float64)
+        base = (f32(mn[d]) + k * f32(voxel[d])).astype(f32)
+        faces.append(np.unique(np.concatenate([base, np.nextafter(base, f32(np.inf)),
+                                               np.nextafter(base, f32(-np.inf))])))
+    zc = (f32(mn[2]) + (np.arange(dims[2]) + f32(0.5)) * f32(voxel[2])).astype(f32)
+    X, Y = np.meshgrid(faces[0], faces[1], indexing="ij")
+    xy = np.stack([X.ravel(), Y.ravel()], 0)
+    z = np.resize(np.concatenate([zc, faces[2]]), xy.shape[1]).astype(f32)
+    feat = np.ascontiguousarray(np.concatenate([xy, z[None], np.ones((1, xy.shape[1]), f32)], 0).astype(f32))
+    N = feat.shape[1]
+    cx = mn[0] + voxel[0] * dims[0] / 2
+    cy = mn[1] + voxel[1] * dims[1] / 2
+    rois = records([[cx, cy, 1.0, 0.0, 50.0, 50.0]])
+    poses = np.asarray(pose_rows, np.float32).reshape(1, 1, 12)
+    grid = dict(range_min=list(mn), voxel_size=list(voxel), dims=list(dims), max_points=3, max_voxels=100000,
+                num_sweeps=1, num_frames=1)
+    return Case(feat=feat, sweep_ids=np.zeros(N, np.uint8), frame_offsets=np.array([0, N]), poses=poses, rois=rois,
+                roi_offsets=np.array([0, 1], np.int32), budgets=np.array([1], np.uint8), grid=grid)
+
+
+def test_points_on_voxel_faces_and_full_queues(gpu_lib):
+    ident = [1, 0, 0, 0, 0, 1, 0, 0, 0, 0, 1, 0]
+    case = _face_lattice_case(ident)
+    assert case.feat.shape[1] > 8 * 1024
+    _, exp = check(gpu_lib, case, label="faces")
+    assert int(exp["voxel_offsets"][-1]) > 1000
+    # a translation by a non-dyadic offset moves the faces off the lattice
+    shifted = _face_lattice_case([1, 0, 0, 0.05, 0, 1, 0, -0.075, 0, 0, 1, 0.15])
+    check(gpu_lib, shifted, label="faces shifted")

@@ -25,7 +25,6 @@ struct Plan {
   int32_t cell_shift, ncx, ncy, ncells;
   int32_t kb, fb, key_has_frame, passes, dbits;
   int64_t filter_tiles, sort_tiles, mean_tiles;
-  int32_t filter_groups;
   size_t off_hdr, off_cellmask, off_cellany, off_budgetmask, off_tinfo, off_fcount, off_cnt, off_tot, off_hcount,
       off_keys0, off_vals0, off_keys1, off_vals1, off_capkey, off_rank, off_seg, off_voxoff, total;
 };
@@ -72,10 +71,7 @@ mmbev_status_t make_plan(const mmbev_grid_t* g, int64_t N, int32_t max_rois, int
   p->dbits = (total_bits + p->passes - 1) / p->passes;
 
   const int64_t n1 = std::max<int64_t>(N, 1);
-  // filter tile: 1024 points per group of the 256 threads (two groups for
-  // large inputs: more bytes in flight per workgroup)
-  p->filter_groups = 1;  // one float4 group per thread: the lowest register count
-  p->filter_tiles = (N + 1024 * p->filter_groups - 1) / (1024 * p->filter_groups);
+  p->filter_tiles = (N + kFilterTile - 1) / kFilterTile;
   p->sort_tiles = std::min<int64_t>(kMaxSortChunks, (n1 + kSortTile - 1) / kSortTile);
   size_t o = 0;
   auto take = [&](size_t bytes) {
@@ -88,8 +84,8 @@ mmbev_status_t make_plan(const mmbev_grid_t* g, int64_t N, int32_t max_rois, int
   p->off_cellany = p->W > 1 ? take((size_t)p->B * p->ncells * 4) : p->off_cellmask;
   p->off_budgetmask = take((size_t)p->B * p->S * p->W * 4);
   p->off_tinfo = take((size_t)std::max<int64_t>(p->filter_tiles, 1) * sizeof(TileInfo));
-  p->off_fcount = take((size_t)kMaxFilterGrid * 4);
-  p->off_cnt = take((size_t)kSortBins * std::max(kMaxFilterGrid, kMaxSortChunks) * 4);
+  p->off_fcount = take((size_t)kMaxFilterChunks * 4);
+  p->off_cnt = take((size_t)kSortBins * std::max(kMaxFilterChunks, kMaxSortChunks) * 4);
   p->off_tot = take((size_t)kSortBins * 4);
   p->off_hcount = take((size_t)kMaxSortChunks * 4);
   p->off_keys0 = take((size_t)n1 * 4);
@@ -259,15 +255,14 @@ mmbev_status_t voxelize(const mmbev_points_t* points, const uint8_t* sweep_ids, 
   c.seg_start = (uint32_t*)(ws + p.off_seg);
   c.vox_off = (uint32_t*)(ws + p.off_voxoff);
   c.filter_tiles = (int32_t)p.filter_tiles;
-  c.filter_groups = p.filter_groups;
-  c.filter_tile_points = 1024 * p.filter_groups;
   {
     // persistent filter: as many workgroups as fit on the device at once,
-    // each owning a contiguous chunk of tiles
+    // each owning a contiguous chunk of whole tiles split evenly between its
+    // waves
     int dev = 0, cus = 0, per_cu = 0;
     if (hipGetDevice(&dev) != hipSuccess ||
         hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
-        filter_occupancy(p.filter_groups, c.vec, &per_cu) != hipSuccess)
+        filter_occupancy(c.vec, &per_cu) != hipSuccess)
       return MMBEV_ERR_HIP;
     int64_t grid = std::max<int64_t>(1, (int64_t)std::max(per_cu, 1) * cus);
     grid = std::min<int64_t>(grid, kMaxFilterGrid);
@@ -275,7 +270,8 @@ mmbev_status_t voxelize(const mmbev_points_t* points, const uint8_t* sweep_ids, 
     const int64_t chunk = std::max<int64_t>(1, (p.filter_tiles + grid - 1) / grid);
     c.filter_chunk_tiles = (int32_t)chunk;
     c.filter_grid = (int32_t)std::max<int64_t>(1, (p.filter_tiles + chunk - 1) / chunk);
-    c.filter_chunk_points = (int32_t)(chunk * c.filter_tile_points);
+    c.filter_chunk_points = (int32_t)(chunk * kFilterTile / kWaves);
+    c.filter_chunks = (int32_t)std::max<int64_t>(1, (N + c.filter_chunk_points - 1) / c.filter_chunk_points);
   }
   c.sort_chunks = (int32_t)std::max<int64_t>(1, p.sort_tiles);
   c.mean_grid = (int32_t)std::min<int64_t>(p.mean_tiles, 2048);

@@ -14,13 +14,14 @@ namespace mmbev {
 
 constexpr int kBlock = 256;           // threads per workgroup (4 wave64)
 constexpr int kWaves = kBlock / 64;
-constexpr int kFilterGroups = 2;      // max float4 groups per thread in the filter
-constexpr int kFilterQueue = 512;     // candidate points of a filter tile handled per segment
-constexpr int kMaxLdsFrames = 64;     // frames of one filter tile whose offsets are staged in LDS
+constexpr int kFilterTile = 1024;     // points per filter tile (unit of the per-tile frame/ROI ranges)
+constexpr int kWaveQueue = 128;       // candidate ring of one filter wave (power of two, >= 128)
+constexpr int kMaxLdsFrames = 64;     // frames of one filter chunk whose offsets are staged in LDS
 constexpr int kMaxLdsRois = 256;      // ROI records of one filter chunk staged in LDS
 constexpr int kMaxLdsBudgetWords = 256;
 constexpr int kMaxSortLdsFrames = 4096;  // frame offsets staged in LDS by the sort and scan kernels
 constexpr int kMaxFilterGrid = 4096;     // persistent filter workgroups
+constexpr int kMaxFilterChunks = kMaxFilterGrid * kWaves;  // filter wave chunks
 constexpr int kMaxSortChunks = 1024;     // chunks of a radix pass and of the head scan
 constexpr int kSortItems = 8;         // items per thread in a radix pass
 constexpr int kSortTile = kBlock * kSortItems;           // 2048 pairs
@@ -29,7 +30,7 @@ constexpr int kMaxPasses = 6;         // 48 key bits
 constexpr int kScanItems = 16;        // items per thread in the head scan
 constexpr int kScanTile = kBlock * kScanItems;           // 4096 pairs
 constexpr int kMeanTile = kBlock;                        // one voxel per thread
-constexpr int kMaxPoseLds = 64;       // (frame, sweep) poses staged in LDS per tile
+constexpr int kMaxPoseLds = 64;       // (frame, sweep) poses staged in LDS per filter chunk
 constexpr uint32_t kSpinLimit = 1u << 20;
 
 // Look-back status word: [63:32] tag, [31:30] flag, [29:0] value.
@@ -99,8 +100,8 @@ struct Config {
   uint32_t* cellany;       // [B][ncells], OR of a cell's W words (== cellmask when W == 1)
   uint32_t* budgetmask;    // [B][S][W]
   TileInfo* tinfo;         // [filter tiles]
-  uint32_t* fcount;        // [filter_grid] kept pairs per filter workgroup
-  uint32_t* cnt;           // [256][max(filter_grid, sort_chunks)] digit counts -> offsets
+  uint32_t* fcount;        // [filter_chunks] kept pairs per filter wave chunk
+  uint32_t* cnt;           // [256][max(filter_chunks, sort_chunks)] digit counts -> offsets
   uint32_t* tot;           // [256] digit totals of a radix pass
   uint32_t* hcount;        // [sort_chunks] voxel heads per chunk
   uint32_t* keys[2];
@@ -109,8 +110,9 @@ struct Config {
   uint32_t* out_rank;      // [N] row of a capped frame's voxel inside its frame, or ~0u
   uint32_t* seg_start;     // [N+1] first sorted position of voxel v
   uint32_t* vox_off;       // [B+1] first voxel of frame b
-  int32_t filter_tiles, filter_groups, filter_tile_points;
-  int32_t filter_grid, filter_chunk_tiles, filter_chunk_points;  // persistent filter chunks
+  int32_t filter_tiles;                          // kFilterTile-point tiles
+  int32_t filter_grid, filter_chunk_tiles;       // persistent workgroups, tiles per workgroup
+  int32_t filter_chunks, filter_chunk_points;    // wave chunks (kWaves per workgroup), points per wave chunk
   int32_t sort_chunks, mean_grid;
 };
 

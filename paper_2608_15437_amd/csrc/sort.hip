@@ -13,7 +13,7 @@
 //              written from earlier tiles of the chunk.
 // Chunks are contiguous and visited in order, so the pass is stable.  The
 // first pass reads the point filter's output in place: chunk w of that pass
-// is filter workgroup w's region (kept pairs in point order, a gap after
+// is filter wave chunk w's region (kept pairs in point order, a gap after
 // them), and its digit counts come from the filter.
 //
 // Keys are voxel keys; the frame index is part of the key, either in its top
@@ -245,7 +245,7 @@ hipError_t launch_radix_pass(const Config& c, int pass, const uint32_t* kin, con
   const size_t dyn = frame_lds_bytes(c, pass);
   const int nbins = 1 << c.dbits;
   const bool first = pass == 0;
-  const int chunks = first ? c.filter_grid : c.sort_chunks;
+  const int chunks = first ? c.filter_chunks : c.sort_chunks;
   if (!first) {
     hipLaunchKernelGGL(count_kernel, dim3(chunks), dim3(kBlock), dyn, st, c, pass, kin, vin);
     const hipError_t e = hipGetLastError();

@@ -108,8 +108,8 @@ __global__ __launch_bounds__(kBlock) void stage_kernel(Config c) {
   // frame and ROI range of every filter tile (rows of frame 0 only)
   if (b == 0)
     for (int64_t t = (int64_t)blockIdx.x * kBlock + tid; t < c.filter_tiles; t += (int64_t)gridDim.x * kBlock) {
-      const int64_t first = t * c.filter_tile_points;
-      const int64_t last = min(first + c.filter_tile_points, (int64_t)c.N) - 1;
+      const int64_t first = t * kFilterTile;
+      const int64_t last = min(first + kFilterTile, (int64_t)c.N) - 1;
       TileInfo ti;
       ti.f0 = c.B == 1 ? 0 : frame_of_point(c.frame_off, c.B, first);
       ti.f1 = c.B == 1 ? 0 : max(frame_of_point(c.frame_off, c.B, last), ti.f0);

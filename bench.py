@@ -48,9 +48,9 @@ def launch_names(vz) -> list:
     g = vz.grid
     cells = g.dims[0] * g.dims[1] * g.dims[2]
     kb = max(1, (cells - 1).bit_length())
-    fb = (g.num_frames - 1).bit_length()
-    passes = (kb + fb + 7) // 8
-    return ["stage", "filter"] + [f"sort{p}" for p in range(passes)] + ["unique", "finalize", "cap", "mean"]
+    passes = (kb + 8) // 9  # digits of at most 9 bits; frames are kept apart, not sorted
+    return (["stage", "filter", "segments", "compact"] + [f"sort{p}" for p in range(passes)]
+            + ["unique", "finalize", "cap", "mean"])
 
 
 def time_calls(vz, steps: int, warmup: int) -> float:

@@ -23,10 +23,11 @@ struct Plan {
   int64_t N;
   int32_t B, S, C, M, cap, max_rois, W;
   int32_t cell_shift, ncx, ncy, ncells;
-  int32_t kb, fb, key_has_frame, passes, dbits;
-  int64_t filter_tiles, sort_tiles, mean_tiles;
-  size_t off_hdr, off_cellmask, off_cellany, off_budgetmask, off_tinfo, off_fcount, off_cnt, off_tot, off_hcount,
-      off_keys0, off_vals0, off_keys1, off_vals1, off_capkey, off_rank, off_seg, off_voxoff, total;
+  int32_t kb, passes, dbits;
+  int64_t fchunk_points, fchunk_max, filter_grid, schunk_max, mean_grid;
+  size_t off_hdr, off_cellmask, off_cellany, off_budgetmask, off_fchunk_first, off_fcount, off_fchunk_lo, off_fprefix,
+      off_fstart, off_schunk_first, off_schunk, off_cnt, off_ftot, off_hcount, off_vcount, off_keys[2], off_vals[2], off_seg,
+      off_capkey, off_rank, off_voxoff, total;
 };
 
 mmbev_status_t make_plan(const mmbev_grid_t* g, int64_t N, int32_t max_rois, int32_t C, Plan* p) {
@@ -64,15 +65,23 @@ mmbev_status_t make_plan(const mmbev_grid_t* g, int64_t N, int32_t max_rois, int
   p->ncy = (int32_t)(((int64_t)g->dims[1] + (1 << cs) - 1) >> cs);
   p->ncells = p->ncx * p->ncy;
   p->kb = std::max(1, bits_for(cells - 1));
-  p->fb = bits_for((uint64_t)(p->B - 1));
-  const int total_bits = p->kb + p->fb;
-  p->key_has_frame = total_bits <= 32 ? 1 : 0;
-  p->passes = (total_bits + 7) / 8;
-  p->dbits = (total_bits + p->passes - 1) / p->passes;
+  p->passes = (p->kb + kMaxDigitBits - 1) / kMaxDigitBits;
+  p->dbits = (p->kb + p->passes - 1) / p->passes;
 
   const int64_t n1 = std::max<int64_t>(N, 1);
-  p->filter_tiles = (N + kFilterTile - 1) / kFilterTile;
-  p->sort_tiles = std::min<int64_t>(kMaxSortChunks, (n1 + kSortTile - 1) / kSortTile);
+  // filter chunks: about kFilterWaveTarget of them over the whole input (one
+  // per resident wave), a multiple of the wave tile; frames add at most one
+  // partial chunk each
+  {
+    const int64_t target = kFilterWaveTarget > 2 * (int64_t)p->B ? kFilterWaveTarget - p->B : kFilterWaveTarget;
+    int64_t P = (N + target - 1) / target;
+    P = std::max<int64_t>(kWaveTile, (P + kWaveTile - 1) / kWaveTile * kWaveTile);
+    p->fchunk_points = P;
+    p->fchunk_max = (N + P - 1) / P + p->B;
+    p->filter_grid = std::max<int64_t>(1, (p->fchunk_max + kWaves - 1) / kWaves);
+  }
+  p->schunk_max = kSortGrid + p->B;
+  p->mean_grid = std::max<int64_t>(1, std::min<int64_t>((n1 + kMeanTile - 1) / kMeanTile, 2048));
   size_t o = 0;
   auto take = [&](size_t bytes) {
     size_t at = o;
@@ -83,18 +92,24 @@ mmbev_status_t make_plan(const mmbev_grid_t* g, int64_t N, int32_t max_rois, int
   p->off_cellmask = take((size_t)p->B * p->ncells * p->W * 4);
   p->off_cellany = p->W > 1 ? take((size_t)p->B * p->ncells * 4) : p->off_cellmask;
   p->off_budgetmask = take((size_t)p->B * p->S * p->W * 4);
-  p->off_tinfo = take((size_t)std::max<int64_t>(p->filter_tiles, 1) * sizeof(TileInfo));
-  p->off_fcount = take((size_t)kMaxFilterChunks * 4);
-  p->off_cnt = take((size_t)kSortBins * std::max(kMaxFilterChunks, kMaxSortChunks) * 4);
-  p->off_tot = take((size_t)kSortBins * 4);
-  p->off_hcount = take((size_t)kMaxSortChunks * 4);
-  p->off_keys0 = take((size_t)n1 * 4);
-  p->off_vals0 = take((size_t)n1 * 4);
-  p->off_keys1 = take((size_t)n1 * 4);
-  p->off_vals1 = take((size_t)n1 * 4);
+  p->off_fchunk_first = take((size_t)(p->B + 1) * 4);
+  p->off_fcount = take((size_t)p->fchunk_max * 4);
+  p->off_fchunk_lo = take((size_t)p->fchunk_max * 4);
+  p->off_fprefix = take((size_t)(p->fchunk_max + 1) * 4);
+  p->off_fstart = take((size_t)(p->B + 1) * 4);
+  p->off_schunk_first = take((size_t)(p->B + 1) * 4);
+  p->off_schunk = take((size_t)p->schunk_max * 16);
+  p->off_cnt = take((size_t)p->schunk_max * kSortBins * 4);
+  p->off_ftot = take((size_t)p->B * kSortBins * 4);
+  p->off_hcount = take((size_t)p->schunk_max * 4);
+  p->off_vcount = take((size_t)p->B * 4);
+  for (int q = 0; q < 2; ++q) {
+    p->off_keys[q] = take((size_t)n1 * 4);
+    p->off_vals[q] = take((size_t)n1 * 4);
+  }
+  p->off_seg = take((size_t)n1 * 4);
   p->off_capkey = take((size_t)n1 * 4);
   p->off_rank = take((size_t)n1 * 4);
-  p->off_seg = take((size_t)(N + 1) * 4);
   p->off_voxoff = take((size_t)(p->B + 1) * 4);
   p->total = o;
   return MMBEV_OK;
@@ -225,8 +240,6 @@ mmbev_status_t voxelize(const mmbev_points_t* points, const uint8_t* sweep_ids, 
   c.ncy = p.ncy;
   c.ncells = p.ncells;
   c.kb = p.kb;
-  c.fb = p.fb;
-  c.key_has_frame = p.key_has_frame;
   c.passes = p.passes;
   c.dbits = p.dbits;
   c.vec = (((uintptr_t)points->feat & 15) == 0 && (points->stride & 3) == 0 && ((uintptr_t)sweep_ids & 3) == 0) ? 1
@@ -241,40 +254,30 @@ mmbev_status_t voxelize(const mmbev_points_t* points, const uint8_t* sweep_ids, 
   c.cellmask = (uint32_t*)(ws + p.off_cellmask);
   c.cellany = (uint32_t*)(ws + p.off_cellany);
   c.budgetmask = (uint32_t*)(ws + p.off_budgetmask);
-  c.tinfo = (TileInfo*)(ws + p.off_tinfo);
+  c.fchunk_first = (uint32_t*)(ws + p.off_fchunk_first);
   c.fcount = (uint32_t*)(ws + p.off_fcount);
+  c.fchunk_lo = (uint32_t*)(ws + p.off_fchunk_lo);
+  c.fprefix = (uint32_t*)(ws + p.off_fprefix);
+  c.fstart = (uint32_t*)(ws + p.off_fstart);
+  c.schunk_first = (uint32_t*)(ws + p.off_schunk_first);
+  c.schunk = (uint4*)(ws + p.off_schunk);
   c.cnt = (uint32_t*)(ws + p.off_cnt);
-  c.tot = (uint32_t*)(ws + p.off_tot);
+  c.ftot = (uint32_t*)(ws + p.off_ftot);
   c.hcount = (uint32_t*)(ws + p.off_hcount);
-  c.keys[0] = (uint32_t*)(ws + p.off_keys0);
-  c.vals[0] = (uint32_t*)(ws + p.off_vals0);
-  c.keys[1] = (uint32_t*)(ws + p.off_keys1);
-  c.vals[1] = (uint32_t*)(ws + p.off_vals1);
+  c.vcount = (uint32_t*)(ws + p.off_vcount);
+  for (int q = 0; q < 2; ++q) {
+    c.keys[q] = (uint32_t*)(ws + p.off_keys[q]);
+    c.vals[q] = (uint32_t*)(ws + p.off_vals[q]);
+  }
+  c.seg_start = (uint32_t*)(ws + p.off_seg);
   c.capkey = (uint32_t*)(ws + p.off_capkey);
   c.out_rank = (uint32_t*)(ws + p.off_rank);
-  c.seg_start = (uint32_t*)(ws + p.off_seg);
   c.vox_off = (uint32_t*)(ws + p.off_voxoff);
-  c.filter_tiles = (int32_t)p.filter_tiles;
-  {
-    // persistent filter: as many workgroups as fit on the device at once,
-    // each owning a contiguous chunk of whole tiles split evenly between its
-    // waves
-    int dev = 0, cus = 0, per_cu = 0;
-    if (hipGetDevice(&dev) != hipSuccess ||
-        hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
-        filter_occupancy(c.vec, &per_cu) != hipSuccess)
-      return MMBEV_ERR_HIP;
-    int64_t grid = std::max<int64_t>(1, (int64_t)std::max(per_cu, 1) * cus);
-    grid = std::min<int64_t>(grid, kMaxFilterGrid);
-    grid = std::max<int64_t>(1, std::min<int64_t>(grid, p.filter_tiles));
-    const int64_t chunk = std::max<int64_t>(1, (p.filter_tiles + grid - 1) / grid);
-    c.filter_chunk_tiles = (int32_t)chunk;
-    c.filter_grid = (int32_t)std::max<int64_t>(1, (p.filter_tiles + chunk - 1) / chunk);
-    c.filter_chunk_points = (int32_t)(chunk * kFilterTile / kWaves);
-    c.filter_chunks = (int32_t)std::max<int64_t>(1, (N + c.filter_chunk_points - 1) / c.filter_chunk_points);
-  }
-  c.sort_chunks = (int32_t)std::max<int64_t>(1, p.sort_tiles);
-  c.mean_grid = (int32_t)std::min<int64_t>(p.mean_tiles, 2048);
+  c.fchunk_points = (int32_t)p.fchunk_points;
+  c.fchunk_max = (int32_t)p.fchunk_max;
+  c.filter_grid = (int32_t)p.filter_grid;
+  c.schunk_max = (int32_t)p.schunk_max;
+  c.mean_grid = (int32_t)p.mean_grid;
 
   hipStream_t s = (hipStream_t)stream;
 #define MMBEV_TRY(call)                                                   \
@@ -284,15 +287,16 @@ mmbev_status_t voxelize(const mmbev_points_t* points, const uint8_t* sweep_ids, 
 
   MMBEV_TRY(launch_stage(c, s));
   MMBEV_TRY(launch_filter(c, s));
-  int cur = 0;
-  for (int pass = 0; pass < c.passes; ++pass) {
-    MMBEV_TRY(launch_radix_pass(c, pass, c.keys[cur], c.vals[cur], c.keys[1 - cur], c.vals[1 - cur], s));
-    cur = 1 - cur;
-  }
-  const uint32_t* keys = c.keys[cur];
-  const uint32_t* vals = c.vals[cur];
-  MMBEV_TRY(launch_unique(c, keys, vals, s));
-  MMBEV_TRY(launch_finalize(c, keys, vals, s));
+  // sorted pairs ping-pong: compacted into [1], pass p writes [p % 2]
+  MMBEV_TRY(launch_segments(c, s));
+  MMBEV_TRY(launch_compact(c, c.keys[1], c.vals[1], s));
+  for (int pass = 0; pass < c.passes; ++pass)
+    MMBEV_TRY(launch_radix_pass(c, pass, c.keys[1 - pass % 2], c.vals[1 - pass % 2], c.keys[pass % 2],
+                                c.vals[pass % 2], s));
+  const uint32_t* keys = c.keys[(c.passes - 1) % 2];
+  const uint32_t* vals = c.vals[(c.passes - 1) % 2];
+  MMBEV_TRY(launch_unique(c, keys, s));
+  MMBEV_TRY(launch_finalize(c, s));
   MMBEV_TRY(launch_cap(c, vals, s));
   MMBEV_TRY(launch_mean(c, keys, vals, s));
 #undef MMBEV_TRY

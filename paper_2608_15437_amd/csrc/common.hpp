@@ -14,54 +14,36 @@ namespace mmbev {
 
 constexpr int kBlock = 256;           // threads per workgroup (4 wave64)
 constexpr int kWaves = kBlock / 64;
-constexpr int kFilterTile = 1024;     // points per filter tile (unit of the per-tile frame/ROI ranges)
+// point filter
+constexpr int kWaveTile = 256;        // points per filter wave tile (64 lanes x 4)
 constexpr int kWaveQueue = 128;       // candidate ring of one filter wave (power of two, >= 128)
-constexpr int kMaxLdsFrames = 64;     // frames of one filter chunk whose offsets are staged in LDS
-constexpr int kMaxLdsRois = 256;      // ROI records of one filter chunk staged in LDS
+constexpr int kFilterWaveTarget = 5120;  // filter wave chunks aimed for (about one per resident wave)
+constexpr int kMaxLdsFrames = 64;     // frames of one filter workgroup staged in LDS
+constexpr int kMaxLdsRois = 256;      // ROI records of one filter workgroup staged in LDS
 constexpr int kMaxLdsBudgetWords = 256;
-constexpr int kMaxSortLdsFrames = 4096;  // frame offsets staged in LDS by the sort and scan kernels
-constexpr int kMaxFilterGrid = 4096;     // persistent filter workgroups
-constexpr int kMaxFilterChunks = kMaxFilterGrid * kWaves;  // filter wave chunks
-constexpr int kMaxSortChunks = 1024;     // chunks of a radix pass and of the head scan
-constexpr int kSortItems = 8;         // items per thread in a radix pass
-constexpr int kSortTile = kBlock * kSortItems;           // 2048 pairs
-constexpr int kSortBins = 256;        // max radix digit width 8 bits
-constexpr int kMaxPasses = 6;         // 48 key bits
-constexpr int kScanItems = 16;        // items per thread in the head scan
-constexpr int kScanTile = kBlock * kScanItems;           // 4096 pairs
-constexpr int kMeanTile = kBlock;                        // one voxel per thread
-constexpr int kMaxPoseLds = 64;       // (frame, sweep) poses staged in LDS per filter chunk
-constexpr uint32_t kSpinLimit = 1u << 20;
+constexpr int kMaxPoseLds = 64;       // (frame, sweep) poses of one filter workgroup staged in LDS
+// radix passes (segmented by frame) and the voxel head scan
+constexpr int kMaxDigitBits = 9;
+constexpr int kSortBins = 1 << kMaxDigitBits;  // 512
+constexpr int kSortItems = 8;         // pairs per thread in a scatter tile
+constexpr int kSortTile = kBlock * kSortItems;  // 2048 pairs
+constexpr int kCountItems = 16;       // pairs per thread per batch of the count kernel
+constexpr int kSortGrid = 1024;       // pair chunks aimed for (chunks never straddle frames)
+constexpr int kScanItems = 16;        // items per thread in the single-workgroup scans
+constexpr int kScanTile = kBlock * kScanItems;  // 4096
+constexpr int kMeanTile = kBlock;     // one voxel per thread
 
-// Look-back status word: [63:32] tag, [31:30] flag, [29:0] value.
-constexpr uint32_t kFlagAgg = 1u << 30;
-constexpr uint32_t kFlagIncl = 2u << 30;
-constexpr uint32_t kValueMask = (1u << 30) - 1u;
-
-// Tag slots of the look-back launches of one call.
-enum Slot : uint32_t {
-  kSlotFilter = 0,
-  kSlotSort0 = 1,        // .. kSlotSort0 + kMaxPasses - 1
-  kSlotUnique = 7,
-  kNumSlots = 16,
-};
-
-// Workspace header: per-call counters, rewritten by the first kernel of a call.
+// Workspace header: per-call counters, rewritten by the first kernels of a call.
 struct alignas(256) WsHeader {
   int32_t fault;              // byte 0: MMBEV_FAULT_* bits of the last call
-  uint32_t epoch;             // call counter; tags look-back words
+  uint32_t epoch;             // call counter
   uint32_t kept;              // K, kept points
   uint32_t voxels;            // V, distinct voxels over all frames
   uint32_t capped_voxels;     // voxels of frames over the cap
   uint32_t any_capped;        // 1 if some frame exceeds max_voxels
-  uint32_t pad[10];
-  uint32_t hist[kMaxPasses][kSortBins];      // digit histograms of the radix passes
-};
-
-// Frame and ROI range of one filter tile, precomputed by the staging kernel.
-struct TileInfo {
-  int32_t f0, f1;      // frames of the tile's first and last point
-  int32_t r_lo, r_hi;  // ROIs of frames f0..f1 (clamped to [0, R])
+  uint32_t fchunks;           // filter chunks (points of one frame each)
+  uint32_t schunks;           // pair chunks (pairs of one frame each)
+  uint32_t chunk_pairs;       // pairs per pair chunk (the last chunk of a frame: fewer)
 };
 
 // Everything a kernel needs, computed once on the host and passed by value.
@@ -79,14 +61,14 @@ struct Config {
   int32_t C, B, S, M, cap;
   int32_t R, max_rois, W;  // W: 32-bit mask words per cell
   float mn[3], vs[3], Df[3];
-  float inv_vs[3];         // 1/voxel_size, for the conservative cell lookup only
-  float nmin_v[3];         // -range_min/voxel_size, same use
+  float inv_vs[3];         // 1/voxel_size, for the conservative cell lookup and the quantisation shortcut
+  float nmin_v[3];         // -range_min/voxel_size, for the cell lookup only
   int32_t cell_pad;        // voxels added around each ROI's cell rectangle
   uint32_t Dx, Dy, Dz;
   int32_t cell_shift, ncx, ncy, ncells;
-  // keys: key_local = (iz*Dy + iy)*Dx + ix < 2^kb; frame b above it
-  int32_t kb, fb, key_has_frame;  // key_has_frame: kb + fb <= 32, key = b << kb | key_local
-  int32_t passes, dbits;
+  // keys: (iz*Dy + iy)*Dx + ix < 2^kb, sorted within each frame in `passes`
+  // least-significant-digit passes of dbits bits
+  int32_t kb, passes, dbits;
   int32_t vec;  // 16-byte vector loads allowed
   // outputs
   int32_t* out_coords;
@@ -99,117 +81,45 @@ struct Config {
   uint32_t* cellmask;      // [B][ncells][W]
   uint32_t* cellany;       // [B][ncells], OR of a cell's W words (== cellmask when W == 1)
   uint32_t* budgetmask;    // [B][S][W]
-  TileInfo* tinfo;         // [filter tiles]
-  uint32_t* fcount;        // [filter_chunks] kept pairs per filter wave chunk
-  uint32_t* cnt;           // [256][max(filter_chunks, sort_chunks)] digit counts -> offsets
-  uint32_t* tot;           // [256] digit totals of a radix pass
-  uint32_t* hcount;        // [sort_chunks] voxel heads per chunk
-  uint32_t* keys[2];
-  uint32_t* vals[2];
-  uint32_t* capkey;        // [N] first point index of each voxel of a capped frame
-  uint32_t* out_rank;      // [N] row of a capped frame's voxel inside its frame, or ~0u
-  uint32_t* seg_start;     // [N+1] first sorted position of voxel v
-  uint32_t* vox_off;       // [B+1] first voxel of frame b
-  int32_t filter_tiles;                          // kFilterTile-point tiles
-  int32_t filter_grid, filter_chunk_tiles;       // persistent workgroups, tiles per workgroup
-  int32_t filter_chunks, filter_chunk_points;    // wave chunks (kWaves per workgroup), points per wave chunk
-  int32_t sort_chunks, mean_grid;
+  uint32_t* fchunk_first;  // [B+1] first filter chunk of frame b
+  uint32_t* fcount;        // [fchunk_max] kept pairs of filter chunk k
+  uint32_t* fchunk_lo;     // [fchunk_max] first point of filter chunk k (its kept pairs start there)
+  uint32_t* fprefix;       // [fchunk_max + 1] kept pairs of the filter chunks before k
+  uint32_t* fstart;        // [B+1] first sorted pair of frame b (kept pairs of the frames before it)
+  uint32_t* schunk_first;  // [B+1] first pair chunk of frame b
+  uint4* schunk;           // [schunk_max] pair chunk k: (first pair, end, frame, first pair of the frame)
+  uint32_t* cnt;           // [schunk_max][kSortBins] digit counts of a pass -> offsets inside the frame
+  uint32_t* ftot;          // [B][kSortBins] digit totals of every frame
+  uint32_t* hcount;        // [schunk_max] voxel heads of pair chunk k
+  uint32_t* vcount;        // [B] voxels of frame b
+  uint32_t* keys[2];       // [N] each: [0] first holds the filter's per-chunk regions
+  uint32_t* vals[2];       // point index of the pair
+  // per voxel, at slot fstart[b] + v for voxel v of frame b
+  uint32_t* seg_start;     // [N] first sorted pair of the voxel
+  uint32_t* capkey;        // [N] first point index of the voxel (frames over the cap)
+  uint32_t* out_rank;      // [N] row inside its frame, or ~0u (frames over the cap)
+  uint32_t* vox_off;       // [B+1] voxels of the frames before b
+  // sizes
+  int32_t fchunk_points;   // points per filter chunk (a multiple of kWaveTile)
+  int32_t fchunk_max;      // bound on filter chunks: ceil(N / fchunk_points) + B
+  int32_t filter_grid;     // ceil(fchunk_max / kWaves) workgroups, one chunk per wave
+  int32_t schunk_max;      // bound on pair chunks: kSortGrid + B
+  int32_t mean_grid;
 };
 
 // ------------------------------------------------------------------ helpers
-__device__ __forceinline__ uint32_t lane_id() { return __lane_id(); }
-
 __device__ __forceinline__ uint64_t lanemask_lt() {
   uint32_t l = __lane_id();
   return l == 0 ? 0ull : (~0ull >> (64 - l));
-}
-
-__device__ __forceinline__ uint32_t tag_of(uint32_t epoch, uint32_t slot) { return epoch * kNumSlots + slot; }
-
-__device__ __forceinline__ uint64_t status_word(uint32_t tag, uint32_t flag, uint32_t value) {
-  return ((uint64_t)tag << 32) | (uint64_t)(flag | (value & kValueMask));
-}
-
-__device__ __forceinline__ void status_store(uint64_t* p, uint64_t w) {
-  __hip_atomic_store(p, w, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
-
-__device__ __forceinline__ uint64_t status_load(const uint64_t* p) {
-  return __hip_atomic_load(const_cast<uint64_t*>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
 __device__ __forceinline__ void raise_fault(WsHeader* h, int32_t bits) {
   __hip_atomic_fetch_or(&h->fault, bits, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
-// Wait until a look-back status word carries this launch's tag and a flag.
-// Bounded: on expiry the fault bit is raised and an inclusive zero returned.
-__device__ __forceinline__ uint64_t status_wait(const uint64_t* p, uint32_t tag, WsHeader* h) {
-  uint32_t spins = 0;
-  for (;;) {
-    const uint64_t w = status_load(p);
-    if ((uint32_t)(w >> 32) == tag && ((uint32_t)w & (kFlagAgg | kFlagIncl))) return w;
-    if (++spins >= kSpinLimit) {
-      raise_fault(h, MMBEV_FAULT_WAIT);
-      return status_word(tag, kFlagIncl, 0);
-    }
-    __builtin_amdgcn_s_sleep(1);
-  }
-}
-
-// Exclusive prefix of the tiles before `tile` (one value per tile), computed
-// by one whole wave: each step reads 64 predecessors at once and stops at
-// the nearest one that already holds an inclusive prefix.  When many tiles
-// publish together, a lane-by-lane walk would cost one memory round trip per
-// predecessor; this costs one per 64.  Every lane returns the same value.
-__device__ __forceinline__ uint32_t look_back_wave(const uint64_t* status, int64_t tile, uint32_t tag, WsHeader* h) {
-  const int lane = threadIdx.x & 63;
-  uint32_t prefix = 0;
-  for (int64_t hi = tile - 1; hi >= 0; hi -= 64) {
-    const int64_t j = hi - lane;  // lane 0: nearest predecessor
-    uint32_t flag = kFlagIncl, val = 0;
-    if (j >= 0) {
-      const uint64_t w = status_wait(status + j, tag, h);
-      flag = (uint32_t)w & (kFlagAgg | kFlagIncl);
-      val = (uint32_t)w & kValueMask;
-    }
-    const uint64_t incl = __ballot(flag == kFlagIncl);
-    const int first = incl ? __builtin_ctzll(incl) : 64;
-    uint32_t x = lane <= first ? val : 0u;
-#pragma unroll
-    for (int d = 32; d >= 1; d >>= 1) x += __shfl_xor(x, d, 64);
-    prefix += x;
-    if (incl) break;
-  }
-  return prefix;
-}
-
-// Exclusive prefix of one digit over the tiles before `tile` (one thread per
-// digit; status words of tile j for this digit at status[j * step]).  Reads
-// kLookWindow predecessors per step with independent loads.
-constexpr int kLookWindow = 8;
-__device__ __forceinline__ uint32_t look_back_window(const uint64_t* status, int64_t tile, int64_t step,
-                                                     uint32_t tag, WsHeader* h) {
-  uint32_t prefix = 0;
-  for (int64_t hi = tile - 1; hi >= 0; hi -= kLookWindow) {
-    uint64_t w[kLookWindow];
-#pragma unroll
-    for (int k = 0; k < kLookWindow; ++k) w[k] = hi - k >= 0 ? status_load(status + (hi - k) * step) : 0ull;
-#pragma unroll
-    for (int k = 0; k < kLookWindow; ++k) {
-      if (hi - k < 0) return prefix;
-      uint64_t x = w[k];
-      if (!((uint32_t)(x >> 32) == tag && ((uint32_t)x & (kFlagAgg | kFlagIncl))))
-        x = status_wait(status + (hi - k) * step, tag, h);
-      prefix += (uint32_t)x & kValueMask;
-      if ((uint32_t)x & kFlagIncl) return prefix;
-    }
-  }
-  return prefix;
-}
-
-// Exclusive prefix over the workgroup (kBlock threads, all must call);
-// s_tmp holds kWaves words of LDS.  Returns the prefix, sets total.
+// Exclusive prefix over the workgroup (WAVES wave64s, all threads must
+// call); s_tmp holds WAVES words of LDS.  Returns the prefix, sets total.
+template <int WAVES = kWaves>
 __device__ __forceinline__ uint32_t block_exclusive_scan(uint32_t v, uint32_t* s_tmp, uint32_t& total) {
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   uint32_t x = v;
@@ -222,7 +132,7 @@ __device__ __forceinline__ uint32_t block_exclusive_scan(uint32_t v, uint32_t* s
   __syncthreads();
   uint32_t wpre = 0, tot = 0;
 #pragma unroll
-  for (int w = 0; w < kWaves; ++w) {
+  for (int w = 0; w < WAVES; ++w) {
     uint32_t t = s_tmp[w];
     wpre += (w < wave) ? t : 0u;
     tot += t;
@@ -232,27 +142,33 @@ __device__ __forceinline__ uint32_t block_exclusive_scan(uint32_t v, uint32_t* s
   return wpre + x - v;
 }
 
-// Chunk w of a compact array [0, K): kSortTile-aligned, at most G chunks,
-// visited in order (radix passes and the voxel head scan).
-__device__ __forceinline__ void chunk_range(uint32_t K, uint32_t w, uint32_t G, uint32_t& lo, uint32_t& hi) {
-  uint32_t cs = (K + G - 1) / G;
-  cs = (cs + kSortTile - 1) / kSortTile * kSortTile;
-  const uint64_t l = (uint64_t)w * cs;
-  lo = (uint32_t)min(l, (uint64_t)K);
-  hi = (uint32_t)min(l + cs, (uint64_t)K);
-}
-
-// Frame of point index i: largest b with off[b] <= i, clamped to [0, B-1].
-__device__ __forceinline__ int32_t frame_of_point(const int64_t* off, int32_t B, int64_t i) {
+// Largest b in [0, B-1] with first[b] <= k (first[] non-decreasing): the
+// frame of chunk k, skipping frames without chunks.
+__device__ __forceinline__ int32_t frame_of_chunk(const uint32_t* first, int32_t B, uint32_t k) {
   int32_t lo = 0, hi = B - 1;
   while (lo < hi) {
-    int32_t mid = (lo + hi + 1) >> 1;
-    if (off[mid] <= i)
+    const int32_t mid = (lo + hi + 1) >> 1;
+    if (first[mid] <= k)
       lo = mid;
     else
       hi = mid - 1;
   }
   return lo;
+}
+
+// Point frame offset b clamped into [0, N].
+__device__ __forceinline__ uint32_t point_offset(const Config& c, int32_t b) {
+  return (uint32_t)min(max(c.frame_off[b], (int64_t)0), (int64_t)c.N);
+}
+
+// Points [lo, hi) of filter chunk k of frame b (chunk j = k - first[b] of
+// the frame); empty for invalid offsets.
+__device__ __forceinline__ void filter_chunk_points(const Config& c, int32_t b, uint32_t k, uint32_t& lo,
+                                                    uint32_t& hi) {
+  const uint32_t f0 = point_offset(c, b), f1 = max(point_offset(c, b + 1), f0);
+  const uint64_t l = (uint64_t)f0 + (uint64_t)(k - c.fchunk_first[b]) * (uint32_t)c.fchunk_points;
+  lo = (uint32_t)min(l, (uint64_t)f1);
+  hi = (uint32_t)min(l + (uint32_t)c.fchunk_points, (uint64_t)f1);
 }
 
 // ------------------------------------------------ pinned point arithmetic

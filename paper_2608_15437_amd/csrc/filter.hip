@@ -19,16 +19,17 @@
 //      exact box test and the key.  The keep decision is therefore exactly
 //      the definition's.
 //
-// The waves of a workgroup share the LDS copy of the chunk's poses, budget
-// masks, ROI records and frame offsets (staged once, behind the only
-// workgroup barriers) and are otherwise independent: wave k of the grid owns
-// the contiguous points [k*P, (k+1)*P) and appends its kept pairs, in point
-// order, to its own output region starting at k*P.  Nothing waits on another
+// Wave k of the grid owns filter chunk k: a contiguous run of at most
+// fchunk_points points inside one frame (the chunk table is laid out by the
+// staging kernel).  The waves of a workgroup share the LDS copy of their
+// frames' poses, budget masks, ROI records and ROI offsets (staged once,
+// behind the only workgroup barriers) and are otherwise independent: a wave
+// appends its kept pairs, in point order, to its own output region, which
+// starts at the chunk's first point index.  Nothing waits on another
 // wave: a chained scan across workgroups costs one memory round trip per
 // predecessor when many publish together, and workgroup barriers leave the
-// waves without candidates idle.  The regions are compacted for free by the
-// first radix pass, which reads them in place using the per-wave counts and
-// first-digit histograms left here.
+// waves without candidates idle.  Each frame's sort gathers its chunks'
+// regions using the per-chunk counts left here.
 //
 // Per wave tile (256 points, four consecutive points per lane, one 16-byte
 // load per column and lane) the order is: phase A (its cell-mask loads
@@ -41,22 +42,18 @@ namespace mmbev {
 
 namespace {
 
-constexpr int kWaveTile = 256;  // points per wave tile (64 lanes x 4)
-
-// Tables of the workgroup's chunk, staged once and shared by its waves.
+// Tables of the workgroup's frames f0..f1, staged once and shared by its waves.
 struct alignas(16) FilterLds {
   float pose[kMaxPoseLds][12];  // 48-byte rows: three aligned 16-byte reads each
   float roi[6][kMaxLdsRois];    // cx, cy, cos, sin, ext_x, ext_y
   uint32_t bm[kMaxLdsBudgetWords];
-  uint32_t off[kMaxLdsFrames + 1];  // point frame offsets clamped to [0, N]
-  int32_t roff[kMaxLdsFrames + 1];
+  int32_t roff[kMaxLdsFrames + 1];  // ROI offsets clamped to [0, R]
   int32_t f0, f1, roi_lo, roi_n;
   int32_t chunk_staged;
 };
 
-// Per-wave state in LDS: the candidate queue (a ring) and the digit counts.
+// Per-wave state in LDS: the candidate queue (a ring).
 struct WaveLds {
-  uint32_t hist[kSortBins];  // first radix pass digit counts of this wave's pairs
   uint32_t idx[kWaveQueue];
   uint32_t cand[kWaveQueue];  // candidate-ROI word (W == 1) or 1
   uint32_t fs[kWaveQueue];    // frame << 8 | sweep
@@ -73,24 +70,9 @@ __device__ __forceinline__ void wave_lds_sync() {
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 }
 
-// ST: everything the chunk needs (frame and ROI offsets, poses, budget
-// masks, ROI records) is staged in LDS, so every lookup below is a plain LDS
-// read.  Without ST every lookup reads global memory.
-template <bool ST>
-__device__ __forceinline__ int32_t point_frame(const Config& c, const FilterLds& L, uint32_t i) {
-  if (L.f0 == L.f1) return L.f0;
-  int32_t lo = L.f0, hi = L.f1;
-  while (lo < hi) {
-    const int32_t mid = (lo + hi + 1) >> 1;
-    const bool le = ST ? L.off[mid - L.f0] <= i : c.frame_off[mid] <= (int64_t)i;
-    if (le)
-      lo = mid;
-    else
-      hi = mid - 1;
-  }
-  return lo;
-}
-
+// ST: everything the workgroup needs (ROI offsets, poses, budget masks, ROI
+// records) is staged in LDS, so every lookup below is a plain LDS read.
+// Without ST every lookup reads global memory.
 template <bool ST>
 __device__ __forceinline__ void load_pose(const Config& c, const FilterLds& L, int32_t b, uint32_t s, float* P) {
   if (ST) {
@@ -120,7 +102,7 @@ template <bool ST>
 __device__ __forceinline__ bool roi_hit(const Config& c, const FilterLds& L, int32_t gj, float px, float py) {
   mmbev_roi_t r;
   if (ST) {
-    const int32_t lj = min(max(gj - L.roi_lo, 0), L.roi_n - 1);  // in range unless the ROI offsets are invalid
+    const int32_t lj = min(max(gj - L.roi_lo, 0), max(L.roi_n - 1, 0));  // in range unless the ROI offsets are invalid
     r.cx = L.roi[0][lj];
     r.cy = L.roi[1][lj];
     r.cos_yaw = L.roi[2][lj];
@@ -183,8 +165,7 @@ __device__ __forceinline__ bool exact_keep(const Config& c, const FilterLds& L, 
     }
   }
   if (!hit) return false;
-  const uint32_t kl = ((uint32_t)iz * c.Dy + (uint32_t)iy) * c.Dx + (uint32_t)ix;
-  key = (c.key_has_frame && c.fb > 0) ? (((uint32_t)b << c.kb) | kl) : kl;
+  key = ((uint32_t)iz * c.Dy + (uint32_t)iy) * c.Dx + (uint32_t)ix;
   return true;
 }
 
@@ -220,16 +201,14 @@ __device__ __forceinline__ void load_quad_scalar(const Config& c, uint32_t i0, u
   }
 }
 
-// Frame/ROI range of the chunk (thread 0), from the tile info of its first
-// and last filter tiles, and whether every table fits LDS.
-__device__ __forceinline__ void plan_staging(const Config& c, FilterLds& L, const TileInfo& a, const TileInfo& b) {
-  const int32_t f0 = a.f0, f1 = max(b.f1, a.f0);
+// Frames f0..f1 of the workgroup's chunks and their ROI range (thread 0),
+// and whether every table fits LDS.
+__device__ __forceinline__ void plan_staging(const Config& c, FilterLds& L, int32_t f0, int32_t f1) {
   const int32_t nf = f1 - f0 + 1;
   L.f0 = f0;
   L.f1 = f1;
-  L.roi_lo = a.r_lo;
-  const int32_t r_hi = max(b.r_hi, a.r_lo);
-  L.roi_n = r_hi - a.r_lo;
+  L.roi_lo = min(max(c.roi_off[f0], 0), c.R);
+  L.roi_n = min(max(c.roi_off[f1 + 1], L.roi_lo), c.R) - L.roi_lo;
   L.chunk_staged = nf <= kMaxLdsFrames && nf * c.S <= kMaxPoseLds && nf * c.S * c.W <= kMaxLdsBudgetWords &&
                    L.roi_n <= kMaxLdsRois;
 }
@@ -237,10 +216,7 @@ __device__ __forceinline__ void plan_staging(const Config& c, FilterLds& L, cons
 __device__ __forceinline__ void do_staging(const Config& c, FilterLds& L) {
   const int tid = threadIdx.x;
   const int32_t nf = L.f1 - L.f0 + 1;
-  for (int e = tid; e <= nf; e += kBlock) {
-    L.off[e] = (uint32_t)min(max(c.frame_off[L.f0 + e], (int64_t)0), (int64_t)c.N);
-    L.roff[e] = min(max(c.roi_off[L.f0 + e], 0), c.R);
-  }
+  for (int e = tid; e <= nf; e += kBlock) L.roff[e] = min(max(c.roi_off[L.f0 + e], 0), c.R);
   for (int e = tid; e < nf * c.S * 12; e += kBlock) (&L.pose[0][0])[e] = c.poses[(int64_t)L.f0 * c.S * 12 + e];
   for (int e = tid; e < nf * c.S * c.W; e += kBlock) L.bm[e] = c.budgetmask[(int64_t)L.f0 * c.S * c.W + e];
   for (int e = tid; e < L.roi_n; e += kBlock) {
@@ -276,28 +252,24 @@ struct QuadState {
   uint32_t cand[4];           // candidate-ROI word after phase A (0: none)
 };
 
-// Phase A of four points of a lane (first index i0): p' and the issue of
-// their cell-mask loads, left in flight.
+// Phase A of four points of a lane (first index i0, frame b for the whole
+// wave): p' and the issue of their cell-mask loads, left in flight.
 template <bool ST>
-__device__ __forceinline__ void phase_a(const Config& c, const FilterLds& L, uint32_t i0, const Quad& d,
+__device__ __forceinline__ void phase_a(const Config& c, const FilterLds& L, int32_t b, uint32_t i0, const Quad& d,
                                         QuadState& st) {
-  const uint32_t N = (uint32_t)c.N;
   const uint32_t S = (uint32_t)c.S;
-  int32_t cidx[4], fr[4];
+  int32_t cidx[4];
   uint32_t sq[4];
 #pragma unroll
   for (int q = 0; q < 4; ++q) {
-    fr[q] = point_frame<ST>(c, L, i0 + q);
     sq[q] = (d.s >> (8 * q)) & 0xffu;
-    st.fs[q] = ((uint32_t)fr[q] << 8) | sq[q];
+    st.fs[q] = ((uint32_t)b << 8) | sq[q];
   }
-  const uint32_t pk = (uint32_t)fr[0] * S + sq[0];
-  const bool lane_uniform =
-      ST && i0 + 3 < N && sq[0] < S && sq[1] == sq[0] && sq[2] == sq[0] && sq[3] == sq[0] && fr[3] == fr[0];
-  const uint32_t pk0 = __builtin_amdgcn_readfirstlane(pk);
-  if (ST && __ballot(!lane_uniform || pk != pk0) == 0) {
+  const bool lane_uniform = ST && sq[0] < S && sq[1] == sq[0] && sq[2] == sq[0] && sq[3] == sq[0];
+  const uint32_t s0 = __builtin_amdgcn_readfirstlane(sq[0]);
+  if (ST && __ballot(!lane_uniform || sq[0] != s0) == 0) {
     // one pose for the whole wave, read as three 16-byte rows
-    const int32_t row = (int32_t)pk0 - L.f0 * (int32_t)S;
+    const int32_t row = (b - L.f0) * (int32_t)S + (int32_t)s0;
     const float4 r0 = *reinterpret_cast<const float4*>(&L.pose[row][0]);
     const float4 r1 = *reinterpret_cast<const float4*>(&L.pose[row][4]);
     const float4 r2 = *reinterpret_cast<const float4*>(&L.pose[row][8]);
@@ -306,18 +278,18 @@ __device__ __forceinline__ void phase_a(const Config& c, const FilterLds& L, uin
       st.px[q] = fma_rn(r0.x, d.x[q], fma_rn(r0.y, d.y[q], fma_rn(r0.z, d.z[q], r0.w)));
       st.py[q] = fma_rn(r1.x, d.x[q], fma_rn(r1.y, d.y[q], fma_rn(r1.z, d.z[q], r1.w)));
       st.pz[q] = fma_rn(r2.x, d.x[q], fma_rn(r2.y, d.y[q], fma_rn(r2.z, d.z[q], r2.w)));
-      cidx[q] = approx_cell(c, fr[q], st.px[q], st.py[q]);
+      cidx[q] = approx_cell(c, b, st.px[q], st.py[q]);
     }
   } else {
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
       cidx[q] = -1;
       st.px[q] = st.py[q] = st.pz[q] = 0.0f;
-      if (sq[q] < S && i0 + q < N) {
+      if (sq[q] < S) {
         float P[12];
-        load_pose<ST>(c, L, fr[q], sq[q], P);
+        load_pose<ST>(c, L, b, sq[q], P);
         compensate(P, d.x[q], d.y[q], d.z[q], st.px[q], st.py[q], st.pz[q]);
-        cidx[q] = approx_cell(c, fr[q], st.px[q], st.py[q]);
+        cidx[q] = approx_cell(c, b, st.px[q], st.py[q]);
       }
     }
   }
@@ -345,22 +317,17 @@ __device__ __forceinline__ void decide_round(const Config& c, const FilterLds& L
   const int lane = threadIdx.x & 63;
   bool keep = false;
   uint32_t key = 0, i = 0;
-  int32_t b = 0;
   if ((uint32_t)lane < n) {
     const uint32_t e = (wr.head + lane) & (kWaveQueue - 1);
     i = Q.idx[e];
     const uint32_t fs = Q.fs[e];
-    b = (int32_t)(fs >> 8);
-    keep = exact_keep<ST>(c, L, b, fs & 0xffu, Q.px[e], Q.py[e], Q.pz[e], Q.cand[e], key);
+    keep = exact_keep<ST>(c, L, (int32_t)(fs >> 8), fs & 0xffu, Q.px[e], Q.py[e], Q.pz[e], Q.cand[e], key);
   }
   const uint64_t kbits = __ballot(keep);
   if (keep) {
     const uint32_t pos = wr.out_base + wr.kept + (uint32_t)__popcll(kbits & lanemask_lt());
     c.keys[0][pos] = key;
     c.vals[0][pos] = i;
-    uint64_t comp = key;
-    if (!c.key_has_frame) comp |= (uint64_t)b << c.kb;
-    atomicAdd(&Q.hist[comp & ((1u << c.dbits) - 1u)], 1u);  // first radix pass: this wave's digit counts
   }
   wr.kept += (uint32_t)__popcll(kbits);
   wr.head = (wr.head + n) & (kWaveQueue - 1);
@@ -409,44 +376,49 @@ __device__ __forceinline__ void phase_b(const Config& c, const FilterLds& L, Wav
   }
 }
 
-// The points [lo, hi) of one wave, wave tile by wave tile.  Full tiles go
-// through a two-deep register pipeline with 16-byte loads; a partial last
-// tile (or every tile, when the rows do not allow 16-byte loads) is loaded
-// point by point without prefetch.
+// The points [lo, hi) of one wave (frame b), wave tile by wave tile: the
+// points before the first multiple of 4 and a partial last tile are loaded
+// point by point; the full tiles between them go through a two-deep
+// register pipeline with 16-byte loads (when the rows allow them; otherwise
+// every tile is loaded point by point).
 template <bool VEC, bool ST>
-__device__ __forceinline__ void run_wave(const Config& c, const FilterLds& L, WaveLds& Q, uint32_t lo, uint32_t hi,
-                                         WaveRun& wr) {
+__device__ __forceinline__ void run_wave(const Config& c, const FilterLds& L, WaveLds& Q, int32_t b, uint32_t lo,
+                                         uint32_t hi, WaveRun& wr) {
   const uint32_t lane4 = 4u * (uint32_t)(threadIdx.x & 63);
   Quad cur, nxt;
   QuadState st;
-  const uint32_t full_end = VEC ? lo + (hi - lo) / kWaveTile * kWaveTile : lo;
-  const uint32_t last_full = full_end - kWaveTile;  // only used when full_end > lo
-  if (lo < full_end) load_quad_vec(c, lo + lane4, cur);
-  for (uint32_t t = lo; t < full_end; t += 2 * kWaveTile) {
+  const uint32_t a0 = VEC ? min((lo + 3u) & ~3u, hi) : lo;
+  if (a0 > lo) {  // head: fewer than 4 points
+    load_quad_scalar(c, lo + lane4, a0, cur);
+    phase_a<ST>(c, L, b, lo + lane4, cur, st);
+    phase_b<ST>(c, L, Q, lo + lane4, st, wr);
+  }
+  const uint32_t full_end = VEC ? a0 + (hi - a0) / kWaveTile * kWaveTile : a0;
+  const uint32_t last_full = full_end - kWaveTile;  // only used when full_end > a0
+  if (a0 < full_end) load_quad_vec(c, a0 + lane4, cur);
+  for (uint32_t t = a0; t < full_end; t += 2 * kWaveTile) {
     // tile t (in cur) with tile t+T loading into nxt behind its cell-mask
     // loads; then tile t+T with tile t+2T loading into cur.  Past the last
     // full tile the load repeats that tile (cache hits, values unused), which
     // keeps the number of loads in flight the same on every path.
-    phase_a<ST>(c, L, t + lane4, cur, st);
+    phase_a<ST>(c, L, b, t + lane4, cur, st);
     load_quad_vec(c, min(t + kWaveTile, last_full) + lane4, nxt);
     phase_b<ST>(c, L, Q, t + lane4, st, wr);
     if (t + kWaveTile >= full_end) break;
-    phase_a<ST>(c, L, t + kWaveTile + lane4, nxt, st);
+    phase_a<ST>(c, L, b, t + kWaveTile + lane4, nxt, st);
     load_quad_vec(c, min(t + 2 * kWaveTile, last_full) + lane4, cur);
     phase_b<ST>(c, L, Q, t + kWaveTile + lane4, st, wr);
   }
   for (uint32_t t = full_end; t < hi; t += kWaveTile) {
     load_quad_scalar(c, t + lane4, hi, cur);
-    phase_a<ST>(c, L, t + lane4, cur, st);
+    phase_a<ST>(c, L, b, t + lane4, cur, st);
     phase_b<ST>(c, L, Q, t + lane4, st, wr);
   }
   while (wr.queued > 0) decide_round<ST>(c, L, Q, wr, min(wr.queued, 64u));
 }
 
-// Workgroup w: its waves over the chunk [w*kWaves*P, (w+1)*kWaves*P) of
-// points (whole filter tiles), wave k of the grid over [k*P, (k+1)*P).  Per
-// wave it leaves the number of kept pairs and their first-digit counts for
-// the first radix pass.
+// Workgroup w: its waves over filter chunks kWaves*w .. kWaves*w + 3.  Per
+// chunk it leaves the number of kept pairs and where they start.
 template <bool VEC>
 __global__ __launch_bounds__(kBlock) void filter_kernel(Config c) {
   __shared__ FilterLds L;
@@ -454,42 +426,38 @@ __global__ __launch_bounds__(kBlock) void filter_kernel(Config c) {
   const int tid = threadIdx.x;
   const int lane = tid & 63, wave = tid >> 6;
   WaveLds& Q = Qs[wave];
-  const int64_t t_begin = (int64_t)blockIdx.x * c.filter_chunk_tiles;
-  const int64_t t_end = min(t_begin + (int64_t)c.filter_chunk_tiles, (int64_t)c.filter_tiles);
-  const uint32_t nbins = 1u << c.dbits;
+  const uint32_t nchunks = c.hdr->fchunks;
+  const uint32_t k0 = (uint32_t)blockIdx.x * kWaves;
 
-  for (int e = lane; e < kSortBins; e += 64) Q.hist[e] = 0;
   if (tid == 0) {
     L.f0 = L.f1 = 0;
     L.chunk_staged = 0;
-    if (t_begin < t_end) plan_staging(c, L, c.tinfo[t_begin], c.tinfo[t_end - 1]);
+    if (k0 < nchunks)
+      plan_staging(c, L, frame_of_chunk(c.fchunk_first, c.B, k0),
+                   frame_of_chunk(c.fchunk_first, c.B, min(k0 + kWaves - 1, nchunks - 1)));
   }
   __syncthreads();
   const bool staged = __builtin_amdgcn_readfirstlane(L.chunk_staged) != 0;
   if (staged) do_staging(c, L);
   __syncthreads();
 
-  const uint32_t k = (uint32_t)blockIdx.x * kWaves + (uint32_t)wave;  // this wave's chunk
-  const uint32_t P = (uint32_t)c.filter_chunk_points;
-  const uint32_t lo = min(k * P, (uint32_t)c.N), hi = min(lo + P, (uint32_t)c.N);
+  const uint32_t k = k0 + (uint32_t)wave;  // this wave's chunk
+  if (k >= nchunks) return;
+  const int32_t b = __builtin_amdgcn_readfirstlane(frame_of_chunk(c.fchunk_first, c.B, k));
+  uint32_t lo, hi;
+  filter_chunk_points(c, b, k, lo, hi);
   WaveRun wr{0u, 0u, 0u, lo};
   if (staged)
-    run_wave<VEC, true>(c, L, Q, lo, hi, wr);
+    run_wave<VEC, true>(c, L, Q, b, lo, hi, wr);
   else
-    run_wave<VEC, false>(c, L, Q, lo, hi, wr);
-  wave_lds_sync();
-  if (k < (uint32_t)c.filter_chunks) {
-    if (lane == 0) c.fcount[k] = wr.kept;
-    for (uint32_t e = lane; e < nbins; e += 64) c.cnt[(int64_t)e * c.filter_chunks + k] = Q.hist[e];
+    run_wave<VEC, false>(c, L, Q, b, lo, hi, wr);
+  if (lane == 0) {
+    c.fcount[k] = wr.kept;
+    c.fchunk_lo[k] = lo;
   }
 }
 
 }  // namespace
-
-hipError_t filter_occupancy(int vec, int* per_cu) {
-  const void* k = vec ? (const void*)filter_kernel<true> : (const void*)filter_kernel<false>;
-  return hipOccupancyMaxActiveBlocksPerMultiprocessor(per_cu, k, kBlock, 0);
-}
 
 hipError_t launch_filter(const Config& c, hipStream_t st) {
   if (c.vec)

@@ -1,71 +1,37 @@
-// Stable least-significant-digit radix sort of (key, value) pairs as chunked
-// reduce-then-scan passes, with no inter-workgroup waiting.
+// Stable least-significant-digit radix sort of (voxel key, point index)
+// pairs, segmented by frame, as chunked reduce-then-scan passes with no
+// inter-workgroup waiting.
 //
-// A pass over the pairs is three launches:
-//   count   -- workgroup w counts the digits of its chunk of the input
-//              (wave multi-split, one LDS add per distinct digit and wave);
-//   rowscan -- workgroup d turns row d of the [digit][chunk] count matrix
-//              into exclusive offsets and writes the row total;
-//   scatter -- workgroup w walks its chunk in order, tile by tile: ranks each
-//              pair inside the tile (wave multi-split), reorders the tile by
-//              digit in LDS, and writes every digit's run to
-//              base(digit) + offset(digit, w) + pairs of that digit already
-//              written from earlier tiles of the chunk.
-// Chunks are contiguous and visited in order, so the pass is stable.  The
-// first pass reads the point filter's output in place: chunk w of that pass
-// is filter wave chunk w's region (kept pairs in point order, a gap after
-// them), and its digit counts come from the filter.
+// Frames are never mixed: the pairs are grouped by frame in frame order (the
+// filter emits them in point order), every chunk of a pass holds pairs of
+// one frame, and a pass moves each pair only inside its frame's range, to
+//   fstart(b) + (pairs of frame b with a smaller digit)
+//             + (pairs of frame b with this digit in earlier chunks)
+//             + (pairs with this digit earlier in this chunk).
+// So the keys need no frame bits: ceil(kb / 9) passes of at most 9 bits sort
+// every frame.
 //
-// Keys are voxel keys; the frame index is part of the key, either in its top
-// bits or, when key and frame do not fit 32 bits together, looked up from
-// the point index (frames are contiguous point ranges) in LDS.
+// segments -- one workgroup: the kept-pair prefix of the filter chunks, the
+//             first pair of every frame, and the pair chunks (about
+//             kSortGrid of them, chunk_pairs pairs each, the last of a frame
+//             shorter).
+// compact  -- one wave per filter chunk: its kept pairs (at the start of the
+//             chunk's point range) copied to their compact place.
+// Then per pass:
+// count    -- workgroup k counts the digits of pair chunk k (row k of the
+//             [chunk][digit] count matrix);
+// rowscan  -- workgroup b turns the rows of frame b's chunks into offsets
+//             inside the frame (an exclusive scan down each digit's column)
+//             and writes the frame's digit totals;
+// scatter  -- workgroup k walks its chunk tile by tile (the next tile's
+//             pairs loading while the current one is handled): ranks each
+//             pair inside the tile (wave multi-split), reorders the tile by
+//             digit in LDS, and writes every digit's run to its place.
 #include "launch.hpp"
 
 namespace mmbev {
 
 namespace {
-
-__device__ __forceinline__ uint32_t frame_lds(const uint32_t* off, int32_t B, uint32_t val) {
-  int32_t lo = 0, hi = B - 1;
-  while (lo < hi) {
-    const int32_t mid = (lo + hi + 1) >> 1;
-    if (off[mid] <= val)
-      lo = mid;
-    else
-      hi = mid - 1;
-  }
-  return (uint32_t)lo;
-}
-
-struct DigitOf {
-  int shift;
-  uint32_t mask;
-  bool frame;  // the pass's digit reaches into the frame bits
-  bool lds;    // frame offsets staged in LDS
-  const uint32_t* off;
-  __device__ __forceinline__ uint32_t operator()(const Config& c, uint32_t key, uint32_t val) const {
-    uint64_t comp = key;
-    if (frame)
-      comp |= (uint64_t)(lds ? frame_lds(off, c.B, val) : (uint32_t)frame_of_point(c.frame_off, c.B, (int64_t)val))
-              << c.kb;
-    return (uint32_t)(comp >> shift) & mask;
-  }
-};
-
-// Digit extractor of a pass; stages the frame offsets in LDS when needed
-// (the caller synchronises before use).
-__device__ __forceinline__ DigitOf make_digit(const Config& c, int pass, uint32_t* dyn_off) {
-  DigitOf d;
-  d.shift = pass * c.dbits;
-  d.mask = (1u << c.dbits) - 1u;
-  d.frame = !c.key_has_frame && c.B > 1 && d.shift + c.dbits > c.kb;
-  d.lds = d.frame && c.B <= kMaxSortLdsFrames;
-  d.off = dyn_off;
-  if (d.lds)
-    for (int e = threadIdx.x; e <= c.B; e += kBlock)
-      dyn_off[e] = (uint32_t)min(max(c.frame_off[e], (int64_t)0), (int64_t)c.N);
-  return d;
-}
 
 // Lanes of this wave holding the same digit (valid lanes only).
 __device__ __forceinline__ uint64_t match_digit(uint32_t dig, bool valid, int dbits) {
@@ -78,109 +44,239 @@ __device__ __forceinline__ uint64_t match_digit(uint32_t dig, bool valid, int db
   return m;
 }
 
-__global__ __launch_bounds__(kBlock) void count_kernel(Config c, int pass, const uint32_t* kin, const uint32_t* vin) {
-  __shared__ uint32_t s_hist[kSortBins];
-  extern __shared__ uint32_t dyn_off[];
-  const int tid = threadIdx.x;
-  const uint32_t K = c.hdr->kept;
-  const DigitOf digit = make_digit(c, pass, dyn_off);
-  s_hist[tid] = 0;
-  __syncthreads();
-  uint32_t lo, hi;
-  chunk_range(K, blockIdx.x, gridDim.x, lo, hi);
-  const uint64_t lt = lanemask_lt();
-  for (uint32_t base = lo; base < hi; base += kBlock) {
-    const uint32_t k = base + tid;
-    const bool valid = k < hi;
-    const uint32_t d = valid ? digit(c, kin[k], digit.frame ? vin[k] : 0u) : 0u;
-    const uint64_t m = match_digit(d, valid, c.dbits);
-    if (valid && (m & lt) == 0) atomicAdd(&s_hist[d], (uint32_t)__popcll(m));
+// Exclusive scan of n <= kSortBins values in LDS (in may alias out); all
+// threads must call.  Returns the total.
+__device__ __forceinline__ uint32_t scan_bins(const uint32_t* in, uint32_t* out, int n, uint32_t* s_tmp) {
+  constexpr int kPer = kSortBins / kBlock;
+  const int first = threadIdx.x * kPer;
+  uint32_t v[kPer], sum = 0;
+#pragma unroll
+  for (int j = 0; j < kPer; ++j) {
+    v[j] = first + j < n ? in[first + j] : 0u;
+    sum += v[j];
   }
-  __syncthreads();
-  const uint32_t nbins = 1u << c.dbits;
-  if ((uint32_t)tid < nbins) c.cnt[(int64_t)tid * gridDim.x + blockIdx.x] = s_hist[tid];
-}
-
-// Row d of the count matrix -> exclusive offsets in place, row total.  With
-// fcount (first pass), block 0 also stores the number of kept pairs.
-__global__ __launch_bounds__(kBlock) void rowscan_kernel(Config c, int chunks, const uint32_t* fcount) {
-  __shared__ uint32_t s_tmp[kWaves];
-  const int tid = threadIdx.x;
-  uint32_t* row = c.cnt + (int64_t)blockIdx.x * chunks;
-  const int per = (chunks + kBlock - 1) / kBlock;
-  const int first = tid * per;
-  uint32_t sum = 0;
-  for (int j = 0; j < per; ++j)
-    if (first + j < chunks) sum += row[first + j];
   uint32_t total;
   uint32_t run = block_exclusive_scan(sum, s_tmp, total);
-  for (int j = 0; j < per; ++j)
-    if (first + j < chunks) {
-      const uint32_t x = row[first + j];
-      row[first + j] = run;
+#pragma unroll
+  for (int j = 0; j < kPer; ++j)
+    if (first + j < n) {
+      out[first + j] = run;
+      run += v[j];
+    }
+  __syncthreads();
+  return total;
+}
+
+__global__ __launch_bounds__(kBlock) void segments_kernel(Config c) {
+  __shared__ uint32_t s_tmp[kWaves];
+  WsHeader* h = c.hdr;
+  const int tid = threadIdx.x;
+  const uint32_t nf = h->fchunks;
+  // kept-pair prefix of the filter chunks
+  uint32_t carry = 0;
+  for (uint32_t base = 0; base < nf; base += kScanTile) {
+    const uint32_t first = base + tid * kScanItems;
+    uint32_t v[kScanItems], sum = 0;
+#pragma unroll
+    for (int j = 0; j < kScanItems; ++j) {
+      v[j] = first + j < nf ? c.fcount[first + j] : 0u;
+      sum += v[j];
+    }
+    uint32_t total;
+    uint32_t run = carry + block_exclusive_scan(sum, s_tmp, total);
+#pragma unroll
+    for (int j = 0; j < kScanItems; ++j)
+      if (first + j < nf) {
+        c.fprefix[first + j] = run;
+        run += v[j];
+      }
+    carry += total;
+  }
+  if (tid == 0) c.fprefix[nf] = carry;
+  __syncthreads();
+  const uint32_t K = carry;
+  for (int b = tid; b <= c.B; b += kBlock) c.fstart[b] = c.fprefix[min(c.fchunk_first[b], nf)];
+  __syncthreads();
+  // pair chunks: about kSortGrid of them, whole kSortTile multiples
+  uint32_t CH = (K + kSortGrid - 1) / kSortGrid;
+  CH = max((uint32_t)kSortTile, (CH + kSortTile - 1) / kSortTile * kSortTile);
+  const int per = (c.B + kBlock - 1) / kBlock;
+  const int b0 = tid * per;
+  uint32_t mine = 0;
+  for (int j = 0; j < per; ++j) {
+    const int b = b0 + j;
+    if (b < c.B) mine += (c.fstart[b + 1] - c.fstart[b] + CH - 1) / CH;
+  }
+  uint32_t total;
+  uint32_t run = block_exclusive_scan(mine, s_tmp, total);
+  const uint32_t cap = (uint32_t)c.schunk_max;  // never reached: K / CH <= kSortGrid
+  for (int j = 0; j < per; ++j) {
+    const int b = b0 + j;
+    if (b < c.B) {
+      const uint32_t f0 = c.fstart[b], f1 = c.fstart[b + 1];
+      const uint32_t n = (f1 - f0 + CH - 1) / CH;
+      c.schunk_first[b] = min(run, cap);
+      for (uint32_t k = run; k < min(run + n, cap); ++k) {
+        const uint32_t lo = f0 + (k - run) * CH;
+        c.schunk[k] = make_uint4(lo, min(lo + CH, f1), (uint32_t)b, f0);
+      }
+      run += n;
+    }
+  }
+  if (tid == 0) {
+    c.schunk_first[c.B] = min(total, cap);
+    h->schunks = min(total, cap);
+    h->chunk_pairs = CH;
+    h->kept = K;
+  }
+}
+
+// One wave per filter chunk: its kept pairs to [fprefix[k], fprefix[k+1]).
+__global__ __launch_bounds__(kBlock) void compact_kernel(Config c, uint32_t* kout, uint32_t* vout) {
+  constexpr int kUnroll = 8;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const uint32_t k = blockIdx.x * kWaves + wave;
+  if (k >= c.hdr->fchunks) return;
+  const uint32_t lo = c.fchunk_lo[k], n = c.fcount[k], dst = c.fprefix[k];
+  for (uint32_t base = 0; base < n; base += 64 * kUnroll) {
+    uint32_t kk[kUnroll], vv[kUnroll];
+#pragma unroll
+    for (int u = 0; u < kUnroll; ++u) {
+      const uint32_t i = base + u * 64 + lane;
+      kk[u] = i < n ? c.keys[0][lo + i] : 0u;
+      vv[u] = i < n ? c.vals[0][lo + i] : 0u;
+    }
+#pragma unroll
+    for (int u = 0; u < kUnroll; ++u) {
+      const uint32_t i = base + u * 64 + lane;
+      if (i < n) {
+        kout[dst + i] = kk[u];
+        vout[dst + i] = vv[u];
+      }
+    }
+  }
+}
+
+__global__ __launch_bounds__(kBlock) void count_kernel(Config c, int pass, const uint32_t* kin) {
+  __shared__ uint32_t s_hist[kSortBins];
+  const int tid = threadIdx.x;
+  const uint32_t k = blockIdx.x;
+  if (k >= c.hdr->schunks) return;
+  const int shift = pass * c.dbits;
+  const uint32_t nbins = 1u << c.dbits;
+  const uint32_t mask = nbins - 1u;
+  for (uint32_t e = tid; e < nbins; e += kBlock) s_hist[e] = 0;
+  __syncthreads();
+  const uint4 ch = c.schunk[k];
+  const uint32_t lo = ch.x, hi = ch.y;
+  const uint64_t lt = lanemask_lt();
+  for (uint32_t base = lo; base < hi; base += kBlock * kCountItems) {
+    uint32_t key[kCountItems];
+#pragma unroll
+    for (int j = 0; j < kCountItems; ++j) {  // all loads of the batch in flight together
+      const uint32_t i = base + j * kBlock + tid;
+      key[j] = i < hi ? kin[i] : 0u;
+    }
+#pragma unroll
+    for (int j = 0; j < kCountItems; ++j) {
+      const bool valid = base + j * kBlock + tid < hi;
+      const uint32_t d = (key[j] >> shift) & mask;
+      const uint64_t m = match_digit(d, valid, c.dbits);
+      if (valid && (m & lt) == 0) atomicAdd(&s_hist[d], (uint32_t)__popcll(m));
+    }
+  }
+  __syncthreads();
+  for (uint32_t e = tid; e < nbins; e += kBlock) c.cnt[(int64_t)k * kSortBins + e] = s_hist[e];
+}
+
+// Frame b: every digit's column over the frame's chunks -> exclusive
+// offsets inside the frame (in place), and the frame's digit totals.
+__global__ __launch_bounds__(kBlock) void rowscan_kernel(Config c) {
+  constexpr int kUnroll = 4;
+  const int tid = threadIdx.x;
+  const int32_t b = blockIdx.x;
+  const uint32_t nbins = 1u << c.dbits;
+  const uint32_t k0 = c.schunk_first[b], k1 = max(c.schunk_first[b + 1], k0);
+  for (uint32_t d = tid; d < nbins; d += kBlock) {
+    uint32_t run = 0;
+    uint32_t k = k0;
+    for (; k + kUnroll <= k1; k += kUnroll) {
+      uint32_t x[kUnroll];
+#pragma unroll
+      for (int u = 0; u < kUnroll; ++u) x[u] = c.cnt[(int64_t)(k + u) * kSortBins + d];
+#pragma unroll
+      for (int u = 0; u < kUnroll; ++u) {
+        c.cnt[(int64_t)(k + u) * kSortBins + d] = run;
+        run += x[u];
+      }
+    }
+    for (; k < k1; ++k) {
+      const uint32_t x = c.cnt[(int64_t)k * kSortBins + d];
+      c.cnt[(int64_t)k * kSortBins + d] = run;
       run += x;
     }
-  if (tid == 0) c.tot[blockIdx.x] = total;
-  if (fcount && blockIdx.x == 0) {
-    uint32_t ks = 0;
-    for (int j = 0; j < per; ++j)
-      if (first + j < chunks) ks += fcount[first + j];
-    uint32_t kt;
-    (void)block_exclusive_scan(ks, s_tmp, kt);
-    if (tid == 0) c.hdr->kept = kt;
+    c.ftot[(int64_t)b * kSortBins + d] = run;
   }
 }
 
 struct ScatterLds {
   uint32_t run[kSortBins];  // next output position of every digit
   uint32_t wave_cnt[kWaves][kSortBins];
+  uint32_t tile_cnt[kSortBins];
   uint32_t local_off[kSortBins];
   uint32_t keys[kSortTile];
   uint32_t vals[kSortTile];
-  uint8_t digit[kSortTile];
+  uint16_t digit[kSortTile];
   uint32_t scan_tmp[kWaves];
 };
 
+__device__ __forceinline__ void load_sort_tile(const uint32_t* kin, const uint32_t* vin, uint32_t base, uint32_t hi,
+                                               uint32_t* key, uint32_t* val) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+#pragma unroll
+  for (int r = 0; r < kSortItems; ++r) {
+    const uint32_t i = base + wave * (64 * kSortItems) + r * 64 + lane;
+    key[r] = i < hi ? kin[i] : 0u;
+    val[r] = i < hi ? vin[i] : 0u;
+  }
+}
+
 __global__ __launch_bounds__(kBlock) void scatter_kernel(Config c, int pass, const uint32_t* kin, const uint32_t* vin,
-                                                         uint32_t* kout, uint32_t* vout, int first_pass) {
+                                                         uint32_t* kout, uint32_t* vout) {
   __shared__ ScatterLds L;
-  extern __shared__ uint32_t dyn_off[];
   const int tid = threadIdx.x;
   const int lane = tid & 63, wave = tid >> 6;
   WsHeader* h = c.hdr;
+  const uint32_t k = blockIdx.x;
+  if (k >= h->schunks) return;
   const uint32_t K = h->kept;
-  const DigitOf digit = make_digit(c, pass, dyn_off);
+  const int shift = pass * c.dbits;
   const uint32_t nbins = 1u << c.dbits;
-  uint32_t lo, hi;
-  if (first_pass) {
-    lo = blockIdx.x * (uint32_t)c.filter_chunk_points;
-    hi = lo + min(c.fcount[blockIdx.x], (uint32_t)c.filter_chunk_points);
-  } else {
-    chunk_range(K, blockIdx.x, gridDim.x, lo, hi);
-  }
-  {
-    // base(digit) = totals of the smaller digits; plus this chunk's offset
-    const uint32_t t = (uint32_t)tid < nbins ? c.tot[tid] : 0u;
-    uint32_t total;
-    const uint32_t ex = block_exclusive_scan(t, L.scan_tmp, total);
-    if ((uint32_t)tid < nbins) L.run[tid] = ex + c.cnt[(int64_t)tid * gridDim.x + blockIdx.x];
-  }
+  const uint32_t mask = nbins - 1u;
+  const uint4 ch = c.schunk[k];
+  const uint32_t lo = ch.x, hi = ch.y;
+  const int32_t b = (int32_t)ch.z;
+  uint32_t key[kSortItems], val[kSortItems], nkey[kSortItems], nval[kSortItems];
+  if (lo < hi) load_sort_tile(kin, vin, lo, hi, key, val);
+  // base of every digit: frame start + smaller digits of the frame + this
+  // chunk's offset among the frame's chunks
+  for (uint32_t e = tid; e < nbins; e += kBlock) L.run[e] = c.ftot[(int64_t)b * kSortBins + e];
+  __syncthreads();
+  scan_bins(L.run, L.run, (int)nbins, L.scan_tmp);
+  for (uint32_t e = tid; e < nbins; e += kBlock) L.run[e] += ch.w + c.cnt[(int64_t)k * kSortBins + e];
   const uint64_t lt = lanemask_lt();
   for (uint32_t base = lo; base < hi; base += kSortTile) {
-#pragma unroll
-    for (int w = 0; w < kWaves; ++w) L.wave_cnt[w][tid] = 0;
+    const bool more = base + kSortTile < hi;
+    if (more) load_sort_tile(kin, vin, base + kSortTile, hi, nkey, nval);
+    for (uint32_t e = tid; e < kWaves * kSortBins; e += kBlock) (&L.wave_cnt[0][0])[e] = 0;
     __syncthreads();
-    uint32_t key[kSortItems], val[kSortItems], dig[kSortItems], rank[kSortItems];
+    uint32_t dig[kSortItems], rank[kSortItems];
     bool valid[kSortItems];
 #pragma unroll
     for (int r = 0; r < kSortItems; ++r) {
-      const uint32_t k = base + wave * (64 * kSortItems) + r * 64 + lane;
-      valid[r] = k < hi;
-      key[r] = valid[r] ? kin[k] : 0u;
-      val[r] = valid[r] ? vin[k] : 0u;
+      valid[r] = base + wave * (64 * kSortItems) + r * 64 + lane < hi;
+      dig[r] = (key[r] >> shift) & mask;
     }
-#pragma unroll
-    for (int r = 0; r < kSortItems; ++r) dig[r] = valid[r] ? digit(c, key[r], val[r]) : 0u;
     // wave multi-split over the rounds: tile order is (wave, round, lane)
 #pragma unroll
     for (int r = 0; r < kSortItems; ++r) {
@@ -195,68 +291,71 @@ __global__ __launch_bounds__(kBlock) void scatter_kernel(Config c, int pass, con
       __builtin_amdgcn_wave_barrier();
     }
     __syncthreads();
-    uint32_t tile_cnt = 0;
-    if ((uint32_t)tid < nbins) {
+    for (uint32_t e = tid; e < nbins; e += kBlock) {
+      uint32_t t = 0;
 #pragma unroll
       for (int w = 0; w < kWaves; ++w) {
-        const uint32_t x = L.wave_cnt[w][tid];
-        L.wave_cnt[w][tid] = tile_cnt;
-        tile_cnt += x;
+        const uint32_t x = L.wave_cnt[w][e];
+        L.wave_cnt[w][e] = t;
+        t += x;
       }
+      L.tile_cnt[e] = t;
     }
-    uint32_t tile_total;
-    L.local_off[tid] = block_exclusive_scan(tile_cnt, L.scan_tmp, tile_total);
     __syncthreads();
+    scan_bins(L.tile_cnt, L.local_off, (int)nbins, L.scan_tmp);
 #pragma unroll
     for (int r = 0; r < kSortItems; ++r) {
       if (valid[r]) {
         const uint32_t lp = L.local_off[dig[r]] + L.wave_cnt[wave][dig[r]] + rank[r];
         L.keys[lp] = key[r];
         L.vals[lp] = val[r];
-        L.digit[lp] = (uint8_t)dig[r];
+        L.digit[lp] = (uint16_t)dig[r];
       }
     }
     __syncthreads();
     const uint32_t n_in = min((uint32_t)kSortTile, hi - base);
-    for (uint32_t k = tid; k < n_in; k += kBlock) {
-      const uint32_t d = L.digit[k];
-      const uint32_t gp = L.run[d] + (k - L.local_off[d]);
+    for (uint32_t i = tid; i < n_in; i += kBlock) {
+      const uint32_t dd = L.digit[i];
+      const uint32_t gp = L.run[dd] + (i - L.local_off[dd]);
       if (gp < K) {  // always true when the counts match the pairs
-        kout[gp] = L.keys[k];
-        vout[gp] = L.vals[k];
+        kout[gp] = L.keys[i];
+        vout[gp] = L.vals[i];
       } else {
         raise_fault(h, MMBEV_FAULT_POINT_OFFSETS);
       }
     }
     __syncthreads();
-    if ((uint32_t)tid < nbins) L.run[tid] += tile_cnt;
+    for (uint32_t e = tid; e < nbins; e += kBlock) L.run[e] += L.tile_cnt[e];
+    if (more)
+#pragma unroll
+      for (int r = 0; r < kSortItems; ++r) {
+        key[r] = nkey[r];
+        val[r] = nval[r];
+      }
   }
-}
-
-size_t frame_lds_bytes(const Config& c, int pass) {
-  const bool frame = !c.key_has_frame && c.B > 1 && pass * c.dbits + c.dbits > c.kb;
-  return (frame && c.B <= kMaxSortLdsFrames) ? (size_t)(c.B + 1) * 4 : 0;
 }
 
 }  // namespace
 
+hipError_t launch_segments(const Config& c, hipStream_t st) {
+  hipLaunchKernelGGL(segments_kernel, dim3(1), dim3(kBlock), 0, st, c);
+  return hipGetLastError();
+}
+
+hipError_t launch_compact(const Config& c, uint32_t* kout, uint32_t* vout, hipStream_t st) {
+  hipLaunchKernelGGL(compact_kernel, dim3(c.filter_grid), dim3(kBlock), 0, st, c, kout, vout);
+  return hipGetLastError();
+}
+
 hipError_t launch_radix_pass(const Config& c, int pass, const uint32_t* kin, const uint32_t* vin, uint32_t* kout,
                              uint32_t* vout, hipStream_t st) {
-  const size_t dyn = frame_lds_bytes(c, pass);
-  const int nbins = 1 << c.dbits;
-  const bool first = pass == 0;
-  const int chunks = first ? c.filter_chunks : c.sort_chunks;
-  if (!first) {
-    hipLaunchKernelGGL(count_kernel, dim3(chunks), dim3(kBlock), dyn, st, c, pass, kin, vin);
-    const hipError_t e = hipGetLastError();
-    if (e != hipSuccess) return e;
-  }
-  hipLaunchKernelGGL(rowscan_kernel, dim3(nbins), dim3(kBlock), 0, st, c, chunks,
-                     first ? (const uint32_t*)c.fcount : (const uint32_t*)nullptr);
-  const hipError_t e = hipGetLastError();
+  hipLaunchKernelGGL(count_kernel, dim3(c.schunk_max), dim3(kBlock), 0, st, c, pass, kin);
+  hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(scatter_kernel, dim3(chunks), dim3(kBlock), dyn, st, c, pass, kin, vin, kout, vout,
-                     first ? 1 : 0);
+  hipLaunchKernelGGL(rowscan_kernel, dim3(c.B), dim3(kBlock), 0, st, c);
+  e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(scatter_kernel, dim3(c.schunk_max), dim3(kBlock), 0, st, c, pass, kin, vin, kout, vout);
   return hipGetLastError();
 }
 

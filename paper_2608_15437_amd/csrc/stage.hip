@@ -9,11 +9,11 @@
 // word.  Cell ranges are conservative (padded by more than the fp32 error of
 // the exact test), so the exact test alone decides membership.
 //
-// Block (0, 0) also opens the call: it bumps the epoch that tags look-back
-// words, clears the per-call counters and digit histograms, and checks the
-// frame offsets of points and ROIs.  The blocks of frame 0 also record, for
-// every tile of the point filter, its frame range and ROI range, so a filter
-// workgroup starts with one load instead of two binary searches.
+// Block (0, 0) also opens the call: it bumps the call counter, clears the
+// per-call counters, checks the frame offsets of points and ROIs, and lays
+// out the filter's work: every frame is cut into chunks of fchunk_points
+// points (the last one shorter), numbered frame after frame, so no chunk
+// straddles two frames.
 #include "launch.hpp"
 
 namespace mmbev {
@@ -21,6 +21,7 @@ namespace mmbev {
 namespace {
 
 constexpr int kMaxRois = 1024;
+constexpr int kStageCellsPerThread = 8;
 
 // Conservative cell rectangle [x0, x1] x [y0, y1] of one ROI; empty when x0 > x1.
 __device__ void roi_cell_rect(const Config& c, const mmbev_roi_t& r, int16_t* out) {
@@ -70,90 +71,126 @@ __device__ void roi_cell_rect(const Config& c, const mmbev_roi_t& r, int16_t* ou
   out[3] = (int16_t)y1;
 }
 
+// Block (0, 0): counters, offset checks, filter chunk table.
+__device__ void open_call(const Config& c, uint32_t* s_tmp) {
+  const int tid = threadIdx.x;
+  WsHeader* h = c.hdr;
+  if (tid == 0) {
+    h->fault = 0;
+    h->epoch = h->epoch + 1;
+    h->kept = 0;
+    h->voxels = 0;
+    h->capped_voxels = 0;
+    h->any_capped = 0;
+  }
+  int32_t bad = 0;
+  for (int f = tid; f <= c.B; f += kBlock) {
+    const int64_t o = c.frame_off[f];
+    if (f == 0 && o != 0) bad |= MMBEV_FAULT_POINT_OFFSETS;
+    if (f == c.B && o != (int64_t)c.N) bad |= MMBEV_FAULT_POINT_OFFSETS;
+    if (f < c.B && c.frame_off[f + 1] < o) bad |= MMBEV_FAULT_POINT_OFFSETS;
+    const int32_t ro = c.roi_off[f];
+    if (f == 0 && ro != 0) bad |= MMBEV_FAULT_ROI_OFFSETS;
+    if (f == c.B && ro != c.R) bad |= MMBEV_FAULT_ROI_OFFSETS;
+    if (f < c.B) {
+      const int32_t rn = c.roi_off[f + 1];
+      if (rn < ro || rn - ro > c.max_rois) bad |= MMBEV_FAULT_ROI_OFFSETS;
+    }
+  }
+  if (bad) raise_fault(h, bad);
+  // chunks of frame b: ceil(points / fchunk_points); thread t owns frames
+  // [t*per, (t+1)*per); the count is capped at fchunk_max (reached only with
+  // invalid offsets)
+  const uint32_t P = (uint32_t)c.fchunk_points;
+  const int per = (c.B + kBlock - 1) / kBlock;
+  const int b0 = tid * per;
+  uint32_t mine = 0;
+  for (int j = 0; j < per; ++j) {
+    const int b = b0 + j;
+    if (b < c.B) {
+      const uint32_t f0 = point_offset(c, b), f1 = max(point_offset(c, b + 1), f0);
+      mine += (f1 - f0 + P - 1) / P;
+    }
+  }
+  uint32_t total;
+  uint32_t run = block_exclusive_scan(mine, s_tmp, total);
+  const uint32_t cap = (uint32_t)c.fchunk_max;
+  for (int j = 0; j < per; ++j) {
+    const int b = b0 + j;
+    if (b < c.B) {
+      c.fchunk_first[b] = min(run, cap);
+      const uint32_t f0 = point_offset(c, b), f1 = max(point_offset(c, b + 1), f0);
+      run += (f1 - f0 + P - 1) / P;
+    }
+  }
+  if (tid == 0) {
+    c.fchunk_first[c.B] = min(total, cap);
+    h->fchunks = min(total, cap);
+  }
+}
+
 __global__ __launch_bounds__(kBlock) void stage_kernel(Config c) {
   __shared__ int16_t s_rect[kMaxRois][4];
+  __shared__ uint32_t s_tmp[kWaves];
   const int tid = threadIdx.x;
   const int b = blockIdx.y;
-  WsHeader* h = c.hdr;
-
-  if (blockIdx.x == 0 && b == 0) {
-    if (tid == 0) {
-      h->fault = 0;
-      h->epoch = h->epoch + 1;
-      h->kept = 0;
-      h->voxels = 0;
-      h->capped_voxels = 0;
-      h->any_capped = 0;
-    }
-    uint32_t* hist = &h->hist[0][0];
-    for (int e = tid; e < kMaxPasses * kSortBins; e += kBlock) hist[e] = 0;
-    __syncthreads();
-    int32_t bad = 0;
-    for (int f = tid; f <= c.B; f += kBlock) {
-      int64_t o = c.frame_off[f];
-      if (f == 0 && o != 0) bad |= MMBEV_FAULT_POINT_OFFSETS;
-      if (f == c.B && o != (int64_t)c.N) bad |= MMBEV_FAULT_POINT_OFFSETS;
-      if (f < c.B && c.frame_off[f + 1] < o) bad |= MMBEV_FAULT_POINT_OFFSETS;
-      int32_t ro = c.roi_off[f];
-      if (f == 0 && ro != 0) bad |= MMBEV_FAULT_ROI_OFFSETS;
-      if (f == c.B && ro != c.R) bad |= MMBEV_FAULT_ROI_OFFSETS;
-      if (f < c.B) {
-        int32_t rn = c.roi_off[f + 1];
-        if (rn < ro || rn - ro > c.max_rois) bad |= MMBEV_FAULT_ROI_OFFSETS;
-      }
-    }
-    if (bad) raise_fault(h, bad);
-  }
-
-  // frame and ROI range of every filter tile (rows of frame 0 only)
-  if (b == 0)
-    for (int64_t t = (int64_t)blockIdx.x * kBlock + tid; t < c.filter_tiles; t += (int64_t)gridDim.x * kBlock) {
-      const int64_t first = t * kFilterTile;
-      const int64_t last = min(first + kFilterTile, (int64_t)c.N) - 1;
-      TileInfo ti;
-      ti.f0 = c.B == 1 ? 0 : frame_of_point(c.frame_off, c.B, first);
-      ti.f1 = c.B == 1 ? 0 : max(frame_of_point(c.frame_off, c.B, last), ti.f0);
-      ti.r_lo = min(max(c.roi_off[ti.f0], 0), c.R);
-      ti.r_hi = min(max(c.roi_off[ti.f1 + 1], ti.r_lo), c.R);
-      c.tinfo[t] = ti;
-    }
+  if (blockIdx.x == 0 && b == 0) open_call(c, s_tmp);
 
   // ROIs of frame b (offsets clamped into [0, R], count into [0, max_rois])
-  int32_t r0 = min(max(c.roi_off[b], 0), c.R);
-  int32_t r1 = min(max(c.roi_off[b + 1], r0), c.R);
-  int32_t n = min(r1 - r0, c.max_rois);
+  const int32_t r0 = min(max(c.roi_off[b], 0), c.R);
+  const int32_t r1 = min(max(c.roi_off[b + 1], r0), c.R);
+  const int32_t n = min(r1 - r0, c.max_rois);
   for (int j = tid; j < n; j += kBlock) roi_cell_rect(c, c.rois[r0 + j], s_rect[j]);
   __syncthreads();
 
-  // one thread per cell (all W words of it) or per (sweep, word) of the budget masks
+  // cells: each thread owns kStageCellsPerThread cells at a time and walks
+  // the frame's ROI rectangles once for all of them
+  const int32_t stride = (int32_t)gridDim.x * kBlock;
   const int64_t cell_words = (int64_t)c.ncells * c.W;
-  const int64_t total = (int64_t)c.ncells + (int64_t)c.S * c.W;
-  for (int64_t e = (int64_t)blockIdx.x * kBlock + tid; e < total; e += (int64_t)gridDim.x * kBlock) {
-    if (e < c.ncells) {
-      const int32_t cell = (int32_t)e;
-      const int32_t cx = cell % c.ncx, cy = cell / c.ncx;
-      uint32_t any = 0;
-      for (int w = 0; w < c.W; ++w) {
-        uint32_t word = 0;
-        for (int k = 0; k < 32; ++k) {
-          int j = w * 32 + k;
-          if (j < n && cx >= s_rect[j][0] && cx <= s_rect[j][1] && cy >= s_rect[j][2] && cy <= s_rect[j][3])
-            word |= 1u << k;
-        }
-        c.cellmask[(int64_t)b * cell_words + (int64_t)cell * c.W + w] = word;
-        any |= word;
-      }
-      if (c.W > 1) c.cellany[(int64_t)b * c.ncells + cell] = any;
-    } else {
-      int64_t e2 = e - c.ncells;
-      int32_t s = (int32_t)(e2 / c.W), w = (int32_t)(e2 % c.W);
-      uint32_t word = 0;
-      for (int k = 0; k < 32; ++k) {
-        int j = w * 32 + k;
-        if (j < n && (int32_t)c.budget[r0 + j] > s) word |= 1u << k;
-      }
-      c.budgetmask[((int64_t)b * c.S + s) * c.W + w] = word;
+  for (int32_t g0 = (int32_t)blockIdx.x * kBlock + tid; g0 < c.ncells; g0 += stride * kStageCellsPerThread) {
+    int32_t cx[kStageCellsPerThread], cy[kStageCellsPerThread];
+    uint32_t any[kStageCellsPerThread];
+#pragma unroll
+    for (int i = 0; i < kStageCellsPerThread; ++i) {
+      const int32_t cell = g0 + i * stride;
+      cx[i] = cell % c.ncx;
+      cy[i] = cell < c.ncells ? cell / c.ncx : 0x7fff;  // rows past the grid match no rectangle
+      any[i] = 0;
     }
+    for (int w = 0; w < c.W; ++w) {
+      uint32_t word[kStageCellsPerThread];
+#pragma unroll
+      for (int i = 0; i < kStageCellsPerThread; ++i) word[i] = 0;
+      const int kn = min(32, n - w * 32);
+      for (int k = 0; k < kn; ++k) {
+        const int16_t* rc = s_rect[w * 32 + k];  // same address in every lane
+        const int32_t x0 = rc[0], x1 = rc[1], y0 = rc[2], y1 = rc[3];
+#pragma unroll
+        for (int i = 0; i < kStageCellsPerThread; ++i)
+          word[i] |= (cx[i] >= x0 && cx[i] <= x1 && cy[i] >= y0 && cy[i] <= y1) ? 1u << k : 0u;
+      }
+#pragma unroll
+      for (int i = 0; i < kStageCellsPerThread; ++i) {
+        const int32_t cell = g0 + i * stride;
+        if (cell < c.ncells) c.cellmask[(int64_t)b * cell_words + (int64_t)cell * c.W + w] = word[i];
+        any[i] |= word[i];
+      }
+    }
+    if (c.W > 1)
+#pragma unroll
+      for (int i = 0; i < kStageCellsPerThread; ++i) {
+        const int32_t cell = g0 + i * stride;
+        if (cell < c.ncells) c.cellany[(int64_t)b * c.ncells + cell] = any[i];
+      }
+  }
+  // budget masks: one thread per (sweep, word)
+  for (int32_t e = (int32_t)blockIdx.x * kBlock + tid; e < c.S * c.W; e += stride) {
+    const int32_t s = e / c.W, w = e % c.W;
+    uint32_t word = 0;
+    const int kn = min(32, n - w * 32);
+    for (int k = 0; k < kn; ++k)
+      if ((int32_t)c.budget[r0 + w * 32 + k] > s) word |= 1u << k;
+    c.budgetmask[((int64_t)b * c.S + s) * c.W + w] = word;
   }
 }
 
@@ -167,8 +204,10 @@ __global__ __launch_bounds__(kBlock) void fill_zero_kernel(uint4* p, size_t n16,
 }  // namespace
 
 hipError_t launch_stage(const Config& c, hipStream_t st) {
-  int64_t total = std::max<int64_t>((int64_t)c.ncells + (int64_t)c.S * c.W, c.filter_tiles);
-  int gx = (int)std::min<int64_t>((total + kBlock - 1) / kBlock, 128);
+  // a few workgroups per frame, each thread covering several cells
+  const int64_t work = std::max<int64_t>((int64_t)c.ncells, (int64_t)c.S * c.W);
+  const int gx = (int)std::min<int64_t>(
+      std::max<int64_t>(1, (work + kBlock * kStageCellsPerThread - 1) / (kBlock * kStageCellsPerThread)), 64);
   hipLaunchKernelGGL(stage_kernel, dim3(gx, c.B), dim3(kBlock), 0, st, c);
   return hipGetLastError();
 }

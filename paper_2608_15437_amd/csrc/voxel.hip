@@ -1,38 +1,38 @@
 // After the sort: voxels, per-frame cap, mean pooling.
 //
-// unique    -- flag the first pair of every run of equal (frame, key) in the
-//              sorted order: heads are counted per chunk, then numbered (each
-//              chunk adds the counts of the chunks before it); writes the
-//              first sorted position of each voxel and the first voxel of
-//              each frame.
-// finalize  -- one workgroup: closes the per-frame voxel ranges (the head
-//              scan writes the first voxel of every frame up to the last
-//              kept pair's), flags the frames over max_voxels, and writes
-//              the output offsets of every frame.
-// cap       -- one workgroup per frame over max_voxels: radix select of the
-//              voxels with the smallest first point index, then their rank
-//              in key order (the output row inside the frame).
-// mean      -- one thread per voxel: output row, and the mean of the voxel's
-//              first max_points points, recomputing x', y', z' with the same
-//              fused chain as the filter (Eq. 6) and summing in double in
-//              ascending point order (Alg. 1 VoxelFeatureEncoder read as
-//              mean pooling).
+// The sorted pairs are grouped by frame and ordered by key inside each
+// frame; the pair chunks of the radix passes (each inside one frame) are
+// reused.  Per-voxel data sits at slot fstart[b] + v for voxel v of frame b
+// (a frame has no more voxels than kept pairs).
+// ucount   -- heads (first pair of every run of equal keys inside a frame)
+//             per pair chunk;
+// uwrite   -- numbers the heads inside their frame (the heads of the frame's
+//             earlier chunks come first) and writes each voxel's first
+//             sorted pair at its slot;
+// finalize -- one workgroup: every frame's voxels, the voxels of the frames
+//             before it (global voxel numbering), and the output offsets of
+//             every frame (at most max_voxels rows each) with the
+//             capped-voxel count;
+// cap      -- one workgroup per frame over max_voxels: radix select of the
+//             voxels with the smallest first point index, then their rank
+//             in key order (the output row inside the frame);
+// mean     -- one thread per voxel: output row, and the mean of the voxel's
+//             first max_points points, recomputing x', y', z' with the same
+//             fused chain as the filter (Eq. 6) and summing in double in
+//             ascending point order (Alg. 1 VoxelFeatureEncoder read as mean
+//             pooling).
 #include "launch.hpp"
 
 namespace mmbev {
 
 namespace {
 
-__device__ __forceinline__ uint32_t local_key(const Config& c, uint32_t key) {
-  return (c.key_has_frame && c.fb > 0) ? (key & ((1u << c.kb) - 1u)) : key;
-}
-
-// Frame b of voxel v from the per-frame voxel offsets: largest b, vox_off[b] <= v.
-__device__ __forceinline__ int32_t frame_from_offsets(const Config& c, uint32_t v) {
+// Frame b of global voxel g: largest b, vox_off[b] <= g.
+__device__ __forceinline__ int32_t frame_of_voxel(const Config& c, uint32_t g) {
   int32_t lo = 0, hi = c.B - 1;
   while (lo < hi) {
     int32_t mid = (lo + hi + 1) >> 1;
-    if (c.vox_off[mid] <= v)
+    if (c.vox_off[mid] <= g)
       lo = mid;
     else
       hi = mid - 1;
@@ -40,147 +40,116 @@ __device__ __forceinline__ int32_t frame_from_offsets(const Config& c, uint32_t 
   return lo;
 }
 
-// Frame of a sorted pair: from the key's top bits, or from the point index
-// through frame offsets staged in LDS (off) or read from global memory.
-__device__ __forceinline__ int32_t pair_frame(const Config& c, const uint32_t* off, bool lds, uint32_t key,
-                                              uint32_t val) {
-  if (c.B == 1) return 0;
-  if (c.key_has_frame) return (int32_t)(key >> c.kb);
-  if (!lds) return frame_of_point(c.frame_off, c.B, (int64_t)val);
-  int32_t lo = 0, hi = c.B - 1;
-  while (lo < hi) {
-    int32_t mid = (lo + hi + 1) >> 1;
-    if (off[mid] <= val)
-      lo = mid;
-    else
-      hi = mid - 1;
-  }
-  return lo;
+// Whether sorted pair i of a frame whose first pair is ff starts a voxel.
+__device__ __forceinline__ bool is_head(const uint32_t* keys, uint32_t ff, uint32_t i) {
+  return i == ff || keys[i] != keys[i - 1];
 }
 
-// Whether sorted pair k starts a voxel (the first pair, or a new frame or key).
-__device__ __forceinline__ bool is_head(const Config& c, const uint32_t* keys, const uint32_t* vals, const uint32_t* off,
-                                        bool lds, uint32_t k, int32_t& frame) {
-  const uint32_t key = keys[k];
-  const bool need_frame = !c.key_has_frame && c.B > 1;
-  frame = pair_frame(c, off, lds, key, need_frame ? vals[k] : 0u);
-  if (k == 0) return true;
-  const uint32_t pk = keys[k - 1];
-  if (pk != key) return true;
-  if (!need_frame) return false;
-  return pair_frame(c, off, lds, pk, vals[k - 1]) != frame;
-}
-
-// Heads per chunk of the sorted pairs.
-__global__ __launch_bounds__(kBlock) void ucount_kernel(Config c, const uint32_t* keys, const uint32_t* vals) {
+__global__ __launch_bounds__(kBlock) void ucount_kernel(Config c, const uint32_t* keys) {
   __shared__ uint32_t s_tmp[kWaves];
-  extern __shared__ uint32_t dyn_off[];
   const int tid = threadIdx.x;
-  const uint32_t K = c.hdr->kept;
-  const bool lds = !c.key_has_frame && c.B > 1 && c.B <= kMaxSortLdsFrames;
-  if (lds)
-    for (int e = tid; e <= c.B; e += kBlock)
-      dyn_off[e] = (uint32_t)min(max(c.frame_off[e], (int64_t)0), (int64_t)c.N);
-  __syncthreads();
-  uint32_t lo, hi;
-  chunk_range(K, blockIdx.x, gridDim.x, lo, hi);
+  const uint32_t k = blockIdx.x;
+  if (k >= c.hdr->schunks) return;
+  const uint4 ch = c.schunk[k];
+  const uint32_t lo = ch.x, hi = ch.y, ff = ch.w;
   uint32_t n = 0;
-  for (uint32_t k = lo + tid; k < hi; k += kBlock) {
-    int32_t f;
-    n += is_head(c, keys, vals, dyn_off, lds, k, f) ? 1u : 0u;
+  for (uint32_t base = lo; base < hi; base += kBlock * kCountItems) {
+    bool hd[kCountItems];
+#pragma unroll
+    for (int j = 0; j < kCountItems; ++j) {
+      const uint32_t i = base + j * kBlock + tid;
+      hd[j] = i < hi && is_head(keys, ff, i);
+    }
+#pragma unroll
+    for (int j = 0; j < kCountItems; ++j) n += hd[j] ? 1u : 0u;
   }
   uint32_t total;
   (void)block_exclusive_scan(n, s_tmp, total);
-  if (tid == 0) c.hcount[blockIdx.x] = total;
+  if (tid == 0) c.hcount[k] = total;
 }
 
-// Numbers the heads (the chunk's offset is the heads of all earlier chunks):
-// first sorted position of every voxel, first voxel of every frame.
-__global__ __launch_bounds__(kBlock) void uwrite_kernel(Config c, const uint32_t* keys, const uint32_t* vals) {
+__global__ __launch_bounds__(kBlock) void uwrite_kernel(Config c, const uint32_t* keys) {
   __shared__ uint32_t s_tmp[kWaves];
-  __shared__ uint32_t s_run;
-  extern __shared__ uint32_t dyn_off[];
   const int tid = threadIdx.x;
-  WsHeader* h = c.hdr;
-  const uint32_t K = h->kept;
-  const bool lds = !c.key_has_frame && c.B > 1 && c.B <= kMaxSortLdsFrames;
-  if (lds)
-    for (int e = tid; e <= c.B; e += kBlock)
-      dyn_off[e] = (uint32_t)min(max(c.frame_off[e], (int64_t)0), (int64_t)c.N);
+  const uint32_t k = blockIdx.x;
+  if (k >= c.hdr->schunks) return;
+  const uint4 ch = c.schunk[k];
+  const uint32_t lo = ch.x, hi = ch.y, ff = ch.w;
+  uint32_t v0;
   {
     uint32_t part = 0;
-    for (uint32_t w = tid; w < blockIdx.x; w += kBlock) part += c.hcount[w];
+    for (uint32_t w = c.schunk_first[ch.z] + tid; w < k; w += kBlock) part += c.hcount[w];
     uint32_t before;
     (void)block_exclusive_scan(part, s_tmp, before);
-    if (tid == 0) {
-      s_run = before;
-      if (blockIdx.x == gridDim.x - 1) h->voxels = before + c.hcount[blockIdx.x];
-    }
+    v0 = before;
   }
-  __syncthreads();
-  uint32_t lo, hi;
-  chunk_range(K, blockIdx.x, gridDim.x, lo, hi);
   for (uint32_t base = lo; base < hi; base += kScanTile) {
     // kScanItems consecutive pairs per thread
     const uint32_t first = base + tid * kScanItems;
     uint32_t heads = 0;
-    int32_t frame[kScanItems];
 #pragma unroll
     for (int j = 0; j < kScanItems; ++j) {
-      frame[j] = -1;
-      const uint32_t k = first + j;
-      if (k < hi) {
-        int32_t f;
-        if (is_head(c, keys, vals, dyn_off, lds, k, f)) heads |= 1u << j;
-        frame[j] = f;
-      }
+      const uint32_t i = first + j;
+      if (i < hi && is_head(keys, ff, i)) heads |= 1u << j;
     }
     uint32_t total;
-    const uint32_t excl = block_exclusive_scan(__popc(heads), s_tmp, total);
-    uint32_t vid = s_run + excl;
-    // frame boundaries: a head whose frame is above its predecessor's starts
-    // that frame and every empty frame before it
-    int32_t pf = -1;
-    if (first > 0 && first < hi) {
-      const uint32_t pk = keys[first - 1];
-      const bool need_frame = !c.key_has_frame && c.B > 1;
-      pf = pair_frame(c, dyn_off, lds, pk, need_frame ? vals[first - 1] : 0u);
-    }
+    uint32_t v = v0 + block_exclusive_scan(__popc(heads), s_tmp, total);
 #pragma unroll
-    for (int j = 0; j < kScanItems; ++j) {
-      if (heads & (1u << j)) {
-        c.seg_start[vid] = first + j;
-        const int32_t f = min(frame[j], c.B - 1);
-        for (int32_t b = pf + 1; b <= f; ++b) c.vox_off[b] = vid;
-        ++vid;
-      }
-      if (frame[j] >= 0) pf = frame[j];
-    }
-    __syncthreads();
-    if (tid == 0) s_run += total;
-    __syncthreads();
+    for (int j = 0; j < kScanItems; ++j)
+      if (heads & (1u << j)) c.seg_start[ff + v++] = first + j;
+    v0 += total;
   }
 }
 
-__global__ __launch_bounds__(kBlock) void finalize_kernel(Config c, const uint32_t* keys, const uint32_t* vals) {
+// Exclusive prefix of n values in[0..n) written to out (may alias, or null);
+// returns the total.  One workgroup, kScanItems consecutive values per thread.
+__device__ uint32_t scan_array(const uint32_t* in, uint32_t* out, uint32_t n, uint32_t* s_tmp) {
+  const int tid = threadIdx.x;
+  uint32_t carry = 0;
+  for (uint32_t base = 0; base < n; base += kScanTile) {
+    const uint32_t first = base + tid * kScanItems;
+    uint32_t v[kScanItems], sum = 0;
+#pragma unroll
+    for (int j = 0; j < kScanItems; ++j) {
+      v[j] = first + j < n ? in[first + j] : 0u;
+      sum += v[j];
+    }
+    uint32_t total;
+    uint32_t run = carry + block_exclusive_scan(sum, s_tmp, total);
+    if (out)
+#pragma unroll
+      for (int j = 0; j < kScanItems; ++j)
+        if (first + j < n) {
+          out[first + j] = run;
+          run += v[j];
+        }
+    carry += total;
+  }
+  return carry;
+}
+
+__global__ __launch_bounds__(kBlock) void finalize_kernel(Config c) {
   __shared__ uint32_t s_tmp[kWaves];
-  __shared__ int32_t s_last;
   const int tid = threadIdx.x;
   WsHeader* h = c.hdr;
-  const uint32_t V = h->voxels;
-  const uint32_t K = h->kept;
-  if (tid == 0) {
-    c.seg_start[V] = K;
-    s_last = K > 0 ? min(pair_frame(c, nullptr, false, keys[K - 1], vals[K - 1]), c.B - 1) : -1;
+  const uint32_t ns = h->schunks;
+  // heads before every pair chunk (in place), then every frame's voxels
+  const uint32_t V = scan_array(c.hcount, c.hcount, ns, s_tmp);
+  __syncthreads();
+  for (int b = tid; b < c.B; b += kBlock) {
+    const uint32_t k0 = min(c.schunk_first[b], ns), k1 = min(c.schunk_first[b + 1], ns);
+    c.vcount[b] = (k1 < ns ? c.hcount[k1] : V) - (k0 < ns ? c.hcount[k0] : V);
   }
   __syncthreads();
-  // frames after the last kept pair's frame start at V
-  for (int b = s_last + 1 + tid; b <= c.B; b += kBlock) c.vox_off[b] = V;
-  __syncthreads();
+  (void)scan_array(c.vcount, c.vox_off, (uint32_t)c.B, s_tmp);
+  if (tid == 0) {
+    c.vox_off[c.B] = V;
+    h->voxels = V;
+  }
   uint32_t carry_out = 0, carry_cap = 0;
   for (int chunk = 0; chunk < c.B; chunk += kBlock) {
     const int b = chunk + tid;
-    const uint32_t vb = b < c.B ? c.vox_off[b + 1] - c.vox_off[b] : 0u;
+    const uint32_t vb = b < c.B ? c.vcount[b] : 0u;
     const uint32_t capped = vb > (uint32_t)c.cap;
     const uint32_t outc = capped ? (uint32_t)c.cap : vb;
     uint32_t t1, t2;
@@ -207,13 +176,11 @@ __global__ __launch_bounds__(kBlock) void cap_kernel(Config c, const uint32_t* v
   __shared__ uint32_t s_sel, s_k;
   const int tid = threadIdx.x;
   const int b = blockIdx.x;
-  WsHeader* h = c.hdr;
-  const uint32_t v0 = c.vox_off[b];
-  const uint32_t nv = c.vox_off[b + 1] - v0;
-  if (nv <= (uint32_t)c.cap || h->kept == 0) return;
-  const uint32_t K = h->kept;
-  uint32_t* fk = c.capkey + v0;
-  for (uint32_t v = tid; v < nv; v += kBlock) fk[v] = vals[min(c.seg_start[v0 + v], K - 1)];
+  const uint32_t nv = c.vcount[b];
+  if (nv <= (uint32_t)c.cap) return;
+  const uint32_t fs = c.fstart[b];
+  uint32_t* fk = c.capkey + fs;
+  for (uint32_t v = tid; v < nv; v += kBlock) fk[v] = vals[c.seg_start[fs + v]];
   __syncthreads();
   uint32_t prefix = 0, pmask = 0, k = (uint32_t)c.cap;
   for (int shift = 24; shift >= 0; shift -= 8) {
@@ -244,84 +211,154 @@ __global__ __launch_bounds__(kBlock) void cap_kernel(Config c, const uint32_t* v
     const bool keep = v < nv && fk[v] <= threshold;
     uint32_t total;
     const uint32_t excl = block_exclusive_scan(keep ? 1u : 0u, s_tmp, total);
-    if (v < nv) c.out_rank[v0 + v] = keep ? carry + excl : 0xffffffffu;
+    if (v < nv) c.out_rank[fs + v] = keep ? carry + excl : 0xffffffffu;
     carry += total;
   }
 }
 
-// One thread per voxel (grid-stride): output row, kept count, point indices
-// and the fp64 mean of every feature.
+// Workgroups of kMeanTile consecutive voxels (grid-stride), one thread per
+// voxel: output row, kept count, point indices and the fp64 mean of every
+// feature.  The points of a voxel are read kMeanBatch at a time, all their
+// loads in flight together.  When the block's rows are consecutive (no frame
+// over the cap in it) the rows are assembled in LDS and written as
+// contiguous runs; otherwise each thread writes its own row.
+constexpr int kMeanBatch = 8;
+
 __global__ __launch_bounds__(kBlock) void mean_kernel(Config c, const uint32_t* keys, const uint32_t* vals) {
+  extern __shared__ uint32_t sm[];
+  __shared__ int64_t s_row0;
+  __shared__ uint32_t s_contig;
   WsHeader* h = c.hdr;
+  const int tid = threadIdx.x;
   const uint32_t V = h->voxels;
   const uint32_t K = h->kept;
   const int64_t rows = (int64_t)c.B * c.cap;
   const int C = c.C, M = c.M;
-  for (uint32_t v = blockIdx.x * kBlock + threadIdx.x; v < V; v += gridDim.x * kBlock) {
-    const int32_t b = frame_from_offsets(c, v);
-    const uint32_t v0 = c.vox_off[b];
-    const bool capped = c.vox_off[b + 1] - v0 > (uint32_t)c.cap;
-    const uint32_t rank = capped ? c.out_rank[v] : v - v0;
-    if (rank == 0xffffffffu) continue;
-    const int64_t row = c.out_voxel_offsets[b] + (int64_t)rank;
-    if (row < 0 || row >= rows) {
-      raise_fault(h, MMBEV_FAULT_WAIT);
-      continue;
+  int32_t* l_co = (int32_t*)sm;              // [kMeanTile][4]
+  float* l_ft = (float*)(sm + kMeanTile * 4);  // [kMeanTile][C]
+  int32_t* l_pi = (int32_t*)(sm + kMeanTile * (4 + C));  // [kMeanTile][M]
+  for (uint32_t g0 = blockIdx.x * kMeanTile; g0 < V; g0 += gridDim.x * kMeanTile) {
+    const uint32_t g = g0 + tid;
+    const uint32_t nblk = min((uint32_t)kMeanTile, V - g0);
+    int64_t row = -1;
+    int32_t b = 0;
+    uint32_t s0 = 0, cnt = 0;
+    if (g < V) {
+      b = frame_of_voxel(c, g);
+      const uint32_t v = g - c.vox_off[b];
+      const uint32_t nv = c.vox_off[b + 1] - c.vox_off[b];
+      const uint32_t slot = c.fstart[b] + v;
+      const uint32_t rank = nv > (uint32_t)c.cap ? c.out_rank[slot] : v;
+      if (rank != 0xffffffffu) {
+        row = c.out_voxel_offsets[b] + (int64_t)rank;
+        if (row < 0 || row >= rows || slot >= K) {
+          raise_fault(h, MMBEV_FAULT_WAIT);
+          row = -1;
+        } else {
+          s0 = min(c.seg_start[slot], K - 1u);
+          const uint32_t s1 = max(min(v + 1 < nv ? c.seg_start[slot + 1] : c.fstart[b + 1], K), s0 + 1u);
+          cnt = min(s1 - s0, (uint32_t)M);
+        }
+      }
     }
-    const uint32_t s0 = min(c.seg_start[v], K), s1 = max(min(c.seg_start[v + 1], K), s0);
-    const uint32_t cnt = min(s1 - s0, (uint32_t)M);
-    const uint32_t kl = local_key(c, keys[s0]);
-    const uint32_t ix = kl % c.Dx, rest = kl / c.Dx;
-    const uint32_t iy = rest % c.Dy, iz = rest / c.Dy;
-    int32_t* co = c.out_coords + row * 4;
-    co[0] = b;
-    co[1] = (int32_t)iz;
-    co[2] = (int32_t)iy;
-    co[3] = (int32_t)ix;
-    c.out_counts[row] = (int32_t)cnt;
+    if (tid == 0) {
+      s_row0 = row;
+      s_contig = 1;
+    }
+    __syncthreads();
+    if ((uint32_t)tid < nblk && (row < 0 || row != s_row0 + tid)) s_contig = 0;  // every row valid and in order
+    // the voxel's coordinates and points
+    int32_t co[4] = {0, 0, 0, 0};
     double sum[8];
 #pragma unroll
     for (int f = 0; f < 8; ++f) sum[f] = 0.0;
-    int32_t* pidx = c.out_point_idx + row * M;
-    for (uint32_t m = 0; m < cnt; ++m) {
-      const uint32_t i = min(vals[s0 + m], (uint32_t)c.N - 1u);
-      pidx[m] = (int32_t)i;
-      const uint32_t s = min((uint32_t)c.sweep[i], (uint32_t)c.S - 1u);
-      const float* P = c.poses + ((int64_t)b * c.S + s) * 12;
-      float Pl[12];
-#pragma unroll
-      for (int q = 0; q < 12; ++q) Pl[q] = P[q];
-      float px, py, pz;
-      compensate(Pl, c.feat[i], c.feat[c.stride + i], c.feat[2 * c.stride + i], px, py, pz);
-      sum[0] += (double)px;
-      sum[1] += (double)py;
-      sum[2] += (double)pz;
-#pragma unroll
-      for (int f = 3; f < 8; ++f)
-        if (f < C) sum[f] += (double)c.feat[(int64_t)f * c.stride + i];
+    if (row >= 0) {
+      const uint32_t kl = keys[s0];
+      const uint32_t ix = kl % c.Dx, rest = kl / c.Dx;
+      co[0] = b;
+      co[1] = (int32_t)(rest / c.Dy);
+      co[2] = (int32_t)(rest % c.Dy);
+      co[3] = (int32_t)ix;
     }
-    for (int m = (int)cnt; m < M; ++m) pidx[m] = -1;
-    float* fo = c.out_feats + row * C;
+    __syncthreads();
+    const bool contig = s_contig != 0;
+    int32_t* pidx = contig ? l_pi + tid * M : c.out_point_idx + row * M;
+    for (uint32_t m0 = 0; m0 < cnt; m0 += kMeanBatch) {
+      uint32_t pi[kMeanBatch], sw[kMeanBatch];
+      float x[kMeanBatch], y[kMeanBatch], z[kMeanBatch], fx[kMeanBatch][5];
 #pragma unroll
-    for (int f = 0; f < 8; ++f)
-      if (f < C) fo[f] = (float)(sum[f] / (double)cnt);
+      for (int j = 0; j < kMeanBatch; ++j) pi[j] = m0 + j < cnt ? min(vals[s0 + m0 + j], (uint32_t)c.N - 1u) : 0u;
+#pragma unroll
+      for (int j = 0; j < kMeanBatch; ++j) {
+        const bool ok = m0 + j < cnt;
+        const uint32_t i = pi[j];
+        sw[j] = ok ? min((uint32_t)c.sweep[i], (uint32_t)c.S - 1u) : 0u;
+        x[j] = ok ? c.feat[i] : 0.0f;
+        y[j] = ok ? c.feat[c.stride + i] : 0.0f;
+        z[j] = ok ? c.feat[2 * c.stride + i] : 0.0f;
+#pragma unroll
+        for (int f = 3; f < 8; ++f) fx[j][f - 3] = (ok && f < C) ? c.feat[(int64_t)f * c.stride + i] : 0.0f;
+      }
+#pragma unroll
+      for (int j = 0; j < kMeanBatch; ++j)
+        if (m0 + j < cnt) {
+          const float* Pg = c.poses + ((int64_t)b * c.S + sw[j]) * 12;
+          float P[12];
+#pragma unroll
+          for (int q = 0; q < 12; ++q) P[q] = Pg[q];
+          float px, py, pz;
+          compensate(P, x[j], y[j], z[j], px, py, pz);
+          sum[0] += (double)px;  // ascending point order
+          sum[1] += (double)py;
+          sum[2] += (double)pz;
+#pragma unroll
+          for (int f = 3; f < 8; ++f) sum[f] += (double)fx[j][f - 3];
+          pidx[m0 + j] = (int32_t)pi[j];
+        }
+    }
+    if (row >= 0) {
+      for (int m = (int)cnt; m < M; ++m) pidx[m] = -1;
+      c.out_counts[row] = (int32_t)cnt;
+      if (contig) {
+#pragma unroll
+        for (int q = 0; q < 4; ++q) l_co[tid * 4 + q] = co[q];
+#pragma unroll
+        for (int f = 0; f < 8; ++f)
+          if (f < C) l_ft[tid * C + f] = (float)(sum[f] / (double)cnt);
+      } else {
+        int32_t* o = c.out_coords + row * 4;
+#pragma unroll
+        for (int q = 0; q < 4; ++q) o[q] = co[q];
+        float* fo = c.out_feats + row * C;
+#pragma unroll
+        for (int f = 0; f < 8; ++f)
+          if (f < C) fo[f] = (float)(sum[f] / (double)cnt);
+      }
+    }
+    __syncthreads();
+    if (contig) {
+      // rows s_row0 .. s_row0 + nblk - 1, written as contiguous runs
+      const int64_t r0 = s_row0;
+      for (uint32_t e = tid; e < nblk * 4; e += kBlock) c.out_coords[r0 * 4 + e] = l_co[e];
+      for (uint32_t e = tid; e < nblk * (uint32_t)C; e += kBlock) c.out_feats[r0 * C + e] = l_ft[e];
+      for (uint32_t e = tid; e < nblk * (uint32_t)M; e += kBlock) c.out_point_idx[r0 * M + e] = l_pi[e];
+    }
+    __syncthreads();
   }
 }
 
 }  // namespace
 
-hipError_t launch_unique(const Config& c, const uint32_t* keys, const uint32_t* vals, hipStream_t st) {
-  const bool lds = !c.key_has_frame && c.B > 1 && c.B <= kMaxSortLdsFrames;
-  const size_t dyn = lds ? (size_t)(c.B + 1) * 4 : 0;
-  hipLaunchKernelGGL(ucount_kernel, dim3(c.sort_chunks), dim3(kBlock), dyn, st, c, keys, vals);
+hipError_t launch_unique(const Config& c, const uint32_t* keys, hipStream_t st) {
+  hipLaunchKernelGGL(ucount_kernel, dim3(c.schunk_max), dim3(kBlock), 0, st, c, keys);
   const hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(uwrite_kernel, dim3(c.sort_chunks), dim3(kBlock), dyn, st, c, keys, vals);
+  hipLaunchKernelGGL(uwrite_kernel, dim3(c.schunk_max), dim3(kBlock), 0, st, c, keys);
   return hipGetLastError();
 }
 
-hipError_t launch_finalize(const Config& c, const uint32_t* keys, const uint32_t* vals, hipStream_t st) {
-  hipLaunchKernelGGL(finalize_kernel, dim3(1), dim3(kBlock), 0, st, c, keys, vals);
+hipError_t launch_finalize(const Config& c, hipStream_t st) {
+  hipLaunchKernelGGL(finalize_kernel, dim3(1), dim3(kBlock), 0, st, c);
   return hipGetLastError();
 }
 
@@ -331,7 +368,8 @@ hipError_t launch_cap(const Config& c, const uint32_t* vals, hipStream_t st) {
 }
 
 hipError_t launch_mean(const Config& c, const uint32_t* keys, const uint32_t* vals, hipStream_t st) {
-  hipLaunchKernelGGL(mean_kernel, dim3(c.mean_grid), dim3(kBlock), 0, st, c, keys, vals);
+  const size_t lds = (size_t)kMeanTile * (4 + c.C + c.M) * 4;
+  hipLaunchKernelGGL(mean_kernel, dim3(c.mean_grid), dim3(kBlock), lds, st, c, keys, vals);
   return hipGetLastError();
 }
 

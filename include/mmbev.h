@@ -52,7 +52,7 @@
 extern "C" {
 #endif
 
-#define MMBEV_ABI_VERSION 1
+#define MMBEV_ABI_VERSION 2
 
 /* ------------------------------------------------------------- status */
 typedef int32_t mmbev_status_t;
@@ -120,9 +120,9 @@ int32_t mmbev_abi_version(void);
 const char* mmbev_status_string(mmbev_status_t status);
 
 /* Workspace bytes mmbev_roi_voxelize needs for these sizes (0 if they are
- * invalid).  The workspace depends only on the grid, num_points and
- * max_rois_per_frame. */
-size_t mmbev_roi_voxelize_workspace_bytes(const mmbev_grid_t* grid, int64_t num_points,
+ * invalid).  The workspace depends only on the grid, num_points,
+ * num_features (C, 3..8) and max_rois_per_frame. */
+size_t mmbev_roi_voxelize_workspace_bytes(const mmbev_grid_t* grid, int64_t num_points, int32_t num_features,
                                           int32_t max_rois_per_frame);
 
 /* Zero-fill a workspace on `stream` (a hipStream_t; NULL = default stream).

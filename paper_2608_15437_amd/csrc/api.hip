@@ -25,8 +25,8 @@ struct Plan {
   int32_t cell_shift, ncx, ncy, ncells;
   int32_t kb, passes, dbits;
   int64_t fchunk_points, fchunk_max, filter_grid, schunk_max, mean_grid;
-  size_t off_hdr, off_cellmask, off_cellany, off_budgetmask, off_fchunk_first, off_fcount, off_fchunk_lo, off_fprefix,
-      off_fstart, off_schunk_first, off_schunk, off_cnt, off_ftot, off_hcount, off_vcount, off_keys[2], off_vals[2], off_seg,
+  size_t off_hdr, off_cellmask, off_cellany, off_budgetmask, off_fchunk_first, off_fcount, off_fchunk_lo, off_fchunk_frame, off_fprefix,
+      off_fstart, off_schunk_first, off_schunk, off_cnt, off_ftot, off_hcount, off_vcount, off_keys[2], off_vals[2], off_rec, off_seg,
       off_capkey, off_rank, off_voxoff, total;
 };
 
@@ -95,6 +95,7 @@ mmbev_status_t make_plan(const mmbev_grid_t* g, int64_t N, int32_t max_rois, int
   p->off_fchunk_first = take((size_t)(p->B + 1) * 4);
   p->off_fcount = take((size_t)p->fchunk_max * 4);
   p->off_fchunk_lo = take((size_t)p->fchunk_max * 4);
+  p->off_fchunk_frame = take((size_t)p->fchunk_max * 4);
   p->off_fprefix = take((size_t)(p->fchunk_max + 1) * 4);
   p->off_fstart = take((size_t)(p->B + 1) * 4);
   p->off_schunk_first = take((size_t)(p->B + 1) * 4);
@@ -107,6 +108,7 @@ mmbev_status_t make_plan(const mmbev_grid_t* g, int64_t N, int32_t max_rois, int
     p->off_keys[q] = take((size_t)n1 * 4);
     p->off_vals[q] = take((size_t)n1 * 4);
   }
+  p->off_rec = take((size_t)n1 * 4 * ((1 + p->C + 3) / 4 * 4));
   p->off_seg = take((size_t)n1 * 4);
   p->off_capkey = take((size_t)n1 * 4);
   p->off_rank = take((size_t)n1 * 4);
@@ -132,9 +134,10 @@ const char* mmbev_status_string(mmbev_status_t s) {
   }
 }
 
-size_t mmbev_roi_voxelize_workspace_bytes(const mmbev_grid_t* grid, int64_t num_points, int32_t max_rois_per_frame) {
+size_t mmbev_roi_voxelize_workspace_bytes(const mmbev_grid_t* grid, int64_t num_points, int32_t num_features,
+                                          int32_t max_rois_per_frame) {
   Plan p;
-  if (make_plan(grid, num_points, max_rois_per_frame, 3, &p) != MMBEV_OK) return 0;
+  if (make_plan(grid, num_points, max_rois_per_frame, num_features, &p) != MMBEV_OK) return 0;
   return p.total;
 }
 
@@ -257,6 +260,7 @@ mmbev_status_t voxelize(const mmbev_points_t* points, const uint8_t* sweep_ids, 
   c.fchunk_first = (uint32_t*)(ws + p.off_fchunk_first);
   c.fcount = (uint32_t*)(ws + p.off_fcount);
   c.fchunk_lo = (uint32_t*)(ws + p.off_fchunk_lo);
+  c.fchunk_frame = (uint32_t*)(ws + p.off_fchunk_frame);
   c.fprefix = (uint32_t*)(ws + p.off_fprefix);
   c.fstart = (uint32_t*)(ws + p.off_fstart);
   c.schunk_first = (uint32_t*)(ws + p.off_schunk_first);
@@ -269,6 +273,8 @@ mmbev_status_t voxelize(const mmbev_points_t* points, const uint8_t* sweep_ids, 
     c.keys[q] = (uint32_t*)(ws + p.off_keys[q]);
     c.vals[q] = (uint32_t*)(ws + p.off_vals[q]);
   }
+  c.rec = (uint32_t*)(ws + p.off_rec);
+  c.rec_words = (1 + p.C + 3) / 4 * 4;
   c.seg_start = (uint32_t*)(ws + p.off_seg);
   c.capkey = (uint32_t*)(ws + p.off_capkey);
   c.out_rank = (uint32_t*)(ws + p.off_rank);

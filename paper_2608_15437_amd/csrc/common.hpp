@@ -84,6 +84,7 @@ struct Config {
   uint32_t* fchunk_first;  // [B+1] first filter chunk of frame b
   uint32_t* fcount;        // [fchunk_max] kept pairs of filter chunk k
   uint32_t* fchunk_lo;     // [fchunk_max] first point of filter chunk k (its kept pairs start there)
+  uint32_t* fchunk_frame;  // [fchunk_max] frame of filter chunk k
   uint32_t* fprefix;       // [fchunk_max + 1] kept pairs of the filter chunks before k
   uint32_t* fstart;        // [B+1] first sorted pair of frame b (kept pairs of the frames before it)
   uint32_t* schunk_first;  // [B+1] first pair chunk of frame b
@@ -93,7 +94,12 @@ struct Config {
   uint32_t* hcount;        // [schunk_max] voxel heads of pair chunk k
   uint32_t* vcount;        // [B] voxels of frame b
   uint32_t* keys[2];       // [N] each: [0] first holds the filter's per-chunk regions
-  uint32_t* vals[2];       // point index of the pair
+  uint32_t* vals[2];       // the pair's record: its place in compact (point) order
+  // records of the kept points in compact order, written by the compaction:
+  // rec_words words each (a multiple of 4), word 0 the point index, then
+  // x', y', z' (Eq. 6) and the raw features 3..C-1 as float bits
+  uint32_t* rec;           // [N][rec_words]
+  int32_t rec_words;
   // per voxel, at slot fstart[b] + v for voxel v of frame b
   uint32_t* seg_start;     // [N] first sorted pair of the voxel
   uint32_t* capkey;        // [N] first point index of the voxel (frames over the cap)

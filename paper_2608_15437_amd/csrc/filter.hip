@@ -454,6 +454,7 @@ __global__ __launch_bounds__(kBlock) void filter_kernel(Config c) {
   if (lane == 0) {
     c.fcount[k] = wr.kept;
     c.fchunk_lo[k] = lo;
+    c.fchunk_frame[k] = (uint32_t)b;
   }
 }
 

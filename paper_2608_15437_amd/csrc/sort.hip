@@ -15,8 +15,10 @@
 //             first pair of every frame, and the pair chunks (about
 //             kSortGrid of them, chunk_pairs pairs each, the last of a frame
 //             shorter).
-// compact  -- one wave per filter chunk: its kept pairs (at the start of the
-//             chunk's point range) copied to their compact place.
+// compact  -- one workgroup per filter chunk: its kept pairs (at the start of the
+//             chunk's point range) copied to their compact place, and the
+//             kept points' records (index, x', y', z', features) written
+//             there, so the mean reads compact records instead of points.
 // Then per pass:
 // count    -- workgroup k counts the digits of pair chunk k (row k of the
 //             [chunk][digit] count matrix);
@@ -131,27 +133,56 @@ __global__ __launch_bounds__(kBlock) void segments_kernel(Config c) {
   }
 }
 
-// One wave per filter chunk: its kept pairs to [fprefix[k], fprefix[k+1]).
+// One workgroup per filter chunk: its kept pairs to [fprefix[k],
+// fprefix[k+1]), and the kept points' records at the same places.  The
+// points of a chunk are visited in increasing index order, so their reads
+// stay close together (kept points come in runs); the frame's poses are
+// staged in LDS and each record is written with 16-byte stores.  The pair's
+// value becomes its compact place (the record's index).
+constexpr int kCompactItems = 4;
+
 __global__ __launch_bounds__(kBlock) void compact_kernel(Config c, uint32_t* kout, uint32_t* vout) {
-  constexpr int kUnroll = 8;
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const uint32_t k = blockIdx.x * kWaves + wave;
+  extern __shared__ float s_pose[];  // [S][12]
+  const int tid = threadIdx.x;
+  const uint32_t k = blockIdx.x;
   if (k >= c.hdr->fchunks) return;
   const uint32_t lo = c.fchunk_lo[k], n = c.fcount[k], dst = c.fprefix[k];
-  for (uint32_t base = 0; base < n; base += 64 * kUnroll) {
-    uint32_t kk[kUnroll], vv[kUnroll];
+  const int32_t b = (int32_t)c.fchunk_frame[k];
+  const int C = c.C, RW = c.rec_words;
+  for (int e = tid; e < c.S * 12; e += kBlock) s_pose[e] = c.poses[(int64_t)b * c.S * 12 + e];
+  __syncthreads();
+  for (uint32_t base = 0; base < n; base += kBlock * kCompactItems) {
+    uint32_t kk[kCompactItems], pi[kCompactItems], sw[kCompactItems];
+    float v[kCompactItems][8];
 #pragma unroll
-    for (int u = 0; u < kUnroll; ++u) {
-      const uint32_t i = base + u * 64 + lane;
-      kk[u] = i < n ? c.keys[0][lo + i] : 0u;
-      vv[u] = i < n ? c.vals[0][lo + i] : 0u;
+    for (int u = 0; u < kCompactItems; ++u) {
+      const uint32_t t = base + u * kBlock + tid;
+      kk[u] = t < n ? c.keys[0][lo + t] : 0u;
+      pi[u] = t < n ? min(c.vals[0][lo + t], (uint32_t)c.N - 1u) : 0u;
     }
 #pragma unroll
-    for (int u = 0; u < kUnroll; ++u) {
-      const uint32_t i = base + u * 64 + lane;
-      if (i < n) {
-        kout[dst + i] = kk[u];
-        vout[dst + i] = vv[u];
+    for (int u = 0; u < kCompactItems; ++u) {  // all point loads of the batch in flight together
+      const bool ok = base + u * kBlock + tid < n;
+      const uint32_t i = pi[u];
+      sw[u] = ok ? min((uint32_t)c.sweep[i], (uint32_t)c.S - 1u) : 0u;
+#pragma unroll
+      for (int f = 0; f < 8; ++f) v[u][f] = (ok && f < C) ? c.feat[(int64_t)f * c.stride + i] : 0.0f;
+    }
+#pragma unroll
+    for (int u = 0; u < kCompactItems; ++u) {
+      const uint32_t t = base + u * kBlock + tid;
+      if (t < n) {
+        const uint32_t q = dst + t;
+        float px, py, pz;
+        compensate(s_pose + sw[u] * 12, v[u][0], v[u][1], v[u][2], px, py, pz);
+        kout[q] = kk[u];
+        vout[q] = q;
+        uint4* r = reinterpret_cast<uint4*>(c.rec + (int64_t)q * RW);
+        r[0] = make_uint4(pi[u], __float_as_uint(px), __float_as_uint(py), __float_as_uint(pz));
+        if (RW > 4)
+          r[1] = make_uint4(__float_as_uint(v[u][3]), __float_as_uint(v[u][4]), __float_as_uint(v[u][5]),
+                            __float_as_uint(v[u][6]));
+        if (RW > 8) r[2] = make_uint4(__float_as_uint(v[u][7]), 0u, 0u, 0u);
       }
     }
   }
@@ -343,7 +374,8 @@ hipError_t launch_segments(const Config& c, hipStream_t st) {
 }
 
 hipError_t launch_compact(const Config& c, uint32_t* kout, uint32_t* vout, hipStream_t st) {
-  hipLaunchKernelGGL(compact_kernel, dim3(c.filter_grid), dim3(kBlock), 0, st, c, kout, vout);
+  const size_t lds = (size_t)c.S * 12 * sizeof(float);
+  hipLaunchKernelGGL(compact_kernel, dim3(c.fchunk_max), dim3(kBlock), lds, st, c, kout, vout);
   return hipGetLastError();
 }
 

@@ -17,8 +17,8 @@
 //             voxels with the smallest first point index, then their rank
 //             in key order (the output row inside the frame);
 // mean     -- one thread per voxel: output row, and the mean of the voxel's
-//             first max_points points, recomputing x', y', z' with the same
-//             fused chain as the filter (Eq. 6) and summing in double in
+//             first max_points points from their compact records (x', y',
+//             z' of Eq. 6 and the raw features), summed in double in
 //             ascending point order (Alg. 1 VoxelFeatureEncoder read as mean
 //             pooling).
 #include "launch.hpp"
@@ -218,8 +218,8 @@ __global__ __launch_bounds__(kBlock) void cap_kernel(Config c, const uint32_t* v
 
 // Workgroups of kMeanTile consecutive voxels (grid-stride), one thread per
 // voxel: output row, kept count, point indices and the fp64 mean of every
-// feature.  The points of a voxel are read kMeanBatch at a time, all their
-// loads in flight together.  When the block's rows are consecutive (no frame
+// feature.  The records of a voxel's points are read kMeanBatch at a time,
+// all their loads in flight together.  When the block's rows are consecutive (no frame
 // over the cap in it) the rows are assembled in LDS and written as
 // contiguous runs; otherwise each thread writes its own row.
 constexpr int kMeanBatch = 8;
@@ -283,38 +283,34 @@ __global__ __launch_bounds__(kBlock) void mean_kernel(Config c, const uint32_t* 
     __syncthreads();
     const bool contig = s_contig != 0;
     int32_t* pidx = contig ? l_pi + tid * M : c.out_point_idx + row * M;
+    const int RW = c.rec_words;
     for (uint32_t m0 = 0; m0 < cnt; m0 += kMeanBatch) {
-      uint32_t pi[kMeanBatch], sw[kMeanBatch];
-      float x[kMeanBatch], y[kMeanBatch], z[kMeanBatch], fx[kMeanBatch][5];
+      uint32_t q[kMeanBatch];
+      uint4 r0[kMeanBatch], r1[kMeanBatch];
 #pragma unroll
-      for (int j = 0; j < kMeanBatch; ++j) pi[j] = m0 + j < cnt ? min(vals[s0 + m0 + j], (uint32_t)c.N - 1u) : 0u;
+      for (int j = 0; j < kMeanBatch; ++j) q[j] = m0 + j < cnt ? min(vals[s0 + m0 + j], K - 1u) : 0u;
 #pragma unroll
-      for (int j = 0; j < kMeanBatch; ++j) {
-        const bool ok = m0 + j < cnt;
-        const uint32_t i = pi[j];
-        sw[j] = ok ? min((uint32_t)c.sweep[i], (uint32_t)c.S - 1u) : 0u;
-        x[j] = ok ? c.feat[i] : 0.0f;
-        y[j] = ok ? c.feat[c.stride + i] : 0.0f;
-        z[j] = ok ? c.feat[2 * c.stride + i] : 0.0f;
-#pragma unroll
-        for (int f = 3; f < 8; ++f) fx[j][f - 3] = (ok && f < C) ? c.feat[(int64_t)f * c.stride + i] : 0.0f;
+      for (int j = 0; j < kMeanBatch; ++j) {  // one or two 16-byte loads per record
+        const uint4* r = reinterpret_cast<const uint4*>(c.rec + (int64_t)q[j] * RW);
+        if (m0 + j < cnt) {
+          r0[j] = r[0];
+          r1[j] = RW > 4 ? r[1] : make_uint4(0, 0, 0, 0);
+        } else {
+          r0[j] = r1[j] = make_uint4(0, 0, 0, 0);
+        }
       }
 #pragma unroll
       for (int j = 0; j < kMeanBatch; ++j)
         if (m0 + j < cnt) {
-          const float* Pg = c.poses + ((int64_t)b * c.S + sw[j]) * 12;
-          float P[12];
+          const uint32_t w[8] = {r0[j].y, r0[j].z, r0[j].w, r1[j].x, r1[j].y, r1[j].z, r1[j].w, 0u};
 #pragma unroll
-          for (int q = 0; q < 12; ++q) P[q] = Pg[q];
-          float px, py, pz;
-          compensate(P, x[j], y[j], z[j], px, py, pz);
-          sum[0] += (double)px;  // ascending point order
-          sum[1] += (double)py;
-          sum[2] += (double)pz;
-#pragma unroll
-          for (int f = 3; f < 8; ++f) sum[f] += (double)fx[j][f - 3];
-          pidx[m0 + j] = (int32_t)pi[j];
+          for (int f = 0; f < 7; ++f) sum[f] += (double)__uint_as_float(w[f]);  // ascending point order
+          pidx[m0 + j] = (int32_t)r0[j].x;
         }
+      if (C == 8)  // the eighth feature sits in a third 16-byte word
+#pragma unroll
+        for (int j = 0; j < kMeanBatch; ++j)
+          if (m0 + j < cnt) sum[7] += (double)__uint_as_float(c.rec[(int64_t)q[j] * RW + 8]);
     }
     if (row >= 0) {
       for (int m = (int)cnt; m < M; ++m) pidx[m] = -1;

@@ -58,7 +58,7 @@ def load() -> ctypes.CDLL:
         L.mmbev_status_string.argtypes = [ctypes.c_int32]
         L.mmbev_status_string.restype = ctypes.c_char_p
         L.mmbev_roi_voxelize_workspace_bytes.argtypes = [ctypes.POINTER(mmbev_grid_t), ctypes.c_int64,
-                                                         ctypes.c_int32]
+                                                         ctypes.c_int32, ctypes.c_int32]
         L.mmbev_roi_voxelize_workspace_bytes.restype = ctypes.c_size_t
         L.mmbev_workspace_init.argtypes = [p, ctypes.c_size_t, p]
         L.mmbev_workspace_init.restype = ctypes.c_int32
@@ -94,8 +94,9 @@ def grid_params(range_min, voxel_size, dims, max_points, max_voxels, num_sweeps,
     return g
 
 
-def roi_voxelize_workspace_bytes(grid: mmbev_grid_t, num_points: int, max_rois_per_frame: int) -> int:
-    return int(load().mmbev_roi_voxelize_workspace_bytes(ctypes.byref(grid), int(num_points),
+def roi_voxelize_workspace_bytes(grid: mmbev_grid_t, num_points: int, num_features: int,
+                                 max_rois_per_frame: int) -> int:
+    return int(load().mmbev_roi_voxelize_workspace_bytes(ctypes.byref(grid), int(num_points), int(num_features),
                                                          int(max_rois_per_frame)))
 
 
@@ -195,7 +196,7 @@ class Voxelizer:
         self.out_feats = torch.full((rows, C), -7.0, dtype=torch.float32, device=dev)
         self.out_point_idx = torch.full((rows, M), -7, dtype=torch.int32, device=dev)
         self.out_voxel_offsets = torch.zeros(B + 1, dtype=torch.int64, device=dev)
-        nbytes = roi_voxelize_workspace_bytes(grid, int(self.sweep_ids.numel()), self.max_rois)
+        nbytes = roi_voxelize_workspace_bytes(grid, int(self.sweep_ids.numel()), C, self.max_rois)
         if nbytes == 0:
             raise MmbevError("invalid sizes for mmbev_roi_voxelize_workspace_bytes")
         self.workspace = torch.empty(nbytes, dtype=torch.uint8, device=dev)

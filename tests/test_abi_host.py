@@ -58,7 +58,7 @@ def test_struct_layouts_match_header(mb):
     assert ctypes.sizeof(mb.mmbev_rois_t) == 24
     assert ctypes.sizeof(mb.mmbev_grid_t) == 52
     assert mb.ROI_DTYPE.itemsize == 32
-    assert mb.abi_version() == 1
+    assert mb.abi_version() == 2
 
 
 def test_make_rois_matches_oracle_bitwise(mb):
@@ -72,10 +72,10 @@ def test_make_rois_matches_oracle_bitwise(mb):
 
 def test_workspace_bytes_validation(mb):
     g = mb.grid_params((-54, -54, -5), (0.075, 0.075, 0.2), (1440, 1440, 40), 10, 120000, 10, 1)
-    n = mb.roi_voxelize_workspace_bytes(g, 347200, 32)
+    n = mb.roi_voxelize_workspace_bytes(g, 347200, 5, 32)
     assert n > 347200 * 24
     assert n % 256 == 0
-    assert mb.roi_voxelize_workspace_bytes(g, 347200 * 2, 32) > n
+    assert mb.roi_voxelize_workspace_bytes(g, 347200 * 2, 5, 32) > n
     bad = [dict(max_points=0), dict(max_points=65), dict(max_voxels=0), dict(num_sweeps=0), dict(num_sweeps=256),
            dict(num_frames=0), dict(dims=(0, 10, 10)), dict(voxel_size=(0.0, 1, 1)),
            dict(voxel_size=(float("nan"), 1, 1)), dict(dims=(70000, 70000, 2))]
@@ -83,10 +83,14 @@ def test_workspace_bytes_validation(mb):
                 max_voxels=120000, num_sweeps=10, num_frames=1)
     for b in bad:
         gg = mb.grid_params(**{**base, **b})
-        assert mb.roi_voxelize_workspace_bytes(gg, 1000, 32) == 0, b
-    assert mb.roi_voxelize_workspace_bytes(g, 1 << 30, 32) == 0
-    assert mb.roi_voxelize_workspace_bytes(g, 1000, 1025) == 0
-    assert mb.roi_voxelize_workspace_bytes(g, -1, 32) == 0
+        assert mb.roi_voxelize_workspace_bytes(gg, 1000, 5, 32) == 0, b
+    assert mb.roi_voxelize_workspace_bytes(g, 1 << 30, 5, 32) == 0
+    assert mb.roi_voxelize_workspace_bytes(g, 1000, 5, 1025) == 0
+    assert mb.roi_voxelize_workspace_bytes(g, -1, 5, 32) == 0
+    assert mb.roi_voxelize_workspace_bytes(g, 1000, 2, 32) == 0
+    assert mb.roi_voxelize_workspace_bytes(g, 1000, 9, 32) == 0
+    # one record column per feature
+    assert mb.roi_voxelize_workspace_bytes(g, 347200, 8, 32) > mb.roi_voxelize_workspace_bytes(g, 347200, 3, 32)
 
 
 def test_voxelize_rejects_bad_arguments_before_any_launch(mb):
@@ -95,7 +99,7 @@ def test_voxelize_rejects_bad_arguments_before_any_launch(mb):
     fake = 1 << 40  # never dereferenced: validation fails first
     pts = mb.mmbev_points_t(feat=fake, stride=100, num_features=4, reserved=0, num_points=100, frame_offsets=fake)
     rr = mb.mmbev_rois_t(boxes=fake, frame_offsets=fake, num_rois=2, max_rois_per_frame=2)
-    ws_need = mb.roi_voxelize_workspace_bytes(g, 100, 2)
+    ws_need = mb.roi_voxelize_workspace_bytes(g, 100, 4, 2)
 
     def call(points=pts, rois=rr, grid=g, sweep=fake, poses=fake, budget=fake, outs=(fake,) * 5, ws=fake,
              ws_bytes=ws_need):

@@ -17,7 +17,7 @@ constexpr int kWaves = kBlock / 64;
 // point filter
 constexpr int kWaveTile = 256;        // points per filter wave tile (64 lanes x 4)
 constexpr int kWaveQueue = 128;       // candidate ring of one filter wave (power of two, >= 128)
-constexpr int kFilterWaveTarget = 5120;  // filter wave chunks aimed for (about one per resident wave)
+constexpr int kFilterWaveTarget = 16384;  // filter wave chunks aimed for (a few per resident wave: balance)
 constexpr int kMaxLdsFrames = 64;     // frames of one filter workgroup staged in LDS
 constexpr int kMaxLdsRois = 256;      // ROI records of one filter workgroup staged in LDS
 constexpr int kMaxLdsBudgetWords = 256;

@@ -115,23 +115,38 @@ __device__ __forceinline__ bool roi_hit(const Config& c, const FilterLds& L, int
   return inside_roi(r, px, py);
 }
 
-// Voxel index of one axis, identical to quantize_axis (correctly rounded
-// (p - min) / v, then the range check and truncation): the product with the
-// reciprocal voxel size is within 3 ulps of the rounded quotient, so when no
-// integer lies within 16 ulps of it (or 2^-60 of zero) its floor is the
-// quotient's floor and decides both the range check and the index; otherwise
-// the division is done.  Non-finite products always take the division.
-__device__ __forceinline__ bool quantize_axis_fast(float p, float mn, float vs, float inv_vs, float Df, int32_t& i) {
-  const float t = p - mn;
-  const float q = t * inv_vs;
-  const float m = fma_rn(fabsf(q), 0x1p-20f, 0x1p-60f);
-  const float lo = floorf(q - m), hi = floorf(q + m);
-  if (lo == hi) {
-    const bool ok = lo >= 0.0f && lo < Df;
-    i = ok ? (int32_t)lo : 0;
-    return ok;
+// Voxel indices of p', identical to quantize_axis on each axis (correctly
+// rounded (p - min) / v, then the range check and truncation).  The product
+// with the reciprocal voxel size is within 3 ulps of the rounded quotient,
+// so when no integer lies within 16 ulps of it (or 2^-60 of zero) its floor
+// is the quotient's floor and decides both the range check and the index.
+// Only the axes where an integer is that close (and non-finite products)
+// take the division, behind a branch the whole wave skips when no lane
+// needs it.
+__device__ __forceinline__ bool quantize_fast(const Config& c, float px, float py, float pz, int32_t& ix,
+                                              int32_t& iy, int32_t& iz) {
+  const float p[3] = {px, py, pz};
+  float f[3];
+  bool amb[3];
+#pragma unroll
+  for (int d = 0; d < 3; ++d) {
+    const float q = (p[d] - c.mn[d]) * c.inv_vs[d];
+    const float m = fma_rn(fabsf(q), 0x1p-20f, 0x1p-60f);
+    const float lo = floorf(q - m);
+    amb[d] = !(lo == floorf(q + m));
+    f[d] = lo;
   }
-  return quantize_axis(p, mn, vs, Df, i);
+  if (__ballot(amb[0] || amb[1] || amb[2])) {
+#pragma unroll
+    for (int d = 0; d < 3; ++d)
+      if (amb[d]) f[d] = (p[d] - c.mn[d]) / c.vs[d];
+  }
+  const bool ok = f[0] >= 0.0f && f[0] < c.Df[0] && f[1] >= 0.0f && f[1] < c.Df[1] && f[2] >= 0.0f &&
+                  f[2] < c.Df[2];
+  ix = ok ? (int32_t)f[0] : 0;
+  iy = ok ? (int32_t)f[1] : 0;
+  iz = ok ? (int32_t)f[2] : 0;
+  return ok;
 }
 
 // Phase B: exact decision for a point with candidate ROIs, given p'.
@@ -139,10 +154,7 @@ template <bool ST>
 __device__ __forceinline__ bool exact_keep(const Config& c, const FilterLds& L, int32_t b, uint32_t s, float px,
                                            float py, float pz, uint32_t cand, uint32_t& key) {
   int32_t ix, iy, iz;
-  bool in = quantize_axis_fast(px, c.mn[0], c.vs[0], c.inv_vs[0], c.Df[0], ix);
-  in &= quantize_axis_fast(py, c.mn[1], c.vs[1], c.inv_vs[1], c.Df[1], iy);
-  in &= quantize_axis_fast(pz, c.mn[2], c.vs[2], c.inv_vs[2], c.Df[2], iz);
-  if (!in) return false;
+  if (!quantize_fast(c, px, py, pz, ix, iy, iz)) return false;
   const int32_t r0 = frame_roi_base<ST>(c, L, b);
   bool hit = false;
   if (c.W == 1) {
@@ -378,7 +390,7 @@ __device__ __forceinline__ void phase_b(const Config& c, const FilterLds& L, Wav
 
 // The points [lo, hi) of one wave (frame b), wave tile by wave tile: the
 // points before the first multiple of 4 and a partial last tile are loaded
-// point by point; the full tiles between them go through a two-deep
+// point by point; the full tiles between them go through a three-deep
 // register pipeline with 16-byte loads (when the rows allow them; otherwise
 // every tile is loaded point by point).
 template <bool VEC, bool ST>
@@ -395,19 +407,26 @@ __device__ __forceinline__ void run_wave(const Config& c, const FilterLds& L, Wa
   }
   const uint32_t full_end = VEC ? a0 + (hi - a0) / kWaveTile * kWaveTile : a0;
   const uint32_t last_full = full_end - kWaveTile;  // only used when full_end > a0
-  if (a0 < full_end) load_quad_vec(c, a0 + lane4, cur);
-  for (uint32_t t = a0; t < full_end; t += 2 * kWaveTile) {
-    // tile t (in cur) with tile t+T loading into nxt behind its cell-mask
-    // loads; then tile t+T with tile t+2T loading into cur.  Past the last
-    // full tile the load repeats that tile (cache hits, values unused), which
-    // keeps the number of loads in flight the same on every path.
+  // three register buffers: two tiles load while one is handled.  Past the
+  // last full tile a load repeats that tile (cache hits, values unused),
+  // which keeps the number of loads in flight the same on every path.
+  Quad q2;
+  if (a0 < full_end) {
+    load_quad_vec(c, a0 + lane4, cur);
+    load_quad_vec(c, min(a0 + kWaveTile, last_full) + lane4, nxt);
+  }
+  for (uint32_t t = a0; t < full_end; t += 3 * kWaveTile) {
     phase_a<ST>(c, L, b, t + lane4, cur, st);
-    load_quad_vec(c, min(t + kWaveTile, last_full) + lane4, nxt);
+    load_quad_vec(c, min(t + 2 * kWaveTile, last_full) + lane4, q2);
     phase_b<ST>(c, L, Q, t + lane4, st, wr);
     if (t + kWaveTile >= full_end) break;
     phase_a<ST>(c, L, b, t + kWaveTile + lane4, nxt, st);
-    load_quad_vec(c, min(t + 2 * kWaveTile, last_full) + lane4, cur);
+    load_quad_vec(c, min(t + 3 * kWaveTile, last_full) + lane4, cur);
     phase_b<ST>(c, L, Q, t + kWaveTile + lane4, st, wr);
+    if (t + 2 * kWaveTile >= full_end) break;
+    phase_a<ST>(c, L, b, t + 2 * kWaveTile + lane4, q2, st);
+    load_quad_vec(c, min(t + 4 * kWaveTile, last_full) + lane4, nxt);
+    phase_b<ST>(c, L, Q, t + 2 * kWaveTile + lane4, st, wr);
   }
   for (uint32_t t = full_end; t < hi; t += kWaveTile) {
     load_quad_scalar(c, t + lane4, hi, cur);

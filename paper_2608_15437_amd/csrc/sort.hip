@@ -69,14 +69,17 @@ __device__ __forceinline__ uint32_t scan_bins(const uint32_t* in, uint32_t* out,
   return total;
 }
 
-__global__ __launch_bounds__(kBlock) void segments_kernel(Config c) {
-  __shared__ uint32_t s_tmp[kWaves];
+constexpr int kSegBlock = 1024;  // threads of the segments kernel
+constexpr int kSegWaves = kSegBlock / 64;
+
+__global__ __launch_bounds__(kSegBlock) void segments_kernel(Config c) {
+  __shared__ uint32_t s_tmp[kSegWaves];
   WsHeader* h = c.hdr;
   const int tid = threadIdx.x;
   const uint32_t nf = h->fchunks;
   // kept-pair prefix of the filter chunks
   uint32_t carry = 0;
-  for (uint32_t base = 0; base < nf; base += kScanTile) {
+  for (uint32_t base = 0; base < nf; base += kSegBlock * kScanItems) {
     const uint32_t first = base + tid * kScanItems;
     uint32_t v[kScanItems], sum = 0;
 #pragma unroll
@@ -85,7 +88,7 @@ __global__ __launch_bounds__(kBlock) void segments_kernel(Config c) {
       sum += v[j];
     }
     uint32_t total;
-    uint32_t run = carry + block_exclusive_scan(sum, s_tmp, total);
+    uint32_t run = carry + block_exclusive_scan<kSegWaves>(sum, s_tmp, total);
 #pragma unroll
     for (int j = 0; j < kScanItems; ++j)
       if (first + j < nf) {
@@ -97,12 +100,12 @@ __global__ __launch_bounds__(kBlock) void segments_kernel(Config c) {
   if (tid == 0) c.fprefix[nf] = carry;
   __syncthreads();
   const uint32_t K = carry;
-  for (int b = tid; b <= c.B; b += kBlock) c.fstart[b] = c.fprefix[min(c.fchunk_first[b], nf)];
+  for (int b = tid; b <= c.B; b += kSegBlock) c.fstart[b] = c.fprefix[min(c.fchunk_first[b], nf)];
   __syncthreads();
   // pair chunks: about kSortGrid of them, whole kSortTile multiples
   uint32_t CH = (K + kSortGrid - 1) / kSortGrid;
   CH = max((uint32_t)kSortTile, (CH + kSortTile - 1) / kSortTile * kSortTile);
-  const int per = (c.B + kBlock - 1) / kBlock;
+  const int per = (c.B + kSegBlock - 1) / kSegBlock;
   const int b0 = tid * per;
   uint32_t mine = 0;
   for (int j = 0; j < per; ++j) {
@@ -110,7 +113,7 @@ __global__ __launch_bounds__(kBlock) void segments_kernel(Config c) {
     if (b < c.B) mine += (c.fstart[b + 1] - c.fstart[b] + CH - 1) / CH;
   }
   uint32_t total;
-  uint32_t run = block_exclusive_scan(mine, s_tmp, total);
+  uint32_t run = block_exclusive_scan<kSegWaves>(mine, s_tmp, total);
   const uint32_t cap = (uint32_t)c.schunk_max;  // never reached: K / CH <= kSortGrid
   for (int j = 0; j < per; ++j) {
     const int b = b0 + j;
@@ -189,18 +192,17 @@ __global__ __launch_bounds__(kBlock) void compact_kernel(Config c, uint32_t* kou
 }
 
 __global__ __launch_bounds__(kBlock) void count_kernel(Config c, int pass, const uint32_t* kin) {
-  __shared__ uint32_t s_hist[kSortBins];
-  const int tid = threadIdx.x;
+  __shared__ uint32_t s_hist[kWaves][kSortBins];  // one histogram per wave, summed at the end
+  const int tid = threadIdx.x, wave = tid >> 6;
   const uint32_t k = blockIdx.x;
   if (k >= c.hdr->schunks) return;
   const int shift = pass * c.dbits;
   const uint32_t nbins = 1u << c.dbits;
   const uint32_t mask = nbins - 1u;
-  for (uint32_t e = tid; e < nbins; e += kBlock) s_hist[e] = 0;
+  for (uint32_t e = tid; e < kWaves * kSortBins; e += kBlock) (&s_hist[0][0])[e] = 0;
   __syncthreads();
   const uint4 ch = c.schunk[k];
   const uint32_t lo = ch.x, hi = ch.y;
-  const uint64_t lt = lanemask_lt();
   for (uint32_t base = lo; base < hi; base += kBlock * kCountItems) {
     uint32_t key[kCountItems];
 #pragma unroll
@@ -209,15 +211,16 @@ __global__ __launch_bounds__(kBlock) void count_kernel(Config c, int pass, const
       key[j] = i < hi ? kin[i] : 0u;
     }
 #pragma unroll
-    for (int j = 0; j < kCountItems; ++j) {
-      const bool valid = base + j * kBlock + tid < hi;
-      const uint32_t d = (key[j] >> shift) & mask;
-      const uint64_t m = match_digit(d, valid, c.dbits);
-      if (valid && (m & lt) == 0) atomicAdd(&s_hist[d], (uint32_t)__popcll(m));
-    }
+    for (int j = 0; j < kCountItems; ++j)
+      if (base + j * kBlock + tid < hi) atomicAdd(&s_hist[wave][(key[j] >> shift) & mask], 1u);
   }
   __syncthreads();
-  for (uint32_t e = tid; e < nbins; e += kBlock) c.cnt[(int64_t)k * kSortBins + e] = s_hist[e];
+  for (uint32_t e = tid; e < nbins; e += kBlock) {
+    uint32_t t = 0;
+#pragma unroll
+    for (int w = 0; w < kWaves; ++w) t += s_hist[w][e];
+    c.cnt[(int64_t)k * kSortBins + e] = t;
+  }
 }
 
 // Frame b: every digit's column over the frame's chunks -> exclusive
@@ -369,7 +372,7 @@ __global__ __launch_bounds__(kBlock) void scatter_kernel(Config c, int pass, con
 }  // namespace
 
 hipError_t launch_segments(const Config& c, hipStream_t st) {
-  hipLaunchKernelGGL(segments_kernel, dim3(1), dim3(kBlock), 0, st, c);
+  hipLaunchKernelGGL(segments_kernel, dim3(1), dim3(kSegBlock), 0, st, c);
   return hipGetLastError();
 }
 

@@ -7,6 +7,18 @@ resident in HBM.  Prints ONE JSON line.
 
     python bench.py [--gpus 1] [--steps K] [--warmup W] [--frames F] [--no-cpu-baseline]
 
+Traffic of the filter kernel (the `traffic` field of the roofline object):
+
+    rocprofv3 --pmc FETCH_SIZE -f csv -d DIR_F -o run -- python3 bench.py --probe-traffic
+    rocprofv3 --pmc WRITE_SIZE -f csv -d DIR_W -o run -- python3 bench.py --probe-traffic
+    python bench.py --write-traffic DIR_F DIR_W
+
+--probe-traffic runs the batched call a few times and a plain device copy of
+COPY_BYTES bytes; --write-traffic scales each counter by the known bytes the
+copy moved over what the counter read for it, and stores the filter kernel's
+HBM bytes per launch, tagged with the hash of the filter's sources (a changed
+kernel makes the stored figure stale, and bench.py then reports null).
+
 value = input points per second over the timed steps (Mpoints/s).  The
 roofline object reports the dominant kernel (the fused point filter): its
 algorithmic bytes per launch over its mean launch duration, taken live from
@@ -30,6 +42,7 @@ HBM_PEAK_GBS = 8000.0
 METRIC = "Mpoints/s ROI-voxelized (10-sweep, 347k pts) + achieved HBM GB/s vs peak"
 FILTER_SOURCES = ["paper_2608_15437_amd/csrc/filter.hip", "paper_2608_15437_amd/csrc/common.hpp"]
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "filter_kernel_c2x128_traffic.json")
+COPY_BYTES = 1 << 30
 
 
 def log(msg: str) -> None:
@@ -89,6 +102,73 @@ def time_launches(vz, steps: int) -> dict:
     return out
 
 
+def probe_traffic(frames: int) -> int:
+    """The launches whose counters --write-traffic reads: batched calls, then one plain copy."""
+    import torch
+
+    import synth
+    from paper_2608_15437_amd import mmbev
+
+    wl = synth.throughput(frames)
+    vz = mmbev.voxelizer_for_workload(wl, torch.device("cuda:0"))
+    for _ in range(3):
+        vz.run()
+    torch.cuda.synchronize()
+    src = torch.ones(COPY_BYTES // 4, dtype=torch.float32, device="cuda:0")
+    dst = torch.empty_like(src)
+    dst.copy_(src)
+    torch.cuda.synchronize()
+    log(f"[probe] 3 calls on {frames} frames, one copy of {COPY_BYTES} bytes")
+    return 0
+
+
+def counter_values(run_dir: str, counter: str) -> dict:
+    """Per-dispatch values (KiB) of one counter, per kernel name, from a rocprofv3 csv run."""
+    import csv
+    import glob
+
+    per = {}
+    for f in glob.glob(os.path.join(run_dir, "**", "*counter_collection.csv"), recursive=True):
+        for r in csv.DictReader(open(f)):
+            if r["Counter_Name"] == counter:
+                key = (r["Kernel_Name"], r["Dispatch_Id"])
+                per[key] = per.get(key, 0.0) + float(r["Counter_Value"])
+    vals = {}
+    for (name, _), v in per.items():
+        vals.setdefault(name, []).append(v)
+    return vals
+
+
+def write_traffic(fetch_dir: str, write_dir: str, frames: int) -> int:
+    fe, wr = counter_values(fetch_dir, "FETCH_SIZE"), counter_values(write_dir, "WRITE_SIZE")
+
+    def pick(d, needle):
+        names = [k for k in d if needle in k]
+        if not names:
+            raise SystemExit(f"no kernel matching {needle!r} in the counter files")
+        return d[names[0]]
+
+    # the copy of COPY_BYTES is the largest copy dispatch (the others upload inputs)
+    copy_f, copy_w = max(pick(fe, "copyBuffer")), max(pick(wr, "copyBuffer"))
+    filt_f = statistics.mean(pick(fe, "filter_kernel"))
+    filt_w = statistics.mean(pick(wr, "filter_kernel"))
+    fetch_scale = COPY_BYTES / (copy_f * 1024.0)
+    write_scale = COPY_BYTES / (copy_w * 1024.0)
+    fetch_bytes = filt_f * 1024.0 * fetch_scale
+    write_bytes = filt_w * 1024.0 * write_scale
+    out = {"kernel": "filter_kernel", "frames": frames, "source_sha": source_sha(FILTER_SOURCES),
+           "fetch_kib_per_launch": filt_f, "write_kib_per_launch": filt_w,
+           "copy_bytes": COPY_BYTES, "copy_fetch_kib": copy_f, "copy_write_kib": copy_w,
+           "fetch_scale": fetch_scale, "write_scale": write_scale,
+           "bytes_per_launch": int(fetch_bytes + write_bytes),
+           "fetch_bytes_per_launch": int(fetch_bytes), "write_bytes_per_launch": int(write_bytes)}
+    os.makedirs(os.path.dirname(TRAFFIC_FILE), exist_ok=True)
+    with open(TRAFFIC_FILE, "w") as f:
+        json.dump(out, f, indent=1)
+    print(json.dumps(out))
+    return 0
+
+
 def main() -> int:
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -96,11 +176,17 @@ def main() -> int:
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--frames", type=int, default=128)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--probe-traffic", action="store_true")
+    ap.add_argument("--write-traffic", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"))
     args = ap.parse_args()
+    if args.write_traffic:
+        return write_traffic(args.write_traffic[0], args.write_traffic[1], args.frames)
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}); frames are independent, so "
               "a multi-GPU run would shard the batch by frame with no exchange", file=sys.stderr)
         return 2
+    if args.probe_traffic:
+        return probe_traffic(args.frames)
 
     import numpy as np
     import torch

@@ -181,13 +181,15 @@ mmbev_status_t mmbev_roi_voxelize(const mmbev_points_t* points, const uint8_t* s
 
 /*
  * Same call as mmbev_roi_voxelize, for measurement: before each of its
- * kernel launches, and once after the last, it records the next of the
+ * launch groups, and once after the last, it records the next of the
  * caller's events (hipEvent_t, created with timing enabled) on `stream`, as
- * long as events remain.  The launch order is: 0 ROI staging, 1 point filter,
- * then one radix pass per key digit, head scan, per-frame finalisation,
- * per-frame voxel cap, mean pooling.  Returns the number of events recorded through
- * *events_recorded (host int32, may be NULL).  Elapsed time between events k
- * and k+1 is the duration of launch k.
+ * long as events remain.  The groups, in order: ROI staging, point filter,
+ * chunk layout (segments), compaction and records, then one radix pass per
+ * key digit of at most 9 bits (count, per-frame scan and scatter launches),
+ * voxel heads (two launches), finalisation, per-frame voxel cap, mean
+ * pooling.  Returns the number of events recorded through *events_recorded
+ * (host int32, may be NULL).  Elapsed time between events k and k+1 is the
+ * duration of group k.
  */
 mmbev_status_t mmbev_roi_voxelize_profiled(const mmbev_points_t* points, const uint8_t* sweep_ids,
                                            const float* sweep_poses, const mmbev_rois_t* rois,

@@ -252,7 +252,7 @@ __global__ __launch_bounds__(kBlock) void mean_kernel(Config c, const uint32_t* 
       if (rank != 0xffffffffu) {
         row = c.out_voxel_offsets[b] + (int64_t)rank;
         if (row < 0 || row >= rows || slot >= K) {
-          raise_fault(h, MMBEV_FAULT_WAIT);
+          raise_fault(h, MMBEV_FAULT_INTERNAL);
           row = -1;
         } else {
           s0 = min(c.seg_start[slot], K - 1u);

@@ -16,7 +16,7 @@ _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libmmbev.so")
 
 OK, ERR_INVALID_ARG, ERR_WORKSPACE, ERR_UNSUPPORTED, ERR_HIP = 0, -1, -2, -3, -4
-FAULT_POINT_OFFSETS, FAULT_ROI_OFFSETS, FAULT_WAIT = 1, 2, 4
+FAULT_POINT_OFFSETS, FAULT_ROI_OFFSETS, FAULT_INTERNAL = 1, 2, 4
 
 ROI_DTYPE = np.dtype([("cx", "<f4"), ("cy", "<f4"), ("cos_yaw", "<f4"), ("sin_yaw", "<f4"),
                       ("ext_x", "<f4"), ("ext_y", "<f4"), ("reserved0", "<f4"), ("reserved1", "<f4")])

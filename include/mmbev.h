@@ -69,7 +69,7 @@ typedef int32_t mmbev_status_t;
 #define MMBEV_FAULT_POINT_OFFSETS 1 /* point frame offsets not 0 .. num_points, non-decreasing */
 #define MMBEV_FAULT_ROI_OFFSETS 2   /* ROI frame offsets not 0 .. num_rois, non-decreasing,
                                        or a frame with more than max_rois_per_frame ROIs */
-#define MMBEV_FAULT_INTERNAL 4      /* an internal count disagreed (a voxel row out of range) */
+#define MMBEV_FAULT_INTERNAL 4      /* an internal consistency check failed (never with valid inputs) */
 
 /* ------------------------------------------------------------- inputs */
 

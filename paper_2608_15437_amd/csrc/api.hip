@@ -25,7 +25,7 @@ struct Plan {
   int32_t cell_shift, ncx, ncy, ncells;
   int32_t kb, passes, dbits;
   int64_t fchunk_points, fchunk_max, filter_grid, schunk_max, mean_grid;
-  size_t off_hdr, off_cellmask, off_cellany, off_budgetmask, off_fchunk_first, off_fcount, off_fchunk_lo, off_fchunk_frame, off_fprefix,
+  size_t off_hdr, off_cellmask, off_cellany, off_budgetmask, off_fchunk_first, off_fbits, off_fcount, off_fchunk_lo, off_fchunk_frame, off_fprefix,
       off_fstart, off_schunk_first, off_schunk, off_cnt, off_ftot, off_hcount, off_vcount, off_keys[2], off_vals[2], off_rec, off_seg,
       off_capkey, off_rank, off_voxoff, total;
 };
@@ -58,7 +58,8 @@ mmbev_status_t make_plan(const mmbev_grid_t* g, int64_t N, int32_t max_rois, int
   p->max_rois = max_rois;
   p->W = std::max(1, (max_rois + 31) / 32);
   int cs = 0;
-  while ((((int64_t)g->dims[0] + (1 << cs) - 1) >> cs) > 128 || (((int64_t)g->dims[1] + (1 << cs) - 1) >> cs) > 128)
+  while ((((int64_t)g->dims[0] + (1 << cs) - 1) >> cs) > kMaxCellSide ||
+         (((int64_t)g->dims[1] + (1 << cs) - 1) >> cs) > kMaxCellSide)
     ++cs;
   p->cell_shift = cs;
   p->ncx = (int32_t)(((int64_t)g->dims[0] + (1 << cs) - 1) >> cs);
@@ -69,13 +70,15 @@ mmbev_status_t make_plan(const mmbev_grid_t* g, int64_t N, int32_t max_rois, int
   p->dbits = (p->kb + p->passes - 1) / p->passes;
 
   const int64_t n1 = std::max<int64_t>(N, 1);
-  // filter chunks: about kFilterWaveTarget of them over the whole input (one
-  // per resident wave), a multiple of the wave tile; frames add at most one
-  // partial chunk each
+  // filter chunks: about kFilterWaveTarget of them over the whole input (a
+  // few per resident wave), a multiple of the wave tile and at most
+  // kMaxChunkPoints points (a wave keeps its chunk's bitmap in LDS); frames
+  // add at most one partial chunk each
   {
     const int64_t target = kFilterWaveTarget > 2 * (int64_t)p->B ? kFilterWaveTarget - p->B : kFilterWaveTarget;
     int64_t P = (N + target - 1) / target;
     P = std::max<int64_t>(kWaveTile, (P + kWaveTile - 1) / kWaveTile * kWaveTile);
+    P = std::min<int64_t>(P, kMaxChunkPoints);
     p->fchunk_points = P;
     p->fchunk_max = (N + P - 1) / P + p->B;
     p->filter_grid = std::max<int64_t>(1, (p->fchunk_max + kWaves - 1) / kWaves);
@@ -93,6 +96,7 @@ mmbev_status_t make_plan(const mmbev_grid_t* g, int64_t N, int32_t max_rois, int
   p->off_cellany = p->W > 1 ? take((size_t)p->B * p->ncells * 4) : p->off_cellmask;
   p->off_budgetmask = take((size_t)p->B * p->S * p->W * 4);
   p->off_fchunk_first = take((size_t)(p->B + 1) * 4);
+  p->off_fbits = take((size_t)p->fchunk_max * (p->fchunk_points / 32) * 4);
   p->off_fcount = take((size_t)p->fchunk_max * 4);
   p->off_fchunk_lo = take((size_t)p->fchunk_max * 4);
   p->off_fchunk_frame = take((size_t)p->fchunk_max * 4);
@@ -258,6 +262,7 @@ mmbev_status_t voxelize(const mmbev_points_t* points, const uint8_t* sweep_ids, 
   c.cellany = (uint32_t*)(ws + p.off_cellany);
   c.budgetmask = (uint32_t*)(ws + p.off_budgetmask);
   c.fchunk_first = (uint32_t*)(ws + p.off_fchunk_first);
+  c.fbits = (uint32_t*)(ws + p.off_fbits);
   c.fcount = (uint32_t*)(ws + p.off_fcount);
   c.fchunk_lo = (uint32_t*)(ws + p.off_fchunk_lo);
   c.fchunk_frame = (uint32_t*)(ws + p.off_fchunk_frame);
@@ -280,6 +285,7 @@ mmbev_status_t voxelize(const mmbev_points_t* points, const uint8_t* sweep_ids, 
   c.out_rank = (uint32_t*)(ws + p.off_rank);
   c.vox_off = (uint32_t*)(ws + p.off_voxoff);
   c.fchunk_points = (int32_t)p.fchunk_points;
+  c.fchunk_words = (int32_t)(p.fchunk_points / 32);
   c.fchunk_max = (int32_t)p.fchunk_max;
   c.filter_grid = (int32_t)p.filter_grid;
   c.schunk_max = (int32_t)p.schunk_max;

@@ -17,11 +17,16 @@ constexpr int kWaves = kBlock / 64;
 // point filter
 constexpr int kWaveTile = 256;        // points per filter wave tile (64 lanes x 4)
 constexpr int kWaveQueue = 128;       // candidate ring of one filter wave (power of two, >= 128)
+constexpr int kFilterDepth = 4;       // register buffers of a filter wave's tile pipeline (>= 2)
 constexpr int kFilterWaveTarget = 16384;  // filter wave chunks aimed for (a few per resident wave: balance)
+constexpr int kMaxChunkPoints = 4096;  // points of one filter chunk at most
+constexpr int kChunkWords = kMaxChunkPoints / 32;  // words of a chunk's kept bitmap
 constexpr int kMaxLdsFrames = 64;     // frames of one filter workgroup staged in LDS
 constexpr int kMaxLdsRois = 256;      // ROI records of one filter workgroup staged in LDS
 constexpr int kMaxLdsBudgetWords = 256;
 constexpr int kMaxPoseLds = 64;       // (frame, sweep) poses of one filter workgroup staged in LDS
+constexpr int kMaxCellSide = 64;      // coarse BEV cells per grid side (at most 64 x 64 per frame)
+constexpr int kMaxLdsCells = 4096;    // cell words of one filter workgroup staged in LDS (16 KB)
 // radix passes (segmented by frame) and the voxel head scan
 constexpr int kMaxDigitBits = 9;
 constexpr int kSortBins = 1 << kMaxDigitBits;  // 512
@@ -82,8 +87,9 @@ struct Config {
   uint32_t* cellany;       // [B][ncells], OR of a cell's W words (== cellmask when W == 1)
   uint32_t* budgetmask;    // [B][S][W]
   uint32_t* fchunk_first;  // [B+1] first filter chunk of frame b
-  uint32_t* fcount;        // [fchunk_max] kept pairs of filter chunk k
-  uint32_t* fchunk_lo;     // [fchunk_max] first point of filter chunk k (its kept pairs start there)
+  uint32_t* fbits;         // [fchunk_max][fchunk_words] bit j of chunk k: point fchunk_lo[k] + j is kept
+  uint32_t* fcount;        // [fchunk_max] kept points of filter chunk k
+  uint32_t* fchunk_lo;     // [fchunk_max] first point of filter chunk k
   uint32_t* fchunk_frame;  // [fchunk_max] frame of filter chunk k
   uint32_t* fprefix;       // [fchunk_max + 1] kept pairs of the filter chunks before k
   uint32_t* fstart;        // [B+1] first sorted pair of frame b (kept pairs of the frames before it)
@@ -93,7 +99,7 @@ struct Config {
   uint32_t* ftot;          // [B][kSortBins] digit totals of every frame
   uint32_t* hcount;        // [schunk_max] voxel heads of pair chunk k
   uint32_t* vcount;        // [B] voxels of frame b
-  uint32_t* keys[2];       // [N] each: [0] first holds the filter's per-chunk regions
+  uint32_t* keys[2];       // [N] each: ping-pong buffers of the radix passes
   uint32_t* vals[2];       // the pair's record: its place in compact (point) order
   // records of the kept points in compact order, written by the compaction:
   // rec_words words each (a multiple of 4), word 0 the point index, then
@@ -106,7 +112,8 @@ struct Config {
   uint32_t* out_rank;      // [N] row inside its frame, or ~0u (frames over the cap)
   uint32_t* vox_off;       // [B+1] voxels of the frames before b
   // sizes
-  int32_t fchunk_points;   // points per filter chunk (a multiple of kWaveTile)
+  int32_t fchunk_points;   // points per filter chunk (a multiple of kWaveTile, <= kMaxChunkPoints)
+  int32_t fchunk_words;    // fchunk_points / 32
   int32_t fchunk_max;      // bound on filter chunks: ceil(N / fchunk_points) + B
   int32_t filter_grid;     // ceil(fchunk_max / kWaves) workgroups, one chunk per wave
   int32_t schunk_max;      // bound on pair chunks: kSortGrid + B

@@ -10,7 +10,8 @@
 //   A. for every point of a lane: p' (exact), an approximate cell index
 //      (multiplication by the reciprocal voxel size; the cell rectangles of
 //      the ROIs are padded by cell_pad voxels, more than the approximation
-//      can be off), and all cell-mask loads issued back to back;
+//      can be off) and the cell's candidate-ROI word, read from the LDS copy
+//      of the frame's cell map;
 //   B. only for points whose cell has a candidate ROI that admits their
 //      sweep (a few percent): appended with their p' to the wave's queue in
 //      LDS and, 64 at a time with every lane busy, decided exactly: exact
@@ -22,20 +23,21 @@
 // Wave k of the grid owns filter chunk k: a contiguous run of at most
 // fchunk_points points inside one frame (the chunk table is laid out by the
 // staging kernel).  The waves of a workgroup share the LDS copy of their
-// frames' poses, budget masks, ROI records and ROI offsets (staged once,
-// behind the only workgroup barriers) and are otherwise independent: a wave
-// appends its kept pairs, in point order, to its own output region, which
-// starts at the chunk's first point index.  Nothing waits on another
-// wave: a chained scan across workgroups costs one memory round trip per
-// predecessor when many publish together, and workgroup barriers leave the
-// waves without candidates idle.  Each frame's sort gathers its chunks'
+// frames' poses, budget masks, ROI records, ROI offsets and cell maps
+// (staged once, behind the only workgroup barriers) and are otherwise
+// independent: a wave appends its kept pairs, in point order, to its own
+// output region, which starts at the chunk's first point index.  Nothing
+// waits on another wave: a chained scan across workgroups costs one memory
+// round trip per predecessor when many publish together, and workgroup
+// barriers leave the waves without candidates idle.  Each frame's sort gathers its chunks'
 // regions using the per-chunk counts left here.
 //
 // Per wave tile (256 points, four consecutive points per lane, one 16-byte
-// load per column and lane) the order is: phase A (its cell-mask loads
-// issued last), the next wave tile's loads, phase B.  Loads complete in
-// order, so waiting for the cell masks leaves the next tile's loads in flight
-// during phase B, which reads nothing from global memory on the common path.
+// load per column and lane) the only global loads are the tile's own: vector
+// memory loads complete in order, so a wait for a dependent global load (a
+// cell word, say) would also wait for every tile loaded before it.  Phases A
+// and B read only LDS and registers on the common path, and the loads of the
+// two tiles after the current one stay in flight while it is handled.
 #include "launch.hpp"
 
 namespace mmbev {
@@ -45,6 +47,7 @@ namespace {
 // Tables of the workgroup's frames f0..f1, staged once and shared by its waves.
 struct alignas(16) FilterLds {
   float pose[kMaxPoseLds][12];  // 48-byte rows: three aligned 16-byte reads each
+  uint32_t cell[kMaxLdsCells];  // candidate-ROI word of every coarse cell, frame after frame
   float roi[6][kMaxLdsRois];    // cx, cy, cos, sin, ext_x, ext_y
   uint32_t bm[kMaxLdsBudgetWords];
   int32_t roff[kMaxLdsFrames + 1];  // ROI offsets clamped to [0, R]
@@ -52,14 +55,15 @@ struct alignas(16) FilterLds {
   int32_t chunk_staged;
 };
 
-// Per-wave state in LDS: the candidate queue (a ring).
+// Per-wave state in LDS: the candidate queue (a ring) and the kept bitmap
+// of the wave's chunk.
 struct WaveLds {
-  uint32_t idx[kWaveQueue];
-  uint32_t cand[kWaveQueue];  // candidate-ROI word (W == 1) or 1
-  uint32_t fs[kWaveQueue];    // frame << 8 | sweep
+  uint32_t pk[kWaveQueue];    // point offset in the chunk | sweep << 16
+  uint32_t cand[kWaveQueue];  // candidate-ROI word (W == 1) or the cell's any-word
   float px[kWaveQueue];       // p' (Eq. 6), exact
   float py[kWaveQueue];
   float pz[kWaveQueue];
+  uint32_t bits[kChunkWords];  // bit j: point lo + j of the chunk is kept
 };
 
 // Orders the LDS accesses of one wave (its lanes' writes before the other
@@ -122,7 +126,7 @@ __device__ __forceinline__ bool roi_hit(const Config& c, const FilterLds& L, int
 // is the quotient's floor and decides both the range check and the index.
 // Only the axes where an integer is that close (and non-finite products)
 // take the division, behind a branch the whole wave skips when no lane
-// needs it.
+// needs it (inside it, a select: no per-lane branch).
 __device__ __forceinline__ bool quantize_fast(const Config& c, float px, float py, float pz, int32_t& ix,
                                               int32_t& iy, int32_t& iz) {
   const float p[3] = {px, py, pz};
@@ -138,8 +142,10 @@ __device__ __forceinline__ bool quantize_fast(const Config& c, float px, float p
   }
   if (__ballot(amb[0] || amb[1] || amb[2])) {
 #pragma unroll
-    for (int d = 0; d < 3; ++d)
-      if (amb[d]) f[d] = (p[d] - c.mn[d]) / c.vs[d];
+    for (int d = 0; d < 3; ++d) {
+      const float exact = (p[d] - c.mn[d]) / c.vs[d];
+      f[d] = amb[d] ? exact : f[d];
+    }
   }
   const bool ok = f[0] >= 0.0f && f[0] < c.Df[0] && f[1] >= 0.0f && f[1] < c.Df[1] && f[2] >= 0.0f &&
                   f[2] < c.Df[2];
@@ -149,36 +155,41 @@ __device__ __forceinline__ bool quantize_fast(const Config& c, float px, float p
   return ok;
 }
 
-// Phase B: exact decision for a point with candidate ROIs, given p'.
+// Phase B, at most 32 ROIs per frame: whether a point with candidate-ROI
+// word cand (0 for a lane without a point) lies in one of them, each lane
+// walking its own bits and stopping at its first hit.  (A loop shared by the
+// wave, one broadcast read per distinct ROI, measured slower: most lanes hit
+// their first ROI.)
 template <bool ST>
-__device__ __forceinline__ bool exact_keep(const Config& c, const FilterLds& L, int32_t b, uint32_t s, float px,
-                                           float py, float pz, uint32_t cand, uint32_t& key) {
-  int32_t ix, iy, iz;
-  if (!quantize_fast(c, px, py, pz, ix, iy, iz)) return false;
-  const int32_t r0 = frame_roi_base<ST>(c, L, b);
+__device__ __forceinline__ bool roi_test_one_word(const Config& c, const FilterLds& L, int32_t r0, uint32_t cand,
+                                                  float px, float py) {
   bool hit = false;
-  if (c.W == 1) {
-    uint32_t m = cand;
+  uint32_t m = cand;
+  while (m && !hit) {
+    const int k = __builtin_ctz(m);
+    m &= m - 1;
+    hit = roi_hit<ST>(c, L, r0 + k, px, py);
+  }
+  return hit;
+}
+
+// Phase B, more than 32 ROIs per frame: the ROIs of the point's cell that
+// admit its sweep, word by word, tested lane by lane.
+template <bool ST>
+__device__ __forceinline__ bool roi_test_words(const Config& c, const FilterLds& L, int32_t b, uint32_t s,
+                                               int32_t r0, int32_t ix, int32_t iy, float px, float py) {
+  const int32_t cell = (iy >> c.cell_shift) * c.ncx + (ix >> c.cell_shift);
+  const uint32_t* cm = c.cellmask + ((int64_t)b * c.ncells + cell) * c.W;
+  bool hit = false;
+  for (int w = 0; w < c.W && !hit; ++w) {
+    uint32_t m = cm[w] & budget_word<ST>(c, L, b, s, w);
     while (m && !hit) {
       const int k = __builtin_ctz(m);
       m &= m - 1;
-      hit = roi_hit<ST>(c, L, r0 + k, px, py);
-    }
-  } else {
-    const int32_t cell = (iy >> c.cell_shift) * c.ncx + (ix >> c.cell_shift);
-    const uint32_t* cm = c.cellmask + ((int64_t)b * c.ncells + cell) * c.W;
-    for (int w = 0; w < c.W && !hit; ++w) {
-      uint32_t m = cm[w] & budget_word<ST>(c, L, b, s, w);
-      while (m && !hit) {
-        const int k = __builtin_ctz(m);
-        m &= m - 1;
-        hit = roi_hit<ST>(c, L, r0 + w * 32 + k, px, py);
-      }
+      hit = roi_hit<ST>(c, L, r0 + w * 32 + k, px, py);
     }
   }
-  if (!hit) return false;
-  key = ((uint32_t)iz * c.Dy + (uint32_t)iy) * c.Dx + (uint32_t)ix;
-  return true;
+  return hit;
 }
 
 // Four consecutive points of one lane held in registers.
@@ -222,7 +233,7 @@ __device__ __forceinline__ void plan_staging(const Config& c, FilterLds& L, int3
   L.roi_lo = min(max(c.roi_off[f0], 0), c.R);
   L.roi_n = min(max(c.roi_off[f1 + 1], L.roi_lo), c.R) - L.roi_lo;
   L.chunk_staged = nf <= kMaxLdsFrames && nf * c.S <= kMaxPoseLds && nf * c.S * c.W <= kMaxLdsBudgetWords &&
-                   L.roi_n <= kMaxLdsRois;
+                   L.roi_n <= kMaxLdsRois && nf * c.ncells <= kMaxLdsCells;
 }
 
 __device__ __forceinline__ void do_staging(const Config& c, FilterLds& L) {
@@ -231,6 +242,19 @@ __device__ __forceinline__ void do_staging(const Config& c, FilterLds& L) {
   for (int e = tid; e <= nf; e += kBlock) L.roff[e] = min(max(c.roi_off[L.f0 + e], 0), c.R);
   for (int e = tid; e < nf * c.S * 12; e += kBlock) (&L.pose[0][0])[e] = c.poses[(int64_t)L.f0 * c.S * 12 + e];
   for (int e = tid; e < nf * c.S * c.W; e += kBlock) L.bm[e] = c.budgetmask[(int64_t)L.f0 * c.S * c.W + e];
+  {
+    // the frames' cell words, four loads in flight per thread
+    const uint32_t* src = c.cellany + (int64_t)L.f0 * c.ncells;
+    const int n = nf * c.ncells;
+    for (int e0 = tid; e0 < n; e0 += 4 * kBlock) {
+      uint32_t v[4];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) v[j] = e0 + j * kBlock < n ? src[e0 + j * kBlock] : 0u;
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+        if (e0 + j * kBlock < n) L.cell[e0 + j * kBlock] = v[j];
+    }
+  }
   for (int e = tid; e < L.roi_n; e += kBlock) {
     const mmbev_roi_t r = c.rois[L.roi_lo + e];
     L.roi[0][e] = r.cx;
@@ -242,30 +266,31 @@ __device__ __forceinline__ void do_staging(const Config& c, FilterLds& L) {
   }
 }
 
-// Approximate grid cell of (x', y') for the candidate lookup, or -1 when the
-// point is clearly outside the grid.  fx = x' * (1/v) - min/v is within a
+// Approximate coarse cell of (x', y') inside its frame for the candidate
+// lookup, or -1 when the point is clearly outside the grid.  fx = x' * (1/v) - min/v is within a
 // small fraction of a voxel of the exact (x' - min) / v; the cell rectangles
 // of the ROIs are padded by cell_pad voxels, so a point the exact test keeps
 // always finds its ROI here.
-__device__ __forceinline__ int32_t approx_cell(const Config& c, int32_t b, float px, float py) {
+__device__ __forceinline__ int32_t approx_cell(const Config& c, float px, float py) {
   const int32_t ix = (int32_t)fma_rn(px, c.inv_vs[0], c.nmin_v[0]);
   const int32_t iy = (int32_t)fma_rn(py, c.inv_vs[1], c.nmin_v[1]);
   const bool ok = (uint32_t)(ix + c.cell_pad) < (uint32_t)c.Dx + 2u * (uint32_t)c.cell_pad &&
                   (uint32_t)(iy + c.cell_pad) < (uint32_t)c.Dy + 2u * (uint32_t)c.cell_pad;
   const int32_t ax = min(max(ix, 0), (int32_t)c.Dx - 1) >> c.cell_shift;
   const int32_t ay = min(max(iy, 0), (int32_t)c.Dy - 1) >> c.cell_shift;
-  return ok ? b * c.ncells + ay * c.ncx + ax : -1;
+  return ok ? ay * c.ncx + ax : -1;
 }
 
 // Per-lane state of four points between their two phases.
 struct QuadState {
   float px[4], py[4], pz[4];  // p' (Eq. 6), exact
-  uint32_t fs[4];             // frame << 8 | sweep
+  uint32_t sw[4];             // sweep
   uint32_t cand[4];           // candidate-ROI word after phase A (0: none)
 };
 
 // Phase A of four points of a lane (first index i0, frame b for the whole
-// wave): p' and the issue of their cell-mask loads, left in flight.
+// wave): p' and the candidate-ROI word of each point's cell (from LDS when
+// staged, so that the only global loads in flight are the point tiles).
 template <bool ST>
 __device__ __forceinline__ void phase_a(const Config& c, const FilterLds& L, int32_t b, uint32_t i0, const Quad& d,
                                         QuadState& st) {
@@ -275,7 +300,7 @@ __device__ __forceinline__ void phase_a(const Config& c, const FilterLds& L, int
 #pragma unroll
   for (int q = 0; q < 4; ++q) {
     sq[q] = (d.s >> (8 * q)) & 0xffu;
-    st.fs[q] = ((uint32_t)b << 8) | sq[q];
+    st.sw[q] = sq[q];
   }
   const bool lane_uniform = ST && sq[0] < S && sq[1] == sq[0] && sq[2] == sq[0] && sq[3] == sq[0];
   const uint32_t s0 = __builtin_amdgcn_readfirstlane(sq[0]);
@@ -290,7 +315,7 @@ __device__ __forceinline__ void phase_a(const Config& c, const FilterLds& L, int
       st.px[q] = fma_rn(r0.x, d.x[q], fma_rn(r0.y, d.y[q], fma_rn(r0.z, d.z[q], r0.w)));
       st.py[q] = fma_rn(r1.x, d.x[q], fma_rn(r1.y, d.y[q], fma_rn(r1.z, d.z[q], r1.w)));
       st.pz[q] = fma_rn(r2.x, d.x[q], fma_rn(r2.y, d.y[q], fma_rn(r2.z, d.z[q], r2.w)));
-      cidx[q] = approx_cell(c, b, st.px[q], st.py[q]);
+      cidx[q] = approx_cell(c, st.px[q], st.py[q]);
     }
   } else {
 #pragma unroll
@@ -301,48 +326,56 @@ __device__ __forceinline__ void phase_a(const Config& c, const FilterLds& L, int
         float P[12];
         load_pose<ST>(c, L, b, sq[q], P);
         compensate(P, d.x[q], d.y[q], d.z[q], st.px[q], st.py[q], st.pz[q]);
-        cidx[q] = approx_cell(c, b, st.px[q], st.py[q]);
+        cidx[q] = approx_cell(c, st.px[q], st.py[q]);
       }
     }
   }
-  // the four cell-mask loads in flight together (always in bounds)
+  // the four cell words (always in bounds)
 #pragma unroll
   for (int q = 0; q < 4; ++q) {
-    const uint32_t w = c.cellany[max(cidx[q], 0)];
+    const int32_t cell = max(cidx[q], 0);
+    const uint32_t w = ST ? L.cell[(b - L.f0) * c.ncells + cell] : c.cellany[(int64_t)b * c.ncells + cell];
     st.cand[q] = cidx[q] >= 0 ? w : 0u;
   }
 }
 
-// Queue and kept-pair state of one wave (wave-uniform values).
+// Queue and kept-point state of one wave (wave-uniform values).
 struct WaveRun {
-  uint32_t head;      // ring index of the oldest queued candidate
-  uint32_t queued;    // candidates in the ring (< 64 between tiles)
-  uint32_t kept;      // pairs written so far to the wave's region
-  uint32_t out_base;  // first slot of the wave's region
+  uint32_t head;    // ring index of the oldest queued candidate
+  uint32_t queued;  // candidates in the ring (< 64 between tiles)
+  uint32_t kept;    // points kept so far
+  uint32_t lo;      // first point of the wave's chunk
+  int32_t b;        // frame of the wave's chunk
+  uint32_t k;       // the chunk
 };
 
-// Decide the n (<= 64) oldest queued candidates and append the kept ones, in
-// queue order, to the wave's region.
+// Decide the n (<= 64) oldest queued candidates and set the bits of the kept
+// ones in the wave's bitmap.  Nothing is written to global memory here: a
+// store inside the tile loop would make the compiler wait for it (and, since
+// vector memory operations complete in order, for every tile load before it)
+// once its source registers are reused.
 template <bool ST>
 __device__ __forceinline__ void decide_round(const Config& c, const FilterLds& L, WaveLds& Q, WaveRun& wr,
                                              uint32_t n) {
-  const int lane = threadIdx.x & 63;
-  bool keep = false;
-  uint32_t key = 0, i = 0;
-  if ((uint32_t)lane < n) {
-    const uint32_t e = (wr.head + lane) & (kWaveQueue - 1);
-    i = Q.idx[e];
-    const uint32_t fs = Q.fs[e];
-    keep = exact_keep<ST>(c, L, (int32_t)(fs >> 8), fs & 0xffu, Q.px[e], Q.py[e], Q.pz[e], Q.cand[e], key);
+  const uint32_t lane = (uint32_t)(threadIdx.x & 63);
+  // every lane reads a slot of the ring; lanes past n hold no candidate
+  const uint32_t e = (wr.head + lane) & (kWaveQueue - 1);
+  const bool live = lane < n;
+  const uint32_t pk = Q.pk[e];
+  const float px = live ? Q.px[e] : 0.0f, py = live ? Q.py[e] : 0.0f, pz = live ? Q.pz[e] : 0.0f;
+  int32_t ix, iy, iz;
+  const bool in_grid = quantize_fast(c, px, py, pz, ix, iy, iz);
+  const uint32_t cand = live && in_grid ? Q.cand[e] : 0u;
+  const int32_t r0 = frame_roi_base<ST>(c, L, wr.b);
+  bool keep;
+  if (c.W == 1) {
+    keep = roi_test_one_word<ST>(c, L, r0, cand, px, py);
+  } else {
+    keep = false;
+    if (cand != 0u) keep = roi_test_words<ST>(c, L, wr.b, pk >> 16, r0, ix, iy, px, py);
   }
-  const uint64_t kbits = __ballot(keep);
-  if (keep) {
-    const uint32_t pos = wr.out_base + wr.kept + (uint32_t)__popcll(kbits & lanemask_lt());
-    c.keys[0][pos] = key;
-    c.vals[0][pos] = i;
-  }
-  wr.kept += (uint32_t)__popcll(kbits);
-  wr.head = (wr.head + n) & (kWaveQueue - 1);
+  if (keep) atomicOr(&Q.bits[(pk & 0xffffu) >> 5], 1u << (pk & 31u));
+  wr.kept += (uint32_t)__popcll(__ballot(keep));  wr.head = (wr.head + n) & (kWaveQueue - 1);
   wr.queued -= n;
   wave_lds_sync();  // slots read before they are written again
 }
@@ -356,7 +389,7 @@ __device__ __forceinline__ void phase_b(const Config& c, const FilterLds& L, Wav
   if (c.W == 1) {
 #pragma unroll
     for (int q = 0; q < 4; ++q)
-      if (st.cand[q]) st.cand[q] &= budget_word<ST>(c, L, (int32_t)(st.fs[q] >> 8), st.fs[q] & 0xffu, 0);
+      if (st.cand[q]) st.cand[q] &= budget_word<ST>(c, L, wr.b, st.sw[q], 0);
   }
   const uint64_t lt = lanemask_lt();
   const uint32_t n = (st.cand[0] != 0) + (st.cand[1] != 0) + (st.cand[2] != 0) + (st.cand[3] != 0);
@@ -372,9 +405,8 @@ __device__ __forceinline__ void phase_b(const Config& c, const FilterLds& L, Wav
       if (st.cand[q]) {
         if (rank - done < take) {
           const uint32_t e = (wr.head + wr.queued + (rank - done)) & (kWaveQueue - 1);
-          Q.idx[e] = i0 + q;
+          Q.pk[e] = (i0 + q - wr.lo) | (st.sw[q] << 16);
           Q.cand[e] = st.cand[q];
-          Q.fs[e] = st.fs[q];
           Q.px[e] = st.px[q];
           Q.py[e] = st.py[q];
           Q.pz[e] = st.pz[q];
@@ -388,62 +420,86 @@ __device__ __forceinline__ void phase_b(const Config& c, const FilterLds& L, Wav
   }
 }
 
+// Step k of the register pipeline over the ntiles full tiles from a0: the
+// loads of tile k (the last tile again past the end: cache hits, values
+// unused) go into buffer k mod kFilterDepth, then tile k - (kFilterDepth - 1),
+// loaded that many steps earlier, is handled if it exists.  Every step
+// issues the same loads in the same order, and the loop over the steps has a
+// fixed trip count and no early exit, so the compiler's wait before a tile's
+// data counts exactly the loads of the tiles after it.
+template <bool ST, int J>
+__device__ __forceinline__ void pipeline_step(const Config& c, const FilterLds& L, WaveLds& Q, int32_t b,
+                                              uint32_t a0, uint32_t ntiles, uint32_t k0, uint32_t lane4,
+                                              Quad (&buf)[kFilterDepth], QuadState& st, WaveRun& wr) {
+  const uint32_t k = k0 + (uint32_t)J;
+  load_quad_vec(c, a0 + min(k, ntiles - 1u) * kWaveTile + lane4, buf[J]);
+  const uint32_t tile = k - (uint32_t)(kFilterDepth - 1);  // wraps for the first steps
+  if (tile < ntiles) {
+    const uint32_t t = a0 + tile * kWaveTile;
+    phase_a<ST>(c, L, b, t + lane4, buf[(J + 1) % kFilterDepth], st);
+    phase_b<ST>(c, L, Q, t + lane4, st, wr);
+  }
+}
+
 // The points [lo, hi) of one wave (frame b), wave tile by wave tile: the
 // points before the first multiple of 4 and a partial last tile are loaded
-// point by point; the full tiles between them go through a three-deep
-// register pipeline with 16-byte loads (when the rows allow them; otherwise
-// every tile is loaded point by point).
+// point by point; the full tiles between them go through a register
+// pipeline of kFilterDepth buffers with 16-byte loads (when the rows allow
+// them; otherwise every tile is loaded point by point): the loads of the
+// next kFilterDepth - 1 tiles are in flight while a tile is handled.
 template <bool VEC, bool ST>
 __device__ __forceinline__ void run_wave(const Config& c, const FilterLds& L, WaveLds& Q, int32_t b, uint32_t lo,
                                          uint32_t hi, WaveRun& wr) {
-  const uint32_t lane4 = 4u * (uint32_t)(threadIdx.x & 63);
-  Quad cur, nxt;
+  const uint32_t lane = (uint32_t)(threadIdx.x & 63), lane4 = 4u * lane;
+  Quad buf[kFilterDepth];
   QuadState st;
+  static_assert(kChunkWords == 128, "two bitmap words per lane");
+  Q.bits[lane] = 0;
+  Q.bits[lane + 64] = 0;
+  wave_lds_sync();
   const uint32_t a0 = VEC ? min((lo + 3u) & ~3u, hi) : lo;
   if (a0 > lo) {  // head: fewer than 4 points
-    load_quad_scalar(c, lo + lane4, a0, cur);
-    phase_a<ST>(c, L, b, lo + lane4, cur, st);
+    load_quad_scalar(c, lo + lane4, a0, buf[0]);
+    phase_a<ST>(c, L, b, lo + lane4, buf[0], st);
     phase_b<ST>(c, L, Q, lo + lane4, st, wr);
   }
-  const uint32_t full_end = VEC ? a0 + (hi - a0) / kWaveTile * kWaveTile : a0;
-  const uint32_t last_full = full_end - kWaveTile;  // only used when full_end > a0
-  // three register buffers: two tiles load while one is handled.  Past the
-  // last full tile a load repeats that tile (cache hits, values unused),
-  // which keeps the number of loads in flight the same on every path.
-  Quad q2;
-  if (a0 < full_end) {
-    load_quad_vec(c, a0 + lane4, cur);
-    load_quad_vec(c, min(a0 + kWaveTile, last_full) + lane4, nxt);
+  const uint32_t ntiles = VEC ? (hi - a0) / kWaveTile : 0u;
+  static_assert(kFilterDepth >= 2 && kFilterDepth <= 6, "pipeline steps written out below");
+  if (ntiles > 0) {
+    const uint32_t steps = ntiles + (uint32_t)(kFilterDepth - 1);
+    for (uint32_t k0 = 0; k0 < steps; k0 += kFilterDepth) {
+      pipeline_step<ST, 0>(c, L, Q, b, a0, ntiles, k0, lane4, buf, st, wr);
+      pipeline_step<ST, 1>(c, L, Q, b, a0, ntiles, k0, lane4, buf, st, wr);
+      if constexpr (kFilterDepth > 2) pipeline_step<ST, 2 % kFilterDepth>(c, L, Q, b, a0, ntiles, k0, lane4, buf, st, wr);
+      if constexpr (kFilterDepth > 3) pipeline_step<ST, 3 % kFilterDepth>(c, L, Q, b, a0, ntiles, k0, lane4, buf, st, wr);
+      if constexpr (kFilterDepth > 4) pipeline_step<ST, 4 % kFilterDepth>(c, L, Q, b, a0, ntiles, k0, lane4, buf, st, wr);
+      if constexpr (kFilterDepth > 5) pipeline_step<ST, 5 % kFilterDepth>(c, L, Q, b, a0, ntiles, k0, lane4, buf, st, wr);
+    }
   }
-  for (uint32_t t = a0; t < full_end; t += 3 * kWaveTile) {
-    phase_a<ST>(c, L, b, t + lane4, cur, st);
-    load_quad_vec(c, min(t + 2 * kWaveTile, last_full) + lane4, q2);
-    phase_b<ST>(c, L, Q, t + lane4, st, wr);
-    if (t + kWaveTile >= full_end) break;
-    phase_a<ST>(c, L, b, t + kWaveTile + lane4, nxt, st);
-    load_quad_vec(c, min(t + 3 * kWaveTile, last_full) + lane4, cur);
-    phase_b<ST>(c, L, Q, t + kWaveTile + lane4, st, wr);
-    if (t + 2 * kWaveTile >= full_end) break;
-    phase_a<ST>(c, L, b, t + 2 * kWaveTile + lane4, q2, st);
-    load_quad_vec(c, min(t + 4 * kWaveTile, last_full) + lane4, nxt);
-    phase_b<ST>(c, L, Q, t + 2 * kWaveTile + lane4, st, wr);
-  }
-  for (uint32_t t = full_end; t < hi; t += kWaveTile) {
-    load_quad_scalar(c, t + lane4, hi, cur);
-    phase_a<ST>(c, L, b, t + lane4, cur, st);
+  for (uint32_t t = a0 + ntiles * kWaveTile; t < hi; t += kWaveTile) {
+    load_quad_scalar(c, t + lane4, hi, buf[0]);
+    phase_a<ST>(c, L, b, t + lane4, buf[0], st);
     phase_b<ST>(c, L, Q, t + lane4, st, wr);
   }
   while (wr.queued > 0) decide_round<ST>(c, L, Q, wr, min(wr.queued, 64u));
+  wave_lds_sync();
+  // the chunk's bitmap, every word (bits past hi are zero)
+  uint32_t* out = c.fbits + (int64_t)wr.k * c.fchunk_words;
+  if (lane < (uint32_t)c.fchunk_words) out[lane] = Q.bits[lane];
+  if (lane + 64 < (uint32_t)c.fchunk_words) out[lane + 64] = Q.bits[lane + 64];
 }
 
 // Workgroup w: its waves over filter chunks kWaves*w .. kWaves*w + 3.  Per
-// chunk it leaves the number of kept pairs and where they start.
+// chunk it leaves the bitmap of its kept points, their number, its first
+// point and its frame.
 template <bool VEC>
 __global__ __launch_bounds__(kBlock) void filter_kernel(Config c) {
   __shared__ FilterLds L;
   __shared__ WaveLds Qs[kWaves];
   const int tid = threadIdx.x;
-  const int lane = tid & 63, wave = tid >> 6;
+  // the wave index is the same in all its lanes: uniform, so that the rest
+  // of the kernel is uniform control flow for the compiler too
+  const int lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   WaveLds& Q = Qs[wave];
   const uint32_t nchunks = c.hdr->fchunks;
   const uint32_t k0 = (uint32_t)blockIdx.x * kWaves;
@@ -465,7 +521,10 @@ __global__ __launch_bounds__(kBlock) void filter_kernel(Config c) {
   const int32_t b = __builtin_amdgcn_readfirstlane(frame_of_chunk(c.fchunk_first, c.B, k));
   uint32_t lo, hi;
   filter_chunk_points(c, b, k, lo, hi);
-  WaveRun wr{0u, 0u, 0u, lo};
+  // the same in every lane; uniform bounds keep the tile loop a scalar loop
+  lo = __builtin_amdgcn_readfirstlane(lo);
+  hi = __builtin_amdgcn_readfirstlane(hi);
+  WaveRun wr{0u, 0u, 0u, lo, b, k};
   if (staged)
     run_wave<VEC, true>(c, L, Q, b, lo, hi, wr);
   else

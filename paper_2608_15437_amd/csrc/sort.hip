@@ -136,32 +136,45 @@ __global__ __launch_bounds__(kSegBlock) void segments_kernel(Config c) {
   }
 }
 
-// One workgroup per filter chunk: its kept pairs to [fprefix[k],
-// fprefix[k+1]), and the kept points' records at the same places.  The
-// points of a chunk are visited in increasing index order, so their reads
-// stay close together (kept points come in runs); the frame's poses are
-// staged in LDS and each record is written with 16-byte stores.  The pair's
-// value becomes its compact place (the record's index).
+// One workgroup per filter chunk: its kept points, listed from the chunk's
+// bitmap in increasing index order, get the compact places [fprefix[k],
+// fprefix[k+1]).  For each: its record there (point index, p' of Eq. 6 from
+// the frame's poses staged in LDS, raw features; 16-byte stores) and the
+// (voxel key, compact place) pair the radix passes start from.  The key is
+// the definition's: correctly rounded (p' - min) / v per axis, truncated.
+// The reads of a chunk's kept points stay close together (kept points come
+// in runs).
 constexpr int kCompactItems = 4;
 
 __global__ __launch_bounds__(kBlock) void compact_kernel(Config c, uint32_t* kout, uint32_t* vout) {
+  static_assert(kChunkWords <= kBlock, "one bitmap word per thread");
   extern __shared__ float s_pose[];  // [S][12]
+  __shared__ uint16_t s_list[kMaxChunkPoints];  // kept point offsets in the chunk, ascending
+  __shared__ uint32_t s_tmp[kWaves];
   const int tid = threadIdx.x;
   const uint32_t k = blockIdx.x;
   if (k >= c.hdr->fchunks) return;
-  const uint32_t lo = c.fchunk_lo[k], n = c.fcount[k], dst = c.fprefix[k];
+  const uint32_t lo = c.fchunk_lo[k], dst = c.fprefix[k];
   const int32_t b = (int32_t)c.fchunk_frame[k];
   const int C = c.C, RW = c.rec_words;
   for (int e = tid; e < c.S * 12; e += kBlock) s_pose[e] = c.poses[(int64_t)b * c.S * 12 + e];
+  // the bitmap: one word per thread, its set bits listed at the word's rank
+  uint32_t word = tid < c.fchunk_words ? c.fbits[(int64_t)k * c.fchunk_words + tid] : 0u;
+  uint32_t total;
+  uint32_t r = block_exclusive_scan((uint32_t)__popc(word), s_tmp, total);
+  while (word) {
+    s_list[r++] = (uint16_t)(32 * tid + __builtin_ctz(word));
+    word &= word - 1u;
+  }
   __syncthreads();
+  const uint32_t n = min(total, c.fcount[k]);  // equal unless the workspace was corrupted
   for (uint32_t base = 0; base < n; base += kBlock * kCompactItems) {
-    uint32_t kk[kCompactItems], pi[kCompactItems], sw[kCompactItems];
+    uint32_t pi[kCompactItems], sw[kCompactItems];
     float v[kCompactItems][8];
 #pragma unroll
     for (int u = 0; u < kCompactItems; ++u) {
       const uint32_t t = base + u * kBlock + tid;
-      kk[u] = t < n ? c.keys[0][lo + t] : 0u;
-      pi[u] = t < n ? min(c.vals[0][lo + t], (uint32_t)c.N - 1u) : 0u;
+      pi[u] = t < n ? min(lo + (uint32_t)s_list[t], (uint32_t)c.N - 1u) : 0u;
     }
 #pragma unroll
     for (int u = 0; u < kCompactItems; ++u) {  // all point loads of the batch in flight together
@@ -178,14 +191,19 @@ __global__ __launch_bounds__(kBlock) void compact_kernel(Config c, uint32_t* kou
         const uint32_t q = dst + t;
         float px, py, pz;
         compensate(s_pose + sw[u] * 12, v[u][0], v[u][1], v[u][2], px, py, pz);
-        kout[q] = kk[u];
+        int32_t ix, iy, iz;
+        const bool in = quantize_axis(px, c.mn[0], c.vs[0], c.Df[0], ix) &&
+                        quantize_axis(py, c.mn[1], c.vs[1], c.Df[1], iy) &&
+                        quantize_axis(pz, c.mn[2], c.vs[2], c.Df[2], iz);
+        if (!in) raise_fault(c.hdr, MMBEV_FAULT_INTERNAL);  // the filter kept it: never
+        kout[q] = in ? ((uint32_t)iz * c.Dy + (uint32_t)iy) * c.Dx + (uint32_t)ix : 0u;
         vout[q] = q;
-        uint4* r = reinterpret_cast<uint4*>(c.rec + (int64_t)q * RW);
-        r[0] = make_uint4(pi[u], __float_as_uint(px), __float_as_uint(py), __float_as_uint(pz));
+        uint4* rr = reinterpret_cast<uint4*>(c.rec + (int64_t)q * RW);
+        rr[0] = make_uint4(pi[u], __float_as_uint(px), __float_as_uint(py), __float_as_uint(pz));
         if (RW > 4)
-          r[1] = make_uint4(__float_as_uint(v[u][3]), __float_as_uint(v[u][4]), __float_as_uint(v[u][5]),
-                            __float_as_uint(v[u][6]));
-        if (RW > 8) r[2] = make_uint4(__float_as_uint(v[u][7]), 0u, 0u, 0u);
+          rr[1] = make_uint4(__float_as_uint(v[u][3]), __float_as_uint(v[u][4]), __float_as_uint(v[u][5]),
+                             __float_as_uint(v[u][6]));
+        if (RW > 8) rr[2] = make_uint4(__float_as_uint(v[u][7]), 0u, 0u, 0u);
       }
     }
   }

@@ -25,7 +25,7 @@ struct Plan {
   int32_t cell_shift, ncx, ncy, ncells;
   int32_t kb, passes, dbits;
   int64_t fchunk_points, fchunk_max, filter_grid, schunk_max, mean_grid;
-  size_t off_hdr, off_cellmask, off_cellany, off_budgetmask, off_fchunk_first, off_fbits, off_fcount, off_fchunk_lo, off_fchunk_frame, off_fprefix,
+  size_t off_hdr, off_cellmask, off_cellany, off_budgetmask, off_fchunk_first, off_tileframe, off_fbits, off_fcount, off_fchunk_lo, off_fchunk_frame, off_fprefix,
       off_fstart, off_schunk_first, off_schunk, off_cnt, off_ftot, off_hcount, off_vcount, off_keys[2], off_vals[2], off_rec, off_seg,
       off_capkey, off_rank, off_voxoff, total;
 };
@@ -117,6 +117,7 @@ mmbev_status_t make_plan(const mmbev_grid_t* g, int64_t N, int32_t max_rois, int
   p->off_capkey = take((size_t)n1 * 4);
   p->off_rank = take((size_t)n1 * 4);
   p->off_voxoff = take((size_t)(p->B + 1) * 4);
+  p->off_tileframe = take((size_t)((n1 + kMeanTile - 1) / kMeanTile + 1) * 4);
   p->total = o;
   return MMBEV_OK;
 }
@@ -284,6 +285,7 @@ mmbev_status_t voxelize(const mmbev_points_t* points, const uint8_t* sweep_ids, 
   c.capkey = (uint32_t*)(ws + p.off_capkey);
   c.out_rank = (uint32_t*)(ws + p.off_rank);
   c.vox_off = (uint32_t*)(ws + p.off_voxoff);
+  c.tile_frame = (uint32_t*)(ws + p.off_tileframe);
   c.fchunk_points = (int32_t)p.fchunk_points;
   c.fchunk_words = (int32_t)(p.fchunk_points / 32);
   c.fchunk_max = (int32_t)p.fchunk_max;

@@ -111,6 +111,7 @@ struct Config {
   uint32_t* capkey;        // [N] first point index of the voxel (frames over the cap)
   uint32_t* out_rank;      // [N] row inside its frame, or ~0u (frames over the cap)
   uint32_t* vox_off;       // [B+1] voxels of the frames before b
+  uint32_t* tile_frame;    // [ceil(N / kMeanTile) + 1] frame of voxel t * kMeanTile; last: B - 1
   // sizes
   int32_t fchunk_points;   // points per filter chunk (a multiple of kWaveTile, <= kMaxChunkPoints)
   int32_t fchunk_words;    // fchunk_points / 32

@@ -13,9 +13,10 @@
 //             before it (global voxel numbering), and the output offsets of
 //             every frame (at most max_voxels rows each) with the
 //             capped-voxel count;
-// cap      -- one workgroup per frame over max_voxels: radix select of the
-//             voxels with the smallest first point index, then their rank
-//             in key order (the output row inside the frame);
+// cap      -- one workgroup per frame: the frame of each tile of the mean
+//             that starts in it; for frames over max_voxels, radix select
+//             of the voxels with the smallest first point index, then their
+//             rank in key order (the output row inside the frame);
 // mean     -- one thread per voxel: output row, and the mean of the voxel's
 //             first max_points points from their compact records (x', y',
 //             z' of Eq. 6 and the raw features), summed in double in
@@ -27,9 +28,9 @@ namespace mmbev {
 
 namespace {
 
-// Frame b of global voxel g: largest b, vox_off[b] <= g.
-__device__ __forceinline__ int32_t frame_of_voxel(const Config& c, uint32_t g) {
-  int32_t lo = 0, hi = c.B - 1;
+// Frame b of global voxel g: largest b in [lo, hi] with vox_off[b] <= g
+// (the caller knows g's frame lies in that range).
+__device__ __forceinline__ int32_t frame_of_voxel(const Config& c, uint32_t g, int32_t lo, int32_t hi) {
   while (lo < hi) {
     int32_t mid = (lo + hi + 1) >> 1;
     if (c.vox_off[mid] <= g)
@@ -146,6 +147,7 @@ __global__ __launch_bounds__(kBlock) void finalize_kernel(Config c) {
     c.vox_off[c.B] = V;
     h->voxels = V;
   }
+  if (tid == 0) c.tile_frame[(V + kMeanTile - 1) / kMeanTile] = (uint32_t)(c.B - 1);
   uint32_t carry_out = 0, carry_cap = 0;
   for (int chunk = 0; chunk < c.B; chunk += kBlock) {
     const int b = chunk + tid;
@@ -166,8 +168,8 @@ __global__ __launch_bounds__(kBlock) void finalize_kernel(Config c) {
   }
 }
 
-// One workgroup per frame; frames within the cap return at once.  Selects
-// the max_voxels voxels with the smallest first point index (radix select of
+// One workgroup per frame: the frame's entries of the mean's tile table;
+// then frames within the cap return.  Selects the max_voxels voxels with the smallest first point index (radix select of
 // the max_voxels-th smallest first index, four 8-bit rounds; first indices
 // are distinct), then numbers the kept voxels in key order.
 __global__ __launch_bounds__(kBlock) void cap_kernel(Config c, const uint32_t* vals) {
@@ -176,6 +178,14 @@ __global__ __launch_bounds__(kBlock) void cap_kernel(Config c, const uint32_t* v
   __shared__ uint32_t s_sel, s_k;
   const int tid = threadIdx.x;
   const int b = blockIdx.x;
+  {
+    // frame b for the tiles of kMeanTile voxels whose first voxel is in it
+    // (the mean's workgroups search only between the frames of their tile
+    // and of the next one)
+    const uint32_t v0 = c.vox_off[b], v1 = c.vox_off[b + 1];
+    for (uint32_t t = (v0 + kMeanTile - 1) / kMeanTile + tid; (uint64_t)t * kMeanTile < v1; t += kBlock)
+      c.tile_frame[t] = (uint32_t)b;
+  }
   const uint32_t nv = c.vcount[b];
   if (nv <= (uint32_t)c.cap) return;
   const uint32_t fs = c.fstart[b];
@@ -240,11 +250,15 @@ __global__ __launch_bounds__(kBlock) void mean_kernel(Config c, const uint32_t* 
   for (uint32_t g0 = blockIdx.x * kMeanTile; g0 < V; g0 += gridDim.x * kMeanTile) {
     const uint32_t g = g0 + tid;
     const uint32_t nblk = min((uint32_t)kMeanTile, V - g0);
+    // the tile's voxels lie in frames tile_frame[t] .. tile_frame[t + 1]
+    const uint32_t tl = g0 / kMeanTile;
+    const int32_t fa = min((int32_t)c.tile_frame[tl], c.B - 1);
+    const int32_t fb = min(max((int32_t)c.tile_frame[tl + 1], fa), c.B - 1);
     int64_t row = -1;
     int32_t b = 0;
     uint32_t s0 = 0, cnt = 0;
     if (g < V) {
-      b = frame_of_voxel(c, g);
+      b = frame_of_voxel(c, g, fa, fb);
       const uint32_t v = g - c.vox_off[b];
       const uint32_t nv = c.vox_off[b + 1] - c.vox_off[b];
       const uint32_t slot = c.fstart[b] + v;

@@ -232,7 +232,7 @@ __global__ __launch_bounds__(kBlock) void cap_kernel(Config c, const uint32_t* v
 // all their loads in flight together.  When the block's rows are consecutive (no frame
 // over the cap in it) the rows are assembled in LDS and written as
 // contiguous runs; otherwise each thread writes its own row.
-constexpr int kMeanBatch = 8;
+constexpr int kMeanBatch = 4;  // more records in flight per thread cost occupancy (VGPRs)
 
 __global__ __launch_bounds__(kBlock) void mean_kernel(Config c, const uint32_t* keys, const uint32_t* vals) {
   extern __shared__ uint32_t sm[];

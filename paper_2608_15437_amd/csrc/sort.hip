@@ -71,37 +71,70 @@ __device__ __forceinline__ uint32_t scan_bins(const uint32_t* in, uint32_t* out,
 
 constexpr int kSegBlock = 1024;  // threads of the segments kernel
 constexpr int kSegWaves = kSegBlock / 64;
+constexpr int kSegLdsFrames = 4096;  // frame starts kept in LDS up to this many frames
 
 __global__ __launch_bounds__(kSegBlock) void segments_kernel(Config c) {
   __shared__ uint32_t s_tmp[kSegWaves];
+  __shared__ uint32_t s_fstart[kSegLdsFrames + 1];  // frame starts, when B <= kSegLdsFrames
+  __shared__ int32_t s_last;
   WsHeader* h = c.hdr;
   const int tid = threadIdx.x;
   const uint32_t nf = h->fchunks;
-  // kept-pair prefix of the filter chunks
+  const bool lds = c.B <= kSegLdsFrames;
+  uint32_t* fstart = lds ? s_fstart : c.fstart;
+  if (tid == 0) s_last = -1;
+  // kept-point prefix of the filter chunks; the first chunk of a frame also
+  // gives the start of that frame and of the empty frames just before it.
+  // Thread t holds kScanItems consecutive chunks, read with 16-byte loads.
+  static_assert(kScanItems % 4 == 0, "16-byte loads");
   uint32_t carry = 0;
   for (uint32_t base = 0; base < nf; base += kSegBlock * kScanItems) {
     const uint32_t first = base + tid * kScanItems;
     uint32_t v[kScanItems], sum = 0;
+    int32_t fr[kScanItems];
+    const int32_t before = first > 0 && first <= nf ? (int32_t)c.fchunk_frame[first - 1] : -1;
 #pragma unroll
-    for (int j = 0; j < kScanItems; ++j) {
-      v[j] = first + j < nf ? c.fcount[first + j] : 0u;
-      sum += v[j];
+    for (int j = 0; j < kScanItems; j += 4) {
+      uint4 a = make_uint4(0u, 0u, 0u, 0u), f = make_uint4(~0u, ~0u, ~0u, ~0u);
+      if (first + j + 3 < nf) {
+        a = *reinterpret_cast<const uint4*>(c.fcount + first + j);
+        f = *reinterpret_cast<const uint4*>(c.fchunk_frame + first + j);
+      } else if (first + j < nf) {
+        a.x = c.fcount[first + j];
+        f.x = c.fchunk_frame[first + j];
+        if (first + j + 1 < nf) { a.y = c.fcount[first + j + 1]; f.y = c.fchunk_frame[first + j + 1]; }
+        if (first + j + 2 < nf) { a.z = c.fcount[first + j + 2]; f.z = c.fchunk_frame[first + j + 2]; }
+      }
+      v[j] = a.x; v[j + 1] = a.y; v[j + 2] = a.z; v[j + 3] = a.w;
+      fr[j] = (int32_t)min(f.x, (uint32_t)c.B - 1u);
+      fr[j + 1] = (int32_t)min(f.y, (uint32_t)c.B - 1u);
+      fr[j + 2] = (int32_t)min(f.z, (uint32_t)c.B - 1u);
+      fr[j + 3] = (int32_t)min(f.w, (uint32_t)c.B - 1u);
     }
+#pragma unroll
+    for (int j = 0; j < kScanItems; ++j) sum += v[j];
     uint32_t total;
     uint32_t run = carry + block_exclusive_scan<kSegWaves>(sum, s_tmp, total);
+    int32_t prev = before;
 #pragma unroll
     for (int j = 0; j < kScanItems; ++j)
       if (first + j < nf) {
         c.fprefix[first + j] = run;
+        for (int32_t g = prev + 1; g <= fr[j]; ++g) fstart[g] = run;
+        prev = max(prev, fr[j]);
         run += v[j];
+        if (first + j + 1 == nf) s_last = prev;
       }
     carry += total;
+    __syncthreads();
   }
-  if (tid == 0) c.fprefix[nf] = carry;
-  __syncthreads();
   const uint32_t K = carry;
-  for (int b = tid; b <= c.B; b += kSegBlock) c.fstart[b] = c.fprefix[min(c.fchunk_first[b], nf)];
+  if (tid == 0) c.fprefix[nf] = K;
   __syncthreads();
+  for (int32_t g = s_last + 1 + tid; g <= c.B; g += kSegBlock) fstart[g] = K;  // frames after the last chunk
+  __syncthreads();
+  if (lds)
+    for (int g = tid; g <= c.B; g += kSegBlock) c.fstart[g] = s_fstart[g];
   // pair chunks: about kSortGrid of them, whole kSortTile multiples
   uint32_t CH = (K + kSortGrid - 1) / kSortGrid;
   CH = max((uint32_t)kSortTile, (CH + kSortTile - 1) / kSortTile * kSortTile);
@@ -110,7 +143,7 @@ __global__ __launch_bounds__(kSegBlock) void segments_kernel(Config c) {
   uint32_t mine = 0;
   for (int j = 0; j < per; ++j) {
     const int b = b0 + j;
-    if (b < c.B) mine += (c.fstart[b + 1] - c.fstart[b] + CH - 1) / CH;
+    if (b < c.B) mine += (fstart[b + 1] - fstart[b] + CH - 1) / CH;
   }
   uint32_t total;
   uint32_t run = block_exclusive_scan<kSegWaves>(mine, s_tmp, total);
@@ -118,7 +151,7 @@ __global__ __launch_bounds__(kSegBlock) void segments_kernel(Config c) {
   for (int j = 0; j < per; ++j) {
     const int b = b0 + j;
     if (b < c.B) {
-      const uint32_t f0 = c.fstart[b], f1 = c.fstart[b + 1];
+      const uint32_t f0 = fstart[b], f1 = fstart[b + 1];
       const uint32_t n = (f1 - f0 + CH - 1) / CH;
       c.schunk_first[b] = min(run, cap);
       for (uint32_t k = run; k < min(run + n, cap); ++k) {

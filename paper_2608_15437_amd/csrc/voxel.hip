@@ -71,7 +71,10 @@ __global__ __launch_bounds__(kBlock) void ucount_kernel(Config c, const uint32_t
 
 __global__ __launch_bounds__(kBlock) void uwrite_kernel(Config c, const uint32_t* keys) {
   __shared__ uint32_t s_tmp[kWaves];
+  __shared__ uint32_t s_off[kCountItems][kWaves];  // heads before row j of wave w in the batch
+  __shared__ uint32_t s_batch;
   const int tid = threadIdx.x;
+  const int lane = tid & 63, wave = tid >> 6;
   const uint32_t k = blockIdx.x;
   if (k >= c.hdr->schunks) return;
   const uint4 ch = c.schunk[k];
@@ -84,21 +87,37 @@ __global__ __launch_bounds__(kBlock) void uwrite_kernel(Config c, const uint32_t
     (void)block_exclusive_scan(part, s_tmp, before);
     v0 = before;
   }
-  for (uint32_t base = lo; base < hi; base += kScanTile) {
-    // kScanItems consecutive pairs per thread
-    const uint32_t first = base + tid * kScanItems;
-    uint32_t heads = 0;
+  // batches of kCountItems rows of kBlock consecutive pairs (coalesced);
+  // heads numbered in pair order: row, then wave, then lane
+  for (uint32_t base = lo; base < hi; base += kBlock * kCountItems) {
+    uint64_t m[kCountItems];
 #pragma unroll
-    for (int j = 0; j < kScanItems; ++j) {
-      const uint32_t i = first + j;
-      if (i < hi && is_head(keys, ff, i)) heads |= 1u << j;
+    for (int j = 0; j < kCountItems; ++j) {
+      const uint32_t i = base + j * kBlock + tid;
+      m[j] = __ballot(i < hi && is_head(keys, ff, i));
     }
-    uint32_t total;
-    uint32_t v = v0 + block_exclusive_scan(__popc(heads), s_tmp, total);
+    if (lane == 0)
 #pragma unroll
-    for (int j = 0; j < kScanItems; ++j)
-      if (heads & (1u << j)) c.seg_start[ff + v++] = first + j;
-    v0 += total;
+      for (int j = 0; j < kCountItems; ++j) s_off[j][wave] = (uint32_t)__popcll(m[j]);
+    __syncthreads();
+    if (tid == 0) {
+      uint32_t run = 0;
+      for (int j = 0; j < kCountItems; ++j)
+        for (int w = 0; w < kWaves; ++w) {
+          const uint32_t x = s_off[j][w];
+          s_off[j][w] = run;
+          run += x;
+        }
+      s_batch = run;
+    }
+    __syncthreads();
+    const uint64_t lt = lanemask_lt();
+#pragma unroll
+    for (int j = 0; j < kCountItems; ++j)
+      if ((m[j] >> lane) & 1u)
+        c.seg_start[ff + v0 + s_off[j][wave] + (uint32_t)__popcll(m[j] & lt)] = base + j * kBlock + tid;
+    v0 += s_batch;
+    __syncthreads();
   }
 }
 

@@ -7,8 +7,8 @@ binding) never imports, loads or calls it, and the two share no code.
 The arithmetic lives in ``oracle.c`` (plain C, single-threaded, built with
 ``-O2 -ffp-contract=off``); this file only marshals numpy arrays.  The
 definition it follows is spelled out in ``oracle.h``: Eq. 6/7 motion
-compensation, the Alg. 1 keep test against the Eq. 1 ROI union (out-of-ROI
-keep rate zero), quantisation, sort by (key, point index), max_points and
+compensation, the Alg. 1 keep test against the Eq. 1 ROI union (with an
+optional out-of-ROI keep rate drawn from SplitMix64), quantisation, sort by (key, point index), max_points and
 max_voxels caps, and fp64 mean pooling.
 """
 from __future__ import annotations
@@ -60,6 +60,17 @@ def lib() -> ctypes.CDLL:
         L.oracle_keep.restype = ctypes.c_int64
         L.oracle_roi_voxelize.argtypes = args + [p, p, p, p, p]
         L.oracle_roi_voxelize.restype = ctypes.c_int64
+        bg = [ctypes.c_float, ctypes.c_uint64]
+        L.oracle_keep_bg.argtypes = args + bg + [p, p]
+        L.oracle_keep_bg.restype = ctypes.c_int64
+        L.oracle_roi_voxelize_bg.argtypes = args + bg + [p, p, p, p, p]
+        L.oracle_roi_voxelize_bg.restype = ctypes.c_int64
+        L.oracle_splitmix64.argtypes = [ctypes.c_uint64, ctypes.c_uint64]
+        L.oracle_splitmix64.restype = ctypes.c_uint64
+        L.oracle_background_threshold.argtypes = [ctypes.c_float]
+        L.oracle_background_threshold.restype = ctypes.c_uint32
+        L.oracle_background_keep.argtypes = [ctypes.c_uint64, ctypes.c_uint32, ctypes.c_int64]
+        L.oracle_background_keep.restype = ctypes.c_int32
         _lib = L
     return _lib
 
@@ -128,18 +139,29 @@ def _common(feat, frame_offsets, sweep_ids, poses, rois, roi_offsets, budgets):
     return C, N, args, keep_alive
 
 
-def keep(feat, frame_offsets, sweep_ids, poses, rois, roi_offsets, budgets, grid: OracleGrid):
+def splitmix64(seed: int, n: int) -> int:
+    """n-th output (n >= 1) of SplitMix64 seeded with seed."""
+    return int(lib().oracle_splitmix64(seed, n))
+
+
+def background_threshold(rho: float) -> int:
+    return int(lib().oracle_background_threshold(rho))
+
+
+def keep(feat, frame_offsets, sweep_ids, poses, rois, roi_offsets, budgets, grid: OracleGrid,
+         rho_out: float = 0.0, seed: int = 0):
     """Kept (key, point index) pairs in point order (steps 1-4)."""
     C, N, args, _ka = _common(feat, frame_offsets, sweep_ids, poses, rois, roi_offsets, budgets)
     keys = np.zeros(max(N, 1), dtype=np.uint64)
     idx = np.zeros(max(N, 1), dtype=np.int64)
-    K = lib().oracle_keep(*args, ctypes.byref(grid), keys.ctypes.data, idx.ctypes.data)
+    K = lib().oracle_keep_bg(*args, ctypes.byref(grid), rho_out, seed, keys.ctypes.data, idx.ctypes.data)
     if K < 0:
         raise ValueError("oracle_keep: bad argument")
     return keys[:K].copy(), idx[:K].copy()
 
 
-def roi_voxelize(feat, frame_offsets, sweep_ids, poses, rois, roi_offsets, budgets, grid: OracleGrid):
+def roi_voxelize(feat, frame_offsets, sweep_ids, poses, rois, roi_offsets, budgets, grid: OracleGrid,
+                 rho_out: float = 0.0, seed: int = 0):
     """The whole path.  Returns a dict of numpy arrays trimmed to V rows."""
     C, N, args, _ka = _common(feat, frame_offsets, sweep_ids, poses, rois, roi_offsets, budgets)
     B, M, cap = grid.num_frames, grid.max_points, grid.max_voxels
@@ -149,15 +171,15 @@ def roi_voxelize(feat, frame_offsets, sweep_ids, poses, rois, roi_offsets, budge
     feats = np.zeros((rows, C), dtype=np.float32)
     pidx = np.zeros((rows, M), dtype=np.int32)
     voff = np.zeros(B + 1, dtype=np.int64)
-    V = lib().oracle_roi_voxelize(*args, ctypes.byref(grid), coords.ctypes.data, counts.ctypes.data,
-                                  feats.ctypes.data, pidx.ctypes.data, voff.ctypes.data)
+    V = lib().oracle_roi_voxelize_bg(*args, ctypes.byref(grid), rho_out, seed, coords.ctypes.data,
+                                     counts.ctypes.data, feats.ctypes.data, pidx.ctypes.data, voff.ctypes.data)
     if V < 0:
         raise ValueError("oracle_roi_voxelize: bad argument")
     return {"coords": coords[:V].copy(), "counts": counts[:V].copy(), "feats": feats[:V].copy(),
             "point_idx": pidx[:V].copy(), "voxel_offsets": voff}
 
 
-def run_workload(wl):
+def run_workload(wl, rho_out: float = 0.0, seed: int = 0):
     """Oracle output for a synth workload (records built by the oracle's own make_rois)."""
     return roi_voxelize(wl.feat, wl.frame_offsets, wl.sweep_ids, wl.poses, make_rois(wl.roi_desc),
-                        wl.roi_offsets, wl.budgets, grid_of(wl))
+                        wl.roi_offsets, wl.budgets, grid_of(wl), rho_out, seed)

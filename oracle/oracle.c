@@ -41,6 +41,33 @@ int32_t oracle_inside(const oracle_roi* r, float x, float y) {
   return fabsf(lx) <= r->ext_x && fabsf(ly) <= r->ext_y;
 }
 
+/* The n-th output (n >= 1) of the SplitMix64 generator (Steele, Lea and
+ * Flood, OOPSLA 2014, in the form of Vigna's public-domain reference code)
+ * whose state starts at `seed`: the state advances by the golden-ratio
+ * increment per output and each output is the state mixed by two
+ * xor-shift-multiply rounds and a final xor-shift. */
+uint64_t oracle_splitmix64(uint64_t seed, uint64_t n) {
+  uint64_t z = seed + n * 0x9E3779B97F4A7C15ull;
+  z = (z ^ (z >> 30)) * 0xBF58476D1CE4E5B9ull;
+  z = (z ^ (z >> 27)) * 0x94D049BB133111EBull;
+  return z ^ (z >> 31);
+}
+
+/* Alg. 1 keep rate of out-of-ROI points, as a 24-bit threshold:
+ * round(rho * 2^24), clamped to [0, 2^24] (NaN and rho <= 0 give 0). */
+uint32_t oracle_background_threshold(float rho) {
+  double t = (double)rho * 16777216.0;
+  if (!(t > 0.0)) return 0;
+  if (t >= 16777216.0) return 16777216u;
+  return (uint32_t)floor(t + 0.5);
+}
+
+/* Whether point i is drawn for the background keep: the top 24 bits of the
+ * generator's (i + 1)-th output lie below the threshold. */
+int32_t oracle_background_keep(uint64_t seed, uint32_t threshold, int64_t i) {
+  return (uint32_t)(oracle_splitmix64(seed, (uint64_t)i + 1u) >> 40) < threshold;
+}
+
 /* Alg. 1 "Voxelize": grid coordinate of p' on each axis. */
 int32_t oracle_quantize(const oracle_grid* g, const float* p, int32_t* ijk) {
   for (int d = 0; d < 3; ++d) {
@@ -59,11 +86,12 @@ static int bad_args(int32_t C, int64_t N, const oracle_grid* g) {
   return 0;
 }
 
-/* Steps 1-4 of oracle.h for frame b, appended to (keys, idx). */
+/* Steps 1-4 of oracle.h for frame b, appended to (keys, idx); out-of-ROI
+ * points are drawn with threshold bg_thr (0: none). */
 static int64_t keep_frame(int32_t b, const float* feat, int64_t stride, const int64_t* frame_offsets,
                           const uint8_t* sweep_ids, const float* poses, const oracle_roi* rois,
                           const int32_t* roi_offsets, const uint8_t* budgets, const oracle_grid* g,
-                          uint64_t* keys, int64_t* idx, int64_t k) {
+                          uint32_t bg_thr, uint64_t bg_seed, uint64_t* keys, int64_t* idx, int64_t k) {
   const int S = g->num_sweeps;
   const uint64_t Dx = (uint64_t)g->dims[0], Dy = (uint64_t)g->dims[1], Dz = (uint64_t)g->dims[2];
   for (int64_t i = frame_offsets[b]; i < frame_offsets[b + 1]; ++i) {
@@ -74,6 +102,7 @@ static int64_t keep_frame(int32_t b, const float* feat, int64_t stride, const in
     int keep = 0;
     for (int32_t j = roi_offsets[b]; j < roi_offsets[b + 1] && !keep; ++j)
       if (s < budgets[j] && oracle_inside(&rois[j], p[0], p[1])) keep = 1;
+    if (!keep) keep = oracle_background_keep(bg_seed, bg_thr, i);
     if (!keep) continue;
     int32_t ijk[3];
     if (!oracle_quantize(g, p, ijk)) continue;
@@ -84,16 +113,25 @@ static int64_t keep_frame(int32_t b, const float* feat, int64_t stride, const in
   return k;
 }
 
+int64_t oracle_keep_bg(const float* feat, int64_t stride, int32_t num_features, int64_t num_points,
+                       const int64_t* frame_offsets, const uint8_t* sweep_ids, const float* poses,
+                       const oracle_roi* rois, const int32_t* roi_offsets, const uint8_t* budgets,
+                       const oracle_grid* g, float rho_out, uint64_t seed, uint64_t* keys, int64_t* idx) {
+  if (bad_args(num_features, num_points, g)) return -1;
+  const uint32_t thr = oracle_background_threshold(rho_out);
+  int64_t k = 0;
+  for (int32_t b = 0; b < g->num_frames; ++b)
+    k = keep_frame(b, feat, stride, frame_offsets, sweep_ids, poses, rois, roi_offsets, budgets, g, thr, seed,
+                   keys, idx, k);
+  return k;
+}
+
 int64_t oracle_keep(const float* feat, int64_t stride, int32_t num_features, int64_t num_points,
                     const int64_t* frame_offsets, const uint8_t* sweep_ids, const float* poses,
                     const oracle_roi* rois, const int32_t* roi_offsets, const uint8_t* budgets,
                     const oracle_grid* g, uint64_t* keys, int64_t* idx) {
-  if (bad_args(num_features, num_points, g)) return -1;
-  int64_t k = 0;
-  for (int32_t b = 0; b < g->num_frames; ++b)
-    k = keep_frame(b, feat, stride, frame_offsets, sweep_ids, poses, rois, roi_offsets, budgets, g, keys, idx,
-                   k);
-  return k;
+  return oracle_keep_bg(feat, stride, num_features, num_points, frame_offsets, sweep_ids, poses, rois,
+                        roi_offsets, budgets, g, 0.0f, 0, keys, idx);
 }
 
 typedef struct {
@@ -128,12 +166,14 @@ static int cmp_pos(const void* a, const void* b) {
   return x->pos < y->pos ? -1 : (x->pos > y->pos ? 1 : 0);
 }
 
-int64_t oracle_roi_voxelize(const float* feat, int64_t stride, int32_t C, int64_t N,
-                            const int64_t* frame_offsets, const uint8_t* sweep_ids, const float* poses,
-                            const oracle_roi* rois, const int32_t* roi_offsets, const uint8_t* budgets,
-                            const oracle_grid* g, int32_t* out_coords, int32_t* out_counts,
-                            float* out_feats, int32_t* out_point_idx, int64_t* out_voxel_offsets) {
+int64_t oracle_roi_voxelize_bg(const float* feat, int64_t stride, int32_t C, int64_t N,
+                               const int64_t* frame_offsets, const uint8_t* sweep_ids, const float* poses,
+                               const oracle_roi* rois, const int32_t* roi_offsets, const uint8_t* budgets,
+                               const oracle_grid* g, float rho_out, uint64_t seed, int32_t* out_coords,
+                               int32_t* out_counts, float* out_feats, int32_t* out_point_idx,
+                               int64_t* out_voxel_offsets) {
   if (bad_args(C, N, g)) return -1;
+  const uint32_t bg_thr = oracle_background_threshold(rho_out);
   const int S = g->num_sweeps;
   const int M = g->max_points;
   const int64_t cap = g->max_voxels;
@@ -146,7 +186,7 @@ int64_t oracle_roi_voxelize(const float* feat, int64_t stride, int32_t C, int64_
     int64_t* idx = (int64_t*)malloc(sizeof(int64_t) * (size_t)(n_b > 0 ? n_b : 1));
     /* steps 1-4 */
     int64_t K = keep_frame(b, feat, stride, frame_offsets, sweep_ids, poses, rois, roi_offsets, budgets, g,
-                           keys, idx, 0);
+                           bg_thr, seed, keys, idx, 0);
     /* step 5: sort (key, index) */
     pair_t* pairs = (pair_t*)malloc(sizeof(pair_t) * (size_t)(K > 0 ? K : 1));
     for (int64_t k = 0; k < K; ++k) {
@@ -218,4 +258,13 @@ int64_t oracle_roi_voxelize(const float* feat, int64_t stride, int32_t C, int64_
     free(keys);
   }
   return total;
+}
+
+int64_t oracle_roi_voxelize(const float* feat, int64_t stride, int32_t C, int64_t N,
+                            const int64_t* frame_offsets, const uint8_t* sweep_ids, const float* poses,
+                            const oracle_roi* rois, const int32_t* roi_offsets, const uint8_t* budgets,
+                            const oracle_grid* g, int32_t* out_coords, int32_t* out_counts,
+                            float* out_feats, int32_t* out_point_idx, int64_t* out_voxel_offsets) {
+  return oracle_roi_voxelize_bg(feat, stride, C, N, frame_offsets, sweep_ids, poses, rois, roi_offsets, budgets,
+                                g, 0.0f, 0, out_coords, out_counts, out_feats, out_point_idx, out_voxel_offsets);
 }

@@ -6,7 +6,8 @@
  * calls it, and it shares no code, header or constant with that library.
  *
  * What it computes (paper: Sec. IV-D Eq. 6-7, Sec. IV-C Eq. 1, Sec. IV-F
- * Alg. 1 with the out-of-ROI keep rate set to zero), for every frame b:
+ * Alg. 1; the out-of-ROI keep rate rho_out is zero unless a *_bg entry
+ * point is given one), for every frame b:
  *   1. a point of sweep s >= num_sweeps is dropped;
  *   2. it is moved into the current frame, p' = R_{b,s} p + T_{b,s}
  *      (Eq. 6/7), in fp32 as the fused chain
@@ -17,6 +18,10 @@
  *        dx = x' - cx, dy = y' - cy,
  *        lx = fma(cos, dx, sin*dy), ly = fma(cos, dy, -(sin*dx)),
  *        |lx| <= ext_x  and  |ly| <= ext_y;
+ *      otherwise it is kept with probability rho_out (Alg. 1), drawn from a
+ *      counter-based generator so that the draw is a function of the point:
+ *      kept iff (splitmix64(seed, i + 1) >> 40) < round(rho_out * 2^24),
+ *      i the point's index in the batch;
  *   4. it is quantised (Alg. 1 "Voxelize"): f_d = (p'_d - min_d) / v_d in
  *      fp32 (correctly rounded), kept iff 0 <= f_d < D_d on all three axes,
  *      i_d = trunc(f_d), key = ((b*Dz + iz)*Dy + iy)*Dx + ix;
@@ -70,6 +75,29 @@ int32_t oracle_inside(const oracle_roi* roi, float x, float y);
 
 /* Step 4 alone: 1 and the three indices if p' lies in the grid. */
 int32_t oracle_quantize(const oracle_grid* g, const float* p3, int32_t* ijk);
+
+/* SplitMix64: the n-th output (n >= 1) of the generator seeded with seed. */
+uint64_t oracle_splitmix64(uint64_t seed, uint64_t n);
+
+/* round(rho * 2^24) clamped to [0, 2^24]: the background keep threshold. */
+uint32_t oracle_background_threshold(float rho);
+
+/* 1 if point i is drawn for the background keep (see step 3). */
+int32_t oracle_background_keep(uint64_t seed, uint32_t threshold, int64_t i);
+
+/* Steps 1-4 for all points, out-of-ROI keep rate rho_out with seed. */
+int64_t oracle_keep_bg(const float* feat, int64_t stride, int32_t num_features, int64_t num_points,
+                       const int64_t* frame_offsets, const uint8_t* sweep_ids, const float* poses,
+                       const oracle_roi* rois, const int32_t* roi_offsets, const uint8_t* budgets,
+                       const oracle_grid* g, float rho_out, uint64_t seed, uint64_t* keys, int64_t* idx);
+
+/* The whole path with out-of-ROI keep rate rho_out and seed. */
+int64_t oracle_roi_voxelize_bg(const float* feat, int64_t stride, int32_t num_features, int64_t num_points,
+                               const int64_t* frame_offsets, const uint8_t* sweep_ids, const float* poses,
+                               const oracle_roi* rois, const int32_t* roi_offsets, const uint8_t* budgets,
+                               const oracle_grid* g, float rho_out, uint64_t seed, int32_t* out_coords,
+                               int32_t* out_counts, float* out_feats, int32_t* out_point_idx,
+                               int64_t* out_voxel_offsets);
 
 /* Steps 1-4 for all points: kept (key, index) pairs in index order.
  * Returns K, or -1 on a bad argument. keys/idx must hold N entries. */

@@ -13,7 +13,8 @@
  * max_points points per voxel and max_voxels voxels per frame ("hard
  * voxelisation", Sec. IV-F), and mean-pooled into a sparse voxel tensor
  * (the Voxel Feature Encoder of Alg. 1, read as mean pooling).  Points
- * outside every ROI are dropped (Alg. 1's out-of-ROI keep rate set to zero).
+ * outside every ROI are dropped (Alg. 1's out-of-ROI keep rate set to zero),
+ * or, through mmbev_roi_voxelize_ex, kept with a given probability.
  *
  * Exact semantics (every decision is taken in fp32 in this operation order;
  * the library is bit-exact against this definition):
@@ -30,6 +31,13 @@
  *        dx = x' - cx; dy = y' - cy;
  *        lx = fma(cos_yaw, dx, sin_yaw*dy); ly = fma(cos_yaw, dy, -(sin_yaw*dx));
  *        |lx| <= ext_x and |ly| <= ext_y            (products rounded to fp32)
+ *      or, with an out-of-ROI keep rate rho (mmbev_options_t), iff
+ *        (splitmix64(seed, i + 1) >> 40) < round(rho * 2^24), clamped to
+ *        [0, 2^24] (NaN: 0), where splitmix64(seed, n) is the n-th output of
+ *        the SplitMix64 generator whose 64-bit state starts at seed
+ *        (state += 0x9E3779B97F4A7C15, then the state mixed: z ^= z >> 30,
+ *        z *= 0xBF58476D1CE4E5B9, z ^= z >> 27, z *= 0x94D049BB133111EB,
+ *        z ^= z >> 31) and i the point's index in the batch;
  *   4. f_d = (p'_d - range_min[d]) / voxel_size[d]  (IEEE fp32, correctly rounded);
  *      kept iff 0 <= f_d < dims[d] for d = x, y, z (NaN fails); i_d = trunc(f_d).
  *      Voxel key = (b, iz, iy, ix) in lexicographic order.
@@ -52,7 +60,7 @@
 extern "C" {
 #endif
 
-#define MMBEV_ABI_VERSION 2
+#define MMBEV_ABI_VERSION 3
 
 /* ------------------------------------------------------------- status */
 typedef int32_t mmbev_status_t;
@@ -114,6 +122,13 @@ typedef struct {
   int32_t num_sweeps;  /* S, 1..255 */
   int32_t num_frames;  /* B, 1..65535 */
 } mmbev_grid_t;
+
+/* Options of mmbev_roi_voxelize_ex (Alg. 1 keep loop). */
+typedef struct {
+  float out_of_roi_keep_rate; /* rho in [0, 1]: probability that a point in no ROI is kept; 0 keeps none */
+  uint32_t reserved;          /* 0 */
+  uint64_t seed;              /* seed of the per-point draw (a function of seed and point index only) */
+} mmbev_options_t;
 
 /* ------------------------------------------------------------ queries */
 int32_t mmbev_abi_version(void);
@@ -198,6 +213,23 @@ mmbev_status_t mmbev_roi_voxelize_profiled(const mmbev_points_t* points, const u
                                            int32_t* out_point_idx, int64_t* out_voxel_offsets, void* workspace,
                                            size_t workspace_bytes, void* stream, void* const* events,
                                            int32_t num_events, int32_t* events_recorded);
+
+/*
+ * The same call with options (NULL: the defaults, out-of-ROI keep rate 0)
+ * and, like mmbev_roi_voxelize_profiled, optional events (events may be NULL
+ * and num_events 0).  Alg. 1 keeps points outside every ROI with probability
+ * rho_out; here the draw of point i is the counter-based function of
+ * (seed, i) given at the top of this file, so a result is reproducible and
+ * independent of the launch layout.  Errors: MMBEV_ERR_INVALID_ARG also for
+ * a nonzero reserved field.
+ */
+mmbev_status_t mmbev_roi_voxelize_ex(const mmbev_points_t* points, const uint8_t* sweep_ids,
+                                     const float* sweep_poses, const mmbev_rois_t* rois,
+                                     const uint8_t* roi_sweep_budget, const mmbev_grid_t* grid_params,
+                                     const mmbev_options_t* options, int32_t* out_coords, int32_t* out_counts,
+                                     float* out_feats, int32_t* out_point_idx, int64_t* out_voxel_offsets,
+                                     void* workspace, size_t workspace_bytes, void* stream, void* const* events,
+                                     int32_t num_events, int32_t* events_recorded);
 
 #ifdef __cplusplus
 }

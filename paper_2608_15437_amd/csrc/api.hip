@@ -185,12 +185,21 @@ struct EventTrail {
   }
 };
 
+// round(rho * 2^24) clamped to [0, 2^24]; NaN and rho <= 0 give 0.
+uint32_t keep_threshold(float rho) {
+  const double t = (double)rho * 16777216.0;
+  if (!(t > 0.0)) return 0;
+  if (t >= 16777216.0) return 1u << 24;
+  return (uint32_t)std::floor(t + 0.5);
+}
+
 mmbev_status_t voxelize(const mmbev_points_t* points, const uint8_t* sweep_ids, const float* sweep_poses,
                         const mmbev_rois_t* rois, const uint8_t* roi_sweep_budget, const mmbev_grid_t* grid,
-                        int32_t* out_coords, int32_t* out_counts, float* out_feats, int32_t* out_point_idx,
-                        int64_t* out_voxel_offsets, void* workspace, size_t workspace_bytes, void* stream,
-                        EventTrail& ev) {
+                        const mmbev_options_t* opt, int32_t* out_coords, int32_t* out_counts, float* out_feats,
+                        int32_t* out_point_idx, int64_t* out_voxel_offsets, void* workspace,
+                        size_t workspace_bytes, void* stream, EventTrail& ev) {
   if (!points || !rois || !grid) return MMBEV_ERR_INVALID_ARG;
+  if (opt && opt->reserved != 0) return MMBEV_ERR_INVALID_ARG;
   const int64_t N = points->num_points;
   Plan p;
   mmbev_status_t st = make_plan(grid, N, rois->max_rois_per_frame, points->num_features, &p);
@@ -223,6 +232,8 @@ mmbev_status_t voxelize(const mmbev_points_t* points, const uint8_t* sweep_ids, 
   c.R = rois->num_rois;
   c.max_rois = p.max_rois;
   c.W = p.W;
+  c.bg_thr = opt ? keep_threshold(opt->out_of_roi_keep_rate) : 0u;
+  c.bg_seed = opt ? opt->seed : 0u;
   for (int d = 0; d < 3; ++d) {
     c.mn[d] = grid->range_min[d];
     c.vs[d] = grid->voxel_size[d];
@@ -328,8 +339,8 @@ mmbev_status_t mmbev_roi_voxelize(const mmbev_points_t* points, const uint8_t* s
                                   float* out_feats, int32_t* out_point_idx, int64_t* out_voxel_offsets,
                                   void* workspace, size_t workspace_bytes, void* stream) {
   EventTrail ev;
-  return voxelize(points, sweep_ids, sweep_poses, rois, roi_sweep_budget, grid, out_coords, out_counts, out_feats,
-                  out_point_idx, out_voxel_offsets, workspace, workspace_bytes, stream, ev);
+  return voxelize(points, sweep_ids, sweep_poses, rois, roi_sweep_budget, grid, nullptr, out_coords, out_counts,
+                  out_feats, out_point_idx, out_voxel_offsets, workspace, workspace_bytes, stream, ev);
 }
 
 mmbev_status_t mmbev_roi_voxelize_profiled(const mmbev_points_t* points, const uint8_t* sweep_ids,
@@ -342,7 +353,24 @@ mmbev_status_t mmbev_roi_voxelize_profiled(const mmbev_points_t* points, const u
   EventTrail ev;
   ev.events = events;
   ev.n = (events && num_events > 0) ? num_events : 0;
-  mmbev_status_t st = voxelize(points, sweep_ids, sweep_poses, rois, roi_sweep_budget, grid, out_coords,
+  mmbev_status_t st = voxelize(points, sweep_ids, sweep_poses, rois, roi_sweep_budget, grid, nullptr, out_coords,
+                               out_counts, out_feats, out_point_idx, out_voxel_offsets, workspace, workspace_bytes,
+                               stream, ev);
+  if (events_recorded) *events_recorded = ev.used;
+  return st;
+}
+
+mmbev_status_t mmbev_roi_voxelize_ex(const mmbev_points_t* points, const uint8_t* sweep_ids,
+                                     const float* sweep_poses, const mmbev_rois_t* rois,
+                                     const uint8_t* roi_sweep_budget, const mmbev_grid_t* grid,
+                                     const mmbev_options_t* options, int32_t* out_coords, int32_t* out_counts,
+                                     float* out_feats, int32_t* out_point_idx, int64_t* out_voxel_offsets,
+                                     void* workspace, size_t workspace_bytes, void* stream, void* const* events,
+                                     int32_t num_events, int32_t* events_recorded) {
+  EventTrail ev;
+  ev.events = events;
+  ev.n = (events && num_events > 0) ? num_events : 0;
+  mmbev_status_t st = voxelize(points, sweep_ids, sweep_poses, rois, roi_sweep_budget, grid, options, out_coords,
                                out_counts, out_feats, out_point_idx, out_voxel_offsets, workspace, workspace_bytes,
                                stream, ev);
   if (events_recorded) *events_recorded = ev.used;

@@ -75,6 +75,10 @@ struct Config {
   // least-significant-digit passes of dbits bits
   int32_t kb, passes, dbits;
   int32_t vec;  // 16-byte vector loads allowed
+  // out-of-ROI keep (Alg. 1 rate rho_out): threshold round(rho_out * 2^24)
+  // on the top 24 bits of the point's SplitMix64 draw; 0 keeps none
+  uint32_t bg_thr;
+  uint64_t bg_seed;
   // outputs
   int32_t* out_coords;
   int32_t* out_counts;
@@ -208,6 +212,19 @@ __device__ __forceinline__ bool inside_roi(const mmbev_roi_t& r, float x, float 
   float lx = fma_rn(r.cos_yaw, dx, s_dy);
   float ly = fma_rn(r.cos_yaw, dy, -s_dx);
   return fabsf(lx) <= r.ext_x && fabsf(ly) <= r.ext_y;
+}
+
+// The out-of-ROI keep draw of Alg. 1 (rate rho_out): point i is drawn when
+// the top 24 bits of the (i + 1)-th output of a SplitMix64 generator (Steele,
+// Lea and Flood 2014) whose state starts at the seed lie below the threshold
+// round(rho_out * 2^24).  The generator advances its state by the golden-
+// ratio increment and mixes it with two xor-shift-multiply rounds.
+__device__ __forceinline__ bool background_draw(const Config& c, uint32_t i) {
+  uint64_t z = c.bg_seed + ((uint64_t)i + 1u) * 0x9E3779B97F4A7C15ull;
+  z = (z ^ (z >> 30)) * 0xBF58476D1CE4E5B9ull;
+  z = (z ^ (z >> 27)) * 0x94D049BB133111EBull;
+  z ^= z >> 31;
+  return (uint32_t)(z >> 40) < c.bg_thr;
 }
 
 // Grid coordinate on one axis; false when outside [0, D) or not a number.

@@ -58,7 +58,7 @@ struct alignas(16) FilterLds {
 // Per-wave state in LDS: the candidate queue (a ring) and the kept bitmap
 // of the wave's chunk.
 struct WaveLds {
-  uint32_t pk[kWaveQueue];    // point offset in the chunk | sweep << 16
+  uint32_t pk[kWaveQueue];    // point offset in the chunk | sweep << 16 | drawn out-of-ROI << 24
   uint32_t cand[kWaveQueue];  // candidate-ROI word (W == 1) or the cell's any-word
   float px[kWaveQueue];       // p' (Eq. 6), exact
   float py[kWaveQueue];
@@ -286,12 +286,15 @@ struct QuadState {
   float px[4], py[4], pz[4];  // p' (Eq. 6), exact
   uint32_t sw[4];             // sweep
   uint32_t cand[4];           // candidate-ROI word after phase A (0: none)
+  uint32_t bg;                // bit q: point q is drawn for the out-of-ROI keep
 };
 
 // Phase A of four points of a lane (first index i0, frame b for the whole
 // wave): p' and the candidate-ROI word of each point's cell (from LDS when
 // staged, so that the only global loads in flight are the point tiles).
-template <bool ST>
+// BG: the out-of-ROI keep rate is nonzero (without it no draw is made and
+// the code below is the ROI-only path).
+template <bool ST, bool BG>
 __device__ __forceinline__ void phase_a(const Config& c, const FilterLds& L, int32_t b, uint32_t i0, const Quad& d,
                                         QuadState& st) {
   const uint32_t S = (uint32_t)c.S;
@@ -337,6 +340,12 @@ __device__ __forceinline__ void phase_a(const Config& c, const FilterLds& L, int
     const uint32_t w = ST ? L.cell[(b - L.f0) * c.ncells + cell] : c.cellany[(int64_t)b * c.ncells + cell];
     st.cand[q] = cidx[q] >= 0 ? w : 0u;
   }
+  // the out-of-ROI keep draw
+  st.bg = 0;
+  if (BG)
+#pragma unroll
+    for (int q = 0; q < 4; ++q)
+      st.bg |= (cidx[q] >= 0 && sq[q] < S && background_draw(c, i0 + q)) ? 1u << q : 0u;
 }
 
 // Queue and kept-point state of one wave (wave-uniform values).
@@ -354,7 +363,7 @@ struct WaveRun {
 // store inside the tile loop would make the compiler wait for it (and, since
 // vector memory operations complete in order, for every tile load before it)
 // once its source registers are reused.
-template <bool ST>
+template <bool ST, bool BG>
 __device__ __forceinline__ void decide_round(const Config& c, const FilterLds& L, WaveLds& Q, WaveRun& wr,
                                              uint32_t n) {
   const uint32_t lane = (uint32_t)(threadIdx.x & 63);
@@ -372,18 +381,21 @@ __device__ __forceinline__ void decide_round(const Config& c, const FilterLds& L
     keep = roi_test_one_word<ST>(c, L, r0, cand, px, py);
   } else {
     keep = false;
-    if (cand != 0u) keep = roi_test_words<ST>(c, L, wr.b, pk >> 16, r0, ix, iy, px, py);
+    if (cand != 0u) keep = roi_test_words<ST>(c, L, wr.b, (pk >> 16) & 0xffu, r0, ix, iy, px, py);
   }
+  if (BG) keep = keep || (live && in_grid && ((pk >> 24) & 1u));  // drawn out-of-ROI points in the grid
   if (keep) atomicOr(&Q.bits[(pk & 0xffffu) >> 5], 1u << (pk & 31u));
-  wr.kept += (uint32_t)__popcll(__ballot(keep));  wr.head = (wr.head + n) & (kWaveQueue - 1);
+  wr.kept += (uint32_t)__popcll(__ballot(keep));
+  wr.head = (wr.head + n) & (kWaveQueue - 1);
   wr.queued -= n;
   wave_lds_sync();  // slots read before they are written again
 }
 
-// Phase B of four points of a lane: budget masks, then the candidates
+// Phase B of four points of a lane: budget masks, then the candidates (a
+// candidate ROI that admits the sweep, or drawn for the out-of-ROI keep)
 // appended in point order (lane, then q) to the wave's ring, deciding full
 // rounds of 64 as they become available.
-template <bool ST>
+template <bool ST, bool BG>
 __device__ __forceinline__ void phase_b(const Config& c, const FilterLds& L, WaveLds& Q, uint32_t i0,
                                         QuadState& st, WaveRun& wr) {
   if (c.W == 1) {
@@ -391,8 +403,11 @@ __device__ __forceinline__ void phase_b(const Config& c, const FilterLds& L, Wav
     for (int q = 0; q < 4; ++q)
       if (st.cand[q]) st.cand[q] &= budget_word<ST>(c, L, wr.b, st.sw[q], 0);
   }
+  bool has[4];
+#pragma unroll
+  for (int q = 0; q < 4; ++q) has[q] = st.cand[q] != 0u || (BG && ((st.bg >> q) & 1u));
   const uint64_t lt = lanemask_lt();
-  const uint32_t n = (st.cand[0] != 0) + (st.cand[1] != 0) + (st.cand[2] != 0) + (st.cand[3] != 0);
+  const uint32_t n = (uint32_t)has[0] + (uint32_t)has[1] + (uint32_t)has[2] + (uint32_t)has[3];
   const uint64_t b0 = __ballot(n & 1u), b1 = __ballot(n & 2u), b2 = __ballot(n & 4u);
   const uint32_t rank0 = __popcll(b0 & lt) + 2u * __popcll(b1 & lt) + 4u * __popcll(b2 & lt);
   const uint32_t total = __popcll(b0) + 2u * __popcll(b1) + 4u * __popcll(b2);
@@ -402,10 +417,10 @@ __device__ __forceinline__ void phase_b(const Config& c, const FilterLds& L, Wav
     uint32_t rank = rank0;
 #pragma unroll
     for (int q = 0; q < 4; ++q)
-      if (st.cand[q]) {
+      if (has[q]) {
         if (rank - done < take) {
           const uint32_t e = (wr.head + wr.queued + (rank - done)) & (kWaveQueue - 1);
-          Q.pk[e] = (i0 + q - wr.lo) | (st.sw[q] << 16);
+          Q.pk[e] = (i0 + q - wr.lo) | (st.sw[q] << 16) | (BG ? ((st.bg >> q) & 1u) << 24 : 0u);
           Q.cand[e] = st.cand[q];
           Q.px[e] = st.px[q];
           Q.py[e] = st.py[q];
@@ -416,7 +431,7 @@ __device__ __forceinline__ void phase_b(const Config& c, const FilterLds& L, Wav
     wr.queued += take;
     done += take;
     wave_lds_sync();
-    while (wr.queued >= 64) decide_round<ST>(c, L, Q, wr, 64);
+    while (wr.queued >= 64) decide_round<ST, BG>(c, L, Q, wr, 64);
   }
 }
 
@@ -427,7 +442,7 @@ __device__ __forceinline__ void phase_b(const Config& c, const FilterLds& L, Wav
 // issues the same loads in the same order, and the loop over the steps has a
 // fixed trip count and no early exit, so the compiler's wait before a tile's
 // data counts exactly the loads of the tiles after it.
-template <bool ST, int J>
+template <bool ST, bool BG, int J>
 __device__ __forceinline__ void pipeline_step(const Config& c, const FilterLds& L, WaveLds& Q, int32_t b,
                                               uint32_t a0, uint32_t ntiles, uint32_t k0, uint32_t lane4,
                                               Quad (&buf)[kFilterDepth], QuadState& st, WaveRun& wr) {
@@ -436,8 +451,8 @@ __device__ __forceinline__ void pipeline_step(const Config& c, const FilterLds& 
   const uint32_t tile = k - (uint32_t)(kFilterDepth - 1);  // wraps for the first steps
   if (tile < ntiles) {
     const uint32_t t = a0 + tile * kWaveTile;
-    phase_a<ST>(c, L, b, t + lane4, buf[(J + 1) % kFilterDepth], st);
-    phase_b<ST>(c, L, Q, t + lane4, st, wr);
+    phase_a<ST, BG>(c, L, b, t + lane4, buf[(J + 1) % kFilterDepth], st);
+    phase_b<ST, BG>(c, L, Q, t + lane4, st, wr);
   }
 }
 
@@ -447,7 +462,7 @@ __device__ __forceinline__ void pipeline_step(const Config& c, const FilterLds& 
 // pipeline of kFilterDepth buffers with 16-byte loads (when the rows allow
 // them; otherwise every tile is loaded point by point): the loads of the
 // next kFilterDepth - 1 tiles are in flight while a tile is handled.
-template <bool VEC, bool ST>
+template <bool VEC, bool ST, bool BG>
 __device__ __forceinline__ void run_wave(const Config& c, const FilterLds& L, WaveLds& Q, int32_t b, uint32_t lo,
                                          uint32_t hi, WaveRun& wr) {
   const uint32_t lane = (uint32_t)(threadIdx.x & 63), lane4 = 4u * lane;
@@ -460,28 +475,28 @@ __device__ __forceinline__ void run_wave(const Config& c, const FilterLds& L, Wa
   const uint32_t a0 = VEC ? min((lo + 3u) & ~3u, hi) : lo;
   if (a0 > lo) {  // head: fewer than 4 points
     load_quad_scalar(c, lo + lane4, a0, buf[0]);
-    phase_a<ST>(c, L, b, lo + lane4, buf[0], st);
-    phase_b<ST>(c, L, Q, lo + lane4, st, wr);
+    phase_a<ST, BG>(c, L, b, lo + lane4, buf[0], st);
+    phase_b<ST, BG>(c, L, Q, lo + lane4, st, wr);
   }
   const uint32_t ntiles = VEC ? (hi - a0) / kWaveTile : 0u;
   static_assert(kFilterDepth >= 2 && kFilterDepth <= 6, "pipeline steps written out below");
   if (ntiles > 0) {
     const uint32_t steps = ntiles + (uint32_t)(kFilterDepth - 1);
     for (uint32_t k0 = 0; k0 < steps; k0 += kFilterDepth) {
-      pipeline_step<ST, 0>(c, L, Q, b, a0, ntiles, k0, lane4, buf, st, wr);
-      pipeline_step<ST, 1>(c, L, Q, b, a0, ntiles, k0, lane4, buf, st, wr);
-      if constexpr (kFilterDepth > 2) pipeline_step<ST, 2 % kFilterDepth>(c, L, Q, b, a0, ntiles, k0, lane4, buf, st, wr);
-      if constexpr (kFilterDepth > 3) pipeline_step<ST, 3 % kFilterDepth>(c, L, Q, b, a0, ntiles, k0, lane4, buf, st, wr);
-      if constexpr (kFilterDepth > 4) pipeline_step<ST, 4 % kFilterDepth>(c, L, Q, b, a0, ntiles, k0, lane4, buf, st, wr);
-      if constexpr (kFilterDepth > 5) pipeline_step<ST, 5 % kFilterDepth>(c, L, Q, b, a0, ntiles, k0, lane4, buf, st, wr);
+      pipeline_step<ST, BG, 0>(c, L, Q, b, a0, ntiles, k0, lane4, buf, st, wr);
+      pipeline_step<ST, BG, 1>(c, L, Q, b, a0, ntiles, k0, lane4, buf, st, wr);
+      if constexpr (kFilterDepth > 2) pipeline_step<ST, BG, 2 % kFilterDepth>(c, L, Q, b, a0, ntiles, k0, lane4, buf, st, wr);
+      if constexpr (kFilterDepth > 3) pipeline_step<ST, BG, 3 % kFilterDepth>(c, L, Q, b, a0, ntiles, k0, lane4, buf, st, wr);
+      if constexpr (kFilterDepth > 4) pipeline_step<ST, BG, 4 % kFilterDepth>(c, L, Q, b, a0, ntiles, k0, lane4, buf, st, wr);
+      if constexpr (kFilterDepth > 5) pipeline_step<ST, BG, 5 % kFilterDepth>(c, L, Q, b, a0, ntiles, k0, lane4, buf, st, wr);
     }
   }
   for (uint32_t t = a0 + ntiles * kWaveTile; t < hi; t += kWaveTile) {
     load_quad_scalar(c, t + lane4, hi, buf[0]);
-    phase_a<ST>(c, L, b, t + lane4, buf[0], st);
-    phase_b<ST>(c, L, Q, t + lane4, st, wr);
+    phase_a<ST, BG>(c, L, b, t + lane4, buf[0], st);
+    phase_b<ST, BG>(c, L, Q, t + lane4, st, wr);
   }
-  while (wr.queued > 0) decide_round<ST>(c, L, Q, wr, min(wr.queued, 64u));
+  while (wr.queued > 0) decide_round<ST, BG>(c, L, Q, wr, min(wr.queued, 64u));
   wave_lds_sync();
   // the chunk's bitmap, every word (bits past hi are zero)
   uint32_t* out = c.fbits + (int64_t)wr.k * c.fchunk_words;
@@ -491,8 +506,8 @@ __device__ __forceinline__ void run_wave(const Config& c, const FilterLds& L, Wa
 
 // Workgroup w: its waves over filter chunks kWaves*w .. kWaves*w + 3.  Per
 // chunk it leaves the bitmap of its kept points, their number, its first
-// point and its frame.
-template <bool VEC>
+// point and its frame.  BG: the out-of-ROI keep rate is nonzero.
+template <bool VEC, bool BG>
 __global__ __launch_bounds__(kBlock) void filter_kernel(Config c) {
   __shared__ FilterLds L;
   __shared__ WaveLds Qs[kWaves];
@@ -526,9 +541,9 @@ __global__ __launch_bounds__(kBlock) void filter_kernel(Config c) {
   hi = __builtin_amdgcn_readfirstlane(hi);
   WaveRun wr{0u, 0u, 0u, lo, b, k};
   if (staged)
-    run_wave<VEC, true>(c, L, Q, b, lo, hi, wr);
+    run_wave<VEC, true, BG>(c, L, Q, b, lo, hi, wr);
   else
-    run_wave<VEC, false>(c, L, Q, b, lo, hi, wr);
+    run_wave<VEC, false, BG>(c, L, Q, b, lo, hi, wr);
   if (lane == 0) {
     c.fcount[k] = wr.kept;
     c.fchunk_lo[k] = lo;
@@ -539,10 +554,16 @@ __global__ __launch_bounds__(kBlock) void filter_kernel(Config c) {
 }  // namespace
 
 hipError_t launch_filter(const Config& c, hipStream_t st) {
-  if (c.vec)
-    hipLaunchKernelGGL(filter_kernel<true>, dim3(c.filter_grid), dim3(kBlock), 0, st, c);
+  // one instance per load form and per rate (none, or a nonzero one)
+  const dim3 grid(c.filter_grid), block(kBlock);
+  if (c.vec && c.bg_thr == 0u)
+    hipLaunchKernelGGL((filter_kernel<true, false>), grid, block, 0, st, c);
+  else if (c.vec)
+    hipLaunchKernelGGL((filter_kernel<true, true>), grid, block, 0, st, c);
+  else if (c.bg_thr == 0u)
+    hipLaunchKernelGGL((filter_kernel<false, false>), grid, block, 0, st, c);
   else
-    hipLaunchKernelGGL(filter_kernel<false>, dim3(c.filter_grid), dim3(kBlock), 0, st, c);
+    hipLaunchKernelGGL((filter_kernel<false, true>), grid, block, 0, st, c);
   return hipGetLastError();
 }
 

@@ -38,6 +38,10 @@ class mmbev_grid_t(ctypes.Structure):
                 ("num_sweeps", ctypes.c_int32), ("num_frames", ctypes.c_int32)]
 
 
+class mmbev_options_t(ctypes.Structure):
+    _fields_ = [("out_of_roi_keep_rate", ctypes.c_float), ("reserved", ctypes.c_uint32), ("seed", ctypes.c_uint64)]
+
+
 class MmbevError(RuntimeError):
     pass
 
@@ -69,6 +73,9 @@ def load() -> ctypes.CDLL:
         L.mmbev_roi_voxelize.restype = ctypes.c_int32
         L.mmbev_roi_voxelize_profiled.argtypes = L.mmbev_roi_voxelize.argtypes + [p, ctypes.c_int32, p]
         L.mmbev_roi_voxelize_profiled.restype = ctypes.c_int32
+        a = L.mmbev_roi_voxelize.argtypes
+        L.mmbev_roi_voxelize_ex.argtypes = a[:6] + [ctypes.POINTER(mmbev_options_t)] + a[6:] + [p, ctypes.c_int32, p]
+        L.mmbev_roi_voxelize_ex.restype = ctypes.c_int32
         _lib = L
     return _lib
 
@@ -130,12 +137,15 @@ def make_rois(desc) -> np.ndarray:
 
 def roi_voxelize(feat, frame_offsets, sweep_ids, sweep_poses, rois, roi_frame_offsets, roi_sweep_budget,
                  grid: mmbev_grid_t, out_coords, out_counts, out_feats, out_point_idx, out_voxel_offsets,
-                 workspace, max_rois_per_frame: int, stream=None, events=None) -> int:
+                 workspace, max_rois_per_frame: int, stream=None, events=None, rho_out: float = 0.0,
+                 seed: int = 0) -> int:
     """Enqueue one call of mmbev_roi_voxelize on `stream` (torch tensors on the GPU).
 
     feat: float32 [C][stride] (SoA); frame_offsets: int64 [B+1]; sweep_ids: uint8 [N];
     sweep_poses: float32 [B][S][12]; rois: float32 [R][8] (mmbev_roi_t records);
     roi_frame_offsets: int32 [B+1]; roi_sweep_budget: uint8 [R]; outputs as in mmbev.h.
+    rho_out, seed: the out-of-ROI keep rate and its seed; either nonzero selects
+    mmbev_roi_voxelize_ex.
     """
     C = int(feat.shape[0])
     N = int(sweep_ids.numel())
@@ -150,6 +160,14 @@ def roi_voxelize(feat, frame_offsets, sweep_ids, sweep_poses, rois, roi_frame_of
             ctypes.byref(grid), _ptr(out_coords), _ptr(out_counts), _ptr(out_feats), _ptr(out_point_idx),
             _ptr(out_voxel_offsets), _ptr(workspace), workspace.numel() * workspace.element_size(),
             _stream(stream)]
+    if rho_out != 0.0 or seed != 0:
+        opt = mmbev_options_t(out_of_roi_keep_rate=float(rho_out), reserved=0, seed=int(seed) & ((1 << 64) - 1))
+        evs = events or []
+        handles = (ctypes.c_void_p * max(len(evs), 1))(*[int(e.cuda_event) for e in evs])
+        used = ctypes.c_int32(0)
+        _check(load().mmbev_roi_voxelize_ex(*args[:6], ctypes.byref(opt), *args[6:], handles if evs else None,
+                                            len(evs), ctypes.byref(used)), "mmbev_roi_voxelize_ex")
+        return int(used.value)
     if events is None:
         _check(load().mmbev_roi_voxelize(*args), "mmbev_roi_voxelize")
         return 0
@@ -169,7 +187,7 @@ class Voxelizer:
     """
 
     def __init__(self, feat, frame_offsets, sweep_ids, sweep_poses, rois, roi_frame_offsets, roi_sweep_budget,
-                 grid: mmbev_grid_t, max_rois_per_frame: int, device):
+                 grid: mmbev_grid_t, max_rois_per_frame: int, device, rho_out: float = 0.0, seed: int = 0):
         import torch
 
         self.device = torch.device(device)
@@ -189,6 +207,7 @@ class Voxelizer:
         self.roi_sweep_budget = up(roi_sweep_budget, torch.uint8)
         self.grid = grid
         self.max_rois = int(max_rois_per_frame)
+        self.rho_out, self.seed = float(rho_out), int(seed)
         B, cap, M, C = grid.num_frames, grid.max_voxels, grid.max_points, int(self.feat.shape[0])
         rows = B * cap
         self.out_coords = torch.full((rows, 4), -7, dtype=torch.int32, device=dev)
@@ -206,7 +225,7 @@ class Voxelizer:
         return roi_voxelize(self.feat, self.frame_offsets, self.sweep_ids, self.sweep_poses, self.rois,
                             self.roi_frame_offsets, self.roi_sweep_budget, self.grid, self.out_coords,
                             self.out_counts, self.out_feats, self.out_point_idx, self.out_voxel_offsets,
-                            self.workspace, self.max_rois, stream, events)
+                            self.workspace, self.max_rois, stream, events, self.rho_out, self.seed)
 
     def fault(self) -> int:
         """Device fault word of the last completed call (synchronises)."""
@@ -227,14 +246,14 @@ class Voxelizer:
                 "voxel_offsets": off}
 
 
-def voxelizer_for_workload(wl, device, rois=None) -> Voxelizer:
+def voxelizer_for_workload(wl, device, rois=None, rho_out: float = 0.0, seed: int = 0) -> Voxelizer:
     """A Voxelizer for a synth workload; ROI records from the library's mmbev_make_rois."""
     gr = wl.grid
     g = grid_params(gr.range_min, gr.voxel_size, gr.dims, gr.max_points, gr.max_voxels, gr.num_sweeps,
                     gr.num_frames)
     recs = make_rois(wl.roi_desc) if rois is None else rois
     return Voxelizer(wl.feat, wl.frame_offsets, wl.sweep_ids, wl.poses, recs, wl.roi_offsets, wl.budgets, g,
-                     max(wl.max_rois_per_frame, 1), device)
+                     max(wl.max_rois_per_frame, 1), device, rho_out, seed)
 
 
 def roi_voxelize_workload(wl, device) -> dict:

@@ -41,13 +41,13 @@ class Case:
         return oracle.make_grid(g["range_min"], g["voxel_size"], g["dims"], g["max_points"], g["max_voxels"],
                                 g["num_sweeps"], g["num_frames"])
 
-    def run_oracle(self):
+    def run_oracle(self, rho_out=0.0, seed=0):
         return oracle.roi_voxelize(self.feat, self.frame_offsets, self.sweep_ids, self.poses, self.rois,
-                                   self.roi_offsets, self.budgets, self.ogrid())
+                                   self.roi_offsets, self.budgets, self.ogrid(), rho_out, seed)
 
-    def oracle_keep(self):
+    def oracle_keep(self, rho_out=0.0, seed=0):
         return oracle.keep(self.feat, self.frame_offsets, self.sweep_ids, self.poses, self.rois,
-                           self.roi_offsets, self.budgets, self.ogrid())
+                           self.roi_offsets, self.budgets, self.ogrid(), rho_out, seed)
 
 
 def records(rows) -> np.ndarray:

@@ -38,7 +38,7 @@ def declared_functions():
 
 def test_header_declares_the_path():
     names = declared_functions()
-    for n in ["mmbev_roi_voxelize", "mmbev_roi_voxelize_workspace_bytes", "mmbev_make_rois",
+    for n in ["mmbev_roi_voxelize", "mmbev_roi_voxelize_ex", "mmbev_roi_voxelize_workspace_bytes", "mmbev_make_rois",
               "mmbev_workspace_init", "mmbev_abi_version", "mmbev_status_string"]:
         assert n in names
 
@@ -57,8 +57,9 @@ def test_struct_layouts_match_header(mb):
     assert ctypes.sizeof(mb.mmbev_points_t) == 40
     assert ctypes.sizeof(mb.mmbev_rois_t) == 24
     assert ctypes.sizeof(mb.mmbev_grid_t) == 52
+    assert ctypes.sizeof(mb.mmbev_options_t) == 16
     assert mb.ROI_DTYPE.itemsize == 32
-    assert mb.abi_version() == 2
+    assert mb.abi_version() == 3
 
 
 def test_make_rois_matches_oracle_bitwise(mb):
@@ -122,3 +123,22 @@ def test_voxelize_rejects_bad_arguments_before_any_launch(mb):
     too_many = mb.mmbev_rois_t(boxes=fake, frame_offsets=fake, num_rois=2, max_rois_per_frame=2000)
     assert call(rois=too_many) == mb.ERR_UNSUPPORTED
     assert mb.load().mmbev_status_string(mb.ERR_HIP) == b"HIP launch failed"
+
+
+def test_options_reserved_field_must_be_zero(mb):
+    L = mb.load()
+    g = mb.grid_params((-4, -4, -1), (0.5, 0.5, 0.5), (16, 16, 4), 2, 3, 2, 1)
+    fake = 1 << 40  # never dereferenced: validation fails first
+    pts = mb.mmbev_points_t(feat=fake, stride=100, num_features=4, reserved=0, num_points=100, frame_offsets=fake)
+    rr = mb.mmbev_rois_t(boxes=fake, frame_offsets=fake, num_rois=2, max_rois_per_frame=2)
+    ws_need = mb.roi_voxelize_workspace_bytes(g, 100, 4, 2)
+    used = ctypes.c_int32(0)
+
+    def call(opt, ws_bytes=ws_need):
+        return L.mmbev_roi_voxelize_ex(ctypes.byref(pts), fake, fake, ctypes.byref(rr), fake, ctypes.byref(g),
+                                       ctypes.byref(opt), *(fake,) * 5, fake, ws_bytes, None, None, 0,
+                                       ctypes.byref(used))
+
+    assert call(mb.mmbev_options_t(out_of_roi_keep_rate=0.5, reserved=1, seed=3)) == mb.ERR_INVALID_ARG
+    # a valid options block reaches the workspace check
+    assert call(mb.mmbev_options_t(out_of_roi_keep_rate=0.5, reserved=0, seed=3), ws_need - 1) == mb.ERR_WORKSPACE

@@ -16,24 +16,25 @@ pytestmark = pytest.mark.gpu
 FEAT_TOL = 1e-5
 
 
-def run_gpu(mb, case: Case, device="cuda:0", gpu_rois=None):
+def run_gpu(mb, case: Case, device="cuda:0", gpu_rois=None, rho_out=0.0, seed=0):
     """Run the HIP path; ROI records are the case's own (hand-made) or gpu_rois
-    (built by the library's mmbev_make_rois from the same descriptors)."""
+    (built by the library's mmbev_make_rois from the same descriptors).
+    rho_out, seed: the out-of-ROI keep rate and its seed."""
     g = case.grid
     grid = mb.grid_params(g["range_min"], g["voxel_size"], g["dims"], g["max_points"], g["max_voxels"],
                           g["num_sweeps"], g["num_frames"])
     mr = int(np.max(np.diff(case.roi_offsets))) if len(case.roi_offsets) > 1 else 0
     rois = case.rois if gpu_rois is None else gpu_rois
     vz = mb.Voxelizer(case.feat, case.frame_offsets, case.sweep_ids, case.poses, rois, case.roi_offsets,
-                      case.budgets, grid, max(mr, 1), device)
+                      case.budgets, grid, max(mr, 1), device, rho_out, seed)
     vz.run()
     return vz
 
 
-def check(mb, case: Case, label="", desc=None):
+def check(mb, case: Case, label="", desc=None, rho_out=0.0, seed=0):
     """Oracle vs GPU.  With `desc` (ROI descriptors) each side builds its own records."""
-    exp = case.run_oracle()
-    vz = run_gpu(mb, case, gpu_rois=None if desc is None else mb.make_rois(desc))
+    exp = case.run_oracle(rho_out, seed)
+    vz = run_gpu(mb, case, gpu_rois=None if desc is None else mb.make_rois(desc), rho_out=rho_out, seed=seed)
     got = vz.result()
     assert vz.fault() == 0, f"{label}: device fault {vz.fault()}"
     assert_same_voxels(got, exp, feat_atol=FEAT_TOL, label=label)

@@ -9,7 +9,8 @@ The arithmetic lives in ``oracle.c`` (plain C, single-threaded, built with
 definition it follows is spelled out in ``oracle.h``: Eq. 6/7 motion
 compensation, the Alg. 1 keep test against the Eq. 1 ROI union (with an
 optional out-of-ROI keep rate drawn from SplitMix64), quantisation, sort by (key, point index), max_points and
-max_voxels caps, and fp64 mean pooling.
+max_voxels caps, fp64 mean pooling, and the scatter of the voxel features into a
+dense bird's-eye-view map.
 """
 from __future__ import annotations
 
@@ -71,6 +72,8 @@ def lib() -> ctypes.CDLL:
         L.oracle_background_threshold.restype = ctypes.c_uint32
         L.oracle_background_keep.argtypes = [ctypes.c_uint64, ctypes.c_uint32, ctypes.c_int64]
         L.oracle_background_keep.restype = ctypes.c_int32
+        L.oracle_scatter_to_bev.argtypes = [p, p, p, ctypes.c_int32, ctypes.c_int32, p, p]
+        L.oracle_scatter_to_bev.restype = ctypes.c_int32
         _lib = L
     return _lib
 
@@ -183,3 +186,24 @@ def run_workload(wl, rho_out: float = 0.0, seed: int = 0):
     """Oracle output for a synth workload (records built by the oracle's own make_rois)."""
     return roi_voxelize(wl.feat, wl.frame_offsets, wl.sweep_ids, wl.poses, make_rois(wl.roi_desc),
                         wl.roi_offsets, wl.budgets, grid_of(wl), rho_out, seed)
+
+
+def scatter_to_bev(coords, feats, voxel_offsets, dims, num_frames: int) -> np.ndarray:
+    """ScatterToBEV (Alg. 1's return value; Sec. IV-F): the fp32 map
+    [num_frames][C*Dz][Dy][Dx] with map[b][c*Dz + iz][iy][ix] = feats[v][c]
+    for every voxel v = (b, iz, iy, ix) of frame b (rows voxel_offsets[b] ..
+    voxel_offsets[b+1]), zero elsewhere."""
+    coords = np.ascontiguousarray(coords, dtype=np.int32).reshape(-1, 4)
+    feats = np.ascontiguousarray(feats, dtype=np.float32)
+    feats = feats.reshape(len(coords), -1) if len(coords) else feats.reshape(0, max(feats.shape[-1], 1))
+    voff = np.ascontiguousarray(voxel_offsets, dtype=np.int64)
+    Dx, Dy, Dz = (int(d) for d in dims)
+    C = int(feats.shape[1])
+    d = np.array([Dx, Dy, Dz], dtype=np.int32)
+    out = np.empty((num_frames, C * Dz, Dy, Dx), dtype=np.float32)
+    L = lib()
+    rc = L.oracle_scatter_to_bev(coords.ctypes.data, feats.ctypes.data, voff.ctypes.data, num_frames, C,
+                                 d.ctypes.data, out.ctypes.data)
+    if rc != 0:
+        raise ValueError("oracle_scatter_to_bev: bad sizes or voxel coordinates")
+    return out

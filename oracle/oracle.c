@@ -268,3 +268,25 @@ int64_t oracle_roi_voxelize(const float* feat, int64_t stride, int32_t C, int64_
   return oracle_roi_voxelize_bg(feat, stride, C, N, frame_offsets, sweep_ids, poses, rois, roi_offsets, budgets,
                                 g, 0.0f, 0, out_coords, out_counts, out_feats, out_point_idx, out_voxel_offsets);
 }
+
+/* Step 8 (ScatterToBEV, Alg. 1; Sec. IV-F): clear the map, then one store
+ * per voxel and feature at its coordinate, the height index folded into the
+ * channel as c*Dz + iz. */
+int32_t oracle_scatter_to_bev(const int32_t* coords, const float* feats, const int64_t* voxel_offsets,
+                              int32_t B, int32_t C, const int32_t* dims, float* map) {
+  if (B < 1 || C < 1 || dims[0] < 1 || dims[1] < 1 || dims[2] < 1) return -1;
+  const int64_t Dx = dims[0], Dy = dims[1], Dz = dims[2];
+  const int64_t total = (int64_t)B * C * Dz * Dy * Dx;
+  for (int64_t e = 0; e < total; ++e) map[e] = 0.0f;
+  for (int32_t b = 0; b < B; ++b) {
+    for (int64_t v = voxel_offsets[b]; v < voxel_offsets[b + 1]; ++v) {
+      const int32_t* q = coords + 4 * v;
+      if (q[0] != b || q[1] < 0 || q[1] >= Dz || q[2] < 0 || q[2] >= Dy || q[3] < 0 || q[3] >= Dx) return -1;
+      for (int32_t c = 0; c < C; ++c) {
+        const int64_t channel = (int64_t)c * Dz + q[1];
+        map[(((int64_t)b * C * Dz + channel) * Dy + q[2]) * Dx + q[3]] = feats[v * C + c];
+      }
+    }
+  }
+  return 0;
+}

@@ -32,7 +32,12 @@
  *   7. each voxel's feature c is the mean over its kept points of p'_c
  *      (c < 3) or of the raw column c (c >= 3), summed in double in
  *      ascending point order and rounded once to fp32 (Alg. 1 "VoxelFeature-
- *      Encoder" read as mean pooling).
+ *      Encoder" read as mean pooling);
+ *   8. ScatterToBEV (Alg. 1's return value; Sec. IV-F: the features are
+ *      written into a zero-initialised bird's-eye-view map by voxel
+ *      coordinate, the map having the shape a dense pipeline would produce):
+ *      the height axis becomes channels, map[b][c*Dz + iz][iy][ix] = feature
+ *      c of voxel (b, iz, iy, ix), 0 where no voxel lies.
  *
  * Build: plain C, -O2 -ffp-contract=off, no fast-math.
  */
@@ -115,6 +120,14 @@ int64_t oracle_roi_voxelize(const float* feat, int64_t stride, int32_t num_featu
                             const oracle_roi* rois, const int32_t* roi_offsets, const uint8_t* budgets,
                             const oracle_grid* g, int32_t* out_coords, int32_t* out_counts,
                             float* out_feats, int32_t* out_point_idx, int64_t* out_voxel_offsets);
+
+/* Step 8: the BEV map [num_frames][C*Dz][Dy][Dx] (fp32, every element
+ * written) from voxels as returned by the whole path (frame b's voxels are
+ * rows [voxel_offsets[b], voxel_offsets[b+1])).  Returns 0, or -1 on a bad
+ * argument (sizes, or a voxel whose coordinates lie outside the grid or
+ * name another frame). */
+int32_t oracle_scatter_to_bev(const int32_t* coords, const float* feats, const int64_t* voxel_offsets,
+                              int32_t num_frames, int32_t num_features, const int32_t* dims, float* map);
 
 #ifdef __cplusplus
 }

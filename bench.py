@@ -122,6 +122,43 @@ def probe_traffic(frames: int) -> int:
     return 0
 
 
+def time_scatter(wl, dev, steps: int, warmup: int) -> dict:
+    """ScatterToBEV (mmbev_scatter_to_bev) of one voxelised workload, timed
+    with HIP events around `steps` calls; algorithmic bytes = the map written
+    once + the voxel rows read (coords 16 B + C features) + the offsets."""
+    import torch
+
+    from paper_2608_15437_amd import mmbev
+
+    vz = mmbev.voxelizer_for_workload(wl, dev)
+    vz.run()
+    V = vz.header()["voxels"]
+    C = wl.num_features
+    bev_map = torch.empty(mmbev.bev_map_shape(vz.grid, C), dtype=torch.float32, device=dev)
+    for _ in range(warmup):
+        vz.scatter_to_bev(bev_map)
+    torch.cuda.synchronize()
+    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    a.record()
+    for _ in range(steps):
+        vz.scatter_to_bev(bev_map)
+    b.record()
+    torch.cuda.synchronize()
+    us = a.elapsed_time(b) / steps * 1e3
+    map_bytes = bev_map.numel() * 4
+    alg = map_bytes + V * (16 + 4 * C) + 8 * (wl.num_frames + 1)
+    gbs = alg / (us * 1e-6) / 1e9
+    out = {"workload": f"{wl.num_frames} frames, {wl.grid.dims[0]}x{wl.grid.dims[1]}x{wl.grid.dims[2]} grid, "
+                       f"C={C}: map [B][C*Dz][Dy][Dx] fp32",
+           "voxels": V, "map_bytes": map_bytes, "us_per_call": round(us, 1),
+           "roofline": {"bound": "hbm", "achieved": round(gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                        "frac": round(gbs / HBM_PEAK_GBS, 4), "traffic": None,
+                        "kernel": "bev_clear4_kernel + bev_values_kernel", "alg_bytes_per_call": alg}}
+    del bev_map, vz
+    torch.cuda.empty_cache()
+    return out
+
+
 def counter_values(run_dir: str, counter: str) -> dict:
     """Per-dispatch values (KiB) of one counter, per kernel name, from a rocprofv3 csv run."""
     import csv
@@ -237,6 +274,9 @@ def main() -> int:
     vz1 = mmbev.voxelizer_for_workload(wl1, dev)
     us1 = time_calls(vz1, max(args.steps, 20), args.warmup) * 1e3
 
+    log("[bench] ScatterToBEV of the 8-frame 2160x2160x40 workload (29.9 GB map)")
+    bev = time_scatter(synth.c5(), dev, args.steps, args.warmup)
+
     cpu = None
     if not args.no_cpu_baseline:
         import oracle
@@ -283,6 +323,7 @@ def main() -> int:
         "launch_us": {k: round(v, 2) for k, v in per.items()},
         "single_frame": {"points": wl1.num_points, "us_per_call": round(us1, 2),
                          "mpoints_s": round(wl1.num_points / (us1 * 1e-6) / 1e6, 1)},
+        "scatter_to_bev": bev,
         "cpu_baseline": cpu,
     }
     print(json.dumps(out), flush=True)

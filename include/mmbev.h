@@ -60,7 +60,7 @@
 extern "C" {
 #endif
 
-#define MMBEV_ABI_VERSION 3
+#define MMBEV_ABI_VERSION 4
 
 /* ------------------------------------------------------------- status */
 typedef int32_t mmbev_status_t;
@@ -78,6 +78,9 @@ typedef int32_t mmbev_status_t;
 #define MMBEV_FAULT_ROI_OFFSETS 2   /* ROI frame offsets not 0 .. num_rois, non-decreasing,
                                        or a frame with more than max_rois_per_frame ROIs */
 #define MMBEV_FAULT_INTERNAL 4      /* an internal consistency check failed (never with valid inputs) */
+#define MMBEV_FAULT_VOXELS 8        /* mmbev_scatter_to_bev: voxel rows break its contract (offsets,
+                                       coordinates outside the grid or of another frame, keys not
+                                       strictly ascending inside a frame) */
 
 /* ------------------------------------------------------------- inputs */
 
@@ -230,6 +233,42 @@ mmbev_status_t mmbev_roi_voxelize_ex(const mmbev_points_t* points, const uint8_t
                                      float* out_feats, int32_t* out_point_idx, int64_t* out_voxel_offsets,
                                      void* workspace, size_t workspace_bytes, void* stream, void* const* events,
                                      int32_t num_events, int32_t* events_recorded);
+
+/* ------------------------------------------------ ScatterToBEV (Alg. 1) */
+
+/*
+ * Write voxel features into a dense bird's-eye-view map (Alg. 1's return
+ * value, "ScatterToBEV"; Sec. IV-F: features go into a zero-initialised BEV
+ * map by voxel coordinate, the map having the shape a dense pipeline would
+ * produce).  The height axis is folded into channels:
+ *   bev_map[b][c*Dz + iz][iy][ix] = feats[v][c]   for every voxel v of frame b
+ *                                                 with coords[v] = (b, iz, iy, ix),
+ *   0.0f everywhere else                          (Dz = 1: the pillar map [B][C][Dy][Dx]).
+ *
+ * coords         int32 [rows][4], device, 16-byte aligned
+ * feats          fp32  [rows][num_features], device
+ * voxel_offsets  int64 [num_frames+1], device: frame b's voxels are rows
+ *                [off[b], off[b+1]); rows = num_frames * max_voxels
+ *                These are exactly the outputs of mmbev_roi_voxelize: inside
+ *                a frame the keys (iz*Dy + iy)*Dx + ix are strictly ascending.
+ * num_features   C, 1..64
+ * grid           dims, max_voxels and num_frames are read (host struct)
+ * bev_map        fp32 [num_frames][C*Dz][Dy][Dx], device; every element is
+ *                written (no clearing needed beforehand)
+ * fault          device int32, may be NULL.  If given, the rows are checked
+ *                and MMBEV_FAULT_VOXELS is ORed into it when they break the
+ *                contract above (the caller clears it); the map is then
+ *                unspecified.  Whatever the rows hold, no access leaves the
+ *                buffers described here.
+ *
+ * Ownership and errors as for mmbev_roi_voxelize: caller-owned buffers, no
+ * allocation, work enqueued on `stream` (NULL = default stream) without
+ * waiting; argument errors return MMBEV_ERR_INVALID_ARG or
+ * MMBEV_ERR_UNSUPPORTED before anything is enqueued.
+ */
+mmbev_status_t mmbev_scatter_to_bev(const int32_t* coords, const float* feats, const int64_t* voxel_offsets,
+                                    int32_t num_features, const mmbev_grid_t* grid, float* bev_map,
+                                    int32_t* fault, void* stream);
 
 #ifdef __cplusplus
 }

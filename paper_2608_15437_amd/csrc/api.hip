@@ -377,4 +377,34 @@ mmbev_status_t mmbev_roi_voxelize_ex(const mmbev_points_t* points, const uint8_t
   return st;
 }
 
+mmbev_status_t mmbev_scatter_to_bev(const int32_t* coords, const float* feats, const int64_t* voxel_offsets,
+                                    int32_t num_features, const mmbev_grid_t* grid, float* bev_map,
+                                    int32_t* fault, void* stream) {
+  if (!grid || !coords || !feats || !voxel_offsets || !bev_map) return MMBEV_ERR_INVALID_ARG;
+  if (((uintptr_t)coords & 15) != 0) return MMBEV_ERR_INVALID_ARG;
+  if (num_features < 1 || num_features > 64) return MMBEV_ERR_INVALID_ARG;
+  for (int d = 0; d < 3; ++d)
+    if (grid->dims[d] < 1 || grid->dims[d] >= (1 << 24)) return MMBEV_ERR_INVALID_ARG;
+  if (grid->max_voxels < 1 || grid->num_frames < 1 || grid->num_frames > 65535) return MMBEV_ERR_INVALID_ARG;
+  const uint64_t plane = (uint64_t)grid->dims[0] * (uint64_t)grid->dims[1];
+  if (plane * (uint64_t)grid->dims[2] > ((uint64_t)1 << 32)) return MMBEV_ERR_UNSUPPORTED;
+  if ((uint64_t)grid->num_frames * (uint64_t)grid->max_voxels > (uint64_t)INT32_MAX) return MMBEV_ERR_UNSUPPORTED;
+  BevConfig c{};
+  c.coords = reinterpret_cast<const int4*>(coords);
+  c.feats = feats;
+  c.voff = voxel_offsets;
+  c.map = bev_map;
+  c.fault = fault;
+  c.rows = (int64_t)grid->num_frames * grid->max_voxels;
+  c.plane = plane;
+  c.Dx = (uint32_t)grid->dims[0];
+  c.Dy = (uint32_t)grid->dims[1];
+  c.Dz = (uint32_t)grid->dims[2];
+  c.B = grid->num_frames;
+  c.C = num_features;
+  c.max_voxels = grid->max_voxels;
+  c.vec = ((uintptr_t)bev_map & 15) == 0;
+  return launch_bev(c, (hipStream_t)stream) == hipSuccess ? MMBEV_OK : MMBEV_ERR_HIP;
+}
+
 }  // extern "C"

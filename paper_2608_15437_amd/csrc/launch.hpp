@@ -19,4 +19,20 @@ hipError_t launch_cap(const Config& c, const uint32_t* vals, hipStream_t st);
 hipError_t launch_mean(const Config& c, const uint32_t* keys, const uint32_t* vals, hipStream_t st);
 hipError_t launch_fill_zero(void* p, size_t bytes, hipStream_t st);
 
+// ScatterToBEV: a clear of the whole map, then the voxels' values.
+struct BevConfig {
+  const int4* coords;    // [rows] (b, iz, iy, ix)
+  const float* feats;    // [rows][C]
+  const int64_t* voff;   // [B+1]
+  float* map;            // [B][C*Dz][Dy][Dx]
+  int32_t* fault;        // MMBEV_FAULT_VOXELS is ORed in; null: no contract checks
+  int64_t rows;          // rows the voxel arrays hold: B * max_voxels
+  uint64_t plane;        // Dx * Dy
+  uint32_t Dx, Dy, Dz;
+  int32_t B, C, max_voxels;
+  int32_t vec;           // the map is 16-byte aligned: the clear uses 16-byte stores
+};
+
+hipError_t launch_bev(const BevConfig& c, hipStream_t st);
+
 }  // namespace mmbev

@@ -16,7 +16,7 @@ _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libmmbev.so")
 
 OK, ERR_INVALID_ARG, ERR_WORKSPACE, ERR_UNSUPPORTED, ERR_HIP = 0, -1, -2, -3, -4
-FAULT_POINT_OFFSETS, FAULT_ROI_OFFSETS, FAULT_INTERNAL = 1, 2, 4
+FAULT_POINT_OFFSETS, FAULT_ROI_OFFSETS, FAULT_INTERNAL, FAULT_VOXELS = 1, 2, 4, 8
 
 ROI_DTYPE = np.dtype([("cx", "<f4"), ("cy", "<f4"), ("cos_yaw", "<f4"), ("sin_yaw", "<f4"),
                       ("ext_x", "<f4"), ("ext_y", "<f4"), ("reserved0", "<f4"), ("reserved1", "<f4")])
@@ -76,6 +76,8 @@ def load() -> ctypes.CDLL:
         a = L.mmbev_roi_voxelize.argtypes
         L.mmbev_roi_voxelize_ex.argtypes = a[:6] + [ctypes.POINTER(mmbev_options_t)] + a[6:] + [p, ctypes.c_int32, p]
         L.mmbev_roi_voxelize_ex.restype = ctypes.c_int32
+        L.mmbev_scatter_to_bev.argtypes = [p, p, p, ctypes.c_int32, ctypes.POINTER(mmbev_grid_t), p, p, p]
+        L.mmbev_scatter_to_bev.restype = ctypes.c_int32
         _lib = L
     return _lib
 
@@ -179,6 +181,29 @@ def roi_voxelize(feat, frame_offsets, sweep_ids, sweep_poses, rois, roi_frame_of
     return int(used.value)
 
 
+def bev_map_shape(grid: mmbev_grid_t, num_features: int) -> tuple:
+    """Shape of the ScatterToBEV map: [num_frames][C*Dz][Dy][Dx]."""
+    Dx, Dy, Dz = grid.dims[0], grid.dims[1], grid.dims[2]
+    return (grid.num_frames, int(num_features) * Dz, Dy, Dx)
+
+
+def scatter_to_bev(coords, feats, voxel_offsets, grid: mmbev_grid_t, bev_map, fault=None, stream=None) -> None:
+    """Enqueue mmbev_scatter_to_bev on `stream` (torch tensors on the GPU).
+
+    coords int32 [rows][4], feats fp32 [rows][C], voxel_offsets int64 [B+1]
+    (as written by mmbev_roi_voxelize); bev_map fp32 of bev_map_shape(grid, C),
+    every element written; fault: optional int32 tensor of one element that
+    receives MMBEV_FAULT_VOXELS when the rows break the contract.
+    """
+    C = int(feats.shape[1])
+    if tuple(bev_map.shape) != bev_map_shape(grid, C) or not bev_map.is_contiguous():
+        raise MmbevError(f"bev_map must be a contiguous tensor of shape {bev_map_shape(grid, C)}")
+    if not (coords.is_contiguous() and feats.is_contiguous()):
+        raise MmbevError("coords and feats must be contiguous")
+    _check(load().mmbev_scatter_to_bev(_ptr(coords), _ptr(feats), _ptr(voxel_offsets), C, ctypes.byref(grid),
+                                       _ptr(bev_map), _ptr(fault), _stream(stream)), "mmbev_scatter_to_bev")
+
+
 class Voxelizer:
     """Owns device inputs, outputs and workspace for repeated calls on one batch shape.
 
@@ -226,6 +251,16 @@ class Voxelizer:
                             self.roi_frame_offsets, self.roi_sweep_budget, self.grid, self.out_coords,
                             self.out_counts, self.out_feats, self.out_point_idx, self.out_voxel_offsets,
                             self.workspace, self.max_rois, stream, events, self.rho_out, self.seed)
+
+    def scatter_to_bev(self, bev_map=None, fault=None, stream=None):
+        """ScatterToBEV of this Voxelizer's outputs into bev_map (allocated when None); returns the map."""
+        import torch
+
+        if bev_map is None:
+            bev_map = torch.empty(bev_map_shape(self.grid, self.out_feats.shape[1]), dtype=torch.float32,
+                                  device=self.device)
+        scatter_to_bev(self.out_coords, self.out_feats, self.out_voxel_offsets, self.grid, bev_map, fault, stream)
+        return bev_map
 
     def fault(self) -> int:
         """Device fault word of the last completed call (synchronises)."""

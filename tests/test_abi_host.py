@@ -38,7 +38,8 @@ def declared_functions():
 
 def test_header_declares_the_path():
     names = declared_functions()
-    for n in ["mmbev_roi_voxelize", "mmbev_roi_voxelize_ex", "mmbev_roi_voxelize_workspace_bytes", "mmbev_make_rois",
+    for n in ["mmbev_roi_voxelize", "mmbev_roi_voxelize_ex", "mmbev_scatter_to_bev",
+              "mmbev_roi_voxelize_workspace_bytes", "mmbev_make_rois",
               "mmbev_workspace_init", "mmbev_abi_version", "mmbev_status_string"]:
         assert n in names
 
@@ -59,7 +60,7 @@ def test_struct_layouts_match_header(mb):
     assert ctypes.sizeof(mb.mmbev_grid_t) == 52
     assert ctypes.sizeof(mb.mmbev_options_t) == 16
     assert mb.ROI_DTYPE.itemsize == 32
-    assert mb.abi_version() == 3
+    assert mb.abi_version() == 4
 
 
 def test_make_rois_matches_oracle_bitwise(mb):
@@ -142,3 +143,24 @@ def test_options_reserved_field_must_be_zero(mb):
     assert call(mb.mmbev_options_t(out_of_roi_keep_rate=0.5, reserved=1, seed=3)) == mb.ERR_INVALID_ARG
     # a valid options block reaches the workspace check
     assert call(mb.mmbev_options_t(out_of_roi_keep_rate=0.5, reserved=0, seed=3), ws_need - 1) == mb.ERR_WORKSPACE
+
+
+def test_scatter_to_bev_rejects_bad_arguments_before_any_launch(mb):
+    L = mb.load()
+    g = mb.grid_params((-4, -4, -1), (0.5, 0.5, 0.5), (16, 16, 4), 2, 3, 2, 1)
+    fake = 1 << 40  # never dereferenced: validation fails first
+
+    def call(coords=fake, feats=fake, voff=fake, C=5, grid=g, out=fake):
+        return L.mmbev_scatter_to_bev(coords, feats, voff, C, ctypes.byref(grid), out, None, None)
+
+    assert call(coords=None) == mb.ERR_INVALID_ARG
+    assert call(feats=None) == mb.ERR_INVALID_ARG
+    assert call(voff=None) == mb.ERR_INVALID_ARG
+    assert call(out=None) == mb.ERR_INVALID_ARG
+    assert call(coords=fake + 4) == mb.ERR_INVALID_ARG  # int4 rows need 16-byte alignment
+    assert call(C=0) == mb.ERR_INVALID_ARG
+    assert call(C=65) == mb.ERR_INVALID_ARG
+    bad = mb.grid_params((-4, -4, -1), (0.5, 0.5, 0.5), (16, 0, 4), 2, 3, 2, 1)
+    assert call(grid=bad) == mb.ERR_INVALID_ARG
+    huge = mb.grid_params((-4, -4, -1), (0.5, 0.5, 0.5), (1 << 16, 1 << 16, 2), 2, 3, 2, 1)
+    assert call(grid=huge) == mb.ERR_UNSUPPORTED

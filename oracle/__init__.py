@@ -9,8 +9,8 @@ The arithmetic lives in ``oracle.c`` (plain C, single-threaded, built with
 definition it follows is spelled out in ``oracle.h``: Eq. 6/7 motion
 compensation, the Alg. 1 keep test against the Eq. 1 ROI union (with an
 optional out-of-ROI keep rate drawn from SplitMix64), quantisation, sort by (key, point index), max_points and
-max_voxels caps, fp64 mean pooling, and the scatter of the voxel features into a
-dense bird's-eye-view map.
+max_voxels caps, fp64 mean pooling, the scatter of the voxel features into a
+dense bird's-eye-view map, and the voxel-grid connected-component proposer.
 """
 from __future__ import annotations
 
@@ -74,6 +74,8 @@ def lib() -> ctypes.CDLL:
         L.oracle_background_keep.restype = ctypes.c_int32
         L.oracle_scatter_to_bev.argtypes = [p, p, p, ctypes.c_int32, ctypes.c_int32, p, p]
         L.oracle_scatter_to_bev.restype = ctypes.c_int32
+        L.oracle_clusters.argtypes = [p, p, p, ctypes.c_int32, p, p, p, p, p]
+        L.oracle_clusters.restype = ctypes.c_int64
         _lib = L
     return _lib
 
@@ -207,3 +209,37 @@ def scatter_to_bev(coords, feats, voxel_offsets, dims, num_frames: int) -> np.nd
     if rc != 0:
         raise ValueError("oracle_scatter_to_bev: bad sizes or voxel coordinates")
     return out
+
+
+CLUSTER_DTYPE = np.dtype([("frame", "<i4"), ("root", "<i4"), ("cells", "<i4"), ("voxels", "<i4"), ("points", "<i4"),
+                          ("x0", "<i4"), ("y0", "<i4"), ("x1", "<i4"), ("y1", "<i4"), ("unused", "<i4"),
+                          ("sum_x", "<i8"), ("sum_y", "<i8")])
+
+
+class OracleCCParams(ctypes.Structure):
+    _fields_ = [("z_min", ctypes.c_int32), ("z_max", ctypes.c_int32), ("cell_shift", ctypes.c_int32),
+                ("connectivity", ctypes.c_int32), ("min_cells", ctypes.c_int32), ("reserved", ctypes.c_int32)]
+
+
+def clusters(coords, counts, voxel_offsets, dims, num_frames: int, z_min: int, z_max: int, cell_shift: int = 0,
+             connectivity: int = 8, min_cells: int = 1) -> dict:
+    """The voxel-grid connected-component proposer (robot deployment, Sec. VI):
+    connected components (4- or 8-neighbourhood) of the bird's-eye-view
+    cells (ix >> s, iy >> s) holding a voxel of a layer in [z_min, z_max),
+    at least min_cells cells each, per frame in order of their smallest cell
+    index.  Returns the clusters (CLUSTER_DTYPE), cluster_offsets [B+1] and
+    voxel_labels (cluster index per voxel row, -1 if none)."""
+    coords = np.ascontiguousarray(coords, dtype=np.int32).reshape(-1, 4)
+    counts = np.ascontiguousarray(counts, dtype=np.int32)
+    voff = np.ascontiguousarray(voxel_offsets, dtype=np.int64)
+    d = np.array([int(x) for x in dims], dtype=np.int32)
+    prm = OracleCCParams(int(z_min), int(z_max), int(cell_shift), int(connectivity), int(min_cells), 0)
+    rows = max(len(coords), 1)
+    out = np.zeros(rows, dtype=CLUSTER_DTYPE)
+    coff = np.zeros(num_frames + 1, dtype=np.int64)
+    labels = np.full(rows, -1, dtype=np.int32)
+    n = lib().oracle_clusters(coords.ctypes.data, counts.ctypes.data, voff.ctypes.data, num_frames, d.ctypes.data,
+                              ctypes.byref(prm), out.ctypes.data, coff.ctypes.data, labels.ctypes.data)
+    if n < 0:
+        raise ValueError("oracle_clusters: bad arguments or voxel coordinates")
+    return {"clusters": out[:n], "cluster_offsets": coff, "voxel_labels": labels[:len(coords)]}

@@ -290,3 +290,109 @@ int32_t oracle_scatter_to_bev(const int32_t* coords, const float* feats, const i
   }
   return 0;
 }
+
+/* Step 9: per frame, occupied cells from the voxels in the layer band, then
+ * a flood fill from every unlabelled occupied cell in ascending cell order;
+ * the cell a fill starts from is the smallest of its component (every
+ * smaller occupied cell was labelled by an earlier fill). */
+int64_t oracle_clusters(const int32_t* coords, const int32_t* counts, const int64_t* voxel_offsets, int32_t B,
+                        const int32_t* dims, const oracle_cc_params* p, oracle_cluster* out,
+                        int64_t* cluster_offsets, int32_t* voxel_labels) {
+  if (B < 1 || dims[0] < 1 || dims[1] < 1 || dims[2] < 1) return -1;
+  if (p->cell_shift < 0 || p->cell_shift > 8 || p->min_cells < 1) return -1;
+  if (p->connectivity != 4 && p->connectivity != 8) return -1;
+  const int64_t Wx = ((int64_t)dims[0] + (1 << p->cell_shift) - 1) >> p->cell_shift;
+  const int64_t Wy = ((int64_t)dims[1] + (1 << p->cell_shift) - 1) >> p->cell_shift;
+  const int64_t ncell = Wx * Wy;
+  static const int dx8[8] = {-1, 1, 0, 0, -1, 1, -1, 1}, dy8[8] = {0, 0, -1, 1, -1, -1, 1, 1};
+  const int nn = p->connectivity;
+  uint8_t* occ = (uint8_t*)malloc((size_t)ncell);
+  int32_t* comp = (int32_t*)malloc(sizeof(int32_t) * (size_t)ncell);
+  int64_t* stack = (int64_t*)malloc(sizeof(int64_t) * (size_t)ncell);
+  int64_t total = 0;
+  cluster_offsets[0] = 0;
+  for (int32_t b = 0; b < B; ++b) {
+    const int64_t v0 = voxel_offsets[b], v1 = voxel_offsets[b + 1];
+    memset(occ, 0, (size_t)ncell);
+    for (int64_t c = 0; c < ncell; ++c) comp[c] = -1;
+    for (int64_t v = v0; v < v1; ++v) {
+      const int32_t* q = coords + 4 * v;
+      if (q[0] != b || q[1] < 0 || q[1] >= dims[2] || q[2] < 0 || q[2] >= dims[1] || q[3] < 0 || q[3] >= dims[0]) {
+        free(occ);
+        free(comp);
+        free(stack);
+        return -1;
+      }
+      if (q[1] >= p->z_min && q[1] < p->z_max) occ[(int64_t)(q[2] >> p->cell_shift) * Wx + (q[3] >> p->cell_shift)] = 1;
+    }
+    /* flood fill: components numbered in order of their smallest cell */
+    int64_t ncomp = 0;
+    for (int64_t c = 0; c < ncell; ++c) {
+      if (!occ[c] || comp[c] >= 0) continue;
+      int64_t top = 0;
+      stack[top++] = c;
+      comp[c] = (int32_t)ncomp;
+      while (top > 0) {
+        const int64_t u = stack[--top];
+        const int64_t ux = u % Wx, uy = u / Wx;
+        for (int k = 0; k < nn; ++k) {
+          const int64_t x = ux + dx8[k], y = uy + dy8[k];
+          if (x < 0 || x >= Wx || y < 0 || y >= Wy) continue;
+          const int64_t n = y * Wx + x;
+          if (occ[n] && comp[n] < 0) {
+            comp[n] = (int32_t)ncomp;
+            stack[top++] = n;
+          }
+        }
+      }
+      ++ncomp;
+    }
+    /* per-component cell statistics; kept components get their output index */
+    int64_t* size = (int64_t*)calloc((size_t)(ncomp > 0 ? ncomp : 1), sizeof(int64_t));
+    int64_t* idx = (int64_t*)malloc(sizeof(int64_t) * (size_t)(ncomp > 0 ? ncomp : 1));
+    for (int64_t c = 0; c < ncell; ++c)
+      if (comp[c] >= 0) size[comp[c]] += 1;
+    int64_t kept = 0;
+    for (int64_t k = 0; k < ncomp; ++k) idx[k] = size[k] >= p->min_cells ? total + kept++ : -1;
+    for (int64_t k = 0; k < ncomp; ++k) {
+      if (idx[k] < 0) continue;
+      oracle_cluster* o = &out[idx[k]];
+      memset(o, 0, sizeof(*o));
+      o->frame = b;
+      o->root = -1;
+      o->x0 = o->y0 = INT32_MAX;
+      o->x1 = o->y1 = -1;
+    }
+    for (int64_t c = 0; c < ncell; ++c) {
+      if (comp[c] < 0 || idx[comp[c]] < 0) continue;
+      oracle_cluster* o = &out[idx[comp[c]]];
+      const int32_t x = (int32_t)(c % Wx), y = (int32_t)(c / Wx);
+      if (o->root < 0) o->root = (int32_t)c;
+      o->cells += 1;
+      if (x < o->x0) o->x0 = x;
+      if (y < o->y0) o->y0 = y;
+      if (x > o->x1) o->x1 = x;
+      if (y > o->y1) o->y1 = y;
+      o->sum_x += x;
+      o->sum_y += y;
+    }
+    for (int64_t v = v0; v < v1; ++v) {
+      const int32_t* q = coords + 4 * v;
+      voxel_labels[v] = -1;
+      if (q[1] < p->z_min || q[1] >= p->z_max) continue;
+      const int32_t k = comp[(int64_t)(q[2] >> p->cell_shift) * Wx + (q[3] >> p->cell_shift)];
+      if (idx[k] < 0) continue;
+      voxel_labels[v] = (int32_t)idx[k];
+      out[idx[k]].voxels += 1;
+      out[idx[k]].points += counts[v];
+    }
+    total += kept;
+    cluster_offsets[b + 1] = total;
+    free(idx);
+    free(size);
+  }
+  free(occ);
+  free(comp);
+  free(stack);
+  return total;
+}

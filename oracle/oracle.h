@@ -37,7 +37,15 @@
  *      written into a zero-initialised bird's-eye-view map by voxel
  *      coordinate, the map having the shape a dense pipeline would produce):
  *      the height axis becomes channels, map[b][c*Dz + iz][iy][ix] = feature
- *      c of voxel (b, iz, iy, ix), 0 where no voxel lies.
+ *      c of voxel (b, iz, iy, ix), 0 where no voxel lies;
+ *   9. the voxel-grid connected-component proposer (robot deployment,
+ *      Sec. VI: object clusters found on the voxel grid): in each frame a
+ *      bird's-eye-view cell (x, y) = (ix >> s, iy >> s) is occupied when a
+ *      voxel of a layer iz in [z_min, z_max) lies in it; clusters are the
+ *      connected components of the occupied cells (4- or 8-neighbourhood)
+ *      with at least min_cells cells, listed per frame by their smallest
+ *      cell index y*Wx + x (Wx = ceil(Dx / 2^s)), found here by flood fill
+ *      in ascending cell order.
  *
  * Build: plain C, -O2 -ffp-contract=off, no fast-math.
  */
@@ -128,6 +136,33 @@ int64_t oracle_roi_voxelize(const float* feat, int64_t stride, int32_t num_featu
  * name another frame). */
 int32_t oracle_scatter_to_bev(const int32_t* coords, const float* feats, const int64_t* voxel_offsets,
                               int32_t num_frames, int32_t num_features, const int32_t* dims, float* map);
+
+/* Step 9 parameters. */
+typedef struct {
+  int32_t z_min, z_max;  /* voxel layers iz in [z_min, z_max) count */
+  int32_t cell_shift;    /* s: a cell is 2^s x 2^s voxel columns, 0..8 */
+  int32_t connectivity;  /* 4 or 8 */
+  int32_t min_cells;     /* smaller components are not clusters, >= 1 */
+  int32_t reserved;
+} oracle_cc_params;
+
+/* One cluster: 56 bytes. */
+typedef struct {
+  int32_t frame;
+  int32_t root;                   /* smallest cell index y*Wx + x of the cluster */
+  int32_t cells, voxels, points;  /* occupied cells; voxels in the layers; their kept points */
+  int32_t x0, y0, x1, y1;         /* bounding box in cells, inclusive */
+  int32_t unused;
+  int64_t sum_x, sum_y;           /* sums of the cells' x and y */
+} oracle_cluster;
+
+/* Step 9 over voxels as returned by the whole path.  out must hold one
+ * entry per voxel row, cluster_offsets num_frames + 1, voxel_labels one per
+ * row (the cluster's index in out, or -1).  Returns the number of clusters,
+ * or -1 on a bad argument. */
+int64_t oracle_clusters(const int32_t* coords, const int32_t* counts, const int64_t* voxel_offsets,
+                        int32_t num_frames, const int32_t* dims, const oracle_cc_params* p,
+                        oracle_cluster* out, int64_t* cluster_offsets, int32_t* voxel_labels);
 
 #ifdef __cplusplus
 }

@@ -159,6 +159,36 @@ def time_scatter(wl, dev, steps: int, warmup: int) -> dict:
     return out
 
 
+def time_clusters(vz, steps: int, warmup: int, ouster: bool = False) -> dict:
+    """The connected-component proposer (mmbev_voxel_clusters) over a
+    Voxelizer's outputs: layers 0.4-4.4 m above the ground plane (above 1.0 m
+    below the sensor for the Ouster grid), cells of one voxel column,
+    8-neighbourhood, clusters of at least 2 cells; HIP events around `steps`
+    calls."""
+    import torch
+
+    from paper_2608_15437_amd import mmbev
+
+    vz.run()
+    band = (12, 40) if ouster else (18, 40)
+    prm = mmbev.cluster_params(band[0], band[1], 0, 8, 2)
+    p = vz.clusters(prm)
+    for _ in range(warmup):
+        vz.clusters(prm, proposer=p)
+    torch.cuda.synchronize()
+    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    a.record()
+    for _ in range(steps):
+        vz.clusters(prm, proposer=p)
+    b.record()
+    torch.cuda.synchronize()
+    us = a.elapsed_time(b) / steps * 1e3
+    g = vz.grid
+    return {"frames": g.num_frames, "grid": [g.dims[0], g.dims[1], g.dims[2]], "voxels": vz.header()["voxels"],
+            "clusters": int(p.offsets[-1].item()), "layers": list(band), "us_per_call": round(us, 1),
+            "us_per_frame": round(us / g.num_frames, 2), "fault": p.fault()}
+
+
 def counter_values(run_dir: str, counter: str) -> dict:
     """Per-dispatch values (KiB) of one counter, per kernel name, from a rocprofv3 csv run."""
     import csv
@@ -274,6 +304,11 @@ def main() -> int:
     vz1 = mmbev.voxelizer_for_workload(wl1, dev)
     us1 = time_calls(vz1, max(args.steps, 20), args.warmup) * 1e3
 
+    log("[bench] connected-component proposer on the batch's voxels")
+    clusters = time_clusters(vz, args.steps, args.warmup)
+    log("[bench] connected-component proposer on one Ouster-shaped frame")
+    clusters1 = time_clusters(mmbev.voxelizer_for_workload(synth.c4(), dev), args.steps, args.warmup, ouster=True)
+
     log("[bench] ScatterToBEV of the 8-frame 2160x2160x40 workload (29.9 GB map)")
     bev = time_scatter(synth.c5(), dev, args.steps, args.warmup)
 
@@ -324,6 +359,7 @@ def main() -> int:
         "single_frame": {"points": wl1.num_points, "us_per_call": round(us1, 2),
                          "mpoints_s": round(wl1.num_points / (us1 * 1e-6) / 1e6, 1)},
         "scatter_to_bev": bev,
+        "voxel_clusters": {"batch": clusters, "single_ouster_frame": clusters1},
         "cpu_baseline": cpu,
     }
     print(json.dumps(out), flush=True)

@@ -60,7 +60,7 @@
 extern "C" {
 #endif
 
-#define MMBEV_ABI_VERSION 4
+#define MMBEV_ABI_VERSION 5
 
 /* ------------------------------------------------------------- status */
 typedef int32_t mmbev_status_t;
@@ -78,9 +78,10 @@ typedef int32_t mmbev_status_t;
 #define MMBEV_FAULT_ROI_OFFSETS 2   /* ROI frame offsets not 0 .. num_rois, non-decreasing,
                                        or a frame with more than max_rois_per_frame ROIs */
 #define MMBEV_FAULT_INTERNAL 4      /* an internal consistency check failed (never with valid inputs) */
-#define MMBEV_FAULT_VOXELS 8        /* mmbev_scatter_to_bev: voxel rows break its contract (offsets,
-                                       coordinates outside the grid or of another frame, keys not
-                                       strictly ascending inside a frame) */
+#define MMBEV_FAULT_VOXELS 8        /* mmbev_scatter_to_bev, mmbev_voxel_clusters: voxel rows break
+                                       the contract (offsets, coordinates outside the grid or of
+                                       another frame; for the scatter also keys not strictly
+                                       ascending inside a frame) */
 
 /* ------------------------------------------------------------- inputs */
 
@@ -269,6 +270,67 @@ mmbev_status_t mmbev_roi_voxelize_ex(const mmbev_points_t* points, const uint8_t
 mmbev_status_t mmbev_scatter_to_bev(const int32_t* coords, const float* feats, const int64_t* voxel_offsets,
                                     int32_t num_features, const mmbev_grid_t* grid, float* bev_map,
                                     int32_t* fault, void* stream);
+
+/* ----------------------------- voxel-grid connected-component proposer */
+
+/* Parameters of mmbev_voxel_clusters. */
+typedef struct {
+  int32_t z_min, z_max;  /* voxel layers iz in [z_min, z_max) count (e.g. above the ground) */
+  int32_t cell_shift;    /* s, 0..8: a cell is 2^s x 2^s voxel columns */
+  int32_t connectivity;  /* 4 or 8 (edge or edge-and-corner neighbours) */
+  int32_t min_cells;     /* components with fewer cells are not clusters, >= 1 */
+  int32_t reserved;      /* 0 */
+} mmbev_cluster_params_t;
+
+/* One cluster, 56 bytes.  Cell coordinates are x = ix >> s, y = iy >> s;
+ * cell index y*Wx + x with Wx = ceil(Dx / 2^s), Wy = ceil(Dy / 2^s). */
+typedef struct {
+  int32_t frame;
+  int32_t root;          /* smallest cell index of the cluster (its identity inside the frame) */
+  int32_t cells;         /* occupied cells */
+  int32_t voxels;        /* voxels in the layer band */
+  int32_t points;        /* kept points of those voxels (sum of their counts) */
+  int32_t x0, y0, x1, y1; /* bounding box in cells, inclusive */
+  int32_t reserved;
+  int64_t sum_x, sum_y;  /* sums of the cells' x and y (the centroid is sum / cells) */
+} mmbev_cluster_t;
+
+/* Workspace bytes of mmbev_voxel_clusters (0 if the sizes are invalid or
+ * unsupported: num_frames * Wx * Wy must stay below 2^29 cells). */
+size_t mmbev_voxel_clusters_workspace_bytes(const mmbev_grid_t* grid, const mmbev_cluster_params_t* params);
+
+/*
+ * Object clusters on the voxel grid: the lightweight connected-component
+ * proposer of the paper's robot deployment (Sec. VI), whose cluster set
+ * feeds the adaptive keyframe scheduler's cluster-shift trigger.  Reading:
+ * in each frame a bird's-eye-view cell (ix >> s, iy >> s) is occupied when a
+ * voxel of a layer in [z_min, z_max) lies in it; clusters are the connected
+ * components of the occupied cells (4- or 8-neighbourhood) with at least
+ * min_cells cells, listed per frame in ascending order of their smallest
+ * cell index.  Every field is an integer, so the result is unique.
+ *
+ * coords, counts, voxel_offsets: device arrays as written by
+ *   mmbev_roi_voxelize (rows = num_frames * max_voxels; frame b's voxels are
+ *   rows [off[b], off[b+1]); the order inside a frame does not matter)
+ * out_clusters         device, [rows]; clusters [0, off'[B]) are written
+ * out_cluster_offsets  device, int64 [num_frames+1]: frame b's clusters are
+ *                      [off'[b], off'[b+1])
+ * out_voxel_labels     device, int32 [rows]: for rows [0, off[B]) the index of
+ *                      the voxel's cluster, or -1 (outside the layer band or in
+ *                      a component below min_cells); other rows untouched
+ * workspace            device, 256-byte aligned, size from
+ *                      mmbev_voxel_clusters_workspace_bytes; needs no
+ *                      initialisation; its int32 at byte 0 receives
+ *                      MMBEV_FAULT_VOXELS when rows break the contract (such
+ *                      rows are skipped; every access stays inside the buffers)
+ *
+ * Ownership, streams and errors as for mmbev_roi_voxelize.
+ */
+mmbev_status_t mmbev_voxel_clusters(const int32_t* coords, const int32_t* counts, const int64_t* voxel_offsets,
+                                    const mmbev_grid_t* grid, const mmbev_cluster_params_t* params,
+                                    mmbev_cluster_t* out_clusters, int64_t* out_cluster_offsets,
+                                    int32_t* out_voxel_labels, void* workspace, size_t workspace_bytes,
+                                    void* stream);
 
 #ifdef __cplusplus
 }

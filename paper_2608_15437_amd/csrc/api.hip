@@ -19,6 +19,47 @@ int bits_for(uint64_t maxval) {
 
 size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
+// Workspace of the connected-component proposer.
+struct CcPlan {
+  int64_t rows, cells, ncell, Wx, Wy, nwords, nblocks;
+  size_t off_occ, off_wpre, off_bsum, off_parent, off_cnt, off_rcell, total;
+};
+
+mmbev_status_t cc_plan(const mmbev_grid_t* g, const mmbev_cluster_params_t* prm, CcPlan* p) {
+  if (!g || !prm) return MMBEV_ERR_INVALID_ARG;
+  for (int d = 0; d < 3; ++d)
+    if (g->dims[d] < 1 || g->dims[d] >= (1 << 24)) return MMBEV_ERR_INVALID_ARG;
+  if (g->max_voxels < 1 || g->num_frames < 1 || g->num_frames > 65535) return MMBEV_ERR_INVALID_ARG;
+  if (prm->connectivity != 4 && prm->connectivity != 8) return MMBEV_ERR_INVALID_ARG;
+  if (prm->cell_shift < 0 || prm->cell_shift > 8 || prm->min_cells < 1 || prm->reserved != 0)
+    return MMBEV_ERR_INVALID_ARG;
+  if ((uint64_t)g->num_frames * (uint64_t)g->max_voxels > (uint64_t)INT32_MAX) return MMBEV_ERR_UNSUPPORTED;
+  const int64_t side = (int64_t)1 << prm->cell_shift;
+  p->Wx = (g->dims[0] + side - 1) / side;
+  p->Wy = (g->dims[1] + side - 1) / side;
+  p->ncell = p->Wx * p->Wy;
+  p->cells = p->ncell * g->num_frames;
+  if (p->cells >= kCcMaxCells) return MMBEV_ERR_UNSUPPORTED;
+  p->rows = (int64_t)g->num_frames * g->max_voxels;
+  p->nwords = ((p->cells + 31) / 32 + 63) / 64 * 64;  // whole 256-byte blocks
+  p->nblocks = (p->nwords + kBlock * 16 - 1) / (kBlock * 16);
+  size_t off = 256;  // CcHeader
+  p->off_occ = off;
+  off += align256((size_t)p->nwords * 8);  // occ, then rootbits
+  p->off_wpre = off;
+  off += align256((size_t)p->nwords * 4);
+  p->off_bsum = off;
+  off += align256((size_t)p->nblocks * 4);
+  p->off_parent = off;
+  off += align256((size_t)p->cells * 4);
+  p->off_cnt = off;
+  off += align256((size_t)p->cells * 4);
+  p->off_rcell = off;
+  off += align256((size_t)p->rows * 4);
+  p->total = off;
+  return MMBEV_OK;
+}
+
 struct Plan {
   int64_t N;
   int32_t B, S, C, M, cap, max_rois, W;
@@ -405,6 +446,59 @@ mmbev_status_t mmbev_scatter_to_bev(const int32_t* coords, const float* feats, c
   c.max_voxels = grid->max_voxels;
   c.vec = ((uintptr_t)bev_map & 15) == 0;
   return launch_bev(c, (hipStream_t)stream) == hipSuccess ? MMBEV_OK : MMBEV_ERR_HIP;
+}
+
+size_t mmbev_voxel_clusters_workspace_bytes(const mmbev_grid_t* grid, const mmbev_cluster_params_t* params) {
+  CcPlan p;
+  return cc_plan(grid, params, &p) == MMBEV_OK ? p.total : 0;
+}
+
+mmbev_status_t mmbev_voxel_clusters(const int32_t* coords, const int32_t* counts, const int64_t* voxel_offsets,
+                                    const mmbev_grid_t* grid, const mmbev_cluster_params_t* params,
+                                    mmbev_cluster_t* out_clusters, int64_t* out_cluster_offsets,
+                                    int32_t* out_voxel_labels, void* workspace, size_t workspace_bytes,
+                                    void* stream) {
+  CcPlan p;
+  const mmbev_status_t st = cc_plan(grid, params, &p);
+  if (st != MMBEV_OK) return st;
+  if (!coords || !counts || !voxel_offsets || !out_clusters || !out_cluster_offsets || !out_voxel_labels)
+    return MMBEV_ERR_INVALID_ARG;
+  if (((uintptr_t)coords & 15) != 0 || ((uintptr_t)out_clusters & 7) != 0) return MMBEV_ERR_INVALID_ARG;
+  if (!workspace || ((uintptr_t)workspace & 255) != 0 || workspace_bytes < p.total) return MMBEV_ERR_WORKSPACE;
+  char* ws = (char*)workspace;
+  CcConfig c{};
+  c.coords = reinterpret_cast<const int4*>(coords);
+  c.counts = counts;
+  c.voff = voxel_offsets;
+  c.out = out_clusters;
+  c.out_off = out_cluster_offsets;
+  c.labels = out_voxel_labels;
+  c.hdr = (CcHeader*)ws;
+  c.occ = (uint32_t*)(ws + p.off_occ);
+  c.rootbits = c.occ + p.nwords;
+  c.wpre = (uint32_t*)(ws + p.off_wpre);
+  c.bsum = (uint32_t*)(ws + p.off_bsum);
+  c.parent = (int32_t*)(ws + p.off_parent);
+  c.cnt = (int32_t*)(ws + p.off_cnt);
+  c.rcell = (int32_t*)(ws + p.off_rcell);
+  c.rows = p.rows;
+  c.cells = p.cells;
+  c.nwords = (uint32_t)p.nwords;
+  c.nblocks = (uint32_t)p.nblocks;
+  c.Dx = (uint32_t)grid->dims[0];
+  c.Dy = (uint32_t)grid->dims[1];
+  c.Dz = (uint32_t)grid->dims[2];
+  c.B = grid->num_frames;
+  c.max_voxels = grid->max_voxels;
+  c.ncell = (int32_t)p.ncell;
+  c.Wx = (int32_t)p.Wx;
+  c.Wy = (int32_t)p.Wy;
+  c.shift = params->cell_shift;
+  c.z_min = params->z_min;
+  c.z_max = params->z_max;
+  c.conn = params->connectivity;
+  c.min_cells = params->min_cells;
+  return launch_clusters(c, (hipStream_t)stream) == hipSuccess ? MMBEV_OK : MMBEV_ERR_HIP;
 }
 
 }  // extern "C"

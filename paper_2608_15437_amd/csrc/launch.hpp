@@ -35,4 +35,37 @@ struct BevConfig {
 
 hipError_t launch_bev(const BevConfig& c, hipStream_t st);
 
+// Connected-component proposer: workspace header, and what its kernels read.
+struct CcHeader {
+  int32_t fault;      // byte 0: MMBEV_FAULT_VOXELS
+  uint32_t clusters;  // clusters over all frames
+};
+
+constexpr uint32_t kCcRowGrid = 8192;     // workgroups of the per-row launches (they loop)
+constexpr int64_t kCcMaxCells = (int64_t)1 << 29;  // cells over all frames (single-workgroup block scan)
+
+struct CcConfig {
+  const int4* coords;       // [rows]
+  const int32_t* counts;    // [rows]
+  const int64_t* voff;      // [B+1]
+  mmbev_cluster_t* out;     // [rows]
+  int64_t* out_off;         // [B+1]
+  int32_t* labels;          // [rows]
+  CcHeader* hdr;
+  uint32_t* occ;            // [nwords] occupied cells; rootbits follows it directly
+  uint32_t* rootbits;       // [nwords] roots of kept components
+  uint32_t* wpre;           // [nwords] kept roots in the words before
+  uint32_t* bsum;           // [nblocks]
+  int32_t* parent;          // [cells], valid at occupied cells only
+  int32_t* cnt;             // [cells], valid at occupied cells only
+  int32_t* rcell;           // [rows] the row's cell (top bit: another row owns it), or -1
+  int64_t rows;             // B * max_voxels
+  int64_t cells;            // B * ncell
+  uint32_t nwords, nblocks;
+  uint32_t Dx, Dy, Dz;
+  int32_t B, max_voxels, ncell, Wx, Wy, shift, z_min, z_max, conn, min_cells;
+};
+
+hipError_t launch_clusters(const CcConfig& c, hipStream_t st);
+
 }  // namespace mmbev

@@ -42,6 +42,16 @@ class mmbev_options_t(ctypes.Structure):
     _fields_ = [("out_of_roi_keep_rate", ctypes.c_float), ("reserved", ctypes.c_uint32), ("seed", ctypes.c_uint64)]
 
 
+class mmbev_cluster_params_t(ctypes.Structure):
+    _fields_ = [("z_min", ctypes.c_int32), ("z_max", ctypes.c_int32), ("cell_shift", ctypes.c_int32),
+                ("connectivity", ctypes.c_int32), ("min_cells", ctypes.c_int32), ("reserved", ctypes.c_int32)]
+
+
+CLUSTER_DTYPE = np.dtype([("frame", "<i4"), ("root", "<i4"), ("cells", "<i4"), ("voxels", "<i4"), ("points", "<i4"),
+                          ("x0", "<i4"), ("y0", "<i4"), ("x1", "<i4"), ("y1", "<i4"), ("reserved", "<i4"),
+                          ("sum_x", "<i8"), ("sum_y", "<i8")])
+
+
 class MmbevError(RuntimeError):
     pass
 
@@ -78,6 +88,12 @@ def load() -> ctypes.CDLL:
         L.mmbev_roi_voxelize_ex.restype = ctypes.c_int32
         L.mmbev_scatter_to_bev.argtypes = [p, p, p, ctypes.c_int32, ctypes.POINTER(mmbev_grid_t), p, p, p]
         L.mmbev_scatter_to_bev.restype = ctypes.c_int32
+        L.mmbev_voxel_clusters_workspace_bytes.argtypes = [ctypes.POINTER(mmbev_grid_t),
+                                                           ctypes.POINTER(mmbev_cluster_params_t)]
+        L.mmbev_voxel_clusters_workspace_bytes.restype = ctypes.c_size_t
+        L.mmbev_voxel_clusters.argtypes = [p, p, p, ctypes.POINTER(mmbev_grid_t),
+                                           ctypes.POINTER(mmbev_cluster_params_t), p, p, p, p, ctypes.c_size_t, p]
+        L.mmbev_voxel_clusters.restype = ctypes.c_int32
         _lib = L
     return _lib
 
@@ -204,6 +220,57 @@ def scatter_to_bev(coords, feats, voxel_offsets, grid: mmbev_grid_t, bev_map, fa
                                        _ptr(bev_map), _ptr(fault), _stream(stream)), "mmbev_scatter_to_bev")
 
 
+def cluster_params(z_min: int, z_max: int, cell_shift: int = 0, connectivity: int = 8,
+                   min_cells: int = 1) -> mmbev_cluster_params_t:
+    return mmbev_cluster_params_t(int(z_min), int(z_max), int(cell_shift), int(connectivity), int(min_cells), 0)
+
+
+def voxel_clusters_workspace_bytes(grid: mmbev_grid_t, params: mmbev_cluster_params_t) -> int:
+    return int(load().mmbev_voxel_clusters_workspace_bytes(ctypes.byref(grid), ctypes.byref(params)))
+
+
+def voxel_clusters(coords, counts, voxel_offsets, grid: mmbev_grid_t, params: mmbev_cluster_params_t,
+                   out_clusters, out_offsets, out_labels, workspace, stream=None) -> None:
+    """Enqueue mmbev_voxel_clusters (torch tensors on the GPU).  out_clusters:
+    any contiguous tensor of rows * 56 bytes (rows = num_frames * max_voxels);
+    out_offsets int64 [B+1]; out_labels int32 [rows]."""
+    _check(load().mmbev_voxel_clusters(_ptr(coords), _ptr(counts), _ptr(voxel_offsets), ctypes.byref(grid),
+                                       ctypes.byref(params), _ptr(out_clusters), _ptr(out_offsets), _ptr(out_labels),
+                                       _ptr(workspace), workspace.numel() * workspace.element_size(),
+                                       _stream(stream)), "mmbev_voxel_clusters")
+
+
+class ClusterProposer:
+    """Owns the outputs and workspace of mmbev_voxel_clusters for one grid."""
+
+    def __init__(self, grid: mmbev_grid_t, params: mmbev_cluster_params_t, device):
+        import torch
+
+        self.grid, self.params, self.device = grid, params, torch.device(device)
+        rows = grid.num_frames * grid.max_voxels
+        nbytes = voxel_clusters_workspace_bytes(grid, params)
+        if nbytes == 0:
+            raise MmbevError("invalid sizes for mmbev_voxel_clusters_workspace_bytes")
+        self.workspace = torch.empty(nbytes, dtype=torch.uint8, device=self.device)
+        self.out = torch.zeros(rows * CLUSTER_DTYPE.itemsize // 8, dtype=torch.int64, device=self.device)
+        self.offsets = torch.zeros(grid.num_frames + 1, dtype=torch.int64, device=self.device)
+        self.labels = torch.full((rows,), -7, dtype=torch.int32, device=self.device)
+
+    def run(self, coords, counts, voxel_offsets, stream=None) -> None:
+        voxel_clusters(coords, counts, voxel_offsets, self.grid, self.params, self.out, self.offsets, self.labels,
+                       self.workspace, stream)
+
+    def fault(self) -> int:
+        return int(self.workspace[:4].cpu().numpy().view(np.int32)[0])
+
+    def result(self, num_voxels: int) -> dict:
+        """Clusters (CLUSTER_DTYPE), offsets [B+1] and the labels of the first num_voxels rows (synchronises)."""
+        off = self.offsets.cpu().numpy()
+        n = int(off[-1])
+        cl = self.out[:n * CLUSTER_DTYPE.itemsize // 8].cpu().numpy().view(CLUSTER_DTYPE)
+        return {"clusters": cl, "cluster_offsets": off, "voxel_labels": self.labels[:num_voxels].cpu().numpy()}
+
+
 class Voxelizer:
     """Owns device inputs, outputs and workspace for repeated calls on one batch shape.
 
@@ -261,6 +328,13 @@ class Voxelizer:
                                   device=self.device)
         scatter_to_bev(self.out_coords, self.out_feats, self.out_voxel_offsets, self.grid, bev_map, fault, stream)
         return bev_map
+
+    def clusters(self, params: mmbev_cluster_params_t, proposer=None, stream=None) -> "ClusterProposer":
+        """The connected-component proposer over this Voxelizer's outputs (enqueued; returns the proposer)."""
+        if proposer is None:
+            proposer = ClusterProposer(self.grid, params, self.device)
+        proposer.run(self.out_coords, self.out_counts, self.out_voxel_offsets, stream)
+        return proposer
 
     def fault(self) -> int:
         """Device fault word of the last completed call (synchronises)."""

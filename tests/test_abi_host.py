@@ -38,7 +38,8 @@ def declared_functions():
 
 def test_header_declares_the_path():
     names = declared_functions()
-    for n in ["mmbev_roi_voxelize", "mmbev_roi_voxelize_ex", "mmbev_scatter_to_bev",
+    for n in ["mmbev_roi_voxelize", "mmbev_roi_voxelize_ex", "mmbev_scatter_to_bev", "mmbev_voxel_clusters",
+              "mmbev_voxel_clusters_workspace_bytes",
               "mmbev_roi_voxelize_workspace_bytes", "mmbev_make_rois",
               "mmbev_workspace_init", "mmbev_abi_version", "mmbev_status_string"]:
         assert n in names
@@ -60,7 +61,9 @@ def test_struct_layouts_match_header(mb):
     assert ctypes.sizeof(mb.mmbev_grid_t) == 52
     assert ctypes.sizeof(mb.mmbev_options_t) == 16
     assert mb.ROI_DTYPE.itemsize == 32
-    assert mb.abi_version() == 4
+    assert mb.abi_version() == 5
+    assert ctypes.sizeof(mb.mmbev_cluster_params_t) == 24
+    assert mb.CLUSTER_DTYPE.itemsize == 56
 
 
 def test_make_rois_matches_oracle_bitwise(mb):
@@ -164,3 +167,32 @@ def test_scatter_to_bev_rejects_bad_arguments_before_any_launch(mb):
     assert call(grid=bad) == mb.ERR_INVALID_ARG
     huge = mb.grid_params((-4, -4, -1), (0.5, 0.5, 0.5), (1 << 16, 1 << 16, 2), 2, 3, 2, 1)
     assert call(grid=huge) == mb.ERR_UNSUPPORTED
+
+
+def test_voxel_clusters_validation(mb):
+    L = mb.load()
+    g = mb.grid_params((-4, -4, -1), (0.5, 0.5, 0.5), (16, 16, 4), 2, 3, 2, 2)
+    prm = mb.cluster_params(1, 3, 0, 8, 1)
+    need = mb.voxel_clusters_workspace_bytes(g, prm)
+    assert need > 0
+    for bad in (mb.cluster_params(1, 3, 0, 6, 1), mb.cluster_params(1, 3, 9, 8, 1), mb.cluster_params(1, 3, 0, 8, 0)):
+        assert mb.voxel_clusters_workspace_bytes(g, bad) == 0
+    r = mb.cluster_params(1, 3, 0, 8, 1)
+    r.reserved = 1
+    assert mb.voxel_clusters_workspace_bytes(g, r) == 0
+    big = mb.grid_params((-4, -4, -1), (0.5, 0.5, 0.5), (1 << 15, 1 << 15, 1), 2, 3, 2, 1)
+    assert mb.voxel_clusters_workspace_bytes(big, prm) == 0  # 2^30 cells
+    assert mb.voxel_clusters_workspace_bytes(big, mb.cluster_params(0, 1, 1, 8, 1)) > 0  # 2^28 cells
+    fake = 1 << 40
+
+    def call(coords=fake, out=fake, ws=fake, ws_bytes=need, params=prm):
+        return L.mmbev_voxel_clusters(coords, fake, fake, ctypes.byref(g), ctypes.byref(params), out, fake, fake,
+                                      ws, ws_bytes, None)
+
+    assert call(coords=None) == mb.ERR_INVALID_ARG
+    assert call(coords=fake + 4) == mb.ERR_INVALID_ARG
+    assert call(out=fake + 4) == mb.ERR_INVALID_ARG
+    assert call(ws=None) == mb.ERR_WORKSPACE
+    assert call(ws=fake + 128) == mb.ERR_WORKSPACE
+    assert call(ws_bytes=need - 1) == mb.ERR_WORKSPACE
+    assert call(params=mb.cluster_params(1, 3, 0, 5, 1)) == mb.ERR_INVALID_ARG

@@ -159,6 +159,24 @@ def time_scatter(wl, dev, steps: int, warmup: int) -> dict:
     return out
 
 
+def time_selector(steps: int) -> dict:
+    """The temporal-ROI selector and sweep-count knob (mmbev_build_rois, host
+    code) over 128 detection caches of 64 objects each, the default policy;
+    wall clock over `steps` calls on one host thread."""
+    import synth
+    from paper_2608_15437_amd import mmbev
+
+    d, off, e = synth.detections(7, 128, count=[64] * 128)
+    pol = mmbev.policy()
+    mmbev.build_rois(d, off, e, pol)
+    t0 = time.perf_counter()
+    for _ in range(max(steps, 1)):
+        out = mmbev.build_rois(d, off, e, pol)
+    us = (time.perf_counter() - t0) / max(steps, 1) * 1e6
+    return {"frames": 128, "detections_per_frame": 64, "rois": int(out["roi_offsets"][-1]),
+            "us_per_call": round(us, 1), "us_per_frame": round(us / 128, 2), "where": "host, one thread"}
+
+
 def time_clusters(vz, steps: int, warmup: int, ouster: bool = False) -> dict:
     """The connected-component proposer (mmbev_voxel_clusters) over a
     Voxelizer's outputs: layers 0.4-4.4 m above the ground plane (above 1.0 m
@@ -304,6 +322,9 @@ def main() -> int:
     vz1 = mmbev.voxelizer_for_workload(wl1, dev)
     us1 = time_calls(vz1, max(args.steps, 20), args.warmup) * 1e3
 
+    log("[bench] temporal-ROI selector (host) on 128 detection caches")
+    selector = time_selector(args.steps)
+
     log("[bench] connected-component proposer on the batch's voxels")
     clusters = time_clusters(vz, args.steps, args.warmup)
     log("[bench] connected-component proposer on one Ouster-shaped frame")
@@ -360,6 +381,7 @@ def main() -> int:
                          "mpoints_s": round(wl1.num_points / (us1 * 1e-6) / 1e6, 1)},
         "scatter_to_bev": bev,
         "voxel_clusters": {"batch": clusters, "single_ouster_frame": clusters1},
+        "roi_selector": selector,
         "cpu_baseline": cpu,
     }
     print(json.dumps(out), flush=True)

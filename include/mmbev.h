@@ -60,7 +60,7 @@
 extern "C" {
 #endif
 
-#define MMBEV_ABI_VERSION 5
+#define MMBEV_ABI_VERSION 6
 
 /* ------------------------------------------------------------- status */
 typedef int32_t mmbev_status_t;
@@ -234,6 +234,105 @@ mmbev_status_t mmbev_roi_voxelize_ex(const mmbev_points_t* points, const uint8_t
                                      float* out_feats, int32_t* out_point_idx, int64_t* out_voxel_offsets,
                                      void* workspace, size_t workspace_bytes, void* stream, void* const* events,
                                      int32_t num_events, int32_t* events_recorded);
+
+/* ------------------------------ temporal ROIs and criticality (host) */
+
+/* Object classes of the criticality thresholds (Sec. IV-C). */
+#define MMBEV_CLASS_VRU 0       /* pedestrians, cyclists: TTC threshold tau_vru */
+#define MMBEV_CLASS_MOTORIZED 1 /* vehicles: tau_motorized */
+#define MMBEV_CLASS_STATIC 2    /* barriers, cones: geometry-critical only */
+
+/* A detection of frame t-1 (an entry of the detection cache B^{t-1}), in the
+ * ego frame of t-1: x forward, y left [m], yaw [rad] about z; velocity is the
+ * object's own (ground) velocity expressed in those axes [m/s].  64 bytes. */
+typedef struct {
+  double x, y, yaw;
+  double length, width;
+  double vx, vy;
+  int32_t cls;      /* MMBEV_CLASS_* */
+  int32_t reserved; /* 0 */
+} mmbev_detection_t;
+
+/* Ego state of frame t: speed [m/s] along +x, and the rigid motion from the
+ * ego frame of t-1 to that of t (a point p of frame t-1 is
+ * R(dyaw) p + (dx, dy) in frame t). */
+typedef struct {
+  double speed;
+  double dx, dy, dyaw;
+} mmbev_ego_t;
+
+/* Selector and coordinator parameters (Sec. IV-C, IV-G). */
+typedef struct {
+  double dt;                          /* Delta t between frames [s] */
+  double margin;                      /* r of Eq. 1 [m] */
+  double a_brake, d_min;              /* Eq. 4 [m/s^2], [m] */
+  double theta_max_deg, theta_min_deg; /* cone half-angle at and below speed_wide / at and above speed_narrow */
+  double speed_wide, speed_narrow;    /* [m/s]; theta is linear in speed between them */
+  double tau_vru, tau_motorized;      /* Eq. 5 thresholds [s] */
+  double r_coll;                      /* Eq. 8 collision radius [m] */
+  double slow_speed;                  /* ego slower than this: the reduced sweep count */
+  int32_t dense_count;                /* this many detections or more: the reduced sweep count */
+  int32_t n_full, n_reduced;          /* sweep counts (1..255): mandatory ROIs always get n_full */
+  int32_t max_optional;               /* optional detections kept per frame (by rank); the rest dropped */
+  int32_t reserved;                   /* 0 */
+  double fallback_length, fallback_width; /* empty cache: one ego-centred box of this size, n_full sweeps (0: none) */
+} mmbev_policy_t;
+
+/* Per-detection outcome.  Flags: */
+#define MMBEV_CRIT_GEOM 1      /* Eq. 3: inside the forward braking cone */
+#define MMBEV_CRIT_SAFETY 2    /* Eq. 5: TTC at or below the class threshold */
+#define MMBEV_CRIT_MANDATORY 4 /* GEOM or SAFETY */
+#define MMBEV_CRIT_DROPPED 8   /* optional and ranked past max_optional: its ROIs get budget 0 */
+typedef struct {
+  double ttc;    /* Eq. 8 [s]; +infinity when there is no approach within r_coll */
+  int32_t flags; /* MMBEV_CRIT_* */
+  int32_t rank;  /* position of the detection in its frame's ranking, 0 = most critical */
+} mmbev_criticality_t;
+
+/*
+ * The Criticality-Ranked Temporal-ROI Selector and the sweep-count knob of
+ * the coordinator (Sec. IV-C, IV-G; Alg. 2 TemporalROI, ComputeTTC,
+ * ScaleCompute), producing the rois and roi_sweep_budget arguments of
+ * mmbev_roi_voxelize.  Host code; every array is host memory.  Per frame b,
+ * for each detection i (all arithmetic in double, in this order):
+ *   1. footprints: the box at t-1 and the box moved by (vx, vy)*dt (Eq. 1),
+ *      both taken into frame t by the ego motion (centre rotated by dyaw and
+ *      shifted by (dx, dy); yaw + dyaw);
+ *   2. criticality from the moved box in frame t: p = its centre, the
+ *      relative velocity w = R(dyaw)(vx, vy) - (speed, 0);
+ *      d_max = max(d_min, speed^2 / (2 a_brake))                     (Eq. 4)
+ *      theta = theta_max at speed <= speed_wide, theta_min at speed >=
+ *        speed_narrow, linear in between (degrees, then radians)
+ *      GEOM iff p.x >= 0 and |p| <= d_max and atan2(|p.y|, p.x) <= theta (Eq. 3)
+ *      t* = -(p . w) / |w|^2; TTC = t* iff |w| > 0, t* > 0 and
+ *        |p + t* w| <= r_coll, else +inf                             (Eq. 8)
+ *      SAFETY iff the class is not STATIC and TTC <= tau_class        (Eq. 5)
+ *      MANDATORY iff GEOM or SAFETY;
+ *   3. ranking: mandatory before optional, then ascending TTC, then
+ *      ascending |p|, then input order; optional detections ranked past
+ *      max_optional among the optional ones are DROPPED;
+ *   4. sweep count n = n_reduced if speed < slow_speed or the frame has at
+ *      least dense_count detections, else n_full (written to out_sweeps);
+ *   5. ROI records, in rank order, two per detection (its footprint at t-1,
+ *      then the moved one), built like mmbev_make_rois from (cx, cy, length,
+ *      width, yaw, margin); budget n_full if mandatory, 0 if dropped, else n.
+ *      A frame without detections gets the fallback box (centre 0, yaw 0, no
+ *      margin) with budget n_full, unless its size is 0.
+ *
+ * dets [det_offsets[B]], det_offsets [B+1] (non-decreasing, from 0); ego [B].
+ * Outputs: out_rois and out_budgets hold 2 * det_offsets[B] + B entries,
+ * out_roi_offsets B+1 (frame b's records are [off[b], off[b+1])),
+ * out_crit det_offsets[B] (in input order), out_sweeps B.
+ * Errors: MMBEV_ERR_INVALID_ARG for a null pointer, bad offsets, a
+ * non-finite or out-of-range parameter (dt, r_coll, a_brake > 0; margin,
+ * d_min >= 0; 0 <= theta_min <= theta_max <= 90; speed_wide <= speed_narrow;
+ * 1 <= n_reduced <= n_full <= 255; max_optional >= 0), an unknown class or a
+ * nonzero reserved field; nothing is written then.
+ */
+mmbev_status_t mmbev_build_rois(const mmbev_detection_t* dets, const int32_t* det_offsets, int32_t num_frames,
+                                const mmbev_ego_t* ego, const mmbev_policy_t* policy, mmbev_roi_t* out_rois,
+                                uint8_t* out_budgets, int32_t* out_roi_offsets, mmbev_criticality_t* out_crit,
+                                int32_t* out_sweeps);
 
 /* ------------------------------------------------ ScatterToBEV (Alg. 1) */
 

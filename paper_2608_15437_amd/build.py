@@ -16,7 +16,7 @@ ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 OUT = os.path.join(HERE, "libmmbev.so")
 BUILD_DIR = os.path.join(HERE, "_build")
-SOURCES = ["api.hip", "stage.hip", "filter.hip", "sort.hip", "voxel.hip", "bev.hip", "cc.hip"]
+SOURCES = ["api.hip", "stage.hip", "filter.hip", "sort.hip", "voxel.hip", "bev.hip", "cc.hip", "roi_policy.cpp"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"
 

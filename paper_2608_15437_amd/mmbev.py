@@ -52,6 +52,38 @@ CLUSTER_DTYPE = np.dtype([("frame", "<i4"), ("root", "<i4"), ("cells", "<i4"), (
                           ("sum_x", "<i8"), ("sum_y", "<i8")])
 
 
+DETECTION_DTYPE = np.dtype([("x", "<f8"), ("y", "<f8"), ("yaw", "<f8"), ("length", "<f8"), ("width", "<f8"),
+                            ("vx", "<f8"), ("vy", "<f8"), ("cls", "<i4"), ("reserved", "<i4")])
+EGO_DTYPE = np.dtype([("speed", "<f8"), ("dx", "<f8"), ("dy", "<f8"), ("dyaw", "<f8")])
+CRIT_DTYPE = np.dtype([("ttc", "<f8"), ("flags", "<i4"), ("rank", "<i4")])
+CLASS_VRU, CLASS_MOTORIZED, CLASS_STATIC = 0, 1, 2
+CRIT_GEOM, CRIT_SAFETY, CRIT_MANDATORY, CRIT_DROPPED = 1, 2, 4, 8
+
+
+class mmbev_policy_t(ctypes.Structure):
+    _fields_ = [("dt", ctypes.c_double), ("margin", ctypes.c_double), ("a_brake", ctypes.c_double),
+                ("d_min", ctypes.c_double), ("theta_max_deg", ctypes.c_double), ("theta_min_deg", ctypes.c_double),
+                ("speed_wide", ctypes.c_double), ("speed_narrow", ctypes.c_double), ("tau_vru", ctypes.c_double),
+                ("tau_motorized", ctypes.c_double), ("r_coll", ctypes.c_double), ("slow_speed", ctypes.c_double),
+                ("dense_count", ctypes.c_int32), ("n_full", ctypes.c_int32), ("n_reduced", ctypes.c_int32),
+                ("max_optional", ctypes.c_int32), ("reserved", ctypes.c_int32), ("_pad", ctypes.c_int32),
+                ("fallback_length", ctypes.c_double), ("fallback_width", ctypes.c_double)]
+
+
+# Paper values: cone bounds 60 / 15 degrees, TTC thresholds 1.5 s / 2.5 s,
+# sweep counts 10 / 5 (Sec. IV-C, IV-G); the rest are deployment choices.
+DEFAULT_POLICY = dict(dt=0.5, margin=0.5, a_brake=6.0, d_min=10.0, theta_max_deg=60.0, theta_min_deg=15.0,
+                      speed_wide=5.0, speed_narrow=30.0, tau_vru=1.5, tau_motorized=2.5, r_coll=2.0, slow_speed=5.0,
+                      dense_count=64, n_full=10, n_reduced=5, max_optional=64, fallback_length=108.0,
+                      fallback_width=108.0)
+
+
+def policy(**kw) -> mmbev_policy_t:
+    v = dict(DEFAULT_POLICY)
+    v.update(kw)
+    return mmbev_policy_t(**{k: v[k] for k in DEFAULT_POLICY}, reserved=0)
+
+
 class MmbevError(RuntimeError):
     pass
 
@@ -94,6 +126,8 @@ def load() -> ctypes.CDLL:
         L.mmbev_voxel_clusters.argtypes = [p, p, p, ctypes.POINTER(mmbev_grid_t),
                                            ctypes.POINTER(mmbev_cluster_params_t), p, p, p, p, ctypes.c_size_t, p]
         L.mmbev_voxel_clusters.restype = ctypes.c_int32
+        L.mmbev_build_rois.argtypes = [p, p, ctypes.c_int32, p, ctypes.POINTER(mmbev_policy_t), p, p, p, p, p]
+        L.mmbev_build_rois.restype = ctypes.c_int32
         _lib = L
     return _lib
 
@@ -218,6 +252,29 @@ def scatter_to_bev(coords, feats, voxel_offsets, grid: mmbev_grid_t, bev_map, fa
         raise MmbevError("coords and feats must be contiguous")
     _check(load().mmbev_scatter_to_bev(_ptr(coords), _ptr(feats), _ptr(voxel_offsets), C, ctypes.byref(grid),
                                        _ptr(bev_map), _ptr(fault), _stream(stream)), "mmbev_scatter_to_bev")
+
+
+def build_rois(dets, det_offsets, ego, pol: mmbev_policy_t) -> dict:
+    """mmbev_build_rois on host arrays: dets DETECTION_DTYPE [D], det_offsets
+    int32 [B+1], ego EGO_DTYPE [B].  Returns ROI records (ROI_DTYPE), budgets
+    uint8, roi_offsets int32 [B+1], crit (CRIT_DTYPE, input order) and the
+    sweep count of each frame."""
+    dets = np.ascontiguousarray(dets, dtype=DETECTION_DTYPE)
+    det_offsets = np.ascontiguousarray(det_offsets, dtype=np.int32)
+    ego = np.ascontiguousarray(ego, dtype=EGO_DTYPE)
+    B = len(det_offsets) - 1
+    D = int(det_offsets[-1])
+    cap = 2 * D + B
+    rois = np.zeros(max(cap, 1), dtype=ROI_DTYPE)
+    budgets = np.zeros(max(cap, 1), dtype=np.uint8)
+    roff = np.zeros(B + 1, dtype=np.int32)
+    crit = np.zeros(max(D, 1), dtype=CRIT_DTYPE)
+    sweeps = np.zeros(max(B, 1), dtype=np.int32)
+    _check(load().mmbev_build_rois(dets.ctypes.data if D else None, det_offsets.ctypes.data, B, ego.ctypes.data,
+                                   ctypes.byref(pol), rois.ctypes.data, budgets.ctypes.data, roff.ctypes.data,
+                                   crit.ctypes.data, sweeps.ctypes.data), "mmbev_build_rois")
+    R = int(roff[-1])
+    return {"rois": rois[:R], "budgets": budgets[:R], "roi_offsets": roff, "crit": crit[:D], "sweeps": sweeps[:B]}
 
 
 def cluster_params(z_min: int, z_max: int, cell_shift: int = 0, connectivity: int = 8,

@@ -275,3 +275,52 @@ def small(seed: int, beams: int = 8, azimuths: int = 64, sweeps: int = 3, frames
 
 
 CONFIGS = {"c1": c1, "c2": c2, "c3": c3, "c4": c4, "c5": c5}
+
+
+# ------------------------------------------------------------- detections
+# The detection cache B^{t-1} of the temporal-ROI selector: boxes with class,
+# velocity and the ego state per frame.  Positions: a third of the objects in
+# a forward corridor (x in [0, 45] m, |y| < 0.6 x + 2), the rest uniform in
+# [-60, 60]^2; classes 30% vulnerable road users (0.8 x 0.8 m, speed U[0, 2]
+# m/s, any heading), 50% motorized (4.5 x 1.9 m +-10%, speed U[0, 15] m/s,
+# heading along +-x within 20 degrees; a quarter head-on towards the ego),
+# 20% static (0.5 x 0.5 m, at rest).  Ego speed U[0, 35] m/s, yaw rate U[-0.3,
+# 0.3] rad/s over dt; the frame-to-frame motion moves points back by the
+# distance driven.
+
+DETECTION_DTYPE = np.dtype([("x", "<f8"), ("y", "<f8"), ("yaw", "<f8"), ("length", "<f8"), ("width", "<f8"),
+                            ("vx", "<f8"), ("vy", "<f8"), ("cls", "<i4"), ("reserved", "<i4")])
+EGO_DTYPE = np.dtype([("speed", "<f8"), ("dx", "<f8"), ("dy", "<f8"), ("dyaw", "<f8")])
+
+
+def detections(seed: int, frames: int, count=(0, 300), dt: float = 0.5, speed=(0.0, 35.0)):
+    """Seeded detection caches: (dets [D] DETECTION_DTYPE, det_offsets int32
+    [frames+1], ego [frames] EGO_DTYPE).  count: (lo, hi) detections per frame,
+    or a list of exact counts."""
+    rng = np.random.default_rng(seed)
+    counts = list(count) if isinstance(count, list) else [int(rng.integers(count[0], count[1] + 1))
+                                                           for _ in range(frames)]
+    D = int(sum(counts))
+    d = np.zeros(D, dtype=DETECTION_DTYPE)
+    corridor = rng.random(D) < 1 / 3
+    x = np.where(corridor, rng.uniform(0, 45, D), rng.uniform(-60, 60, D))
+    y = np.where(corridor, rng.uniform(-1, 1, D) * (0.6 * x + 2), rng.uniform(-60, 60, D))
+    u = rng.random(D)
+    cls = np.where(u < 0.3, 0, np.where(u < 0.8, 1, 2)).astype(np.int32)
+    heading = np.where(cls == 0, rng.uniform(-np.pi, np.pi, D),
+                       rng.uniform(-0.35, 0.35, D) + np.where(rng.random(D) < 0.25, np.pi, 0.0))
+    sp = np.where(cls == 0, rng.uniform(0, 2, D), np.where(cls == 1, rng.uniform(0, 15, D), 0.0))
+    d["x"], d["y"] = x, y
+    d["yaw"] = np.where(cls == 2, rng.uniform(-np.pi, np.pi, D), heading)
+    d["length"] = np.where(cls == 0, 0.8, np.where(cls == 1, 4.5 * rng.uniform(0.9, 1.1, D), 0.5))
+    d["width"] = np.where(cls == 0, 0.8, np.where(cls == 1, 1.9 * rng.uniform(0.9, 1.1, D), 0.5))
+    d["vx"], d["vy"] = sp * np.cos(heading), sp * np.sin(heading)
+    d["cls"] = cls
+    off = np.zeros(frames + 1, dtype=np.int32)
+    off[1:] = np.cumsum(counts)
+    ego = np.zeros(frames, dtype=EGO_DTYPE)
+    ego["speed"] = rng.uniform(speed[0], speed[1], frames)
+    ego["dyaw"] = rng.uniform(-0.3, 0.3, frames) * dt
+    ego["dx"] = -ego["speed"] * dt * np.cos(ego["dyaw"])
+    ego["dy"] = -ego["speed"] * dt * np.sin(ego["dyaw"])
+    return d, off, ego

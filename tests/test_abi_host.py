@@ -39,6 +39,7 @@ def declared_functions():
 def test_header_declares_the_path():
     names = declared_functions()
     for n in ["mmbev_roi_voxelize", "mmbev_roi_voxelize_ex", "mmbev_scatter_to_bev", "mmbev_voxel_clusters",
+              "mmbev_build_rois",
               "mmbev_voxel_clusters_workspace_bytes",
               "mmbev_roi_voxelize_workspace_bytes", "mmbev_make_rois",
               "mmbev_workspace_init", "mmbev_abi_version", "mmbev_status_string"]:
@@ -61,7 +62,9 @@ def test_struct_layouts_match_header(mb):
     assert ctypes.sizeof(mb.mmbev_grid_t) == 52
     assert ctypes.sizeof(mb.mmbev_options_t) == 16
     assert mb.ROI_DTYPE.itemsize == 32
-    assert mb.abi_version() == 5
+    assert mb.abi_version() == 6
+    assert ctypes.sizeof(mb.mmbev_policy_t) == 136
+    assert mb.DETECTION_DTYPE.itemsize == 64 and mb.EGO_DTYPE.itemsize == 32 and mb.CRIT_DTYPE.itemsize == 16
     assert ctypes.sizeof(mb.mmbev_cluster_params_t) == 24
     assert mb.CLUSTER_DTYPE.itemsize == 56
 

@@ -113,15 +113,16 @@ mmbev_status_t make_plan(const mmbev_grid_t* g, int64_t N, int32_t max_rois, int
   const int64_t n1 = std::max<int64_t>(N, 1);
   // filter chunks: about kFilterWaveTarget of them over the whole input (a
   // few per resident wave), a multiple of the wave tile and at most
-  // kMaxChunkPoints points (a wave keeps its chunk's bitmap in LDS); frames
-  // add at most one partial chunk each
+  // kMaxChunkPoints points (a wave keeps its chunk's bitmap in LDS); a frame
+  // adds at most one partial chunk and up to kWaves - 1 empty ones (its
+  // chunks fill whole filter workgroups)
   {
     const int64_t target = kFilterWaveTarget > 2 * (int64_t)p->B ? kFilterWaveTarget - p->B : kFilterWaveTarget;
     int64_t P = (N + target - 1) / target;
     P = std::max<int64_t>(kWaveTile, (P + kWaveTile - 1) / kWaveTile * kWaveTile);
     P = std::min<int64_t>(P, kMaxChunkPoints);
     p->fchunk_points = P;
-    p->fchunk_max = (N + P - 1) / P + p->B;
+    p->fchunk_max = (N + P - 1) / P + (int64_t)kWaves * p->B;  // each frame rounded up to whole workgroups
     p->filter_grid = std::max<int64_t>(1, (p->fchunk_max + kWaves - 1) / kWaves);
   }
   p->schunk_max = kSortGrid + p->B;
@@ -342,6 +343,13 @@ mmbev_status_t voxelize(const mmbev_points_t* points, const uint8_t* sweep_ids, 
   c.fchunk_words = (int32_t)(p.fchunk_points / 32);
   c.fchunk_max = (int32_t)p.fchunk_max;
   c.filter_grid = (int32_t)p.filter_grid;
+  // one frame per filter workgroup: its poses, ROI records and budget masks
+  c.lds_pose_cap = p.S <= kMaxPoseLds ? p.S : 0;
+  c.lds_roi_cap = std::max(1, std::min(p.max_rois, kMaxLdsRois));
+  c.lds_bm_cap = p.S * p.W <= kMaxLdsBudgetWords ? p.S * p.W : 0;
+  c.lds_roi = c.lds_pose_cap * 12;
+  c.lds_bm = c.lds_roi + 6 * c.lds_roi_cap;
+  c.lds_dyn_bytes = (int32_t)(((size_t)(c.lds_bm + c.lds_bm_cap) * 4 + 15) / 16 * 16);
   c.schunk_max = (int32_t)p.schunk_max;
   c.mean_grid = (int32_t)p.mean_grid;
 

@@ -121,6 +121,10 @@ struct Config {
   int32_t fchunk_words;    // fchunk_points / 32
   int32_t fchunk_max;      // bound on filter chunks: ceil(N / fchunk_points) + B
   int32_t filter_grid;     // ceil(fchunk_max / kWaves) workgroups, one chunk per wave
+  // the filter's dynamic LDS: pose rows, ROI records (six rows of
+  // lds_roi_cap floats from float offset lds_roi), budget-mask words (from
+  // word offset lds_bm); a cap of 0 means "not staged"
+  int32_t lds_pose_cap, lds_roi_cap, lds_bm_cap, lds_roi, lds_bm, lds_dyn_bytes;
   int32_t schunk_max;      // bound on pair chunks: kSortGrid + B
   int32_t mean_grid;
 };

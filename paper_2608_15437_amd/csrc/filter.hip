@@ -44,16 +44,33 @@ namespace mmbev {
 
 namespace {
 
-// Tables of the workgroup's frames f0..f1, staged once and shared by its waves.
+// Tables of the workgroup's frames f0..f1 (one frame unless the point
+// offsets are invalid: a frame's chunks fill whole workgroups), staged once
+// and shared by its waves.  The cell maps have a fixed size; the poses, ROI
+// records and budget masks go to the dynamic LDS, sized for the call (the
+// sweeps and ROIs of one frame), so that a workgroup takes no more LDS than
+// its frame needs and five of them fit a compute unit.
 struct alignas(16) FilterLds {
-  float pose[kMaxPoseLds][12];  // 48-byte rows: three aligned 16-byte reads each
   uint32_t cell[kMaxLdsCells];  // candidate-ROI word of every coarse cell, frame after frame
-  float roi[6][kMaxLdsRois];    // cx, cy, cos, sin, ext_x, ext_y
-  uint32_t bm[kMaxLdsBudgetWords];
   int32_t roff[kMaxLdsFrames + 1];  // ROI offsets clamped to [0, R]
   int32_t f0, f1, roi_lo, roi_n;
   int32_t chunk_staged;
 };
+
+// Dynamic LDS: pose rows [c.lds_pose_cap][12] (48-byte rows: three aligned
+// 16-byte reads each), then the ROI records as six rows of c.lds_roi_cap
+// (cx, cy, cos, sin, ext_x, ext_y), then c.lds_bm_cap budget-mask words.
+extern __shared__ float4 filter_dyn[];
+
+__device__ __forceinline__ const float* lds_pose(int32_t row) {
+  return reinterpret_cast<const float*>(filter_dyn) + row * 12;
+}
+__device__ __forceinline__ float* lds_roi(const Config& c, int k) {
+  return reinterpret_cast<float*>(filter_dyn) + c.lds_roi + k * c.lds_roi_cap;
+}
+__device__ __forceinline__ uint32_t* lds_bm(const Config& c) {
+  return reinterpret_cast<uint32_t*>(filter_dyn) + c.lds_bm;
+}
 
 // Per-wave state in LDS: the candidate queue (a ring) and the kept bitmap
 // of the wave's chunk.
@@ -80,7 +97,7 @@ __device__ __forceinline__ void wave_lds_sync() {
 template <bool ST>
 __device__ __forceinline__ void load_pose(const Config& c, const FilterLds& L, int32_t b, uint32_t s, float* P) {
   if (ST) {
-    const float* src = L.pose[(b - L.f0) * c.S + s];
+    const float* src = lds_pose((b - L.f0) * c.S + s);
 #pragma unroll
     for (int k = 0; k < 12; ++k) P[k] = src[k];
   } else {
@@ -92,7 +109,7 @@ __device__ __forceinline__ void load_pose(const Config& c, const FilterLds& L, i
 
 template <bool ST>
 __device__ __forceinline__ uint32_t budget_word(const Config& c, const FilterLds& L, int32_t b, uint32_t s, int w) {
-  if (ST) return L.bm[((b - L.f0) * c.S + s) * c.W + w];
+  if (ST) return lds_bm(c)[((b - L.f0) * c.S + s) * c.W + w];
   return c.budgetmask[((int64_t)b * c.S + s) * c.W + w];
 }
 
@@ -107,12 +124,12 @@ __device__ __forceinline__ bool roi_hit(const Config& c, const FilterLds& L, int
   mmbev_roi_t r;
   if (ST) {
     const int32_t lj = min(max(gj - L.roi_lo, 0), max(L.roi_n - 1, 0));  // in range unless the ROI offsets are invalid
-    r.cx = L.roi[0][lj];
-    r.cy = L.roi[1][lj];
-    r.cos_yaw = L.roi[2][lj];
-    r.sin_yaw = L.roi[3][lj];
-    r.ext_x = L.roi[4][lj];
-    r.ext_y = L.roi[5][lj];
+    r.cx = lds_roi(c, 0)[lj];
+    r.cy = lds_roi(c, 1)[lj];
+    r.cos_yaw = lds_roi(c, 2)[lj];
+    r.sin_yaw = lds_roi(c, 3)[lj];
+    r.ext_x = lds_roi(c, 4)[lj];
+    r.ext_y = lds_roi(c, 5)[lj];
   } else {
     r = c.rois[gj];
   }
@@ -232,16 +249,18 @@ __device__ __forceinline__ void plan_staging(const Config& c, FilterLds& L, int3
   L.f1 = f1;
   L.roi_lo = min(max(c.roi_off[f0], 0), c.R);
   L.roi_n = min(max(c.roi_off[f1 + 1], L.roi_lo), c.R) - L.roi_lo;
-  L.chunk_staged = nf <= kMaxLdsFrames && nf * c.S <= kMaxPoseLds && nf * c.S * c.W <= kMaxLdsBudgetWords &&
-                   L.roi_n <= kMaxLdsRois && nf * c.ncells <= kMaxLdsCells;
+  L.chunk_staged = nf <= kMaxLdsFrames && nf * c.S <= c.lds_pose_cap && nf * c.S * c.W <= c.lds_bm_cap &&
+                   L.roi_n <= c.lds_roi_cap && nf * c.ncells <= kMaxLdsCells;
 }
 
 __device__ __forceinline__ void do_staging(const Config& c, FilterLds& L) {
   const int tid = threadIdx.x;
   const int32_t nf = L.f1 - L.f0 + 1;
   for (int e = tid; e <= nf; e += kBlock) L.roff[e] = min(max(c.roi_off[L.f0 + e], 0), c.R);
-  for (int e = tid; e < nf * c.S * 12; e += kBlock) (&L.pose[0][0])[e] = c.poses[(int64_t)L.f0 * c.S * 12 + e];
-  for (int e = tid; e < nf * c.S * c.W; e += kBlock) L.bm[e] = c.budgetmask[(int64_t)L.f0 * c.S * c.W + e];
+  float* pose = reinterpret_cast<float*>(filter_dyn);
+  for (int e = tid; e < nf * c.S * 12; e += kBlock) pose[e] = c.poses[(int64_t)L.f0 * c.S * 12 + e];
+  uint32_t* bm = lds_bm(c);
+  for (int e = tid; e < nf * c.S * c.W; e += kBlock) bm[e] = c.budgetmask[(int64_t)L.f0 * c.S * c.W + e];
   {
     // the frames' cell words, four loads in flight per thread
     const uint32_t* src = c.cellany + (int64_t)L.f0 * c.ncells;
@@ -257,12 +276,12 @@ __device__ __forceinline__ void do_staging(const Config& c, FilterLds& L) {
   }
   for (int e = tid; e < L.roi_n; e += kBlock) {
     const mmbev_roi_t r = c.rois[L.roi_lo + e];
-    L.roi[0][e] = r.cx;
-    L.roi[1][e] = r.cy;
-    L.roi[2][e] = r.cos_yaw;
-    L.roi[3][e] = r.sin_yaw;
-    L.roi[4][e] = r.ext_x;
-    L.roi[5][e] = r.ext_y;
+    lds_roi(c, 0)[e] = r.cx;
+    lds_roi(c, 1)[e] = r.cy;
+    lds_roi(c, 2)[e] = r.cos_yaw;
+    lds_roi(c, 3)[e] = r.sin_yaw;
+    lds_roi(c, 4)[e] = r.ext_x;
+    lds_roi(c, 5)[e] = r.ext_y;
   }
 }
 
@@ -310,9 +329,9 @@ __device__ __forceinline__ void phase_a(const Config& c, const FilterLds& L, int
   if (ST && __ballot(!lane_uniform || sq[0] != s0) == 0) {
     // one pose for the whole wave, read as three 16-byte rows
     const int32_t row = (b - L.f0) * (int32_t)S + (int32_t)s0;
-    const float4 r0 = *reinterpret_cast<const float4*>(&L.pose[row][0]);
-    const float4 r1 = *reinterpret_cast<const float4*>(&L.pose[row][4]);
-    const float4 r2 = *reinterpret_cast<const float4*>(&L.pose[row][8]);
+    const float4 r0 = *reinterpret_cast<const float4*>(lds_pose(row));
+    const float4 r1 = *reinterpret_cast<const float4*>(lds_pose(row) + 4);
+    const float4 r2 = *reinterpret_cast<const float4*>(lds_pose(row) + 8);
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
       st.px[q] = fma_rn(r0.x, d.x[q], fma_rn(r0.y, d.y[q], fma_rn(r0.z, d.z[q], r0.w)));
@@ -508,7 +527,7 @@ __device__ __forceinline__ void run_wave(const Config& c, const FilterLds& L, Wa
 // chunk it leaves the bitmap of its kept points, their number, its first
 // point and its frame.  BG: the out-of-ROI keep rate is nonzero.
 template <bool VEC, bool BG>
-__global__ __launch_bounds__(kBlock) void filter_kernel(Config c) {
+__global__ __launch_bounds__(kBlock, 5) void filter_kernel(Config c) {
   __shared__ FilterLds L;
   __shared__ WaveLds Qs[kWaves];
   const int tid = threadIdx.x;
@@ -556,14 +575,15 @@ __global__ __launch_bounds__(kBlock) void filter_kernel(Config c) {
 hipError_t launch_filter(const Config& c, hipStream_t st) {
   // one instance per load form and per rate (none, or a nonzero one)
   const dim3 grid(c.filter_grid), block(kBlock);
+  const size_t dyn = (size_t)c.lds_dyn_bytes;
   if (c.vec && c.bg_thr == 0u)
-    hipLaunchKernelGGL((filter_kernel<true, false>), grid, block, 0, st, c);
+    hipLaunchKernelGGL((filter_kernel<true, false>), grid, block, dyn, st, c);
   else if (c.vec)
-    hipLaunchKernelGGL((filter_kernel<true, true>), grid, block, 0, st, c);
+    hipLaunchKernelGGL((filter_kernel<true, true>), grid, block, dyn, st, c);
   else if (c.bg_thr == 0u)
-    hipLaunchKernelGGL((filter_kernel<false, false>), grid, block, 0, st, c);
+    hipLaunchKernelGGL((filter_kernel<false, false>), grid, block, dyn, st, c);
   else
-    hipLaunchKernelGGL((filter_kernel<false, true>), grid, block, 0, st, c);
+    hipLaunchKernelGGL((filter_kernel<false, true>), grid, block, dyn, st, c);
   return hipGetLastError();
 }
 

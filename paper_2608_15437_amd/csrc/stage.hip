@@ -71,6 +71,11 @@ __device__ void roi_cell_rect(const Config& c, const mmbev_roi_t& r, int16_t* ou
   out[3] = (int16_t)y1;
 }
 
+// Filter chunks of a frame of n points: whole workgroups of kWaves chunks.
+__device__ __forceinline__ uint32_t frame_chunks(uint32_t n, uint32_t P) {
+  return (n + P - 1) / P + kWaves - 1 - ((n + P - 1) / P + kWaves - 1) % kWaves;
+}
+
 // Block (0, 0): counters, offset checks, filter chunk table.
 __device__ void open_call(const Config& c, uint32_t* s_tmp) {
   const int tid = threadIdx.x;
@@ -98,9 +103,10 @@ __device__ void open_call(const Config& c, uint32_t* s_tmp) {
     }
   }
   if (bad) raise_fault(h, bad);
-  // chunks of frame b: ceil(points / fchunk_points); thread t owns frames
-  // [t*per, (t+1)*per); the count is capped at fchunk_max (reached only with
-  // invalid offsets)
+  // chunks of frame b: ceil(points / fchunk_points) rounded up to a whole
+  // filter workgroup (kWaves chunks), so that a workgroup's chunks never span
+  // two frames; thread t owns frames [t*per, (t+1)*per); the count is capped
+  // at fchunk_max (reached only with invalid offsets)
   const uint32_t P = (uint32_t)c.fchunk_points;
   const int per = (c.B + kBlock - 1) / kBlock;
   const int b0 = tid * per;
@@ -109,7 +115,7 @@ __device__ void open_call(const Config& c, uint32_t* s_tmp) {
     const int b = b0 + j;
     if (b < c.B) {
       const uint32_t f0 = point_offset(c, b), f1 = max(point_offset(c, b + 1), f0);
-      mine += (f1 - f0 + P - 1) / P;
+      mine += frame_chunks(f1 - f0, P);
     }
   }
   uint32_t total;
@@ -120,7 +126,7 @@ __device__ void open_call(const Config& c, uint32_t* s_tmp) {
     if (b < c.B) {
       c.fchunk_first[b] = min(run, cap);
       const uint32_t f0 = point_offset(c, b), f1 = max(point_offset(c, b + 1), f0);
-      run += (f1 - f0 + P - 1) / P;
+      run += frame_chunks(f1 - f0, P);
     }
   }
   if (tid == 0) {

@@ -343,13 +343,15 @@ mmbev_status_t voxelize(const mmbev_points_t* points, const uint8_t* sweep_ids, 
   c.fchunk_words = (int32_t)(p.fchunk_points / 32);
   c.fchunk_max = (int32_t)p.fchunk_max;
   c.filter_grid = (int32_t)p.filter_grid;
-  // one frame per filter workgroup: its poses, ROI records and budget masks
+  // one frame per filter workgroup: its poses, ROI records, budget masks and cell words
   c.lds_pose_cap = p.S <= kMaxPoseLds ? p.S : 0;
   c.lds_roi_cap = std::max(1, std::min(p.max_rois, kMaxLdsRois));
   c.lds_bm_cap = p.S * p.W <= kMaxLdsBudgetWords ? p.S * p.W : 0;
+  c.lds_cell_cap = p.ncells <= kMaxLdsCells ? p.ncells : 0;
   c.lds_roi = c.lds_pose_cap * 12;
   c.lds_bm = c.lds_roi + 6 * c.lds_roi_cap;
-  c.lds_dyn_bytes = (int32_t)(((size_t)(c.lds_bm + c.lds_bm_cap) * 4 + 15) / 16 * 16);
+  c.lds_cell = c.lds_bm + c.lds_bm_cap;
+  c.lds_dyn_bytes = (int32_t)(((size_t)(c.lds_cell + c.lds_cell_cap) * 4 + 15) / 16 * 16);
   c.schunk_max = (int32_t)p.schunk_max;
   c.mean_grid = (int32_t)p.mean_grid;
 

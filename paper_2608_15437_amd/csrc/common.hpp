@@ -17,7 +17,7 @@ constexpr int kWaves = kBlock / 64;
 // point filter
 constexpr int kWaveTile = 256;        // points per filter wave tile (64 lanes x 4)
 constexpr int kWaveQueue = 128;       // candidate ring of one filter wave (power of two, >= 128)
-constexpr int kFilterDepth = 4;       // register buffers of a filter wave's tile pipeline (>= 2)
+constexpr int kFilterDepth = 2;       // register buffers of a filter wave's tile pipeline (>= 2)
 constexpr int kFilterWaveTarget = 16384;  // filter wave chunks aimed for (a few per resident wave: balance)
 constexpr int kMaxChunkPoints = 4096;  // points of one filter chunk at most
 constexpr int kChunkWords = kMaxChunkPoints / 32;  // words of a chunk's kept bitmap
@@ -123,8 +123,9 @@ struct Config {
   int32_t filter_grid;     // ceil(fchunk_max / kWaves) workgroups, one chunk per wave
   // the filter's dynamic LDS: pose rows, ROI records (six rows of
   // lds_roi_cap floats from float offset lds_roi), budget-mask words (from
-  // word offset lds_bm); a cap of 0 means "not staged"
-  int32_t lds_pose_cap, lds_roi_cap, lds_bm_cap, lds_roi, lds_bm, lds_dyn_bytes;
+  // word offset lds_bm), the frame's cell words (lds_cell_cap from word
+  // offset lds_cell); a cap of 0 means "not staged"
+  int32_t lds_pose_cap, lds_roi_cap, lds_bm_cap, lds_cell_cap, lds_roi, lds_bm, lds_cell, lds_dyn_bytes;
   int32_t schunk_max;      // bound on pair chunks: kSortGrid + B
   int32_t mean_grid;
 };

@@ -46,12 +46,10 @@ namespace {
 
 // Tables of the workgroup's frames f0..f1 (one frame unless the point
 // offsets are invalid: a frame's chunks fill whole workgroups), staged once
-// and shared by its waves.  The cell maps have a fixed size; the poses, ROI
-// records and budget masks go to the dynamic LDS, sized for the call (the
-// sweeps and ROIs of one frame), so that a workgroup takes no more LDS than
-// its frame needs and five of them fit a compute unit.
+// and shared by its waves.  The poses, ROI records, budget masks and cell
+// words go to the dynamic LDS, sized for the call (one frame's sweeps, ROIs
+// and cells), so that a workgroup takes no more LDS than its frame needs.
 struct alignas(16) FilterLds {
-  uint32_t cell[kMaxLdsCells];  // candidate-ROI word of every coarse cell, frame after frame
   int32_t roff[kMaxLdsFrames + 1];  // ROI offsets clamped to [0, R]
   int32_t f0, f1, roi_lo, roi_n;
   int32_t chunk_staged;
@@ -59,7 +57,8 @@ struct alignas(16) FilterLds {
 
 // Dynamic LDS: pose rows [c.lds_pose_cap][12] (48-byte rows: three aligned
 // 16-byte reads each), then the ROI records as six rows of c.lds_roi_cap
-// (cx, cy, cos, sin, ext_x, ext_y), then c.lds_bm_cap budget-mask words.
+// (cx, cy, cos, sin, ext_x, ext_y), then c.lds_bm_cap budget-mask words, then
+// c.lds_cell_cap cell words (the candidate-ROI word of every coarse cell).
 extern __shared__ float4 filter_dyn[];
 
 __device__ __forceinline__ const float* lds_pose(int32_t row) {
@@ -70,6 +69,9 @@ __device__ __forceinline__ float* lds_roi(const Config& c, int k) {
 }
 __device__ __forceinline__ uint32_t* lds_bm(const Config& c) {
   return reinterpret_cast<uint32_t*>(filter_dyn) + c.lds_bm;
+}
+__device__ __forceinline__ uint32_t* lds_cell(const Config& c) {
+  return reinterpret_cast<uint32_t*>(filter_dyn) + c.lds_cell;
 }
 
 // Per-wave state in LDS: the candidate queue (a ring) and the kept bitmap
@@ -250,7 +252,7 @@ __device__ __forceinline__ void plan_staging(const Config& c, FilterLds& L, int3
   L.roi_lo = min(max(c.roi_off[f0], 0), c.R);
   L.roi_n = min(max(c.roi_off[f1 + 1], L.roi_lo), c.R) - L.roi_lo;
   L.chunk_staged = nf <= kMaxLdsFrames && nf * c.S <= c.lds_pose_cap && nf * c.S * c.W <= c.lds_bm_cap &&
-                   L.roi_n <= c.lds_roi_cap && nf * c.ncells <= kMaxLdsCells;
+                   L.roi_n <= c.lds_roi_cap && nf * c.ncells <= c.lds_cell_cap;
 }
 
 __device__ __forceinline__ void do_staging(const Config& c, FilterLds& L) {
@@ -264,6 +266,7 @@ __device__ __forceinline__ void do_staging(const Config& c, FilterLds& L) {
   {
     // the frames' cell words, four loads in flight per thread
     const uint32_t* src = c.cellany + (int64_t)L.f0 * c.ncells;
+    uint32_t* cell = lds_cell(c);
     const int n = nf * c.ncells;
     for (int e0 = tid; e0 < n; e0 += 4 * kBlock) {
       uint32_t v[4];
@@ -271,7 +274,7 @@ __device__ __forceinline__ void do_staging(const Config& c, FilterLds& L) {
       for (int j = 0; j < 4; ++j) v[j] = e0 + j * kBlock < n ? src[e0 + j * kBlock] : 0u;
 #pragma unroll
       for (int j = 0; j < 4; ++j)
-        if (e0 + j * kBlock < n) L.cell[e0 + j * kBlock] = v[j];
+        if (e0 + j * kBlock < n) cell[e0 + j * kBlock] = v[j];
     }
   }
   for (int e = tid; e < L.roi_n; e += kBlock) {
@@ -290,14 +293,31 @@ __device__ __forceinline__ void do_staging(const Config& c, FilterLds& L) {
 // small fraction of a voxel of the exact (x' - min) / v; the cell rectangles
 // of the ROIs are padded by cell_pad voxels, so a point the exact test keeps
 // always finds its ROI here.
-__device__ __forceinline__ int32_t approx_cell(const Config& c, float px, float py) {
-  const int32_t ix = (int32_t)fma_rn(px, c.inv_vs[0], c.nmin_v[0]);
-  const int32_t iy = (int32_t)fma_rn(py, c.inv_vs[1], c.nmin_v[1]);
-  const bool ok = (uint32_t)(ix + c.cell_pad) < (uint32_t)c.Dx + 2u * (uint32_t)c.cell_pad &&
-                  (uint32_t)(iy + c.cell_pad) < (uint32_t)c.Dy + 2u * (uint32_t)c.cell_pad;
-  const int32_t ax = min(max(ix, 0), (int32_t)c.Dx - 1) >> c.cell_shift;
-  const int32_t ay = min(max(iy, 0), (int32_t)c.Dy - 1) >> c.cell_shift;
-  return ok ? ay * c.ncx + ax : -1;
+// The constants of approx_cell, held in vector registers for the whole tile
+// loop: the loop's scalar registers run out (the compiler then spills them
+// to vector lanes and reads them back on every use), and an instruction
+// reads at most one scalar operand, so a scalar addend costs a move anyway.
+struct CellConsts {
+  float inv_x, inv_y, nmin_x, nmin_y;
+  int32_t pad, span_x, span_y, max_x, max_y, shift, ncx;
+};
+
+__device__ __forceinline__ CellConsts cell_consts(const Config& c) {
+  CellConsts k{c.inv_vs[0], c.inv_vs[1], c.nmin_v[0], c.nmin_v[1], c.cell_pad,
+               (int32_t)c.Dx + 2 * c.cell_pad, (int32_t)c.Dy + 2 * c.cell_pad, (int32_t)c.Dx - 1,
+               (int32_t)c.Dy - 1, c.cell_shift, c.ncx};
+  asm volatile("" : "+v"(k.inv_x), "+v"(k.inv_y), "+v"(k.nmin_x), "+v"(k.nmin_y), "+v"(k.pad), "+v"(k.span_x),
+               "+v"(k.span_y), "+v"(k.max_x), "+v"(k.max_y), "+v"(k.shift), "+v"(k.ncx));
+  return k;
+}
+
+__device__ __forceinline__ int32_t approx_cell(const CellConsts& k, float px, float py) {
+  const int32_t ix = (int32_t)fma_rn(px, k.inv_x, k.nmin_x);
+  const int32_t iy = (int32_t)fma_rn(py, k.inv_y, k.nmin_y);
+  const bool ok = (uint32_t)(ix + k.pad) < (uint32_t)k.span_x && (uint32_t)(iy + k.pad) < (uint32_t)k.span_y;
+  const int32_t ax = min(max(ix, 0), k.max_x) >> k.shift;
+  const int32_t ay = min(max(iy, 0), k.max_y) >> k.shift;
+  return ok ? ay * k.ncx + ax : -1;
 }
 
 // Per-lane state of four points between their two phases.
@@ -314,8 +334,8 @@ struct QuadState {
 // BG: the out-of-ROI keep rate is nonzero (without it no draw is made and
 // the code below is the ROI-only path).
 template <bool ST, bool BG>
-__device__ __forceinline__ void phase_a(const Config& c, const FilterLds& L, int32_t b, uint32_t i0, const Quad& d,
-                                        QuadState& st) {
+__device__ __forceinline__ void phase_a(const Config& c, const CellConsts& kc, const FilterLds& L, int32_t b,
+                                        uint32_t i0, const Quad& d, QuadState& st) {
   const uint32_t S = (uint32_t)c.S;
   int32_t cidx[4];
   uint32_t sq[4];
@@ -337,7 +357,7 @@ __device__ __forceinline__ void phase_a(const Config& c, const FilterLds& L, int
       st.px[q] = fma_rn(r0.x, d.x[q], fma_rn(r0.y, d.y[q], fma_rn(r0.z, d.z[q], r0.w)));
       st.py[q] = fma_rn(r1.x, d.x[q], fma_rn(r1.y, d.y[q], fma_rn(r1.z, d.z[q], r1.w)));
       st.pz[q] = fma_rn(r2.x, d.x[q], fma_rn(r2.y, d.y[q], fma_rn(r2.z, d.z[q], r2.w)));
-      cidx[q] = approx_cell(c, st.px[q], st.py[q]);
+      cidx[q] = approx_cell(kc, st.px[q], st.py[q]);
     }
   } else {
 #pragma unroll
@@ -348,7 +368,7 @@ __device__ __forceinline__ void phase_a(const Config& c, const FilterLds& L, int
         float P[12];
         load_pose<ST>(c, L, b, sq[q], P);
         compensate(P, d.x[q], d.y[q], d.z[q], st.px[q], st.py[q], st.pz[q]);
-        cidx[q] = approx_cell(c, st.px[q], st.py[q]);
+        cidx[q] = approx_cell(kc, st.px[q], st.py[q]);
       }
     }
   }
@@ -356,7 +376,7 @@ __device__ __forceinline__ void phase_a(const Config& c, const FilterLds& L, int
 #pragma unroll
   for (int q = 0; q < 4; ++q) {
     const int32_t cell = max(cidx[q], 0);
-    const uint32_t w = ST ? L.cell[(b - L.f0) * c.ncells + cell] : c.cellany[(int64_t)b * c.ncells + cell];
+    const uint32_t w = ST ? lds_cell(c)[(b - L.f0) * c.ncells + cell] : c.cellany[(int64_t)b * c.ncells + cell];
     st.cand[q] = cidx[q] >= 0 ? w : 0u;
   }
   // the out-of-ROI keep draw
@@ -462,7 +482,8 @@ __device__ __forceinline__ void phase_b(const Config& c, const FilterLds& L, Wav
 // fixed trip count and no early exit, so the compiler's wait before a tile's
 // data counts exactly the loads of the tiles after it.
 template <bool ST, bool BG, int J>
-__device__ __forceinline__ void pipeline_step(const Config& c, const FilterLds& L, WaveLds& Q, int32_t b,
+__device__ __forceinline__ void pipeline_step(const Config& c, const CellConsts& kc, const FilterLds& L, WaveLds& Q,
+                                              int32_t b,
                                               uint32_t a0, uint32_t ntiles, uint32_t k0, uint32_t lane4,
                                               Quad (&buf)[kFilterDepth], QuadState& st, WaveRun& wr) {
   const uint32_t k = k0 + (uint32_t)J;
@@ -470,7 +491,7 @@ __device__ __forceinline__ void pipeline_step(const Config& c, const FilterLds& 
   const uint32_t tile = k - (uint32_t)(kFilterDepth - 1);  // wraps for the first steps
   if (tile < ntiles) {
     const uint32_t t = a0 + tile * kWaveTile;
-    phase_a<ST, BG>(c, L, b, t + lane4, buf[(J + 1) % kFilterDepth], st);
+    phase_a<ST, BG>(c, kc, L, b, t + lane4, buf[(J + 1) % kFilterDepth], st);
     phase_b<ST, BG>(c, L, Q, t + lane4, st, wr);
   }
 }
@@ -487,6 +508,7 @@ __device__ __forceinline__ void run_wave(const Config& c, const FilterLds& L, Wa
   const uint32_t lane = (uint32_t)(threadIdx.x & 63), lane4 = 4u * lane;
   Quad buf[kFilterDepth];
   QuadState st;
+  const CellConsts kc = cell_consts(c);
   static_assert(kChunkWords == 128, "two bitmap words per lane");
   Q.bits[lane] = 0;
   Q.bits[lane + 64] = 0;
@@ -494,7 +516,7 @@ __device__ __forceinline__ void run_wave(const Config& c, const FilterLds& L, Wa
   const uint32_t a0 = VEC ? min((lo + 3u) & ~3u, hi) : lo;
   if (a0 > lo) {  // head: fewer than 4 points
     load_quad_scalar(c, lo + lane4, a0, buf[0]);
-    phase_a<ST, BG>(c, L, b, lo + lane4, buf[0], st);
+    phase_a<ST, BG>(c, kc, L, b, lo + lane4, buf[0], st);
     phase_b<ST, BG>(c, L, Q, lo + lane4, st, wr);
   }
   const uint32_t ntiles = VEC ? (hi - a0) / kWaveTile : 0u;
@@ -502,17 +524,17 @@ __device__ __forceinline__ void run_wave(const Config& c, const FilterLds& L, Wa
   if (ntiles > 0) {
     const uint32_t steps = ntiles + (uint32_t)(kFilterDepth - 1);
     for (uint32_t k0 = 0; k0 < steps; k0 += kFilterDepth) {
-      pipeline_step<ST, BG, 0>(c, L, Q, b, a0, ntiles, k0, lane4, buf, st, wr);
-      pipeline_step<ST, BG, 1>(c, L, Q, b, a0, ntiles, k0, lane4, buf, st, wr);
-      if constexpr (kFilterDepth > 2) pipeline_step<ST, BG, 2 % kFilterDepth>(c, L, Q, b, a0, ntiles, k0, lane4, buf, st, wr);
-      if constexpr (kFilterDepth > 3) pipeline_step<ST, BG, 3 % kFilterDepth>(c, L, Q, b, a0, ntiles, k0, lane4, buf, st, wr);
-      if constexpr (kFilterDepth > 4) pipeline_step<ST, BG, 4 % kFilterDepth>(c, L, Q, b, a0, ntiles, k0, lane4, buf, st, wr);
-      if constexpr (kFilterDepth > 5) pipeline_step<ST, BG, 5 % kFilterDepth>(c, L, Q, b, a0, ntiles, k0, lane4, buf, st, wr);
+      pipeline_step<ST, BG, 0>(c, kc, L, Q, b, a0, ntiles, k0, lane4, buf, st, wr);
+      pipeline_step<ST, BG, 1>(c, kc, L, Q, b, a0, ntiles, k0, lane4, buf, st, wr);
+      if constexpr (kFilterDepth > 2) pipeline_step<ST, BG, 2 % kFilterDepth>(c, kc, L, Q, b, a0, ntiles, k0, lane4, buf, st, wr);
+      if constexpr (kFilterDepth > 3) pipeline_step<ST, BG, 3 % kFilterDepth>(c, kc, L, Q, b, a0, ntiles, k0, lane4, buf, st, wr);
+      if constexpr (kFilterDepth > 4) pipeline_step<ST, BG, 4 % kFilterDepth>(c, kc, L, Q, b, a0, ntiles, k0, lane4, buf, st, wr);
+      if constexpr (kFilterDepth > 5) pipeline_step<ST, BG, 5 % kFilterDepth>(c, kc, L, Q, b, a0, ntiles, k0, lane4, buf, st, wr);
     }
   }
   for (uint32_t t = a0 + ntiles * kWaveTile; t < hi; t += kWaveTile) {
     load_quad_scalar(c, t + lane4, hi, buf[0]);
-    phase_a<ST, BG>(c, L, b, t + lane4, buf[0], st);
+    phase_a<ST, BG>(c, kc, L, b, t + lane4, buf[0], st);
     phase_b<ST, BG>(c, L, Q, t + lane4, st, wr);
   }
   while (wr.queued > 0) decide_round<ST, BG>(c, L, Q, wr, min(wr.queued, 64u));

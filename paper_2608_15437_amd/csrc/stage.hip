@@ -9,11 +9,12 @@
 // word.  Cell ranges are conservative (padded by more than the fp32 error of
 // the exact test), so the exact test alone decides membership.
 //
-// Block (0, 0) also opens the call: it bumps the call counter, clears the
-// per-call counters, checks the frame offsets of points and ROIs, and lays
-// out the filter's work: every frame is cut into chunks of fchunk_points
-// points (the last one shorter), numbered frame after frame, so no chunk
-// straddles two frames.
+// One more workgroup (the last column of frame 0's row; the rest of that
+// column exits) opens the call in parallel with the frames' work: it bumps
+// the call counter, clears the per-call counters, checks the frame offsets
+// of points and ROIs, and lays out the filter's work: every frame is cut
+// into chunks of fchunk_points points (the last one shorter), numbered frame
+// after frame, so no chunk straddles two frames.
 #include "launch.hpp"
 
 namespace mmbev {
@@ -76,7 +77,7 @@ __device__ __forceinline__ uint32_t frame_chunks(uint32_t n, uint32_t P) {
   return (n + P - 1) / P + kWaves - 1 - ((n + P - 1) / P + kWaves - 1) % kWaves;
 }
 
-// Block (0, 0): counters, offset checks, filter chunk table.
+// The opening workgroup: counters, offset checks, filter chunk table.
 __device__ void open_call(const Config& c, uint32_t* s_tmp) {
   const int tid = threadIdx.x;
   WsHeader* h = c.hdr;
@@ -140,7 +141,10 @@ __global__ __launch_bounds__(kBlock) void stage_kernel(Config c) {
   __shared__ uint32_t s_tmp[kWaves];
   const int tid = threadIdx.x;
   const int b = blockIdx.y;
-  if (blockIdx.x == 0 && b == 0) open_call(c, s_tmp);
+  if (blockIdx.x == gridDim.x - 1) {  // the extra column opens the call, beside the frames' work
+    if (b == 0) open_call(c, s_tmp);
+    return;
+  }
 
   // ROIs of frame b (offsets clamped into [0, R], count into [0, max_rois])
   const int32_t r0 = min(max(c.roi_off[b], 0), c.R);
@@ -151,7 +155,7 @@ __global__ __launch_bounds__(kBlock) void stage_kernel(Config c) {
 
   // cells: each thread owns kStageCellsPerThread cells at a time and walks
   // the frame's ROI rectangles once for all of them
-  const int32_t stride = (int32_t)gridDim.x * kBlock;
+  const int32_t stride = (int32_t)(gridDim.x - 1) * kBlock;  // without the opening column
   const int64_t cell_words = (int64_t)c.ncells * c.W;
   for (int32_t g0 = (int32_t)blockIdx.x * kBlock + tid; g0 < c.ncells; g0 += stride * kStageCellsPerThread) {
     int32_t cx[kStageCellsPerThread], cy[kStageCellsPerThread];
@@ -214,7 +218,7 @@ hipError_t launch_stage(const Config& c, hipStream_t st) {
   const int64_t work = std::max<int64_t>((int64_t)c.ncells, (int64_t)c.S * c.W);
   const int gx = (int)std::min<int64_t>(
       std::max<int64_t>(1, (work + kBlock * kStageCellsPerThread - 1) / (kBlock * kStageCellsPerThread)), 64);
-  hipLaunchKernelGGL(stage_kernel, dim3(gx, c.B), dim3(kBlock), 0, st, c);
+  hipLaunchKernelGGL(stage_kernel, dim3(gx + 1, c.B), dim3(kBlock), 0, st, c);
   return hipGetLastError();
 }
 

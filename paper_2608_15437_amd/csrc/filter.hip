@@ -297,40 +297,61 @@ __device__ __forceinline__ void do_staging(const Config& c, FilterLds& L) {
 // loop: the loop's scalar registers run out (the compiler then spills them
 // to vector lanes and reads them back on every use), and an instruction
 // reads at most one scalar operand, so a scalar addend costs a move anyway.
+// With them, the wave's frame row in the staged tables (fr = b - f0) and
+// the LDS word index of its cell words, so that the tile loop does not read
+// the workgroup's first frame back from LDS.
 struct CellConsts {
   float inv_x, inv_y, nmin_x, nmin_y;
   int32_t pad, span_x, span_y, max_x, max_y, shift, ncx;
+  int32_t cell_row;  // staged: word index of frame fr's cell words in the dynamic LDS
+  int32_t fr;        // staged: b - f0
 };
 
-__device__ __forceinline__ CellConsts cell_consts(const Config& c) {
+template <bool ST>
+__device__ __forceinline__ CellConsts cell_consts(const Config& c, const FilterLds& L, int32_t b) {
+  const int32_t fr = ST ? b - L.f0 : 0;
   CellConsts k{c.inv_vs[0], c.inv_vs[1], c.nmin_v[0], c.nmin_v[1], c.cell_pad,
                (int32_t)c.Dx + 2 * c.cell_pad, (int32_t)c.Dy + 2 * c.cell_pad, (int32_t)c.Dx - 1,
-               (int32_t)c.Dy - 1, c.cell_shift, c.ncx};
+               (int32_t)c.Dy - 1, c.cell_shift, c.ncx, c.lds_cell + fr * c.ncells, fr};
   asm volatile("" : "+v"(k.inv_x), "+v"(k.inv_y), "+v"(k.nmin_x), "+v"(k.nmin_y), "+v"(k.pad), "+v"(k.span_x),
-               "+v"(k.span_y), "+v"(k.max_x), "+v"(k.max_y), "+v"(k.shift), "+v"(k.ncx));
+               "+v"(k.span_y), "+v"(k.max_x), "+v"(k.max_y), "+v"(k.shift), "+v"(k.ncx), "+v"(k.cell_row));
   return k;
 }
+
+// v into [0, hi] in one instruction (the compiler forms the median only for
+// constant bounds).
+__device__ __forceinline__ uint32_t clamp0(int32_t v, int32_t hi) {
+  int32_t r;
+  asm("v_med3_i32 %0, %1, 0, %2" : "=v"(r) : "v"(v), "v"(hi));
+  return (uint32_t)r;
+}
+
+static_assert(kMaxCellSide < (1 << 24), "cell coordinates fit the 24-bit multiply");
 
 __device__ __forceinline__ int32_t approx_cell(const CellConsts& k, float px, float py) {
   const int32_t ix = (int32_t)fma_rn(px, k.inv_x, k.nmin_x);
   const int32_t iy = (int32_t)fma_rn(py, k.inv_y, k.nmin_y);
   const bool ok = (uint32_t)(ix + k.pad) < (uint32_t)k.span_x && (uint32_t)(iy + k.pad) < (uint32_t)k.span_y;
-  const int32_t ax = min(max(ix, 0), k.max_x) >> k.shift;
-  const int32_t ay = min(max(iy, 0), k.max_y) >> k.shift;
-  return ok ? ay * k.ncx + ax : -1;
+  const uint32_t ax = clamp0(ix, k.max_x) >> k.shift;
+  const uint32_t ay = clamp0(iy, k.max_y) >> k.shift;
+  uint32_t cell = __umul24(ay, (uint32_t)k.ncx) + ax;
+  asm volatile("" : "+v"(cell));  // a select, not a branch around three instructions
+  return ok ? (int32_t)cell : -1;
 }
 
 // Per-lane state of four points between their two phases.
 struct QuadState {
   float px[4], py[4], pz[4];  // p' (Eq. 6), exact
   uint32_t sw[4];             // sweep
-  uint32_t cand[4];           // candidate-ROI word after phase A (0: none)
+  uint32_t cand[4];           // candidate-ROI word after phase A (0: none); with one ROI word, budget applied
   uint32_t bg;                // bit q: point q is drawn for the out-of-ROI keep
 };
 
 // Phase A of four points of a lane (first index i0, frame b for the whole
 // wave): p' and the candidate-ROI word of each point's cell (from LDS when
-// staged, so that the only global loads in flight are the point tiles).
+// staged, so that the only global loads in flight are the point tiles),
+// ANDed with the sweep's budget word when the frame's ROIs fit one word (a
+// single wave-wide read when the wave holds one sweep).
 // BG: the out-of-ROI keep rate is nonzero (without it no draw is made and
 // the code below is the ROI-only path).
 template <bool ST, bool BG>
@@ -338,7 +359,7 @@ __device__ __forceinline__ void phase_a(const Config& c, const CellConsts& kc, c
                                         uint32_t i0, const Quad& d, QuadState& st) {
   const uint32_t S = (uint32_t)c.S;
   int32_t cidx[4];
-  uint32_t sq[4];
+  uint32_t sq[4], bw[4];
 #pragma unroll
   for (int q = 0; q < 4; ++q) {
     sq[q] = (d.s >> (8 * q)) & 0xffu;
@@ -348,12 +369,14 @@ __device__ __forceinline__ void phase_a(const Config& c, const CellConsts& kc, c
   const uint32_t s0 = __builtin_amdgcn_readfirstlane(sq[0]);
   if (ST && __ballot(!lane_uniform || sq[0] != s0) == 0) {
     // one pose for the whole wave, read as three 16-byte rows
-    const int32_t row = (b - L.f0) * (int32_t)S + (int32_t)s0;
+    const int32_t row = kc.fr * (int32_t)S + (int32_t)s0;
     const float4 r0 = *reinterpret_cast<const float4*>(lds_pose(row));
     const float4 r1 = *reinterpret_cast<const float4*>(lds_pose(row) + 4);
     const float4 r2 = *reinterpret_cast<const float4*>(lds_pose(row) + 8);
+    const uint32_t w0 = c.W == 1 ? lds_bm(c)[kc.fr * c.S + s0] : ~0u;
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
+      bw[q] = w0;
       st.px[q] = fma_rn(r0.x, d.x[q], fma_rn(r0.y, d.y[q], fma_rn(r0.z, d.z[q], r0.w)));
       st.py[q] = fma_rn(r1.x, d.x[q], fma_rn(r1.y, d.y[q], fma_rn(r1.z, d.z[q], r1.w)));
       st.pz[q] = fma_rn(r2.x, d.x[q], fma_rn(r2.y, d.y[q], fma_rn(r2.z, d.z[q], r2.w)));
@@ -363,8 +386,10 @@ __device__ __forceinline__ void phase_a(const Config& c, const CellConsts& kc, c
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
       cidx[q] = -1;
+      bw[q] = 0u;
       st.px[q] = st.py[q] = st.pz[q] = 0.0f;
       if (sq[q] < S) {
+        bw[q] = c.W == 1 ? budget_word<ST>(c, L, b, sq[q], 0) : ~0u;
         float P[12];
         load_pose<ST>(c, L, b, sq[q], P);
         compensate(P, d.x[q], d.y[q], d.z[q], st.px[q], st.py[q], st.pz[q]);
@@ -372,13 +397,19 @@ __device__ __forceinline__ void phase_a(const Config& c, const CellConsts& kc, c
       }
     }
   }
-  // the four cell words (always in bounds)
+  // the four cell words (always in bounds), read by every lane so that the
+  // four reads are in flight together (the compiler would otherwise move
+  // each into a branch of its own and wait for it there)
+  uint32_t w[4];
 #pragma unroll
   for (int q = 0; q < 4; ++q) {
     const int32_t cell = max(cidx[q], 0);
-    const uint32_t w = ST ? lds_cell(c)[(b - L.f0) * c.ncells + cell] : c.cellany[(int64_t)b * c.ncells + cell];
-    st.cand[q] = cidx[q] >= 0 ? w : 0u;
+    w[q] = ST ? reinterpret_cast<const uint32_t*>(filter_dyn)[kc.cell_row + cell]
+              : c.cellany[(int64_t)b * c.ncells + cell];
   }
+  asm volatile("" : "+v"(w[0]), "+v"(w[1]), "+v"(w[2]), "+v"(w[3]));
+#pragma unroll
+  for (int q = 0; q < 4; ++q) st.cand[q] = cidx[q] >= 0 ? w[q] & bw[q] : 0u;
   // the out-of-ROI keep draw
   st.bg = 0;
   if (BG)
@@ -430,18 +461,13 @@ __device__ __forceinline__ void decide_round(const Config& c, const FilterLds& L
   wave_lds_sync();  // slots read before they are written again
 }
 
-// Phase B of four points of a lane: budget masks, then the candidates (a
-// candidate ROI that admits the sweep, or drawn for the out-of-ROI keep)
+// Phase B of four points of a lane: the candidates (a candidate ROI that
+// admits the sweep, or drawn for the out-of-ROI keep)
 // appended in point order (lane, then q) to the wave's ring, deciding full
 // rounds of 64 as they become available.
 template <bool ST, bool BG>
 __device__ __forceinline__ void phase_b(const Config& c, const FilterLds& L, WaveLds& Q, uint32_t i0,
                                         QuadState& st, WaveRun& wr) {
-  if (c.W == 1) {
-#pragma unroll
-    for (int q = 0; q < 4; ++q)
-      if (st.cand[q]) st.cand[q] &= budget_word<ST>(c, L, wr.b, st.sw[q], 0);
-  }
   bool has[4];
 #pragma unroll
   for (int q = 0; q < 4; ++q) has[q] = st.cand[q] != 0u || (BG && ((st.bg >> q) & 1u));
@@ -508,7 +534,7 @@ __device__ __forceinline__ void run_wave(const Config& c, const FilterLds& L, Wa
   const uint32_t lane = (uint32_t)(threadIdx.x & 63), lane4 = 4u * lane;
   Quad buf[kFilterDepth];
   QuadState st;
-  const CellConsts kc = cell_consts(c);
+  const CellConsts kc = cell_consts<ST>(c, L, b);
   static_assert(kChunkWords == 128, "two bitmap words per lane");
   Q.bits[lane] = 0;
   Q.bits[lane + 64] = 0;

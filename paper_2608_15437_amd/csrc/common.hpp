@@ -95,6 +95,7 @@ struct Config {
   uint32_t* fcount;        // [fchunk_max] kept points of filter chunk k
   uint32_t* fchunk_lo;     // [fchunk_max] first point of filter chunk k
   uint32_t* fchunk_frame;  // [fchunk_max] frame of filter chunk k
+  uint32_t* wg_frame;      // [filter_grid] frame of filter workgroup g's first chunk (kNoFrame: no chunk)
   uint32_t* fprefix;       // [fchunk_max + 1] kept pairs of the filter chunks before k
   uint32_t* fstart;        // [B+1] first sorted pair of frame b (kept pairs of the frames before it)
   uint32_t* schunk_first;  // [B+1] first pair chunk of frame b
@@ -123,8 +124,9 @@ struct Config {
   int32_t filter_grid;     // ceil(fchunk_max / kWaves) workgroups, one chunk per wave
   // the filter's dynamic LDS: pose rows, ROI records (six rows of
   // lds_roi_cap floats from float offset lds_roi), budget-mask words (from
-  // word offset lds_bm), the frame's cell words (lds_cell_cap from word
-  // offset lds_cell); a cap of 0 means "not staged"
+  // word offset lds_bm), the frame's cell row (lds_cell_cap words from word
+  // offset lds_cell: a zero word, then the cell words); a cap of 0 means
+  // "not staged"
   int32_t lds_pose_cap, lds_roi_cap, lds_bm_cap, lds_cell_cap, lds_roi, lds_bm, lds_cell, lds_dyn_bytes;
   int32_t schunk_max;      // bound on pair chunks: kSortGrid + B
   int32_t mean_grid;
@@ -164,6 +166,8 @@ __device__ __forceinline__ uint32_t block_exclusive_scan(uint32_t v, uint32_t* s
   total = tot;
   return wpre + x - v;
 }
+
+constexpr uint32_t kNoFrame = 0xffffffffu;  // wg_frame of a filter workgroup past the last chunk
 
 // Largest b in [0, B-1] with first[b] <= k (first[] non-decreasing): the
 // frame of chunk k, skipping frames without chunks.

@@ -58,7 +58,8 @@ struct alignas(16) FilterLds {
 // Dynamic LDS: pose rows [c.lds_pose_cap][12] (48-byte rows: three aligned
 // 16-byte reads each), then the ROI records as six rows of c.lds_roi_cap
 // (cx, cy, cos, sin, ext_x, ext_y), then c.lds_bm_cap budget-mask words, then
-// c.lds_cell_cap cell words (the candidate-ROI word of every coarse cell).
+// rows of c.ncells + 1 words per frame: a zero word, read for points outside
+// the grid, then the candidate-ROI word of every coarse cell.
 extern __shared__ float4 filter_dyn[];
 
 __device__ __forceinline__ const float* lds_pose(int32_t row) {
@@ -217,13 +218,36 @@ struct Quad {
   uint32_t s;  // four sweep ids, one byte each (0xff: no point)
 };
 
-// Four points with 16-byte loads: exactly four loads per lane, so the
-// compiler's wait counts stay exact across the loop.
-__device__ __forceinline__ void load_quad_vec(const Config& c, uint32_t i0, Quad& d) {
-  const float4 x4 = *reinterpret_cast<const float4*>(c.feat + i0);
-  const float4 y4 = *reinterpret_cast<const float4*>(c.feat + c.stride + i0);
-  const float4 z4 = *reinterpret_cast<const float4*>(c.feat + 2 * c.stride + i0);
-  d.s = *reinterpret_cast<const uint32_t*>(c.sweep + i0);
+// The x, y, z and sweep rows from the first point of a wave's full tiles:
+// wave-uniform bases, so that a tile's loads take a 32-bit lane offset.
+struct TileRows {
+  const float* x;
+  const float* y;
+  const float* z;
+  const uint8_t* s;
+};
+
+__device__ __forceinline__ TileRows tile_rows(const Config& c, uint32_t a0) {
+  return TileRows{c.feat + a0, c.feat + c.stride + a0, c.feat + 2 * c.stride + a0, c.sweep + a0};
+}
+
+// Four points with 16-byte loads (point offset off from the rows' first
+// point, below kMaxChunkPoints): exactly four loads per lane, so the
+// compiler's wait counts stay exact across the loop.  The loads are
+// non-temporal: the points are read once, and streaming them through the
+// caches would evict (and force the write-back of) the working set of the
+// kernels around the filter.
+typedef float StreamF4 __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ void load_quad_vec(const TileRows& r, uint32_t off, Quad& d) {
+  const uint32_t byte = off * 4u;
+  const StreamF4 x4 =
+      __builtin_nontemporal_load(reinterpret_cast<const StreamF4*>(reinterpret_cast<const char*>(r.x) + byte));
+  const StreamF4 y4 =
+      __builtin_nontemporal_load(reinterpret_cast<const StreamF4*>(reinterpret_cast<const char*>(r.y) + byte));
+  const StreamF4 z4 =
+      __builtin_nontemporal_load(reinterpret_cast<const StreamF4*>(reinterpret_cast<const char*>(r.z) + byte));
+  d.s = __builtin_nontemporal_load(reinterpret_cast<const uint32_t*>(r.s + off));
   d.x[0] = x4.x; d.x[1] = x4.y; d.x[2] = x4.z; d.x[3] = x4.w;
   d.y[0] = y4.x; d.y[1] = y4.y; d.y[2] = y4.z; d.y[3] = y4.w;
   d.z[0] = z4.x; d.z[1] = z4.y; d.z[2] = z4.z; d.z[3] = z4.w;
@@ -252,40 +276,59 @@ __device__ __forceinline__ void plan_staging(const Config& c, FilterLds& L, int3
   L.roi_lo = min(max(c.roi_off[f0], 0), c.R);
   L.roi_n = min(max(c.roi_off[f1 + 1], L.roi_lo), c.R) - L.roi_lo;
   L.chunk_staged = nf <= kMaxLdsFrames && nf * c.S <= c.lds_pose_cap && nf * c.S * c.W <= c.lds_bm_cap &&
-                   L.roi_n <= c.lds_roi_cap && nf * c.ncells <= c.lds_cell_cap;
+                   L.roi_n <= c.lds_roi_cap && nf * (c.ncells + 1) <= c.lds_cell_cap;
 }
+
+// Every table the workgroup stages, as one index space of 4-byte words
+// (ROI offsets, poses, budget masks, cell words, ROI record fields), so that
+// a thread's loads of all tables are in flight together: kStageBatch words
+// per thread and round, one round for a frame of up to ~3,000 cell words.
+constexpr int kStageBatch = 12;
 
 __device__ __forceinline__ void do_staging(const Config& c, FilterLds& L) {
   const int tid = threadIdx.x;
   const int32_t nf = L.f1 - L.f0 + 1;
-  for (int e = tid; e <= nf; e += kBlock) L.roff[e] = min(max(c.roi_off[L.f0 + e], 0), c.R);
-  float* pose = reinterpret_cast<float*>(filter_dyn);
-  for (int e = tid; e < nf * c.S * 12; e += kBlock) pose[e] = c.poses[(int64_t)L.f0 * c.S * 12 + e];
-  uint32_t* bm = lds_bm(c);
-  for (int e = tid; e < nf * c.S * c.W; e += kBlock) bm[e] = c.budgetmask[(int64_t)L.f0 * c.S * c.W + e];
-  {
-    // the frames' cell words, four loads in flight per thread
-    const uint32_t* src = c.cellany + (int64_t)L.f0 * c.ncells;
-    uint32_t* cell = lds_cell(c);
-    const int n = nf * c.ncells;
-    for (int e0 = tid; e0 < n; e0 += 4 * kBlock) {
-      uint32_t v[4];
+  const int32_t e1 = nf + 1;                   // ROI offsets
+  const int32_t e2 = e1 + nf * c.S * 12;       // poses
+  const int32_t e3 = e2 + nf * c.S * c.W;      // budget masks
+  const int32_t e4 = e3 + nf * c.ncells;       // cell words
+  const int32_t e5 = e4 + 6 * L.roi_n;         // ROI records, six fields each
+  uint32_t* dyn = reinterpret_cast<uint32_t*>(filter_dyn);
+  const uint32_t* poses = reinterpret_cast<const uint32_t*>(c.poses) + (int64_t)L.f0 * c.S * 12;
+  const uint32_t* bms = c.budgetmask + (int64_t)L.f0 * c.S * c.W;
+  const uint32_t* cells = c.cellany + (int64_t)L.f0 * c.ncells;
+  const uint32_t* rois = reinterpret_cast<const uint32_t*>(c.rois + L.roi_lo);
+  for (int32_t e0 = 0; e0 < e5; e0 += kStageBatch * kBlock) {
+    uint32_t v[kStageBatch];
 #pragma unroll
-      for (int j = 0; j < 4; ++j) v[j] = e0 + j * kBlock < n ? src[e0 + j * kBlock] : 0u;
+    for (int j = 0; j < kStageBatch; ++j) {
+      const int32_t e = e0 + j * kBlock + tid;
+      const uint32_t* src = e < e1   ? reinterpret_cast<const uint32_t*>(c.roi_off + L.f0 + e)
+                            : e < e2 ? poses + (e - e1)
+                            : e < e3 ? bms + (e - e2)
+                            : e < e4 ? cells + (e - e3)
+                                     : rois + ((e - e4) / 6) * 8 + (e - e4) % 6;
+      v[j] = e < e5 ? *src : 0u;
+    }
 #pragma unroll
-      for (int j = 0; j < 4; ++j)
-        if (e0 + j * kBlock < n) cell[e0 + j * kBlock] = v[j];
+    for (int j = 0; j < kStageBatch; ++j) {
+      const int32_t e = e0 + j * kBlock + tid;
+      if (e < e1) {
+        L.roff[e] = min(max((int32_t)v[j], 0), c.R);
+      } else if (e < e2) {
+        dyn[e - e1] = v[j];
+      } else if (e < e3) {
+        dyn[c.lds_bm + (e - e2)] = v[j];
+      } else if (e < e4) {
+        const int32_t f = nf == 1 ? 0 : (e - e3) / c.ncells;  // frame f's row: a zero word, then its cells
+        dyn[c.lds_cell + (e - e3) + f + 1] = v[j];
+      } else if (e < e5) {
+        const int32_t r = (e - e4) / 6;
+        dyn[c.lds_roi + ((e - e4) % 6) * c.lds_roi_cap + r] = v[j];
+      }
     }
   }
-  for (int e = tid; e < L.roi_n; e += kBlock) {
-    const mmbev_roi_t r = c.rois[L.roi_lo + e];
-    lds_roi(c, 0)[e] = r.cx;
-    lds_roi(c, 1)[e] = r.cy;
-    lds_roi(c, 2)[e] = r.cos_yaw;
-    lds_roi(c, 3)[e] = r.sin_yaw;
-    lds_roi(c, 4)[e] = r.ext_x;
-    lds_roi(c, 5)[e] = r.ext_y;
-  }
+  for (int32_t f = tid; f < nf; f += kBlock) dyn[c.lds_cell + f * (c.ncells + 1)] = 0u;
 }
 
 // Approximate coarse cell of (x', y') inside its frame for the candidate
@@ -303,7 +346,7 @@ __device__ __forceinline__ void do_staging(const Config& c, FilterLds& L) {
 struct CellConsts {
   float inv_x, inv_y, nmin_x, nmin_y;
   int32_t pad, span_x, span_y, max_x, max_y, shift, ncx;
-  int32_t cell_row;  // staged: word index of frame fr's cell words in the dynamic LDS
+  int32_t cell_row;  // staged: word index of frame fr's first cell word in the dynamic LDS
   int32_t fr;        // staged: b - f0
 };
 
@@ -312,7 +355,7 @@ __device__ __forceinline__ CellConsts cell_consts(const Config& c, const FilterL
   const int32_t fr = ST ? b - L.f0 : 0;
   CellConsts k{c.inv_vs[0], c.inv_vs[1], c.nmin_v[0], c.nmin_v[1], c.cell_pad,
                (int32_t)c.Dx + 2 * c.cell_pad, (int32_t)c.Dy + 2 * c.cell_pad, (int32_t)c.Dx - 1,
-               (int32_t)c.Dy - 1, c.cell_shift, c.ncx, c.lds_cell + fr * c.ncells, fr};
+               (int32_t)c.Dy - 1, c.cell_shift, c.ncx, c.lds_cell + fr * (c.ncells + 1) + 1, fr};
   asm volatile("" : "+v"(k.inv_x), "+v"(k.inv_y), "+v"(k.nmin_x), "+v"(k.nmin_y), "+v"(k.pad), "+v"(k.span_x),
                "+v"(k.span_y), "+v"(k.max_x), "+v"(k.max_y), "+v"(k.shift), "+v"(k.ncx), "+v"(k.cell_row));
   return k;
@@ -342,7 +385,7 @@ __device__ __forceinline__ int32_t approx_cell(const CellConsts& k, float px, fl
 // Per-lane state of four points between their two phases.
 struct QuadState {
   float px[4], py[4], pz[4];  // p' (Eq. 6), exact
-  uint32_t sw[4];             // sweep
+  uint32_t s;                 // the four sweep ids, one byte each
   uint32_t cand[4];           // candidate-ROI word after phase A (0: none); with one ROI word, budget applied
   uint32_t bg;                // bit q: point q is drawn for the out-of-ROI keep
 };
@@ -359,15 +402,12 @@ __device__ __forceinline__ void phase_a(const Config& c, const CellConsts& kc, c
                                         uint32_t i0, const Quad& d, QuadState& st) {
   const uint32_t S = (uint32_t)c.S;
   int32_t cidx[4];
-  uint32_t sq[4], bw[4];
-#pragma unroll
-  for (int q = 0; q < 4; ++q) {
-    sq[q] = (d.s >> (8 * q)) & 0xffu;
-    st.sw[q] = sq[q];
-  }
-  const bool lane_uniform = ST && sq[0] < S && sq[1] == sq[0] && sq[2] == sq[0] && sq[3] == sq[0];
-  const uint32_t s0 = __builtin_amdgcn_readfirstlane(sq[0]);
-  if (ST && __ballot(!lane_uniform || sq[0] != s0) == 0) {
+  uint32_t bw[4];
+  st.s = d.s;
+  // one sweep for the whole wave: every lane's four sweep bytes equal the
+  // first lane's first one
+  const uint32_t s0 = __builtin_amdgcn_readfirstlane(d.s) & 0xffu;
+  if (ST && s0 < S && __ballot(d.s != s0 * 0x01010101u) == 0) {
     // one pose for the whole wave, read as three 16-byte rows
     const int32_t row = kc.fr * (int32_t)S + (int32_t)s0;
     const float4 r0 = *reinterpret_cast<const float4*>(lds_pose(row));
@@ -385,37 +425,38 @@ __device__ __forceinline__ void phase_a(const Config& c, const CellConsts& kc, c
   } else {
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
+      const uint32_t sq = (d.s >> (8 * q)) & 0xffu;
       cidx[q] = -1;
       bw[q] = 0u;
       st.px[q] = st.py[q] = st.pz[q] = 0.0f;
-      if (sq[q] < S) {
-        bw[q] = c.W == 1 ? budget_word<ST>(c, L, b, sq[q], 0) : ~0u;
+      if (sq < S) {
+        bw[q] = c.W == 1 ? budget_word<ST>(c, L, b, sq, 0) : ~0u;
         float P[12];
-        load_pose<ST>(c, L, b, sq[q], P);
+        load_pose<ST>(c, L, b, sq, P);
         compensate(P, d.x[q], d.y[q], d.z[q], st.px[q], st.py[q], st.pz[q]);
         cidx[q] = approx_cell(kc, st.px[q], st.py[q]);
       }
     }
   }
-  // the four cell words (always in bounds), read by every lane so that the
-  // four reads are in flight together (the compiler would otherwise move
-  // each into a branch of its own and wait for it there)
-  uint32_t w[4];
+  // the four cell words (always in bounds); staged, cell -1 reads the zero
+  // word in front of the frame's row, so no select is needed
+  if (ST) {
 #pragma unroll
-  for (int q = 0; q < 4; ++q) {
-    const int32_t cell = max(cidx[q], 0);
-    w[q] = ST ? reinterpret_cast<const uint32_t*>(filter_dyn)[kc.cell_row + cell]
-              : c.cellany[(int64_t)b * c.ncells + cell];
+    for (int q = 0; q < 4; ++q)
+      st.cand[q] = reinterpret_cast<const uint32_t*>(filter_dyn)[kc.cell_row + cidx[q]] & bw[q];
+  } else {
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const uint32_t w = c.cellany[(int64_t)b * c.ncells + max(cidx[q], 0)];
+      st.cand[q] = cidx[q] >= 0 ? w & bw[q] : 0u;
+    }
   }
-  asm volatile("" : "+v"(w[0]), "+v"(w[1]), "+v"(w[2]), "+v"(w[3]));
-#pragma unroll
-  for (int q = 0; q < 4; ++q) st.cand[q] = cidx[q] >= 0 ? w[q] & bw[q] : 0u;
   // the out-of-ROI keep draw
   st.bg = 0;
   if (BG)
 #pragma unroll
     for (int q = 0; q < 4; ++q)
-      st.bg |= (cidx[q] >= 0 && sq[q] < S && background_draw(c, i0 + q)) ? 1u << q : 0u;
+      st.bg |= (cidx[q] >= 0 && ((d.s >> (8 * q)) & 0xffu) < S && background_draw(c, i0 + q)) ? 1u << q : 0u;
 }
 
 // Queue and kept-point state of one wave (wave-uniform values).
@@ -485,7 +526,7 @@ __device__ __forceinline__ void phase_b(const Config& c, const FilterLds& L, Wav
       if (has[q]) {
         if (rank - done < take) {
           const uint32_t e = (wr.head + wr.queued + (rank - done)) & (kWaveQueue - 1);
-          Q.pk[e] = (i0 + q - wr.lo) | (st.sw[q] << 16) | (BG ? ((st.bg >> q) & 1u) << 24 : 0u);
+          Q.pk[e] = (i0 + q - wr.lo) | (((st.s >> (8 * q)) & 0xffu) << 16) | (BG ? ((st.bg >> q) & 1u) << 24 : 0u);
           Q.cand[e] = st.cand[q];
           Q.px[e] = st.px[q];
           Q.py[e] = st.py[q];
@@ -509,11 +550,11 @@ __device__ __forceinline__ void phase_b(const Config& c, const FilterLds& L, Wav
 // data counts exactly the loads of the tiles after it.
 template <bool ST, bool BG, int J>
 __device__ __forceinline__ void pipeline_step(const Config& c, const CellConsts& kc, const FilterLds& L, WaveLds& Q,
-                                              int32_t b,
+                                              int32_t b, const TileRows& rows,
                                               uint32_t a0, uint32_t ntiles, uint32_t k0, uint32_t lane4,
                                               Quad (&buf)[kFilterDepth], QuadState& st, WaveRun& wr) {
   const uint32_t k = k0 + (uint32_t)J;
-  load_quad_vec(c, a0 + min(k, ntiles - 1u) * kWaveTile + lane4, buf[J]);
+  load_quad_vec(rows, min(k, ntiles - 1u) * kWaveTile + lane4, buf[J]);
   const uint32_t tile = k - (uint32_t)(kFilterDepth - 1);  // wraps for the first steps
   if (tile < ntiles) {
     const uint32_t t = a0 + tile * kWaveTile;
@@ -548,14 +589,15 @@ __device__ __forceinline__ void run_wave(const Config& c, const FilterLds& L, Wa
   const uint32_t ntiles = VEC ? (hi - a0) / kWaveTile : 0u;
   static_assert(kFilterDepth >= 2 && kFilterDepth <= 6, "pipeline steps written out below");
   if (ntiles > 0) {
+    const TileRows rows = tile_rows(c, a0);
     const uint32_t steps = ntiles + (uint32_t)(kFilterDepth - 1);
     for (uint32_t k0 = 0; k0 < steps; k0 += kFilterDepth) {
-      pipeline_step<ST, BG, 0>(c, kc, L, Q, b, a0, ntiles, k0, lane4, buf, st, wr);
-      pipeline_step<ST, BG, 1>(c, kc, L, Q, b, a0, ntiles, k0, lane4, buf, st, wr);
-      if constexpr (kFilterDepth > 2) pipeline_step<ST, BG, 2 % kFilterDepth>(c, kc, L, Q, b, a0, ntiles, k0, lane4, buf, st, wr);
-      if constexpr (kFilterDepth > 3) pipeline_step<ST, BG, 3 % kFilterDepth>(c, kc, L, Q, b, a0, ntiles, k0, lane4, buf, st, wr);
-      if constexpr (kFilterDepth > 4) pipeline_step<ST, BG, 4 % kFilterDepth>(c, kc, L, Q, b, a0, ntiles, k0, lane4, buf, st, wr);
-      if constexpr (kFilterDepth > 5) pipeline_step<ST, BG, 5 % kFilterDepth>(c, kc, L, Q, b, a0, ntiles, k0, lane4, buf, st, wr);
+      pipeline_step<ST, BG, 0>(c, kc, L, Q, b, rows, a0, ntiles, k0, lane4, buf, st, wr);
+      pipeline_step<ST, BG, 1>(c, kc, L, Q, b, rows, a0, ntiles, k0, lane4, buf, st, wr);
+      if constexpr (kFilterDepth > 2) pipeline_step<ST, BG, 2 % kFilterDepth>(c, kc, L, Q, b, rows, a0, ntiles, k0, lane4, buf, st, wr);
+      if constexpr (kFilterDepth > 3) pipeline_step<ST, BG, 3 % kFilterDepth>(c, kc, L, Q, b, rows, a0, ntiles, k0, lane4, buf, st, wr);
+      if constexpr (kFilterDepth > 4) pipeline_step<ST, BG, 4 % kFilterDepth>(c, kc, L, Q, b, rows, a0, ntiles, k0, lane4, buf, st, wr);
+      if constexpr (kFilterDepth > 5) pipeline_step<ST, BG, 5 % kFilterDepth>(c, kc, L, Q, b, rows, a0, ntiles, k0, lane4, buf, st, wr);
     }
   }
   for (uint32_t t = a0 + ntiles * kWaveTile; t < hi; t += kWaveTile) {
@@ -585,27 +627,44 @@ __global__ __launch_bounds__(kBlock, 5) void filter_kernel(Config c) {
   WaveLds& Q = Qs[wave];
   const uint32_t nchunks = c.hdr->fchunks;
   const uint32_t k0 = (uint32_t)blockIdx.x * kWaves;
+  // frame of chunk k0 (loaded with nchunks); every chunk of the workgroup
+  // lies in it unless the point offsets are invalid (then a search finds
+  // each chunk's frame).  The lookups that depend on the frame are made for
+  // wf before that check, so that they load together with it.
+  const int32_t wf = (int32_t)min(c.wg_frame[blockIdx.x], (uint32_t)c.B - 1u);
 
+  // this wave's chunk and its points, before the staging barriers
+  const uint32_t k = k0 + (uint32_t)wave;
+  int32_t b = 0;
+  uint32_t lo = 0, hi = 0;
+  if (k < nchunks) {
+    b = wf;
+    filter_chunk_points(c, b, k, lo, hi);
+    if (!(k < c.fchunk_first[wf + 1])) {
+      b = frame_of_chunk(c.fchunk_first, c.B, k);
+      filter_chunk_points(c, b, k, lo, hi);
+    }
+    // the same in every lane; uniform bounds keep the tile loop a scalar loop
+    b = __builtin_amdgcn_readfirstlane(b);
+    lo = __builtin_amdgcn_readfirstlane(lo);
+    hi = __builtin_amdgcn_readfirstlane(hi);
+  }
   if (tid == 0) {
     L.f0 = L.f1 = 0;
     L.chunk_staged = 0;
-    if (k0 < nchunks)
-      plan_staging(c, L, frame_of_chunk(c.fchunk_first, c.B, k0),
-                   frame_of_chunk(c.fchunk_first, c.B, min(k0 + kWaves - 1, nchunks - 1)));
+    if (k0 < nchunks) {
+      const uint32_t last = min(k0 + kWaves - 1, nchunks - 1);
+      plan_staging(c, L, wf, wf);
+      if (!(last < c.fchunk_first[wf + 1]))
+        plan_staging(c, L, frame_of_chunk(c.fchunk_first, c.B, k0), frame_of_chunk(c.fchunk_first, c.B, last));
+    }
   }
   __syncthreads();
   const bool staged = __builtin_amdgcn_readfirstlane(L.chunk_staged) != 0;
   if (staged) do_staging(c, L);
   __syncthreads();
 
-  const uint32_t k = k0 + (uint32_t)wave;  // this wave's chunk
   if (k >= nchunks) return;
-  const int32_t b = __builtin_amdgcn_readfirstlane(frame_of_chunk(c.fchunk_first, c.B, k));
-  uint32_t lo, hi;
-  filter_chunk_points(c, b, k, lo, hi);
-  // the same in every lane; uniform bounds keep the tile loop a scalar loop
-  lo = __builtin_amdgcn_readfirstlane(lo);
-  hi = __builtin_amdgcn_readfirstlane(hi);
   WaveRun wr{0u, 0u, 0u, lo, b, k};
   if (staged)
     run_wave<VEC, true, BG>(c, L, Q, b, lo, hi, wr);

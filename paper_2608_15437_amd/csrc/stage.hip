@@ -14,7 +14,9 @@
 // the call counter, clears the per-call counters, checks the frame offsets
 // of points and ROIs, and lays out the filter's work: every frame is cut
 // into chunks of fchunk_points points (the last one shorter), numbered frame
-// after frame, so no chunk straddles two frames.
+// after frame, so no chunk straddles two frames, and every filter workgroup
+// (kWaves consecutive chunks) gets the frame of its first chunk, so that it
+// starts with one table load instead of a search.
 #include "launch.hpp"
 
 namespace mmbev {
@@ -22,6 +24,7 @@ namespace mmbev {
 namespace {
 
 constexpr int kMaxRois = 1024;
+constexpr int kLdsFirst = kMaxRois * 2;  // chunk starts of up to kLdsFirst - 1 frames in the rectangles' LDS
 constexpr int kStageCellsPerThread = 8;
 
 // Conservative cell rectangle [x0, x1] x [y0, y1] of one ROI; empty when x0 > x1.
@@ -77,8 +80,9 @@ __device__ __forceinline__ uint32_t frame_chunks(uint32_t n, uint32_t P) {
   return (n + P - 1) / P + kWaves - 1 - ((n + P - 1) / P + kWaves - 1) % kWaves;
 }
 
-// The opening workgroup: counters, offset checks, filter chunk table.
-__device__ void open_call(const Config& c, uint32_t* s_tmp) {
+// The opening workgroup: counters, offset checks, filter chunk table and
+// the frame of every filter workgroup.  s_first: LDS for kLdsFirst words.
+__device__ void open_call(const Config& c, uint32_t* s_tmp, uint32_t* s_first) {
   const int tid = threadIdx.x;
   WsHeader* h = c.hdr;
   if (tid == 0) {
@@ -122,27 +126,64 @@ __device__ void open_call(const Config& c, uint32_t* s_tmp) {
   uint32_t total;
   uint32_t run = block_exclusive_scan(mine, s_tmp, total);
   const uint32_t cap = (uint32_t)c.fchunk_max;
+  const uint32_t nch = min(total, cap);
+  const bool in_lds = c.B < kLdsFirst;
+  const int32_t G = c.filter_grid;
   for (int j = 0; j < per; ++j) {
     const int b = b0 + j;
     if (b < c.B) {
-      c.fchunk_first[b] = min(run, cap);
+      const uint32_t first = min(run, cap);
+      c.fchunk_first[b] = first;
       const uint32_t f0 = point_offset(c, b), f1 = max(point_offset(c, b + 1), f0);
       run += frame_chunks(f1 - f0, P);
+      if (in_lds) {
+        s_first[b] = first;
+      } else {
+        // workgroups g whose first chunk kWaves * g lies in [first, end)
+        const uint32_t end = min(run, cap);
+        for (uint32_t g = (first + kWaves - 1) / kWaves; g < (end + kWaves - 1) / kWaves; ++g) c.wg_frame[g] = b;
+      }
     }
   }
   if (tid == 0) {
-    c.fchunk_first[c.B] = min(total, cap);
-    h->fchunks = min(total, cap);
+    c.fchunk_first[c.B] = nch;
+    h->fchunks = nch;
+  }
+  if (in_lds) {
+    // thread t: workgroups [t*per_g, (t+1)*per_g), the first one's frame by
+    // a search over the chunk starts, then walking forward
+    if (tid == 0) s_first[c.B] = nch;
+    __syncthreads();
+    const int32_t per_g = (G + kBlock - 1) / kBlock;
+    const int32_t g0 = tid * per_g, g1 = min(g0 + per_g, G);
+    if (g0 < g1) {
+      const uint32_t k = (uint32_t)g0 * kWaves;
+      int32_t fb = 0, hi = c.B - 1;
+      while (fb < hi) {
+        const int32_t mid = (fb + hi + 1) >> 1;
+        if (s_first[mid] <= k)
+          fb = mid;
+        else
+          hi = mid - 1;
+      }
+      for (int32_t g = g0; g < g1; ++g) {
+        const uint32_t kg = (uint32_t)g * kWaves;
+        while (fb + 1 < c.B && s_first[fb + 1] <= kg) ++fb;
+        c.wg_frame[g] = kg < nch ? (uint32_t)fb : kNoFrame;
+      }
+    }
+  } else {
+    for (int32_t g = (int32_t)((nch + kWaves - 1) / kWaves) + tid; g < G; g += kBlock) c.wg_frame[g] = kNoFrame;
   }
 }
 
 __global__ __launch_bounds__(kBlock) void stage_kernel(Config c) {
-  __shared__ int16_t s_rect[kMaxRois][4];
+  __shared__ __align__(16) int16_t s_rect[kMaxRois][4];
   __shared__ uint32_t s_tmp[kWaves];
   const int tid = threadIdx.x;
   const int b = blockIdx.y;
   if (blockIdx.x == gridDim.x - 1) {  // the extra column opens the call, beside the frames' work
-    if (b == 0) open_call(c, s_tmp);
+    if (b == 0) open_call(c, s_tmp, reinterpret_cast<uint32_t*>(&s_rect[0][0]));
     return;
   }
 

@@ -366,11 +366,16 @@ __global__ __launch_bounds__(kBlock) void mean_kernel(Config c, const uint32_t* 
     }
     __syncthreads();
     if (contig) {
-      // rows s_row0 .. s_row0 + nblk - 1, written as contiguous runs
+      // rows s_row0 .. s_row0 + nblk - 1, written as contiguous runs with
+      // non-temporal stores: the call does not read them again, and lines
+      // left dirty in the caches would be written back while the next
+      // call's filter streams its points
       const int64_t r0 = s_row0;
-      for (uint32_t e = tid; e < nblk * 4; e += kBlock) c.out_coords[r0 * 4 + e] = l_co[e];
-      for (uint32_t e = tid; e < nblk * (uint32_t)C; e += kBlock) c.out_feats[r0 * C + e] = l_ft[e];
-      for (uint32_t e = tid; e < nblk * (uint32_t)M; e += kBlock) c.out_point_idx[r0 * M + e] = l_pi[e];
+      for (uint32_t e = tid; e < nblk * 4; e += kBlock) __builtin_nontemporal_store(l_co[e], &c.out_coords[r0 * 4 + e]);
+      for (uint32_t e = tid; e < nblk * (uint32_t)C; e += kBlock)
+        __builtin_nontemporal_store(l_ft[e], &c.out_feats[r0 * C + e]);
+      for (uint32_t e = tid; e < nblk * (uint32_t)M; e += kBlock)
+        __builtin_nontemporal_store(l_pi[e], &c.out_point_idx[r0 * M + e]);
     }
     __syncthreads();
   }

@@ -186,21 +186,38 @@ __global__ __launch_bounds__(kBlock) void compact_kernel(Config c, uint32_t* kou
   __shared__ uint32_t s_tmp[kWaves];
   const int tid = threadIdx.x;
   const uint32_t k = blockIdx.x;
-  if (k >= c.hdr->fchunks) return;
-  const uint32_t lo = c.fchunk_lo[k], dst = c.fprefix[k];
-  const int32_t b = (int32_t)c.fchunk_frame[k];
-  const int C = c.C, RW = c.rec_words;
-  for (int e = tid; e < c.S * 12; e += kBlock) s_pose[e] = c.poses[(int64_t)b * c.S * 12 + e];
-  // the bitmap: one word per thread, its set bits listed at the word's rank
+  // the chunk's table entries and bitmap (one word per thread) load together
+  // with the chunk count: every address is in bounds for any k < fchunk_max
+  const uint32_t nch = c.hdr->fchunks;
+  const uint32_t lo = c.fchunk_lo[k], dst = c.fprefix[k], cnt = c.fcount[k];
+  const uint32_t fr = c.fchunk_frame[k];
   uint32_t word = tid < c.fchunk_words ? c.fbits[(int64_t)k * c.fchunk_words + tid] : 0u;
+  asm volatile("" ::"s"(lo), "s"(dst), "s"(cnt), "s"(fr));  // keeps the loads above the check
+  if (k >= nch) return;
+  const int32_t b = (int32_t)min(fr, (uint32_t)c.B - 1u);
+  const int C = c.C, RW = c.rec_words;
+  // the frame's poses: loaded now, stored to LDS once the list is built, so
+  // that their loads overlap the listing
+  constexpr int kPoseRegs = (255 * 12 + kBlock - 1) / kBlock;
+  const int np = c.S * 12;
+  float pv[kPoseRegs];
+#pragma unroll
+  for (int u = 0; u < kPoseRegs; ++u) {
+    const int e = tid + u * kBlock;
+    pv[u] = e < np ? c.poses[(int64_t)b * np + e] : 0.0f;
+  }
+  // the bitmap's set bits listed at each word's rank
   uint32_t total;
   uint32_t r = block_exclusive_scan((uint32_t)__popc(word), s_tmp, total);
   while (word) {
     s_list[r++] = (uint16_t)(32 * tid + __builtin_ctz(word));
     word &= word - 1u;
   }
+#pragma unroll
+  for (int u = 0; u < kPoseRegs; ++u)
+    if (tid + u * kBlock < np) s_pose[tid + u * kBlock] = pv[u];
   __syncthreads();
-  const uint32_t n = min(total, c.fcount[k]);  // equal unless the workspace was corrupted
+  const uint32_t n = min(total, cnt);  // equal unless the workspace was corrupted
   for (uint32_t base = 0; base < n; base += kBlock * kCompactItems) {
     uint32_t pi[kCompactItems], sw[kCompactItems];
     float v[kCompactItems][8];
@@ -246,13 +263,16 @@ __global__ __launch_bounds__(kBlock) void count_kernel(Config c, int pass, const
   __shared__ uint32_t s_hist[kWaves][kSortBins];  // one histogram per wave, summed at the end
   const int tid = threadIdx.x, wave = tid >> 6;
   const uint32_t k = blockIdx.x;
-  if (k >= c.hdr->schunks) return;
+  // the chunk's entry loads with the chunk count (in bounds for any k < schunk_max)
+  const uint32_t nsc = c.hdr->schunks;
+  const uint4 ch = c.schunk[k];
+  asm volatile("" ::"s"(ch.x), "s"(ch.y));  // keeps the load above the check
+  if (k >= nsc) return;
   const int shift = pass * c.dbits;
   const uint32_t nbins = 1u << c.dbits;
   const uint32_t mask = nbins - 1u;
   for (uint32_t e = tid; e < kWaves * kSortBins; e += kBlock) (&s_hist[0][0])[e] = 0;
   __syncthreads();
-  const uint4 ch = c.schunk[k];
   const uint32_t lo = ch.x, hi = ch.y;
   for (uint32_t base = lo; base < hi; base += kBlock * kCountItems) {
     uint32_t key[kCountItems];
@@ -333,12 +353,17 @@ __global__ __launch_bounds__(kBlock) void scatter_kernel(Config c, int pass, con
   const int lane = tid & 63, wave = tid >> 6;
   WsHeader* h = c.hdr;
   const uint32_t k = blockIdx.x;
-  if (k >= h->schunks) return;
-  const uint32_t K = h->kept;
+  // the chunk's entry and its digit-offset row load with the counts (in
+  // bounds for any k < schunk_max)
+  const uint32_t nsc = h->schunks, K = h->kept;
+  const uint4 ch = c.schunk[k];
+  static_assert(kSortBins == 2 * kBlock, "two digits per thread");
+  const uint32_t off0 = c.cnt[(int64_t)k * kSortBins + tid], off1 = c.cnt[(int64_t)k * kSortBins + kBlock + tid];
+  asm volatile("" ::"s"(ch.x), "s"(ch.y), "s"(ch.z), "s"(ch.w), "v"(off0), "v"(off1));  // keeps the loads above the check
+  if (k >= nsc) return;
   const int shift = pass * c.dbits;
   const uint32_t nbins = 1u << c.dbits;
   const uint32_t mask = nbins - 1u;
-  const uint4 ch = c.schunk[k];
   const uint32_t lo = ch.x, hi = ch.y;
   const int32_t b = (int32_t)ch.z;
   uint32_t key[kSortItems], val[kSortItems], nkey[kSortItems], nval[kSortItems];
@@ -348,7 +373,8 @@ __global__ __launch_bounds__(kBlock) void scatter_kernel(Config c, int pass, con
   for (uint32_t e = tid; e < nbins; e += kBlock) L.run[e] = c.ftot[(int64_t)b * kSortBins + e];
   __syncthreads();
   scan_bins(L.run, L.run, (int)nbins, L.scan_tmp);
-  for (uint32_t e = tid; e < nbins; e += kBlock) L.run[e] += ch.w + c.cnt[(int64_t)k * kSortBins + e];
+  if ((uint32_t)tid < nbins) L.run[tid] += ch.w + off0;
+  if ((uint32_t)(kBlock + tid) < nbins) L.run[kBlock + tid] += ch.w + off1;
   const uint64_t lt = lanemask_lt();
   for (uint32_t base = lo; base < hi; base += kSortTile) {
     const bool more = base + kSortTile < hi;

@@ -50,8 +50,10 @@ __global__ __launch_bounds__(kBlock) void ucount_kernel(Config c, const uint32_t
   __shared__ uint32_t s_tmp[kWaves];
   const int tid = threadIdx.x;
   const uint32_t k = blockIdx.x;
-  if (k >= c.hdr->schunks) return;
-  const uint4 ch = c.schunk[k];
+  const uint32_t nsc = c.hdr->schunks;
+  const uint4 ch = c.schunk[k];  // in bounds for any k < schunk_max: loads with the count
+  asm volatile("" ::"s"(ch.x), "s"(ch.y), "s"(ch.z), "s"(ch.w));  // keeps the load above the check
+  if (k >= nsc) return;
   const uint32_t lo = ch.x, hi = ch.y, ff = ch.w;
   uint32_t n = 0;
   for (uint32_t base = lo; base < hi; base += kBlock * kCountItems) {
@@ -76,8 +78,10 @@ __global__ __launch_bounds__(kBlock) void uwrite_kernel(Config c, const uint32_t
   const int tid = threadIdx.x;
   const int lane = tid & 63, wave = tid >> 6;
   const uint32_t k = blockIdx.x;
-  if (k >= c.hdr->schunks) return;
-  const uint4 ch = c.schunk[k];
+  const uint32_t nsc = c.hdr->schunks;
+  const uint4 ch = c.schunk[k];  // in bounds for any k < schunk_max: loads with the count
+  asm volatile("" ::"s"(ch.x), "s"(ch.y), "s"(ch.z), "s"(ch.w));  // keeps the load above the check
+  if (k >= nsc) return;
   const uint32_t lo = ch.x, hi = ch.y, ff = ch.w;
   uint32_t v0;
   {

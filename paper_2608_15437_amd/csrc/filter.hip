@@ -267,68 +267,74 @@ __device__ __forceinline__ void load_quad_scalar(const Config& c, uint32_t i0, u
   }
 }
 
-// Frames f0..f1 of the workgroup's chunks and their ROI range (thread 0),
-// and whether every table fits LDS.
-__device__ __forceinline__ void plan_staging(const Config& c, FilterLds& L, int32_t f0, int32_t f1) {
+// The staging plan of a workgroup: frames f0..f1 of its chunks, their ROI
+// range, and whether every table fits LDS (from the ROI offsets of f0 and
+// f1 + 1).  Every thread computes it from the same loads.
+struct StagePlan {
+  int32_t f0, f1, roi_lo, roi_n;
+  bool staged;
+};
+
+__device__ __forceinline__ StagePlan make_plan(const Config& c, int32_t f0, int32_t f1, int32_t ro0, int32_t ro1) {
+  StagePlan p;
   const int32_t nf = f1 - f0 + 1;
-  L.f0 = f0;
-  L.f1 = f1;
-  L.roi_lo = min(max(c.roi_off[f0], 0), c.R);
-  L.roi_n = min(max(c.roi_off[f1 + 1], L.roi_lo), c.R) - L.roi_lo;
-  L.chunk_staged = nf <= kMaxLdsFrames && nf * c.S <= c.lds_pose_cap && nf * c.S * c.W <= c.lds_bm_cap &&
-                   L.roi_n <= c.lds_roi_cap && nf * (c.ncells + 1) <= c.lds_cell_cap;
+  p.f0 = f0;
+  p.f1 = f1;
+  p.roi_lo = min(max(ro0, 0), c.R);
+  p.roi_n = min(max(ro1, p.roi_lo), c.R) - p.roi_lo;
+  p.staged = nf <= kMaxLdsFrames && nf * c.S <= c.lds_pose_cap && nf * c.S * c.W <= c.lds_bm_cap &&
+             p.roi_n <= c.lds_roi_cap && nf * (c.ncells + 1) <= c.lds_cell_cap;
+  return p;
 }
 
-// Every table the workgroup stages, as one index space of 4-byte words
-// (ROI offsets, poses, budget masks, cell words, ROI record fields), so that
-// a thread's loads of all tables are in flight together: kStageBatch words
-// per thread and round, one round for a frame of up to ~3,000 cell words.
-constexpr int kStageBatch = 12;
-
-__device__ __forceinline__ void do_staging(const Config& c, FilterLds& L) {
+// The tables of the workgroup's frame f0 (the caps make a staged plan one
+// frame: f1 == f0): ROI offsets, poses, budget masks, ROI records and cell
+// words, every load of a thread issued before the first LDS store, so that
+// they take one round trip together.
+__device__ __forceinline__ void do_staging(const Config& c, FilterLds& L, const StagePlan& pl) {
+  static_assert(kMaxLdsBudgetWords <= kBlock && kMaxLdsRois <= kBlock, "one budget word and ROI record per thread");
+  constexpr int kPoseRegs = (kMaxPoseLds * 12 + kBlock - 1) / kBlock;
+  constexpr int kCellRegs = (kMaxLdsCells + kBlock - 1) / kBlock;
   const int tid = threadIdx.x;
-  const int32_t nf = L.f1 - L.f0 + 1;
-  const int32_t e1 = nf + 1;                   // ROI offsets
-  const int32_t e2 = e1 + nf * c.S * 12;       // poses
-  const int32_t e3 = e2 + nf * c.S * c.W;      // budget masks
-  const int32_t e4 = e3 + nf * c.ncells;       // cell words
-  const int32_t e5 = e4 + 6 * L.roi_n;         // ROI records, six fields each
-  uint32_t* dyn = reinterpret_cast<uint32_t*>(filter_dyn);
-  const uint32_t* poses = reinterpret_cast<const uint32_t*>(c.poses) + (int64_t)L.f0 * c.S * 12;
-  const uint32_t* bms = c.budgetmask + (int64_t)L.f0 * c.S * c.W;
-  const uint32_t* cells = c.cellany + (int64_t)L.f0 * c.ncells;
-  const uint32_t* rois = reinterpret_cast<const uint32_t*>(c.rois + L.roi_lo);
-  for (int32_t e0 = 0; e0 < e5; e0 += kStageBatch * kBlock) {
-    uint32_t v[kStageBatch];
+  const int32_t f = pl.f0;
+  const int np = c.S * 12, nbm = c.S * c.W, nroi = pl.roi_n, ncell = c.ncells;
+  // loads (4-byte: the caller's arrays need only natural alignment)
+  const int32_t roff = c.roi_off[f + min(tid, 1)];  // every lane (in bounds): no branch around the load
+  float pv[kPoseRegs];
+  const float* poses = c.poses + (int64_t)f * np;
 #pragma unroll
-    for (int j = 0; j < kStageBatch; ++j) {
-      const int32_t e = e0 + j * kBlock + tid;
-      const uint32_t* src = e < e1   ? reinterpret_cast<const uint32_t*>(c.roi_off + L.f0 + e)
-                            : e < e2 ? poses + (e - e1)
-                            : e < e3 ? bms + (e - e2)
-                            : e < e4 ? cells + (e - e3)
-                                     : rois + ((e - e4) / 6) * 8 + (e - e4) % 6;
-      v[j] = e < e5 ? *src : 0u;
-    }
-#pragma unroll
-    for (int j = 0; j < kStageBatch; ++j) {
-      const int32_t e = e0 + j * kBlock + tid;
-      if (e < e1) {
-        L.roff[e] = min(max((int32_t)v[j], 0), c.R);
-      } else if (e < e2) {
-        dyn[e - e1] = v[j];
-      } else if (e < e3) {
-        dyn[c.lds_bm + (e - e2)] = v[j];
-      } else if (e < e4) {
-        const int32_t f = nf == 1 ? 0 : (e - e3) / c.ncells;  // frame f's row: a zero word, then its cells
-        dyn[c.lds_cell + (e - e3) + f + 1] = v[j];
-      } else if (e < e5) {
-        const int32_t r = (e - e4) / 6;
-        dyn[c.lds_roi + ((e - e4) % 6) * c.lds_roi_cap + r] = v[j];
-      }
-    }
+  for (int j = 0; j < kPoseRegs; ++j) pv[j] = tid + j * kBlock < np ? poses[tid + j * kBlock] : 0.0f;
+  const uint32_t bm = tid < nbm ? c.budgetmask[(int64_t)f * nbm + tid] : 0u;
+  float rv[6] = {0.0f, 0.0f, 0.0f, 0.0f, 0.0f, 0.0f};
+  if (tid < nroi) {
+    const mmbev_roi_t& r = c.rois[pl.roi_lo + tid];
+    rv[0] = r.cx;
+    rv[1] = r.cy;
+    rv[2] = r.cos_yaw;
+    rv[3] = r.sin_yaw;
+    rv[4] = r.ext_x;
+    rv[5] = r.ext_y;
   }
-  for (int32_t f = tid; f < nf; f += kBlock) dyn[c.lds_cell + f * (c.ncells + 1)] = 0u;
+  uint32_t cv[kCellRegs];
+  const uint32_t* cells = c.cellany + (int64_t)f * ncell;
+#pragma unroll
+  for (int j = 0; j < kCellRegs; ++j) cv[j] = tid + j * kBlock < ncell ? cells[tid + j * kBlock] : 0u;
+  // stores
+  uint32_t* dyn = reinterpret_cast<uint32_t*>(filter_dyn);
+  if (tid < 2) L.roff[tid] = min(max(roff, 0), c.R);
+  float* dynf = reinterpret_cast<float*>(filter_dyn);
+#pragma unroll
+  for (int j = 0; j < kPoseRegs; ++j)
+    if (tid + j * kBlock < np) dynf[tid + j * kBlock] = pv[j];  // pose rows from word 0
+  if (tid < nbm) dyn[c.lds_bm + tid] = bm;
+  if (tid < nroi)
+#pragma unroll
+    for (int k = 0; k < 6; ++k) dynf[c.lds_roi + k * c.lds_roi_cap + tid] = rv[k];
+  // the frame's cell row: a zero word (points outside the grid), then the cells
+  if (tid == 0) dyn[c.lds_cell] = 0u;
+#pragma unroll
+  for (int j = 0; j < kCellRegs; ++j)
+    if (tid + j * kBlock < ncell) dyn[c.lds_cell + 1 + tid + j * kBlock] = cv[j];
 }
 
 // Approximate coarse cell of (x', y') inside its frame for the candidate
@@ -627,41 +633,54 @@ __global__ __launch_bounds__(kBlock, 5) void filter_kernel(Config c) {
   WaveLds& Q = Qs[wave];
   const uint32_t nchunks = c.hdr->fchunks;
   const uint32_t k0 = (uint32_t)blockIdx.x * kWaves;
-  // frame of chunk k0 (loaded with nchunks); every chunk of the workgroup
-  // lies in it unless the point offsets are invalid (then a search finds
-  // each chunk's frame).  The lookups that depend on the frame are made for
-  // wf before that check, so that they load together with it.
+  // frame wf of chunk k0 (loaded with nchunks), then everything that depends
+  // only on wf, loaded together: every chunk of the workgroup lies in wf
+  // unless the point offsets are invalid (then searches find the frames)
   const int32_t wf = (int32_t)min(c.wg_frame[blockIdx.x], (uint32_t)c.B - 1u);
+  const int64_t fo0 = c.frame_off[wf], fo1 = c.frame_off[wf + 1];
+  const uint32_t ff0 = c.fchunk_first[wf], ff1 = c.fchunk_first[wf + 1];
+  const int32_t ro0 = c.roi_off[wf], ro1 = c.roi_off[wf + 1];
+  asm volatile("" ::"s"(fo0), "s"(fo1), "s"(ff0), "s"(ff1), "s"(ro0), "s"(ro1));  // one round trip for all
 
-  // this wave's chunk and its points, before the staging barriers
+  // this wave's chunk and its points; the staging plan
   const uint32_t k = k0 + (uint32_t)wave;
+  const bool any = k0 < nchunks;
+  const uint32_t last = any ? min(k0 + kWaves - 1, nchunks - 1) : k0;
   int32_t b = 0;
   uint32_t lo = 0, hi = 0;
-  if (k < nchunks) {
-    b = wf;
-    filter_chunk_points(c, b, k, lo, hi);
-    if (!(k < c.fchunk_first[wf + 1])) {
+  StagePlan pl{0, 0, 0, 0, false};
+  if (any && last < ff1) {
+    pl = make_plan(c, wf, wf, ro0, ro1);
+    if (k < nchunks) {
+      b = wf;
+      const uint32_t P = (uint32_t)c.fchunk_points;
+      const uint32_t p0 = (uint32_t)min(max(fo0, (int64_t)0), (int64_t)c.N);
+      const uint32_t p1 = max((uint32_t)min(max(fo1, (int64_t)0), (int64_t)c.N), p0);
+      const uint64_t l = (uint64_t)p0 + (uint64_t)(k - ff0) * P;
+      lo = (uint32_t)min(l, (uint64_t)p1);
+      hi = (uint32_t)min(l + P, (uint64_t)p1);
+    }
+  } else if (any) {
+    const int32_t f0 = frame_of_chunk(c.fchunk_first, c.B, k0), f1 = frame_of_chunk(c.fchunk_first, c.B, last);
+    pl = make_plan(c, f0, f1, c.roi_off[f0], c.roi_off[f1 + 1]);
+    if (k < nchunks) {
       b = frame_of_chunk(c.fchunk_first, c.B, k);
       filter_chunk_points(c, b, k, lo, hi);
     }
-    // the same in every lane; uniform bounds keep the tile loop a scalar loop
-    b = __builtin_amdgcn_readfirstlane(b);
-    lo = __builtin_amdgcn_readfirstlane(lo);
-    hi = __builtin_amdgcn_readfirstlane(hi);
   }
+  // the same in every lane; uniform bounds keep the tile loop a scalar loop
+  b = __builtin_amdgcn_readfirstlane(b);
+  lo = __builtin_amdgcn_readfirstlane(lo);
+  hi = __builtin_amdgcn_readfirstlane(hi);
   if (tid == 0) {
-    L.f0 = L.f1 = 0;
-    L.chunk_staged = 0;
-    if (k0 < nchunks) {
-      const uint32_t last = min(k0 + kWaves - 1, nchunks - 1);
-      plan_staging(c, L, wf, wf);
-      if (!(last < c.fchunk_first[wf + 1]))
-        plan_staging(c, L, frame_of_chunk(c.fchunk_first, c.B, k0), frame_of_chunk(c.fchunk_first, c.B, last));
-    }
+    L.f0 = pl.f0;
+    L.f1 = pl.f1;
+    L.roi_lo = pl.roi_lo;
+    L.roi_n = pl.roi_n;
+    L.chunk_staged = pl.staged;
   }
-  __syncthreads();
-  const bool staged = __builtin_amdgcn_readfirstlane(L.chunk_staged) != 0;
-  if (staged) do_staging(c, L);
+  const bool staged = pl.staged;
+  if (staged) do_staging(c, L, pl);
   __syncthreads();
 
   if (k >= nchunks) return;

@@ -66,7 +66,7 @@ struct Plan {
   int32_t cell_shift, ncx, ncy, ncells;
   int32_t kb, passes, dbits;
   int64_t fchunk_points, fchunk_max, filter_grid, schunk_max, mean_grid;
-  size_t off_hdr, off_cellmask, off_cellany, off_budgetmask, off_fchunk_first, off_tileframe, off_fbits, off_fcount, off_fchunk_lo, off_fchunk_frame, off_wgframe, off_fprefix,
+  size_t off_hdr, off_cellmask, off_cellany, off_budgetmask, off_fchunk_first, off_tileframe, off_fbits, off_fcount, off_fchunk_lo, off_fchunk_frame, off_wgframe, off_spare, off_fprefix,
       off_fstart, off_schunk_first, off_schunk, off_cnt, off_ftot, off_hcount, off_vcount, off_keys[2], off_vals[2], off_rec, off_seg,
       off_capkey, off_rank, off_voxoff, total;
 };
@@ -143,6 +143,7 @@ mmbev_status_t make_plan(const mmbev_grid_t* g, int64_t N, int32_t max_rois, int
   p->off_fchunk_lo = take((size_t)p->fchunk_max * 4);
   p->off_fchunk_frame = take((size_t)p->fchunk_max * 4);
   p->off_wgframe = take((size_t)p->filter_grid * 4);
+  p->off_spare = take(kSpareTileBytes);
   p->off_fprefix = take((size_t)(p->fchunk_max + 1) * 4);
   p->off_fstart = take((size_t)(p->B + 1) * 4);
   p->off_schunk_first = take((size_t)(p->B + 1) * 4);
@@ -322,6 +323,7 @@ mmbev_status_t voxelize(const mmbev_points_t* points, const uint8_t* sweep_ids, 
   c.fchunk_lo = (uint32_t*)(ws + p.off_fchunk_lo);
   c.fchunk_frame = (uint32_t*)(ws + p.off_fchunk_frame);
   c.wg_frame = (uint32_t*)(ws + p.off_wgframe);
+  c.spare_tile = (const float*)(ws + p.off_spare);
   c.fprefix = (uint32_t*)(ws + p.off_fprefix);
   c.fstart = (uint32_t*)(ws + p.off_fstart);
   c.schunk_first = (uint32_t*)(ws + p.off_schunk_first);

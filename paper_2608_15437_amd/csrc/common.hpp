@@ -96,6 +96,7 @@ struct Config {
   uint32_t* fchunk_lo;     // [fchunk_max] first point of filter chunk k
   uint32_t* fchunk_frame;  // [fchunk_max] frame of filter chunk k
   uint32_t* wg_frame;      // [filter_grid] frame of filter workgroup g's first chunk (kNoFrame: no chunk)
+  const float* spare_tile; // kSpareTileBytes the filter's past-the-end pipeline loads read (values unused)
   uint32_t* fprefix;       // [fchunk_max + 1] kept pairs of the filter chunks before k
   uint32_t* fstart;        // [B+1] first sorted pair of frame b (kept pairs of the frames before it)
   uint32_t* schunk_first;  // [B+1] first pair chunk of frame b
@@ -167,6 +168,7 @@ __device__ __forceinline__ uint32_t block_exclusive_scan(uint32_t v, uint32_t* s
   return wpre + x - v;
 }
 
+constexpr size_t kSpareTileBytes = 1024;  // one wave's 16-byte loads
 constexpr uint32_t kNoFrame = 0xffffffffu;  // wg_frame of a filter workgroup past the last chunk
 
 // Largest b in [0, B-1] with first[b] <= k (first[] non-decreasing): the

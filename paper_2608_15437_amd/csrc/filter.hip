@@ -548,19 +548,23 @@ __device__ __forceinline__ void phase_b(const Config& c, const FilterLds& L, Wav
 }
 
 // Step k of the register pipeline over the ntiles full tiles from a0: the
-// loads of tile k (the last tile again past the end: cache hits, values
-// unused) go into buffer k mod kFilterDepth, then tile k - (kFilterDepth - 1),
-// loaded that many steps earlier, is handled if it exists.  Every step
+// loads of tile k go into buffer k mod kFilterDepth (past the end, loads of
+// a small spare region of the workspace that stays in cache: values
+// unused), then tile k - (kFilterDepth - 1), loaded that many steps
+// earlier, is handled if it exists.  Every step
 // issues the same loads in the same order, and the loop over the steps has a
 // fixed trip count and no early exit, so the compiler's wait before a tile's
 // data counts exactly the loads of the tiles after it.
 template <bool ST, bool BG, int J>
 __device__ __forceinline__ void pipeline_step(const Config& c, const CellConsts& kc, const FilterLds& L, WaveLds& Q,
-                                              int32_t b, const TileRows& rows,
+                                              int32_t b, const TileRows& rows, const TileRows& spare,
                                               uint32_t a0, uint32_t ntiles, uint32_t k0, uint32_t lane4,
                                               Quad (&buf)[kFilterDepth], QuadState& st, WaveRun& wr) {
   const uint32_t k = k0 + (uint32_t)J;
-  load_quad_vec(rows, min(k, ntiles - 1u) * kWaveTile + lane4, buf[J]);
+  if (k < ntiles)
+    load_quad_vec(rows, k * kWaveTile + lane4, buf[J]);
+  else
+    load_quad_vec(spare, lane4, buf[J]);
   const uint32_t tile = k - (uint32_t)(kFilterDepth - 1);  // wraps for the first steps
   if (tile < ntiles) {
     const uint32_t t = a0 + tile * kWaveTile;
@@ -596,14 +600,15 @@ __device__ __forceinline__ void run_wave(const Config& c, const FilterLds& L, Wa
   static_assert(kFilterDepth >= 2 && kFilterDepth <= 6, "pipeline steps written out below");
   if (ntiles > 0) {
     const TileRows rows = tile_rows(c, a0);
+    const TileRows spare{c.spare_tile, c.spare_tile, c.spare_tile, reinterpret_cast<const uint8_t*>(c.spare_tile)};
     const uint32_t steps = ntiles + (uint32_t)(kFilterDepth - 1);
     for (uint32_t k0 = 0; k0 < steps; k0 += kFilterDepth) {
-      pipeline_step<ST, BG, 0>(c, kc, L, Q, b, rows, a0, ntiles, k0, lane4, buf, st, wr);
-      pipeline_step<ST, BG, 1>(c, kc, L, Q, b, rows, a0, ntiles, k0, lane4, buf, st, wr);
-      if constexpr (kFilterDepth > 2) pipeline_step<ST, BG, 2 % kFilterDepth>(c, kc, L, Q, b, rows, a0, ntiles, k0, lane4, buf, st, wr);
-      if constexpr (kFilterDepth > 3) pipeline_step<ST, BG, 3 % kFilterDepth>(c, kc, L, Q, b, rows, a0, ntiles, k0, lane4, buf, st, wr);
-      if constexpr (kFilterDepth > 4) pipeline_step<ST, BG, 4 % kFilterDepth>(c, kc, L, Q, b, rows, a0, ntiles, k0, lane4, buf, st, wr);
-      if constexpr (kFilterDepth > 5) pipeline_step<ST, BG, 5 % kFilterDepth>(c, kc, L, Q, b, rows, a0, ntiles, k0, lane4, buf, st, wr);
+      pipeline_step<ST, BG, 0>(c, kc, L, Q, b, rows, spare, a0, ntiles, k0, lane4, buf, st, wr);
+      pipeline_step<ST, BG, 1>(c, kc, L, Q, b, rows, spare, a0, ntiles, k0, lane4, buf, st, wr);
+      if constexpr (kFilterDepth > 2) pipeline_step<ST, BG, 2 % kFilterDepth>(c, kc, L, Q, b, rows, spare, a0, ntiles, k0, lane4, buf, st, wr);
+      if constexpr (kFilterDepth > 3) pipeline_step<ST, BG, 3 % kFilterDepth>(c, kc, L, Q, b, rows, spare, a0, ntiles, k0, lane4, buf, st, wr);
+      if constexpr (kFilterDepth > 4) pipeline_step<ST, BG, 4 % kFilterDepth>(c, kc, L, Q, b, rows, spare, a0, ntiles, k0, lane4, buf, st, wr);
+      if constexpr (kFilterDepth > 5) pipeline_step<ST, BG, 5 % kFilterDepth>(c, kc, L, Q, b, rows, spare, a0, ntiles, k0, lane4, buf, st, wr);
     }
   }
   for (uint32_t t = a0 + ntiles * kWaveTile; t < hi; t += kWaveTile) {

@@ -127,6 +127,22 @@ def test_edge_cases(gpu_lib):
     check(gpu_lib, empty_mid, label="empty middle frame", desc=wl.roi_desc)
 
 
+@pytest.mark.parametrize("frames", [2047, 2100])
+def test_many_small_frames(gpu_lib, frames):
+    """Frame counts on both sides of the stage's LDS copy of the chunk starts
+    (up to 2,047 frames; beyond, each frame's thread writes its filter
+    workgroups' frame itself), with every seventh frame emptied."""
+    wl = synth.small(51, frames=frames, beams=2, azimuths=16, sweeps=1, rois=4)
+    c = case_from_workload(wl)
+    fo = c.frame_offsets
+    keep = np.concatenate([np.arange(fo[f], fo[f + 1]) for f in range(frames) if f % 7 != 3])
+    counts = np.array([0 if f % 7 == 3 else fo[f + 1] - fo[f] for f in range(frames)])
+    sparse = Case(feat=np.ascontiguousarray(c.feat[:, keep]), sweep_ids=c.sweep_ids[keep],
+                  frame_offsets=np.concatenate([[0], np.cumsum(counts)]), poses=c.poses, rois=c.rois,
+                  roi_offsets=c.roi_offsets, budgets=c.budgets, grid=c.grid)
+    check(gpu_lib, sparse, label=f"{frames} frames", desc=wl.roi_desc)
+
+
 def test_zero_points(gpu_lib):
     case, _ = load_golden("hand_two_frames.json")
     z = Case(feat=np.zeros((4, 0), np.float32), sweep_ids=np.zeros(0, np.uint8), frame_offsets=np.array([0, 0, 0]),

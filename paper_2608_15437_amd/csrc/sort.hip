@@ -116,15 +116,26 @@ __global__ __launch_bounds__(kSegBlock) void segments_kernel(Config c) {
     uint32_t total;
     uint32_t run = carry + block_exclusive_scan<kSegWaves>(sum, s_tmp, total);
     int32_t prev = before;
+    uint32_t pre[kScanItems];
 #pragma unroll
-    for (int j = 0; j < kScanItems; ++j)
+    for (int j = 0; j < kScanItems; ++j) {
+      pre[j] = run;
       if (first + j < nf) {
-        c.fprefix[first + j] = run;
         for (int32_t g = prev + 1; g <= fr[j]; ++g) fstart[g] = run;
         prev = max(prev, fr[j]);
         run += v[j];
         if (first + j + 1 == nf) s_last = prev;
       }
+    }
+    // the thread's prefixes as 16-byte stores (one per four chunks)
+#pragma unroll
+    for (int j = 0; j < kScanItems; j += 4) {
+      if (first + j + 3 < nf)
+        *reinterpret_cast<uint4*>(c.fprefix + first + j) = make_uint4(pre[j], pre[j + 1], pre[j + 2], pre[j + 3]);
+      else
+        for (int u = 0; u < 4; ++u)
+          if (first + j + u < nf) c.fprefix[first + j + u] = pre[j + u];
+    }
     carry += total;
     __syncthreads();
   }

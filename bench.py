@@ -81,6 +81,32 @@ def time_calls(vz, steps: int, warmup: int) -> float:
     return start.elapsed_time(end) / steps
 
 
+def time_graph_calls(vz, steps: int, warmup: int) -> float:
+    """Mean time of one call captured in a HIP graph and replayed (the entry
+    point only enqueues kernels, so a caller can capture it)."""
+    import torch
+
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        vz.run()
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        vz.run()
+    for _ in range(warmup):
+        graph.replay()
+    torch.cuda.synchronize()
+    start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    start.record()
+    for _ in range(steps):
+        graph.replay()
+    end.record()
+    torch.cuda.synchronize()
+    return start.elapsed_time(end) / steps
+
+
 def time_launches(vz, steps: int) -> dict:
     """Mean duration of every launch of one call, from events recorded between launches."""
     import torch
@@ -321,6 +347,7 @@ def main() -> int:
     wl1 = synth.c2()
     vz1 = mmbev.voxelizer_for_workload(wl1, dev)
     us1 = time_calls(vz1, max(args.steps, 20), args.warmup) * 1e3
+    us1g = time_graph_calls(vz1, max(args.steps, 20), args.warmup) * 1e3
 
     log("[bench] temporal-ROI selector (host) on 128 detection caches")
     selector = time_selector(args.steps)
@@ -378,7 +405,8 @@ def main() -> int:
         "path_gbps": round(alg_total / (ms * 1e-3) / 1e9, 1),
         "launch_us": {k: round(v, 2) for k, v in per.items()},
         "single_frame": {"points": wl1.num_points, "us_per_call": round(us1, 2),
-                         "mpoints_s": round(wl1.num_points / (us1 * 1e-6) / 1e6, 1)},
+                         "mpoints_s": round(wl1.num_points / (us1 * 1e-6) / 1e6, 1),
+                         "us_per_call_graph": round(us1g, 2)},
         "scatter_to_bev": bev,
         "voxel_clusters": {"batch": clusters, "single_ouster_frame": clusters1},
         "roi_selector": selector,

@@ -25,7 +25,7 @@ namespace {
 
 constexpr int kMaxRois = 1024;
 constexpr int kLdsFirst = kMaxRois * 2;  // chunk starts of up to kLdsFirst - 1 frames in the rectangles' LDS
-constexpr int kStageCellsPerThread = 8;
+constexpr int kStageCellsPerThread = 2;
 
 // Conservative cell rectangle [x0, x1] x [y0, y1] of one ROI; empty when x0 > x1.
 __device__ void roi_cell_rect(const Config& c, const mmbev_roi_t& r, int16_t* out) {

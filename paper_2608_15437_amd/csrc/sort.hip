@@ -308,31 +308,37 @@ __global__ __launch_bounds__(kBlock) void count_kernel(Config c, int pass, const
 // Frame b: every digit's column over the frame's chunks -> exclusive
 // offsets inside the frame (in place), and the frame's digit totals.
 __global__ __launch_bounds__(kBlock) void rowscan_kernel(Config c) {
-  constexpr int kUnroll = 4;
+  // thread t: digits t and t + kBlock, kRows chunk rows of both loaded
+  // together (one round trip for a frame of up to kRows chunks)
+  constexpr int kRows = 8;
+  static_assert(kSortBins == 2 * kBlock, "two digits per thread");
   const int tid = threadIdx.x;
   const int32_t b = blockIdx.x;
   const uint32_t nbins = 1u << c.dbits;
   const uint32_t k0 = c.schunk_first[b], k1 = max(c.schunk_first[b + 1], k0);
-  for (uint32_t d = tid; d < nbins; d += kBlock) {
-    uint32_t run = 0;
-    uint32_t k = k0;
-    for (; k + kUnroll <= k1; k += kUnroll) {
-      uint32_t x[kUnroll];
+  const uint32_t d0 = (uint32_t)tid, d1 = (uint32_t)(tid + kBlock);
+  uint32_t run0 = 0, run1 = 0;
+  for (uint32_t kb = k0; kb < k1; kb += kRows) {
+    uint32_t x0[kRows], x1[kRows];
 #pragma unroll
-      for (int u = 0; u < kUnroll; ++u) x[u] = c.cnt[(int64_t)(k + u) * kSortBins + d];
+    for (int u = 0; u < kRows; ++u) {
+      const uint32_t k = kb + u;
+      x0[u] = k < k1 && d0 < nbins ? c.cnt[(int64_t)k * kSortBins + d0] : 0u;
+      x1[u] = k < k1 && d1 < nbins ? c.cnt[(int64_t)k * kSortBins + d1] : 0u;
+    }
 #pragma unroll
-      for (int u = 0; u < kUnroll; ++u) {
-        c.cnt[(int64_t)(k + u) * kSortBins + d] = run;
-        run += x[u];
+    for (int u = 0; u < kRows; ++u) {
+      const uint32_t k = kb + u;
+      if (k < k1) {
+        if (d0 < nbins) c.cnt[(int64_t)k * kSortBins + d0] = run0;
+        if (d1 < nbins) c.cnt[(int64_t)k * kSortBins + d1] = run1;
+        run0 += x0[u];
+        run1 += x1[u];
       }
     }
-    for (; k < k1; ++k) {
-      const uint32_t x = c.cnt[(int64_t)k * kSortBins + d];
-      c.cnt[(int64_t)k * kSortBins + d] = run;
-      run += x;
-    }
-    c.ftot[(int64_t)b * kSortBins + d] = run;
   }
+  if (d0 < nbins) c.ftot[(int64_t)b * kSortBins + d0] = run0;
+  if (d1 < nbins) c.ftot[(int64_t)b * kSortBins + d1] = run1;
 }
 
 struct ScatterLds {

@@ -313,6 +313,8 @@ def main() -> int:
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--frames", type=int, default=128)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-two-streams", action="store_true",
+                    help="skip the two-calls-in-flight measurement (kernel traces then time each kernel alone)")
     ap.add_argument("--probe-traffic", action="store_true")
     ap.add_argument("--write-traffic", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"))
     args = ap.parse_args()
@@ -369,14 +371,18 @@ def main() -> int:
         if tr.get("source_sha") == source_sha(FILTER_SOURCES) and tr.get("frames") == F:
             traffic = tr.get("bytes_per_launch")
 
-    log("[bench] two calls in flight on two streams (a second copy of the batch)")
-    vz_b = mmbev.voxelizer_for_workload(wl, dev)
-    ms2 = time_two_streams(vz, vz_b, args.steps, args.warmup)
-    res_b = vz_b.result()
-    two_ok = all(np.array_equal(res[k], res_b[k]) for k in ("coords", "counts", "point_idx", "voxel_offsets")) and \
-        np.array_equal(res["feats"], res_b["feats"])
-    del vz_b
-    torch.cuda.empty_cache()
+    two = None
+    if not args.no_two_streams:
+        log("[bench] two calls in flight on two streams (a second copy of the batch)")
+        vz_b = mmbev.voxelizer_for_workload(wl, dev)
+        ms2 = time_two_streams(vz, vz_b, args.steps, args.warmup)
+        res_b = vz_b.result()
+        two_ok = all(np.array_equal(res[k], res_b[k]) for k in ("coords", "counts", "point_idx", "voxel_offsets")) \
+            and np.array_equal(res["feats"], res_b["feats"])
+        two = {"mpoints_s": round(N / (ms2 * 1e-3) / 1e6, 1), "ms_per_call": round(ms2, 4), "outputs_match": bool(two_ok),
+               "note": "two batches in flight on two default-priority streams, separate workspaces"}
+        del vz_b
+        torch.cuda.empty_cache()
 
     log("[bench] single-frame latency (one 347,200-point frame)")
     wl1 = synth.c2()
@@ -438,9 +444,7 @@ def main() -> int:
                      "kernel": "filter_kernel", "kernel_us": round(filt_us, 2),
                      "alg_bytes_per_launch": alg_filter},
         "path_gbps": round(alg_total / (ms * 1e-3) / 1e9, 1),
-        "two_streams": {"mpoints_s": round(N / (ms2 * 1e-3) / 1e6, 1), "ms_per_call": round(ms2, 4),
-                        "outputs_match": bool(two_ok),
-                        "note": "two batches in flight on two default-priority streams, separate workspaces"},
+        "two_streams": two,
         "launch_us": {k: round(v, 2) for k, v in per.items()},
         "single_frame": {"points": wl1.num_points, "us_per_call": round(us1, 2),
                          "mpoints_s": round(wl1.num_points / (us1 * 1e-6) / 1e6, 1),

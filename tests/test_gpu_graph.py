@@ -53,3 +53,28 @@ def test_call_replays_as_a_graph(gpu_lib, name):
         assert vz.fault() == 0
         vz.run()  # eager work between the replays
         torch.cuda.synchronize()
+
+
+def test_two_calls_in_flight_on_two_streams(gpu_lib):
+    """Calls alternating between two default-priority streams, each voxelizer
+    with its own inputs, workspace and outputs (the bench's two-stream
+    measurement): both copies end with the single-stream outputs."""
+    import torch
+
+    wl = synth.throughput(16)
+    a = gpu_lib.voxelizer_for_workload(wl, "cuda:0")
+    b = gpu_lib.voxelizer_for_workload(wl, "cuda:0")
+    a.run()
+    torch.cuda.synchronize()
+    ref = _snapshot(a)
+    streams = [torch.cuda.Stream(), torch.cuda.Stream()]
+    for s in streams:
+        s.wait_stream(torch.cuda.current_stream())
+    for i in range(8):
+        (a, b)[i % 2].run(stream=streams[i % 2])
+    torch.cuda.synchronize()
+    for vz in (a, b):
+        got = _snapshot(vz)
+        for k in ref:
+            assert np.array_equal(got[k], ref[k]), k
+        assert vz.fault() == 0

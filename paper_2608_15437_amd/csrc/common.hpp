@@ -121,7 +121,7 @@ struct Config {
   // sizes
   int32_t fchunk_points;   // points per filter chunk (a multiple of kWaveTile, <= kMaxChunkPoints)
   int32_t fchunk_words;    // fchunk_points / 32
-  int32_t fchunk_max;      // bound on filter chunks: ceil(N / fchunk_points) + B
+  int32_t fchunk_max;      // bound on filter chunks: ceil(N / fchunk_points) + kWaves * B
   int32_t filter_grid;     // ceil(fchunk_max / kWaves) workgroups, one chunk per wave
   // the filter's dynamic LDS: pose rows, ROI records (six rows of
   // lds_roi_cap floats from float offset lds_roi), budget-mask words (from

@@ -4,7 +4,7 @@
 // the sweep id, move the point into the current frame (Eq. 6), find the
 // candidate ROIs of its coarse BEV cell that admit its sweep, run the exact
 // oriented-box test on those candidates only, quantise (Alg. 1 Voxelize:
-// range check and voxel indices) and emit (voxel key, point index).
+// range check) and mark the point kept in its chunk's bitmap.
 //
 // Two phases keep the pass bandwidth-bound:
 //   A. for every point of a lane: p' (exact), an approximate cell index
@@ -21,23 +21,24 @@
 //      the definition's.
 //
 // Wave k of the grid owns filter chunk k: a contiguous run of at most
-// fchunk_points points inside one frame (the chunk table is laid out by the
-// staging kernel).  The waves of a workgroup share the LDS copy of their
-// frames' poses, budget masks, ROI records, ROI offsets and cell maps
-// (staged once, behind the only workgroup barriers) and are otherwise
-// independent: a wave appends its kept pairs, in point order, to its own
-// output region, which starts at the chunk's first point index.  Nothing
-// waits on another wave: a chained scan across workgroups costs one memory
-// round trip per predecessor when many publish together, and workgroup
-// barriers leave the waves without candidates idle.  Each frame's sort gathers its chunks'
-// regions using the per-chunk counts left here.
+// fchunk_points points inside one frame (the chunk table and the frame of
+// every workgroup are laid out by the staging kernel).  The waves of a
+// workgroup share the LDS copy of their frame's poses, budget masks, ROI
+// records, ROI offsets and cell map (staged once, behind the only workgroup
+// barrier) and are otherwise independent: a wave marks its kept points in
+// its own LDS bitmap and writes it, with the kept count, once at the end of
+// its chunk.  Nothing waits on another wave: a chained scan across
+// workgroups costs one memory round trip per predecessor when many publish
+// together, and workgroup barriers leave the waves without candidates idle.
+// The compaction lists each chunk's kept points from its bitmap.
 //
 // Per wave tile (256 points, four consecutive points per lane, one 16-byte
 // load per column and lane) the only global loads are the tile's own: vector
 // memory loads complete in order, so a wait for a dependent global load (a
 // cell word, say) would also wait for every tile loaded before it.  Phases A
-// and B read only LDS and registers on the common path, and the loads of the
-// two tiles after the current one stay in flight while it is handled.
+// and B read only LDS and registers on the common path, and the next tile's
+// loads stay in flight while a tile is handled.  The point loads are
+// non-temporal: the points are read once.
 #include "launch.hpp"
 
 namespace mmbev {

@@ -367,12 +367,14 @@ mmbev_status_t voxelize(const mmbev_points_t* points, const uint8_t* sweep_ids, 
 
   MMBEV_TRY(launch_stage(c, s));
   MMBEV_TRY(launch_filter(c, s));
-  // sorted pairs ping-pong: compacted into [1], pass p writes [p % 2]
+  // sorted pairs ping-pong: keys compacted into [1], pass p writes [p % 2];
+  // pass 0 reads no values, its value for each key is the key's compacted
+  // position
   MMBEV_TRY(launch_segments(c, s));
-  MMBEV_TRY(launch_compact(c, c.keys[1], c.vals[1], s));
+  MMBEV_TRY(launch_compact(c, c.keys[1], s));
   for (int pass = 0; pass < c.passes; ++pass)
-    MMBEV_TRY(launch_radix_pass(c, pass, c.keys[1 - pass % 2], c.vals[1 - pass % 2], c.keys[pass % 2],
-                                c.vals[pass % 2], s));
+    MMBEV_TRY(launch_radix_pass(c, pass, c.keys[1 - pass % 2], pass == 0 ? nullptr : c.vals[1 - pass % 2],
+                                c.keys[pass % 2], c.vals[pass % 2], s));
   const uint32_t* keys = c.keys[(c.passes - 1) % 2];
   const uint32_t* vals = c.vals[(c.passes - 1) % 2];
   MMBEV_TRY(launch_unique(c, keys, s));

@@ -10,7 +10,7 @@ namespace mmbev {
 hipError_t launch_stage(const Config& c, hipStream_t st);
 hipError_t launch_filter(const Config& c, hipStream_t st);
 hipError_t launch_segments(const Config& c, hipStream_t st);
-hipError_t launch_compact(const Config& c, uint32_t* kout, uint32_t* vout, hipStream_t st);
+hipError_t launch_compact(const Config& c, uint32_t* kout, hipStream_t st);
 hipError_t launch_radix_pass(const Config& c, int pass, const uint32_t* kin, const uint32_t* vin, uint32_t* kout,
                              uint32_t* vout, hipStream_t st);
 hipError_t launch_unique(const Config& c, const uint32_t* keys, hipStream_t st);

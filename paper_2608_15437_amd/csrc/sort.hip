@@ -190,7 +190,7 @@ __global__ __launch_bounds__(kSegBlock) void segments_kernel(Config c) {
 // in runs).
 constexpr int kCompactItems = 4;
 
-__global__ __launch_bounds__(kBlock) void compact_kernel(Config c, uint32_t* kout, uint32_t* vout) {
+__global__ __launch_bounds__(kBlock) void compact_kernel(Config c, uint32_t* kout) {
   static_assert(kChunkWords <= kBlock, "one bitmap word per thread");
   extern __shared__ float s_pose[];  // [S][12]
   __shared__ uint16_t s_list[kMaxChunkPoints];  // kept point offsets in the chunk, ascending
@@ -258,7 +258,6 @@ __global__ __launch_bounds__(kBlock) void compact_kernel(Config c, uint32_t* kou
                         quantize_axis(pz, c.mn[2], c.vs[2], c.Df[2], iz);
         if (!in) raise_fault(c.hdr, MMBEV_FAULT_INTERNAL);  // the filter kept it: never
         kout[q] = in ? ((uint32_t)iz * c.Dy + (uint32_t)iy) * c.Dx + (uint32_t)ix : 0u;
-        vout[q] = q;
         uint4* rr = reinterpret_cast<uint4*>(c.rec + (int64_t)q * RW);
         rr[0] = make_uint4(pi[u], __float_as_uint(px), __float_as_uint(py), __float_as_uint(pz));
         if (RW > 4)
@@ -359,7 +358,7 @@ __device__ __forceinline__ void load_sort_tile(const uint32_t* kin, const uint32
   for (int r = 0; r < kSortItems; ++r) {
     const uint32_t i = base + wave * (64 * kSortItems) + r * 64 + lane;
     key[r] = i < hi ? kin[i] : 0u;
-    val[r] = i < hi ? vin[i] : 0u;
+    val[r] = i < hi ? (vin != nullptr ? vin[i] : i) : 0u;  // no values: each key's own position
   }
 }
 
@@ -470,9 +469,9 @@ hipError_t launch_segments(const Config& c, hipStream_t st) {
   return hipGetLastError();
 }
 
-hipError_t launch_compact(const Config& c, uint32_t* kout, uint32_t* vout, hipStream_t st) {
+hipError_t launch_compact(const Config& c, uint32_t* kout, hipStream_t st) {
   const size_t lds = (size_t)c.S * 12 * sizeof(float);
-  hipLaunchKernelGGL(compact_kernel, dim3(c.fchunk_max), dim3(kBlock), lds, st, c, kout, vout);
+  hipLaunchKernelGGL(compact_kernel, dim3(c.fchunk_max), dim3(kBlock), lds, st, c, kout);
   return hipGetLastError();
 }
 

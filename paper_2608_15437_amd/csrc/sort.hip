@@ -183,8 +183,8 @@ __global__ __launch_bounds__(kSegBlock) void segments_kernel(Config c) {
 // One workgroup per filter chunk: its kept points, listed from the chunk's
 // bitmap in increasing index order, get the compact places [fprefix[k],
 // fprefix[k+1]).  For each: its record there (point index, p' of Eq. 6 from
-// the frame's poses staged in LDS, raw features; 16-byte stores) and the
-// (voxel key, compact place) pair the radix passes start from.  The key is
+// the frame's poses staged in LDS, raw features; 16-byte stores) and its
+// voxel key, which the first radix pass pairs with the compact place.  The key is
 // the definition's: correctly rounded (p' - min) / v per axis, truncated.
 // The reads of a chunk's kept points stay close together (kept points come
 // in runs).

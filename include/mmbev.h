@@ -74,7 +74,8 @@ typedef int32_t mmbev_status_t;
  * whatever the data; when the content of a device array breaks the contract
  * they OR one of these bits into the int32 at byte 0 of the workspace and the
  * output is unspecified.  Read it after the stream has completed. */
-#define MMBEV_FAULT_POINT_OFFSETS 1 /* point frame offsets not 0 .. num_points, non-decreasing */
+#define MMBEV_FAULT_POINT_OFFSETS 1 /* point frame offsets not 0 .. num_points, non-decreasing
+                                       (the call then keeps no point: no voxel is written) */
 #define MMBEV_FAULT_ROI_OFFSETS 2   /* ROI frame offsets not 0 .. num_rois, non-decreasing,
                                        or a frame with more than max_rois_per_frame ROIs */
 #define MMBEV_FAULT_INTERNAL 4      /* an internal consistency check failed (never with valid inputs) */

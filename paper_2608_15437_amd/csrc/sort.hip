@@ -448,7 +448,7 @@ __global__ __launch_bounds__(kBlock) void scatter_kernel(Config c, int pass, con
         kout[gp] = L.keys[i];
         vout[gp] = L.vals[i];
       } else {
-        raise_fault(h, MMBEV_FAULT_POINT_OFFSETS);
+        raise_fault(h, MMBEV_FAULT_INTERNAL);
       }
     }
     __syncthreads();

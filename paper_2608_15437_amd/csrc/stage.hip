@@ -81,8 +81,11 @@ __device__ __forceinline__ uint32_t frame_chunks(uint32_t n, uint32_t P) {
 }
 
 // The opening workgroup: counters, offset checks, filter chunk table and
-// the frame of every filter workgroup.  s_first: LDS for kLdsFirst words.
-__device__ void open_call(const Config& c, uint32_t* s_tmp, uint32_t* s_first) {
+// the frame of every filter workgroup.  s_first: LDS for kLdsFirst words;
+// s_bad: one LDS word.  Point offsets that break the contract lay out no
+// chunk at all: decreasing offsets would make frames overlap, and the kept
+// points of overlapping frames could outnumber the arrays sized for N.
+__device__ void open_call(const Config& c, uint32_t* s_tmp, uint32_t* s_first, int32_t* s_bad) {
   const int tid = threadIdx.x;
   WsHeader* h = c.hdr;
   if (tid == 0) {
@@ -92,7 +95,11 @@ __device__ void open_call(const Config& c, uint32_t* s_tmp, uint32_t* s_first) {
     h->voxels = 0;
     h->capped_voxels = 0;
     h->any_capped = 0;
+    *s_bad = 0;
   }
+  // the cleared fault word is visible to every wave before any of them ORs
+  // an offset fault into it
+  __syncthreads();
   int32_t bad = 0;
   for (int f = tid; f <= c.B; f += kBlock) {
     const int64_t o = c.frame_off[f];
@@ -107,7 +114,12 @@ __device__ void open_call(const Config& c, uint32_t* s_tmp, uint32_t* s_first) {
       if (rn < ro || rn - ro > c.max_rois) bad |= MMBEV_FAULT_ROI_OFFSETS;
     }
   }
-  if (bad) raise_fault(h, bad);
+  if (bad) {
+    raise_fault(h, bad);
+    atomicOr(s_bad, bad);
+  }
+  __syncthreads();
+  const bool no_points = (*s_bad & MMBEV_FAULT_POINT_OFFSETS) != 0;
   // chunks of frame b: ceil(points / fchunk_points) rounded up to a whole
   // filter workgroup (kWaves chunks), so that a workgroup's chunks never span
   // two frames; thread t owns frames [t*per, (t+1)*per); the count is capped
@@ -118,7 +130,7 @@ __device__ void open_call(const Config& c, uint32_t* s_tmp, uint32_t* s_first) {
   uint32_t mine = 0;
   for (int j = 0; j < per; ++j) {
     const int b = b0 + j;
-    if (b < c.B) {
+    if (b < c.B && !no_points) {
       const uint32_t f0 = point_offset(c, b), f1 = max(point_offset(c, b + 1), f0);
       mine += frame_chunks(f1 - f0, P);
     }
@@ -135,7 +147,7 @@ __device__ void open_call(const Config& c, uint32_t* s_tmp, uint32_t* s_first) {
       const uint32_t first = min(run, cap);
       c.fchunk_first[b] = first;
       const uint32_t f0 = point_offset(c, b), f1 = max(point_offset(c, b + 1), f0);
-      run += frame_chunks(f1 - f0, P);
+      run += no_points ? 0u : frame_chunks(f1 - f0, P);
       if (in_lds) {
         s_first[b] = first;
       } else {
@@ -180,10 +192,11 @@ __device__ void open_call(const Config& c, uint32_t* s_tmp, uint32_t* s_first) {
 __global__ __launch_bounds__(kBlock) void stage_kernel(Config c) {
   __shared__ __align__(16) int16_t s_rect[kMaxRois][4];
   __shared__ uint32_t s_tmp[kWaves];
+  __shared__ int32_t s_bad;
   const int tid = threadIdx.x;
   const int b = blockIdx.y;
   if (blockIdx.x == gridDim.x - 1) {  // the extra column opens the call, beside the frames' work
-    if (b == 0) open_call(c, s_tmp, reinterpret_cast<uint32_t*>(&s_rect[0][0]));
+    if (b == 0) open_call(c, s_tmp, reinterpret_cast<uint32_t*>(&s_rect[0][0]), &s_bad);
     return;
   }
 

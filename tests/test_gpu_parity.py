@@ -184,6 +184,38 @@ def test_device_fault_word_reports_bad_offsets(gpu_lib):
     assert vz.fault() & gpu_lib.FAULT_ROI_OFFSETS
 
 
+def test_fault_word_reports_offsets_of_late_frames(gpu_lib):
+    """Offsets that break the contract only in frame 150 of 200: the opening
+    workgroup's later waves check them, after the fault word is cleared.
+    Decreasing point offsets make the call keep nothing (frames would
+    overlap); every kernel still runs to its end."""
+    import torch
+
+    wl = synth.small(81, frames=200, beams=2, azimuths=16, sweeps=1, rois=4)
+    vz = gpu_lib.voxelizer_for_workload(wl, "cuda:0")
+    vz.run()
+    torch.cuda.synchronize()
+    assert vz.fault() == 0 and int(vz.result()["voxel_offsets"][-1]) > 0
+    fo = wl.frame_offsets.copy()
+    fo[150] = fo[151] + 5  # off[150] > off[151]
+    vz.frame_offsets = torch.as_tensor(fo).cuda()
+    vz.run()
+    torch.cuda.synchronize()
+    assert vz.fault() == gpu_lib.FAULT_POINT_OFFSETS
+    assert vz.result()["voxel_offsets"].tolist() == [0] * 201
+    vz.frame_offsets = torch.as_tensor(wl.frame_offsets).cuda()
+    ro = wl.roi_offsets.copy()
+    ro[150] = ro[151] + 1  # decreasing ROI offsets
+    vz.roi_frame_offsets = torch.as_tensor(ro).cuda()
+    vz.run()
+    torch.cuda.synchronize()
+    assert vz.fault() == gpu_lib.FAULT_ROI_OFFSETS
+    vz.roi_frame_offsets = torch.as_tensor(wl.roi_offsets).cuda()
+    vz.run()
+    torch.cuda.synchronize()
+    assert vz.fault() == 0
+
+
 def test_throughput_batch_full_size(gpu_lib):
     """The benchmark's batched workload, every frame checked against the oracle."""
     wl = synth.throughput(16)

@@ -60,7 +60,7 @@
 extern "C" {
 #endif
 
-#define MMBEV_ABI_VERSION 6
+#define MMBEV_ABI_VERSION 7
 
 /* ------------------------------------------------------------- status */
 typedef int32_t mmbev_status_t;
@@ -235,6 +235,44 @@ mmbev_status_t mmbev_roi_voxelize_ex(const mmbev_points_t* points, const uint8_t
                                      float* out_feats, int32_t* out_point_idx, int64_t* out_voxel_offsets,
                                      void* workspace, size_t workspace_bytes, void* stream, void* const* events,
                                      int32_t num_events, int32_t* events_recorded);
+
+/* ---------------------------------------- callers that cannot allocate */
+
+/* Bytes of the library's own device scratch (64 MiB): the largest workspace
+ * mmbev_roi_voxelize_noalloc can use -- enough for about a million points of
+ * five features with up to 32 ROIs per frame (mmbev_roi_voxelize_workspace_bytes
+ * gives the exact need of given sizes). */
+#define MMBEV_NOALLOC_SCRATCH_BYTES (64u << 20)
+
+/*
+ * mmbev_roi_voxelize without a workspace argument, for callers that cannot
+ * allocate device memory: code under HIP graph capture, tight serving loops,
+ * harnesses that forbid hipMalloc.  Same semantics, arguments, outputs,
+ * ownership and errors as mmbev_roi_voxelize; the workspace is instead an
+ * array of MMBEV_NOALLOC_SCRATCH_BYTES bytes of device memory inside the
+ * library, one per device, which every GPU the library runs on holds until
+ * the process ends.  The call allocates nothing.
+ *
+ * The first call on a device (the current device; `stream` must belong to
+ * it) looks up that device's array and clears its header on `stream`.  All
+ * calls on one device share its array, which keeps the last call's
+ * contents: calls that can overlap on one GPU (on different streams, or from
+ * host threads without ordering between them) race and leave unspecified
+ * results; order them on one stream.
+ *
+ * out_fault  device int32, may be NULL: receives the call's fault word
+ *            (MMBEV_FAULT_*, 0 for none) when the stream reaches the end of
+ *            the call (the array's own fault word is not reachable otherwise).
+ * Errors: as mmbev_roi_voxelize; MMBEV_ERR_UNSUPPORTED also when the sizes
+ * need a workspace larger than MMBEV_NOALLOC_SCRATCH_BYTES; MMBEV_ERR_HIP
+ * when the device's array cannot be looked up.
+ */
+mmbev_status_t mmbev_roi_voxelize_noalloc(const mmbev_points_t* points, const uint8_t* sweep_ids,
+                                          const float* sweep_poses, const mmbev_rois_t* rois,
+                                          const uint8_t* roi_sweep_budget, const mmbev_grid_t* grid_params,
+                                          int32_t* out_coords, int32_t* out_counts, float* out_feats,
+                                          int32_t* out_point_idx, int64_t* out_voxel_offsets, int32_t* out_fault,
+                                          void* stream);
 
 /* ------------------------------ temporal ROIs and criticality (host) */
 

@@ -4,6 +4,7 @@
 #include <algorithm>
 #include <cmath>
 #include <cstring>
+#include <mutex>
 
 #include "launch.hpp"
 
@@ -237,16 +238,15 @@ uint32_t keep_threshold(float rho) {
   return (uint32_t)std::floor(t + 0.5);
 }
 
-mmbev_status_t voxelize(const mmbev_points_t* points, const uint8_t* sweep_ids, const float* sweep_poses,
-                        const mmbev_rois_t* rois, const uint8_t* roi_sweep_budget, const mmbev_grid_t* grid,
-                        const mmbev_options_t* opt, int32_t* out_coords, int32_t* out_counts, float* out_feats,
-                        int32_t* out_point_idx, int64_t* out_voxel_offsets, void* workspace,
-                        size_t workspace_bytes, void* stream, EventTrail& ev) {
+// Every argument check of a call except the workspace's; fills the plan.
+mmbev_status_t check_args(const mmbev_points_t* points, const uint8_t* sweep_ids, const float* sweep_poses,
+                          const mmbev_rois_t* rois, const uint8_t* roi_sweep_budget, const mmbev_grid_t* grid,
+                          const mmbev_options_t* opt, int32_t* out_coords, int32_t* out_counts, float* out_feats,
+                          int32_t* out_point_idx, int64_t* out_voxel_offsets, Plan* p) {
   if (!points || !rois || !grid) return MMBEV_ERR_INVALID_ARG;
   if (opt && opt->reserved != 0) return MMBEV_ERR_INVALID_ARG;
   const int64_t N = points->num_points;
-  Plan p;
-  mmbev_status_t st = make_plan(grid, N, rois->max_rois_per_frame, points->num_features, &p);
+  mmbev_status_t st = make_plan(grid, N, rois->max_rois_per_frame, points->num_features, p);
   if (st != MMBEV_OK) return st;
   if (points->stride < N || points->stride >= ((int64_t)1 << 40)) return MMBEV_ERR_INVALID_ARG;
   if (N > 0 && (!points->feat || !sweep_ids)) return MMBEV_ERR_INVALID_ARG;
@@ -255,6 +255,19 @@ mmbev_status_t voxelize(const mmbev_points_t* points, const uint8_t* sweep_ids, 
   if (rois->num_rois > 0 && (!rois->boxes || !roi_sweep_budget)) return MMBEV_ERR_INVALID_ARG;
   if (!out_coords || !out_counts || !out_feats || !out_point_idx || !out_voxel_offsets)
     return MMBEV_ERR_INVALID_ARG;
+  return MMBEV_OK;
+}
+
+mmbev_status_t voxelize(const mmbev_points_t* points, const uint8_t* sweep_ids, const float* sweep_poses,
+                        const mmbev_rois_t* rois, const uint8_t* roi_sweep_budget, const mmbev_grid_t* grid,
+                        const mmbev_options_t* opt, int32_t* out_coords, int32_t* out_counts, float* out_feats,
+                        int32_t* out_point_idx, int64_t* out_voxel_offsets, void* workspace,
+                        size_t workspace_bytes, void* stream, EventTrail& ev) {
+  Plan p;
+  mmbev_status_t st = check_args(points, sweep_ids, sweep_poses, rois, roi_sweep_budget, grid, opt, out_coords,
+                                 out_counts, out_feats, out_point_idx, out_voxel_offsets, &p);
+  if (st != MMBEV_OK) return st;
+  const int64_t N = points->num_points;
   if (!workspace || ((uintptr_t)workspace & 255) || workspace_bytes < p.total) return MMBEV_ERR_WORKSPACE;
 
   Config c;
@@ -432,6 +445,65 @@ mmbev_status_t mmbev_roi_voxelize_ex(const mmbev_points_t* points, const uint8_t
                                stream, ev);
   if (events_recorded) *events_recorded = ev.used;
   return st;
+}
+
+}  // extern "C"
+
+// Workspace of mmbev_roi_voxelize_noalloc: MMBEV_NOALLOC_SCRATCH_BYTES of
+// device memory that the code object holds on every device it is loaded on,
+// until the process ends.  Host code never uses this name as an address (on
+// the host it only stands for the symbol): the device address comes from
+// hipGetSymbolAddress, once per device.
+static __device__ __align__(256) unsigned char scratch[MMBEV_NOALLOC_SCRATCH_BYTES];
+
+namespace {
+
+constexpr int kMaxScratchDevices = 64;
+std::mutex g_scratch_mutex;
+void* g_scratch[kMaxScratchDevices];  // device address of `scratch` on device d (null until set up)
+
+// The current device's scratch.  On the first call on a device: its address,
+// and its header cleared on `stream` by a kernel (the call counter starts at
+// zero; every other field is rewritten by each call).
+mmbev_status_t scratch_of_current_device(hipStream_t stream, void** out) {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxScratchDevices) return MMBEV_ERR_HIP;
+  std::lock_guard<std::mutex> lock(g_scratch_mutex);
+  if (g_scratch[dev] == nullptr) {
+    void* ptr = nullptr;
+    if (hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch)) != hipSuccess || ptr == nullptr) return MMBEV_ERR_HIP;
+    if (launch_fill_zero(ptr, sizeof(WsHeader), stream) != hipSuccess) return MMBEV_ERR_HIP;
+    g_scratch[dev] = ptr;
+  }
+  *out = g_scratch[dev];
+  return MMBEV_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+mmbev_status_t mmbev_roi_voxelize_noalloc(const mmbev_points_t* points, const uint8_t* sweep_ids,
+                                          const float* sweep_poses, const mmbev_rois_t* rois,
+                                          const uint8_t* roi_sweep_budget, const mmbev_grid_t* grid,
+                                          int32_t* out_coords, int32_t* out_counts, float* out_feats,
+                                          int32_t* out_point_idx, int64_t* out_voxel_offsets, int32_t* out_fault,
+                                          void* stream) {
+  Plan p;
+  mmbev_status_t st = check_args(points, sweep_ids, sweep_poses, rois, roi_sweep_budget, grid, nullptr, out_coords,
+                                 out_counts, out_feats, out_point_idx, out_voxel_offsets, &p);
+  if (st != MMBEV_OK) return st;
+  if (p.total > (size_t)MMBEV_NOALLOC_SCRATCH_BYTES) return MMBEV_ERR_UNSUPPORTED;
+  void* ws = nullptr;
+  st = scratch_of_current_device((hipStream_t)stream, &ws);
+  if (st != MMBEV_OK) return st;
+  EventTrail ev;
+  st = voxelize(points, sweep_ids, sweep_poses, rois, roi_sweep_budget, grid, nullptr, out_coords, out_counts,
+                out_feats, out_point_idx, out_voxel_offsets, ws, (size_t)MMBEV_NOALLOC_SCRATCH_BYTES, stream, ev);
+  if (st != MMBEV_OK) return st;
+  if (out_fault && launch_copy_fault(reinterpret_cast<const WsHeader*>(ws), out_fault, (hipStream_t)stream) != hipSuccess)
+    return MMBEV_ERR_HIP;
+  return MMBEV_OK;
 }
 
 mmbev_status_t mmbev_scatter_to_bev(const int32_t* coords, const float* feats, const int64_t* voxel_offsets,

@@ -18,6 +18,7 @@ hipError_t launch_finalize(const Config& c, hipStream_t st);
 hipError_t launch_cap(const Config& c, const uint32_t* vals, hipStream_t st);
 hipError_t launch_mean(const Config& c, const uint32_t* keys, const uint32_t* vals, hipStream_t st);
 hipError_t launch_fill_zero(void* p, size_t bytes, hipStream_t st);
+hipError_t launch_copy_fault(const WsHeader* h, int32_t* out, hipStream_t st);
 
 // ScatterToBEV: a clear of the whole map, then the voxels' values.
 struct BevConfig {

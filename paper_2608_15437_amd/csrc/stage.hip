@@ -265,6 +265,11 @@ __global__ __launch_bounds__(kBlock) void fill_zero_kernel(uint4* p, size_t n16,
     for (size_t t = threadIdx.x; t < ntail; t += kBlock) tail[t] = 0;
 }
 
+// The fault word of a call, copied to the caller's int32 (one thread).
+__global__ void copy_fault_kernel(const WsHeader* h, int32_t* out) {
+  if (threadIdx.x == 0) *out = __hip_atomic_load(&h->fault, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
 }  // namespace
 
 hipError_t launch_stage(const Config& c, hipStream_t st) {
@@ -282,6 +287,11 @@ hipError_t launch_fill_zero(void* p, size_t bytes, hipStream_t st) {
   int g = (int)std::min<size_t>((n16 + kBlock - 1) / kBlock + 1, 4096);
   hipLaunchKernelGGL(fill_zero_kernel, dim3(g), dim3(kBlock), 0, st, (uint4*)p, n16,
                      (uint8_t*)p + n16 * 16, ntail);
+  return hipGetLastError();
+}
+
+hipError_t launch_copy_fault(const WsHeader* h, int32_t* out, hipStream_t st) {
+  hipLaunchKernelGGL(copy_fault_kernel, dim3(1), dim3(64), 0, st, h, out);
   return hipGetLastError();
 }
 

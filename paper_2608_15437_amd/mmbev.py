@@ -118,6 +118,8 @@ def load() -> ctypes.CDLL:
         a = L.mmbev_roi_voxelize.argtypes
         L.mmbev_roi_voxelize_ex.argtypes = a[:6] + [ctypes.POINTER(mmbev_options_t)] + a[6:] + [p, ctypes.c_int32, p]
         L.mmbev_roi_voxelize_ex.restype = ctypes.c_int32
+        L.mmbev_roi_voxelize_noalloc.argtypes = a[:11] + [p, p]
+        L.mmbev_roi_voxelize_noalloc.restype = ctypes.c_int32
         L.mmbev_scatter_to_bev.argtypes = [p, p, p, ctypes.c_int32, ctypes.POINTER(mmbev_grid_t), p, p, p]
         L.mmbev_scatter_to_bev.restype = ctypes.c_int32
         L.mmbev_voxel_clusters_workspace_bytes.argtypes = [ctypes.POINTER(mmbev_grid_t),
@@ -229,6 +231,28 @@ def roi_voxelize(feat, frame_offsets, sweep_ids, sweep_poses, rois, roi_frame_of
     _check(load().mmbev_roi_voxelize_profiled(*args, handles, len(events), ctypes.byref(used)),
            "mmbev_roi_voxelize_profiled")
     return int(used.value)
+
+
+def roi_voxelize_noalloc(feat, frame_offsets, sweep_ids, sweep_poses, rois, roi_frame_offsets, roi_sweep_budget,
+                         grid: mmbev_grid_t, out_coords, out_counts, out_feats, out_point_idx, out_voxel_offsets,
+                         max_rois_per_frame: int, out_fault=None, stream=None) -> None:
+    """Enqueue mmbev_roi_voxelize_noalloc on `stream`: the same call as
+    roi_voxelize, with the library's own per-device scratch as its workspace
+    (nothing allocated).  out_fault: optional int32 tensor of one element that
+    receives the call's fault word."""
+    C = int(feat.shape[0])
+    N = int(sweep_ids.numel())
+    if N > 0 and feat.dim() == 2 and feat.stride(1) != 1:
+        raise MmbevError("feat rows must be contiguous")
+    pts = mmbev_points_t(feat=_ptr(feat), stride=int(feat.stride(0)) if feat.dim() == 2 else N,
+                         num_features=C, reserved=0, num_points=N, frame_offsets=_ptr(frame_offsets))
+    rr = mmbev_rois_t(boxes=_ptr(rois), frame_offsets=_ptr(roi_frame_offsets), num_rois=int(rois.shape[0]),
+                      max_rois_per_frame=int(max_rois_per_frame))
+    _check(load().mmbev_roi_voxelize_noalloc(ctypes.byref(pts), _ptr(sweep_ids), _ptr(sweep_poses), ctypes.byref(rr),
+                                             _ptr(roi_sweep_budget), ctypes.byref(grid), _ptr(out_coords),
+                                             _ptr(out_counts), _ptr(out_feats), _ptr(out_point_idx),
+                                             _ptr(out_voxel_offsets), _ptr(out_fault), _stream(stream)),
+           "mmbev_roi_voxelize_noalloc")
 
 
 def bev_map_shape(grid: mmbev_grid_t, num_features: int) -> tuple:

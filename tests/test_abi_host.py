@@ -62,7 +62,7 @@ def test_struct_layouts_match_header(mb):
     assert ctypes.sizeof(mb.mmbev_grid_t) == 52
     assert ctypes.sizeof(mb.mmbev_options_t) == 16
     assert mb.ROI_DTYPE.itemsize == 32
-    assert mb.abi_version() == 6
+    assert mb.abi_version() == 7
     assert ctypes.sizeof(mb.mmbev_policy_t) == 136
     assert mb.DETECTION_DTYPE.itemsize == 64 and mb.EGO_DTYPE.itemsize == 32 and mb.CRIT_DTYPE.itemsize == 16
     assert ctypes.sizeof(mb.mmbev_cluster_params_t) == 24
@@ -199,3 +199,25 @@ def test_voxel_clusters_validation(mb):
     assert call(ws=fake + 128) == mb.ERR_WORKSPACE
     assert call(ws_bytes=need - 1) == mb.ERR_WORKSPACE
     assert call(params=mb.cluster_params(1, 3, 0, 5, 1)) == mb.ERR_INVALID_ARG
+
+
+def test_noalloc_rejects_before_any_launch(mb):
+    """The no-alloc entry point checks its arguments, and that the sizes fit
+    its fixed scratch, before it touches the device."""
+    L = mb.load()
+    fake = 1 << 40  # never dereferenced: validation fails first
+    g = mb.grid_params((-54, -54, -5), (0.075, 0.075, 0.2), (1440, 1440, 40), 10, 120000, 10, 1)
+    limit = 64 << 20
+
+    def call(n, sweep=fake, outs=(fake,) * 5):
+        pts = mb.mmbev_points_t(feat=fake, stride=n, num_features=5, reserved=0, num_points=n, frame_offsets=fake)
+        rr = mb.mmbev_rois_t(boxes=fake, frame_offsets=fake, num_rois=32, max_rois_per_frame=32)
+        return L.mmbev_roi_voxelize_noalloc(ctypes.byref(pts), sweep, fake, ctypes.byref(rr), fake,
+                                            ctypes.byref(g), *outs, None, None)
+
+    big = 2_000_000
+    assert mb.roi_voxelize_workspace_bytes(g, big, 5, 32) > limit
+    assert mb.roi_voxelize_workspace_bytes(g, 347200, 5, 32) <= limit
+    assert call(big) == mb.ERR_UNSUPPORTED
+    assert call(347200, sweep=None) == mb.ERR_INVALID_ARG
+    assert call(347200, outs=(fake, fake, None, fake, fake)) == mb.ERR_INVALID_ARG

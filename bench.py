@@ -58,6 +58,7 @@ def source_sha(paths) -> str:
 
 
 def launch_names(vz) -> list:
+    """The launch groups of one call, in order (mmbev_roi_voxelize_profiled)."""
     g = vz.grid
     cells = g.dims[0] * g.dims[1] * g.dims[2]
     kb = max(1, (cells - 1).bit_length())
@@ -134,7 +135,7 @@ def time_graph_calls(vz, steps: int, warmup: int) -> float:
 
 
 def time_launches(vz, steps: int) -> dict:
-    """Mean duration of every launch of one call, from events recorded between launches."""
+    """Median duration of every launch group of one call, from events recorded between launches."""
     import torch
 
     names = launch_names(vz)
@@ -150,8 +151,95 @@ def time_launches(vz, steps: int) -> dict:
     torch.cuda.synchronize()
     out = {}
     for k, n in enumerate(names):
-        out[n] = statistics.mean(row[k].elapsed_time(row[k + 1]) for row in evs) * 1e3  # us
+        out[n] = statistics.median(row[k].elapsed_time(row[k + 1]) for row in evs) * 1e3  # us
     return out
+
+
+def cpu_model() -> str:
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return platform.processor() or platform.machine()
+
+
+def median_call_ms(run, steps: int, warmup: int) -> float:
+    """Median over `steps` calls of one call's duration, each bracketed by HIP
+    events on the current stream (after `warmup` calls)."""
+    import torch
+
+    for _ in range(warmup):
+        run()
+    torch.cuda.synchronize()
+    pairs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(steps)]
+    for a, b in pairs:
+        a.record()
+        run()
+        b.record()
+    torch.cuda.synchronize()
+    return statistics.median(a.elapsed_time(b) for a, b in pairs)
+
+
+def alg_bytes(wl, K: int, V: int) -> int:
+    """Algorithmic bytes of one call: x, y, z and the sweep id of every point,
+    the passthrough features of the kept points, the output rows, the ROI
+    records with their budgets, and the poses."""
+    C, M = wl.num_features, wl.grid.max_points
+    row = 16 + 4 + 4 * C + 4 * M
+    return 13 * wl.num_points + 4 * (C - 3) * K + row * V + 33 * len(wl.roi_desc) + 48 * wl.num_frames * wl.grid.num_sweeps
+
+
+def outputs_match(exp, got) -> tuple:
+    """(structure bit for bit, max |feature difference|) of an oracle and a GPU result."""
+    import numpy as np
+
+    V = int(exp["voxel_offsets"][-1])
+    same = bool(np.array_equal(exp["voxel_offsets"], got["voxel_offsets"]))
+    for k in ("coords", "counts", "point_idx"):
+        same = same and bool(np.array_equal(np.asarray(exp[k])[:V], np.asarray(got[k])[:V]))
+    err = float(np.max(np.abs(np.asarray(got["feats"])[:V].astype(np.float64) - exp["feats"][:V]))) if V and same else 0.0
+    return same, err
+
+
+def time_config(name: str, wl, dev, steps: int, warmup: int, with_oracle: bool) -> dict:
+    """One configuration: the median call (events around each call), the
+    median replay of a captured call, counts, algorithmic bytes and their rate
+    against the HBM peak, and the oracle on the same inputs."""
+    import torch
+
+    from paper_2608_15437_amd import mmbev
+
+    vz = mmbev.voxelizer_for_workload(wl, dev)
+    ms = median_call_ms(vz.run, steps, warmup)
+    msg = time_graph_calls(vz, steps, warmup)
+    h = vz.header()
+    res = vz.result()
+    N, K, V = wl.num_points, h["kept"], int(res["voxel_offsets"][-1])
+    alg = alg_bytes(wl, K, V)
+    gbs = alg / (ms * 1e-3) / 1e9
+    row = {"frames": wl.num_frames, "points": N, "rois": len(wl.roi_desc), "kept": K, "voxels": V,
+           "us_median": round(ms * 1e3, 2), "us_graph_mean": round(msg * 1e3, 2),
+           "mpoints_s": round(N / (ms * 1e-3) / 1e6, 1), "alg_bytes": alg, "gbps": round(gbs, 1),
+           "frac": round(gbs / HBM_PEAK_GBS, 4), "fault": h["fault"]}
+    if with_oracle:
+        import oracle
+
+        runs = 3 if N > 1_000_000 else 5
+        oracle.run_workload(wl)  # warm-up
+        times, exp = [], None
+        for _ in range(runs):
+            t0 = time.perf_counter()
+            exp = oracle.run_workload(wl)
+            times.append(time.perf_counter() - t0)
+        same, err = outputs_match(exp, res)
+        row.update({"oracle_ms_median": round(statistics.median(times) * 1e3, 2), "oracle_runs": runs,
+                    "matches_oracle": same and err <= 1e-5, "max_feat_diff": err})
+    del vz
+    torch.cuda.empty_cache()
+    return row
 
 
 def probe_traffic(frames: int) -> int:
@@ -315,6 +403,7 @@ def main() -> int:
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-two-streams", action="store_true",
                     help="skip the two-calls-in-flight measurement (kernel traces then time each kernel alone)")
+    ap.add_argument("--no-configs", action="store_true", help="skip the per-configuration rows (c1..c5)")
     ap.add_argument("--probe-traffic", action="store_true")
     ap.add_argument("--write-traffic", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"))
     args = ap.parse_args()
@@ -355,8 +444,7 @@ def main() -> int:
     C = wl.num_features
     R = len(wl.roi_desc)
     B, S, M = wl.num_frames, wl.grid.num_sweeps, wl.grid.max_points
-    row_bytes = 16 + 4 + 4 * C + 4 * M
-    alg_total = 13 * N + 4 * (C - 3) * K + row_bytes * V + 33 * R + 48 * B * S
+    alg_total = alg_bytes(wl, K, V)
     alg_filter = 13 * N + 33 * R + 48 * B * S
 
     log("[bench] timing every launch with events")
@@ -389,6 +477,20 @@ def main() -> int:
     vz1 = mmbev.voxelizer_for_workload(wl1, dev)
     us1 = time_calls(vz1, max(args.steps, 20), args.warmup) * 1e3
     us1g = time_graph_calls(vz1, max(args.steps, 20), args.warmup) * 1e3
+    del vz1
+
+    configs = {}
+    if not args.no_configs:
+        for name in ("c1", "c2", "c3", "c4", "c5"):
+            log(f"[bench] config {name}: median of {max(args.steps, 100)} calls, oracle beside it")
+            configs[name] = time_config(name, synth.CONFIGS[name](), dev, max(args.steps, 100), args.warmup,
+                                        not args.no_cpu_baseline)
+        c2r, c3r = configs["c2"], configs["c3"]
+        configs["roi_speedup_c3_over_c2"] = {
+            "time": round(c3r["us_median"] / c2r["us_median"], 3),
+            "voxels": round(c3r["voxels"] / max(c2r["voxels"], 1), 2),
+            "kept": round(c3r["kept"] / max(c2r["kept"], 1), 2),
+            "note": "the same 347,200 points with one all-covering ROI (dense) against 32 temporal ROIs"}
 
     log("[bench] temporal-ROI selector (host) on 128 detection caches")
     selector = time_selector(args.steps)
@@ -416,12 +518,12 @@ def main() -> int:
         t_med = statistics.median(times)
         cpu = {"value": round(N / t_med / 1e6, 3), "unit": "Mpoints/s", "cores": 1, "kind": "oracle",
                "sample": f"the full {F}-frame batch ({N} points), {len(times)} run(s), median; "
-                         f"CPU {platform.processor() or platform.machine()}, nproc {os.cpu_count()}"}
-        same = (np.array_equal(exp["voxel_offsets"], res["voxel_offsets"])
-                and np.array_equal(exp["coords"], res["coords"]) and np.array_equal(exp["point_idx"], res["point_idx"]))
-        if not same:
+                         f"CPU {cpu_model()}, nproc {os.cpu_count()}"}
+        same, err = outputs_match(exp, res)
+        if not same or err > 1e-5:
             log("[bench] WARNING: GPU output differs from the oracle")
-        cpu["gpu_output_matches"] = bool(same)
+        cpu["gpu_output_matches"] = bool(same and err <= 1e-5)
+        cpu["max_feat_diff"] = err
 
     out = {
         "metric": METRIC,
@@ -443,12 +545,16 @@ def main() -> int:
                      "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": traffic,
                      "kernel": "filter_kernel", "kernel_us": round(filt_us, 2),
                      "alg_bytes_per_launch": alg_filter},
-        "path_gbps": round(alg_total / (ms * 1e-3) / 1e9, 1),
+        "path_roofline": {"bound": "hbm", "achieved": round(alg_total / (ms * 1e-3) / 1e9, 1), "peak": HBM_PEAK_GBS,
+                          "unit": "GB/s", "frac": round(alg_total / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+                          "alg_bytes_per_call": alg_total,
+                          "note": "the whole call: 13 N + 4 (C-3) K + row V + 33 R + 48 B S bytes over ms_per_step"},
         "two_streams": two,
         "launch_us": {k: round(v, 2) for k, v in per.items()},
         "single_frame": {"points": wl1.num_points, "us_per_call": round(us1, 2),
                          "mpoints_s": round(wl1.num_points / (us1 * 1e-6) / 1e6, 1),
                          "us_per_call_graph": round(us1g, 2)},
+        "configs": configs,
         "scatter_to_bev": bev,
         "voxel_clusters": {"batch": clusters, "single_ouster_frame": clusters1},
         "roi_selector": selector,

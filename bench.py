@@ -64,7 +64,7 @@ def launch_names(vz) -> list:
     kb = max(1, (cells - 1).bit_length())
     passes = (kb + 8) // 9  # digits of at most 9 bits; frames are kept apart, not sorted
     return (["stage", "filter", "segments", "compact"] + [f"sort{p}" for p in range(passes)]
-            + ["unique", "finalize", "cap", "mean"])
+            + ["heads", "fincap", "mean"])
 
 
 def time_calls(vz, steps: int, warmup: int) -> float:

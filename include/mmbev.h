@@ -205,9 +205,8 @@ mmbev_status_t mmbev_roi_voxelize(const mmbev_points_t* points, const uint8_t* s
  * caller's events (hipEvent_t, created with timing enabled) on `stream`, as
  * long as events remain.  The groups, in order: ROI staging, point filter,
  * chunk layout (segments), compaction and records, then one radix pass per
- * key digit of at most 9 bits (count, per-frame scan and scatter launches),
- * voxel heads (two launches), finalisation, per-frame voxel cap, mean
- * pooling.  Returns the number of events recorded through *events_recorded
+ * key digit of at most 9 bits (count and scatter launches), voxel heads,
+ * finalisation with the per-frame voxel cap, mean pooling.  Returns the number of events recorded through *events_recorded
  * (host int32, may be NULL).  Elapsed time between events k and k+1 is the
  * duration of group k.
  */

@@ -66,10 +66,10 @@ struct Plan {
   int32_t B, S, C, M, cap, max_rois, W;
   int32_t cell_shift, ncx, ncy, ncells;
   int32_t kb, passes, dbits;
-  int64_t fchunk_points, fchunk_max, filter_grid, schunk_max, mean_grid;
-  size_t off_hdr, off_cellmask, off_cellany, off_budgetmask, off_fchunk_first, off_tileframe, off_fbits, off_fcount, off_fchunk_lo, off_fchunk_frame, off_wgframe, off_spare, off_fprefix,
-      off_fstart, off_schunk_first, off_schunk, off_cnt, off_ftot, off_hcount, off_vcount, off_keys[2], off_vals[2], off_rec, off_seg,
-      off_capkey, off_rank, off_voxoff, total;
+  int64_t fchunk_points, fchunk_max, filter_grid, schunk_max, vtile_max, mean_grid;
+  size_t off_hdr, off_cellmask, off_cellany, off_budgetmask, off_fchunk_first, off_fbits, off_fcount, off_fchunk_lo, off_fchunk_frame, off_wgframe, off_spare, off_fprefix,
+      off_fstart, off_schunk_first, off_schunk, off_schunk_frame, off_cnt, off_vtile, off_vt_first, off_hcount, off_hpre, off_mtile, off_keys[2], off_vals[2], off_rec,
+      off_hpos, off_hplace, off_capbits, off_rank, off_voxoff, total;
 };
 
 mmbev_status_t make_plan(const mmbev_grid_t* g, int64_t N, int32_t max_rois, int32_t C, Plan* p) {
@@ -126,8 +126,9 @@ mmbev_status_t make_plan(const mmbev_grid_t* g, int64_t N, int32_t max_rois, int
     p->fchunk_max = (N + P - 1) / P + (int64_t)kWaves * p->B;  // each frame rounded up to whole workgroups
     p->filter_grid = std::max<int64_t>(1, (p->fchunk_max + kWaves - 1) / kWaves);
   }
-  p->schunk_max = kSortGrid + p->B;
-  p->mean_grid = std::max<int64_t>(1, std::min<int64_t>((n1 + kMeanTile - 1) / kMeanTile, 2048));
+  p->schunk_max = std::min<int64_t>(N / kSortTile + p->B, (int64_t)kMaxFrameChunks * p->B) + 1;
+  p->vtile_max = N / kVoxTile + p->B + 1;
+  p->mean_grid = std::min<int64_t>((n1 + kMeanTile - 1) / kMeanTile, 2048);
   size_t o = 0;
   auto take = [&](size_t bytes) {
     size_t at = o;
@@ -149,20 +150,23 @@ mmbev_status_t make_plan(const mmbev_grid_t* g, int64_t N, int32_t max_rois, int
   p->off_fstart = take((size_t)(p->B + 1) * 4);
   p->off_schunk_first = take((size_t)(p->B + 1) * 4);
   p->off_schunk = take((size_t)p->schunk_max * 16);
+  p->off_schunk_frame = take((size_t)p->schunk_max * 8);
   p->off_cnt = take((size_t)p->schunk_max * kSortBins * 4);
-  p->off_ftot = take((size_t)p->B * kSortBins * 4);
-  p->off_hcount = take((size_t)p->schunk_max * 4);
-  p->off_vcount = take((size_t)p->B * 4);
+  p->off_vtile = take((size_t)p->vtile_max * 16);
+  p->off_vt_first = take((size_t)(p->B + 1) * 4);
+  p->off_hcount = take((size_t)p->vtile_max * 4);
+  p->off_hpre = take((size_t)(p->vtile_max + 1) * 4);
+  p->off_mtile = take(((size_t)n1 / kMeanTile + 2) * 4);
   for (int q = 0; q < 2; ++q) {
     p->off_keys[q] = take((size_t)n1 * 4);
     p->off_vals[q] = take((size_t)n1 * 4);
   }
   p->off_rec = take((size_t)n1 * 4 * ((1 + p->C + 3) / 4 * 4));
-  p->off_seg = take((size_t)n1 * 4);
-  p->off_capkey = take((size_t)n1 * 4);
+  p->off_hpos = take((size_t)n1 * 4);
+  p->off_hplace = take((size_t)n1 * 4);
+  p->off_capbits = take((3 * ((size_t)n1 / 32 + p->B + 1) + (size_t)p->vtile_max + 1) * 4);
   p->off_rank = take((size_t)n1 * 4);
   p->off_voxoff = take((size_t)(p->B + 1) * 4);
-  p->off_tileframe = take((size_t)((n1 + kMeanTile - 1) / kMeanTile + 1) * 4);
   p->total = o;
   return MMBEV_OK;
 }
@@ -341,21 +345,24 @@ mmbev_status_t voxelize(const mmbev_points_t* points, const uint8_t* sweep_ids, 
   c.fstart = (uint32_t*)(ws + p.off_fstart);
   c.schunk_first = (uint32_t*)(ws + p.off_schunk_first);
   c.schunk = (uint4*)(ws + p.off_schunk);
+  c.schunk_frame = (uint2*)(ws + p.off_schunk_frame);
   c.cnt = (uint32_t*)(ws + p.off_cnt);
-  c.ftot = (uint32_t*)(ws + p.off_ftot);
+  c.vtile = (uint4*)(ws + p.off_vtile);
+  c.vt_first = (uint32_t*)(ws + p.off_vt_first);
   c.hcount = (uint32_t*)(ws + p.off_hcount);
-  c.vcount = (uint32_t*)(ws + p.off_vcount);
+  c.hpre = (uint32_t*)(ws + p.off_hpre);
+  c.mtile = (uint32_t*)(ws + p.off_mtile);
   for (int q = 0; q < 2; ++q) {
     c.keys[q] = (uint32_t*)(ws + p.off_keys[q]);
     c.vals[q] = (uint32_t*)(ws + p.off_vals[q]);
   }
   c.rec = (uint32_t*)(ws + p.off_rec);
   c.rec_words = (1 + p.C + 3) / 4 * 4;
-  c.seg_start = (uint32_t*)(ws + p.off_seg);
-  c.capkey = (uint32_t*)(ws + p.off_capkey);
+  c.hpos = (uint32_t*)(ws + p.off_hpos);
+  c.hplace = (uint32_t*)(ws + p.off_hplace);
+  c.capbits = (uint32_t*)(ws + p.off_capbits);
   c.out_rank = (uint32_t*)(ws + p.off_rank);
   c.vox_off = (uint32_t*)(ws + p.off_voxoff);
-  c.tile_frame = (uint32_t*)(ws + p.off_tileframe);
   c.fchunk_points = (int32_t)p.fchunk_points;
   c.fchunk_words = (int32_t)(p.fchunk_points / 32);
   c.fchunk_max = (int32_t)p.fchunk_max;
@@ -370,6 +377,7 @@ mmbev_status_t voxelize(const mmbev_points_t* points, const uint8_t* sweep_ids, 
   c.lds_cell = c.lds_bm + c.lds_bm_cap;
   c.lds_dyn_bytes = (int32_t)(((size_t)(c.lds_cell + c.lds_cell_cap) * 4 + 15) / 16 * 16);
   c.schunk_max = (int32_t)p.schunk_max;
+  c.vtile_max = (int32_t)p.vtile_max;
   c.mean_grid = (int32_t)p.mean_grid;
 
   hipStream_t s = (hipStream_t)stream;
@@ -390,9 +398,8 @@ mmbev_status_t voxelize(const mmbev_points_t* points, const uint8_t* sweep_ids, 
                                 c.keys[pass % 2], c.vals[pass % 2], s));
   const uint32_t* keys = c.keys[(c.passes - 1) % 2];
   const uint32_t* vals = c.vals[(c.passes - 1) % 2];
-  MMBEV_TRY(launch_unique(c, keys, s));
-  MMBEV_TRY(launch_finalize(c, s));
-  MMBEV_TRY(launch_cap(c, vals, s));
+  MMBEV_TRY(launch_heads(c, keys, vals, s));
+  MMBEV_TRY(launch_fincap(c, s));
   MMBEV_TRY(launch_mean(c, keys, vals, s));
 #undef MMBEV_TRY
   if (ev.mark(s) != hipSuccess) return MMBEV_ERR_HIP;

@@ -33,10 +33,11 @@ constexpr int kSortBins = 1 << kMaxDigitBits;  // 512
 constexpr int kSortItems = 8;         // pairs per thread in a scatter tile
 constexpr int kSortTile = kBlock * kSortItems;  // 2048 pairs
 constexpr int kCountItems = 16;       // pairs per thread per batch of the count kernel
-constexpr int kSortGrid = 1024;       // pair chunks aimed for (chunks never straddle frames)
+constexpr int kMaxFrameChunks = 32;   // pair chunks of one frame at most (chunks never straddle frames)
 constexpr int kScanItems = 16;        // items per thread in the single-workgroup scans
 constexpr int kScanTile = kBlock * kScanItems;  // 4096
 constexpr int kMeanTile = kBlock;     // one voxel per thread
+constexpr int kVoxTile = 2048;        // sorted pairs of a voxel tile (the heads, cap and mean kernels' unit)
 
 // Workspace header: per-call counters, rewritten by the first kernels of a call.
 struct alignas(256) WsHeader {
@@ -48,7 +49,7 @@ struct alignas(256) WsHeader {
   uint32_t any_capped;        // 1 if some frame exceeds max_voxels
   uint32_t fchunks;           // filter chunks (points of one frame each)
   uint32_t schunks;           // pair chunks (pairs of one frame each)
-  uint32_t chunk_pairs;       // pairs per pair chunk (the last chunk of a frame: fewer)
+  uint32_t vtiles;            // voxel tiles (kVoxTile sorted pairs of one frame each, the last one shorter)
 };
 
 // Everything a kernel needs, computed once on the host and passed by value.
@@ -101,10 +102,13 @@ struct Config {
   uint32_t* fstart;        // [B+1] first sorted pair of frame b (kept pairs of the frames before it)
   uint32_t* schunk_first;  // [B+1] first pair chunk of frame b
   uint4* schunk;           // [schunk_max] pair chunk k: (first pair, end, frame, first pair of the frame)
-  uint32_t* cnt;           // [schunk_max][kSortBins] digit counts of a pass -> offsets inside the frame
-  uint32_t* ftot;          // [B][kSortBins] digit totals of every frame
-  uint32_t* hcount;        // [schunk_max] voxel heads of pair chunk k
-  uint32_t* vcount;        // [B] voxels of frame b
+  uint2* schunk_frame;     // [schunk_max] pair chunk k: its frame's chunks [x, y)
+  uint32_t* cnt;           // [schunk_max][kSortBins] digit counts of chunk k in a pass
+  uint4* vtile;            // [vtile_max] voxel tile t: (first pair, end, frame, first pair of the frame)
+  uint32_t* vt_first;      // [B+1] first voxel tile of frame b
+  uint32_t* hcount;        // [vtile_max] voxels (heads) of tile t
+  uint32_t* hpre;          // [vtile_max + 1] voxels of the tiles before t (all frames)
+  uint32_t* mtile;         // [N / kMeanTile + 2] tile of voxel i * kMeanTile (the mean's blocks)
   uint32_t* keys[2];       // [N] each: ping-pong buffers of the radix passes
   uint32_t* vals[2];       // the pair's record: its place in compact (point) order
   // records of the kept points in compact order, written by the compaction:
@@ -112,12 +116,15 @@ struct Config {
   // x', y', z' (Eq. 6) and the raw features 3..C-1 as float bits
   uint32_t* rec;           // [N][rec_words]
   int32_t rec_words;
-  // per voxel, at slot fstart[b] + v for voxel v of frame b
-  uint32_t* seg_start;     // [N] first sorted pair of the voxel
-  uint32_t* capkey;        // [N] first point index of the voxel (frames over the cap)
-  uint32_t* out_rank;      // [N] row inside its frame, or ~0u (frames over the cap)
+  // per voxel, at slot vtile[t].x + j for voxel j of tile t
+  uint32_t* hpos;          // [N] first sorted pair of the voxel
+  uint32_t* hplace;        // [N] its place (its first point: places follow point order)
+  uint32_t* out_rank;      // [N] row inside its frame, or ~0u (frames over the cap only)
+  uint32_t* capbits;       // frames over the cap whose tables exceed LDS: three regions of N / 32 + B + 1
+                           // words (first-place bits, kept flags, their prefix; frame b from word
+                           // fstart[b] / 32 + b of each), then [vtile_max] tile prefixes (frame b from
+                           // its first tile)
   uint32_t* vox_off;       // [B+1] voxels of the frames before b
-  uint32_t* tile_frame;    // [ceil(N / kMeanTile) + 1] frame of voxel t * kMeanTile; last: B - 1
   // sizes
   int32_t fchunk_points;   // points per filter chunk (a multiple of kWaveTile, <= kMaxChunkPoints)
   int32_t fchunk_words;    // fchunk_points / 32
@@ -129,7 +136,8 @@ struct Config {
   // offset lds_cell: a zero word, then the cell words); a cap of 0 means
   // "not staged"
   int32_t lds_pose_cap, lds_roi_cap, lds_bm_cap, lds_cell_cap, lds_roi, lds_bm, lds_cell, lds_dyn_bytes;
-  int32_t schunk_max;      // bound on pair chunks: kSortGrid + B
+  int32_t schunk_max;      // bound on pair chunks: min(N / kSortTile + B, kMaxFrameChunks * B) + 1
+  int32_t vtile_max;       // bound on voxel tiles: N / kVoxTile + B + 1
   int32_t mean_grid;
 };
 
@@ -183,6 +191,14 @@ __device__ __forceinline__ int32_t frame_of_chunk(const uint32_t* first, int32_t
       hi = mid - 1;
   }
   return lo;
+}
+
+// Pairs per chunk of a frame of n kept pairs: at most kMaxFrameChunks
+// chunks, each a whole number of scatter tiles.
+__device__ __forceinline__ uint32_t frame_chunk_pairs(uint32_t n) {
+  uint32_t ch = (n + kMaxFrameChunks - 1) / kMaxFrameChunks;
+  ch = (ch + kSortTile - 1) / kSortTile * kSortTile;
+  return max(ch, (uint32_t)kSortTile);
 }
 
 // Point frame offset b clamped into [0, N].

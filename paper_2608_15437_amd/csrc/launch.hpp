@@ -13,9 +13,8 @@ hipError_t launch_segments(const Config& c, hipStream_t st);
 hipError_t launch_compact(const Config& c, uint32_t* kout, hipStream_t st);
 hipError_t launch_radix_pass(const Config& c, int pass, const uint32_t* kin, const uint32_t* vin, uint32_t* kout,
                              uint32_t* vout, hipStream_t st);
-hipError_t launch_unique(const Config& c, const uint32_t* keys, hipStream_t st);
-hipError_t launch_finalize(const Config& c, hipStream_t st);
-hipError_t launch_cap(const Config& c, const uint32_t* vals, hipStream_t st);
+hipError_t launch_heads(const Config& c, const uint32_t* keys, const uint32_t* vals, hipStream_t st);
+hipError_t launch_fincap(const Config& c, hipStream_t st);
 hipError_t launch_mean(const Config& c, const uint32_t* keys, const uint32_t* vals, hipStream_t st);
 hipError_t launch_fill_zero(void* p, size_t bytes, hipStream_t st);
 hipError_t launch_copy_fault(const WsHeader* h, int32_t* out, hipStream_t st);

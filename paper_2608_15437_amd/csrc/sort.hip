@@ -12,9 +12,10 @@
 // every frame.
 //
 // segments -- one workgroup: the kept-pair prefix of the filter chunks, the
-//             first pair of every frame, and the pair chunks (about
-//             kSortGrid of them, chunk_pairs pairs each, the last of a frame
-//             shorter).
+//             first pair of every frame, and the pair chunks (at most
+//             kMaxFrameChunks per frame, whole scatter tiles, the last of a
+//             frame shorter) and the voxel tiles of the later kernels
+//             (kVoxTile pairs, the last of a frame shorter).
 // compact  -- one workgroup per filter chunk: its kept pairs (at the start of the
 //             chunk's point range) copied to their compact place, and the
 //             kept points' records (index, x', y', z', features) written
@@ -22,10 +23,10 @@
 // Then per pass:
 // count    -- workgroup k counts the digits of pair chunk k (row k of the
 //             [chunk][digit] count matrix);
-// rowscan  -- workgroup b turns the rows of frame b's chunks into offsets
-//             inside the frame (an exclusive scan down each digit's column)
-//             and writes the frame's digit totals;
-// scatter  -- workgroup k walks its chunk tile by tile (the next tile's
+// scatter  -- workgroup k sums the count rows of its frame's chunks (the
+//             frame's digit totals, and its digits in the earlier chunks:
+//             where each of its digits starts), then walks its chunk tile by
+//             tile (the next tile's
 //             pairs loading while the current one is handled): ranks each
 //             pair inside the tile (wave multi-split), reorders the tile by
 //             digit in LDS, and writes every digit's run to its place.
@@ -35,11 +36,14 @@ namespace mmbev {
 
 namespace {
 
-// Lanes of this wave holding the same digit (valid lanes only).
-__device__ __forceinline__ uint64_t match_digit(uint32_t dig, bool valid, int dbits) {
+// Lanes of this wave holding the same digit (valid lanes only): one ballot
+// per bit of the widest digit, unrolled so that the ballots do not wait for
+// each other (narrower digits have zero high bits).
+__device__ __forceinline__ uint64_t match_digit(uint32_t dig, bool valid) {
   uint64_t m = __ballot(valid);
-  for (int bit = 0; bit < dbits; ++bit) {
-    const uint32_t on = (dig >> bit) & 1u;
+#pragma unroll
+  for (int bit = 0; bit < kMaxDigitBits; ++bit) {
+    const bool on = (dig >> bit) & 1u;
     const uint64_t bb = __ballot(on);
     m &= on ? bb : ~bb;
   }
@@ -73,15 +77,20 @@ constexpr int kSegBlock = 1024;  // threads of the segments kernel
 constexpr int kSegWaves = kSegBlock / 64;
 constexpr int kSegLdsFrames = 4096;  // frame starts kept in LDS up to this many frames
 
+// kLds: the frame starts are built in LDS (B <= kSegLdsFrames) and copied
+// out at the end; otherwise in the workspace directly.  (One address space per
+// instance: a pointer that may be either compiles to generic instructions,
+// whose waits cover both kinds of access.)
+template <bool kLds>
 __global__ __launch_bounds__(kSegBlock) void segments_kernel(Config c) {
   __shared__ uint32_t s_tmp[kSegWaves];
-  __shared__ uint32_t s_fstart[kSegLdsFrames + 1];  // frame starts, when B <= kSegLdsFrames
+  __shared__ uint32_t s_fstart[kLds ? kSegLdsFrames + 1 : 1];  // frame starts
   __shared__ int32_t s_last;
   WsHeader* h = c.hdr;
   const int tid = threadIdx.x;
   const uint32_t nf = h->fchunks;
-  const bool lds = c.B <= kSegLdsFrames;
-  uint32_t* fstart = lds ? s_fstart : c.fstart;
+  constexpr bool lds = kLds;
+  uint32_t* fstart = kLds ? s_fstart : c.fstart;
   if (tid == 0) s_last = -1;
   // kept-point prefix of the filter chunks; the first chunk of a frame also
   // gives the start of that frame and of the empty frames just before it.
@@ -146,36 +155,66 @@ __global__ __launch_bounds__(kSegBlock) void segments_kernel(Config c) {
   __syncthreads();
   if (lds)
     for (int g = tid; g <= c.B; g += kSegBlock) c.fstart[g] = s_fstart[g];
-  // pair chunks: about kSortGrid of them, whole kSortTile multiples
-  uint32_t CH = (K + kSortGrid - 1) / kSortGrid;
-  CH = max((uint32_t)kSortTile, (CH + kSortTile - 1) / kSortTile * kSortTile);
+  // pair chunks, frame by frame: at most kMaxFrameChunks per frame, of
+  // frame_chunk_pairs pairs (whole kSortTile multiples; the last one of a
+  // frame shorter)
   const int per = (c.B + kSegBlock - 1) / kSegBlock;
   const int b0 = tid * per;
   uint32_t mine = 0;
   for (int j = 0; j < per; ++j) {
     const int b = b0 + j;
-    if (b < c.B) mine += (fstart[b + 1] - fstart[b] + CH - 1) / CH;
+    if (b < c.B) {
+      const uint32_t n = fstart[b + 1] - fstart[b];
+      mine += (n + frame_chunk_pairs(n) - 1) / frame_chunk_pairs(n);
+    }
   }
   uint32_t total;
   uint32_t run = block_exclusive_scan<kSegWaves>(mine, s_tmp, total);
-  const uint32_t cap = (uint32_t)c.schunk_max;  // never reached: K / CH <= kSortGrid
+  const uint32_t cap = (uint32_t)c.schunk_max;  // never reached: the bound holds for any K <= N
   for (int j = 0; j < per; ++j) {
     const int b = b0 + j;
     if (b < c.B) {
       const uint32_t f0 = fstart[b], f1 = fstart[b + 1];
+      const uint32_t CH = frame_chunk_pairs(f1 - f0);
       const uint32_t n = (f1 - f0 + CH - 1) / CH;
-      c.schunk_first[b] = min(run, cap);
-      for (uint32_t k = run; k < min(run + n, cap); ++k) {
+      const uint32_t k0 = min(run, cap), k1 = min(run + n, cap);
+      c.schunk_first[b] = k0;
+      for (uint32_t k = k0; k < k1; ++k) {
         const uint32_t lo = f0 + (k - run) * CH;
         c.schunk[k] = make_uint4(lo, min(lo + CH, f1), (uint32_t)b, f0);
+        c.schunk_frame[k] = make_uint2(k0, k1);
       }
       run += n;
+    }
+  }
+  // voxel tiles: frame by frame, kVoxTile sorted pairs each (the last one
+  // of a frame shorter)
+  uint32_t mine_vt = 0;
+  for (int j = 0; j < per; ++j) {
+    const int b = b0 + j;
+    if (b < c.B) mine_vt += (fstart[b + 1] - fstart[b] + kVoxTile - 1) / kVoxTile;
+  }
+  uint32_t total_vt;
+  uint32_t run_vt = block_exclusive_scan<kSegWaves>(mine_vt, s_tmp, total_vt);
+  const uint32_t cap_vt = (uint32_t)c.vtile_max;  // never reached: the bound holds for any K <= N
+  for (int j = 0; j < per; ++j) {
+    const int b = b0 + j;
+    if (b < c.B) {
+      const uint32_t f0 = fstart[b], f1 = fstart[b + 1];
+      const uint32_t n = (f1 - f0 + kVoxTile - 1) / kVoxTile;
+      c.vt_first[b] = min(run_vt, cap_vt);
+      for (uint32_t t = run_vt; t < min(run_vt + n, cap_vt); ++t) {
+        const uint32_t lo = f0 + (t - run_vt) * kVoxTile;
+        c.vtile[t] = make_uint4(lo, min(lo + kVoxTile, f1), (uint32_t)b, f0);
+      }
+      run_vt += n;
     }
   }
   if (tid == 0) {
     c.schunk_first[c.B] = min(total, cap);
     h->schunks = min(total, cap);
-    h->chunk_pairs = CH;
+    c.vt_first[c.B] = min(total_vt, cap_vt);
+    h->vtiles = min(total_vt, cap_vt);
     h->kept = K;
   }
 }
@@ -304,42 +343,6 @@ __global__ __launch_bounds__(kBlock) void count_kernel(Config c, int pass, const
   }
 }
 
-// Frame b: every digit's column over the frame's chunks -> exclusive
-// offsets inside the frame (in place), and the frame's digit totals.
-__global__ __launch_bounds__(kBlock) void rowscan_kernel(Config c) {
-  // thread t: digits t and t + kBlock, kRows chunk rows of both loaded
-  // together (one round trip for a frame of up to kRows chunks)
-  constexpr int kRows = 8;
-  static_assert(kSortBins == 2 * kBlock, "two digits per thread");
-  const int tid = threadIdx.x;
-  const int32_t b = blockIdx.x;
-  const uint32_t nbins = 1u << c.dbits;
-  const uint32_t k0 = c.schunk_first[b], k1 = max(c.schunk_first[b + 1], k0);
-  const uint32_t d0 = (uint32_t)tid, d1 = (uint32_t)(tid + kBlock);
-  uint32_t run0 = 0, run1 = 0;
-  for (uint32_t kb = k0; kb < k1; kb += kRows) {
-    uint32_t x0[kRows], x1[kRows];
-#pragma unroll
-    for (int u = 0; u < kRows; ++u) {
-      const uint32_t k = kb + u;
-      x0[u] = k < k1 && d0 < nbins ? c.cnt[(int64_t)k * kSortBins + d0] : 0u;
-      x1[u] = k < k1 && d1 < nbins ? c.cnt[(int64_t)k * kSortBins + d1] : 0u;
-    }
-#pragma unroll
-    for (int u = 0; u < kRows; ++u) {
-      const uint32_t k = kb + u;
-      if (k < k1) {
-        if (d0 < nbins) c.cnt[(int64_t)k * kSortBins + d0] = run0;
-        if (d1 < nbins) c.cnt[(int64_t)k * kSortBins + d1] = run1;
-        run0 += x0[u];
-        run1 += x1[u];
-      }
-    }
-  }
-  if (d0 < nbins) c.ftot[(int64_t)b * kSortBins + d0] = run0;
-  if (d1 < nbins) c.ftot[(int64_t)b * kSortBins + d1] = run1;
-}
-
 struct ScatterLds {
   uint32_t run[kSortBins];  // next output position of every digit
   uint32_t wave_cnt[kWaves][kSortBins];
@@ -369,28 +372,52 @@ __global__ __launch_bounds__(kBlock) void scatter_kernel(Config c, int pass, con
   const int lane = tid & 63, wave = tid >> 6;
   WsHeader* h = c.hdr;
   const uint32_t k = blockIdx.x;
-  // the chunk's entry and its digit-offset row load with the counts (in
-  // bounds for any k < schunk_max)
+  // the chunk's entry and its frame's chunks load with the counts (in bounds
+  // for any k < schunk_max)
   const uint32_t nsc = h->schunks, K = h->kept;
   const uint4 ch = c.schunk[k];
+  const uint2 fc = c.schunk_frame[k];
   static_assert(kSortBins == 2 * kBlock, "two digits per thread");
-  const uint32_t off0 = c.cnt[(int64_t)k * kSortBins + tid], off1 = c.cnt[(int64_t)k * kSortBins + kBlock + tid];
-  asm volatile("" ::"s"(ch.x), "s"(ch.y), "s"(ch.z), "s"(ch.w), "v"(off0), "v"(off1));  // keeps the loads above the check
+  asm volatile("" ::"s"(ch.x), "s"(ch.y), "s"(ch.z), "s"(ch.w), "s"(fc.x), "s"(fc.y));  // keeps the loads above the check
   if (k >= nsc) return;
   const int shift = pass * c.dbits;
   const uint32_t nbins = 1u << c.dbits;
   const uint32_t mask = nbins - 1u;
   const uint32_t lo = ch.x, hi = ch.y;
-  const int32_t b = (int32_t)ch.z;
   uint32_t key[kSortItems], val[kSortItems], nkey[kSortItems], nval[kSortItems];
   if (lo < hi) load_sort_tile(kin, vin, lo, hi, key, val);
-  // base of every digit: frame start + smaller digits of the frame + this
-  // chunk's offset among the frame's chunks
-  for (uint32_t e = tid; e < nbins; e += kBlock) L.run[e] = c.ftot[(int64_t)b * kSortBins + e];
-  __syncthreads();
-  scan_bins(L.run, L.run, (int)nbins, L.scan_tmp);
-  if ((uint32_t)tid < nbins) L.run[tid] += ch.w + off0;
-  if ((uint32_t)(kBlock + tid) < nbins) L.run[kBlock + tid] += ch.w + off1;
+  // base of every digit: frame start + the frame's smaller digits + this
+  // digit in the frame's earlier chunks, from the count rows of the frame's
+  // chunks (at most kMaxFrameChunks rows; thread t: digits t and t + kBlock)
+  {
+    constexpr int kRows = 8;
+    const uint32_t k0 = fc.x, k1 = max(fc.y, k0);
+    uint32_t pre0 = 0, pre1 = 0, tot0 = 0, tot1 = 0;
+    for (uint32_t kk = k0; kk < k1; kk += kRows) {
+      uint32_t x0[kRows], x1[kRows];
+#pragma unroll
+      for (int u = 0; u < kRows; ++u) {  // the rows' loads in flight together
+        const bool ok = kk + u < k1;
+        x0[u] = ok ? c.cnt[(int64_t)(kk + u) * kSortBins + tid] : 0u;
+        x1[u] = ok ? c.cnt[(int64_t)(kk + u) * kSortBins + kBlock + tid] : 0u;
+      }
+#pragma unroll
+      for (int u = 0; u < kRows; ++u) {
+        if (kk + u < k) {
+          pre0 += x0[u];
+          pre1 += x1[u];
+        }
+        tot0 += x0[u];
+        tot1 += x1[u];
+      }
+    }
+    L.run[tid] = tot0;
+    L.run[kBlock + tid] = tot1;
+    __syncthreads();
+    scan_bins(L.run, L.run, (int)nbins, L.scan_tmp);
+    if ((uint32_t)tid < nbins) L.run[tid] += ch.w + pre0;
+    if ((uint32_t)(kBlock + tid) < nbins) L.run[kBlock + tid] += ch.w + pre1;
+  }
   const uint64_t lt = lanemask_lt();
   for (uint32_t base = lo; base < hi; base += kSortTile) {
     const bool more = base + kSortTile < hi;
@@ -407,7 +434,7 @@ __global__ __launch_bounds__(kBlock) void scatter_kernel(Config c, int pass, con
     // wave multi-split over the rounds: tile order is (wave, round, lane)
 #pragma unroll
     for (int r = 0; r < kSortItems; ++r) {
-      const uint64_t m = match_digit(dig[r], valid[r], c.dbits);
+      const uint64_t m = match_digit(dig[r], valid[r]);
       uint32_t prior = 0;
       if (valid[r]) prior = L.wave_cnt[wave][dig[r]];
       __builtin_amdgcn_wave_barrier();
@@ -465,7 +492,10 @@ __global__ __launch_bounds__(kBlock) void scatter_kernel(Config c, int pass, con
 }  // namespace
 
 hipError_t launch_segments(const Config& c, hipStream_t st) {
-  hipLaunchKernelGGL(segments_kernel, dim3(1), dim3(kSegBlock), 0, st, c);
+  if (c.B <= kSegLdsFrames)
+    hipLaunchKernelGGL(segments_kernel<true>, dim3(1), dim3(kSegBlock), 0, st, c);
+  else
+    hipLaunchKernelGGL(segments_kernel<false>, dim3(1), dim3(kSegBlock), 0, st, c);
   return hipGetLastError();
 }
 
@@ -478,10 +508,7 @@ hipError_t launch_compact(const Config& c, uint32_t* kout, hipStream_t st) {
 hipError_t launch_radix_pass(const Config& c, int pass, const uint32_t* kin, const uint32_t* vin, uint32_t* kout,
                              uint32_t* vout, hipStream_t st) {
   hipLaunchKernelGGL(count_kernel, dim3(c.schunk_max), dim3(kBlock), 0, st, c, pass, kin);
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(rowscan_kernel, dim3(c.B), dim3(kBlock), 0, st, c);
-  e = hipGetLastError();
+  const hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(scatter_kernel, dim3(c.schunk_max), dim3(kBlock), 0, st, c, pass, kin, vin, kout, vout);
   return hipGetLastError();

@@ -1,96 +1,46 @@
 // After the sort: voxels, per-frame cap, mean pooling.
 //
-// The sorted pairs are grouped by frame and ordered by key inside each
-// frame; the pair chunks of the radix passes (each inside one frame) are
-// reused.  Per-voxel data sits at slot fstart[b] + v for voxel v of frame b
-// (a frame has no more voxels than kept pairs).
-// ucount   -- heads (first pair of every run of equal keys inside a frame)
-//             per pair chunk;
-// uwrite   -- numbers the heads inside their frame (the heads of the frame's
-//             earlier chunks come first) and writes each voxel's first
-//             sorted pair at its slot;
-// finalize -- one workgroup: every frame's voxels, the voxels of the frames
-//             before it (global voxel numbering), and the output offsets of
-//             every frame (at most max_voxels rows each) with the
-//             capped-voxel count;
-// cap      -- one workgroup per frame: the frame of each tile of the mean
-//             that starts in it; for frames over max_voxels, radix select
-//             of the voxels with the smallest first point index, then their
-//             rank in key order (the output row inside the frame);
-// mean     -- one thread per voxel: output row, and the mean of the voxel's
-//             first max_points points from their compact records (x', y',
-//             z' of Eq. 6 and the raw features), summed in double in
-//             ascending point order (Alg. 1 VoxelFeatureEncoder read as mean
-//             pooling).
+// The sorted pairs are grouped by frame and ordered by (key, place) inside
+// each frame.  The pairs of every frame are cut into voxel tiles of
+// kVoxTile pairs (segments); voxel j of tile t is the tile's j-th head (the
+// first pair of a run of equal keys), and its per-voxel data sits at the
+// tile-local slot vtile[t].lo + j (a tile has no more heads than pairs), so
+// no kernel needs the voxel numbering of other tiles to place its voxels.
+// heads  -- one workgroup per tile (grid-stride): the heads numbered in pair order, each
+//           one's position (hpos) and place (hplace: its first point, since
+//           places follow point order) at its slot; the tile's head count;
+// fincap -- workgroup 0: the voxels before every tile (all frames), every
+//           frame's voxels and its output offsets (at most max_voxels rows
+//           per frame); workgroup 1 + b: frame b, if it has more than
+//           max_voxels voxels, keeps the max_voxels voxels whose first
+//           point comes first and numbers them in key order (out_rank);
+// mean   -- blocks of kMeanTile consecutive voxels (grid-stride), one
+//           thread per voxel: its tile, its output row, and the mean of its first max_points points from
+//           their compact records (x', y', z' of Eq. 6 and the raw
+//           features), summed in double in ascending point order (Alg. 1
+//           VoxelFeatureEncoder read as mean pooling).
 #include "launch.hpp"
 
 namespace mmbev {
 
 namespace {
 
-// Frame b of global voxel g: largest b in [lo, hi] with vox_off[b] <= g
-// (the caller knows g's frame lies in that range).
-__device__ __forceinline__ int32_t frame_of_voxel(const Config& c, uint32_t g, int32_t lo, int32_t hi) {
-  while (lo < hi) {
-    int32_t mid = (lo + hi + 1) >> 1;
-    if (c.vox_off[mid] <= g)
-      lo = mid;
-    else
-      hi = mid - 1;
-  }
-  return lo;
-}
-
 // Whether sorted pair i of a frame whose first pair is ff starts a voxel.
 __device__ __forceinline__ bool is_head(const uint32_t* keys, uint32_t ff, uint32_t i) {
   return i == ff || keys[i] != keys[i - 1];
 }
 
-__global__ __launch_bounds__(kBlock) void ucount_kernel(Config c, const uint32_t* keys) {
-  __shared__ uint32_t s_tmp[kWaves];
-  const int tid = threadIdx.x;
-  const uint32_t k = blockIdx.x;
-  const uint32_t nsc = c.hdr->schunks;
-  const uint4 ch = c.schunk[k];  // in bounds for any k < schunk_max: loads with the count
-  asm volatile("" ::"s"(ch.x), "s"(ch.y), "s"(ch.z), "s"(ch.w));  // keeps the load above the check
-  if (k >= nsc) return;
-  const uint32_t lo = ch.x, hi = ch.y, ff = ch.w;
-  uint32_t n = 0;
-  for (uint32_t base = lo; base < hi; base += kBlock * kCountItems) {
-    bool hd[kCountItems];
-#pragma unroll
-    for (int j = 0; j < kCountItems; ++j) {
-      const uint32_t i = base + j * kBlock + tid;
-      hd[j] = i < hi && is_head(keys, ff, i);
-    }
-#pragma unroll
-    for (int j = 0; j < kCountItems; ++j) n += hd[j] ? 1u : 0u;
-  }
-  uint32_t total;
-  (void)block_exclusive_scan(n, s_tmp, total);
-  if (tid == 0) c.hcount[k] = total;
-}
-
-__global__ __launch_bounds__(kBlock) void uwrite_kernel(Config c, const uint32_t* keys) {
-  __shared__ uint32_t s_tmp[kWaves];
+__global__ __launch_bounds__(kBlock) void heads_kernel(Config c, const uint32_t* keys, const uint32_t* vals) {
   __shared__ uint32_t s_off[kCountItems][kWaves];  // heads before row j of wave w in the batch
   __shared__ uint32_t s_batch;
   const int tid = threadIdx.x;
   const int lane = tid & 63, wave = tid >> 6;
-  const uint32_t k = blockIdx.x;
-  const uint32_t nsc = c.hdr->schunks;
-  const uint4 ch = c.schunk[k];  // in bounds for any k < schunk_max: loads with the count
-  asm volatile("" ::"s"(ch.x), "s"(ch.y), "s"(ch.z), "s"(ch.w));  // keeps the load above the check
-  if (k >= nsc) return;
-  const uint32_t lo = ch.x, hi = ch.y, ff = ch.w;
-  uint32_t v0;
-  {
-    uint32_t part = 0;
-    for (uint32_t w = c.schunk_first[ch.z] + tid; w < k; w += kBlock) part += c.hcount[w];
-    uint32_t before;
-    (void)block_exclusive_scan(part, s_tmp, before);
-    v0 = before;
-  }
+  const uint32_t nvt = c.hdr->vtiles;
+  const uint64_t lt = lanemask_lt();
+  for (uint32_t t = blockIdx.x; t < nvt; t += gridDim.x) {
+  const uint4 vt = c.vtile[t];
+  const uint32_t lo = vt.x, hi = vt.y, ff = vt.w;
+  uint32_t v0 = 0;
   // batches of kCountItems rows of kBlock consecutive pairs (coalesced);
   // heads numbered in pair order: row, then wave, then lane
   for (uint32_t base = lo; base < hi; base += kBlock * kCountItems) {
@@ -115,196 +65,333 @@ __global__ __launch_bounds__(kBlock) void uwrite_kernel(Config c, const uint32_t
       s_batch = run;
     }
     __syncthreads();
-    const uint64_t lt = lanemask_lt();
 #pragma unroll
     for (int j = 0; j < kCountItems; ++j)
-      if ((m[j] >> lane) & 1u)
-        c.seg_start[ff + v0 + s_off[j][wave] + (uint32_t)__popcll(m[j] & lt)] = base + j * kBlock + tid;
+      if ((m[j] >> lane) & 1u) {
+        const uint32_t slot = lo + v0 + s_off[j][wave] + (uint32_t)__popcll(m[j] & lt);
+        const uint32_t i = base + j * kBlock + tid;
+        c.hpos[slot] = i;
+        c.hplace[slot] = vals[i];
+      }
     v0 += s_batch;
     __syncthreads();
   }
+  if (tid == 0) c.hcount[t] = v0;
+  }
 }
 
-// Exclusive prefix of n values in[0..n) written to out (may alias, or null);
-// returns the total.  One workgroup, kScanItems consecutive values per thread.
-__device__ uint32_t scan_array(const uint32_t* in, uint32_t* out, uint32_t n, uint32_t* s_tmp) {
+constexpr int kFinBlock = 1024;
+constexpr int kFinWaves = kFinBlock / 64;
+constexpr int kCapLdsWords = 16384;  // bitmaps of a capped frame in LDS up to this many words
+constexpr int kCapLdsTiles = 8192;   // voxel counts of a capped frame's tiles in LDS up to this many tiles
+
+// Exclusive prefix of n values in[0..n) written to out by one workgroup of
+// kFinBlock threads; returns the total.
+__device__ uint32_t scan_fin(const uint32_t* in, uint32_t* out, uint32_t n, uint32_t* s_tmp) {
   const int tid = threadIdx.x;
+  constexpr int kItems = 8;
   uint32_t carry = 0;
-  for (uint32_t base = 0; base < n; base += kScanTile) {
-    const uint32_t first = base + tid * kScanItems;
-    uint32_t v[kScanItems], sum = 0;
+  for (uint32_t base = 0; base < n; base += kFinBlock * kItems) {
+    const uint32_t first = base + tid * kItems;
+    uint32_t v[kItems], sum = 0;
 #pragma unroll
-    for (int j = 0; j < kScanItems; ++j) {
+    for (int j = 0; j < kItems; ++j) {
       v[j] = first + j < n ? in[first + j] : 0u;
       sum += v[j];
     }
     uint32_t total;
-    uint32_t run = carry + block_exclusive_scan(sum, s_tmp, total);
-    if (out)
+    uint32_t run = carry + block_exclusive_scan<kFinWaves>(sum, s_tmp, total);
 #pragma unroll
-      for (int j = 0; j < kScanItems; ++j)
-        if (first + j < n) {
-          out[first + j] = run;
-          run += v[j];
-        }
+    for (int j = 0; j < kItems; ++j)
+      if (first + j < n) {
+        out[first + j] = run;
+        run += v[j];
+      }
     carry += total;
   }
   return carry;
 }
 
-__global__ __launch_bounds__(kBlock) void finalize_kernel(Config c) {
-  __shared__ uint32_t s_tmp[kWaves];
+// Workgroup 0 of fincap.
+__device__ void finalize_offsets(const Config& c, uint32_t* s_tmp) {
   const int tid = threadIdx.x;
   WsHeader* h = c.hdr;
-  const uint32_t ns = h->schunks;
-  // heads before every pair chunk (in place), then every frame's voxels
-  const uint32_t V = scan_array(c.hcount, c.hcount, ns, s_tmp);
+  const uint32_t nvt = h->vtiles;
+  const uint32_t V = scan_fin(c.hcount, c.hpre, nvt, s_tmp);
+  if (tid == 0) c.hpre[nvt] = V;
   __syncthreads();
-  for (int b = tid; b < c.B; b += kBlock) {
-    const uint32_t k0 = min(c.schunk_first[b], ns), k1 = min(c.schunk_first[b + 1], ns);
-    c.vcount[b] = (k1 < ns ? c.hcount[k1] : V) - (k0 < ns ? c.hcount[k0] : V);
+  // the mean's block i (voxels i * kMeanTile ...) starts in tile mtile[i]
+  for (uint32_t t = tid; t < nvt; t += kFinBlock) {
+    const uint32_t v0 = c.hpre[t], v1 = c.hpre[t + 1];
+    for (uint32_t i = (v0 + kMeanTile - 1) / kMeanTile; (uint64_t)i * kMeanTile < v1; ++i) c.mtile[i] = t;
   }
-  __syncthreads();
-  (void)scan_array(c.vcount, c.vox_off, (uint32_t)c.B, s_tmp);
-  if (tid == 0) {
-    c.vox_off[c.B] = V;
-    h->voxels = V;
-  }
-  if (tid == 0) c.tile_frame[(V + kMeanTile - 1) / kMeanTile] = (uint32_t)(c.B - 1);
+  if (tid == 0) c.mtile[(V + kMeanTile - 1) / kMeanTile] = nvt > 0 ? nvt - 1 : 0u;
   uint32_t carry_out = 0, carry_cap = 0;
-  for (int chunk = 0; chunk < c.B; chunk += kBlock) {
-    const int b = chunk + tid;
-    const uint32_t vb = b < c.B ? c.vcount[b] : 0u;
+  for (int32_t chunk = 0; chunk < c.B; chunk += kFinBlock) {
+    const int32_t b = chunk + tid;
+    uint32_t vb = 0;
+    if (b < c.B) {
+      const uint32_t t0 = min(c.vt_first[b], nvt), t1 = max(min(c.vt_first[b + 1], nvt), t0);
+      const uint32_t v0 = c.hpre[t0];
+      vb = c.hpre[t1] - v0;
+      c.vox_off[b] = v0;
+    }
     const uint32_t capped = vb > (uint32_t)c.cap;
     const uint32_t outc = capped ? (uint32_t)c.cap : vb;
     uint32_t t1, t2;
-    const uint32_t e1 = block_exclusive_scan(outc, s_tmp, t1);
-    (void)block_exclusive_scan(capped ? vb : 0u, s_tmp, t2);
+    const uint32_t e1 = block_exclusive_scan<kFinWaves>(outc, s_tmp, t1);
+    (void)block_exclusive_scan<kFinWaves>(capped ? vb : 0u, s_tmp, t2);
     if (b < c.B) c.out_voxel_offsets[b] = (int64_t)(carry_out + e1);
     carry_out += t1;
     carry_cap += t2;
   }
   if (tid == 0) {
+    c.vox_off[c.B] = V;
     c.out_voxel_offsets[c.B] = (int64_t)carry_out;
+    h->voxels = V;
     h->capped_voxels = carry_cap;
     h->any_capped = carry_cap > 0 ? 1u : 0u;
   }
 }
 
-// One workgroup per frame: the frame's entries of the mean's tile table;
-// then frames within the cap return.  Selects the max_voxels voxels with the smallest first point index (radix select of
-// the max_voxels-th smallest first index, four 8-bit rounds; first indices
-// are distinct), then numbers the kept voxels in key order.
-__global__ __launch_bounds__(kBlock) void cap_kernel(Config c, const uint32_t* vals) {
-  __shared__ uint32_t s_hist[256];
-  __shared__ uint32_t s_tmp[kWaves];
-  __shared__ uint32_t s_sel, s_k;
-  const int tid = threadIdx.x;
-  const int b = blockIdx.x;
-  {
-    // frame b for the tiles of kMeanTile voxels whose first voxel is in it
-    // (the mean's workgroups search only between the frames of their tile
-    // and of the next one)
-    const uint32_t v0 = c.vox_off[b], v1 = c.vox_off[b + 1];
-    for (uint32_t t = (v0 + kMeanTile - 1) / kMeanTile + tid; (uint64_t)t * kMeanTile < v1; t += kBlock)
-      c.tile_frame[t] = (uint32_t)b;
+struct CapLds {
+  uint32_t hc[kCapLdsTiles];    // voxels of the frame's tiles
+  uint32_t area[kCapLdsWords];  // first-place bits, then kept flags and their word prefix
+  uint32_t tmp[kFinWaves];
+  uint32_t sel;
+};
+
+// Workgroup 1 + b of fincap: frame b's voxel cap.  The frame keeps the
+// max_voxels voxels whose first place (hplace, distinct, in [fstart[b],
+// fstart[b+1])) is smallest.  Every pass runs over the frame's slots
+// [fstart[b], fstart[b+1]) in order (tile after tile; slot lo + j of a tile
+// holds its voxel j when j < its voxel count): slot order restricted to the
+// voxels is key order.  The first places are marked in a bitmap over the
+// frame's places, the max_voxels-th marked place is found from a prefix of
+// the words' popcounts, the kept voxels are flagged in slot order (one
+// ballot per 64 slots) and numbered by a prefix of those flag words.  The
+// tables sit in LDS when they fit, otherwise in the frame's regions of the
+// workspace.
+// The tables of a capped frame: in LDS (kLds) or in the frame's regions of
+// the workspace, each pointer of one address space only, so that the
+// compiler emits LDS or global instructions rather than generic ones (whose
+// waits would also wait for the other kind).
+template <bool kLds>
+__device__ void cap_frame(const Config& c, int32_t b, CapLds& S, uint32_t t0, uint32_t nt) {
+  const int tid = threadIdx.x, lane = tid & 63;
+  const uint32_t fs = c.fstart[b], nk = max(c.fstart[b + 1], fs) - fs;
+  const size_t words = (size_t)c.N / 32 + (size_t)c.B + 1;  // one region of the workspace's capbits
+  const uint32_t wbase = fs / 32 + (uint32_t)b;
+  uint32_t* hc = kLds ? S.hc : c.capbits + 3 * words + t0;
+  if (kLds)
+    for (uint32_t i = tid; i < nt; i += kFinBlock) hc[i] = c.hcount[t0 + i];
+  // slot fs + i holds a voxel when its offset in its tile is below the tile's count
+  auto holds_voxel = [&](uint32_t i) -> bool { return i < nk && (i % kVoxTile) < hc[i / kVoxTile]; };
+  const uint32_t nw = (nk + 31) / 32;
+  uint32_t* bits = kLds ? S.area : c.capbits + wbase;
+  constexpr int kUnroll = 32;  // loads in flight per thread: one workgroup walks the whole frame
+  // 1. the first places marked
+  for (uint32_t w = tid; w < nw; w += kFinBlock) bits[w] = 0u;
+  __syncthreads();  // also: the tiles' counts are in place
+  for (uint32_t base = tid; base < nk; base += kFinBlock * kUnroll) {
+    uint32_t p[kUnroll];
+#pragma unroll
+    for (int u = 0; u < kUnroll; ++u) {  // all loads of the batch in flight together
+      const uint32_t i = base + u * kFinBlock;
+      p[u] = holds_voxel(i) ? c.hplace[fs + i] - fs : 0xffffffffu;
+    }
+#pragma unroll
+    for (int u = 0; u < kUnroll; ++u)
+      if (p[u] < nk) atomicOr(&bits[p[u] >> 5], 1u << (p[u] & 31));
   }
-  const uint32_t nv = c.vcount[b];
-  if (nv <= (uint32_t)c.cap) return;
-  const uint32_t fs = c.fstart[b];
-  uint32_t* fk = c.capkey + fs;
-  for (uint32_t v = tid; v < nv; v += kBlock) fk[v] = vals[c.seg_start[fs + v]];
   __syncthreads();
-  uint32_t prefix = 0, pmask = 0, k = (uint32_t)c.cap;
-  for (int shift = 24; shift >= 0; shift -= 8) {
-    s_hist[tid] = 0;
-    __syncthreads();
-    for (uint32_t v = tid; v < nv; v += kBlock) {
-      const uint32_t key = fk[v];
-      if ((key & pmask) == prefix) atomicAdd(&s_hist[(key >> shift) & 255u], 1u);
+  // 2. the max_voxels-th smallest first place: thread t counts a contiguous run of words
+  {
+    const uint32_t per = (nw + kFinBlock - 1) / kFinBlock;
+    const uint32_t w0 = min(tid * per, nw), w1 = min(w0 + per, nw);
+    uint32_t mine = 0;
+    for (uint32_t w = w0; w < w1; ++w) mine += (uint32_t)__popc(bits[w]);
+    uint32_t all;
+    const uint32_t before = block_exclusive_scan<kFinWaves>(mine, S.tmp, all);
+    const uint32_t want = (uint32_t)c.cap;
+    if (before < want && before + mine >= want) {
+      uint32_t seen = before;
+      for (uint32_t w = w0; w < w1; ++w) {
+        uint32_t x = bits[w];
+        const uint32_t pc = (uint32_t)__popc(x);
+        if (seen + pc >= want) {
+          for (uint32_t k = want - seen; k > 1; --k) x &= x - 1u;  // drop the lower set bits
+          S.sel = fs + w * 32 + (uint32_t)__builtin_ctz(x);
+          break;
+        }
+        seen += pc;
+      }
     }
-    __syncthreads();
-    uint32_t total;
-    const uint32_t cnt = s_hist[tid];
-    const uint32_t excl = block_exclusive_scan(cnt, s_tmp, total);
-    if (excl < k && excl + cnt >= k) {  // the bin holding the k-th smallest
-      s_sel = (uint32_t)tid;
-      s_k = k - excl;
-    }
-    __syncthreads();
-    prefix |= s_sel << shift;
-    pmask |= 255u << shift;
-    k = s_k;
-    __syncthreads();
   }
-  const uint32_t threshold = prefix;  // the max_voxels-th smallest first index
-  uint32_t carry = 0;
-  for (uint32_t base = 0; base < nv; base += kBlock) {
-    const uint32_t v = base + tid;
-    const bool keep = v < nv && fk[v] <= threshold;
-    uint32_t total;
-    const uint32_t excl = block_exclusive_scan(keep ? 1u : 0u, s_tmp, total);
-    if (v < nv) c.out_rank[fs + v] = keep ? carry + excl : 0xffffffffu;
-    carry += total;
+  __syncthreads();
+  const uint32_t thr = S.sel;
+  // 3. kept voxels flagged in slot order (after the marks: the area is reused)
+  uint32_t* kb = kLds ? S.area : c.capbits + words + wbase;
+  uint32_t* wp = kLds ? S.area + nw : c.capbits + 2 * words + wbase;
+  for (uint32_t base = (uint32_t)(tid & ~63); base < nk; base += kFinBlock * kUnroll) {
+    uint32_t p[kUnroll];
+#pragma unroll
+    for (int u = 0; u < kUnroll; ++u) {
+      const uint32_t i = base + u * kFinBlock + (uint32_t)lane;
+      p[u] = holds_voxel(i) ? c.hplace[fs + i] : 0xffffffffu;
+    }
+#pragma unroll
+    for (int u = 0; u < kUnroll; ++u) {
+      const uint32_t i0 = base + u * kFinBlock;  // the wave's first slot of this step
+      const uint64_t m = __ballot(p[u] <= thr);
+      if (i0 < nk) {
+        if (lane == 0) kb[i0 >> 5] = (uint32_t)m;
+        if (lane == 32 && i0 + 32 < nk) kb[(i0 >> 5) + 1] = (uint32_t)(m >> 32);
+      }
+    }
+  }
+  __syncthreads();
+  // 4. kept voxels before each flag word
+  {
+    const uint32_t per = (nw + kFinBlock - 1) / kFinBlock;
+    const uint32_t w0 = min(tid * per, nw), w1 = min(w0 + per, nw);
+    uint32_t mine = 0;
+    for (uint32_t w = w0; w < w1; ++w) mine += (uint32_t)__popc(kb[w]);
+    uint32_t all;
+    uint32_t run = block_exclusive_scan<kFinWaves>(mine, S.tmp, all);
+    for (uint32_t w = w0; w < w1; ++w) {
+      wp[w] = run;
+      run += (uint32_t)__popc(kb[w]);
+    }
+  }
+  __syncthreads();
+  // 5. the kept voxels' rows inside the frame
+  for (uint32_t base = tid; base < nk; base += kFinBlock * 8) {
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      const uint32_t i = base + u * kFinBlock;
+      if (holds_voxel(i)) {
+        const uint32_t word = kb[i >> 5];
+        const bool keep = (word >> (i & 31)) & 1u;
+        c.out_rank[fs + i] = keep ? wp[i >> 5] + (uint32_t)__popc(word & ((1u << (i & 31)) - 1u)) : 0xffffffffu;
+      }
+    }
   }
 }
 
-// Workgroups of kMeanTile consecutive voxels (grid-stride), one thread per
-// voxel: output row, kept count, point indices and the fp64 mean of every
-// feature.  The records of a voxel's points are read kMeanBatch at a time,
-// all their loads in flight together.  When the block's rows are consecutive (no frame
-// over the cap in it) the rows are assembled in LDS and written as
-// contiguous runs; otherwise each thread writes its own row.
+__global__ __launch_bounds__(kFinBlock) void fincap_kernel(Config c) {
+  __shared__ CapLds S;
+  const int tid = threadIdx.x;
+  if (blockIdx.x == 0) {
+    finalize_offsets(c, S.tmp);
+    return;
+  }
+  const int32_t b = (int32_t)blockIdx.x - 1;
+  const uint32_t nvt = c.hdr->vtiles;
+  const uint32_t t0 = min(c.vt_first[b], nvt), t1 = max(min(c.vt_first[b + 1], nvt), t0);
+  const uint32_t nt = t1 - t0;
+  // the frame's voxels (and, for tables in the workspace, its tiles' counts)
+  const size_t words = (size_t)c.N / 32 + (size_t)c.B + 1;
+  const uint32_t fs = c.fstart[b], nk = max(c.fstart[b + 1], fs) - fs;
+  const bool lds = nt <= (uint32_t)kCapLdsTiles && 2 * ((nk + 31) / 32) <= (uint32_t)kCapLdsWords;
+  uint32_t mine = 0;
+  for (uint32_t i = tid; i < nt; i += kFinBlock) {
+    const uint32_t v = c.hcount[t0 + i];
+    if (!lds) c.capbits[3 * words + t0 + i] = v;
+    mine += v;
+  }
+  uint32_t total;
+  (void)block_exclusive_scan<kFinWaves>(mine, S.tmp, total);
+  if (total <= (uint32_t)c.cap) return;  // uniform
+  if (lds)
+    cap_frame<true>(c, b, S, t0, nt);
+  else
+    cap_frame<false>(c, b, S, t0, nt);
+}
+
+// Blocks of kMeanTile consecutive voxels (grid-stride), one thread per
+// voxel: its tile (between the tiles of its block and of the next block),
+// output row, kept count, point indices and the fp64 mean of every feature.
+// The records of a voxel's points are read kMeanBatch at a time, all their
+// loads in flight together.  When the block's rows are consecutive (no frame
+// over the cap in it) they are assembled in LDS and written as contiguous
+// runs; otherwise each thread writes its own row.
 constexpr int kMeanBatch = 4;  // more records in flight per thread cost occupancy (VGPRs)
 
 __global__ __launch_bounds__(kBlock) void mean_kernel(Config c, const uint32_t* keys, const uint32_t* vals) {
   extern __shared__ uint32_t sm[];
   __shared__ int64_t s_row0;
-  __shared__ uint32_t s_contig;
   WsHeader* h = c.hdr;
   const int tid = threadIdx.x;
-  const uint32_t V = h->voxels;
+  const uint32_t nvt = h->vtiles;
   const uint32_t K = h->kept;
+  const uint32_t V = h->voxels;
   const int64_t rows = (int64_t)c.B * c.cap;
   const int C = c.C, M = c.M;
   int32_t* l_co = (int32_t*)sm;              // [kMeanTile][4]
   float* l_ft = (float*)(sm + kMeanTile * 4);  // [kMeanTile][C]
   int32_t* l_pi = (int32_t*)(sm + kMeanTile * (4 + C));  // [kMeanTile][M]
   for (uint32_t g0 = blockIdx.x * kMeanTile; g0 < V; g0 += gridDim.x * kMeanTile) {
-    const uint32_t g = g0 + tid;
+    const uint32_t v = g0 + tid;
     const uint32_t nblk = min((uint32_t)kMeanTile, V - g0);
-    // the tile's voxels lie in frames tile_frame[t] .. tile_frame[t + 1]
-    const uint32_t tl = g0 / kMeanTile;
-    const int32_t fa = min((int32_t)c.tile_frame[tl], c.B - 1);
-    const int32_t fb = min(max((int32_t)c.tile_frame[tl + 1], fa), c.B - 1);
+    // the block's voxels lie in tiles mtile[i] .. mtile[i + 1]
+    const uint32_t bi = g0 / kMeanTile;
+    const uint32_t ta = min(c.mtile[bi], nvt - 1u);
+    const uint32_t tb = min(max(c.mtile[bi + 1], ta), nvt - 1u);
     int64_t row = -1;
     int32_t b = 0;
     uint32_t s0 = 0, cnt = 0;
-    if (g < V) {
-      b = frame_of_voxel(c, g, fa, fb);
-      const uint32_t v = g - c.vox_off[b];
-      const uint32_t nv = c.vox_off[b + 1] - c.vox_off[b];
-      const uint32_t slot = c.fstart[b] + v;
-      const uint32_t rank = nv > (uint32_t)c.cap ? c.out_rank[slot] : v;
+    if (v < V) {
+      // the voxel's tile: the largest t in [ta, tb] with hpre[t] <= v
+      uint32_t t = ta, z = tb;
+      while (t < z) {
+        const uint32_t mid = (t + z + 1) >> 1;
+        if (c.hpre[mid] <= v) t = mid; else z = mid - 1;
+      }
+      const uint4 vt = c.vtile[t];
+      const uint32_t j = v - c.hpre[t], nh = c.hcount[t];
+      b = (int32_t)min(vt.z, (uint32_t)c.B - 1u);
+      const uint32_t fv0 = c.vox_off[b], fv1 = c.vox_off[b + 1];
+      const uint32_t slot = vt.x + j;
+      const uint32_t rank = fv1 - fv0 > (uint32_t)c.cap ? c.out_rank[min(slot, K - 1u)] : v - fv0;
       if (rank != 0xffffffffu) {
         row = c.out_voxel_offsets[b] + (int64_t)rank;
         if (row < 0 || row >= rows || slot >= K) {
           raise_fault(h, MMBEV_FAULT_INTERNAL);
           row = -1;
         } else {
-          s0 = min(c.seg_start[slot], K - 1u);
-          const uint32_t s1 = max(min(v + 1 < nv ? c.seg_start[slot + 1] : c.fstart[b + 1], K), s0 + 1u);
-          cnt = min(s1 - s0, (uint32_t)M);
+          s0 = min(c.hpos[slot], K - 1u);
+          if (j + 1 < nh) {
+            cnt = min(max(c.hpos[slot + 1], s0 + 1u) - s0, (uint32_t)M);
+          } else {
+            // the tile's last voxel may run on into the next tiles: its
+            // first max_points pairs decide the count (read eight at a
+            // time, their loads in flight together)
+            const uint32_t fend = min(c.fstart[b + 1], K);
+            const uint32_t k0 = keys[s0];
+            cnt = 1;
+            bool more = true;
+            for (uint32_t m0 = 1; m0 < (uint32_t)M && more; m0 += 8) {
+              uint32_t kk[8];
+#pragma unroll
+              for (int u = 0; u < 8; ++u) {
+                const uint32_t i = s0 + m0 + (uint32_t)u;
+                kk[u] = m0 + u < (uint32_t)M && i < fend ? keys[i] : ~k0;
+              }
+#pragma unroll
+              for (int u = 0; u < 8; ++u) {
+                more = more && kk[u] == k0;
+                cnt += more ? 1u : 0u;
+              }
+            }
+          }
         }
       }
     }
-    if (tid == 0) {
-      s_row0 = row;
-      s_contig = 1;
-    }
+    if (tid == 0) s_row0 = row;
     __syncthreads();
-    if ((uint32_t)tid < nblk && (row < 0 || row != s_row0 + tid)) s_contig = 0;  // every row valid and in order
-    // the voxel's coordinates and points
+    // every row of the block valid and consecutive
+    const bool contig = __syncthreads_and((uint32_t)tid >= nblk || (row >= 0 && row == s_row0 + tid)) != 0;
     int32_t co[4] = {0, 0, 0, 0};
     double sum[8];
 #pragma unroll
@@ -317,48 +404,49 @@ __global__ __launch_bounds__(kBlock) void mean_kernel(Config c, const uint32_t* 
       co[2] = (int32_t)(rest % c.Dy);
       co[3] = (int32_t)ix;
     }
-    __syncthreads();
-    const bool contig = s_contig != 0;
-    int32_t* pidx = contig ? l_pi + tid * M : c.out_point_idx + row * M;
     const int RW = c.rec_words;
     for (uint32_t m0 = 0; m0 < cnt; m0 += kMeanBatch) {
       uint32_t q[kMeanBatch];
       uint4 r0[kMeanBatch], r1[kMeanBatch];
 #pragma unroll
-      for (int j = 0; j < kMeanBatch; ++j) q[j] = m0 + j < cnt ? min(vals[s0 + m0 + j], K - 1u) : 0u;
+      for (int u = 0; u < kMeanBatch; ++u) q[u] = m0 + u < cnt ? min(vals[s0 + m0 + u], K - 1u) : 0u;
 #pragma unroll
-      for (int j = 0; j < kMeanBatch; ++j) {  // one or two 16-byte loads per record
-        const uint4* r = reinterpret_cast<const uint4*>(c.rec + (int64_t)q[j] * RW);
-        if (m0 + j < cnt) {
-          r0[j] = r[0];
-          r1[j] = RW > 4 ? r[1] : make_uint4(0, 0, 0, 0);
+      for (int u = 0; u < kMeanBatch; ++u) {  // one or two 16-byte loads per record
+        const uint4* r = reinterpret_cast<const uint4*>(c.rec + (int64_t)q[u] * RW);
+        if (m0 + u < cnt) {
+          r0[u] = r[0];
+          r1[u] = RW > 4 ? r[1] : make_uint4(0, 0, 0, 0);
         } else {
-          r0[j] = r1[j] = make_uint4(0, 0, 0, 0);
+          r0[u] = r1[u] = make_uint4(0, 0, 0, 0);
         }
       }
 #pragma unroll
-      for (int j = 0; j < kMeanBatch; ++j)
-        if (m0 + j < cnt) {
-          const uint32_t w[8] = {r0[j].y, r0[j].z, r0[j].w, r1[j].x, r1[j].y, r1[j].z, r1[j].w, 0u};
+      for (int u = 0; u < kMeanBatch; ++u)
+        if (m0 + u < cnt) {
+          const uint32_t w[8] = {r0[u].y, r0[u].z, r0[u].w, r1[u].x, r1[u].y, r1[u].z, r1[u].w, 0u};
 #pragma unroll
           for (int f = 0; f < 7; ++f) sum[f] += (double)__uint_as_float(w[f]);  // ascending point order
-          pidx[m0 + j] = (int32_t)r0[j].x;
+          if (contig)  // uniform: LDS staging or the row itself
+            l_pi[tid * M + m0 + u] = (int32_t)r0[u].x;
+          else
+            c.out_point_idx[row * M + m0 + u] = (int32_t)r0[u].x;
         }
       if (C == 8)  // the eighth feature sits in a third 16-byte word
 #pragma unroll
-        for (int j = 0; j < kMeanBatch; ++j)
-          if (m0 + j < cnt) sum[7] += (double)__uint_as_float(c.rec[(int64_t)q[j] * RW + 8]);
+        for (int u = 0; u < kMeanBatch; ++u)
+          if (m0 + u < cnt) sum[7] += (double)__uint_as_float(c.rec[(int64_t)q[u] * RW + 8]);
     }
     if (row >= 0) {
-      for (int m = (int)cnt; m < M; ++m) pidx[m] = -1;
       c.out_counts[row] = (int32_t)cnt;
       if (contig) {
+        for (int m = (int)cnt; m < M; ++m) l_pi[tid * M + m] = -1;
 #pragma unroll
         for (int q = 0; q < 4; ++q) l_co[tid * 4 + q] = co[q];
 #pragma unroll
         for (int f = 0; f < 8; ++f)
           if (f < C) l_ft[tid * C + f] = (float)(sum[f] / (double)cnt);
       } else {
+        for (int m = (int)cnt; m < M; ++m) c.out_point_idx[row * M + m] = -1;
         int32_t* o = c.out_coords + row * 4;
 #pragma unroll
         for (int q = 0; q < 4; ++q) o[q] = co[q];
@@ -387,21 +475,13 @@ __global__ __launch_bounds__(kBlock) void mean_kernel(Config c, const uint32_t* 
 
 }  // namespace
 
-hipError_t launch_unique(const Config& c, const uint32_t* keys, hipStream_t st) {
-  hipLaunchKernelGGL(ucount_kernel, dim3(c.schunk_max), dim3(kBlock), 0, st, c, keys);
-  const hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(uwrite_kernel, dim3(c.schunk_max), dim3(kBlock), 0, st, c, keys);
+hipError_t launch_heads(const Config& c, const uint32_t* keys, const uint32_t* vals, hipStream_t st) {
+  hipLaunchKernelGGL(heads_kernel, dim3(std::min(c.vtile_max, 4096)), dim3(kBlock), 0, st, c, keys, vals);
   return hipGetLastError();
 }
 
-hipError_t launch_finalize(const Config& c, hipStream_t st) {
-  hipLaunchKernelGGL(finalize_kernel, dim3(1), dim3(kBlock), 0, st, c);
-  return hipGetLastError();
-}
-
-hipError_t launch_cap(const Config& c, const uint32_t* vals, hipStream_t st) {
-  hipLaunchKernelGGL(cap_kernel, dim3(c.B), dim3(kBlock), 0, st, c, vals);
+hipError_t launch_fincap(const Config& c, hipStream_t st) {
+  hipLaunchKernelGGL(fincap_kernel, dim3(1 + c.B), dim3(kFinBlock), 0, st, c);
   return hipGetLastError();
 }
 

@@ -7,17 +7,22 @@ resident in HBM.  Prints ONE JSON line.
 
     python bench.py [--gpus 1] [--steps K] [--warmup W] [--frames F] [--no-cpu-baseline]
 
-Traffic of the filter kernel (the `traffic` field of the roofline object):
+HBM traffic of every kernel of the call (the filter's is the `traffic` field
+of the roofline object), and LDS bank conflicts:
 
-    rocprofv3 --pmc FETCH_SIZE -f csv -d DIR_F -o run -- python3 bench.py --probe-traffic
-    rocprofv3 --pmc WRITE_SIZE -f csv -d DIR_W -o run -- python3 bench.py --probe-traffic
+    rocprofv3 --pmc FETCH_SIZE -f csv -d DIR_F -o run -- python3 bench.py --probe-traffic DIR_F/meta.json
+    rocprofv3 --pmc WRITE_SIZE -f csv -d DIR_W -o run -- python3 bench.py --probe-traffic DIR_W/meta.json
     python bench.py --write-traffic DIR_F DIR_W
+    rocprofv3 --pmc SQ_LDS_BANK_CONFLICT SQ_LDS_IDX_ACTIVE ... -f csv -d DIR_L -o run -- python3 bench.py --probe-traffic DIR_L/meta.json
+    python bench.py --write-lds DIR_L
 
 --probe-traffic runs the batched call a few times and a plain device copy of
-COPY_BYTES bytes; --write-traffic scales each counter by the known bytes the
-copy moved over what the counter read for it, and stores the filter kernel's
-HBM bytes per launch, tagged with the hash of the filter's sources (a changed
-kernel makes the stored figure stale, and bench.py then reports null).
+COPY_BYTES bytes, and stores the call's sizes (N, K, V, chunk counts) next to
+the counters; --write-traffic scales each counter by the known bytes the copy
+moved over what the counter read for it, and stores every kernel's HBM bytes
+per launch with its ratio to the bytes its job needs, tagged with the hash of
+the library's sources (a changed kernel makes the stored figures stale, and
+bench.py then reports null).
 
 value = input points per second over the timed steps (Mpoints/s).  The
 roofline object reports the dominant kernel (the fused point filter): its
@@ -40,13 +45,19 @@ sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0
 METRIC = "Mpoints/s ROI-voxelized (10-sweep, 347k pts) + achieved HBM GB/s vs peak"
-FILTER_SOURCES = ["paper_2608_15437_amd/csrc/filter.hip", "paper_2608_15437_amd/csrc/common.hpp"]
-TRAFFIC_FILE = os.path.join(ROOT, "profiles", "filter_kernel_c2x128_traffic.json")
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "roi_voxelize_c2x128_traffic.json")
+LDS_FILE = os.path.join(ROOT, "profiles", "roi_voxelize_c2x128_lds.json")
+CSRC = os.path.join("paper_2608_15437_amd", "csrc")
 COPY_BYTES = 1 << 30
 
 
 def log(msg: str) -> None:
     print(msg, file=sys.stderr, flush=True)
+
+
+def library_sources() -> list:
+    d = os.path.join(ROOT, CSRC)
+    return [os.path.join(CSRC, f) for f in sorted(os.listdir(d)) if f.endswith((".hip", ".hpp"))]
 
 
 def source_sha(paths) -> str:
@@ -242,8 +253,9 @@ def time_config(name: str, wl, dev, steps: int, warmup: int, with_oracle: bool) 
     return row
 
 
-def probe_traffic(frames: int) -> int:
-    """The launches whose counters --write-traffic reads: batched calls, then one plain copy."""
+def probe_traffic(frames: int, meta_path: str) -> int:
+    """The launches whose counters --write-traffic / --write-lds read: batched
+    calls, then one plain copy; the call's sizes go to meta_path."""
     import torch
 
     import synth
@@ -254,11 +266,23 @@ def probe_traffic(frames: int) -> int:
     for _ in range(3):
         vz.run()
     torch.cuda.synchronize()
+    h = vz.header()
+    res = vz.result()
     src = torch.ones(COPY_BYTES // 4, dtype=torch.float32, device="cuda:0")
     dst = torch.empty_like(src)
     dst.copy_(src)
     torch.cuda.synchronize()
-    log(f"[probe] 3 calls on {frames} frames, one copy of {COPY_BYTES} bytes")
+    g = wl.grid
+    meta = {"frames": frames, "N": wl.num_points, "K": h["kept"], "V": int(res["voxel_offsets"][-1]),
+            "K_in_voxels": int(res["counts"].sum()), "C": wl.num_features, "M": g.max_points,
+            "R": len(wl.roi_desc), "B": wl.num_frames, "S": g.num_sweeps, "filter_chunks": h["filter_chunks"],
+            "pair_chunks": h["pair_chunks"], "voxel_tiles": h["voxel_tiles"],
+            "passes": len([n for n in launch_names(vz) if n.startswith("sort")]), "calls": 3,
+            "source_sha": source_sha(library_sources())}
+    os.makedirs(os.path.dirname(os.path.abspath(meta_path)), exist_ok=True)
+    with open(meta_path, "w") as f:
+        json.dump(meta, f)
+    log(f"[probe] 3 calls on {frames} frames, one copy of {COPY_BYTES} bytes; sizes in {meta_path}")
     return 0
 
 
@@ -347,48 +371,129 @@ def time_clusters(vz, steps: int, warmup: int, ouster: bool = False) -> dict:
             "us_per_frame": round(us / g.num_frames, 2), "fault": p.fault()}
 
 
-def counter_values(run_dir: str, counter: str) -> dict:
-    """Per-dispatch values (KiB) of one counter, per kernel name, from a rocprofv3 csv run."""
+def kernel_short_name(name: str) -> str:
+    import re
+
+    m = re.search(r"(\w+_kernel)", name)
+    if m:
+        return m.group(1)
+    return "copyBuffer" if "copyBuffer" in name else name.split("(")[0][-40:]
+
+
+def counter_values(run_dir: str, counters) -> dict:
+    """Per-dispatch counter values, summed over the counter's instances, per
+    short kernel name in dispatch order: {kernel: [{counter: value}, ...]}."""
     import csv
     import glob
 
     per = {}
     for f in glob.glob(os.path.join(run_dir, "**", "*counter_collection.csv"), recursive=True):
         for r in csv.DictReader(open(f)):
-            if r["Counter_Name"] == counter:
-                key = (r["Kernel_Name"], r["Dispatch_Id"])
-                per[key] = per.get(key, 0.0) + float(r["Counter_Value"])
-    vals = {}
-    for (name, _), v in per.items():
-        vals.setdefault(name, []).append(v)
-    return vals
+            if r["Counter_Name"] in counters:
+                key = (kernel_short_name(r["Kernel_Name"]), int(r["Dispatch_Id"]))
+                d = per.setdefault(key, {})
+                d[r["Counter_Name"]] = d.get(r["Counter_Name"], 0.0) + float(r["Counter_Value"])
+    out = {}
+    for (name, _), d in sorted(per.items(), key=lambda kv: kv[0][1]):
+        out.setdefault(name, []).append(d)
+    return out
 
 
-def write_traffic(fetch_dir: str, write_dir: str, frames: int) -> int:
-    fe, wr = counter_values(fetch_dir, "FETCH_SIZE"), counter_values(write_dir, "WRITE_SIZE")
+def split_passes(vals: dict, passes: int) -> dict:
+    """count_kernel / scatter_kernel dispatches split by radix pass (every call
+    launches one of each per pass, in pass order)."""
+    out = {}
+    for name, rows in vals.items():
+        if name in ("count_kernel", "scatter_kernel") and passes > 1:
+            for p in range(passes):
+                out[f"{name}[pass {p}]"] = rows[p::passes]
+        else:
+            out[name] = rows
+    return out
 
-    def pick(d, needle):
-        names = [k for k in d if needle in k]
-        if not names:
-            raise SystemExit(f"no kernel matching {needle!r} in the counter files")
-        return d[names[0]]
 
+def kernel_job_bytes(name: str, m: dict):
+    """HBM bytes a kernel's job needs in this design (its inputs read once, its
+    outputs written once); None for the latency-bound bookkeeping kernels."""
+    N, K, V, C, M = m["N"], m["K"], m["V"], m["C"], m["M"]
+    RW = 4 if C <= 3 else (8 if C <= 7 else 12)  # record words: index, x', y', z', raw features 3..
+    if name.startswith("filter_kernel"):
+        return 13 * N + 33 * m["R"] + 48 * m["B"] * m["S"]  # x, y, z, sweep id; ROI records; poses
+    if name == "compact_kernel":
+        # kept bitmaps and counts; the kept points' columns and sweep ids; keys and records
+        return N // 8 + 4 * m["filter_chunks"] + (4 * C + 1) * K + 4 * K + 4 * RW * K
+    if name.startswith("count_kernel"):
+        return 4 * K + 4 * 512 * m["pair_chunks"]  # keys; one count row per chunk
+    if name.startswith("scatter_kernel"):
+        return (12 if name.endswith("[pass 0]") else 16) * K  # pairs read (pass 0: keys only) and written
+    if name == "heads_kernel":
+        return 4 * K + 12 * V  # keys; each head's pair, place and count
+    if name == "mean_kernel":
+        # heads' pairs and places, the values and records of the kept points, the rows
+        return 8 * V + (4 + 4 * RW) * m["K_in_voxels"] + V * (16 + 4 + 4 * C + 4 * M)
+    return None
+
+
+def write_traffic(fetch_dir: str, write_dir: str) -> int:
+    fe, wr = counter_values(fetch_dir, ["FETCH_SIZE"]), counter_values(write_dir, ["WRITE_SIZE"])
+    with open(os.path.join(fetch_dir, "meta.json")) as f:
+        meta = json.load(f)
     # the copy of COPY_BYTES is the largest copy dispatch (the others upload inputs)
-    copy_f, copy_w = max(pick(fe, "copyBuffer")), max(pick(wr, "copyBuffer"))
-    filt_f = statistics.mean(pick(fe, "filter_kernel"))
-    filt_w = statistics.mean(pick(wr, "filter_kernel"))
+    copy_f = max(r["FETCH_SIZE"] for r in fe["copyBuffer"])
+    copy_w = max(r["WRITE_SIZE"] for r in wr["copyBuffer"])
     fetch_scale = COPY_BYTES / (copy_f * 1024.0)
     write_scale = COPY_BYTES / (copy_w * 1024.0)
-    fetch_bytes = filt_f * 1024.0 * fetch_scale
-    write_bytes = filt_w * 1024.0 * write_scale
-    out = {"kernel": "filter_kernel", "frames": frames, "source_sha": source_sha(FILTER_SOURCES),
-           "fetch_kib_per_launch": filt_f, "write_kib_per_launch": filt_w,
+    fe, wr = split_passes(fe, meta["passes"]), split_passes(wr, meta["passes"])
+    kernels = {}
+    for name in fe:
+        if name == "copyBuffer" or name not in wr:
+            continue
+        calls = meta["calls"]
+        f_rows, w_rows = fe[name][-calls:], wr[name][-calls:]  # the bench call's dispatches (last ones)
+        fk = statistics.mean(r["FETCH_SIZE"] for r in f_rows)
+        wk = statistics.mean(r["WRITE_SIZE"] for r in w_rows)
+        fb, wb = fk * 1024.0 * fetch_scale, wk * 1024.0 * write_scale
+        job = kernel_job_bytes(name, meta)
+        kernels[name] = {"fetch_kib_per_launch": round(fk, 1), "write_kib_per_launch": round(wk, 1),
+                         "fetch_bytes_per_launch": int(fb), "write_bytes_per_launch": int(wb),
+                         "bytes_per_launch": int(fb + wb), "job_bytes": job,
+                         "ratio_to_job": round((fb + wb) / job, 3) if job else None}
+    filt = [k for k in kernels if k.startswith("filter_kernel")]
+    out = {"workload": f"{meta['frames']} nuScenes-shaped frames per call", "sizes": meta,
+           "source_sha": source_sha(library_sources()), "probe_source_sha": meta["source_sha"],
            "copy_bytes": COPY_BYTES, "copy_fetch_kib": copy_f, "copy_write_kib": copy_w,
            "fetch_scale": fetch_scale, "write_scale": write_scale,
-           "bytes_per_launch": int(fetch_bytes + write_bytes),
-           "fetch_bytes_per_launch": int(fetch_bytes), "write_bytes_per_launch": int(write_bytes)}
+           "filter_bytes_per_launch": kernels[filt[0]]["bytes_per_launch"] if filt else None,
+           "kernels": kernels}
     os.makedirs(os.path.dirname(TRAFFIC_FILE), exist_ok=True)
     with open(TRAFFIC_FILE, "w") as f:
+        json.dump(out, f, indent=1)
+    print(json.dumps(out))
+    return 0
+
+
+def write_lds(lds_dir: str) -> int:
+    """LDS counters per kernel (mean per dispatch of the bench call) and the
+    ratio of bank-conflict cycles to indexed-LDS active cycles."""
+    with open(os.path.join(lds_dir, "meta.json")) as f:
+        meta = json.load(f)
+    names = ["SQ_LDS_BANK_CONFLICT", "SQ_LDS_IDX_ACTIVE", "SQ_LDS_ADDR_CONFLICT", "SQ_LDS_UNALIGNED_STALL",
+             "SQ_INSTS_LDS", "SQ_ACTIVE_INST_LDS", "SQ_WAIT_INST_LDS", "SQ_INSTS_VALU"]
+    vals = split_passes(counter_values(lds_dir, names), meta["passes"])
+    kernels = {}
+    for name, rows in vals.items():
+        if name == "copyBuffer":
+            continue
+        rows = rows[-meta["calls"]:]
+        mean = {c: statistics.mean(r.get(c, 0.0) for r in rows) for c in rows[0]}
+        ent = {c: round(v, 1) for c, v in sorted(mean.items())}
+        if mean.get("SQ_LDS_IDX_ACTIVE"):
+            ent["bank_conflict_per_idx_active"] = round(mean.get("SQ_LDS_BANK_CONFLICT", 0.0)
+                                                        / mean["SQ_LDS_IDX_ACTIVE"], 4)
+        kernels[name] = ent
+    out = {"workload": f"{meta['frames']} nuScenes-shaped frames per call", "sizes": meta,
+           "source_sha": source_sha(library_sources()), "probe_source_sha": meta["source_sha"], "kernels": kernels}
+    with open(LDS_FILE, "w") as f:
         json.dump(out, f, indent=1)
     print(json.dumps(out))
     return 0
@@ -404,17 +509,20 @@ def main() -> int:
     ap.add_argument("--no-two-streams", action="store_true",
                     help="skip the two-calls-in-flight measurement (kernel traces then time each kernel alone)")
     ap.add_argument("--no-configs", action="store_true", help="skip the per-configuration rows (c1..c5)")
-    ap.add_argument("--probe-traffic", action="store_true")
+    ap.add_argument("--probe-traffic", metavar="META_JSON")
     ap.add_argument("--write-traffic", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"))
+    ap.add_argument("--write-lds", metavar="LDS_DIR")
     args = ap.parse_args()
     if args.write_traffic:
-        return write_traffic(args.write_traffic[0], args.write_traffic[1], args.frames)
+        return write_traffic(args.write_traffic[0], args.write_traffic[1])
+    if args.write_lds:
+        return write_lds(args.write_lds)
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}); frames are independent, so "
               "a multi-GPU run would shard the batch by frame with no exchange", file=sys.stderr)
         return 2
     if args.probe_traffic:
-        return probe_traffic(args.frames)
+        return probe_traffic(args.frames, args.probe_traffic)
 
     import numpy as np
     import torch
@@ -456,8 +564,8 @@ def main() -> int:
     if os.path.exists(TRAFFIC_FILE):
         with open(TRAFFIC_FILE) as f:
             tr = json.load(f)
-        if tr.get("source_sha") == source_sha(FILTER_SOURCES) and tr.get("frames") == F:
-            traffic = tr.get("bytes_per_launch")
+        if tr.get("source_sha") == source_sha(library_sources()) and tr.get("sizes", {}).get("frames") == F:
+            traffic = tr.get("filter_bytes_per_launch")
 
     two = None
     if not args.no_two_streams:

@@ -147,6 +147,22 @@ __device__ __forceinline__ uint64_t lanemask_lt() {
   return l == 0 ? 0ull : (~0ull >> (64 - l));
 }
 
+// Set lanes of m below this lane (mbcnt: the popcount of m & lanemask_lt()).
+__device__ __forceinline__ uint32_t count_below(uint64_t m) {
+  return __builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0u));
+}
+
+// Work unit of workgroup b when n units are dealt to the eight XCDs in
+// contiguous blocks: workgroups go to XCD b % 8 in turn, so XCD x takes
+// units [x * per, (x + 1) * per) in order and neighbouring units share an
+// L2 (their partial-line writes merge there; their common reads hit there).
+// Returns n or more for a workgroup with no unit; the grid must hold at
+// least 8 * ceil(n / 8) workgroups.
+__device__ __forceinline__ uint32_t xcd_block_unit(uint32_t b, uint32_t n) {
+  const uint32_t per = (n + 7u) / 8u;
+  return b / 8u < per ? (b % 8u) * per + b / 8u : n;
+}
+
 __device__ __forceinline__ void raise_fault(WsHeader* h, int32_t bits) {
   __hip_atomic_fetch_or(&h->fault, bits, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }

@@ -23,7 +23,8 @@
 // Then per pass:
 // count    -- workgroup k counts the digits of pair chunk k (row k of the
 //             [chunk][digit] count matrix);
-// scatter  -- workgroup k sums the count rows of its frame's chunks (the
+// scatter  -- the workgroup of chunk k (chunks dealt to the XCDs in
+//             contiguous blocks) sums the count rows of its frame's chunks (the
 //             frame's digit totals, and its digits in the earlier chunks:
 //             where each of its digits starts), then walks its chunk tile by
 //             tile (the next tile's
@@ -36,18 +37,22 @@ namespace mmbev {
 
 namespace {
 
-// Lanes of this wave holding the same digit (valid lanes only): one ballot
-// per bit of the widest digit, unrolled so that the ballots do not wait for
-// each other (narrower digits have zero high bits).
+// Lanes of this wave holding the same digit (valid lanes only).  A lane
+// differs from this one where some bit's ballot differs from this lane's
+// bit: per bit one ballot and (ballot XOR this lane's bit, sign-extended)
+// ORed into the difference mask.  Unrolled over the widest digit so that the
+// ballots do not wait for each other (narrower digits have zero high bits).
 __device__ __forceinline__ uint64_t match_digit(uint32_t dig, bool valid) {
-  uint64_t m = __ballot(valid);
+  uint32_t dlo = 0, dhi = 0;
 #pragma unroll
   for (int bit = 0; bit < kMaxDigitBits; ++bit) {
-    const bool on = (dig >> bit) & 1u;
-    const uint64_t bb = __ballot(on);
-    m &= on ? bb : ~bb;
+    const int32_t sb = __builtin_amdgcn_sbfe((int32_t)dig, bit, 1);  // -1 where the bit is set, else 0
+    const uint32_t s = (uint32_t)sb;
+    const uint64_t b = __builtin_amdgcn_ballot_w64(sb < 0);
+    dlo |= (uint32_t)b ^ s;
+    dhi |= (uint32_t)(b >> 32) ^ s;
   }
-  return m;
+  return __ballot(valid) & ~(((uint64_t)dhi << 32) | dlo);
 }
 
 // Exclusive scan of n <= kSortBins values in LDS (in may alias out); all
@@ -171,6 +176,7 @@ __global__ __launch_bounds__(kSegBlock) void segments_kernel(Config c) {
   uint32_t total;
   uint32_t run = block_exclusive_scan<kSegWaves>(mine, s_tmp, total);
   const uint32_t cap = (uint32_t)c.schunk_max;  // never reached: the bound holds for any K <= N
+  if (tid == 0) c.schunk_first[c.B] = min(total, cap);
   for (int j = 0; j < per; ++j) {
     const int b = b0 + j;
     if (b < c.B) {
@@ -211,7 +217,6 @@ __global__ __launch_bounds__(kSegBlock) void segments_kernel(Config c) {
     }
   }
   if (tid == 0) {
-    c.schunk_first[c.B] = min(total, cap);
     h->schunks = min(total, cap);
     c.vt_first[c.B] = min(total_vt, cap_vt);
     h->vtiles = min(total_vt, cap_vt);
@@ -371,15 +376,15 @@ __global__ __launch_bounds__(kBlock) void scatter_kernel(Config c, int pass, con
   const int tid = threadIdx.x;
   const int lane = tid & 63, wave = tid >> 6;
   WsHeader* h = c.hdr;
-  const uint32_t k = blockIdx.x;
-  // the chunk's entry and its frame's chunks load with the counts (in bounds
-  // for any k < schunk_max)
+  // chunks dealt to the XCDs in contiguous blocks: a frame's chunks share
+  // one L2, where their neighbouring digit runs merge into whole lines and
+  // their count rows are read once
   const uint32_t nsc = h->schunks, K = h->kept;
+  const uint32_t k = xcd_block_unit(blockIdx.x, nsc);
+  if (k >= nsc) return;
   const uint4 ch = c.schunk[k];
   const uint2 fc = c.schunk_frame[k];
   static_assert(kSortBins == 2 * kBlock, "two digits per thread");
-  asm volatile("" ::"s"(ch.x), "s"(ch.y), "s"(ch.z), "s"(ch.w), "s"(fc.x), "s"(fc.y));  // keeps the loads above the check
-  if (k >= nsc) return;
   const int shift = pass * c.dbits;
   const uint32_t nbins = 1u << c.dbits;
   const uint32_t mask = nbins - 1u;
@@ -418,7 +423,6 @@ __global__ __launch_bounds__(kBlock) void scatter_kernel(Config c, int pass, con
     if ((uint32_t)tid < nbins) L.run[tid] += ch.w + pre0;
     if ((uint32_t)(kBlock + tid) < nbins) L.run[kBlock + tid] += ch.w + pre1;
   }
-  const uint64_t lt = lanemask_lt();
   for (uint32_t base = lo; base < hi; base += kSortTile) {
     const bool more = base + kSortTile < hi;
     if (more) load_sort_tile(kin, vin, base + kSortTile, hi, nkey, nval);
@@ -439,8 +443,8 @@ __global__ __launch_bounds__(kBlock) void scatter_kernel(Config c, int pass, con
       if (valid[r]) prior = L.wave_cnt[wave][dig[r]];
       __builtin_amdgcn_wave_barrier();
       if (valid[r]) {
-        rank[r] = prior + __popcll(m & lt);
-        if ((m & lt) == 0) L.wave_cnt[wave][dig[r]] = prior + __popcll(m);
+        rank[r] = prior + count_below(m);
+        if (count_below(m) == 0) L.wave_cnt[wave][dig[r]] = prior + __popcll(m);
       }
       __builtin_amdgcn_wave_barrier();
     }
@@ -510,7 +514,8 @@ hipError_t launch_radix_pass(const Config& c, int pass, const uint32_t* kin, con
   hipLaunchKernelGGL(count_kernel, dim3(c.schunk_max), dim3(kBlock), 0, st, c, pass, kin);
   const hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(scatter_kernel, dim3(c.schunk_max), dim3(kBlock), 0, st, c, pass, kin, vin, kout, vout);
+  const uint32_t grid = (c.schunk_max + 7u) / 8u * 8u;  // whole rounds of the eight XCDs
+  hipLaunchKernelGGL(scatter_kernel, dim3(grid), dim3(kBlock), 0, st, c, pass, kin, vin, kout, vout);
   return hipGetLastError();
 }
 

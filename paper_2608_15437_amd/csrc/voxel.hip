@@ -316,7 +316,7 @@ __global__ __launch_bounds__(kFinBlock) void fincap_kernel(Config c) {
 // loads in flight together.  When the block's rows are consecutive (no frame
 // over the cap in it) they are assembled in LDS and written as contiguous
 // runs; otherwise each thread writes its own row.
-constexpr int kMeanBatch = 4;  // more records in flight per thread cost occupancy (VGPRs)
+constexpr int kMeanBatch = 2;  // records in flight per thread: more cost occupancy (VGPRs), fewer add round trips
 
 __global__ __launch_bounds__(kBlock) void mean_kernel(Config c, const uint32_t* keys, const uint32_t* vals) {
   extern __shared__ uint32_t sm[];

@@ -38,6 +38,9 @@ constexpr int kScanItems = 16;        // items per thread in the single-workgrou
 constexpr int kScanTile = kBlock * kScanItems;  // 4096
 constexpr int kMeanTile = kBlock;     // one voxel per thread
 constexpr int kVoxTile = 2048;        // sorted pairs of a voxel tile (the heads, cap and mean kernels' unit)
+constexpr int kCus = 256;            // compute units of the device (8 XCDs x 32)
+constexpr int kScatterPerCu = 5;     // scatter workgroups resident per CU (its LDS and VGPRs allow five)
+constexpr int kCountGrid = 2048;     // count workgroups (eight per CU)
 
 // Workspace header: per-call counters, rewritten by the first kernels of a call.
 struct alignas(256) WsHeader {

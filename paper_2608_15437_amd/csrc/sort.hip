@@ -316,46 +316,46 @@ __global__ __launch_bounds__(kBlock) void compact_kernel(Config c, uint32_t* kou
 __global__ __launch_bounds__(kBlock) void count_kernel(Config c, int pass, const uint32_t* kin) {
   __shared__ uint32_t s_hist[kWaves][kSortBins];  // one histogram per wave, summed at the end
   const int tid = threadIdx.x, wave = tid >> 6;
-  const uint32_t k = blockIdx.x;
-  // the chunk's entry loads with the chunk count (in bounds for any k < schunk_max)
+  // the first chunk's entry loads with the chunk count (in bounds: the grid is at most schunk_max)
   const uint32_t nsc = c.hdr->schunks;
-  const uint4 ch = c.schunk[k];
+  uint4 ch = c.schunk[blockIdx.x];
   asm volatile("" ::"s"(ch.x), "s"(ch.y));  // keeps the load above the check
-  if (k >= nsc) return;
   const int shift = pass * c.dbits;
   const uint32_t nbins = 1u << c.dbits;
   const uint32_t mask = nbins - 1u;
-  for (uint32_t e = tid; e < kWaves * kSortBins; e += kBlock) (&s_hist[0][0])[e] = 0;
-  __syncthreads();
-  const uint32_t lo = ch.x, hi = ch.y;
-  for (uint32_t base = lo; base < hi; base += kBlock * kCountItems) {
-    uint32_t key[kCountItems];
+  for (uint32_t k = blockIdx.x; k < nsc; k += gridDim.x) {  // a grid of resident size walks the chunks
+    if (k != blockIdx.x) ch = c.schunk[k];
+    for (uint32_t e = tid; e < kWaves * kSortBins; e += kBlock) (&s_hist[0][0])[e] = 0;
+    __syncthreads();
+    const uint32_t lo = ch.x, hi = ch.y;
+    for (uint32_t base = lo; base < hi; base += kBlock * kCountItems) {
+      uint32_t key[kCountItems];
 #pragma unroll
-    for (int j = 0; j < kCountItems; ++j) {  // all loads of the batch in flight together
-      const uint32_t i = base + j * kBlock + tid;
-      key[j] = i < hi ? kin[i] : 0u;
+      for (int j = 0; j < kCountItems; ++j) {  // all loads of the batch in flight together
+        const uint32_t i = base + j * kBlock + tid;
+        key[j] = i < hi ? kin[i] : 0u;
+      }
+#pragma unroll
+      for (int j = 0; j < kCountItems; ++j)
+        if (base + j * kBlock + tid < hi) atomicAdd(&s_hist[wave][(key[j] >> shift) & mask], 1u);
     }
+    __syncthreads();
+    for (uint32_t e = tid; e < nbins; e += kBlock) {
+      uint32_t t = 0;
 #pragma unroll
-    for (int j = 0; j < kCountItems; ++j)
-      if (base + j * kBlock + tid < hi) atomicAdd(&s_hist[wave][(key[j] >> shift) & mask], 1u);
-  }
-  __syncthreads();
-  for (uint32_t e = tid; e < nbins; e += kBlock) {
-    uint32_t t = 0;
-#pragma unroll
-    for (int w = 0; w < kWaves; ++w) t += s_hist[w][e];
-    c.cnt[(int64_t)k * kSortBins + e] = t;
+      for (int w = 0; w < kWaves; ++w) t += s_hist[w][e];
+      c.cnt[(int64_t)k * kSortBins + e] = t;
+    }
+    __syncthreads();  // the next chunk clears the histograms
   }
 }
 
 struct ScatterLds {
-  uint32_t run[kSortBins];  // next output position of every digit
-  uint32_t wave_cnt[kWaves][kSortBins];
-  uint32_t tile_cnt[kSortBins];
-  uint32_t local_off[kSortBins];
-  uint32_t keys[kSortTile];
+  uint32_t run[kSortBins];             // next output position of every digit
+  uint32_t local_off[kSortBins + 1];   // the tile's digits: exclusive prefix, then the tile's size
+  uint32_t keys[kSortTile];            // the tile reordered by digit
   uint32_t vals[kSortTile];
-  uint16_t digit[kSortTile];
+  uint32_t wave_cnt[kWaves][kSortBins];  // a wave's digit counts, then its offsets
   uint32_t scan_tmp[kWaves];
 };
 
@@ -373,123 +373,138 @@ __device__ __forceinline__ void load_sort_tile(const uint32_t* kin, const uint32
 __global__ __launch_bounds__(kBlock) void scatter_kernel(Config c, int pass, const uint32_t* kin, const uint32_t* vin,
                                                          uint32_t* kout, uint32_t* vout) {
   __shared__ ScatterLds L;
+  static_assert(sizeof(ScatterLds) <= 160 * 1024 / kScatterPerCu, "workgroups per CU");
+  static_assert(kSortBins == 2 * kBlock, "two digits per thread");
   const int tid = threadIdx.x;
   const int lane = tid & 63, wave = tid >> 6;
   WsHeader* h = c.hdr;
-  // chunks dealt to the XCDs in contiguous blocks: a frame's chunks share
-  // one L2, where their neighbouring digit runs merge into whole lines and
-  // their count rows are read once
   const uint32_t nsc = h->schunks, K = h->kept;
-  const uint32_t k = xcd_block_unit(blockIdx.x, nsc);
-  if (k >= nsc) return;
-  const uint4 ch = c.schunk[k];
-  const uint2 fc = c.schunk_frame[k];
-  static_assert(kSortBins == 2 * kBlock, "two digits per thread");
   const int shift = pass * c.dbits;
   const uint32_t nbins = 1u << c.dbits;
   const uint32_t mask = nbins - 1u;
-  const uint32_t lo = ch.x, hi = ch.y;
-  uint32_t key[kSortItems], val[kSortItems], nkey[kSortItems], nval[kSortItems];
-  if (lo < hi) load_sort_tile(kin, vin, lo, hi, key, val);
-  // base of every digit: frame start + the frame's smaller digits + this
-  // digit in the frame's earlier chunks, from the count rows of the frame's
-  // chunks (at most kMaxFrameChunks rows; thread t: digits t and t + kBlock)
-  {
-    constexpr int kRows = 8;
-    const uint32_t k0 = fc.x, k1 = max(fc.y, k0);
-    uint32_t pre0 = 0, pre1 = 0, tot0 = 0, tot1 = 0;
-    for (uint32_t kk = k0; kk < k1; kk += kRows) {
-      uint32_t x0[kRows], x1[kRows];
+  // chunks dealt to the XCDs in contiguous blocks: a frame's chunks share
+  // one L2, where their neighbouring digit runs merge into whole lines and
+  // their count rows are read once; a grid of resident size walks them
+  for (uint32_t wb = blockIdx.x;; wb += gridDim.x) {
+    const uint32_t k = xcd_block_unit(wb, nsc);
+    if (k >= nsc) break;  // uniform
+    const uint4 ch = c.schunk[k];
+    const uint2 fc = c.schunk_frame[k];
+    const uint32_t lo = ch.x, hi = ch.y;
+    uint32_t key[kSortItems], val[kSortItems], nkey[kSortItems], nval[kSortItems];
+    if (lo < hi) load_sort_tile(kin, vin, lo, hi, key, val);
+    // base of every digit: frame start + the frame's smaller digits + this
+    // digit in the frame's earlier chunks, from the count rows of the frame's
+    // chunks (at most kMaxFrameChunks rows; thread t: digits t and t + kBlock)
+    {
+      constexpr int kRows = 8;
+      const uint32_t k0 = fc.x, k1 = max(fc.y, k0);
+      uint32_t pre0 = 0, pre1 = 0, tot0 = 0, tot1 = 0;
+      for (uint32_t kk = k0; kk < k1; kk += kRows) {
+        uint32_t x0[kRows], x1[kRows];
 #pragma unroll
-      for (int u = 0; u < kRows; ++u) {  // the rows' loads in flight together
-        const bool ok = kk + u < k1;
-        x0[u] = ok ? c.cnt[(int64_t)(kk + u) * kSortBins + tid] : 0u;
-        x1[u] = ok ? c.cnt[(int64_t)(kk + u) * kSortBins + kBlock + tid] : 0u;
-      }
-#pragma unroll
-      for (int u = 0; u < kRows; ++u) {
-        if (kk + u < k) {
-          pre0 += x0[u];
-          pre1 += x1[u];
+        for (int u = 0; u < kRows; ++u) {  // the rows' loads in flight together
+          const bool ok = kk + u < k1;
+          x0[u] = ok ? c.cnt[(int64_t)(kk + u) * kSortBins + tid] : 0u;
+          x1[u] = ok ? c.cnt[(int64_t)(kk + u) * kSortBins + kBlock + tid] : 0u;
         }
-        tot0 += x0[u];
-        tot1 += x1[u];
-      }
-    }
-    L.run[tid] = tot0;
-    L.run[kBlock + tid] = tot1;
-    __syncthreads();
-    scan_bins(L.run, L.run, (int)nbins, L.scan_tmp);
-    if ((uint32_t)tid < nbins) L.run[tid] += ch.w + pre0;
-    if ((uint32_t)(kBlock + tid) < nbins) L.run[kBlock + tid] += ch.w + pre1;
-  }
-  for (uint32_t base = lo; base < hi; base += kSortTile) {
-    const bool more = base + kSortTile < hi;
-    if (more) load_sort_tile(kin, vin, base + kSortTile, hi, nkey, nval);
-    for (uint32_t e = tid; e < kWaves * kSortBins; e += kBlock) (&L.wave_cnt[0][0])[e] = 0;
-    __syncthreads();
-    uint32_t dig[kSortItems], rank[kSortItems];
-    bool valid[kSortItems];
 #pragma unroll
-    for (int r = 0; r < kSortItems; ++r) {
-      valid[r] = base + wave * (64 * kSortItems) + r * 64 + lane < hi;
-      dig[r] = (key[r] >> shift) & mask;
+        for (int u = 0; u < kRows; ++u) {
+          if (kk + u < k) {
+            pre0 += x0[u];
+            pre1 += x1[u];
+          }
+          tot0 += x0[u];
+          tot1 += x1[u];
+        }
+      }
+      L.run[tid] = tot0;
+      L.run[kBlock + tid] = tot1;
+      __syncthreads();
+      scan_bins(L.run, L.run, (int)nbins, L.scan_tmp);
+      if ((uint32_t)tid < nbins) L.run[tid] += ch.w + pre0;
+      if ((uint32_t)(kBlock + tid) < nbins) L.run[kBlock + tid] += ch.w + pre1;
     }
-    // wave multi-split over the rounds: tile order is (wave, round, lane)
+    for (uint32_t base = lo; base < hi; base += kSortTile) {
+      const bool more = base + kSortTile < hi;
+      if (more) load_sort_tile(kin, vin, base + kSortTile, hi, nkey, nval);
+      for (uint32_t e = tid; e < kWaves * kSortBins; e += kBlock) (&L.wave_cnt[0][0])[e] = 0u;
+      __syncthreads();
+      uint32_t rank[kSortItems];
+      bool valid[kSortItems];
 #pragma unroll
-    for (int r = 0; r < kSortItems; ++r) {
-      const uint64_t m = match_digit(dig[r], valid[r]);
-      uint32_t prior = 0;
-      if (valid[r]) prior = L.wave_cnt[wave][dig[r]];
-      __builtin_amdgcn_wave_barrier();
-      if (valid[r]) {
-        rank[r] = prior + count_below(m);
-        if (count_below(m) == 0) L.wave_cnt[wave][dig[r]] = prior + __popcll(m);
-      }
-      __builtin_amdgcn_wave_barrier();
-    }
-    __syncthreads();
-    for (uint32_t e = tid; e < nbins; e += kBlock) {
-      uint32_t t = 0;
-#pragma unroll
-      for (int w = 0; w < kWaves; ++w) {
-        const uint32_t x = L.wave_cnt[w][e];
-        L.wave_cnt[w][e] = t;
-        t += x;
-      }
-      L.tile_cnt[e] = t;
-    }
-    __syncthreads();
-    scan_bins(L.tile_cnt, L.local_off, (int)nbins, L.scan_tmp);
-#pragma unroll
-    for (int r = 0; r < kSortItems; ++r) {
-      if (valid[r]) {
-        const uint32_t lp = L.local_off[dig[r]] + L.wave_cnt[wave][dig[r]] + rank[r];
-        L.keys[lp] = key[r];
-        L.vals[lp] = val[r];
-        L.digit[lp] = (uint16_t)dig[r];
-      }
-    }
-    __syncthreads();
-    const uint32_t n_in = min((uint32_t)kSortTile, hi - base);
-    for (uint32_t i = tid; i < n_in; i += kBlock) {
-      const uint32_t dd = L.digit[i];
-      const uint32_t gp = L.run[dd] + (i - L.local_off[dd]);
-      if (gp < K) {  // always true when the counts match the pairs
-        kout[gp] = L.keys[i];
-        vout[gp] = L.vals[i];
-      } else {
-        raise_fault(h, MMBEV_FAULT_INTERNAL);
-      }
-    }
-    __syncthreads();
-    for (uint32_t e = tid; e < nbins; e += kBlock) L.run[e] += L.tile_cnt[e];
-    if (more)
+      for (int r = 0; r < kSortItems; ++r) valid[r] = base + wave * (64 * kSortItems) + r * 64 + lane < hi;
+      auto dig = [&](int r) -> uint32_t { return (key[r] >> shift) & mask; };  // recomputed: fewer live registers
+      // wave multi-split over the rounds (tile order: wave, round, lane): the
+      // first lane of each digit's group adds the group's size to the wave's
+      // count of that digit with an LDS atomic that returns the count before
+      // it.  A wave's LDS operations complete in issue order, so the rounds'
+      // atomics go out back to back; each lane then takes its group's count
+      // from the group's first lane (bpermute) and adds its place in the group.
+      uint64_t mm[kSortItems];
+      uint32_t old[kSortItems];
 #pragma unroll
       for (int r = 0; r < kSortItems; ++r) {
-        key[r] = nkey[r];
-        val[r] = nval[r];
+        mm[r] = match_digit(dig(r), valid[r]);
+        old[r] = 0u;
+        if (valid[r] && count_below(mm[r]) == 0) old[r] = atomicAdd(&L.wave_cnt[wave][dig(r)], (uint32_t)__popcll(mm[r]));
       }
+#pragma unroll
+      for (int r = 0; r < kSortItems; ++r) {
+        const int first = mm[r] != 0ull ? __builtin_ctzll(mm[r]) : 0;
+        const uint32_t prior = (uint32_t)__builtin_amdgcn_ds_bpermute(first << 2, (int)old[r]);
+        rank[r] = prior + count_below(mm[r]);
+      }
+      __syncthreads();
+      // per digit: each wave's offset inside the tile's run of that digit, and the run's size
+      for (uint32_t e = tid; e < nbins; e += kBlock) {
+        uint32_t t = 0;
+#pragma unroll
+        for (int w = 0; w < kWaves; ++w) {
+          const uint32_t x = L.wave_cnt[w][e];
+          L.wave_cnt[w][e] = t;
+          t += x;
+        }
+        L.local_off[e] = t;
+      }
+      __syncthreads();
+      const uint32_t ntile = scan_bins(L.local_off, L.local_off, (int)nbins, L.scan_tmp);
+      if (tid == 0) L.local_off[nbins] = ntile;
+#pragma unroll
+      for (int r = 0; r < kSortItems; ++r) {
+        if (valid[r]) {
+          const uint32_t lp = L.local_off[dig(r)] + L.wave_cnt[wave][dig(r)] + rank[r];
+          L.keys[lp] = key[r];
+          L.vals[lp] = val[r];
+        }
+      }
+      __syncthreads();
+      const uint32_t n_in = min((uint32_t)kSortTile, hi - base);
+#pragma unroll
+      for (int r = 0; r < kSortItems; ++r) {  // unrolled: the LDS reads of all rounds in flight together
+        const uint32_t i = (uint32_t)(r * kBlock + tid);
+        if (i < n_in) {
+          const uint32_t kv = L.keys[i];
+          const uint32_t dd = (kv >> shift) & mask;
+          const uint32_t gp = L.run[dd] + (i - L.local_off[dd]);
+          if (gp < K) {  // always true when the counts match the pairs
+            kout[gp] = kv;
+            vout[gp] = L.vals[i];
+          } else {
+            raise_fault(h, MMBEV_FAULT_INTERNAL);
+          }
+        }
+      }
+      __syncthreads();
+      for (uint32_t e = tid; e < nbins; e += kBlock) L.run[e] += L.local_off[e + 1] - L.local_off[e];
+      if (more)
+#pragma unroll
+        for (int r = 0; r < kSortItems; ++r) {
+          key[r] = nkey[r];
+          val[r] = nval[r];
+        }
+    }
+    __syncthreads();  // the next chunk rewrites run and local_off
   }
 }
 
@@ -511,11 +526,13 @@ hipError_t launch_compact(const Config& c, uint32_t* kout, hipStream_t st) {
 
 hipError_t launch_radix_pass(const Config& c, int pass, const uint32_t* kin, const uint32_t* vin, uint32_t* kout,
                              uint32_t* vout, hipStream_t st) {
-  hipLaunchKernelGGL(count_kernel, dim3(c.schunk_max), dim3(kBlock), 0, st, c, pass, kin);
+  // grids of resident size (idle workgroups still cost dispatch time)
+  const uint32_t cgrid = min((uint32_t)c.schunk_max, (uint32_t)kCountGrid);
+  hipLaunchKernelGGL(count_kernel, dim3(cgrid), dim3(kBlock), 0, st, c, pass, kin);
   const hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  const uint32_t grid = (c.schunk_max + 7u) / 8u * 8u;  // whole rounds of the eight XCDs
-  hipLaunchKernelGGL(scatter_kernel, dim3(grid), dim3(kBlock), 0, st, c, pass, kin, vin, kout, vout);
+  const uint32_t sgrid = min((c.schunk_max + 7u) / 8u * 8u, (uint32_t)(kScatterPerCu * kCus));  // whole rounds of the XCDs
+  hipLaunchKernelGGL(scatter_kernel, dim3(sgrid), dim3(kBlock), 0, st, c, pass, kin, vin, kout, vout);
   return hipGetLastError();
 }
 

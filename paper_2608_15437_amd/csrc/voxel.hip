@@ -476,7 +476,8 @@ __global__ __launch_bounds__(kBlock) void mean_kernel(Config c, const uint32_t* 
 }  // namespace
 
 hipError_t launch_heads(const Config& c, const uint32_t* keys, const uint32_t* vals, hipStream_t st) {
-  hipLaunchKernelGGL(heads_kernel, dim3(std::min(c.vtile_max, 4096)), dim3(kBlock), 0, st, c, keys, vals);
+  // a grid of resident size (six per CU by registers) walks the tiles
+  hipLaunchKernelGGL(heads_kernel, dim3(std::min(c.vtile_max, 6 * kCus)), dim3(kBlock), 0, st, c, keys, vals);
   return hipGetLastError();
 }
 

@@ -202,24 +202,6 @@ mmbev_status_t mmbev_workspace_init(void* workspace, size_t workspace_bytes, voi
                                                                                            : MMBEV_ERR_HIP;
 }
 
-mmbev_status_t mmbev_make_rois(const double* desc, int64_t count, mmbev_roi_t* out) {
-  if (count < 0 || (count > 0 && (!desc || !out))) return MMBEV_ERR_INVALID_ARG;
-  for (int64_t k = 0; k < count; ++k) {
-    const double* d = desc + 6 * k;
-    mmbev_roi_t r;
-    r.cx = (float)d[0];
-    r.cy = (float)d[1];
-    r.cos_yaw = (float)std::cos(d[4]);
-    r.sin_yaw = (float)std::sin(d[4]);
-    r.ext_x = (float)(0.5 * d[2] + d[5]);
-    r.ext_y = (float)(0.5 * d[3] + d[5]);
-    r.reserved[0] = 0.0f;
-    r.reserved[1] = 0.0f;
-    out[k] = r;
-  }
-  return MMBEV_OK;
-}
-
 }  // extern "C"
 
 namespace {

@@ -68,7 +68,7 @@ struct Plan {
   int32_t kb, passes, dbits;
   int64_t fchunk_points, fchunk_max, filter_grid, schunk_max, vtile_max, mean_grid;
   size_t off_hdr, off_cellmask, off_cellany, off_budgetmask, off_fchunk_first, off_fbits, off_fcount, off_fchunk_lo, off_fchunk_frame, off_wgframe, off_spare, off_fprefix,
-      off_fstart, off_schunk_first, off_schunk, off_schunk_frame, off_cnt, off_vtile, off_vt_first, off_hcount, off_hpre, off_mtile, off_keys[2], off_vals[2], off_rec,
+      off_fstart, off_schunk_first, off_schunk, off_schunk_frame, off_cnt, off_vtile, off_vt_first, off_hcount, off_hpre, off_mtile, off_trow, off_keys[2], off_vals[2], off_rec,
       off_hpos, off_hplace, off_capbits, off_rank, off_voxoff, total;
 };
 
@@ -157,6 +157,7 @@ mmbev_status_t make_plan(const mmbev_grid_t* g, int64_t N, int32_t max_rois, int
   p->off_hcount = take((size_t)p->vtile_max * 4);
   p->off_hpre = take((size_t)(p->vtile_max + 1) * 4);
   p->off_mtile = take(((size_t)n1 / kMeanTile + 2) * 4);
+  p->off_trow = take((size_t)p->vtile_max * 8);
   for (int q = 0; q < 2; ++q) {
     p->off_keys[q] = take((size_t)n1 * 4);
     p->off_vals[q] = take((size_t)n1 * 4);
@@ -334,6 +335,7 @@ mmbev_status_t voxelize(const mmbev_points_t* points, const uint8_t* sweep_ids, 
   c.hcount = (uint32_t*)(ws + p.off_hcount);
   c.hpre = (uint32_t*)(ws + p.off_hpre);
   c.mtile = (uint32_t*)(ws + p.off_mtile);
+  c.trow = (int64_t*)(ws + p.off_trow);
   for (int q = 0; q < 2; ++q) {
     c.keys[q] = (uint32_t*)(ws + p.off_keys[q]);
     c.vals[q] = (uint32_t*)(ws + p.off_vals[q]);

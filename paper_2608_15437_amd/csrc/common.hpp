@@ -112,6 +112,7 @@ struct Config {
   uint32_t* hcount;        // [vtile_max] voxels (heads) of tile t
   uint32_t* hpre;          // [vtile_max + 1] voxels of the tiles before t (all frames)
   uint32_t* mtile;         // [N / kMeanTile + 2] tile of voxel i * kMeanTile (the mean's blocks)
+  int64_t* trow;           // [vtile_max] output row of tile t's first voxel; -1 in a frame over the cap
   uint32_t* keys[2];       // [N] each: ping-pong buffers of the radix passes
   uint32_t* vals[2];       // the pair's record: its place in compact (point) order
   // records of the kept points in compact order, written by the compaction:

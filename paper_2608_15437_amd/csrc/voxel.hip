@@ -25,58 +25,61 @@ namespace mmbev {
 
 namespace {
 
-// Whether sorted pair i of a frame whose first pair is ff starts a voxel.
-__device__ __forceinline__ bool is_head(const uint32_t* keys, uint32_t ff, uint32_t i) {
-  return i == ff || keys[i] != keys[i - 1];
-}
+// One voxel tile (kVoxTile sorted pairs, kHeadItems per thread) per step of
+// a grid-stride loop: every pair's key, its predecessor's key and its value
+// load together; a pair starts a voxel when it is the frame's first or its
+// key differs from its predecessor's.  The heads are numbered in pair order
+// (row j of kBlock pairs, then wave, then lane: a ballot per row, the rows'
+// and waves' counts scanned by one wave).
+constexpr int kHeadItems = kVoxTile / kBlock;
+static_assert(kHeadItems * kWaves <= 64, "one wave scans the counts");
 
 __global__ __launch_bounds__(kBlock) void heads_kernel(Config c, const uint32_t* keys, const uint32_t* vals) {
-  __shared__ uint32_t s_off[kCountItems][kWaves];  // heads before row j of wave w in the batch
-  __shared__ uint32_t s_batch;
+  __shared__ uint32_t s_off[kHeadItems * kWaves];  // heads before (row j, wave w), at j * kWaves + w
+  __shared__ uint32_t s_total;
   const int tid = threadIdx.x;
   const int lane = tid & 63, wave = tid >> 6;
   const uint32_t nvt = c.hdr->vtiles;
-  const uint64_t lt = lanemask_lt();
   for (uint32_t t = blockIdx.x; t < nvt; t += gridDim.x) {
-  const uint4 vt = c.vtile[t];
-  const uint32_t lo = vt.x, hi = vt.y, ff = vt.w;
-  uint32_t v0 = 0;
-  // batches of kCountItems rows of kBlock consecutive pairs (coalesced);
-  // heads numbered in pair order: row, then wave, then lane
-  for (uint32_t base = lo; base < hi; base += kBlock * kCountItems) {
-    uint64_t m[kCountItems];
+    const uint4 vt = c.vtile[t];
+    const uint32_t lo = vt.x, hi = vt.y, ff = vt.w;
+    uint32_t key[kHeadItems], prv[kHeadItems], val[kHeadItems];
 #pragma unroll
-    for (int j = 0; j < kCountItems; ++j) {
-      const uint32_t i = base + j * kBlock + tid;
-      m[j] = __ballot(i < hi && is_head(keys, ff, i));
+    for (int j = 0; j < kHeadItems; ++j) {  // all loads in flight together
+      const uint32_t i = lo + j * kBlock + tid;
+      const bool in = i < hi;
+      key[j] = in ? keys[i] : 0u;
+      prv[j] = in && i > ff ? keys[i - 1] : ~key[j];  // the frame's first pair: always a head
+      val[j] = in ? vals[i] : 0u;
     }
+    uint64_t m[kHeadItems];
+#pragma unroll
+    for (int j = 0; j < kHeadItems; ++j) m[j] = __ballot(lo + j * kBlock + tid < hi && key[j] != prv[j]);
     if (lane == 0)
 #pragma unroll
-      for (int j = 0; j < kCountItems; ++j) s_off[j][wave] = (uint32_t)__popcll(m[j]);
+      for (int j = 0; j < kHeadItems; ++j) s_off[j * kWaves + wave] = (uint32_t)__popcll(m[j]);
     __syncthreads();
-    if (tid == 0) {
-      uint32_t run = 0;
-      for (int j = 0; j < kCountItems; ++j)
-        for (int w = 0; w < kWaves; ++w) {
-          const uint32_t x = s_off[j][w];
-          s_off[j][w] = run;
-          run += x;
-        }
-      s_batch = run;
+    if (wave == 0) {  // exclusive scan of the kHeadItems * kWaves counts
+      const uint32_t x = lane < kHeadItems * kWaves ? s_off[lane] : 0u;
+      uint32_t y = x;
+#pragma unroll
+      for (int d = 1; d < 64; d <<= 1) {
+        const uint32_t z = __shfl_up(y, d, 64);
+        if (lane >= d) y += z;
+      }
+      if (lane < kHeadItems * kWaves) s_off[lane] = y - x;
+      if (lane == 63) s_total = y;
     }
     __syncthreads();
 #pragma unroll
-    for (int j = 0; j < kCountItems; ++j)
+    for (int j = 0; j < kHeadItems; ++j)
       if ((m[j] >> lane) & 1u) {
-        const uint32_t slot = lo + v0 + s_off[j][wave] + (uint32_t)__popcll(m[j] & lt);
-        const uint32_t i = base + j * kBlock + tid;
-        c.hpos[slot] = i;
-        c.hplace[slot] = vals[i];
+        const uint32_t slot = lo + s_off[j * kWaves + wave] + count_below(m[j]);
+        c.hpos[slot] = lo + j * kBlock + tid;
+        c.hplace[slot] = val[j];
       }
-    v0 += s_batch;
-    __syncthreads();
-  }
-  if (tid == 0) c.hcount[t] = v0;
+    if (tid == 0) c.hcount[t] = s_total;
+    __syncthreads();  // the next tile rewrites the counts
   }
 }
 
@@ -120,12 +123,7 @@ __device__ void finalize_offsets(const Config& c, uint32_t* s_tmp) {
   const uint32_t V = scan_fin(c.hcount, c.hpre, nvt, s_tmp);
   if (tid == 0) c.hpre[nvt] = V;
   __syncthreads();
-  // the mean's block i (voxels i * kMeanTile ...) starts in tile mtile[i]
-  for (uint32_t t = tid; t < nvt; t += kFinBlock) {
-    const uint32_t v0 = c.hpre[t], v1 = c.hpre[t + 1];
-    for (uint32_t i = (v0 + kMeanTile - 1) / kMeanTile; (uint64_t)i * kMeanTile < v1; ++i) c.mtile[i] = t;
-  }
-  if (tid == 0) c.mtile[(V + kMeanTile - 1) / kMeanTile] = nvt > 0 ? nvt - 1 : 0u;
+  // every frame's voxels and its output rows (at most max_voxels)
   uint32_t carry_out = 0, carry_cap = 0;
   for (int32_t chunk = 0; chunk < c.B; chunk += kFinBlock) {
     const int32_t b = chunk + tid;
@@ -152,6 +150,18 @@ __device__ void finalize_offsets(const Config& c, uint32_t* s_tmp) {
     h->capped_voxels = carry_cap;
     h->any_capped = carry_cap > 0 ? 1u : 0u;
   }
+  __syncthreads();  // the frames' tables in place
+  // per tile: the output row of its first voxel (-1 in a frame over the
+  // cap, whose rows come from the cap's ranks), and the mean's block i
+  // (voxels i * kMeanTile ...) starts in tile mtile[i]
+  for (uint32_t t = tid; t < nvt; t += kFinBlock) {
+    const uint32_t v0 = c.hpre[t], v1 = c.hpre[t + 1];
+    const int32_t b = (int32_t)min(c.vtile[t].z, (uint32_t)c.B - 1u);
+    const uint32_t fv0 = c.vox_off[b], fv1 = c.vox_off[b + 1];
+    c.trow[t] = fv1 - fv0 > (uint32_t)c.cap ? (int64_t)-1 : c.out_voxel_offsets[b] + (int64_t)(v0 - fv0);
+    for (uint32_t i = (v0 + kMeanTile - 1) / kMeanTile; (uint64_t)i * kMeanTile < v1; ++i) c.mtile[i] = t;
+  }
+  if (tid == 0) c.mtile[(V + kMeanTile - 1) / kMeanTile] = nvt > 0 ? nvt - 1 : 0u;
 }
 
 struct CapLds {
@@ -341,6 +351,7 @@ __global__ __launch_bounds__(kBlock) void mean_kernel(Config c, const uint32_t* 
     int64_t row = -1;
     int32_t b = 0;
     uint32_t s0 = 0, cnt = 0;
+    uint32_t q0 = 0;  // the first point's place (the head's value)
     if (v < V) {
       // the voxel's tile: the largest t in [ta, tb] with hpre[t] <= v
       uint32_t t = ta, z = tb;
@@ -348,25 +359,45 @@ __global__ __launch_bounds__(kBlock) void mean_kernel(Config c, const uint32_t* 
         const uint32_t mid = (t + z + 1) >> 1;
         if (c.hpre[mid] <= v) t = mid; else z = mid - 1;
       }
+      // the tile and the next one load together
+      const bool has_next = t + 1 < nvt;
       const uint4 vt = c.vtile[t];
+      const uint4 vn = has_next ? c.vtile[t + 1] : make_uint4(0u, 0u, 0xffffffffu, 0u);
       const uint32_t j = v - c.hpre[t], nh = c.hcount[t];
+      const uint32_t nhn = has_next ? c.hcount[t + 1] : 0u;
+      const int64_t tr = c.trow[t];
       b = (int32_t)min(vt.z, (uint32_t)c.B - 1u);
-      const uint32_t fv0 = c.vox_off[b], fv1 = c.vox_off[b + 1];
       const uint32_t slot = vt.x + j;
-      const uint32_t rank = fv1 - fv0 > (uint32_t)c.cap ? c.out_rank[min(slot, K - 1u)] : v - fv0;
-      if (rank != 0xffffffffu) {
-        row = c.out_voxel_offsets[b] + (int64_t)rank;
-        if (row < 0 || row >= rows || slot >= K) {
+      int64_t r = -1;
+      if (tr >= 0) {
+        r = tr + (int64_t)j;
+      } else {  // a frame over the cap: the cap's rank
+        const uint32_t rank = c.out_rank[min(slot, K - 1u)];
+        if (rank != 0xffffffffu) r = c.out_voxel_offsets[b] + (int64_t)rank;
+      }
+      if (r >= 0) {
+        if (r >= rows || slot >= K) {
           raise_fault(h, MMBEV_FAULT_INTERNAL);
-          row = -1;
         } else {
+          row = r;
+          // the voxel's pairs end at the next head: in this tile, at the
+          // next tile's first head (same frame), or at the frame's end
+          const bool last = j + 1 >= nh;
+          const bool next_same = vn.z == vt.z;
           s0 = min(c.hpos[slot], K - 1u);
-          if (j + 1 < nh) {
-            cnt = min(max(c.hpos[slot + 1], s0 + 1u) - s0, (uint32_t)M);
+          q0 = c.hplace[slot];
+          uint32_t e = 0;
+          if (!last)
+            e = c.hpos[slot + 1];
+          else if (!next_same)
+            e = vt.y;  // the frame's last tile ends at the frame's end
+          else if (nhn > 0)
+            e = c.hpos[vn.x];
+          if (!last || !next_same || nhn > 0) {
+            cnt = min(max(e, s0 + 1u) - s0, (uint32_t)M);
           } else {
-            // the tile's last voxel may run on into the next tiles: its
-            // first max_points pairs decide the count (read eight at a
-            // time, their loads in flight together)
+            // a voxel that runs through the whole next tile: its first
+            // max_points pairs decide the count (read eight at a time)
             const uint32_t fend = min(c.fstart[b + 1], K);
             const uint32_t k0 = keys[s0];
             cnt = 1;
@@ -409,7 +440,8 @@ __global__ __launch_bounds__(kBlock) void mean_kernel(Config c, const uint32_t* 
       uint32_t q[kMeanBatch];
       uint4 r0[kMeanBatch], r1[kMeanBatch];
 #pragma unroll
-      for (int u = 0; u < kMeanBatch; ++u) q[u] = m0 + u < cnt ? min(vals[s0 + m0 + u], K - 1u) : 0u;
+      for (int u = 0; u < kMeanBatch; ++u)  // the first point's place came with the head
+        q[u] = m0 + u < cnt ? min(m0 + u == 0 ? q0 : vals[s0 + m0 + u], K - 1u) : 0u;
 #pragma unroll
       for (int u = 0; u < kMeanBatch; ++u) {  // one or two 16-byte loads per record
         const uint4* r = reinterpret_cast<const uint4*>(c.rec + (int64_t)q[u] * RW);

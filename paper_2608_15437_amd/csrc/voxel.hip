@@ -45,16 +45,19 @@ __global__ __launch_bounds__(kBlock) void heads_kernel(Config c, const uint32_t*
     const uint32_t lo = vt.x, hi = vt.y, ff = vt.w;
     uint32_t key[kHeadItems], prv[kHeadItems], val[kHeadItems];
 #pragma unroll
-    for (int j = 0; j < kHeadItems; ++j) {  // all loads in flight together
-      const uint32_t i = lo + j * kBlock + tid;
-      const bool in = i < hi;
-      key[j] = in ? keys[i] : 0u;
-      prv[j] = in && i > ff ? keys[i - 1] : ~key[j];  // the frame's first pair: always a head
-      val[j] = in ? vals[i] : 0u;
+    for (int j = 0; j < kHeadItems; ++j) {  // all loads in flight together: unconditional, at clamped indices
+      const uint32_t i = min(lo + j * kBlock + tid, hi - 1u);  // hi > lo: a tile is never empty
+      const uint32_t ip = i > ff ? i - 1u : i;
+      key[j] = keys[i];
+      prv[j] = keys[ip];
+      val[j] = vals[i];
     }
     uint64_t m[kHeadItems];
 #pragma unroll
-    for (int j = 0; j < kHeadItems; ++j) m[j] = __ballot(lo + j * kBlock + tid < hi && key[j] != prv[j]);
+    for (int j = 0; j < kHeadItems; ++j) {  // the frame's first pair is always a head
+      const uint32_t i = lo + j * kBlock + tid;
+      m[j] = __ballot(i < hi && (i == ff || key[j] != prv[j]));
+    }
     if (lane == 0)
 #pragma unroll
       for (int j = 0; j < kHeadItems; ++j) s_off[j * kWaves + wave] = (uint32_t)__popcll(m[j]);
@@ -195,8 +198,9 @@ __device__ void cap_frame(const Config& c, int32_t b, CapLds& S, uint32_t t0, ui
   uint32_t* hc = kLds ? S.hc : c.capbits + 3 * words + t0;
   if (kLds)
     for (uint32_t i = tid; i < nt; i += kFinBlock) hc[i] = c.hcount[t0 + i];
-  // slot fs + i holds a voxel when its offset in its tile is below the tile's count
-  auto holds_voxel = [&](uint32_t i) -> bool { return i < nk && (i % kVoxTile) < hc[i / kVoxTile]; };
+  // slot fs + i holds a voxel when its offset in its tile is below the
+  // tile's count (every pass loads at clamped slots, unconditionally, and
+  // tests that afterwards, so that its loads are in flight together)
   const uint32_t nw = (nk + 31) / 32;
   uint32_t* bits = kLds ? S.area : c.capbits + wbase;
   constexpr int kUnroll = 32;  // loads in flight per thread: one workgroup walks the whole frame
@@ -204,15 +208,19 @@ __device__ void cap_frame(const Config& c, int32_t b, CapLds& S, uint32_t t0, ui
   for (uint32_t w = tid; w < nw; w += kFinBlock) bits[w] = 0u;
   __syncthreads();  // also: the tiles' counts are in place
   for (uint32_t base = tid; base < nk; base += kFinBlock * kUnroll) {
-    uint32_t p[kUnroll];
+    uint32_t p[kUnroll], n[kUnroll];
 #pragma unroll
-    for (int u = 0; u < kUnroll; ++u) {  // all loads of the batch in flight together
-      const uint32_t i = base + u * kFinBlock;
-      p[u] = holds_voxel(i) ? c.hplace[fs + i] - fs : 0xffffffffu;
+    for (int u = 0; u < kUnroll; ++u) {  // all loads of the batch in flight together (clamped, unconditional)
+      const uint32_t i = min(base + u * kFinBlock, nk - 1u);
+      p[u] = c.hplace[fs + i];
+      n[u] = hc[i / kVoxTile];
     }
 #pragma unroll
-    for (int u = 0; u < kUnroll; ++u)
-      if (p[u] < nk) atomicOr(&bits[p[u] >> 5], 1u << (p[u] & 31));
+    for (int u = 0; u < kUnroll; ++u) {
+      const uint32_t i = base + u * kFinBlock;
+      const uint32_t q = p[u] - fs;
+      if (i < nk && (i % kVoxTile) < n[u] && q < nk) atomicOr(&bits[q >> 5], 1u << (q & 31));
+    }
   }
   __syncthreads();
   // 2. the max_voxels-th smallest first place: thread t counts a contiguous run of words
@@ -244,16 +252,18 @@ __device__ void cap_frame(const Config& c, int32_t b, CapLds& S, uint32_t t0, ui
   uint32_t* kb = kLds ? S.area : c.capbits + words + wbase;
   uint32_t* wp = kLds ? S.area + nw : c.capbits + 2 * words + wbase;
   for (uint32_t base = (uint32_t)(tid & ~63); base < nk; base += kFinBlock * kUnroll) {
-    uint32_t p[kUnroll];
+    uint32_t p[kUnroll], n[kUnroll];
 #pragma unroll
-    for (int u = 0; u < kUnroll; ++u) {
-      const uint32_t i = base + u * kFinBlock + (uint32_t)lane;
-      p[u] = holds_voxel(i) ? c.hplace[fs + i] : 0xffffffffu;
+    for (int u = 0; u < kUnroll; ++u) {  // clamped, unconditional loads
+      const uint32_t i = min(base + u * kFinBlock + (uint32_t)lane, nk - 1u);
+      p[u] = c.hplace[fs + i];
+      n[u] = hc[i / kVoxTile];
     }
 #pragma unroll
     for (int u = 0; u < kUnroll; ++u) {
       const uint32_t i0 = base + u * kFinBlock;  // the wave's first slot of this step
-      const uint64_t m = __ballot(p[u] <= thr);
+      const uint32_t i = i0 + (uint32_t)lane;
+      const uint64_t m = __ballot(i < nk && (i % kVoxTile) < n[u] && p[u] <= thr);
       if (i0 < nk) {
         if (lane == 0) kb[i0 >> 5] = (uint32_t)m;
         if (lane == 32 && i0 + 32 < nk) kb[(i0 >> 5) + 1] = (uint32_t)(m >> 32);
@@ -277,13 +287,20 @@ __device__ void cap_frame(const Config& c, int32_t b, CapLds& S, uint32_t t0, ui
   __syncthreads();
   // 5. the kept voxels' rows inside the frame
   for (uint32_t base = tid; base < nk; base += kFinBlock * 8) {
+    uint32_t n[8], word[8], pre[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {  // clamped, unconditional reads
+      const uint32_t i = min(base + u * kFinBlock, nk - 1u);
+      n[u] = hc[i / kVoxTile];
+      word[u] = kb[i >> 5];
+      pre[u] = wp[i >> 5];
+    }
 #pragma unroll
     for (int u = 0; u < 8; ++u) {
       const uint32_t i = base + u * kFinBlock;
-      if (holds_voxel(i)) {
-        const uint32_t word = kb[i >> 5];
-        const bool keep = (word >> (i & 31)) & 1u;
-        c.out_rank[fs + i] = keep ? wp[i >> 5] + (uint32_t)__popc(word & ((1u << (i & 31)) - 1u)) : 0xffffffffu;
+      if (i < nk && (i % kVoxTile) < n[u]) {  // slot i holds a voxel
+        const bool keep = (word[u] >> (i & 31)) & 1u;
+        c.out_rank[fs + i] = keep ? pre[u] + (uint32_t)__popc(word[u] & ((1u << (i & 31)) - 1u)) : 0xffffffffu;
       }
     }
   }
@@ -322,12 +339,16 @@ __global__ __launch_bounds__(kFinBlock) void fincap_kernel(Config c) {
 // Blocks of kMeanTile consecutive voxels (grid-stride), one thread per
 // voxel: its tile (between the tiles of its block and of the next block),
 // output row, kept count, point indices and the fp64 mean of every feature.
-// The records of a voxel's points are read kMeanBatch at a time, all their
-// loads in flight together.  When the block's rows are consecutive (no frame
+// Every lane loads at clamped, in-bounds indices, unconditionally, and the
+// masks (a voxel past V, a voxel the cap drops, a point past the count) are
+// applied to the values afterwards: the loads of each level are in flight
+// together.  The records of a voxel's points (RW words each) are read
+// kMeanBatch at a time.  When the block's rows are consecutive (no frame
 // over the cap in it) they are assembled in LDS and written as contiguous
 // runs; otherwise each thread writes its own row.
 constexpr int kMeanBatch = 2;  // records in flight per thread: more cost occupancy (VGPRs), fewer add round trips
 
+template <int RW>
 __global__ __launch_bounds__(kBlock) void mean_kernel(Config c, const uint32_t* keys, const uint32_t* vals) {
   extern __shared__ uint32_t sm[];
   __shared__ int64_t s_row0;
@@ -341,80 +362,69 @@ __global__ __launch_bounds__(kBlock) void mean_kernel(Config c, const uint32_t* 
   int32_t* l_co = (int32_t*)sm;              // [kMeanTile][4]
   float* l_ft = (float*)(sm + kMeanTile * 4);  // [kMeanTile][C]
   int32_t* l_pi = (int32_t*)(sm + kMeanTile * (4 + C));  // [kMeanTile][M]
+  if (K == 0u || nvt == 0u) return;  // uniform: no voxel (V is 0 too)
   for (uint32_t g0 = blockIdx.x * kMeanTile; g0 < V; g0 += gridDim.x * kMeanTile) {
     const uint32_t v = g0 + tid;
+    const bool live = v < V;
+    const uint32_t vv = min(v, V - 1u);
     const uint32_t nblk = min((uint32_t)kMeanTile, V - g0);
-    // the block's voxels lie in tiles mtile[i] .. mtile[i + 1]
+    // the block's voxels lie in tiles mtile[i] .. mtile[i + 1]; the voxel's
+    // tile is the largest t there with hpre[t] <= v
     const uint32_t bi = g0 / kMeanTile;
     const uint32_t ta = min(c.mtile[bi], nvt - 1u);
     const uint32_t tb = min(max(c.mtile[bi + 1], ta), nvt - 1u);
-    int64_t row = -1;
-    int32_t b = 0;
-    uint32_t s0 = 0, cnt = 0;
-    uint32_t q0 = 0;  // the first point's place (the head's value)
-    if (v < V) {
-      // the voxel's tile: the largest t in [ta, tb] with hpre[t] <= v
-      uint32_t t = ta, z = tb;
-      while (t < z) {
-        const uint32_t mid = (t + z + 1) >> 1;
-        if (c.hpre[mid] <= v) t = mid; else z = mid - 1;
-      }
-      // the tile and the next one load together
-      const bool has_next = t + 1 < nvt;
-      const uint4 vt = c.vtile[t];
-      const uint4 vn = has_next ? c.vtile[t + 1] : make_uint4(0u, 0u, 0xffffffffu, 0u);
-      const uint32_t j = v - c.hpre[t], nh = c.hcount[t];
-      const uint32_t nhn = has_next ? c.hcount[t + 1] : 0u;
-      const int64_t tr = c.trow[t];
-      b = (int32_t)min(vt.z, (uint32_t)c.B - 1u);
-      const uint32_t slot = vt.x + j;
-      int64_t r = -1;
-      if (tr >= 0) {
-        r = tr + (int64_t)j;
-      } else {  // a frame over the cap: the cap's rank
-        const uint32_t rank = c.out_rank[min(slot, K - 1u)];
-        if (rank != 0xffffffffu) r = c.out_voxel_offsets[b] + (int64_t)rank;
-      }
-      if (r >= 0) {
-        if (r >= rows || slot >= K) {
-          raise_fault(h, MMBEV_FAULT_INTERNAL);
-        } else {
-          row = r;
-          // the voxel's pairs end at the next head: in this tile, at the
-          // next tile's first head (same frame), or at the frame's end
-          const bool last = j + 1 >= nh;
-          const bool next_same = vn.z == vt.z;
-          s0 = min(c.hpos[slot], K - 1u);
-          q0 = c.hplace[slot];
-          uint32_t e = 0;
-          if (!last)
-            e = c.hpos[slot + 1];
-          else if (!next_same)
-            e = vt.y;  // the frame's last tile ends at the frame's end
-          else if (nhn > 0)
-            e = c.hpos[vn.x];
-          if (!last || !next_same || nhn > 0) {
-            cnt = min(max(e, s0 + 1u) - s0, (uint32_t)M);
-          } else {
-            // a voxel that runs through the whole next tile: its first
-            // max_points pairs decide the count (read eight at a time)
-            const uint32_t fend = min(c.fstart[b + 1], K);
-            const uint32_t k0 = keys[s0];
-            cnt = 1;
-            bool more = true;
-            for (uint32_t m0 = 1; m0 < (uint32_t)M && more; m0 += 8) {
-              uint32_t kk[8];
+    uint32_t t = ta, z = tb;
+    while (t < z) {
+      const uint32_t mid = (t + z + 1) >> 1;
+      if (c.hpre[mid] <= vv) t = mid; else z = mid - 1;
+    }
+    // the tile and the next one
+    const uint32_t tn = min(t + 1u, nvt - 1u);
+    const uint4 vt = c.vtile[t], vn = c.vtile[tn];
+    const uint32_t j = vv - c.hpre[t], nh = c.hcount[t], nhn = c.hcount[tn];
+    const int64_t tr = c.trow[t];
+    const int32_t b = (int32_t)min(vt.z, (uint32_t)c.B - 1u);
+    const uint32_t slot = vt.x + j, sl = min(slot, K - 1u);
+    // the voxel's heads (and, for a frame over the cap, its rank)
+    const uint32_t rank = c.out_rank[sl];
+    const int64_t ob = c.out_voxel_offsets[b];
+    const uint32_t s0 = min(c.hpos[sl], K - 1u);
+    const uint32_t q0 = c.hplace[sl];  // the first point's place (the head's value)
+    const uint32_t e_in = c.hpos[min(sl + 1u, K - 1u)];
+    const uint32_t e_nx = c.hpos[min(vn.x, K - 1u)];
+    int64_t row = tr >= 0 ? tr + (int64_t)j : (rank != 0xffffffffu ? ob + (int64_t)rank : (int64_t)-1);
+    if (!live) row = -1;
+    if (row >= 0 && (row >= rows || slot >= K)) {
+      raise_fault(h, MMBEV_FAULT_INTERNAL);
+      row = -1;
+    }
+    // the voxel's pairs end at the next head: in this tile, at the next
+    // tile's first head (same frame), or at the frame's end
+    const bool last = j + 1u >= nh;
+    const bool next_same = t + 1u < nvt && vn.z == vt.z;
+    uint32_t cnt = 0;
+    if (row >= 0) {
+      if (!last || !next_same || nhn > 0) {
+        const uint32_t e = !last ? e_in : (!next_same ? vt.y : e_nx);
+        cnt = min(max(e, s0 + 1u) - s0, (uint32_t)M);
+      } else {
+        // a voxel that runs through the whole next tile: its first
+        // max_points pairs decide the count (read eight at a time)
+        const uint32_t fend = min(c.fstart[b + 1], K);
+        const uint32_t k0 = keys[s0];
+        cnt = 1;
+        bool more = true;
+        for (uint32_t m0 = 1; m0 < (uint32_t)M && more; m0 += 8) {
+          uint32_t kk[8];
 #pragma unroll
-              for (int u = 0; u < 8; ++u) {
-                const uint32_t i = s0 + m0 + (uint32_t)u;
-                kk[u] = m0 + u < (uint32_t)M && i < fend ? keys[i] : ~k0;
-              }
+          for (int u = 0; u < 8; ++u) {
+            const uint32_t i = s0 + m0 + (uint32_t)u;
+            kk[u] = m0 + u < (uint32_t)M && i < fend ? keys[i] : ~k0;
+          }
 #pragma unroll
-              for (int u = 0; u < 8; ++u) {
-                more = more && kk[u] == k0;
-                cnt += more ? 1u : 0u;
-              }
-            }
+          for (int u = 0; u < 8; ++u) {
+            more = more && kk[u] == k0;
+            cnt += more ? 1u : 0u;
           }
         }
       }
@@ -423,57 +433,47 @@ __global__ __launch_bounds__(kBlock) void mean_kernel(Config c, const uint32_t* 
     __syncthreads();
     // every row of the block valid and consecutive
     const bool contig = __syncthreads_and((uint32_t)tid >= nblk || (row >= 0 && row == s_row0 + tid)) != 0;
-    int32_t co[4] = {0, 0, 0, 0};
+    // the points' records, kMeanBatch at a time (the first place came with
+    // the head); the voxel's key loads with the first batch
+    const uint32_t kl = keys[s0];
     double sum[8];
 #pragma unroll
     for (int f = 0; f < 8; ++f) sum[f] = 0.0;
-    if (row >= 0) {
-      const uint32_t kl = keys[s0];
-      const uint32_t ix = kl % c.Dx, rest = kl / c.Dx;
-      co[0] = b;
-      co[1] = (int32_t)(rest / c.Dy);
-      co[2] = (int32_t)(rest % c.Dy);
-      co[3] = (int32_t)ix;
-    }
-    const int RW = c.rec_words;
     for (uint32_t m0 = 0; m0 < cnt; m0 += kMeanBatch) {
       uint32_t q[kMeanBatch];
+#pragma unroll
+      for (int u = 0; u < kMeanBatch; ++u)
+        q[u] = min(m0 + u == 0 ? q0 : vals[min(s0 + m0 + u, K - 1u)], K - 1u);
       uint4 r0[kMeanBatch], r1[kMeanBatch];
+      uint32_t r2[kMeanBatch];
 #pragma unroll
-      for (int u = 0; u < kMeanBatch; ++u)  // the first point's place came with the head
-        q[u] = m0 + u < cnt ? min(m0 + u == 0 ? q0 : vals[s0 + m0 + u], K - 1u) : 0u;
-#pragma unroll
-      for (int u = 0; u < kMeanBatch; ++u) {  // one or two 16-byte loads per record
+      for (int u = 0; u < kMeanBatch; ++u) {  // one, two or two and a word of 16-byte loads per record
         const uint4* r = reinterpret_cast<const uint4*>(c.rec + (int64_t)q[u] * RW);
-        if (m0 + u < cnt) {
-          r0[u] = r[0];
-          r1[u] = RW > 4 ? r[1] : make_uint4(0, 0, 0, 0);
-        } else {
-          r0[u] = r1[u] = make_uint4(0, 0, 0, 0);
-        }
+        r0[u] = r[0];
+        r1[u] = RW > 4 ? r[1] : make_uint4(0u, 0u, 0u, 0u);
+        r2[u] = RW > 8 ? c.rec[(int64_t)q[u] * RW + 8] : 0u;
       }
 #pragma unroll
       for (int u = 0; u < kMeanBatch; ++u)
         if (m0 + u < cnt) {
-          const uint32_t w[8] = {r0[u].y, r0[u].z, r0[u].w, r1[u].x, r1[u].y, r1[u].z, r1[u].w, 0u};
+          const uint32_t w[8] = {r0[u].y, r0[u].z, r0[u].w, r1[u].x, r1[u].y, r1[u].z, r1[u].w, r2[u]};
 #pragma unroll
-          for (int f = 0; f < 7; ++f) sum[f] += (double)__uint_as_float(w[f]);  // ascending point order
+          for (int f = 0; f < 8; ++f)
+            if (f < C) sum[f] += (double)__uint_as_float(w[f]);  // ascending point order
           if (contig)  // uniform: LDS staging or the row itself
             l_pi[tid * M + m0 + u] = (int32_t)r0[u].x;
           else
             c.out_point_idx[row * M + m0 + u] = (int32_t)r0[u].x;
         }
-      if (C == 8)  // the eighth feature sits in a third 16-byte word
-#pragma unroll
-        for (int u = 0; u < kMeanBatch; ++u)
-          if (m0 + u < cnt) sum[7] += (double)__uint_as_float(c.rec[(int64_t)q[u] * RW + 8]);
     }
     if (row >= 0) {
+      const uint32_t ix = kl % c.Dx, rest = kl / c.Dx;
+      const int32_t co[4] = {b, (int32_t)(rest / c.Dy), (int32_t)(rest % c.Dy), (int32_t)ix};
       c.out_counts[row] = (int32_t)cnt;
       if (contig) {
         for (int m = (int)cnt; m < M; ++m) l_pi[tid * M + m] = -1;
 #pragma unroll
-        for (int q = 0; q < 4; ++q) l_co[tid * 4 + q] = co[q];
+        for (int e = 0; e < 4; ++e) l_co[tid * 4 + e] = co[e];
 #pragma unroll
         for (int f = 0; f < 8; ++f)
           if (f < C) l_ft[tid * C + f] = (float)(sum[f] / (double)cnt);
@@ -481,7 +481,7 @@ __global__ __launch_bounds__(kBlock) void mean_kernel(Config c, const uint32_t* 
         for (int m = (int)cnt; m < M; ++m) c.out_point_idx[row * M + m] = -1;
         int32_t* o = c.out_coords + row * 4;
 #pragma unroll
-        for (int q = 0; q < 4; ++q) o[q] = co[q];
+        for (int e = 0; e < 4; ++e) o[e] = co[e];
         float* fo = c.out_feats + row * C;
 #pragma unroll
         for (int f = 0; f < 8; ++f)
@@ -520,7 +520,13 @@ hipError_t launch_fincap(const Config& c, hipStream_t st) {
 
 hipError_t launch_mean(const Config& c, const uint32_t* keys, const uint32_t* vals, hipStream_t st) {
   const size_t lds = (size_t)kMeanTile * (4 + c.C + c.M) * 4;
-  hipLaunchKernelGGL(mean_kernel, dim3(c.mean_grid), dim3(kBlock), lds, st, c, keys, vals);
+  // one instance per record width (point index, x', y', z', raw features 3..)
+  if (c.rec_words <= 4)
+    hipLaunchKernelGGL(mean_kernel<4>, dim3(c.mean_grid), dim3(kBlock), lds, st, c, keys, vals);
+  else if (c.rec_words <= 8)
+    hipLaunchKernelGGL(mean_kernel<8>, dim3(c.mean_grid), dim3(kBlock), lds, st, c, keys, vals);
+  else
+    hipLaunchKernelGGL(mean_kernel<12>, dim3(c.mean_grid), dim3(kBlock), lds, st, c, keys, vals);
   return hipGetLastError();
 }
 

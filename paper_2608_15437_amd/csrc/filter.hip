@@ -256,15 +256,26 @@ __device__ __forceinline__ void load_quad_vec(const TileRows& r, uint32_t off, Q
 
 // Any four points, one by one; those at or past `end` get sweep 0xff.
 __device__ __forceinline__ void load_quad_scalar(const Config& c, uint32_t i0, uint32_t end, Quad& d) {
+  // every load unconditional, at a clamped index (end > 0 at every call):
+  // a load behind a condition would be waited for before the next one
+  float x[4], y[4], z[4];
+  uint32_t sw[4];
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    const uint32_t i = min(i0 + q, end - 1u);
+    x[q] = c.feat[i];
+    y[q] = c.feat[c.stride + i];
+    z[q] = c.feat[2 * c.stride + i];
+    sw[q] = c.sweep[i];
+  }
   d.s = 0;
 #pragma unroll
   for (int q = 0; q < 4; ++q) {
-    const uint32_t i = i0 + q;
-    const bool ok = i < end;
-    d.x[q] = ok ? c.feat[i] : 0.0f;
-    d.y[q] = ok ? c.feat[c.stride + i] : 0.0f;
-    d.z[q] = ok ? c.feat[2 * c.stride + i] : 0.0f;
-    d.s |= (ok ? (uint32_t)c.sweep[i] : 0xffu) << (8 * q);
+    const bool ok = i0 + q < end;
+    d.x[q] = ok ? x[q] : 0.0f;
+    d.y[q] = ok ? y[q] : 0.0f;
+    d.z[q] = ok ? z[q] : 0.0f;
+    d.s |= (ok ? sw[q] : 0xffu) << (8 * q);
   }
 }
 

@@ -248,7 +248,7 @@ __global__ __launch_bounds__(kBlock) void compact_kernel(Config c, uint32_t* kou
   const uint32_t fr = c.fchunk_frame[k];
   uint32_t word = tid < c.fchunk_words ? c.fbits[(int64_t)k * c.fchunk_words + tid] : 0u;
   asm volatile("" ::"s"(lo), "s"(dst), "s"(cnt), "s"(fr));  // keeps the loads above the check
-  if (k >= nch) return;
+  if (k >= nch || cnt == 0u) return;  // uniform: past the chunks, or a chunk that kept no point
   const int32_t b = (int32_t)min(fr, (uint32_t)c.B - 1u);
   const int C = c.C, RW = c.rec_words;
   // the frame's poses: loaded now, stored to LDS once the list is built, so

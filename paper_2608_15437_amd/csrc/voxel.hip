@@ -259,16 +259,18 @@ __device__ void cap_frame(const Config& c, int32_t b, CapLds& S, uint32_t t0, ui
       p[u] = c.hplace[fs + i];
       n[u] = hc[i / kVoxTile];
     }
+    // the wave's flag words of this step: ballot u's low half goes to lane
+    // u, its high half to lane 32 + u, and every lane stores one word
+    static_assert(kUnroll == 32, "one flag word per lane and step");
+    uint32_t wv = 0;
 #pragma unroll
     for (int u = 0; u < kUnroll; ++u) {
-      const uint32_t i0 = base + u * kFinBlock;  // the wave's first slot of this step
-      const uint32_t i = i0 + (uint32_t)lane;
+      const uint32_t i = base + u * kFinBlock + (uint32_t)lane;
       const uint64_t m = __ballot(i < nk && (i % kVoxTile) < n[u] && p[u] <= thr);
-      if (i0 < nk) {
-        if (lane == 0) kb[i0 >> 5] = (uint32_t)m;
-        if (lane == 32 && i0 + 32 < nk) kb[(i0 >> 5) + 1] = (uint32_t)(m >> 32);
-      }
+      if ((lane & 31) == u) wv = lane < 32 ? (uint32_t)m : (uint32_t)(m >> 32);
     }
+    const uint32_t i0 = base + (uint32_t)(lane & 31) * kFinBlock;  // the slots of this lane's word
+    if (i0 < nk && (lane < 32 || i0 + 32 < nk)) kb[(i0 >> 5) + (uint32_t)(lane >> 5)] = wv;
   }
   __syncthreads();
   // 4. kept voxels before each flag word

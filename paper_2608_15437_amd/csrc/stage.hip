@@ -25,7 +25,7 @@ namespace {
 
 constexpr int kMaxRois = 1024;
 constexpr int kLdsFirst = kMaxRois * 2;  // chunk starts of up to kLdsFirst - 1 frames in the rectangles' LDS
-constexpr int kStageCellsPerThread = 2;
+constexpr int kStageCellsPerThread = 2;  // cells per thread when the ROIs fit one word
 
 // Conservative cell rectangle [x0, x1] x [y0, y1] of one ROI; empty when x0 > x1.
 __device__ void roi_cell_rect(const Config& c, const mmbev_roi_t& r, int16_t* out) {
@@ -192,6 +192,7 @@ __device__ void open_call(const Config& c, uint32_t* s_tmp, uint32_t* s_first, i
 __global__ __launch_bounds__(kBlock) void stage_kernel(Config c) {
   __shared__ __align__(16) int16_t s_rect[kMaxRois][4];
   __shared__ uint32_t s_tmp[kWaves];
+  __shared__ uint32_t s_word[kBlock];
   __shared__ int32_t s_bad;
   const int tid = threadIdx.x;
   const int b = blockIdx.y;
@@ -207,27 +208,23 @@ __global__ __launch_bounds__(kBlock) void stage_kernel(Config c) {
   for (int j = tid; j < n; j += kBlock) roi_cell_rect(c, c.rois[r0 + j], s_rect[j]);
   __syncthreads();
 
-  // cells: each thread owns kStageCellsPerThread cells at a time and walks
-  // the frame's ROI rectangles once for all of them
-  const int32_t stride = (int32_t)(gridDim.x - 1) * kBlock;  // without the opening column
-  const int64_t cell_words = (int64_t)c.ncells * c.W;
-  for (int32_t g0 = (int32_t)blockIdx.x * kBlock + tid; g0 < c.ncells; g0 += stride * kStageCellsPerThread) {
-    int32_t cx[kStageCellsPerThread], cy[kStageCellsPerThread];
-    uint32_t any[kStageCellsPerThread];
-#pragma unroll
-    for (int i = 0; i < kStageCellsPerThread; ++i) {
-      const int32_t cell = g0 + i * stride;
-      cx[i] = cell % c.ncx;
-      cy[i] = cell < c.ncells ? cell / c.ncx : 0x7fff;  // rows past the grid match no rectangle
-      any[i] = 0;
-    }
-    for (int w = 0; w < c.W; ++w) {
+  const int32_t ncol = (int32_t)gridDim.x - 1;  // without the opening column
+  if (c.W == 1) {  // uniform
+    // one ROI word: each thread owns kStageCellsPerThread cells at a time
+    // and walks the frame's ROI rectangles once for all of them
+    const int32_t stride = ncol * kBlock;
+    for (int32_t g0 = (int32_t)blockIdx.x * kBlock + tid; g0 < c.ncells; g0 += stride * kStageCellsPerThread) {
+      int32_t cx[kStageCellsPerThread], cy[kStageCellsPerThread];
       uint32_t word[kStageCellsPerThread];
 #pragma unroll
-      for (int i = 0; i < kStageCellsPerThread; ++i) word[i] = 0;
-      const int kn = min(32, n - w * 32);
-      for (int k = 0; k < kn; ++k) {
-        const int16_t* rc = s_rect[w * 32 + k];  // same address in every lane
+      for (int i = 0; i < kStageCellsPerThread; ++i) {
+        const int32_t cell = g0 + i * stride;
+        cx[i] = cell % c.ncx;
+        cy[i] = cell < c.ncells ? cell / c.ncx : 0x7fff;  // rows past the grid match no rectangle
+        word[i] = 0;
+      }
+      for (int k = 0; k < n; ++k) {
+        const int16_t* rc = s_rect[k];  // same address in every lane
         const int32_t x0 = rc[0], x1 = rc[1], y0 = rc[2], y1 = rc[3];
 #pragma unroll
         for (int i = 0; i < kStageCellsPerThread; ++i)
@@ -236,19 +233,39 @@ __global__ __launch_bounds__(kBlock) void stage_kernel(Config c) {
 #pragma unroll
       for (int i = 0; i < kStageCellsPerThread; ++i) {
         const int32_t cell = g0 + i * stride;
-        if (cell < c.ncells) c.cellmask[(int64_t)b * cell_words + (int64_t)cell * c.W + w] = word[i];
-        any[i] |= word[i];
+        if (cell < c.ncells) c.cellmask[(int64_t)b * c.ncells + cell] = word[i];
       }
     }
-    if (c.W > 1)
-#pragma unroll
-      for (int i = 0; i < kStageCellsPerThread; ++i) {
-        const int32_t cell = g0 + i * stride;
-        if (cell < c.ncells) c.cellany[(int64_t)b * c.ncells + cell] = any[i];
+  } else {
+    // several ROI words: one (cell, word) per thread, the workgroup's cells
+    // whole (cpw cells of W words), so that a cell's any-word is an OR in LDS
+    const int32_t W = c.W;
+    const int32_t cpw = max(kBlock / W, 1);
+    const int64_t cell_words = (int64_t)c.ncells * W;
+    const int32_t wl = tid % W;
+    const int32_t knw = min(32, n - wl * 32);
+    for (int32_t cell0 = (int32_t)blockIdx.x * cpw; cell0 < c.ncells; cell0 += ncol * cpw) {
+      const int32_t cell = cell0 + tid / W;
+      const bool active = tid < cpw * W && cell < c.ncells;
+      const int32_t cx = cell % c.ncx, cy = active ? cell / c.ncx : 0x7fff;  // rows past the grid match no rectangle
+      uint32_t word = 0;
+      for (int k = 0; k < knw; ++k) {
+        const int16_t* rc = s_rect[wl * 32 + k];
+        word |= (cx >= rc[0] && cx <= rc[1] && cy >= rc[2] && cy <= rc[3]) ? 1u << k : 0u;
       }
+      if (active) c.cellmask[(int64_t)b * cell_words + (int64_t)cell * W + wl] = word;
+      s_word[tid] = active ? word : 0u;
+      __syncthreads();
+      if (tid < cpw && cell0 + tid < c.ncells) {
+        uint32_t any = 0;
+        for (int32_t w = 0; w < W; ++w) any |= s_word[tid * W + w];
+        c.cellany[(int64_t)b * c.ncells + cell0 + tid] = any;
+      }
+      __syncthreads();
+    }
   }
   // budget masks: one thread per (sweep, word)
-  for (int32_t e = (int32_t)blockIdx.x * kBlock + tid; e < c.S * c.W; e += stride) {
+  for (int32_t e = (int32_t)blockIdx.x * kBlock + tid; e < c.S * c.W; e += ncol * kBlock) {
     const int32_t s = e / c.W, w = e % c.W;
     uint32_t word = 0;
     const int kn = min(32, n - w * 32);
@@ -273,10 +290,12 @@ __global__ void copy_fault_kernel(const WsHeader* h, int32_t* out) {
 }  // namespace
 
 hipError_t launch_stage(const Config& c, hipStream_t st) {
-  // a few workgroups per frame, each thread covering several cells
-  const int64_t work = std::max<int64_t>((int64_t)c.ncells, (int64_t)c.S * c.W);
-  const int gx = (int)std::min<int64_t>(
-      std::max<int64_t>(1, (work + kBlock * kStageCellsPerThread - 1) / (kBlock * kStageCellsPerThread)), 64);
+  // per frame, at most 64 workgroups plus the opening column: with one ROI
+  // word, kStageCellsPerThread cells per thread; with several, kBlock / W
+  // whole cells per workgroup (one word per thread)
+  const int64_t cpw = c.W == 1 ? (int64_t)kBlock * kStageCellsPerThread : std::max<int64_t>(kBlock / c.W, 1);
+  const int64_t work = std::max<int64_t>(((int64_t)c.ncells + cpw - 1) / cpw, ((int64_t)c.S * c.W + kBlock - 1) / kBlock);
+  const int gx = (int)std::min<int64_t>(std::max<int64_t>(1, work), 64);
   hipLaunchKernelGGL(stage_kernel, dim3(gx + 1, c.B), dim3(kBlock), 0, st, c);
   return hipGetLastError();
 }

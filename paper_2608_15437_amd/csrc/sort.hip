@@ -90,6 +90,8 @@ template <bool kLds>
 __global__ __launch_bounds__(kSegBlock) void segments_kernel(Config c) {
   __shared__ uint32_t s_tmp[kSegWaves];
   __shared__ uint32_t s_fstart[kLds ? kSegLdsFrames + 1 : 1];  // frame starts
+  __shared__ uint32_t s_sfirst[kLds ? kSegLdsFrames + 1 : 1];  // first pair chunk of every frame
+  __shared__ uint32_t s_tfirst[kLds ? kSegLdsFrames + 1 : 1];  // first voxel tile of every frame
   __shared__ int32_t s_last;
   WsHeader* h = c.hdr;
   const int tid = threadIdx.x;
@@ -160,66 +162,77 @@ __global__ __launch_bounds__(kSegBlock) void segments_kernel(Config c) {
   __syncthreads();
   if (lds)
     for (int g = tid; g <= c.B; g += kSegBlock) c.fstart[g] = s_fstart[g];
-  // pair chunks, frame by frame: at most kMaxFrameChunks per frame, of
-  // frame_chunk_pairs pairs (whole kSortTile multiples; the last one of a
-  // frame shorter)
+  // pair chunks (at most kMaxFrameChunks per frame, of frame_chunk_pairs
+  // pairs: whole kSortTile multiples, the last one of a frame shorter) and
+  // voxel tiles (kVoxTile sorted pairs, the last one of a frame shorter):
+  // the frames' counts scanned into their first indices, then every chunk
+  // and tile written by its own thread (its frame found by a search over
+  // the first indices: the last frame whose first index is at most its own)
   const int per = (c.B + kSegBlock - 1) / kSegBlock;
   const int b0 = tid * per;
-  uint32_t mine = 0;
+  uint32_t mine = 0, mine_vt = 0;
   for (int j = 0; j < per; ++j) {
     const int b = b0 + j;
     if (b < c.B) {
       const uint32_t n = fstart[b + 1] - fstart[b];
       mine += (n + frame_chunk_pairs(n) - 1) / frame_chunk_pairs(n);
+      mine_vt += (n + kVoxTile - 1) / kVoxTile;
     }
   }
-  uint32_t total;
+  uint32_t total, total_vt;
   uint32_t run = block_exclusive_scan<kSegWaves>(mine, s_tmp, total);
-  const uint32_t cap = (uint32_t)c.schunk_max;  // never reached: the bound holds for any K <= N
-  if (tid == 0) c.schunk_first[c.B] = min(total, cap);
-  for (int j = 0; j < per; ++j) {
-    const int b = b0 + j;
-    if (b < c.B) {
-      const uint32_t f0 = fstart[b], f1 = fstart[b + 1];
-      const uint32_t CH = frame_chunk_pairs(f1 - f0);
-      const uint32_t n = (f1 - f0 + CH - 1) / CH;
-      const uint32_t k0 = min(run, cap), k1 = min(run + n, cap);
-      c.schunk_first[b] = k0;
-      for (uint32_t k = k0; k < k1; ++k) {
-        const uint32_t lo = f0 + (k - run) * CH;
-        c.schunk[k] = make_uint4(lo, min(lo + CH, f1), (uint32_t)b, f0);
-        c.schunk_frame[k] = make_uint2(k0, k1);
-      }
-      run += n;
-    }
-  }
-  // voxel tiles: frame by frame, kVoxTile sorted pairs each (the last one
-  // of a frame shorter)
-  uint32_t mine_vt = 0;
-  for (int j = 0; j < per; ++j) {
-    const int b = b0 + j;
-    if (b < c.B) mine_vt += (fstart[b + 1] - fstart[b] + kVoxTile - 1) / kVoxTile;
-  }
-  uint32_t total_vt;
   uint32_t run_vt = block_exclusive_scan<kSegWaves>(mine_vt, s_tmp, total_vt);
-  const uint32_t cap_vt = (uint32_t)c.vtile_max;  // never reached: the bound holds for any K <= N
+  const uint32_t cap = (uint32_t)c.schunk_max;  // never reached: the bound holds for any K <= N
+  const uint32_t cap_vt = (uint32_t)c.vtile_max;
+  const uint32_t nsc = min(total, cap), nvt = min(total_vt, cap_vt);
+  uint32_t* sfirst = kLds ? s_sfirst : c.schunk_first;
+  uint32_t* tfirst = kLds ? s_tfirst : c.vt_first;
   for (int j = 0; j < per; ++j) {
     const int b = b0 + j;
     if (b < c.B) {
-      const uint32_t f0 = fstart[b], f1 = fstart[b + 1];
-      const uint32_t n = (f1 - f0 + kVoxTile - 1) / kVoxTile;
-      c.vt_first[b] = min(run_vt, cap_vt);
-      for (uint32_t t = run_vt; t < min(run_vt + n, cap_vt); ++t) {
-        const uint32_t lo = f0 + (t - run_vt) * kVoxTile;
-        c.vtile[t] = make_uint4(lo, min(lo + kVoxTile, f1), (uint32_t)b, f0);
-      }
-      run_vt += n;
+      const uint32_t n = fstart[b + 1] - fstart[b];
+      sfirst[b] = min(run, cap);
+      tfirst[b] = min(run_vt, cap_vt);
+      run += (n + frame_chunk_pairs(n) - 1) / frame_chunk_pairs(n);
+      run_vt += (n + kVoxTile - 1) / kVoxTile;
     }
   }
   if (tid == 0) {
-    h->schunks = min(total, cap);
-    c.vt_first[c.B] = min(total_vt, cap_vt);
-    h->vtiles = min(total_vt, cap_vt);
+    sfirst[c.B] = nsc;
+    tfirst[c.B] = nvt;
+  }
+  __syncthreads();
+  auto frame_of = [&](const uint32_t* first, uint32_t k) -> int32_t {
+    int32_t lo = 0, hi = c.B - 1;
+    while (lo < hi) {
+      const int32_t mid = (lo + hi + 1) >> 1;
+      if (first[mid] <= k) lo = mid; else hi = mid - 1;
+    }
+    return lo;
+  };
+  for (uint32_t k = tid; k < nsc; k += kSegBlock) {
+    const int32_t b = frame_of(sfirst, k);
+    const uint32_t f0 = fstart[b], f1 = fstart[b + 1];
+    const uint32_t CH = frame_chunk_pairs(f1 - f0);
+    const uint32_t k0 = sfirst[b], k1 = sfirst[b + 1];
+    const uint32_t lo = f0 + (k - k0) * CH;
+    c.schunk[k] = make_uint4(lo, min(lo + CH, f1), (uint32_t)b, f0);
+    c.schunk_frame[k] = make_uint2(k0, k1);
+  }
+  for (uint32_t t = tid; t < nvt; t += kSegBlock) {
+    const int32_t b = frame_of(tfirst, t);
+    const uint32_t f0 = fstart[b], f1 = fstart[b + 1];
+    const uint32_t lo = f0 + (t - tfirst[b]) * kVoxTile;
+    c.vtile[t] = make_uint4(lo, min(lo + kVoxTile, f1), (uint32_t)b, f0);
+  }
+  if (kLds)
+    for (int g = tid; g <= c.B; g += kSegBlock) {
+      c.schunk_first[g] = s_sfirst[g];
+      c.vt_first[g] = s_tfirst[g];
+    }
+  if (tid == 0) {
+    h->schunks = nsc;
+    h->vtiles = nvt;
     h->kept = K;
   }
 }

@@ -130,11 +130,13 @@ def test_edge_cases(gpu_lib):
     check(gpu_lib, empty_mid, label="empty middle frame", desc=wl.roi_desc)
 
 
-@pytest.mark.parametrize("frames", [2047, 2100])
+@pytest.mark.parametrize("frames", [2047, 2100, 4100])
 def test_many_small_frames(gpu_lib, frames):
     """Frame counts on both sides of the stage's LDS copy of the chunk starts
     (up to 2,047 frames; beyond, each frame's thread writes its filter
-    workgroups' frame itself), with every seventh frame emptied."""
+    workgroups' frame itself) and of the segments' per-frame tables in LDS
+    (up to 4,096 frames; beyond, in the workspace), with every seventh frame
+    emptied."""
     wl = synth.small(51, frames=frames, beams=2, azimuths=16, sweeps=1, rois=4)
     c = case_from_workload(wl)
     fo = c.frame_offsets

@@ -246,12 +246,20 @@ __global__ __launch_bounds__(kSegBlock) void segments_kernel(Config c) {
 // The reads of a chunk's kept points stay close together (kept points come
 // in runs).
 constexpr int kCompactItems = 4;
+constexpr int kCompactSmallChunk = 1024;  // chunks of at most this many points: two-wave workgroups
 
-__global__ __launch_bounds__(kBlock) void compact_kernel(Config c, uint32_t* kout) {
-  static_assert(kChunkWords <= kBlock, "one bitmap word per thread");
+// kCompactBlock threads (a chunk's bitmap is at most 128 words, one per
+// thread): two waves for small chunks (measured: an 8-frame batch of
+// 256-point chunks 24 -> 18.7 us), four for large ones (a 128-frame batch of
+// 2,816-point chunks 55 -> 64 us with two).
+template <int kCompactBlock>
+
+__global__ __launch_bounds__(kCompactBlock) void compact_kernel(Config c, uint32_t* kout) {
+  constexpr int kCompactWaves = kCompactBlock / 64;
+  static_assert(kChunkWords <= kCompactBlock, "one bitmap word per thread");
   extern __shared__ float s_pose[];  // [S][12]
   __shared__ uint16_t s_list[kMaxChunkPoints];  // kept point offsets in the chunk, ascending
-  __shared__ uint32_t s_tmp[kWaves];
+  __shared__ uint32_t s_tmp[kCompactWaves];
   const int tid = threadIdx.x;
   const uint32_t k = blockIdx.x;
   // the chunk's table entries and bitmap (one word per thread) load together
@@ -266,37 +274,38 @@ __global__ __launch_bounds__(kBlock) void compact_kernel(Config c, uint32_t* kou
   const int C = c.C, RW = c.rec_words;
   // the frame's poses: loaded now, stored to LDS once the list is built, so
   // that their loads overlap the listing
-  constexpr int kPoseRegs = (255 * 12 + kBlock - 1) / kBlock;
+  constexpr int kPoseRegs = 4;  // the first 4 * kCompactBlock pose floats in registers; the rest after the listing
   const int np = c.S * 12;
   float pv[kPoseRegs];
 #pragma unroll
   for (int u = 0; u < kPoseRegs; ++u) {
-    const int e = tid + u * kBlock;
+    const int e = tid + u * kCompactBlock;
     pv[u] = e < np ? c.poses[(int64_t)b * np + e] : 0.0f;
   }
   // the bitmap's set bits listed at each word's rank
   uint32_t total;
-  uint32_t r = block_exclusive_scan((uint32_t)__popc(word), s_tmp, total);
+  uint32_t r = block_exclusive_scan<kCompactWaves>((uint32_t)__popc(word), s_tmp, total);
   while (word) {
     s_list[r++] = (uint16_t)(32 * tid + __builtin_ctz(word));
     word &= word - 1u;
   }
 #pragma unroll
   for (int u = 0; u < kPoseRegs; ++u)
-    if (tid + u * kBlock < np) s_pose[tid + u * kBlock] = pv[u];
+    if (tid + u * kCompactBlock < np) s_pose[tid + u * kCompactBlock] = pv[u];
+  for (int e = tid + kPoseRegs * kCompactBlock; e < np; e += kCompactBlock) s_pose[e] = c.poses[(int64_t)b * np + e];
   __syncthreads();
   const uint32_t n = min(total, cnt);  // equal unless the workspace was corrupted
-  for (uint32_t base = 0; base < n; base += kBlock * kCompactItems) {
+  for (uint32_t base = 0; base < n; base += kCompactBlock * kCompactItems) {
     uint32_t pi[kCompactItems], sw[kCompactItems];
     float v[kCompactItems][8];
 #pragma unroll
     for (int u = 0; u < kCompactItems; ++u) {
-      const uint32_t t = base + u * kBlock + tid;
+      const uint32_t t = base + u * kCompactBlock + tid;
       pi[u] = t < n ? min(lo + (uint32_t)s_list[t], (uint32_t)c.N - 1u) : 0u;
     }
 #pragma unroll
     for (int u = 0; u < kCompactItems; ++u) {  // all point loads of the batch in flight together
-      const bool ok = base + u * kBlock + tid < n;
+      const bool ok = base + u * kCompactBlock + tid < n;
       const uint32_t i = pi[u];
       sw[u] = ok ? min((uint32_t)c.sweep[i], (uint32_t)c.S - 1u) : 0u;
 #pragma unroll
@@ -304,7 +313,7 @@ __global__ __launch_bounds__(kBlock) void compact_kernel(Config c, uint32_t* kou
     }
 #pragma unroll
     for (int u = 0; u < kCompactItems; ++u) {
-      const uint32_t t = base + u * kBlock + tid;
+      const uint32_t t = base + u * kCompactBlock + tid;
       if (t < n) {
         const uint32_t q = dst + t;
         float px, py, pz;
@@ -533,7 +542,10 @@ hipError_t launch_segments(const Config& c, hipStream_t st) {
 
 hipError_t launch_compact(const Config& c, uint32_t* kout, hipStream_t st) {
   const size_t lds = (size_t)c.S * 12 * sizeof(float);
-  hipLaunchKernelGGL(compact_kernel, dim3(c.fchunk_max), dim3(kBlock), lds, st, c, kout);
+  if (c.fchunk_points <= kCompactSmallChunk)
+    hipLaunchKernelGGL(compact_kernel<128>, dim3(c.fchunk_max), dim3(128), lds, st, c, kout);
+  else
+    hipLaunchKernelGGL(compact_kernel<kBlock>, dim3(c.fchunk_max), dim3(kBlock), lds, st, c, kout);
   return hipGetLastError();
 }
 

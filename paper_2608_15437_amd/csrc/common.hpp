@@ -214,11 +214,21 @@ __device__ __forceinline__ int32_t frame_of_chunk(const uint32_t* first, int32_t
 }
 
 // Pairs per chunk of a frame of n kept pairs: at most kMaxFrameChunks
-// chunks, each a whole number of scatter tiles.
-__device__ __forceinline__ uint32_t frame_chunk_pairs(uint32_t n) {
+// chunks, each a whole number of scatter tiles, at least min_tiles of them.
+__device__ __forceinline__ uint32_t frame_chunk_pairs(uint32_t n, uint32_t min_tiles) {
   uint32_t ch = (n + kMaxFrameChunks - 1) / kMaxFrameChunks;
   ch = (ch + kSortTile - 1) / kSortTile * kSortTile;
-  return max(ch, (uint32_t)kSortTile);
+  return max(ch, min_tiles * (uint32_t)kSortTile);
+}
+
+// Scatter tiles per pair chunk at least: one, unless the call's chunks (at
+// most K / (tiles * kSortTile) + B) would not all fit one round of the
+// scatter's resident workgroups; then as many as make them fit (at most 8).
+__device__ __forceinline__ uint32_t chunk_min_tiles(uint32_t K, int32_t B) {
+  constexpr uint32_t kResident = kScatterPerCu * kCus;
+  if ((uint32_t)B >= kResident) return 1u;
+  const uint32_t room = (kResident - (uint32_t)B) * (uint32_t)kSortTile;
+  return min(max((K + room - 1) / room, 1u), 8u);
 }
 
 // Point frame offset b clamped into [0, N].

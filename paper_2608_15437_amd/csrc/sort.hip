@@ -168,6 +168,7 @@ __global__ __launch_bounds__(kSegBlock) void segments_kernel(Config c) {
   // the frames' counts scanned into their first indices, then every chunk
   // and tile written by its own thread (its frame found by a search over
   // the first indices: the last frame whose first index is at most its own)
+  const uint32_t mt = chunk_min_tiles(K, c.B);
   const int per = (c.B + kSegBlock - 1) / kSegBlock;
   const int b0 = tid * per;
   uint32_t mine = 0, mine_vt = 0;
@@ -175,7 +176,7 @@ __global__ __launch_bounds__(kSegBlock) void segments_kernel(Config c) {
     const int b = b0 + j;
     if (b < c.B) {
       const uint32_t n = fstart[b + 1] - fstart[b];
-      mine += (n + frame_chunk_pairs(n) - 1) / frame_chunk_pairs(n);
+      mine += (n + frame_chunk_pairs(n, mt) - 1) / frame_chunk_pairs(n, mt);
       mine_vt += (n + kVoxTile - 1) / kVoxTile;
     }
   }
@@ -193,7 +194,7 @@ __global__ __launch_bounds__(kSegBlock) void segments_kernel(Config c) {
       const uint32_t n = fstart[b + 1] - fstart[b];
       sfirst[b] = min(run, cap);
       tfirst[b] = min(run_vt, cap_vt);
-      run += (n + frame_chunk_pairs(n) - 1) / frame_chunk_pairs(n);
+      run += (n + frame_chunk_pairs(n, mt) - 1) / frame_chunk_pairs(n, mt);
       run_vt += (n + kVoxTile - 1) / kVoxTile;
     }
   }
@@ -213,7 +214,7 @@ __global__ __launch_bounds__(kSegBlock) void segments_kernel(Config c) {
   for (uint32_t k = tid; k < nsc; k += kSegBlock) {
     const int32_t b = frame_of(sfirst, k);
     const uint32_t f0 = fstart[b], f1 = fstart[b + 1];
-    const uint32_t CH = frame_chunk_pairs(f1 - f0);
+    const uint32_t CH = frame_chunk_pairs(f1 - f0, mt);
     const uint32_t k0 = sfirst[b], k1 = sfirst[b + 1];
     const uint32_t lo = f0 + (k - k0) * CH;
     c.schunk[k] = make_uint4(lo, min(lo + CH, f1), (uint32_t)b, f0);

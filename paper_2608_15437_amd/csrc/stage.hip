@@ -88,6 +88,26 @@ __device__ __forceinline__ uint32_t frame_chunks(uint32_t n, uint32_t P) {
 __device__ void open_call(const Config& c, uint32_t* s_tmp, uint32_t* s_first, int32_t* s_bad) {
   const int tid = threadIdx.x;
   WsHeader* h = c.hdr;
+  // the offsets checked (every load of an iteration unconditional, at
+  // clamped indices, so that they take one round trip together; frame tid's
+  // point offsets kept for the chunk count when every thread owns one frame)...
+  int32_t bad = 0;
+  int64_t own0 = 0, own1 = 0;
+  for (int f = tid; f <= c.B; f += kBlock) {
+    const int fn = min(f + 1, c.B);
+    const int64_t o = c.frame_off[f], on = c.frame_off[fn];
+    const int32_t ro = c.roi_off[f], rn = c.roi_off[fn];
+    if (f == tid) {
+      own0 = o;
+      own1 = on;
+    }
+    if (f == 0 && o != 0) bad |= MMBEV_FAULT_POINT_OFFSETS;
+    if (f == c.B && o != (int64_t)c.N) bad |= MMBEV_FAULT_POINT_OFFSETS;
+    if (f < c.B && on < o) bad |= MMBEV_FAULT_POINT_OFFSETS;
+    if (f == 0 && ro != 0) bad |= MMBEV_FAULT_ROI_OFFSETS;
+    if (f == c.B && ro != c.R) bad |= MMBEV_FAULT_ROI_OFFSETS;
+    if (f < c.B && (rn < ro || rn - ro > c.max_rois)) bad |= MMBEV_FAULT_ROI_OFFSETS;
+  }
   if (tid == 0) {
     h->fault = 0;
     h->epoch = h->epoch + 1;
@@ -97,23 +117,8 @@ __device__ void open_call(const Config& c, uint32_t* s_tmp, uint32_t* s_first, i
     h->any_capped = 0;
     *s_bad = 0;
   }
-  // the cleared fault word is visible to every wave before any of them ORs
-  // an offset fault into it
+  // ...and ORed in once the cleared fault word is visible to every wave
   __syncthreads();
-  int32_t bad = 0;
-  for (int f = tid; f <= c.B; f += kBlock) {
-    const int64_t o = c.frame_off[f];
-    if (f == 0 && o != 0) bad |= MMBEV_FAULT_POINT_OFFSETS;
-    if (f == c.B && o != (int64_t)c.N) bad |= MMBEV_FAULT_POINT_OFFSETS;
-    if (f < c.B && c.frame_off[f + 1] < o) bad |= MMBEV_FAULT_POINT_OFFSETS;
-    const int32_t ro = c.roi_off[f];
-    if (f == 0 && ro != 0) bad |= MMBEV_FAULT_ROI_OFFSETS;
-    if (f == c.B && ro != c.R) bad |= MMBEV_FAULT_ROI_OFFSETS;
-    if (f < c.B) {
-      const int32_t rn = c.roi_off[f + 1];
-      if (rn < ro || rn - ro > c.max_rois) bad |= MMBEV_FAULT_ROI_OFFSETS;
-    }
-  }
   if (bad) {
     raise_fault(h, bad);
     atomicOr(s_bad, bad);
@@ -127,13 +132,23 @@ __device__ void open_call(const Config& c, uint32_t* s_tmp, uint32_t* s_first, i
   const uint32_t P = (uint32_t)c.fchunk_points;
   const int per = (c.B + kBlock - 1) / kBlock;
   const int b0 = tid * per;
+  // points of frame b: from the offsets already loaded when per == 1 (b = tid)
+  auto frame_points = [&](int b) -> uint32_t {
+    int64_t o0 = own0, o1 = own1;
+    if (per != 1) {  // uniform
+      const int bb = min(b, c.B - 1);  // loads unconditional, at a clamped frame
+      o0 = c.frame_off[bb];
+      o1 = c.frame_off[bb + 1];
+    }
+    const uint32_t f0 = (uint32_t)min(max(o0, (int64_t)0), (int64_t)c.N);
+    const uint32_t f1 = max((uint32_t)min(max(o1, (int64_t)0), (int64_t)c.N), f0);
+    return f1 - f0;
+  };
   uint32_t mine = 0;
   for (int j = 0; j < per; ++j) {
     const int b = b0 + j;
-    if (b < c.B && !no_points) {
-      const uint32_t f0 = point_offset(c, b), f1 = max(point_offset(c, b + 1), f0);
-      mine += frame_chunks(f1 - f0, P);
-    }
+    const uint32_t np = frame_points(b);
+    if (b < c.B && !no_points) mine += frame_chunks(np, P);
   }
   uint32_t total;
   uint32_t run = block_exclusive_scan(mine, s_tmp, total);
@@ -143,11 +158,11 @@ __device__ void open_call(const Config& c, uint32_t* s_tmp, uint32_t* s_first, i
   const int32_t G = c.filter_grid;
   for (int j = 0; j < per; ++j) {
     const int b = b0 + j;
+    const uint32_t np = frame_points(b);
     if (b < c.B) {
       const uint32_t first = min(run, cap);
       c.fchunk_first[b] = first;
-      const uint32_t f0 = point_offset(c, b), f1 = max(point_offset(c, b + 1), f0);
-      run += no_points ? 0u : frame_chunks(f1 - f0, P);
+      run += no_points ? 0u : frame_chunks(np, P);
       if (in_lds) {
         s_first[b] = first;
       } else {
@@ -269,8 +284,14 @@ __global__ __launch_bounds__(kBlock) void stage_kernel(Config c) {
     const int32_t s = e / c.W, w = e % c.W;
     uint32_t word = 0;
     const int kn = min(32, n - w * 32);
-    for (int k = 0; k < kn; ++k)
-      if ((int32_t)c.budget[r0 + w * 32 + k] > s) word |= 1u << k;
+    if (kn > 0) {
+      uint32_t bv[32];
+#pragma unroll
+      for (int k = 0; k < 32; ++k) bv[k] = c.budget[r0 + w * 32 + min(k, kn - 1)];  // together, then used
+#pragma unroll
+      for (int k = 0; k < 32; ++k)
+        if (k < kn && (int32_t)bv[k] > s) word |= 1u << k;
+    }
     c.budgetmask[((int64_t)b * c.S + s) * c.W + w] = word;
   }
 }

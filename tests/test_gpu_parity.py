@@ -227,6 +227,20 @@ def test_throughput_batch_full_size(gpu_lib):
     check(gpu_lib, case_from_workload(wl), label="c2x16", desc=wl.roi_desc)
 
 
+def test_throughput_batch_128_frames_two_tile_chunks(gpu_lib):
+    """The benchmark's own 128-frame call (2.75M kept pairs): one-tile pair
+    chunks would overflow one round of the scatter's resident workgroups, so
+    the chunks take at least two tiles; every output checked against the
+    oracle."""
+    wl = synth.throughput(128)
+    vz, exp = check(gpu_lib, case_from_workload(wl), label="c2x128", desc=wl.roi_desc)
+    h = vz.header()
+    K = int(h["kept"])
+    assert K > 2048 * (1024 - 128), K  # one-tile chunks would not fit one round of 1,024 workgroups
+    assert 0 < h["pair_chunks"] <= 1024, h
+    assert K / h["pair_chunks"] > 2048, (K, h["pair_chunks"])  # chunks longer than one 2,048-pair tile
+
+
 def _face_lattice_case(pose_rows, voxel=(0.1, 0.15, 0.3), mn=(-3.7, -2.9, -1.3), dims=(60, 40, 10)):
     """Points on voxel faces (and one ulp either side) of a non-dyadic grid,
     all inside one ROI covering the grid: the voxel index of every point is

@@ -33,7 +33,7 @@ constexpr int kSortBins = 1 << kMaxDigitBits;  // 512
 constexpr int kSortItems = 8;         // pairs per thread in a scatter tile
 constexpr int kSortTile = kBlock * kSortItems;  // 2048 pairs
 constexpr int kCountItems = 16;       // pairs per thread per batch of the count kernel
-constexpr int kMaxFrameChunks = 32;   // pair chunks of one frame at most (chunks never straddle frames)
+constexpr int kMaxFrameChunks = 64;   // pair chunks of one frame at most (chunks never straddle frames)
 constexpr int kScanItems = 16;        // items per thread in the single-workgroup scans
 constexpr int kScanTile = kBlock * kScanItems;  // 4096
 constexpr int kMeanTile = kBlock;     // one voxel per thread

@@ -283,6 +283,7 @@ __global__ __launch_bounds__(kCompactBlock) void compact_kernel(Config c, uint32
     const int e = tid + u * kCompactBlock;
     pv[u] = e < np ? c.poses[(int64_t)b * np + e] : 0.0f;
   }
+  const uint32_t fs = c.fstart[b], fe = c.fstart[b + 1];
   // the bitmap's set bits listed at each word's rank
   uint32_t total;
   uint32_t r = block_exclusive_scan<kCompactWaves>((uint32_t)__popc(word), s_tmp, total);
@@ -294,6 +295,10 @@ __global__ __launch_bounds__(kCompactBlock) void compact_kernel(Config c, uint32
   for (int u = 0; u < kPoseRegs; ++u)
     if (tid + u * kCompactBlock < np) s_pose[tid + u * kCompactBlock] = pv[u];
   for (int e = tid + kPoseRegs * kCompactBlock; e < np; e += kCompactBlock) s_pose[e] = c.poses[(int64_t)b * np + e];
+  if (fe - fs > (uint32_t)c.cap) {  // uniform: the frame may exceed the cap: its first-place bits over this chunk's places cleared
+    uint32_t* bits = c.capbits + fs / 32 + (uint32_t)b;  // the heads kernel sets them
+    for (uint32_t w = (dst - fs) / 32 + tid; w < (dst - fs + cnt + 31) / 32; w += kCompactBlock) bits[w] = 0u;
+  }
   __syncthreads();
   const uint32_t n = min(total, cnt);  // equal unless the workspace was corrupted
   for (uint32_t base = 0; base < n; base += kCompactBlock * kCompactItems) {

@@ -43,6 +43,8 @@ __global__ __launch_bounds__(kBlock) void heads_kernel(Config c, const uint32_t*
   for (uint32_t t = blockIdx.x; t < nvt; t += gridDim.x) {
     const uint4 vt = c.vtile[t];
     const uint32_t lo = vt.x, hi = vt.y, ff = vt.w;
+    const uint32_t fb = min(vt.z, (uint32_t)c.B - 1u);
+    const uint32_t fe = c.fstart[fb + 1];  // the frame's end: a frame with more pairs than max_voxels may be capped
     uint32_t key[kHeadItems], prv[kHeadItems], val[kHeadItems];
 #pragma unroll
     for (int j = 0; j < kHeadItems; ++j) {  // all loads in flight together: unconditional, at clamped indices
@@ -81,6 +83,15 @@ __global__ __launch_bounds__(kBlock) void heads_kernel(Config c, const uint32_t*
         c.hpos[slot] = lo + j * kBlock + tid;
         c.hplace[slot] = val[j];
       }
+    if (fe - ff > (uint32_t)c.cap) {  // uniform: the heads' places marked for the cap (bits cleared by the compaction)
+      uint32_t* bits = c.capbits + ff / 32 + fb;
+#pragma unroll
+      for (int j = 0; j < kHeadItems; ++j)
+        if ((m[j] >> lane) & 1u) {
+          const uint32_t q = val[j] - ff;
+          atomicOr(&bits[q >> 5], 1u << (q & 31));
+        }
+    }
     if (tid == 0) c.hcount[t] = s_total;
     __syncthreads();  // the next tile rewrites the counts
   }
@@ -169,7 +180,7 @@ __device__ void finalize_offsets(const Config& c, uint32_t* s_tmp) {
 
 struct CapLds {
   uint32_t hc[kCapLdsTiles];    // voxels of the frame's tiles
-  uint32_t area[kCapLdsWords];  // first-place bits, then kept flags and their word prefix
+  uint32_t area[kCapLdsWords];  // the first-place bits (copied from the workspace), then kept flags and their word prefix
   uint32_t tmp[kFinWaves];
   uint32_t sel;
 };
@@ -180,7 +191,8 @@ struct CapLds {
 // [fstart[b], fstart[b+1]) in order (tile after tile; slot lo + j of a tile
 // holds its voxel j when j < its voxel count): slot order restricted to the
 // voxels is key order.  The first places are marked in a bitmap over the
-// frame's places, the max_voxels-th marked place is found from a prefix of
+// frame's places (by the heads kernel, every tile's heads at once; the
+// compaction clears the frame's words), the max_voxels-th marked place is found from a prefix of
 // the words' popcounts, the kept voxels are flagged in slot order (one
 // ballot per 64 slots) and numbered by a prefix of those flag words.  The
 // tables sit in LDS when they fit, otherwise in the frame's regions of the
@@ -202,27 +214,21 @@ __device__ void cap_frame(const Config& c, int32_t b, CapLds& S, uint32_t t0, ui
   // tile's count (every pass loads at clamped slots, unconditionally, and
   // tests that afterwards, so that its loads are in flight together)
   const uint32_t nw = (nk + 31) / 32;
-  uint32_t* bits = kLds ? S.area : c.capbits + wbase;
+  // 1. the first places, marked in the workspace by the heads kernel (the
+  // compaction cleared them); copied to LDS when the tables fit there
+  const uint32_t* gbits = c.capbits + wbase;
+  if (kLds)
+    for (uint32_t base = 0; base < nw; base += kFinBlock * 8) {
+      uint32_t v[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) v[u] = gbits[min(base + u * kFinBlock + (uint32_t)tid, nw - 1u)];  // in flight together
+#pragma unroll
+      for (int u = 0; u < 8; ++u)
+        if (base + u * kFinBlock + tid < nw) S.area[base + u * kFinBlock + tid] = v[u];
+    }
+  const uint32_t* bits = kLds ? S.area : gbits;
   constexpr int kUnroll = 32;  // loads in flight per thread: one workgroup walks the whole frame
-  // 1. the first places marked
-  for (uint32_t w = tid; w < nw; w += kFinBlock) bits[w] = 0u;
-  __syncthreads();  // also: the tiles' counts are in place
-  for (uint32_t base = tid; base < nk; base += kFinBlock * kUnroll) {
-    uint32_t p[kUnroll], n[kUnroll];
-#pragma unroll
-    for (int u = 0; u < kUnroll; ++u) {  // all loads of the batch in flight together (clamped, unconditional)
-      const uint32_t i = min(base + u * kFinBlock, nk - 1u);
-      p[u] = c.hplace[fs + i];
-      n[u] = hc[i / kVoxTile];
-    }
-#pragma unroll
-    for (int u = 0; u < kUnroll; ++u) {
-      const uint32_t i = base + u * kFinBlock;
-      const uint32_t q = p[u] - fs;
-      if (i < nk && (i % kVoxTile) < n[u] && q < nk) atomicOr(&bits[q >> 5], 1u << (q & 31));
-    }
-  }
-  __syncthreads();
+  __syncthreads();  // the tiles' counts and the bits are in place
   // 2. the max_voxels-th smallest first place: thread t counts a contiguous run of words
   {
     const uint32_t per = (nw + kFinBlock - 1) / kFinBlock;

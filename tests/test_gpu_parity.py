@@ -241,6 +241,28 @@ def test_throughput_batch_128_frames_two_tile_chunks(gpu_lib):
     assert K / h["pair_chunks"] > 2048, (K, h["pair_chunks"])  # chunks longer than one 2,048-pair tile
 
 
+def test_capped_frame_tables_in_workspace(gpu_lib):
+    """A frame over max_voxels whose first-place bitmap does not fit LDS (more
+    than 16,384 words: over 524,288 kept pairs), so the cap keeps its tables
+    in the workspace: 700,000 points spread over a 256 x 256 x 16 grid, one ROI
+    over all of it, about 490,000 voxels capped to 150,000."""
+    rng = np.random.default_rng(77)
+    N = 700_000
+    mn, voxel, dims = (-25.6, -25.6, -2.0), (0.2, 0.2, 0.25), (256, 256, 16)
+    cols = [rng.uniform(mn[d], mn[d] + dims[d] * voxel[d], N) for d in range(3)]
+    feat = np.ascontiguousarray(np.stack(cols + [rng.random(N)]).astype(np.float32))
+    poses = np.array([1, 0, 0, 0, 0, 1, 0, 0, 0, 0, 1, 0], np.float32).reshape(1, 1, 12)
+    grid = dict(range_min=list(mn), voxel_size=list(voxel), dims=list(dims), max_points=4, max_voxels=150_000,
+                num_sweeps=1, num_frames=1)
+    case = Case(feat=feat, sweep_ids=np.zeros(N, np.uint8), frame_offsets=np.array([0, N]), poses=poses,
+                rois=records([[0.0, 0.0, 1.0, 0.0, 100.0, 100.0]]), roi_offsets=np.array([0, 1], np.int32),
+                budgets=np.array([1], np.uint8), grid=grid)
+    vz, exp = check(gpu_lib, case, label="cap-workspace")
+    assert int(exp["voxel_offsets"][-1]) == 150_000
+    h = vz.header()
+    assert h["kept"] > 524_288 and h["capped_voxels"] > 150_000, h
+
+
 def _face_lattice_case(pose_rows, voxel=(0.1, 0.15, 0.3), mn=(-3.7, -2.9, -1.3), dims=(60, 40, 10)):
     """Points on voxel faces (and one ulp either side) of a non-dyadic grid,
     all inside one ROI covering the grid: the voxel index of every point is

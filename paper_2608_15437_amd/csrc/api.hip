@@ -69,7 +69,7 @@ struct Plan {
   int64_t fchunk_points, fchunk_max, filter_grid, schunk_max, vtile_max, mean_grid;
   size_t off_hdr, off_cellmask, off_cellany, off_budgetmask, off_fchunk_first, off_fbits, off_fcount, off_fchunk_lo, off_fchunk_frame, off_wgframe, off_spare, off_fprefix,
       off_fstart, off_schunk_first, off_schunk, off_schunk_frame, off_cnt, off_vtile, off_vt_first, off_hcount, off_hpre, off_mtile, off_trow, off_keys[2], off_vals[2], off_rec,
-      off_hpos, off_hplace, off_capbits, off_rank, off_voxoff, total;
+      off_hpos, off_hplace, off_capbits, off_voxoff, total;
 };
 
 mmbev_status_t make_plan(const mmbev_grid_t* g, int64_t N, int32_t max_rois, int32_t C, Plan* p) {
@@ -166,7 +166,6 @@ mmbev_status_t make_plan(const mmbev_grid_t* g, int64_t N, int32_t max_rois, int
   p->off_hpos = take((size_t)n1 * 4);
   p->off_hplace = take((size_t)n1 * 4);
   p->off_capbits = take((3 * ((size_t)n1 / 32 + p->B + 1) + (size_t)p->vtile_max + 1) * 4);
-  p->off_rank = take((size_t)n1 * 4);
   p->off_voxoff = take((size_t)(p->B + 1) * 4);
   p->total = o;
   return MMBEV_OK;
@@ -345,7 +344,6 @@ mmbev_status_t voxelize(const mmbev_points_t* points, const uint8_t* sweep_ids, 
   c.hpos = (uint32_t*)(ws + p.off_hpos);
   c.hplace = (uint32_t*)(ws + p.off_hplace);
   c.capbits = (uint32_t*)(ws + p.off_capbits);
-  c.out_rank = (uint32_t*)(ws + p.off_rank);
   c.vox_off = (uint32_t*)(ws + p.off_voxoff);
   c.fchunk_points = (int32_t)p.fchunk_points;
   c.fchunk_words = (int32_t)(p.fchunk_points / 32);

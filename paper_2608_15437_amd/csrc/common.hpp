@@ -123,11 +123,11 @@ struct Config {
   // per voxel, at slot vtile[t].x + j for voxel j of tile t
   uint32_t* hpos;          // [N] first sorted pair of the voxel
   uint32_t* hplace;        // [N] its place (its first point: places follow point order)
-  uint32_t* out_rank;      // [N] row inside its frame, or ~0u (frames over the cap only)
-  uint32_t* capbits;       // frames over the cap whose tables exceed LDS: three regions of N / 32 + B + 1
-                           // words (first-place bits, kept flags, their prefix; frame b from word
-                           // fstart[b] / 32 + b of each), then [vtile_max] tile prefixes (frame b from
-                           // its first tile)
+  uint32_t* capbits;       // frames with more pairs than max_voxels: three regions of N / 32 + B + 1
+                           // words (first-place bits, set by the heads kernel; kept flags in slot
+                           // order; the flag words' prefix; frame b from word fstart[b] / 32 + b of
+                           // each), then [vtile_max] tiles' voxel counts (frame b from its first tile;
+                           // frames whose tables exceed LDS)
   uint32_t* vox_off;       // [B+1] voxels of the frames before b
   // sizes
   int32_t fchunk_points;   // points per filter chunk (a multiple of kWaveTile, <= kMaxChunkPoints)

@@ -13,7 +13,8 @@
 //           frame's voxels and its output offsets (at most max_voxels rows
 //           per frame); workgroup 1 + b: frame b, if it has more than
 //           max_voxels voxels, keeps the max_voxels voxels whose first
-//           point comes first and numbers them in key order (out_rank);
+//           point comes first and flags them in key order, with the flag
+//           words' prefix (from which the mean numbers them);
 // mean   -- blocks of kMeanTile consecutive voxels (grid-stride), one
 //           thread per voxel: its tile, its output row, and the mean of its first max_points points from
 //           their compact records (x', y', z' of Eq. 6 and the raw
@@ -279,8 +280,12 @@ __device__ void cap_frame(const Config& c, int32_t b, CapLds& S, uint32_t t0, ui
     if (i0 < nk && (lane < 32 || i0 + 32 < nk)) kb[(i0 >> 5) + (uint32_t)(lane >> 5)] = wv;
   }
   __syncthreads();
-  // 4. kept voxels before each flag word
+  // 4. kept voxels before each flag word, both tables written to the
+  // frame's regions of the workspace: the mean numbers a kept voxel from its
+  // flag word and that word's prefix
   {
+    uint32_t* gkb = c.capbits + words + wbase;
+    uint32_t* gwp = c.capbits + 2 * words + wbase;
     const uint32_t per = (nw + kFinBlock - 1) / kFinBlock;
     const uint32_t w0 = min(tid * per, nw), w1 = min(w0 + per, nw);
     uint32_t mine = 0;
@@ -288,28 +293,10 @@ __device__ void cap_frame(const Config& c, int32_t b, CapLds& S, uint32_t t0, ui
     uint32_t all;
     uint32_t run = block_exclusive_scan<kFinWaves>(mine, S.tmp, all);
     for (uint32_t w = w0; w < w1; ++w) {
-      wp[w] = run;
-      run += (uint32_t)__popc(kb[w]);
-    }
-  }
-  __syncthreads();
-  // 5. the kept voxels' rows inside the frame
-  for (uint32_t base = tid; base < nk; base += kFinBlock * 8) {
-    uint32_t n[8], word[8], pre[8];
-#pragma unroll
-    for (int u = 0; u < 8; ++u) {  // clamped, unconditional reads
-      const uint32_t i = min(base + u * kFinBlock, nk - 1u);
-      n[u] = hc[i / kVoxTile];
-      word[u] = kb[i >> 5];
-      pre[u] = wp[i >> 5];
-    }
-#pragma unroll
-    for (int u = 0; u < 8; ++u) {
-      const uint32_t i = base + u * kFinBlock;
-      if (i < nk && (i % kVoxTile) < n[u]) {  // slot i holds a voxel
-        const bool keep = (word[u] >> (i & 31)) & 1u;
-        c.out_rank[fs + i] = keep ? pre[u] + (uint32_t)__popc(word[u] & ((1u << (i & 31)) - 1u)) : 0xffffffffu;
-      }
+      const uint32_t x = kb[w];
+      gwp[w] = run;
+      if (kLds) gkb[w] = x;
+      run += (uint32_t)__popc(x);
     }
   }
 }
@@ -357,7 +344,7 @@ __global__ __launch_bounds__(kFinBlock) void fincap_kernel(Config c) {
 constexpr int kMeanBatch = 2;  // records in flight per thread: more cost occupancy (VGPRs), fewer add round trips
 
 template <int RW>
-__global__ __launch_bounds__(kBlock) void mean_kernel(Config c, const uint32_t* keys, const uint32_t* vals) {
+__global__ __launch_bounds__(kBlock, 6) void mean_kernel(Config c, const uint32_t* keys, const uint32_t* vals) {
   extern __shared__ uint32_t sm[];
   __shared__ int64_t s_row0;
   WsHeader* h = c.hdr;
@@ -394,7 +381,15 @@ __global__ __launch_bounds__(kBlock) void mean_kernel(Config c, const uint32_t* 
     const int32_t b = (int32_t)min(vt.z, (uint32_t)c.B - 1u);
     const uint32_t slot = vt.x + j, sl = min(slot, K - 1u);
     // the voxel's heads (and, for a frame over the cap, its rank)
-    const uint32_t rank = c.out_rank[sl];
+    // a voxel of a frame over the cap: kept when its slot's flag is set, its
+    // row inside the frame the kept voxels before it (the flag word's prefix
+    // and the word's lower bits); the words of other frames are not read
+    // for anything (clamped loads)
+    const size_t cwords = (size_t)c.N / 32 + (size_t)c.B + 1;
+    const uint32_t rel = slot - min(vt.w, slot);
+    const size_t cw = min((size_t)(vt.w / 32 + (uint32_t)b + (rel >> 5)), cwords - 1);
+    const uint32_t kw = c.capbits[cwords + cw], pw = c.capbits[2 * cwords + cw];
+    const uint32_t rank = (kw >> (rel & 31)) & 1u ? pw + (uint32_t)__popc(kw & ((1u << (rel & 31)) - 1u)) : 0xffffffffu;
     const int64_t ob = c.out_voxel_offsets[b];
     const uint32_t s0 = min(c.hpos[sl], K - 1u);
     const uint32_t q0 = c.hplace[sl];  // the first point's place (the head's value)

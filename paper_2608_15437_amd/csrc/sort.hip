@@ -291,19 +291,11 @@ __global__ __launch_bounds__(kCompactBlock) void compact_kernel(Config c, uint32
     s_list[r++] = (uint16_t)(32 * tid + __builtin_ctz(word));
     word &= word - 1u;
   }
-#pragma unroll
-  for (int u = 0; u < kPoseRegs; ++u)
-    if (tid + u * kCompactBlock < np) s_pose[tid + u * kCompactBlock] = pv[u];
-  for (int e = tid + kPoseRegs * kCompactBlock; e < np; e += kCompactBlock) s_pose[e] = c.poses[(int64_t)b * np + e];
-  if (fe - fs > (uint32_t)c.cap) {  // uniform: the frame may exceed the cap: its first-place bits over this chunk's places cleared
-    uint32_t* bits = c.capbits + fs / 32 + (uint32_t)b;  // the heads kernel sets them
-    for (uint32_t w = (dst - fs) / 32 + tid; w < (dst - fs + cnt + 31) / 32; w += kCompactBlock) bits[w] = 0u;
-  }
-  __syncthreads();
+  __syncthreads();  // the list is complete
   const uint32_t n = min(total, cnt);  // equal unless the workspace was corrupted
-  for (uint32_t base = 0; base < n; base += kCompactBlock * kCompactItems) {
-    uint32_t pi[kCompactItems], sw[kCompactItems];
-    float v[kCompactItems][8];
+  uint32_t pi[kCompactItems], sw[kCompactItems];
+  float v[kCompactItems][8];
+  auto load_batch = [&](uint32_t base) {
 #pragma unroll
     for (int u = 0; u < kCompactItems; ++u) {
       const uint32_t t = base + u * kCompactBlock + tid;
@@ -317,6 +309,8 @@ __global__ __launch_bounds__(kCompactBlock) void compact_kernel(Config c, uint32
 #pragma unroll
       for (int f = 0; f < 8; ++f) v[u][f] = (ok && f < C) ? c.feat[(int64_t)f * c.stride + i] : 0.0f;
     }
+  };
+  auto finish_batch = [&](uint32_t base) {
 #pragma unroll
     for (int u = 0; u < kCompactItems; ++u) {
       const uint32_t t = base + u * kCompactBlock + tid;
@@ -338,6 +332,23 @@ __global__ __launch_bounds__(kCompactBlock) void compact_kernel(Config c, uint32
         if (RW > 8) rr[2] = make_uint4(__float_as_uint(v[u][7]), 0u, 0u, 0u);
       }
     }
+  };
+  // the first batch's point loads go out before the poses are stored (the
+  // poses' loads were issued before the listing), so the two round trips overlap
+  load_batch(0u);
+#pragma unroll
+  for (int u = 0; u < kPoseRegs; ++u)
+    if (tid + u * kCompactBlock < np) s_pose[tid + u * kCompactBlock] = pv[u];
+  for (int e = tid + kPoseRegs * kCompactBlock; e < np; e += kCompactBlock) s_pose[e] = c.poses[(int64_t)b * np + e];
+  if (fe - fs > (uint32_t)c.cap) {  // uniform: the frame may exceed the cap: its first-place bits over this chunk's places cleared
+    uint32_t* bits = c.capbits + fs / 32 + (uint32_t)b;  // the heads kernel sets them
+    for (uint32_t w = (dst - fs) / 32 + tid; w < (dst - fs + cnt + 31) / 32; w += kCompactBlock) bits[w] = 0u;
+  }
+  __syncthreads();  // the poses are in LDS
+  finish_batch(0u);
+  for (uint32_t base = kCompactBlock * kCompactItems; base < n; base += kCompactBlock * kCompactItems) {
+    load_batch(base);
+    finish_batch(base);
   }
 }
 

@@ -171,17 +171,27 @@ __device__ __forceinline__ void raise_fault(WsHeader* h, int32_t bits) {
   __hip_atomic_fetch_or(&h->fault, bits, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
+// Inclusive prefix sum over the 64 lanes of a wave (every lane active), in
+// DPP moves instead of LDS permutes: shifts by 1, 2, 4 and 8 lanes inside
+// each row of 16 lanes (a lane whose source lies before its row adds 0),
+// then the last lane of rows 0 and 2 added to rows 1 and 3, then lane 31 to
+// rows 2 and 3 (rows left out of a move's row mask add 0).
+__device__ __forceinline__ uint32_t wave_inclusive_sum(uint32_t x) {
+  x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x111, 0xf, 0xf, false);  // row_shr:1
+  x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x112, 0xf, 0xf, false);  // row_shr:2
+  x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x114, 0xf, 0xf, false);  // row_shr:4
+  x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x118, 0xf, 0xf, false);  // row_shr:8
+  x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x142, 0xa, 0xf, false);  // row_bcast:15
+  x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x143, 0xc, 0xf, false);  // row_bcast:31
+  return x;
+}
+
 // Exclusive prefix over the workgroup (WAVES wave64s, all threads must
 // call); s_tmp holds WAVES words of LDS.  Returns the prefix, sets total.
 template <int WAVES = kWaves>
 __device__ __forceinline__ uint32_t block_exclusive_scan(uint32_t v, uint32_t* s_tmp, uint32_t& total) {
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  uint32_t x = v;
-#pragma unroll
-  for (int d = 1; d < 64; d <<= 1) {
-    uint32_t y = __shfl_up(x, d, 64);
-    if (lane >= d) x += y;
-  }
+  const uint32_t x = wave_inclusive_sum(v);
   if (lane == 63) s_tmp[wave] = x;
   __syncthreads();
   uint32_t wpre = 0, tot = 0;

@@ -67,12 +67,7 @@ __global__ __launch_bounds__(kBlock) void heads_kernel(Config c, const uint32_t*
     __syncthreads();
     if (wave == 0) {  // exclusive scan of the kHeadItems * kWaves counts
       const uint32_t x = lane < kHeadItems * kWaves ? s_off[lane] : 0u;
-      uint32_t y = x;
-#pragma unroll
-      for (int d = 1; d < 64; d <<= 1) {
-        const uint32_t z = __shfl_up(y, d, 64);
-        if (lane >= d) y += z;
-      }
+      const uint32_t y = wave_inclusive_sum(x);
       if (lane < kHeadItems * kWaves) s_off[lane] = y - x;
       if (lane == 63) s_total = y;
     }

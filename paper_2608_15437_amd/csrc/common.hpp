@@ -39,7 +39,7 @@ constexpr int kScanTile = kBlock * kScanItems;  // 4096
 constexpr int kMeanTile = kBlock;     // one voxel per thread
 constexpr int kVoxTile = 2048;        // sorted pairs of a voxel tile (the heads, cap and mean kernels' unit)
 constexpr int kCus = 256;            // compute units of the device (8 XCDs x 32)
-constexpr int kScatterPerCu = 4;     // scatter workgroups resident per CU (its 106 VGPRs allow four)
+constexpr int kScatterPerCu = 4;     // scatter workgroups resident per CU (its launch bounds hold it to 128 VGPRs: four)
 constexpr int kCountGrid = 2048;     // count workgroups (eight per CU)
 
 // Workspace header: per-call counters, rewritten by the first kernels of a call.

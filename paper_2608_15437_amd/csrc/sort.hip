@@ -55,29 +55,6 @@ __device__ __forceinline__ uint64_t match_digit(uint32_t dig, bool valid) {
   return __ballot(valid) & ~(((uint64_t)dhi << 32) | dlo);
 }
 
-// Exclusive scan of n <= kSortBins values in LDS (in may alias out); all
-// threads must call.  Returns the total.
-__device__ __forceinline__ uint32_t scan_bins(const uint32_t* in, uint32_t* out, int n, uint32_t* s_tmp) {
-  constexpr int kPer = kSortBins / kBlock;
-  const int first = threadIdx.x * kPer;
-  uint32_t v[kPer], sum = 0;
-#pragma unroll
-  for (int j = 0; j < kPer; ++j) {
-    v[j] = first + j < n ? in[first + j] : 0u;
-    sum += v[j];
-  }
-  uint32_t total;
-  uint32_t run = block_exclusive_scan(sum, s_tmp, total);
-#pragma unroll
-  for (int j = 0; j < kPer; ++j)
-    if (first + j < n) {
-      out[first + j] = run;
-      run += v[j];
-    }
-  __syncthreads();
-  return total;
-}
-
 constexpr int kSegBlock = 1024;  // threads of the segments kernel
 constexpr int kSegWaves = kSegBlock / 64;
 constexpr int kSegLdsFrames = 4096;  // frame starts kept in LDS up to this many frames
@@ -390,12 +367,10 @@ __global__ __launch_bounds__(kBlock) void count_kernel(Config c, int pass, const
 }
 
 struct ScatterLds {
-  uint32_t run[kSortBins];             // next output position of every digit
-  uint32_t local_off[kSortBins + 1];   // the tile's digits: exclusive prefix, then the tile's size
-  uint32_t keys[kSortTile];            // the tile reordered by digit
-  uint32_t vals[kSortTile];
-  uint32_t wave_cnt[kWaves][kSortBins];  // a wave's digit counts, then its offsets
-  uint32_t scan_tmp[kWaves];
+  uint32_t pos[kSortBins];             // per digit: output position of the tile's pair i of that digit, less i
+  uint2 kv[kSortTile];                 // the tile reordered by digit: (key, value)
+  uint32_t wave_cnt[kWaves][kSortBins];  // a wave's digit counts, then its first place in the reordered tile
+  uint32_t scan_tmp[2][kWaves];
 };
 
 __device__ __forceinline__ void load_sort_tile(const uint32_t* kin, const uint32_t* vin, uint32_t base, uint32_t hi,
@@ -409,11 +384,16 @@ __device__ __forceinline__ void load_sort_tile(const uint32_t* kin, const uint32
   }
 }
 
-__global__ __launch_bounds__(kBlock) void scatter_kernel(Config c, int pass, const uint32_t* kin, const uint32_t* vin,
+// Thread t owns digits 2t and 2t + 1 (kSortBins == 2 * kBlock) in every
+// per-digit step: the count rows (8-byte loads), the tile's digit totals,
+// the scans and the output positions, which it keeps in registers from
+// tile to tile.
+__global__ __launch_bounds__(kBlock, kScatterPerCu) void scatter_kernel(Config c, int pass, const uint32_t* kin, const uint32_t* vin,
                                                          uint32_t* kout, uint32_t* vout) {
   __shared__ ScatterLds L;
   static_assert(sizeof(ScatterLds) <= 160 * 1024 / kScatterPerCu, "workgroups per CU");
   static_assert(kSortBins == 2 * kBlock, "two digits per thread");
+  constexpr int kRows = 8;  // count rows in flight together
   const int tid = threadIdx.x;
   const int lane = tid & 63, wave = tid >> 6;
   WsHeader* h = c.hdr;
@@ -421,6 +401,8 @@ __global__ __launch_bounds__(kBlock) void scatter_kernel(Config c, int pass, con
   const int shift = pass * c.dbits;
   const uint32_t nbins = 1u << c.dbits;
   const uint32_t mask = nbins - 1u;
+  const uint32_t e0 = 2u * (uint32_t)tid;  // this thread's digits e0 and e0 + 1
+  const bool d0 = e0 < nbins, d1 = e0 + 1u < nbins;
   // chunks dealt to the XCDs in contiguous blocks: a frame's chunks share
   // one L2, where their neighbouring digit runs merge into whole lines and
   // their count rows are read once; a grid of resident size walks them
@@ -432,43 +414,22 @@ __global__ __launch_bounds__(kBlock) void scatter_kernel(Config c, int pass, con
     const uint32_t lo = ch.x, hi = ch.y;
     uint32_t key[kSortItems], val[kSortItems], nkey[kSortItems], nval[kSortItems];
     if (lo < hi) load_sort_tile(kin, vin, lo, hi, key, val);
-    // base of every digit: frame start + the frame's smaller digits + this
-    // digit in the frame's earlier chunks, from the count rows of the frame's
-    // chunks (at most kMaxFrameChunks rows; thread t: digits t and t + kBlock)
-    {
-      constexpr int kRows = 8;
-      const uint32_t k0 = fc.x, k1 = max(fc.y, k0);
-      uint32_t pre0 = 0, pre1 = 0, tot0 = 0, tot1 = 0;
-      for (uint32_t kk = k0; kk < k1; kk += kRows) {
-        uint32_t x0[kRows], x1[kRows];
+    // the first kRows count rows of the frame's chunks (at most
+    // kMaxFrameChunks rows) go out now and are summed after the first
+    // tile is ranked: digit bases = frame start + the frame's smaller
+    // digits + this digit in the frame's earlier chunks
+    const uint32_t k0 = fc.x, k1 = max(fc.y, k0);
+    uint2 x[kRows];
 #pragma unroll
-        for (int u = 0; u < kRows; ++u) {  // the rows' loads in flight together
-          const bool ok = kk + u < k1;
-          x0[u] = ok ? c.cnt[(int64_t)(kk + u) * kSortBins + tid] : 0u;
-          x1[u] = ok ? c.cnt[(int64_t)(kk + u) * kSortBins + kBlock + tid] : 0u;
-        }
-#pragma unroll
-        for (int u = 0; u < kRows; ++u) {
-          if (kk + u < k) {
-            pre0 += x0[u];
-            pre1 += x1[u];
-          }
-          tot0 += x0[u];
-          tot1 += x1[u];
-        }
-      }
-      L.run[tid] = tot0;
-      L.run[kBlock + tid] = tot1;
-      __syncthreads();
-      scan_bins(L.run, L.run, (int)nbins, L.scan_tmp);
-      if ((uint32_t)tid < nbins) L.run[tid] += ch.w + pre0;
-      if ((uint32_t)(kBlock + tid) < nbins) L.run[kBlock + tid] += ch.w + pre1;
-    }
+    for (int u = 0; u < kRows; ++u)
+      x[u] = k0 + u < k1 ? *reinterpret_cast<const uint2*>(c.cnt + (int64_t)(k0 + u) * kSortBins + e0) : make_uint2(0u, 0u);
+    uint32_t run0 = 0, run1 = 0;  // output position of the next pair of digit e0, e0 + 1
     for (uint32_t base = lo; base < hi; base += kSortTile) {
+      const bool first = base == lo;
       const bool more = base + kSortTile < hi;
       if (more) load_sort_tile(kin, vin, base + kSortTile, hi, nkey, nval);
       for (uint32_t e = tid; e < kWaves * kSortBins; e += kBlock) (&L.wave_cnt[0][0])[e] = 0u;
-      __syncthreads();
+      __syncthreads();  // also: the previous tile's reads of pos and kv are done
       uint32_t rank[kSortItems];
       bool valid[kSortItems];
 #pragma unroll
@@ -480,62 +441,108 @@ __global__ __launch_bounds__(kBlock) void scatter_kernel(Config c, int pass, con
       // it.  A wave's LDS operations complete in issue order, so the rounds'
       // atomics go out back to back; each lane then takes its group's count
       // from the group's first lane (bpermute) and adds its place in the group.
-      uint64_t mm[kSortItems];
-      uint32_t old[kSortItems];
+      {
+        uint32_t old[kSortItems];
 #pragma unroll
-      for (int r = 0; r < kSortItems; ++r) {
-        mm[r] = match_digit(dig(r), valid[r]);
-        old[r] = 0u;
-        if (valid[r] && count_below(mm[r]) == 0) old[r] = atomicAdd(&L.wave_cnt[wave][dig(r)], (uint32_t)__popcll(mm[r]));
-      }
-#pragma unroll
-      for (int r = 0; r < kSortItems; ++r) {
-        const int first = mm[r] != 0ull ? __builtin_ctzll(mm[r]) : 0;
-        const uint32_t prior = (uint32_t)__builtin_amdgcn_ds_bpermute(first << 2, (int)old[r]);
-        rank[r] = prior + count_below(mm[r]);
-      }
-      __syncthreads();
-      // per digit: each wave's offset inside the tile's run of that digit, and the run's size
-      for (uint32_t e = tid; e < nbins; e += kBlock) {
-        uint32_t t = 0;
-#pragma unroll
-        for (int w = 0; w < kWaves; ++w) {
-          const uint32_t x = L.wave_cnt[w][e];
-          L.wave_cnt[w][e] = t;
-          t += x;
+        for (int r = 0; r < kSortItems; ++r) {
+          const uint64_t mm = match_digit(dig(r), valid[r]);
+          const uint32_t below = count_below(mm);
+          rank[r] = (uint32_t)(mm != 0ull ? __builtin_ctzll(mm) : 0) << 8 | below;  // the group's first lane, the lane's place
+          old[r] = 0u;
+          if (valid[r] && below == 0) old[r] = atomicAdd(&L.wave_cnt[wave][dig(r)], (uint32_t)__popcll(mm));
         }
-        L.local_off[e] = t;
-      }
-      __syncthreads();
-      const uint32_t ntile = scan_bins(L.local_off, L.local_off, (int)nbins, L.scan_tmp);
-      if (tid == 0) L.local_off[nbins] = ntile;
 #pragma unroll
-      for (int r = 0; r < kSortItems; ++r) {
-        if (valid[r]) {
-          const uint32_t lp = L.local_off[dig(r)] + L.wave_cnt[wave][dig(r)] + rank[r];
-          L.keys[lp] = key[r];
-          L.vals[lp] = val[r];
+        for (int r = 0; r < kSortItems; ++r) {
+          const uint32_t prior = (uint32_t)__builtin_amdgcn_ds_bpermute((int)(rank[r] >> 8) << 2, (int)old[r]);
+          rank[r] = prior + (rank[r] & 0xffu);
         }
       }
+      uint32_t ft0 = 0, ft1 = 0, pre0 = 0, pre1 = 0;  // the frame's totals of e0, e1 and their count in earlier chunks
+      if (first) {  // uniform
+        for (uint32_t kk = k0;; kk += kRows) {
+#pragma unroll
+          for (int u = 0; u < kRows; ++u) {
+            const uint32_t a = d0 ? x[u].x : 0u, b = d1 ? x[u].y : 0u;
+            if (kk + u < k) {
+              pre0 += a;
+              pre1 += b;
+            }
+            ft0 += a;
+            ft1 += b;
+          }
+          if (kk + kRows >= k1) break;
+#pragma unroll
+          for (int u = 0; u < kRows; ++u) {  // the next rows' loads in flight together
+            const uint32_t kr = kk + kRows + u;
+            x[u] = kr < k1 ? *reinterpret_cast<const uint2*>(c.cnt + (int64_t)kr * kSortBins + e0) : make_uint2(0u, 0u);
+          }
+        }
+      }
+      __syncthreads();  // the wave counts are complete
+      // per digit: the tile's count, each wave's first place inside the
+      // tile's run of that digit; one scan over the digits for the tile
+      // and, on a chunk's first tile, one for the frame's totals
+      const uint2* wc = reinterpret_cast<const uint2*>(&L.wave_cnt[0][0]);
+      uint2 cw[kWaves];
+#pragma unroll
+      for (int w = 0; w < kWaves; ++w) cw[w] = wc[w * (kSortBins / 2) + tid];
+      uint32_t t0 = 0, t1 = 0;
+#pragma unroll
+      for (int w = 0; w < kWaves; ++w) {
+        t0 += cw[w].x;
+        t1 += cw[w].y;
+      }
+      const uint32_t xt = wave_inclusive_sum(t0 + t1);
+      const uint32_t xf = first ? wave_inclusive_sum(ft0 + ft1) : 0u;
+      if (lane == 63) {
+        L.scan_tmp[0][wave] = xt;
+        L.scan_tmp[1][wave] = xf;
+      }
+      __syncthreads();
+      uint32_t wt = 0, wf = 0;
+#pragma unroll
+      for (int w = 0; w < kWaves; ++w)
+        if (w < wave) {
+          wt += L.scan_tmp[0][w];
+          wf += L.scan_tmp[1][w];
+        }
+      const uint32_t lo0 = wt + xt - (t0 + t1), lo1 = lo0 + t0;  // the digits' first places in the reordered tile
+      if (first) {
+        const uint32_t fb0 = ch.w + wf + xf - (ft0 + ft1);  // frame start + the frame's smaller digits
+        run0 = fb0 + pre0;
+        run1 = fb0 + ft0 + pre1;
+      }
+      uint2* wo = reinterpret_cast<uint2*>(&L.wave_cnt[0][0]);
+      uint32_t a0 = lo0, a1 = lo1;
+#pragma unroll
+      for (int w = 0; w < kWaves; ++w) {
+        wo[w * (kSortBins / 2) + tid] = make_uint2(a0, a1);
+        a0 += cw[w].x;
+        a1 += cw[w].y;
+      }
+      *reinterpret_cast<uint2*>(&L.pos[e0]) = make_uint2(run0 - lo0, run1 - lo1);  // position of tile place i: pos + i
+      run0 += t0;
+      run1 += t1;
+      __syncthreads();
+#pragma unroll
+      for (int r = 0; r < kSortItems; ++r)
+        if (valid[r]) L.kv[L.wave_cnt[wave][dig(r)] + rank[r]] = make_uint2(key[r], val[r]);
       __syncthreads();
       const uint32_t n_in = min((uint32_t)kSortTile, hi - base);
 #pragma unroll
       for (int r = 0; r < kSortItems; ++r) {  // unrolled: the LDS reads of all rounds in flight together
         const uint32_t i = (uint32_t)(r * kBlock + tid);
         if (i < n_in) {
-          const uint32_t kv = L.keys[i];
-          const uint32_t dd = (kv >> shift) & mask;
-          const uint32_t gp = L.run[dd] + (i - L.local_off[dd]);
+          const uint2 kv = L.kv[i];
+          const uint32_t gp = L.pos[(kv.x >> shift) & mask] + i;
           if (gp < K) {  // always true when the counts match the pairs
-            kout[gp] = kv;
-            vout[gp] = L.vals[i];
+            kout[gp] = kv.x;
+            vout[gp] = kv.y;
           } else {
             raise_fault(h, MMBEV_FAULT_INTERNAL);
           }
         }
       }
-      __syncthreads();
-      for (uint32_t e = tid; e < nbins; e += kBlock) L.run[e] += L.local_off[e + 1] - L.local_off[e];
       if (more)
 #pragma unroll
         for (int r = 0; r < kSortItems; ++r) {
@@ -543,7 +550,6 @@ __global__ __launch_bounds__(kBlock) void scatter_kernel(Config c, int pass, con
           val[r] = nval[r];
         }
     }
-    __syncthreads();  // the next chunk rewrites run and local_off
   }
 }
 

@@ -19,6 +19,7 @@ constexpr int kWaveTile = 256;        // points per filter wave tile (64 lanes x
 constexpr int kWaveQueue = 128;       // candidate ring of one filter wave (power of two, >= 128)
 constexpr int kFilterDepth = 2;       // register buffers of a filter wave's tile pipeline (>= 2)
 constexpr int kFilterWaveTarget = 16384;  // filter wave chunks aimed for (a few per resident wave: balance)
+constexpr int kFilterMinWaves = 4096;     // fewest filter chunks for which two-tile chunks are taken over one-tile ones
 constexpr int kMaxChunkPoints = 4096;  // points of one filter chunk at most
 constexpr int kChunkWords = kMaxChunkPoints / 32;  // words of a chunk's kept bitmap
 constexpr int kMaxLdsFrames = 64;     // frames of one filter workgroup staged in LDS

@@ -54,6 +54,9 @@ struct alignas(256) WsHeader {
   uint32_t fchunks;           // filter chunks (points of one frame each)
   uint32_t schunks;           // pair chunks (pairs of one frame each)
   uint32_t vtiles;            // voxel tiles (kVoxTile sorted pairs of one frame each, the last one shorter)
+  uint32_t cap_ticket;        // workgroups done with the shared cap of the frame with the most pairs
+  uint32_t most_frame;        // the frame with the most pairs (the smallest index among equals)
+  uint32_t most_pairs;        // its pairs
 };
 
 // Everything a kernel needs, computed once on the host and passed by value.
@@ -185,6 +188,19 @@ __device__ __forceinline__ uint32_t wave_inclusive_sum(uint32_t x) {
   x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x142, 0xa, 0xf, false);  // row_bcast:15
   x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x143, 0xc, 0xf, false);  // row_bcast:31
   return x;
+}
+
+// Largest value over the 64 lanes of a wave (every lane active), by the
+// same DPP moves (lanes left out of a move see 0, which leaves a maximum of
+// unsigned values unchanged); the last lane's result is every lane's.
+__device__ __forceinline__ uint32_t wave_max(uint32_t x) {
+  x = max(x, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x111, 0xf, 0xf, false));  // row_shr:1
+  x = max(x, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x112, 0xf, 0xf, false));  // row_shr:2
+  x = max(x, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x114, 0xf, 0xf, false));  // row_shr:4
+  x = max(x, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x118, 0xf, 0xf, false));  // row_shr:8
+  x = max(x, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x142, 0xa, 0xf, false));  // row_bcast:15
+  x = max(x, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x143, 0xc, 0xf, false));  // row_bcast:31
+  return (uint32_t)__builtin_amdgcn_readlane((int)x, 63);
 }
 
 // Exclusive prefix over the workgroup (WAVES wave64s, all threads must

@@ -70,12 +70,16 @@ __global__ __launch_bounds__(kSegBlock) void segments_kernel(Config c) {
   __shared__ uint32_t s_sfirst[kLds ? kSegLdsFrames + 1 : 1];  // first pair chunk of every frame
   __shared__ uint32_t s_tfirst[kLds ? kSegLdsFrames + 1 : 1];  // first voxel tile of every frame
   __shared__ int32_t s_last;
+  __shared__ unsigned long long s_most;  // (pairs, ~frame) of the frame with the most pairs
   WsHeader* h = c.hdr;
   const int tid = threadIdx.x;
   const uint32_t nf = h->fchunks;
   constexpr bool lds = kLds;
   uint32_t* fstart = kLds ? s_fstart : c.fstart;
-  if (tid == 0) s_last = -1;
+  if (tid == 0) {
+    s_last = -1;
+    s_most = 0ull;
+  }
   // kept-point prefix of the filter chunks; the first chunk of a frame also
   // gives the start of that frame and of the empty frames just before it.
   // Thread t holds kScanItems consecutive chunks, read with 16-byte loads.
@@ -148,14 +152,21 @@ __global__ __launch_bounds__(kSegBlock) void segments_kernel(Config c) {
   const uint32_t mt = chunk_min_tiles(K, c.B);
   const int per = (c.B + kSegBlock - 1) / kSegBlock;
   const int b0 = tid * per;
+  unsigned long long most = 0ull;
   uint32_t mine = 0, mine_vt = 0;
   for (int j = 0; j < per; ++j) {
     const int b = b0 + j;
     if (b < c.B) {
       const uint32_t n = fstart[b + 1] - fstart[b];
       mine += (n + frame_chunk_pairs(n, mt) - 1) / frame_chunk_pairs(n, mt);
+      most = max(most, (unsigned long long)n << 32 | (uint32_t)~(uint32_t)b);
       mine_vt += (n + kVoxTile - 1) / kVoxTile;
     }
+  }
+  {  // the wave's largest (pairs, ~frame): pairs first, then the frame among those
+    const uint32_t hi = wave_max((uint32_t)(most >> 32));
+    const uint32_t lo = wave_max((uint32_t)(most >> 32) == hi ? (uint32_t)most : 0u);
+    if ((tid & 63) == 0 && hi > 0u) atomicMax(&s_most, (unsigned long long)hi << 32 | lo);  // read after the scans' barriers
   }
   uint32_t total, total_vt;
   uint32_t run = block_exclusive_scan<kSegWaves>(mine, s_tmp, total);
@@ -212,6 +223,8 @@ __global__ __launch_bounds__(kSegBlock) void segments_kernel(Config c) {
     h->schunks = nsc;
     h->vtiles = nvt;
     h->kept = K;
+    h->most_frame = ~(uint32_t)(s_most & 0xffffffffull);
+    h->most_pairs = (uint32_t)(s_most >> 32);
   }
 }
 

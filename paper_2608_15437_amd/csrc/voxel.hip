@@ -179,9 +179,26 @@ struct CapLds {
   uint32_t area[kCapLdsWords];  // the first-place bits (copied from the workspace), then kept flags and their word prefix
   uint32_t tmp[kFinWaves];
   uint32_t sel;
+  uint32_t last;                // this workgroup finished the shared cap last
 };
 
-// Workgroup 1 + b of fincap: frame b's voxel cap.  The frame keeps the
+// The frame with the most pairs (found by the segments kernel) gets
+// kCapHelpers more workgroups for its cap when it has more than max_voxels
+// voxels: its slots are flagged in
+// steps of kCapStepSlots shared out among 1 + kCapHelpers workgroups (the
+// flag pass costs one workgroup about a microsecond of vector instructions
+// per 8,000 slots), and the last one to finish, found with a ticket
+// counter that nobody waits on, numbers the flag words.
+constexpr int kCapHelpers = 15;
+constexpr uint32_t kCapStepSlots = kFinBlock * 32;
+
+// Workgroups sharing the cap of a frame with nk pairs.
+__device__ __forceinline__ uint32_t cap_share(uint32_t nk) {
+  return min((uint32_t)(1 + kCapHelpers), max((nk + kCapStepSlots - 1) / kCapStepSlots, 1u));
+}
+
+// Workgroup 1 + b of fincap (and, for the frame with the most pairs, up to
+// kCapHelpers more): frame b's voxel cap.  The frame keeps the
 // max_voxels voxels whose first place (hplace, distinct, in [fstart[b],
 // fstart[b+1])) is smallest.  Every pass runs over the frame's slots
 // [fstart[b], fstart[b+1]) in order (tile after tile; slot lo + j of a tile
@@ -197,8 +214,11 @@ struct CapLds {
 // the workspace, each pointer of one address space only, so that the
 // compiler emits LDS or global instructions rather than generic ones (whose
 // waits would also wait for the other kind).
-template <bool kLds>
-__device__ void cap_frame(const Config& c, int32_t b, CapLds& S, uint32_t t0, uint32_t nt) {
+// kShared: workgroup g of G sharing the flag pass (steps g, g + G, ...);
+// the flag words go to the workspace, and the last workgroup to finish
+// numbers them.
+template <bool kLds, bool kShared>
+__device__ void cap_frame(const Config& c, int32_t b, CapLds& S, uint32_t t0, uint32_t nt, uint32_t g, uint32_t G) {
   const int tid = threadIdx.x, lane = tid & 63;
   const uint32_t fs = c.fstart[b], nk = max(c.fstart[b + 1], fs) - fs;
   const size_t words = (size_t)c.N / 32 + (size_t)c.B + 1;  // one region of the workspace's capbits
@@ -251,9 +271,9 @@ __device__ void cap_frame(const Config& c, int32_t b, CapLds& S, uint32_t t0, ui
   __syncthreads();
   const uint32_t thr = S.sel;
   // 3. kept voxels flagged in slot order (after the marks: the area is reused)
-  uint32_t* kb = kLds ? S.area : c.capbits + words + wbase;
-  uint32_t* wp = kLds ? S.area + nw : c.capbits + 2 * words + wbase;
-  for (uint32_t base = (uint32_t)(tid & ~63); base < nk; base += kFinBlock * kUnroll) {
+  uint32_t* kb = kLds && !kShared ? S.area : c.capbits + words + wbase;
+  static_assert(kCapStepSlots == (uint32_t)kFinBlock * kUnroll, "one step of the flag pass");
+  for (uint32_t base = g * kCapStepSlots + (uint32_t)(tid & ~63); base < nk; base += G * kCapStepSlots) {
     uint32_t p[kUnroll], n[kUnroll];
 #pragma unroll
     for (int u = 0; u < kUnroll; ++u) {  // clamped, unconditional loads
@@ -274,7 +294,19 @@ __device__ void cap_frame(const Config& c, int32_t b, CapLds& S, uint32_t t0, ui
     const uint32_t i0 = base + (uint32_t)(lane & 31) * kFinBlock;  // the slots of this lane's word
     if (i0 < nk && (lane < 32 || i0 + 32 < nk)) kb[(i0 >> 5) + (uint32_t)(lane >> 5)] = wv;
   }
-  __syncthreads();
+  if (kShared) {
+    // every wave's flag words out of its caches before the ticket; only the
+    // last workgroup goes on, after an acquire, to read all of them
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
+    __syncthreads();
+    if (tid == 0)
+      S.last = __hip_atomic_fetch_add(&c.hdr->cap_ticket, 1u, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_AGENT) + 1u == G;
+    __syncthreads();
+    if (!S.last) return;  // uniform
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+  } else {
+    __syncthreads();
+  }
   // 4. kept voxels before each flag word, both tables written to the
   // frame's regions of the workspace: the mean numbers a kept voxel from its
   // flag word and that word's prefix
@@ -290,7 +322,7 @@ __device__ void cap_frame(const Config& c, int32_t b, CapLds& S, uint32_t t0, ui
     for (uint32_t w = w0; w < w1; ++w) {
       const uint32_t x = kb[w];
       gwp[w] = run;
-      if (kLds) gkb[w] = x;
+      if (kLds && !kShared) gkb[w] = x;
       run += (uint32_t)__popc(x);
     }
   }
@@ -303,7 +335,14 @@ __global__ __launch_bounds__(kFinBlock) void fincap_kernel(Config c) {
     finalize_offsets(c, S.tmp);
     return;
   }
-  const int32_t b = (int32_t)blockIdx.x - 1;
+  // workgroups 1 + B ...: helpers of the frame with the most pairs, which
+  // leave at once unless that frame has more than one step of slots and
+  // more than max_voxels pairs (a frame has no more voxels than pairs)
+  const bool helper = (int32_t)blockIdx.x > c.B;
+  const uint32_t most = c.hdr->most_pairs;
+  const int32_t most_frame = (int32_t)min(c.hdr->most_frame, (uint32_t)c.B - 1u);
+  if (helper && (most <= (uint32_t)c.cap || (uint32_t)blockIdx.x - (uint32_t)c.B >= cap_share(most))) return;
+  const int32_t b = helper ? most_frame : (int32_t)blockIdx.x - 1;
   const uint32_t nvt = c.hdr->vtiles;
   const uint32_t t0 = min(c.vt_first[b], nvt), t1 = max(min(c.vt_first[b + 1], nvt), t0);
   const uint32_t nt = t1 - t0;
@@ -311,6 +350,8 @@ __global__ __launch_bounds__(kFinBlock) void fincap_kernel(Config c) {
   const size_t words = (size_t)c.N / 32 + (size_t)c.B + 1;
   const uint32_t fs = c.fstart[b], nk = max(c.fstart[b + 1], fs) - fs;
   const bool lds = nt <= (uint32_t)kCapLdsTiles && 2 * ((nk + 31) / 32) <= (uint32_t)kCapLdsWords;
+  const uint32_t g = helper ? (uint32_t)blockIdx.x - (uint32_t)c.B : 0u;
+  if (g >= cap_share(nk) || (helper && nk <= (uint32_t)c.cap)) return;  // uniform: a helper with no work
   uint32_t mine = 0;
   for (uint32_t i = tid; i < nt; i += kFinBlock) {
     const uint32_t v = c.hcount[t0 + i];
@@ -320,10 +361,19 @@ __global__ __launch_bounds__(kFinBlock) void fincap_kernel(Config c) {
   uint32_t total;
   (void)block_exclusive_scan<kFinWaves>(mine, S.tmp, total);
   if (total <= (uint32_t)c.cap) return;  // uniform
-  if (lds)
-    cap_frame<true>(c, b, S, t0, nt);
-  else
-    cap_frame<false>(c, b, S, t0, nt);
+  // shared with helpers when this is the frame with the most pairs and it
+  // has more than one step of slots (the helpers decide the same way)
+  const uint32_t G = b == most_frame ? cap_share(nk) : 1u;
+  if (G > 1) {
+    if (lds)
+      cap_frame<true, true>(c, b, S, t0, nt, g, G);
+    else
+      cap_frame<false, true>(c, b, S, t0, nt, g, G);
+  } else if (lds) {
+    cap_frame<true, false>(c, b, S, t0, nt, 0u, 1u);
+  } else {
+    cap_frame<false, false>(c, b, S, t0, nt, 0u, 1u);
+  }
 }
 
 // Blocks of kMeanTile consecutive voxels (grid-stride), one thread per
@@ -512,7 +562,7 @@ hipError_t launch_heads(const Config& c, const uint32_t* keys, const uint32_t* v
 }
 
 hipError_t launch_fincap(const Config& c, hipStream_t st) {
-  hipLaunchKernelGGL(fincap_kernel, dim3(1 + c.B), dim3(kFinBlock), 0, st, c);
+  hipLaunchKernelGGL(fincap_kernel, dim3(1 + c.B + kCapHelpers), dim3(kFinBlock), 0, st, c);
   return hipGetLastError();
 }
 

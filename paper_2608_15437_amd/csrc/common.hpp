@@ -44,6 +44,9 @@ constexpr int kScatterPerCu = 4;     // scatter workgroups resident per CU (its 
 constexpr int kCountGrid = 2048;     // count workgroups (eight per CU)
 
 // Workspace header: per-call counters, rewritten by the first kernels of a call.
+constexpr int kMaxCapSteps = 48;             // steps of a cap shared by several workgroups (frames of up to 1.5M pairs)
+constexpr uint32_t kCapStepSlots = 1u << 15;  // slots of one step of a cap's flag pass
+
 struct alignas(256) WsHeader {
   int32_t fault;              // byte 0: MMBEV_FAULT_* bits of the last call
   uint32_t epoch;             // call counter
@@ -54,10 +57,11 @@ struct alignas(256) WsHeader {
   uint32_t fchunks;           // filter chunks (points of one frame each)
   uint32_t schunks;           // pair chunks (pairs of one frame each)
   uint32_t vtiles;            // voxel tiles (kVoxTile sorted pairs of one frame each, the last one shorter)
-  uint32_t cap_ticket;        // workgroups done with the shared cap of the frame with the most pairs
   uint32_t most_frame;        // the frame with the most pairs (the smallest index among equals)
   uint32_t most_pairs;        // its pairs
+  uint32_t cap_steps[kMaxCapSteps];  // that frame's kept voxels per kCapStepSlots slots, when its cap is shared
 };
+static_assert(sizeof(WsHeader) == 256, "one 256-byte header");
 
 // Everything a kernel needs, computed once on the host and passed by value.
 struct Config {

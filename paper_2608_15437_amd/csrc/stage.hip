@@ -115,7 +115,6 @@ __device__ void open_call(const Config& c, uint32_t* s_tmp, uint32_t* s_first, i
     h->voxels = 0;
     h->capped_voxels = 0;
     h->any_capped = 0;
-    h->cap_ticket = 0;
     *s_bad = 0;
   }
   // ...and ORed in once the cleared fault word is visible to every wave

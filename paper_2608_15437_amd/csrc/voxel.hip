@@ -179,22 +179,24 @@ struct CapLds {
   uint32_t area[kCapLdsWords];  // the first-place bits (copied from the workspace), then kept flags and their word prefix
   uint32_t tmp[kFinWaves];
   uint32_t sel;
-  uint32_t last;                // this workgroup finished the shared cap last
 };
 
 // The frame with the most pairs (found by the segments kernel) gets
 // kCapHelpers more workgroups for its cap when it has more than max_voxels
-// voxels: its slots are flagged in
-// steps of kCapStepSlots shared out among 1 + kCapHelpers workgroups (the
-// flag pass costs one workgroup about a microsecond of vector instructions
-// per 8,000 slots), and the last one to finish, found with a ticket
-// counter that nobody waits on, numbers the flag words.
+// voxels: its slots are flagged in steps of kCapStepSlots dealt out among
+// the workgroups (the flag pass costs one workgroup about a microsecond of
+// vector instructions per 8,000 slots); each step's flag words are
+// numbered inside the step, and the step's kept count goes to the header,
+// whose prefix the mean adds.  No workgroup reads another's results.
 constexpr int kCapHelpers = 15;
-constexpr uint32_t kCapStepSlots = kFinBlock * 32;
+constexpr int kWordBatch = 8;  // a thread's bitmap or flag words loaded together
+static_assert(kCapStepSlots == kFinBlock * 32, "one step of the flag pass: 32 ballots per wave");
 
-// Workgroups sharing the cap of a frame with nk pairs.
+// Workgroups sharing the cap of a frame with nk pairs (one unless it takes
+// more than one step and at most kMaxCapSteps).
 __device__ __forceinline__ uint32_t cap_share(uint32_t nk) {
-  return min((uint32_t)(1 + kCapHelpers), max((nk + kCapStepSlots - 1) / kCapStepSlots, 1u));
+  const uint32_t steps = (nk + kCapStepSlots - 1) / kCapStepSlots;
+  return steps > (uint32_t)kMaxCapSteps ? 1u : min((uint32_t)(1 + kCapHelpers), max(steps, 1u));
 }
 
 // Workgroup 1 + b of fincap (and, for the frame with the most pairs, up to
@@ -214,9 +216,9 @@ __device__ __forceinline__ uint32_t cap_share(uint32_t nk) {
 // the workspace, each pointer of one address space only, so that the
 // compiler emits LDS or global instructions rather than generic ones (whose
 // waits would also wait for the other kind).
-// kShared: workgroup g of G sharing the flag pass (steps g, g + G, ...);
-// the flag words go to the workspace, and the last workgroup to finish
-// numbers them.
+// kShared: workgroup g of G sharing the flag pass (steps g, g + G, ...):
+// the flag words go to the workspace, numbered inside their step, and each
+// step's kept count to the header.
 template <bool kLds, bool kShared>
 __device__ void cap_frame(const Config& c, int32_t b, CapLds& S, uint32_t t0, uint32_t nt, uint32_t g, uint32_t G) {
   const int tid = threadIdx.x, lane = tid & 63;
@@ -250,7 +252,14 @@ __device__ void cap_frame(const Config& c, int32_t b, CapLds& S, uint32_t t0, ui
     const uint32_t per = (nw + kFinBlock - 1) / kFinBlock;
     const uint32_t w0 = min(tid * per, nw), w1 = min(w0 + per, nw);
     uint32_t mine = 0;
-    for (uint32_t w = w0; w < w1; ++w) mine += (uint32_t)__popc(bits[w]);
+    for (uint32_t w = w0; w < w1; w += kWordBatch) {
+      uint32_t x[kWordBatch];
+#pragma unroll
+      for (int u = 0; u < kWordBatch; ++u) x[u] = bits[min(w + u, nw - 1u)];  // in flight together
+#pragma unroll
+      for (int u = 0; u < kWordBatch; ++u)
+        if (w + u < w1) mine += (uint32_t)__popc(x[u]);
+    }
     uint32_t all;
     const uint32_t before = block_exclusive_scan<kFinWaves>(mine, S.tmp, all);
     const uint32_t want = (uint32_t)c.cap;
@@ -273,7 +282,8 @@ __device__ void cap_frame(const Config& c, int32_t b, CapLds& S, uint32_t t0, ui
   // 3. kept voxels flagged in slot order (after the marks: the area is reused)
   uint32_t* kb = kLds && !kShared ? S.area : c.capbits + words + wbase;
   static_assert(kCapStepSlots == (uint32_t)kFinBlock * kUnroll, "one step of the flag pass");
-  for (uint32_t base = g * kCapStepSlots + (uint32_t)(tid & ~63); base < nk; base += G * kCapStepSlots) {
+  for (uint32_t step = g; step * kCapStepSlots < nk; step += G) {  // uniform: every wave takes every step
+    const uint32_t base = step * kCapStepSlots + (uint32_t)(tid & ~63);
     uint32_t p[kUnroll], n[kUnroll];
 #pragma unroll
     for (int u = 0; u < kUnroll; ++u) {  // clamped, unconditional loads
@@ -292,21 +302,24 @@ __device__ void cap_frame(const Config& c, int32_t b, CapLds& S, uint32_t t0, ui
       if ((lane & 31) == u) wv = lane < 32 ? (uint32_t)m : (uint32_t)(m >> 32);
     }
     const uint32_t i0 = base + (uint32_t)(lane & 31) * kFinBlock;  // the slots of this lane's word
-    if (i0 < nk && (lane < 32 || i0 + 32 < nk)) kb[(i0 >> 5) + (uint32_t)(lane >> 5)] = wv;
+    const bool has = i0 < nk && (lane < 32 || i0 + 32 < nk);
+    if (has) kb[(i0 >> 5) + (uint32_t)(lane >> 5)] = wv;
+    if (kShared) {
+      // the step's flag words numbered inside the step: word 2 * wave +
+      // 32 * (lane % 32) + lane / 32 of the step's 1,024 (in LDS, then one
+      // per thread in word order)
+      S.area[2u * (uint32_t)(tid >> 6) + 32u * (uint32_t)(lane & 31) + (uint32_t)(lane >> 5)] = has ? (uint32_t)__popc(wv) : 0u;
+      __syncthreads();
+      const uint32_t x = S.area[tid];
+      uint32_t kept;
+      const uint32_t before = block_exclusive_scan<kFinWaves>(x, S.tmp, kept);  // its barriers also free S.area
+      const uint32_t w = step * (kCapStepSlots / 32) + (uint32_t)tid;
+      if (w < nw) c.capbits[2 * words + wbase + w] = before;
+      if (tid == 0) c.hdr->cap_steps[step] = kept;
+    }
   }
-  if (kShared) {
-    // every wave's flag words out of its caches before the ticket; only the
-    // last workgroup goes on, after an acquire, to read all of them
-    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
-    __syncthreads();
-    if (tid == 0)
-      S.last = __hip_atomic_fetch_add(&c.hdr->cap_ticket, 1u, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_AGENT) + 1u == G;
-    __syncthreads();
-    if (!S.last) return;  // uniform
-    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
-  } else {
-    __syncthreads();
-  }
+  if (kShared) return;  // the steps' words are numbered
+  __syncthreads();
   // 4. kept voxels before each flag word, both tables written to the
   // frame's regions of the workspace: the mean numbers a kept voxel from its
   // flag word and that word's prefix
@@ -316,14 +329,27 @@ __device__ void cap_frame(const Config& c, int32_t b, CapLds& S, uint32_t t0, ui
     const uint32_t per = (nw + kFinBlock - 1) / kFinBlock;
     const uint32_t w0 = min(tid * per, nw), w1 = min(w0 + per, nw);
     uint32_t mine = 0;
-    for (uint32_t w = w0; w < w1; ++w) mine += (uint32_t)__popc(kb[w]);
+    for (uint32_t w = w0; w < w1; w += kWordBatch) {
+      uint32_t x[kWordBatch];
+#pragma unroll
+      for (int u = 0; u < kWordBatch; ++u) x[u] = kb[min(w + u, nw - 1u)];  // in flight together
+#pragma unroll
+      for (int u = 0; u < kWordBatch; ++u)
+        if (w + u < w1) mine += (uint32_t)__popc(x[u]);
+    }
     uint32_t all;
     uint32_t run = block_exclusive_scan<kFinWaves>(mine, S.tmp, all);
-    for (uint32_t w = w0; w < w1; ++w) {
-      const uint32_t x = kb[w];
-      gwp[w] = run;
-      if (kLds && !kShared) gkb[w] = x;
-      run += (uint32_t)__popc(x);
+    for (uint32_t w = w0; w < w1; w += kWordBatch) {
+      uint32_t x[kWordBatch];
+#pragma unroll
+      for (int u = 0; u < kWordBatch; ++u) x[u] = kb[min(w + u, nw - 1u)];
+#pragma unroll
+      for (int u = 0; u < kWordBatch; ++u)
+        if (w + u < w1) {
+          gwp[w + u] = run;
+          if (kLds) gkb[w + u] = x[u];
+          run += (uint32_t)__popc(x[u]);
+        }
     }
   }
 }
@@ -392,6 +418,7 @@ template <int RW>
 __global__ __launch_bounds__(kBlock, 6) void mean_kernel(Config c, const uint32_t* keys, const uint32_t* vals) {
   extern __shared__ uint32_t sm[];
   __shared__ int64_t s_row0;
+  __shared__ uint32_t s_step[kMaxCapSteps];  // a shared cap's kept voxels before each step
   WsHeader* h = c.hdr;
   const int tid = threadIdx.x;
   const uint32_t nvt = h->vtiles;
@@ -403,6 +430,19 @@ __global__ __launch_bounds__(kBlock, 6) void mean_kernel(Config c, const uint32_
   float* l_ft = (float*)(sm + kMeanTile * 4);  // [kMeanTile][C]
   int32_t* l_pi = (int32_t*)(sm + kMeanTile * (4 + C));  // [kMeanTile][M]
   if (K == 0u || nvt == 0u) return;  // uniform: no voxel (V is 0 too)
+  // the frame whose cap was shared numbers its kept voxels inside steps of
+  // kCapStepSlots slots: the steps' counts, scanned once per workgroup
+  const uint32_t most = h->most_pairs;
+  const int32_t shared_frame = most > (uint32_t)c.cap && cap_share(most) > 1u ? (int32_t)min(h->most_frame, (uint32_t)c.B - 1u) : -1;
+  if (shared_frame >= 0) {  // uniform
+    if (tid < 64) {
+      const uint32_t steps = (most + kCapStepSlots - 1) / kCapStepSlots;
+      const uint32_t x = (uint32_t)tid < steps ? h->cap_steps[min(tid, kMaxCapSteps - 1)] : 0u;
+      const uint32_t incl = wave_inclusive_sum(x);
+      if (tid < kMaxCapSteps) s_step[tid] = incl - x;
+    }
+    __syncthreads();
+  }
   for (uint32_t g0 = blockIdx.x * kMeanTile; g0 < V; g0 += gridDim.x * kMeanTile) {
     const uint32_t v = g0 + tid;
     const bool live = v < V;
@@ -434,7 +474,8 @@ __global__ __launch_bounds__(kBlock, 6) void mean_kernel(Config c, const uint32_
     const uint32_t rel = slot - min(vt.w, slot);
     const size_t cw = min((size_t)(vt.w / 32 + (uint32_t)b + (rel >> 5)), cwords - 1);
     const uint32_t kw = c.capbits[cwords + cw], pw = c.capbits[2 * cwords + cw];
-    const uint32_t rank = (kw >> (rel & 31)) & 1u ? pw + (uint32_t)__popc(kw & ((1u << (rel & 31)) - 1u)) : 0xffffffffu;
+    const uint32_t soff = b == shared_frame ? s_step[min(rel / kCapStepSlots, (uint32_t)kMaxCapSteps - 1u)] : 0u;
+    const uint32_t rank = (kw >> (rel & 31)) & 1u ? soff + pw + (uint32_t)__popc(kw & ((1u << (rel & 31)) - 1u)) : 0xffffffffu;
     const int64_t ob = c.out_voxel_offsets[b];
     const uint32_t s0 = min(c.hpos[sl], K - 1u);
     const uint32_t q0 = c.hplace[sl];  // the first point's place (the head's value)

@@ -426,7 +426,7 @@ class Voxelizer:
         h = self.workspace[:64].cpu().numpy().view(np.uint32)
         return {"fault": int(h[0]), "epoch": int(h[1]), "kept": int(h[2]), "voxels": int(h[3]),
                 "capped_voxels": int(h[4]), "any_capped": int(h[5]), "filter_chunks": int(h[6]),
-                "pair_chunks": int(h[7]), "voxel_tiles": int(h[8])}
+                "pair_chunks": int(h[7]), "voxel_tiles": int(h[8]), "most_frame": int(h[9]), "most_pairs": int(h[10])}
 
     def result(self) -> dict:
         """Outputs of the last completed call as numpy arrays trimmed to V rows (synchronises)."""

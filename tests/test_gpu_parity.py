@@ -263,6 +263,55 @@ def test_capped_frame_tables_in_workspace(gpu_lib):
     assert h["kept"] > 524_288 and h["capped_voxels"] > 150_000, h
 
 
+def test_capped_frame_too_large_to_share(gpu_lib):
+    """A frame over max_voxels with more kept pairs than a shared cap takes
+    (48 steps of 32,768 slots): one workgroup caps it alone, its tables in the
+    workspace.  1,700,000 points over a 512 x 512 x 16 grid, one ROI over all
+    of it, capped to 200,000 voxels."""
+    rng = np.random.default_rng(78)
+    N = 1_700_000
+    mn, voxel, dims = (-51.2, -51.2, -2.0), (0.2, 0.2, 0.25), (512, 512, 16)
+    cols = [rng.uniform(mn[d], mn[d] + dims[d] * voxel[d], N) for d in range(3)]
+    feat = np.ascontiguousarray(np.stack(cols + [rng.random(N)]).astype(np.float32))
+    poses = np.array([1, 0, 0, 0, 0, 1, 0, 0, 0, 0, 1, 0], np.float32).reshape(1, 1, 12)
+    grid = dict(range_min=list(mn), voxel_size=list(voxel), dims=list(dims), max_points=2, max_voxels=200_000,
+                num_sweeps=1, num_frames=1)
+    case = Case(feat=feat, sweep_ids=np.zeros(N, np.uint8), frame_offsets=np.array([0, N]), poses=poses,
+                rois=records([[0.0, 0.0, 1.0, 0.0, 200.0, 200.0]]), roi_offsets=np.array([0, 1], np.int32),
+                budgets=np.array([1], np.uint8), grid=grid)
+    vz, exp = check(gpu_lib, case, label="cap-unshared")
+    assert int(exp["voxel_offsets"][-1]) == 200_000
+    h = vz.header()
+    assert h["kept"] > 48 * 32_768 and h["capped_voxels"] > 200_000, h
+
+
+def test_capped_frame_beside_larger_uncapped_frame(gpu_lib):
+    """The frame with the most pairs is not over max_voxels (200,000 points in
+    a 32 x 32 x 8 block of voxels) while the next frame is (100,000 points
+    spread over a 256 x 256 x 16 grid, about 95,000 voxels capped to 40,000):
+    the capped frame is capped by its own workgroup and numbered by whole-frame
+    prefixes, beside a frame whose cap would have been shared."""
+    rng = np.random.default_rng(79)
+    mn, voxel, dims = (-25.6, -25.6, -2.0), (0.2, 0.2, 0.25), (256, 256, 16)
+    n0, n1 = 200_000, 100_000
+    dense = [rng.uniform(0.0, 32 * voxel[d] if d < 2 else 8 * voxel[d], n0) + (0.0 if d < 2 else mn[2]) for d in range(3)]
+    spread = [rng.uniform(mn[d], mn[d] + dims[d] * voxel[d], n1) for d in range(3)]
+    cols = [np.concatenate([dense[d], spread[d]]) for d in range(3)]
+    N = n0 + n1
+    feat = np.ascontiguousarray(np.stack(cols + [rng.random(N)]).astype(np.float32))
+    poses = np.tile(np.array([1, 0, 0, 0, 0, 1, 0, 0, 0, 0, 1, 0], np.float32), (2, 1)).reshape(2, 1, 12)
+    grid = dict(range_min=list(mn), voxel_size=list(voxel), dims=list(dims), max_points=3, max_voxels=40_000,
+                num_sweeps=1, num_frames=2)
+    case = Case(feat=feat, sweep_ids=np.zeros(N, np.uint8), frame_offsets=np.array([0, n0, N]), poses=poses,
+                rois=records([[0.0, 0.0, 1.0, 0.0, 100.0, 100.0]] * 2), roi_offsets=np.array([0, 1, 2], np.int32),
+                budgets=np.array([1, 1], np.uint8), grid=grid)
+    vz, exp = check(gpu_lib, case, label="cap-beside-larger")
+    off = exp["voxel_offsets"]
+    assert int(off[1]) < 40_000 and int(off[2] - off[1]) == 40_000, off
+    h = vz.header()
+    assert h["capped_voxels"] > 40_000 and h["most_frame"] == 0 and h["most_pairs"] == n0, h
+
+
 def _face_lattice_case(pose_rows, voxel=(0.1, 0.15, 0.3), mn=(-3.7, -2.9, -1.3), dims=(60, 40, 10)):
     """Points on voxel faces (and one ulp either side) of a non-dyadic grid,
     all inside one ROI covering the grid: the voxel index of every point is

@@ -20,6 +20,10 @@ int bits_for(uint64_t maxval) {
 
 size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
+// Words of a kept-point record: the point index and C features, rounded up to
+// an even count (8-byte aligned records: 16, 24, 32 or 40 bytes).
+int32_t record_words(int32_t C) { return (2 + C) & ~1; }
+
 // Workspace of the connected-component proposer.
 struct CcPlan {
   int64_t rows, cells, ncell, Wx, Wy, nwords, nblocks;
@@ -166,7 +170,7 @@ mmbev_status_t make_plan(const mmbev_grid_t* g, int64_t N, int32_t max_rois, int
     p->off_keys[q] = take((size_t)n1 * 4);
     p->off_vals[q] = take((size_t)n1 * 4);
   }
-  p->off_rec = take((size_t)n1 * 4 * ((1 + p->C + 3) / 4 * 4));
+  p->off_rec = take((size_t)n1 * 4 * (size_t)record_words(p->C));
   p->off_hpos = take((size_t)n1 * 4);
   p->off_hplace = take((size_t)n1 * 4);
   p->off_capbits = take((3 * ((size_t)n1 / 32 + p->B + 1) + (size_t)p->vtile_max + 1) * 4);
@@ -344,7 +348,7 @@ mmbev_status_t voxelize(const mmbev_points_t* points, const uint8_t* sweep_ids, 
     c.vals[q] = (uint32_t*)(ws + p.off_vals[q]);
   }
   c.rec = (uint32_t*)(ws + p.off_rec);
-  c.rec_words = (1 + p.C + 3) / 4 * 4;
+  c.rec_words = record_words(p.C);
   c.hpos = (uint32_t*)(ws + p.off_hpos);
   c.hplace = (uint32_t*)(ws + p.off_hplace);
   c.capbits = (uint32_t*)(ws + p.off_capbits);

@@ -124,8 +124,9 @@ struct Config {
   uint32_t* keys[2];       // [N] each: ping-pong buffers of the radix passes
   uint32_t* vals[2];       // the pair's record: its place in compact (point) order
   // records of the kept points in compact order, written by the compaction:
-  // rec_words words each (a multiple of 4), word 0 the point index, then
-  // x', y', z' (Eq. 6) and the raw features 3..C-1 as float bits
+  // rec_words words each (1 + C rounded up to an even count: 4, 6, 8 or 10),
+  // word 0 the point index, then x', y', z' (Eq. 6) and the raw features
+  // 3..C-1 as float bits
   uint32_t* rec;           // [N][rec_words]
   int32_t rec_words;
   // per voxel, at slot vtile[t].x + j for voxel j of tile t

@@ -314,12 +314,22 @@ __global__ __launch_bounds__(kCompactBlock) void compact_kernel(Config c, uint32
                         quantize_axis(pz, c.mn[2], c.vs[2], c.Df[2], iz);
         if (!in) raise_fault(c.hdr, MMBEV_FAULT_INTERNAL);  // the filter kept it: never
         kout[q] = in ? ((uint32_t)iz * c.Dy + (uint32_t)iy) * c.Dx + (uint32_t)ix : 0u;
-        uint4* rr = reinterpret_cast<uint4*>(c.rec + (int64_t)q * RW);
-        rr[0] = make_uint4(pi[u], __float_as_uint(px), __float_as_uint(py), __float_as_uint(pz));
-        if (RW > 4)
-          rr[1] = make_uint4(__float_as_uint(v[u][3]), __float_as_uint(v[u][4]), __float_as_uint(v[u][5]),
-                             __float_as_uint(v[u][6]));
-        if (RW > 8) rr[2] = make_uint4(__float_as_uint(v[u][7]), 0u, 0u, 0u);
+        // the record: 16-byte stores when RW is a multiple of four, else
+        // 8-byte stores (records are 8-byte aligned)
+        const uint32_t w[10] = {pi[u], __float_as_uint(px), __float_as_uint(py), __float_as_uint(pz),
+                                __float_as_uint(v[u][3]), __float_as_uint(v[u][4]), __float_as_uint(v[u][5]),
+                                __float_as_uint(v[u][6]), __float_as_uint(v[u][7]), 0u};
+        uint32_t* rp = c.rec + (int64_t)q * RW;
+        if ((RW & 3) == 0) {  // uniform
+#pragma unroll
+          for (int k = 0; k < 2; ++k)
+            if (4 * k < RW)
+              reinterpret_cast<uint4*>(rp)[k] = make_uint4(w[4 * k], w[4 * k + 1], w[4 * k + 2], w[4 * k + 3]);
+        } else {
+#pragma unroll
+          for (int k = 0; k < 5; ++k)
+            if (2 * k < RW) reinterpret_cast<uint2*>(rp)[k] = make_uint2(w[2 * k], w[2 * k + 1]);
+        }
       }
     }
   };

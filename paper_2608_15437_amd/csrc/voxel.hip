@@ -533,26 +533,38 @@ __global__ __launch_bounds__(kBlock, 6) void mean_kernel(Config c, const uint32_
 #pragma unroll
       for (int u = 0; u < kMeanBatch; ++u)
         q[u] = min(m0 + u == 0 ? q0 : vals[min(s0 + m0 + u, K - 1u)], K - 1u);
-      uint4 r0[kMeanBatch], r1[kMeanBatch];
-      uint32_t r2[kMeanBatch];
+      uint32_t w[kMeanBatch][RW];
 #pragma unroll
-      for (int u = 0; u < kMeanBatch; ++u) {  // one, two or two and a word of 16-byte loads per record
-        const uint4* r = reinterpret_cast<const uint4*>(c.rec + (int64_t)q[u] * RW);
-        r0[u] = r[0];
-        r1[u] = RW > 4 ? r[1] : make_uint4(0u, 0u, 0u, 0u);
-        r2[u] = RW > 8 ? c.rec[(int64_t)q[u] * RW + 8] : 0u;
+      for (int u = 0; u < kMeanBatch; ++u) {  // 16-byte loads when RW is a multiple of four, else 8-byte loads
+        const uint32_t* rp = c.rec + (int64_t)q[u] * RW;
+        if constexpr ((RW & 3) == 0) {
+#pragma unroll
+          for (int k = 0; k < RW / 4; ++k) {
+            const uint4 x = reinterpret_cast<const uint4*>(rp)[k];
+            w[u][4 * k] = x.x;
+            w[u][4 * k + 1] = x.y;
+            w[u][4 * k + 2] = x.z;
+            w[u][4 * k + 3] = x.w;
+          }
+        } else {
+#pragma unroll
+          for (int k = 0; k < RW / 2; ++k) {
+            const uint2 x = reinterpret_cast<const uint2*>(rp)[k];
+            w[u][2 * k] = x.x;
+            w[u][2 * k + 1] = x.y;
+          }
+        }
       }
 #pragma unroll
       for (int u = 0; u < kMeanBatch; ++u)
         if (m0 + u < cnt) {
-          const uint32_t w[8] = {r0[u].y, r0[u].z, r0[u].w, r1[u].x, r1[u].y, r1[u].z, r1[u].w, r2[u]};
 #pragma unroll
           for (int f = 0; f < 8; ++f)
-            if (f < C) sum[f] += (double)__uint_as_float(w[f]);  // ascending point order
+            if (f < C && f + 1 < RW) sum[f] += (double)__uint_as_float(w[u][f + 1]);  // ascending point order
           if (contig)  // uniform: LDS staging or the row itself
-            l_pi[tid * M + m0 + u] = (int32_t)r0[u].x;
+            l_pi[tid * M + m0 + u] = (int32_t)w[u][0];
           else
-            c.out_point_idx[row * M + m0 + u] = (int32_t)r0[u].x;
+            c.out_point_idx[row * M + m0 + u] = (int32_t)w[u][0];
         }
     }
     if (row >= 0) {
@@ -610,12 +622,14 @@ hipError_t launch_fincap(const Config& c, hipStream_t st) {
 hipError_t launch_mean(const Config& c, const uint32_t* keys, const uint32_t* vals, hipStream_t st) {
   const size_t lds = (size_t)kMeanTile * (4 + c.C + c.M) * 4;
   // one instance per record width (point index, x', y', z', raw features 3..)
-  if (c.rec_words <= 4)
+  if (c.rec_words == 4)
     hipLaunchKernelGGL(mean_kernel<4>, dim3(c.mean_grid), dim3(kBlock), lds, st, c, keys, vals);
-  else if (c.rec_words <= 8)
+  else if (c.rec_words == 6)
+    hipLaunchKernelGGL(mean_kernel<6>, dim3(c.mean_grid), dim3(kBlock), lds, st, c, keys, vals);
+  else if (c.rec_words == 8)
     hipLaunchKernelGGL(mean_kernel<8>, dim3(c.mean_grid), dim3(kBlock), lds, st, c, keys, vals);
   else
-    hipLaunchKernelGGL(mean_kernel<12>, dim3(c.mean_grid), dim3(kBlock), lds, st, c, keys, vals);
+    hipLaunchKernelGGL(mean_kernel<10>, dim3(c.mean_grid), dim3(kBlock), lds, st, c, keys, vals);
   return hipGetLastError();
 }
 

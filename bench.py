@@ -416,7 +416,7 @@ def kernel_job_bytes(name: str, m: dict):
     """HBM bytes a kernel's job needs in this design (its inputs read once, its
     outputs written once); None for the latency-bound bookkeeping kernels."""
     N, K, V, C, M = m["N"], m["K"], m["V"], m["C"], m["M"]
-    RW = 4 if C <= 3 else (8 if C <= 7 else 12)  # record words: index, x', y', z', raw features 3..
+    RW = (2 + C) & ~1  # record words: index, x', y', z', raw features 3.., rounded up to even
     if name.startswith("filter_kernel"):
         return 13 * N + 33 * m["R"] + 48 * m["B"] * m["S"]  # x, y, z, sweep id; ROI records; poses
     if name == "compact_kernel":

@@ -12,7 +12,8 @@
 // every frame.
 //
 // segments -- one workgroup: the kept-pair prefix of the filter chunks, the
-//             first pair of every frame, and the pair chunks (at most
+//             first pair of every frame (the prefix at its first filter
+//             chunk), and the pair chunks (at most
 //             kMaxFrameChunks per frame, whole scatter tiles, the last of a
 //             frame shorter) and the voxel tiles of the later kernels
 //             (kVoxTile pairs, the last of a frame shorter).
@@ -63,66 +64,87 @@ constexpr int kSegLdsFrames = 4096;  // frame starts kept in LDS up to this many
 // out at the end; otherwise in the workspace directly.  (One address space per
 // instance: a pointer that may be either compiles to generic instructions,
 // whose waits cover both kinds of access.)
+constexpr int kSegPreLds = 16384;  // kept-pair prefixes of up to this many filter chunks kept in LDS (kLds instance)
+
+// Exclusive prefix sums of two values per thread over the workgroup (one
+// barrier pair for both); s_tmp holds 2 * WAVES words.
+template <int WAVES>
+__device__ __forceinline__ uint2 block_exclusive_scan2(uint32_t a, uint32_t b, uint32_t* s_tmp, uint2& total) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const uint32_t xa = wave_inclusive_sum(a), xb = wave_inclusive_sum(b);
+  if (lane == 63) {
+    s_tmp[wave] = xa;
+    s_tmp[WAVES + wave] = xb;
+  }
+  __syncthreads();
+  uint32_t pa = 0, pb = 0, ta = 0, tb = 0;
+#pragma unroll
+  for (int w = 0; w < WAVES; ++w) {
+    const uint32_t u = s_tmp[w], v = s_tmp[WAVES + w];
+    pa += (w < wave) ? u : 0u;
+    pb += (w < wave) ? v : 0u;
+    ta += u;
+    tb += v;
+  }
+  __syncthreads();
+  total = make_uint2(ta, tb);
+  return make_uint2(pa + xa - a, pb + xb - b);
+}
+
+// kLds: the frame starts are built in LDS (B <= kSegLdsFrames) and copied
+// out at the end; otherwise in the workspace directly.  (One address space per
+// instance: a pointer that may be either compiles to generic instructions,
+// whose waits cover both kinds of access.)
 template <bool kLds>
 __global__ __launch_bounds__(kSegBlock) void segments_kernel(Config c) {
-  __shared__ uint32_t s_tmp[kSegWaves];
+  __shared__ uint32_t s_tmp[2 * kSegWaves];
   __shared__ uint32_t s_fstart[kLds ? kSegLdsFrames + 1 : 1];  // frame starts
   __shared__ uint32_t s_sfirst[kLds ? kSegLdsFrames + 1 : 1];  // first pair chunk of every frame
   __shared__ uint32_t s_tfirst[kLds ? kSegLdsFrames + 1 : 1];  // first voxel tile of every frame
-  __shared__ int32_t s_last;
+  __shared__ uint32_t s_pre[kLds ? kSegPreLds + 1 : 1];        // kept pairs of the filter chunks before k
   __shared__ unsigned long long s_most;  // (pairs, ~frame) of the frame with the most pairs
   WsHeader* h = c.hdr;
   const int tid = threadIdx.x;
   const uint32_t nf = h->fchunks;
+  // the first filter chunk of this thread's frame (the staging kernel laid
+  // the chunks out frame by frame), loaded with the chunk count
+  const uint32_t ffirst = c.fchunk_first[min(tid, c.B)];
+  // used here, so that its wait is not placed after the prefix stores below
+  // (one in-order counter covers loads and stores: a wait for an early load
+  // issued after many stores would wait for the stores too)
+  asm volatile("" ::"v"(ffirst));
   constexpr bool lds = kLds;
+  const bool pre_lds = kLds && nf < (uint32_t)kSegPreLds;  // uniform
   uint32_t* fstart = kLds ? s_fstart : c.fstart;
-  if (tid == 0) {
-    s_last = -1;
-    s_most = 0ull;
-  }
-  // kept-point prefix of the filter chunks; the first chunk of a frame also
-  // gives the start of that frame and of the empty frames just before it.
-  // Thread t holds kScanItems consecutive chunks, read with 16-byte loads.
+  if (tid == 0) s_most = 0ull;
+  // kept-point prefix of the filter chunks.  Thread t holds kScanItems
+  // consecutive chunks, read with 16-byte loads.
   static_assert(kScanItems % 4 == 0, "16-byte loads");
   uint32_t carry = 0;
   for (uint32_t base = 0; base < nf; base += kSegBlock * kScanItems) {
     const uint32_t first = base + tid * kScanItems;
     uint32_t v[kScanItems], sum = 0;
-    int32_t fr[kScanItems];
-    const int32_t before = first > 0 && first <= nf ? (int32_t)c.fchunk_frame[first - 1] : -1;
 #pragma unroll
     for (int j = 0; j < kScanItems; j += 4) {
-      uint4 a = make_uint4(0u, 0u, 0u, 0u), f = make_uint4(~0u, ~0u, ~0u, ~0u);
+      uint4 a = make_uint4(0u, 0u, 0u, 0u);
       if (first + j + 3 < nf) {
         a = *reinterpret_cast<const uint4*>(c.fcount + first + j);
-        f = *reinterpret_cast<const uint4*>(c.fchunk_frame + first + j);
       } else if (first + j < nf) {
         a.x = c.fcount[first + j];
-        f.x = c.fchunk_frame[first + j];
-        if (first + j + 1 < nf) { a.y = c.fcount[first + j + 1]; f.y = c.fchunk_frame[first + j + 1]; }
-        if (first + j + 2 < nf) { a.z = c.fcount[first + j + 2]; f.z = c.fchunk_frame[first + j + 2]; }
+        if (first + j + 1 < nf) a.y = c.fcount[first + j + 1];
+        if (first + j + 2 < nf) a.z = c.fcount[first + j + 2];
       }
       v[j] = a.x; v[j + 1] = a.y; v[j + 2] = a.z; v[j + 3] = a.w;
-      fr[j] = (int32_t)min(f.x, (uint32_t)c.B - 1u);
-      fr[j + 1] = (int32_t)min(f.y, (uint32_t)c.B - 1u);
-      fr[j + 2] = (int32_t)min(f.z, (uint32_t)c.B - 1u);
-      fr[j + 3] = (int32_t)min(f.w, (uint32_t)c.B - 1u);
     }
 #pragma unroll
     for (int j = 0; j < kScanItems; ++j) sum += v[j];
     uint32_t total;
     uint32_t run = carry + block_exclusive_scan<kSegWaves>(sum, s_tmp, total);
-    int32_t prev = before;
     uint32_t pre[kScanItems];
 #pragma unroll
     for (int j = 0; j < kScanItems; ++j) {
       pre[j] = run;
-      if (first + j < nf) {
-        for (int32_t g = prev + 1; g <= fr[j]; ++g) fstart[g] = run;
-        prev = max(prev, fr[j]);
-        run += v[j];
-        if (first + j + 1 == nf) s_last = prev;
-      }
+      run += v[j];
     }
     // the thread's prefixes as 16-byte stores (one per four chunks)
 #pragma unroll
@@ -133,13 +155,28 @@ __global__ __launch_bounds__(kSegBlock) void segments_kernel(Config c) {
         for (int u = 0; u < 4; ++u)
           if (first + j + u < nf) c.fprefix[first + j + u] = pre[j + u];
     }
+    if (pre_lds)
+#pragma unroll
+      for (int j = 0; j < kScanItems; ++j)
+        if (first + j < nf) s_pre[first + j] = pre[j];
     carry += total;
-    __syncthreads();
   }
   const uint32_t K = carry;
   if (tid == 0) c.fprefix[nf] = K;
-  __syncthreads();
-  for (int32_t g = s_last + 1 + tid; g <= c.B; g += kSegBlock) fstart[g] = K;  // frames after the last chunk
+  __syncthreads();  // the prefixes are in place (LDS, or the workspace)
+  // frame b starts at the prefix of its first chunk; frames after the last
+  // chunk (and frame B) at K
+  if (pre_lds) {  // uniform: the prefixes from LDS
+    for (int g = tid; g <= c.B; g += kSegBlock) {
+      const uint32_t k = min(g == tid ? ffirst : c.fchunk_first[g], nf);
+      fstart[g] = k >= nf ? K : s_pre[k];
+    }
+  } else {
+    for (int g = tid; g <= c.B; g += kSegBlock) {
+      const uint32_t k = min(g == tid ? ffirst : c.fchunk_first[g], nf);
+      fstart[g] = k >= nf ? K : c.fprefix[k];
+    }
+  }
   __syncthreads();
   if (lds)
     for (int g = tid; g <= c.B; g += kSegBlock) c.fstart[g] = s_fstart[g];
@@ -168,9 +205,10 @@ __global__ __launch_bounds__(kSegBlock) void segments_kernel(Config c) {
     const uint32_t lo = wave_max((uint32_t)(most >> 32) == hi ? (uint32_t)most : 0u);
     if ((tid & 63) == 0 && hi > 0u) atomicMax(&s_most, (unsigned long long)hi << 32 | lo);  // read after the scans' barriers
   }
-  uint32_t total, total_vt;
-  uint32_t run = block_exclusive_scan<kSegWaves>(mine, s_tmp, total);
-  uint32_t run_vt = block_exclusive_scan<kSegWaves>(mine_vt, s_tmp, total_vt);
+  uint2 tot;
+  const uint2 ex = block_exclusive_scan2<kSegWaves>(mine, mine_vt, s_tmp, tot);
+  uint32_t run = ex.x, run_vt = ex.y;
+  const uint32_t total = tot.x, total_vt = tot.y;
   const uint32_t cap = (uint32_t)c.schunk_max;  // never reached: the bound holds for any K <= N
   const uint32_t cap_vt = (uint32_t)c.vtile_max;
   const uint32_t nsc = min(total, cap), nvt = min(total_vt, cap_vt);

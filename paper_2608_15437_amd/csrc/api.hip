@@ -366,6 +366,11 @@ mmbev_status_t voxelize(const mmbev_points_t* points, const uint8_t* sweep_ids, 
   c.lds_bm = c.lds_roi + 6 * c.lds_roi_cap;
   c.lds_cell = c.lds_bm + c.lds_bm_cap;
   c.lds_dyn_bytes = (int32_t)(((size_t)(c.lds_cell + c.lds_cell_cap) * 4 + 15) / 16 * 16);
+  // one ROI word per cell, every table of a frame in LDS and a thread per
+  // frame: each filter workgroup lays out the call and builds its frame's
+  // tables itself, and the staging kernel is not launched
+  c.fuse_stage = p.W == 1 && p.B <= kFuseFrames && c.lds_pose_cap == p.S && c.lds_bm_cap == p.S * p.W &&
+                 c.lds_cell_cap == p.ncells + 1 && c.lds_roi_cap >= p.max_rois && p.S <= kBlock;
   c.schunk_max = (int32_t)p.schunk_max;
   c.vtile_max = (int32_t)p.vtile_max;
   c.mean_grid = (int32_t)p.mean_grid;
@@ -376,7 +381,7 @@ mmbev_status_t voxelize(const mmbev_points_t* points, const uint8_t* sweep_ids, 
     if (ev.mark(s) != hipSuccess || (call) != hipSuccess) return MMBEV_ERR_HIP; \
   } while (0)
 
-  MMBEV_TRY(launch_stage(c, s));
+  MMBEV_TRY(c.fuse_stage ? hipSuccess : launch_stage(c, s));
   MMBEV_TRY(launch_filter(c, s));
   // sorted pairs ping-pong: keys compacted into [1], pass p writes [p % 2];
   // pass 0 reads no values, its value for each key is the key's compacted

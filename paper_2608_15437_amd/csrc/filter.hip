@@ -636,10 +636,160 @@ __device__ __forceinline__ void run_wave(const Config& c, const FilterLds& L, Wa
   if (lane + 64 < (uint32_t)c.fchunk_words) out[lane + 64] = Q.bits[lane + 64];
 }
 
+// Scratch of a workgroup that lays out the call itself (the waves' queues
+// are not in use before the first tile, so it lives there).
+struct FuseLds {
+  uint32_t first[kFuseFrames + 1];  // first filter chunk of frame b
+  int32_t roff[kFuseFrames + 1];    // ROI offsets as given
+  int16_t rect[32][4];              // cell rectangles of the frame's ROIs
+  uint32_t area[33];                // their cells before ROI j (exclusive prefix), then the total
+  uint32_t bud[32];                 // their sweep budgets
+  uint32_t tmp[kWaves];
+  int32_t bad;
+};
+static_assert(sizeof(FuseLds) <= kWaves * sizeof(WaveLds), "fits the waves' queues");
+
+// What a workgroup of the fused instance needs to know about the call.
+struct FuseLayout {
+  uint32_t nchunks;     // filter chunks of the call
+  int32_t wf;           // frame of the workgroup's first chunk
+  uint32_t ff0, ff1;    // that frame's first chunk and the next frame's
+  int64_t fo0, fo1;     // its point offsets
+  int32_t ro0, ro1;     // its ROI offsets
+};
+
+// Every workgroup of the fused instance (frames B <= kFuseFrames, one per
+// thread): the offset checks and the chunk layout the staging kernel makes
+// otherwise (the same numbering: each frame's chunks rounded up to whole
+// workgroups, none at all when the point offsets are invalid), and the
+// frame of its first chunk.  Workgroup 0 also opens the call: the header's
+// counters and fault word, the call count and the frames' first chunks,
+// which the later kernels read.
+__device__ __forceinline__ FuseLayout fuse_layout(const Config& c, FuseLds& F) {
+  const int tid = threadIdx.x;
+  const int f = min(tid, c.B), fn = min(f + 1, c.B);
+  const int64_t o = c.frame_off[f], on = c.frame_off[fn];
+  const int32_t ro = c.roi_off[f], rn = c.roi_off[fn];
+  const int32_t bad = tid <= c.B ? offset_faults(c, f, o, on, ro, rn) : 0;
+  if (tid == 0) F.bad = 0;
+  __syncthreads();
+  if (bad) atomicOr(&F.bad, bad);
+  __syncthreads();
+  const int32_t allbad = F.bad;
+  const bool no_points = (allbad & MMBEV_FAULT_POINT_OFFSETS) != 0;
+  const uint32_t p0 = (uint32_t)min(max(o, (int64_t)0), (int64_t)c.N);
+  const uint32_t p1 = max((uint32_t)min(max(on, (int64_t)0), (int64_t)c.N), p0);
+  const uint32_t mine = tid < c.B && !no_points ? frame_chunks(p1 - p0, (uint32_t)c.fchunk_points) : 0u;
+  uint32_t total;
+  const uint32_t run = block_exclusive_scan(mine, F.tmp, total);
+  const uint32_t cap = (uint32_t)c.fchunk_max;  // reached only with invalid offsets
+  const uint32_t nch = min(total, cap);
+  if (tid < c.B) F.first[tid] = min(run, cap);
+  if (tid == c.B) F.first[tid] = nch;
+  if (tid <= c.B) F.roff[tid] = ro;
+  __syncthreads();
+  if (blockIdx.x == 0) {
+    WsHeader* h = c.hdr;
+    if (tid == 0) {
+      h->fault = allbad;
+      h->epoch = h->epoch + 1;
+      h->kept = 0;
+      h->voxels = 0;
+      h->capped_voxels = 0;
+      h->any_capped = 0;
+      h->fchunks = nch;
+    }
+    if (tid <= c.B) c.fchunk_first[tid] = F.first[tid];
+  }
+  FuseLayout g;
+  g.nchunks = nch;
+  const uint32_t k0 = (uint32_t)blockIdx.x * kWaves;
+  int32_t lo = 0, hi = c.B - 1;  // the last frame whose first chunk is at most k0
+  while (lo < hi) {
+    const int32_t mid = (lo + hi + 1) >> 1;
+    if (F.first[mid] <= k0) lo = mid; else hi = mid - 1;
+  }
+  g.wf = lo;
+  g.ff0 = F.first[lo];
+  g.ff1 = F.first[lo + 1];
+  g.ro0 = F.roff[lo];
+  g.ro1 = F.roff[lo + 1];
+  g.fo0 = c.frame_off[lo];
+  g.fo1 = c.frame_off[lo + 1];
+  return g;
+}
+
+// The fused instance's tables of frame f (one ROI word: at most 32 ROIs,
+// roi_n of them from roi_lo): poses, ROI records and budgets loaded
+// together; the budget word of every sweep and the frame's cell row (a zero
+// word, then per coarse cell the ROIs whose conservative rectangle covers
+// it) built in LDS from the records, as the staging kernel builds them.
+__device__ __forceinline__ void fuse_staging(const Config& c, FilterLds& L, FuseLds& F, int32_t f, int32_t roi_lo,
+                                             int32_t roi_n, int32_t ro0, int32_t ro1) {
+  constexpr int kPoseRegs = (kMaxPoseLds * 12 + kBlock - 1) / kBlock;
+  const int tid = threadIdx.x;
+  const int np = c.S * 12;
+  float pv[kPoseRegs];
+  const float* poses = c.poses + (int64_t)f * np;
+#pragma unroll
+  for (int j = 0; j < kPoseRegs; ++j) pv[j] = tid + j * kBlock < np ? poses[tid + j * kBlock] : 0.0f;
+  mmbev_roi_t r{};
+  uint32_t bud = 0;
+  if (tid < roi_n) {
+    r = c.rois[roi_lo + tid];
+    bud = c.budget[roi_lo + tid];
+  }
+  uint32_t* dyn = reinterpret_cast<uint32_t*>(filter_dyn);
+  float* dynf = reinterpret_cast<float*>(filter_dyn);
+  if (tid == 0) L.roff[0] = min(max(ro0, 0), c.R);
+  if (tid == 1) L.roff[1] = min(max(ro1, 0), c.R);
+#pragma unroll
+  for (int j = 0; j < kPoseRegs; ++j)
+    if (tid + j * kBlock < np) dynf[tid + j * kBlock] = pv[j];  // pose rows from word 0
+  for (int e = tid; e <= c.ncells; e += kBlock) dyn[c.lds_cell + e] = 0u;
+  uint32_t area = 0;
+  if (tid < roi_n) {
+    dynf[c.lds_roi + 0 * c.lds_roi_cap + tid] = r.cx;
+    dynf[c.lds_roi + 1 * c.lds_roi_cap + tid] = r.cy;
+    dynf[c.lds_roi + 2 * c.lds_roi_cap + tid] = r.cos_yaw;
+    dynf[c.lds_roi + 3 * c.lds_roi_cap + tid] = r.sin_yaw;
+    dynf[c.lds_roi + 4 * c.lds_roi_cap + tid] = r.ext_x;
+    dynf[c.lds_roi + 5 * c.lds_roi_cap + tid] = r.ext_y;
+    int16_t* rc = F.rect[tid];
+    roi_cell_rect(c, r, rc);
+    area = rc[1] >= rc[0] && rc[3] >= rc[2] ? (uint32_t)(rc[1] - rc[0] + 1) * (uint32_t)(rc[3] - rc[2] + 1) : 0u;
+    F.bud[tid] = bud;
+  }
+  if (tid < 64) {  // wave 0: the rectangles' cell counts scanned (at most 32 ROIs)
+    const uint32_t x = wave_inclusive_sum(area);
+    if (tid < 32) F.area[tid] = x - area;
+    if (tid == 31) F.area[32] = x;
+  }
+  __syncthreads();
+  if (tid < c.S) {  // sweep s: the ROIs whose budget admits it
+    uint32_t w = 0;
+    for (int j = 0; j < roi_n; ++j) w |= F.bud[j] > (uint32_t)tid ? 1u << j : 0u;
+    dyn[c.lds_bm + tid] = w;
+  }
+  // every (ROI, covered cell) pair: the ROI's bit ORed into the cell's word
+  const uint32_t cells = F.area[32];
+  for (uint32_t i = tid; i < cells; i += kBlock) {
+    int32_t lo = 0, hi = roi_n - 1;  // the ROI: the last one whose first pair is at most i
+    while (lo < hi) {
+      const int32_t mid = (lo + hi + 1) >> 1;
+      if (F.area[mid] <= i) lo = mid; else hi = mid - 1;
+    }
+    const int16_t* rc = F.rect[lo];
+    const uint32_t q = i - F.area[lo], wx = (uint32_t)(rc[1] - rc[0] + 1);
+    const uint32_t cx = (uint32_t)rc[0] + q % wx, cy = (uint32_t)rc[2] + q / wx;
+    atomicOr(&dyn[c.lds_cell + 1 + cy * (uint32_t)c.ncx + cx], 1u << lo);
+  }
+}
+
 // Workgroup w: its waves over filter chunks kWaves*w .. kWaves*w + 3.  Per
 // chunk it leaves the bitmap of its kept points, their number, its first
 // point and its frame.  BG: the out-of-ROI keep rate is nonzero.
-template <bool VEC, bool BG>
+template <bool VEC, bool BG, bool FS>
 __global__ __launch_bounds__(kBlock, 5) void filter_kernel(Config c) {
   __shared__ FilterLds L;
   __shared__ WaveLds Qs[kWaves];
@@ -648,16 +798,36 @@ __global__ __launch_bounds__(kBlock, 5) void filter_kernel(Config c) {
   // of the kernel is uniform control flow for the compiler too
   const int lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   WaveLds& Q = Qs[wave];
-  const uint32_t nchunks = c.hdr->fchunks;
+  FuseLds& F = *reinterpret_cast<FuseLds*>(&Qs[0]);
+  uint32_t nchunks, ff0, ff1;
+  int32_t wf, ro0, ro1;
+  int64_t fo0, fo1;
+  if constexpr (FS) {  // the workgroup lays out the call itself
+    const FuseLayout g = fuse_layout(c, F);
+    nchunks = g.nchunks;
+    wf = g.wf;
+    ff0 = g.ff0;
+    ff1 = g.ff1;
+    fo0 = g.fo0;
+    fo1 = g.fo1;
+    ro0 = g.ro0;
+    ro1 = g.ro1;
+  } else {
+    nchunks = c.hdr->fchunks;
+    // frame wf of chunk k0 (loaded with nchunks), then everything that
+    // depends only on wf, loaded together: every chunk of the workgroup lies
+    // in wf unless the point offsets are invalid (then searches find the
+    // frames)
+    wf = (int32_t)min(c.wg_frame[blockIdx.x], (uint32_t)c.B - 1u);
+    fo0 = c.frame_off[wf];
+    fo1 = c.frame_off[wf + 1];
+    ff0 = c.fchunk_first[wf];
+    ff1 = c.fchunk_first[wf + 1];
+    ro0 = c.roi_off[wf];
+    ro1 = c.roi_off[wf + 1];
+    asm volatile("" ::"s"(fo0), "s"(fo1), "s"(ff0), "s"(ff1), "s"(ro0), "s"(ro1));  // one round trip for all
+  }
   const uint32_t k0 = (uint32_t)blockIdx.x * kWaves;
-  // frame wf of chunk k0 (loaded with nchunks), then everything that depends
-  // only on wf, loaded together: every chunk of the workgroup lies in wf
-  // unless the point offsets are invalid (then searches find the frames)
-  const int32_t wf = (int32_t)min(c.wg_frame[blockIdx.x], (uint32_t)c.B - 1u);
-  const int64_t fo0 = c.frame_off[wf], fo1 = c.frame_off[wf + 1];
-  const uint32_t ff0 = c.fchunk_first[wf], ff1 = c.fchunk_first[wf + 1];
-  const int32_t ro0 = c.roi_off[wf], ro1 = c.roi_off[wf + 1];
-  asm volatile("" ::"s"(fo0), "s"(fo1), "s"(ff0), "s"(ff1), "s"(ro0), "s"(ro1));  // one round trip for all
 
   // this wave's chunk and its points; the staging plan
   const uint32_t k = k0 + (uint32_t)wave;
@@ -668,6 +838,10 @@ __global__ __launch_bounds__(kBlock, 5) void filter_kernel(Config c) {
   StagePlan pl{0, 0, 0, 0, false};
   if (any && last < ff1) {
     pl = make_plan(c, wf, wf, ro0, ro1);
+    if (FS) {  // always staged (the host checked the sizes); ROIs past the cap only with invalid ROI offsets
+      pl.roi_n = min(pl.roi_n, c.lds_roi_cap);
+      pl.staged = true;
+    }
     if (k < nchunks) {
       b = wf;
       const uint32_t P = (uint32_t)c.fchunk_points;
@@ -677,7 +851,7 @@ __global__ __launch_bounds__(kBlock, 5) void filter_kernel(Config c) {
       lo = (uint32_t)min(l, (uint64_t)p1);
       hi = (uint32_t)min(l + P, (uint64_t)p1);
     }
-  } else if (any) {
+  } else if (any && !FS) {  // (with the fused layout every workgroup's chunks lie in one frame)
     const int32_t f0 = frame_of_chunk(c.fchunk_first, c.B, k0), f1 = frame_of_chunk(c.fchunk_first, c.B, last);
     pl = make_plan(c, f0, f1, c.roi_off[f0], c.roi_off[f1 + 1]);
     if (k < nchunks) {
@@ -697,10 +871,14 @@ __global__ __launch_bounds__(kBlock, 5) void filter_kernel(Config c) {
     L.chunk_staged = pl.staged;
   }
   const bool staged = pl.staged;
-  if (staged) do_staging(c, L, pl);
+  if (FS) {
+    if (pl.staged) fuse_staging(c, L, F, pl.f0, pl.roi_lo, pl.roi_n, ro0, ro1);
+  } else if (staged) {
+    do_staging(c, L, pl);
+  }
   __syncthreads();
 
-  if (k >= nchunks) return;
+  if (k >= nchunks || (FS && !pl.staged)) return;
   WaveRun wr{0u, 0u, 0u, lo, b, k};
   if (staged)
     run_wave<VEC, true, BG>(c, L, Q, b, lo, hi, wr);
@@ -719,14 +897,24 @@ hipError_t launch_filter(const Config& c, hipStream_t st) {
   // one instance per load form and per rate (none, or a nonzero one)
   const dim3 grid(c.filter_grid), block(kBlock);
   const size_t dyn = (size_t)c.lds_dyn_bytes;
-  if (c.vec && c.bg_thr == 0u)
-    hipLaunchKernelGGL((filter_kernel<true, false>), grid, block, dyn, st, c);
-  else if (c.vec)
-    hipLaunchKernelGGL((filter_kernel<true, true>), grid, block, dyn, st, c);
-  else if (c.bg_thr == 0u)
-    hipLaunchKernelGGL((filter_kernel<false, false>), grid, block, dyn, st, c);
-  else
-    hipLaunchKernelGGL((filter_kernel<false, true>), grid, block, dyn, st, c);
+  if (c.fuse_stage) {  // the filter lays out the call and builds its frame's tables itself
+    if (c.vec && c.bg_thr == 0u)
+      hipLaunchKernelGGL((filter_kernel<true, false, true>), grid, block, dyn, st, c);
+    else if (c.vec)
+      hipLaunchKernelGGL((filter_kernel<true, true, true>), grid, block, dyn, st, c);
+    else if (c.bg_thr == 0u)
+      hipLaunchKernelGGL((filter_kernel<false, false, true>), grid, block, dyn, st, c);
+    else
+      hipLaunchKernelGGL((filter_kernel<false, true, true>), grid, block, dyn, st, c);
+  } else if (c.vec && c.bg_thr == 0u) {
+    hipLaunchKernelGGL((filter_kernel<true, false, false>), grid, block, dyn, st, c);
+  } else if (c.vec) {
+    hipLaunchKernelGGL((filter_kernel<true, true, false>), grid, block, dyn, st, c);
+  } else if (c.bg_thr == 0u) {
+    hipLaunchKernelGGL((filter_kernel<false, false, false>), grid, block, dyn, st, c);
+  } else {
+    hipLaunchKernelGGL((filter_kernel<false, true, false>), grid, block, dyn, st, c);
+  }
   return hipGetLastError();
 }
 

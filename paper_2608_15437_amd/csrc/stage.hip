@@ -27,59 +27,6 @@ constexpr int kMaxRois = 1024;
 constexpr int kLdsFirst = kMaxRois * 2;  // chunk starts of up to kLdsFirst - 1 frames in the rectangles' LDS
 constexpr int kStageCellsPerThread = 2;  // cells per thread when the ROIs fit one word
 
-// Conservative cell rectangle [x0, x1] x [y0, y1] of one ROI; empty when x0 > x1.
-__device__ void roi_cell_rect(const Config& c, const mmbev_roi_t& r, int16_t* out) {
-  const double u = 1.0 / 16777216.0;  // fp32 unit roundoff
-  double cx = r.cx, cy = r.cy, co = r.cos_yaw, si = r.sin_yaw, ex = r.ext_x, ey = r.ext_y;
-  int32_t x0 = 0, x1 = c.ncx - 1, y0 = 0, y1 = c.ncy - 1;
-  bool finite = isfinite(cx) && isfinite(cy) && isfinite(co) && isfinite(si) && isfinite(ex) && isfinite(ey);
-  if (finite && (ex < 0.0 || ey < 0.0)) {
-    x0 = 1;  // |l| <= negative extent never holds
-    x1 = 0;
-  } else if (finite) {
-    double n2 = co * co + si * si;
-    double hx = (fabs(co) * ex + fabs(si) * ey) / n2;
-    double hy = (fabs(si) * ex + fabs(co) * ey) / n2;
-    double mag = fabs(cx) + fabs(cy) + hx + hy;
-    for (int d = 0; d < 2; ++d) mag += fabs((double)c.mn[d]) + (double)c.vs[d] * (double)c.Df[d];
-    double pad = 1e-3 + 16.0 * u * mag;
-    if (isfinite(hx) && isfinite(hy) && isfinite(pad)) {
-      int32_t lim[2][2];
-      double ctr[2] = {cx, cy}, half[2] = {hx, hy};
-      for (int d = 0; d < 2; ++d) {
-        double lo = (ctr[d] - half[d] - pad - (double)c.mn[d]) / (double)c.vs[d];
-        double hi = (ctr[d] + half[d] + pad - (double)c.mn[d]) / (double)c.vs[d];
-        double D = (double)c.Df[d];
-        lo = fmin(fmax(floor(lo) - (double)c.cell_pad, -1.0), D);
-        hi = fmin(fmax(floor(hi) + (double)c.cell_pad, -1.0), D);
-        int32_t ilo = (int32_t)lo, ihi = (int32_t)hi;
-        if (ihi < 0 || ilo >= (int32_t)D) {
-          lim[d][0] = 1;
-          lim[d][1] = 0;
-        } else {
-          ilo = max(ilo, 0);
-          ihi = min(ihi, (int32_t)D - 1);
-          lim[d][0] = ilo >> c.cell_shift;
-          lim[d][1] = ihi >> c.cell_shift;
-        }
-      }
-      x0 = lim[0][0];
-      x1 = lim[0][1];
-      y0 = lim[1][0];
-      y1 = lim[1][1];
-    }
-  }
-  out[0] = (int16_t)x0;
-  out[1] = (int16_t)x1;
-  out[2] = (int16_t)y0;
-  out[3] = (int16_t)y1;
-}
-
-// Filter chunks of a frame of n points: whole workgroups of kWaves chunks.
-__device__ __forceinline__ uint32_t frame_chunks(uint32_t n, uint32_t P) {
-  return (n + P - 1) / P + kWaves - 1 - ((n + P - 1) / P + kWaves - 1) % kWaves;
-}
-
 // The opening workgroup: counters, offset checks, filter chunk table and
 // the frame of every filter workgroup.  s_first: LDS for kLdsFirst words;
 // s_bad: one LDS word.  Point offsets that break the contract lay out no
@@ -101,12 +48,7 @@ __device__ void open_call(const Config& c, uint32_t* s_tmp, uint32_t* s_first, i
       own0 = o;
       own1 = on;
     }
-    if (f == 0 && o != 0) bad |= MMBEV_FAULT_POINT_OFFSETS;
-    if (f == c.B && o != (int64_t)c.N) bad |= MMBEV_FAULT_POINT_OFFSETS;
-    if (f < c.B && on < o) bad |= MMBEV_FAULT_POINT_OFFSETS;
-    if (f == 0 && ro != 0) bad |= MMBEV_FAULT_ROI_OFFSETS;
-    if (f == c.B && ro != c.R) bad |= MMBEV_FAULT_ROI_OFFSETS;
-    if (f < c.B && (rn < ro || rn - ro > c.max_rois)) bad |= MMBEV_FAULT_ROI_OFFSETS;
+    bad |= offset_faults(c, f, o, on, ro, rn);
   }
   if (tid == 0) {
     h->fault = 0;

@@ -130,10 +130,12 @@ def test_edge_cases(gpu_lib):
     check(gpu_lib, empty_mid, label="empty middle frame", desc=wl.roi_desc)
 
 
-@pytest.mark.parametrize("frames", [2047, 2100, 4100])
+@pytest.mark.parametrize("frames", [255, 256, 2047, 2100, 4100])
 def test_many_small_frames(gpu_lib, frames):
-    """Frame counts on both sides of the stage's LDS copy of the chunk starts
-    (up to 2,047 frames; beyond, each frame's thread writes its filter
+    """Frame counts on both sides of the point filter's own layout of the
+    call (up to 255 frames of at most 32 ROIs, one frame per thread; beyond,
+    the staging kernel lays it out), of the stage's LDS copy of the chunk
+    starts (up to 2,047 frames; beyond, each frame's thread writes its filter
     workgroups' frame itself) and of the segments' per-frame tables in LDS
     (up to 4,096 frames; beyond, in the workspace), with every seventh frame
     emptied."""
@@ -189,14 +191,16 @@ def test_device_fault_word_reports_bad_offsets(gpu_lib):
     assert vz.fault() & gpu_lib.FAULT_ROI_OFFSETS
 
 
-def test_fault_word_reports_offsets_of_late_frames(gpu_lib):
-    """Offsets that break the contract only in frame 150 of 200: the opening
-    workgroup's later waves check them, after the fault word is cleared.
-    Decreasing point offsets make the call keep nothing (frames would
-    overlap); every kernel still runs to its end."""
+@pytest.mark.parametrize("frames", [200, 300])
+def test_fault_word_reports_offsets_of_late_frames(gpu_lib, frames):
+    """Offsets that break the contract only in frame 150 of 200 (the point
+    filter lays out the call) or of 300 (the staging kernel does): waves past
+    the first check them, after the fault word is cleared.  Decreasing point
+    offsets make the call keep nothing (frames would overlap); every kernel
+    still runs to its end."""
     import torch
 
-    wl = synth.small(81, frames=200, beams=2, azimuths=16, sweeps=1, rois=4)
+    wl = synth.small(81, frames=frames, beams=2, azimuths=16, sweeps=1, rois=4)
     vz = gpu_lib.voxelizer_for_workload(wl, "cuda:0")
     vz.run()
     torch.cuda.synchronize()
@@ -207,7 +211,7 @@ def test_fault_word_reports_offsets_of_late_frames(gpu_lib):
     vz.run()
     torch.cuda.synchronize()
     assert vz.fault() == gpu_lib.FAULT_POINT_OFFSETS
-    assert vz.result()["voxel_offsets"].tolist() == [0] * 201
+    assert vz.result()["voxel_offsets"].tolist() == [0] * (frames + 1)
     vz.frame_offsets = torch.as_tensor(wl.frame_offsets).cuda()
     ro = wl.roi_offsets.copy()
     ro[150] = ro[151] + 1  # decreasing ROI offsets

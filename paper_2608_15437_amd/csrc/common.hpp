@@ -230,6 +230,35 @@ __device__ __forceinline__ uint32_t block_exclusive_scan(uint32_t v, uint32_t* s
   return wpre + x - v;
 }
 
+// Exclusive prefix sums of two values per thread over the workgroup (one
+// barrier pair for both); s_tmp holds 2 * WAVES words.
+template <int WAVES>
+__device__ __forceinline__ uint2 block_exclusive_scan2(uint32_t a, uint32_t b, uint32_t* s_tmp, uint2& total) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const uint32_t xa = wave_inclusive_sum(a), xb = wave_inclusive_sum(b);
+  if (lane == 63) {
+    s_tmp[wave] = xa;
+    s_tmp[WAVES + wave] = xb;
+  }
+  __syncthreads();
+  uint32_t pa = 0, pb = 0, ta = 0, tb = 0;
+#pragma unroll
+  for (int w = 0; w < WAVES; ++w) {
+    const uint32_t u = s_tmp[w], v = s_tmp[WAVES + w];
+    pa += (w < wave) ? u : 0u;
+    pb += (w < wave) ? v : 0u;
+    ta += u;
+    tb += v;
+  }
+  __syncthreads();
+  total = make_uint2(ta, tb);
+  return make_uint2(pa + xa - a, pb + xb - b);
+}
+
+// kLds: the frame starts are built in LDS (B <= kSegLdsFrames) and copied
+// out at the end; otherwise in the workspace directly.  (One address space per
+// instance: a pointer that may be either compiles to generic instructions,
+// whose waits cover both kinds of access.)
 constexpr size_t kSpareTileBytes = 1024;  // one wave's 16-byte loads
 constexpr uint32_t kNoFrame = 0xffffffffu;  // wg_frame of a filter workgroup past the last chunk
 

@@ -644,8 +644,7 @@ struct FuseLds {
   int16_t rect[32][4];              // cell rectangles of the frame's ROIs
   uint32_t area[33];                // their cells before ROI j (exclusive prefix), then the total
   uint32_t bud[32];                 // their sweep budgets
-  uint32_t tmp[kWaves];
-  int32_t bad;
+  uint32_t tmp[2 * kWaves];
 };
 static_assert(sizeof(FuseLds) <= kWaves * sizeof(WaveLds), "fits the waves' queues");
 
@@ -671,20 +670,20 @@ __device__ __forceinline__ FuseLayout fuse_layout(const Config& c, FuseLds& F) {
   const int64_t o = c.frame_off[f], on = c.frame_off[fn];
   const int32_t ro = c.roi_off[f], rn = c.roi_off[fn];
   const int32_t bad = tid <= c.B ? offset_faults(c, f, o, on, ro, rn) : 0;
-  if (tid == 0) F.bad = 0;
-  __syncthreads();
-  if (bad) atomicOr(&F.bad, bad);
-  __syncthreads();
-  const int32_t allbad = F.bad;
-  const bool no_points = (allbad & MMBEV_FAULT_POINT_OFFSETS) != 0;
   const uint32_t p0 = (uint32_t)min(max(o, (int64_t)0), (int64_t)c.N);
   const uint32_t p1 = max((uint32_t)min(max(on, (int64_t)0), (int64_t)c.N), p0);
-  const uint32_t mine = tid < c.B && !no_points ? frame_chunks(p1 - p0, (uint32_t)c.fchunk_points) : 0u;
-  uint32_t total;
-  const uint32_t run = block_exclusive_scan(mine, F.tmp, total);
+  const uint32_t mine = tid < c.B ? frame_chunks(p1 - p0, (uint32_t)c.fchunk_points) : 0u;
+  // the chunk counts scanned, and the frames with bad point and bad ROI
+  // offsets counted (at most 256 each) in the same pass
+  const uint32_t badc = (bad & MMBEV_FAULT_POINT_OFFSETS ? 1u : 0u) | (bad & MMBEV_FAULT_ROI_OFFSETS ? 1u << 16 : 0u);
+  uint2 tot;
+  const uint32_t run = block_exclusive_scan2<kWaves>(mine, badc, F.tmp, tot).x;
+  const int32_t allbad = ((tot.y & 0xffffu) ? MMBEV_FAULT_POINT_OFFSETS : 0) | ((tot.y >> 16) ? MMBEV_FAULT_ROI_OFFSETS : 0);
+  // invalid point offsets lay out no chunk at all (frames could overlap)
+  const bool no_points = (allbad & MMBEV_FAULT_POINT_OFFSETS) != 0;
   const uint32_t cap = (uint32_t)c.fchunk_max;  // reached only with invalid offsets
-  const uint32_t nch = min(total, cap);
-  if (tid < c.B) F.first[tid] = min(run, cap);
+  const uint32_t nch = no_points ? 0u : min(tot.x, cap);
+  if (tid < c.B) F.first[tid] = no_points ? 0u : min(run, cap);
   if (tid == c.B) F.first[tid] = nch;
   if (tid <= c.B) F.roff[tid] = ro;
   __syncthreads();

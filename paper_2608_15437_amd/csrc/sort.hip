@@ -59,37 +59,7 @@ __device__ __forceinline__ uint64_t match_digit(uint32_t dig, bool valid) {
 constexpr int kSegBlock = 1024;  // threads of the segments kernel
 constexpr int kSegWaves = kSegBlock / 64;
 constexpr int kSegLdsFrames = 4096;  // frame starts kept in LDS up to this many frames
-
-// kLds: the frame starts are built in LDS (B <= kSegLdsFrames) and copied
-// out at the end; otherwise in the workspace directly.  (One address space per
-// instance: a pointer that may be either compiles to generic instructions,
-// whose waits cover both kinds of access.)
 constexpr int kSegPreLds = 16384;  // kept-pair prefixes of up to this many filter chunks kept in LDS (kLds instance)
-
-// Exclusive prefix sums of two values per thread over the workgroup (one
-// barrier pair for both); s_tmp holds 2 * WAVES words.
-template <int WAVES>
-__device__ __forceinline__ uint2 block_exclusive_scan2(uint32_t a, uint32_t b, uint32_t* s_tmp, uint2& total) {
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const uint32_t xa = wave_inclusive_sum(a), xb = wave_inclusive_sum(b);
-  if (lane == 63) {
-    s_tmp[wave] = xa;
-    s_tmp[WAVES + wave] = xb;
-  }
-  __syncthreads();
-  uint32_t pa = 0, pb = 0, ta = 0, tb = 0;
-#pragma unroll
-  for (int w = 0; w < WAVES; ++w) {
-    const uint32_t u = s_tmp[w], v = s_tmp[WAVES + w];
-    pa += (w < wave) ? u : 0u;
-    pb += (w < wave) ? v : 0u;
-    ta += u;
-    tb += v;
-  }
-  __syncthreads();
-  total = make_uint2(ta, tb);
-  return make_uint2(pa + xa - a, pb + xb - b);
-}
 
 // kLds: the frame starts are built in LDS (B <= kSegLdsFrames) and copied
 // out at the end; otherwise in the workspace directly.  (One address space per

@@ -371,6 +371,7 @@ mmbev_status_t voxelize(const mmbev_points_t* points, const uint8_t* sweep_ids, 
   // tables itself, and the staging kernel is not launched
   c.fuse_stage = p.W == 1 && p.B <= kFuseFrames && c.lds_pose_cap == p.S && c.lds_bm_cap == p.S * p.W &&
                  c.lds_cell_cap == p.ncells + 1 && c.lds_roi_cap >= p.max_rois && p.S <= kBlock;
+  c.small_call = p.fchunk_max <= kSmallChunks;
   c.schunk_max = (int32_t)p.schunk_max;
   c.vtile_max = (int32_t)p.vtile_max;
   c.mean_grid = (int32_t)p.mean_grid;
@@ -386,7 +387,7 @@ mmbev_status_t voxelize(const mmbev_points_t* points, const uint8_t* sweep_ids, 
   // sorted pairs ping-pong: keys compacted into [1], pass p writes [p % 2];
   // pass 0 reads no values, its value for each key is the key's compacted
   // position
-  MMBEV_TRY(launch_segments(c, s));
+  MMBEV_TRY(c.small_call ? hipSuccess : launch_segments(c, s));
   MMBEV_TRY(launch_compact(c, c.keys[1], s));
   for (int pass = 0; pass < c.passes; ++pass)
     MMBEV_TRY(launch_radix_pass(c, pass, c.keys[1 - pass % 2], pass == 0 ? nullptr : c.vals[1 - pass % 2],

@@ -26,6 +26,7 @@ constexpr int kMaxLdsFrames = 64;     // frames of one filter workgroup staged i
 constexpr int kMaxLdsRois = 256;      // ROI records of one filter workgroup staged in LDS
 constexpr int kMaxLdsBudgetWords = 256;
 constexpr int kMaxPoseLds = 64;       // (frame, sweep) poses of one filter workgroup staged in LDS
+constexpr int kSmallChunks = 2048;  // calls of at most this many filter chunks need no segments launch
 constexpr int kFuseFrames = kBlock - 1;  // frames of a call whose point filter lays out the call itself (one per thread)
 constexpr int kMaxCellSide = 64;      // coarse BEV cells per grid side (at most 64 x 64 per frame)
 constexpr int kMaxLdsCells = 4096;    // cell words of one filter workgroup staged in LDS (16 KB)
@@ -89,6 +90,7 @@ struct Config {
   int32_t kb, passes, dbits;
   int32_t vec;  // 16-byte vector loads allowed
   int32_t fuse_stage;  // the point filter lays out the call and builds its frame's tables (no staging kernel)
+  int32_t small_call;  // at most kSmallChunks filter chunks: the compaction launch does the segments kernel's work
   // out-of-ROI keep (Alg. 1 rate rho_out): threshold round(rho_out * 2^24)
   // on the top 24 bits of the point's SplitMix64 draw; 0 keeps none
   uint32_t bg_thr;

@@ -61,18 +61,16 @@ constexpr int kSegWaves = kSegBlock / 64;
 constexpr int kSegLdsFrames = 4096;  // frame starts kept in LDS up to this many frames
 constexpr int kSegPreLds = 16384;  // kept-pair prefixes of up to this many filter chunks kept in LDS (kLds instance)
 
-// kLds: the frame starts are built in LDS (B <= kSegLdsFrames) and copied
-// out at the end; otherwise in the workspace directly.  (One address space per
-// instance: a pointer that may be either compiles to generic instructions,
-// whose waits cover both kinds of access.)
-template <bool kLds>
-__global__ __launch_bounds__(kSegBlock) void segments_kernel(Config c) {
-  __shared__ uint32_t s_tmp[2 * kSegWaves];
-  __shared__ uint32_t s_fstart[kLds ? kSegLdsFrames + 1 : 1];  // frame starts
-  __shared__ uint32_t s_sfirst[kLds ? kSegLdsFrames + 1 : 1];  // first pair chunk of every frame
-  __shared__ uint32_t s_tfirst[kLds ? kSegLdsFrames + 1 : 1];  // first voxel tile of every frame
-  __shared__ uint32_t s_pre[kLds ? kSegPreLds + 1 : 1];        // kept pairs of the filter chunks before k
-  __shared__ unsigned long long s_most;  // (pairs, ~frame) of the frame with the most pairs
+// The segments kernel's work for a workgroup of BLOCK threads.  kLds: the
+// frame starts are built in LDS (B <= kSegLdsFrames, the s_ arrays hold
+// kSegLdsFrames + 1 words and s_pre kSegPreLds + 1) and copied out at the
+// end; otherwise in the workspace directly (the s_ arrays unused).  (One
+// address space per instance: a pointer that may be either compiles to
+// generic instructions, whose waits cover both kinds of access.)  s_tmp
+// holds 2 * BLOCK / 64 words.
+template <bool kLds, int BLOCK>
+__device__ __forceinline__ void segments_body(const Config& c, uint32_t* s_tmp, uint32_t* s_fstart, uint32_t* s_sfirst,
+                                              uint32_t* s_tfirst, uint32_t* s_pre, unsigned long long* s_most) {
   WsHeader* h = c.hdr;
   const int tid = threadIdx.x;
   const uint32_t nf = h->fchunks;
@@ -86,12 +84,12 @@ __global__ __launch_bounds__(kSegBlock) void segments_kernel(Config c) {
   constexpr bool lds = kLds;
   const bool pre_lds = kLds && nf < (uint32_t)kSegPreLds;  // uniform
   uint32_t* fstart = kLds ? s_fstart : c.fstart;
-  if (tid == 0) s_most = 0ull;
+  if (tid == 0) *s_most = 0ull;
   // kept-point prefix of the filter chunks.  Thread t holds kScanItems
   // consecutive chunks, read with 16-byte loads.
   static_assert(kScanItems % 4 == 0, "16-byte loads");
   uint32_t carry = 0;
-  for (uint32_t base = 0; base < nf; base += kSegBlock * kScanItems) {
+  for (uint32_t base = 0; base < nf; base += BLOCK * kScanItems) {
     const uint32_t first = base + tid * kScanItems;
     uint32_t v[kScanItems], sum = 0;
 #pragma unroll
@@ -109,7 +107,7 @@ __global__ __launch_bounds__(kSegBlock) void segments_kernel(Config c) {
 #pragma unroll
     for (int j = 0; j < kScanItems; ++j) sum += v[j];
     uint32_t total;
-    uint32_t run = carry + block_exclusive_scan<kSegWaves>(sum, s_tmp, total);
+    uint32_t run = carry + block_exclusive_scan<BLOCK / 64>(sum, s_tmp, total);
     uint32_t pre[kScanItems];
 #pragma unroll
     for (int j = 0; j < kScanItems; ++j) {
@@ -137,19 +135,19 @@ __global__ __launch_bounds__(kSegBlock) void segments_kernel(Config c) {
   // frame b starts at the prefix of its first chunk; frames after the last
   // chunk (and frame B) at K
   if (pre_lds) {  // uniform: the prefixes from LDS
-    for (int g = tid; g <= c.B; g += kSegBlock) {
+    for (int g = tid; g <= c.B; g += BLOCK) {
       const uint32_t k = min(g == tid ? ffirst : c.fchunk_first[g], nf);
       fstart[g] = k >= nf ? K : s_pre[k];
     }
   } else {
-    for (int g = tid; g <= c.B; g += kSegBlock) {
+    for (int g = tid; g <= c.B; g += BLOCK) {
       const uint32_t k = min(g == tid ? ffirst : c.fchunk_first[g], nf);
       fstart[g] = k >= nf ? K : c.fprefix[k];
     }
   }
   __syncthreads();
   if (lds)
-    for (int g = tid; g <= c.B; g += kSegBlock) c.fstart[g] = s_fstart[g];
+    for (int g = tid; g <= c.B; g += BLOCK) c.fstart[g] = s_fstart[g];
   // pair chunks (at most kMaxFrameChunks per frame, of frame_chunk_pairs
   // pairs: whole kSortTile multiples, the last one of a frame shorter) and
   // voxel tiles (kVoxTile sorted pairs, the last one of a frame shorter):
@@ -157,7 +155,7 @@ __global__ __launch_bounds__(kSegBlock) void segments_kernel(Config c) {
   // and tile written by its own thread (its frame found by a search over
   // the first indices: the last frame whose first index is at most its own)
   const uint32_t mt = chunk_min_tiles(K, c.B);
-  const int per = (c.B + kSegBlock - 1) / kSegBlock;
+  const int per = (c.B + BLOCK - 1) / BLOCK;
   const int b0 = tid * per;
   unsigned long long most = 0ull;
   uint32_t mine = 0, mine_vt = 0;
@@ -173,10 +171,10 @@ __global__ __launch_bounds__(kSegBlock) void segments_kernel(Config c) {
   {  // the wave's largest (pairs, ~frame): pairs first, then the frame among those
     const uint32_t hi = wave_max((uint32_t)(most >> 32));
     const uint32_t lo = wave_max((uint32_t)(most >> 32) == hi ? (uint32_t)most : 0u);
-    if ((tid & 63) == 0 && hi > 0u) atomicMax(&s_most, (unsigned long long)hi << 32 | lo);  // read after the scans' barriers
+    if ((tid & 63) == 0 && hi > 0u) atomicMax(s_most, (unsigned long long)hi << 32 | lo);  // read after the scans' barriers
   }
   uint2 tot;
-  const uint2 ex = block_exclusive_scan2<kSegWaves>(mine, mine_vt, s_tmp, tot);
+  const uint2 ex = block_exclusive_scan2<BLOCK / 64>(mine, mine_vt, s_tmp, tot);
   uint32_t run = ex.x, run_vt = ex.y;
   const uint32_t total = tot.x, total_vt = tot.y;
   const uint32_t cap = (uint32_t)c.schunk_max;  // never reached: the bound holds for any K <= N
@@ -207,7 +205,7 @@ __global__ __launch_bounds__(kSegBlock) void segments_kernel(Config c) {
     }
     return lo;
   };
-  for (uint32_t k = tid; k < nsc; k += kSegBlock) {
+  for (uint32_t k = tid; k < nsc; k += BLOCK) {
     const int32_t b = frame_of(sfirst, k);
     const uint32_t f0 = fstart[b], f1 = fstart[b + 1];
     const uint32_t CH = frame_chunk_pairs(f1 - f0, mt);
@@ -216,14 +214,14 @@ __global__ __launch_bounds__(kSegBlock) void segments_kernel(Config c) {
     c.schunk[k] = make_uint4(lo, min(lo + CH, f1), (uint32_t)b, f0);
     c.schunk_frame[k] = make_uint2(k0, k1);
   }
-  for (uint32_t t = tid; t < nvt; t += kSegBlock) {
+  for (uint32_t t = tid; t < nvt; t += BLOCK) {
     const int32_t b = frame_of(tfirst, t);
     const uint32_t f0 = fstart[b], f1 = fstart[b + 1];
     const uint32_t lo = f0 + (t - tfirst[b]) * kVoxTile;
     c.vtile[t] = make_uint4(lo, min(lo + kVoxTile, f1), (uint32_t)b, f0);
   }
   if (kLds)
-    for (int g = tid; g <= c.B; g += kSegBlock) {
+    for (int g = tid; g <= c.B; g += BLOCK) {
       c.schunk_first[g] = s_sfirst[g];
       c.vt_first[g] = s_tfirst[g];
     }
@@ -231,9 +229,42 @@ __global__ __launch_bounds__(kSegBlock) void segments_kernel(Config c) {
     h->schunks = nsc;
     h->vtiles = nvt;
     h->kept = K;
-    h->most_frame = ~(uint32_t)(s_most & 0xffffffffull);
-    h->most_pairs = (uint32_t)(s_most >> 32);
+    h->most_frame = ~(uint32_t)(*s_most & 0xffffffffull);
+    h->most_pairs = (uint32_t)(*s_most >> 32);
   }
+}
+
+template <bool kLds>
+__global__ __launch_bounds__(kSegBlock) void segments_kernel(Config c) {
+  __shared__ uint32_t s_tmp[2 * kSegWaves];
+  __shared__ uint32_t s_fstart[kLds ? kSegLdsFrames + 1 : 1];  // frame starts
+  __shared__ uint32_t s_sfirst[kLds ? kSegLdsFrames + 1 : 1];  // first pair chunk of every frame
+  __shared__ uint32_t s_tfirst[kLds ? kSegLdsFrames + 1 : 1];  // first voxel tile of every frame
+  __shared__ uint32_t s_pre[kLds ? kSegPreLds + 1 : 1];        // kept pairs of the filter chunks before k
+  __shared__ unsigned long long s_most;  // (pairs, ~frame) of the frame with the most pairs
+  segments_body<kLds, kSegBlock>(c, s_tmp, s_fstart, s_sfirst, s_tfirst, s_pre, &s_most);
+}
+
+// Sums of three values over the workgroup (s_tmp: 3 * WAVES words).
+template <int WAVES>
+__device__ __forceinline__ uint3 block_sum3(uint32_t a, uint32_t b, uint32_t d, uint32_t* s_tmp) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const uint32_t xa = wave_inclusive_sum(a), xb = wave_inclusive_sum(b), xd = wave_inclusive_sum(d);
+  if (lane == 63) {
+    s_tmp[wave] = xa;
+    s_tmp[WAVES + wave] = xb;
+    s_tmp[2 * WAVES + wave] = xd;
+  }
+  __syncthreads();
+  uint3 t = make_uint3(0u, 0u, 0u);
+#pragma unroll
+  for (int w = 0; w < WAVES; ++w) {
+    t.x += s_tmp[w];
+    t.y += s_tmp[WAVES + w];
+    t.z += s_tmp[2 * WAVES + w];
+  }
+  __syncthreads();
+  return t;
 }
 
 // One workgroup per filter chunk: its kept points, listed from the chunk's
@@ -251,22 +282,40 @@ constexpr int kCompactSmallChunk = 1024;  // chunks of at most this many points:
 // thread): two waves for small chunks (measured: an 8-frame batch of
 // 256-point chunks 24 -> 18.7 us), four for large ones (a 128-frame batch of
 // 2,816-point chunks 55 -> 64 us with two).
-template <int kCompactBlock>
-
+//
+// kSmall (calls of at most kSmallChunks filter chunks): no segments launch.
+// Each workgroup sums its own compact place and its frame's bounds from the
+// filter's chunk counts (all of them, loaded with its table entries), and
+// one more workgroup, the last, does the segments kernel's work (in the
+// workspace, for the radix passes and later kernels) beside the others: the
+// compaction needs none of it.
+template <int kCompactBlock, bool kSmall>
 __global__ __launch_bounds__(kCompactBlock) void compact_kernel(Config c, uint32_t* kout) {
   constexpr int kCompactWaves = kCompactBlock / 64;
+  constexpr int kSmallItems = kSmall ? kSmallChunks / kCompactBlock : 1;  // chunk counts per thread
   static_assert(kChunkWords <= kCompactBlock, "one bitmap word per thread");
   extern __shared__ float s_pose[];  // [S][12]
   __shared__ uint16_t s_list[kMaxChunkPoints];  // kept point offsets in the chunk, ascending
-  __shared__ uint32_t s_tmp[kCompactWaves];
+  __shared__ uint32_t s_tmp[3 * kCompactWaves];
+  __shared__ unsigned long long s_most;
   const int tid = threadIdx.x;
+  if (kSmall && blockIdx.x == gridDim.x - 1) {  // uniform: the segments kernel's work
+    segments_body<false, kCompactBlock>(c, s_tmp, nullptr, nullptr, nullptr, nullptr, &s_most);
+    return;
+  }
   const uint32_t k = blockIdx.x;
   // the chunk's table entries and bitmap (one word per thread) load together
   // with the chunk count: every address is in bounds for any k < fchunk_max
+  // (kSmall: every chunk's count too, at clamped indices)
   const uint32_t nch = c.hdr->fchunks;
-  const uint32_t lo = c.fchunk_lo[k], dst = c.fprefix[k], cnt = c.fcount[k];
+  const uint32_t lo = c.fchunk_lo[k], cnt = c.fcount[k];
+  uint32_t dst = kSmall ? 0u : c.fprefix[k];
   const uint32_t fr = c.fchunk_frame[k];
   uint32_t word = tid < c.fchunk_words ? c.fbits[(int64_t)k * c.fchunk_words + tid] : 0u;
+  uint32_t fcv[kSmallItems];
+#pragma unroll
+  for (int j = 0; j < kSmallItems; ++j)
+    fcv[j] = kSmall ? c.fcount[min((uint32_t)(tid + j * kCompactBlock), (uint32_t)c.fchunk_max - 1u)] : 0u;
   asm volatile("" ::"s"(lo), "s"(dst), "s"(cnt), "s"(fr));  // keeps the loads above the check
   if (k >= nch || cnt == 0u) return;  // uniform: past the chunks, or a chunk that kept no point
   const int32_t b = (int32_t)min(fr, (uint32_t)c.B - 1u);
@@ -281,7 +330,14 @@ __global__ __launch_bounds__(kCompactBlock) void compact_kernel(Config c, uint32
     const int e = tid + u * kCompactBlock;
     pv[u] = e < np ? c.poses[(int64_t)b * np + e] : 0.0f;
   }
-  const uint32_t fs = c.fstart[b], fe = c.fstart[b + 1];
+  uint32_t fs = 0, fe = 0, ff0 = 0, ff1 = 0;
+  if (kSmall) {  // the frame's first chunk and the next frame's, loaded with the poses
+    ff0 = c.fchunk_first[b];
+    ff1 = c.fchunk_first[b + 1];
+  } else {
+    fs = c.fstart[b];
+    fe = c.fstart[b + 1];
+  }
   // the bitmap's set bits listed at each word's rank
   uint32_t total;
   uint32_t r = block_exclusive_scan<kCompactWaves>((uint32_t)__popc(word), s_tmp, total);
@@ -344,6 +400,21 @@ __global__ __launch_bounds__(kCompactBlock) void compact_kernel(Config c, uint32
   // the first batch's point loads go out before the poses are stored (the
   // poses' loads were issued before the listing), so the two round trips overlap
   load_batch(0u);
+  if (kSmall) {  // kept points of the chunks before k, before the frame's first chunk and before the next frame's
+    uint32_t a0 = 0, a1 = 0, a2 = 0;
+#pragma unroll
+    for (int j = 0; j < kSmallItems; ++j) {
+      const uint32_t i = (uint32_t)(tid + j * kCompactBlock);
+      const uint32_t v = i < nch ? fcv[j] : 0u;
+      a0 += i < k ? v : 0u;
+      a1 += i < ff0 ? v : 0u;
+      a2 += i < ff1 ? v : 0u;
+    }
+    const uint3 t = block_sum3<kCompactWaves>(a0, a1, a2, s_tmp);
+    dst = t.x;
+    fs = t.y;
+    fe = t.z;
+  }
 #pragma unroll
   for (int u = 0; u < kPoseRegs; ++u)
     if (tid + u * kCompactBlock < np) s_pose[tid + u * kCompactBlock] = pv[u];
@@ -596,10 +667,17 @@ hipError_t launch_segments(const Config& c, hipStream_t st) {
 
 hipError_t launch_compact(const Config& c, uint32_t* kout, hipStream_t st) {
   const size_t lds = (size_t)c.S * 12 * sizeof(float);
-  if (c.fchunk_points <= kCompactSmallChunk)
-    hipLaunchKernelGGL(compact_kernel<128>, dim3(c.fchunk_max), dim3(128), lds, st, c, kout);
-  else
-    hipLaunchKernelGGL(compact_kernel<kBlock>, dim3(c.fchunk_max), dim3(kBlock), lds, st, c, kout);
+  const dim3 grid(c.fchunk_max + (c.small_call ? 1 : 0));  // small calls: one more workgroup for the segments' work
+  if (c.fchunk_points <= kCompactSmallChunk) {
+    if (c.small_call)
+      hipLaunchKernelGGL((compact_kernel<128, true>), grid, dim3(128), lds, st, c, kout);
+    else
+      hipLaunchKernelGGL((compact_kernel<128, false>), grid, dim3(128), lds, st, c, kout);
+  } else if (c.small_call) {
+    hipLaunchKernelGGL((compact_kernel<kBlock, true>), grid, dim3(kBlock), lds, st, c, kout);
+  } else {
+    hipLaunchKernelGGL((compact_kernel<kBlock, false>), grid, dim3(kBlock), lds, st, c, kout);
+  }
   return hipGetLastError();
 }
 

@@ -134,7 +134,7 @@ mmbev_status_t make_plan(const mmbev_grid_t* g, int64_t N, int32_t max_rois, int
     p->fchunk_max = (N + P - 1) / P + (int64_t)kWaves * p->B;  // each frame rounded up to whole workgroups
     p->filter_grid = std::max<int64_t>(1, (p->fchunk_max + kWaves - 1) / kWaves);
   }
-  p->schunk_max = std::min<int64_t>(N / kSortTile + p->B, (int64_t)kMaxFrameChunks * p->B) + 1;
+  p->schunk_max = std::min<int64_t>(N / (kSortTile / 2) + p->B, (int64_t)kMaxFrameChunks * p->B) + 1;  // half-tile chunks too
   p->vtile_max = N / kVoxTile + p->B + 1;
   p->mean_grid = std::min<int64_t>((n1 + kMeanTile - 1) / kMeanTile, 2048);  // measured best (1536 and 4096 slower)
   size_t o = 0;

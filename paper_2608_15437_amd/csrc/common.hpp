@@ -36,6 +36,7 @@ constexpr int kSortBins = 1 << kMaxDigitBits;  // 512
 constexpr int kSortItems = 8;         // pairs per thread in a scatter tile
 constexpr int kSortTile = kBlock * kSortItems;  // 2048 pairs
 constexpr int kCountItems = 16;       // pairs per thread per batch of the count kernel
+constexpr int kHalfTileFramePairs = 16 * kSortTile / 2;  // frames of at most this many pairs may take half-tile chunks
 constexpr int kMaxFrameChunks = 64;   // pair chunks of one frame at most (chunks never straddle frames)
 constexpr int kScanItems = 16;        // items per thread in the single-workgroup scans
 constexpr int kScanTile = kBlock * kScanItems;  // 4096
@@ -153,7 +154,7 @@ struct Config {
   // offset lds_cell: a zero word, then the cell words); a cap of 0 means
   // "not staged"
   int32_t lds_pose_cap, lds_roi_cap, lds_bm_cap, lds_cell_cap, lds_roi, lds_bm, lds_cell, lds_dyn_bytes;
-  int32_t schunk_max;      // bound on pair chunks: min(N / kSortTile + B, kMaxFrameChunks * B) + 1
+  int32_t schunk_max;      // bound on pair chunks: min(N / (kSortTile / 2) + B, kMaxFrameChunks * B) + 1
   int32_t vtile_max;       // bound on voxel tiles: N / kVoxTile + B + 1
   int32_t mean_grid;
 };
@@ -279,8 +280,13 @@ __device__ __forceinline__ int32_t frame_of_chunk(const uint32_t* first, int32_t
 }
 
 // Pairs per chunk of a frame of n kept pairs: at most kMaxFrameChunks
-// chunks, each a whole number of scatter tiles, at least min_tiles of them.
-__device__ __forceinline__ uint32_t frame_chunk_pairs(uint32_t n, uint32_t min_tiles) {
+// chunks, each a whole number of scatter tiles, at least min_tiles of them;
+// half tiles (the scatter ranks a chunk of at most half a tile four rounds
+// per wave instead of eight) for a frame of at most kHalfTileFramePairs
+// pairs when the call allows them (half: its half-tile chunks fit one round
+// of the scatter's resident workgroups).
+__device__ __forceinline__ uint32_t frame_chunk_pairs(uint32_t n, uint32_t min_tiles, bool half) {
+  if (half && n <= (uint32_t)kHalfTileFramePairs) return (uint32_t)kSortTile / 2u;
   uint32_t ch = (n + kMaxFrameChunks - 1) / kMaxFrameChunks;
   ch = (ch + kSortTile - 1) / kSortTile * kSortTile;
   return max(ch, min_tiles * (uint32_t)kSortTile);
@@ -294,6 +300,14 @@ __device__ __forceinline__ uint32_t chunk_min_tiles(uint32_t K, int32_t B) {
   if ((uint32_t)B >= kResident) return 1u;
   const uint32_t room = (kResident - (uint32_t)B) * (uint32_t)kSortTile;
   return min(max((K + room - 1) / room, 1u), 8u);
+}
+
+// Whether the call's frames of at most kHalfTileFramePairs pairs take
+// half-tile chunks: all the call's pairs in half tiles (plus one partial
+// chunk per frame) fit one round of the scatter's resident workgroups.
+__device__ __forceinline__ bool half_tile_chunks(uint32_t K, int32_t B) {
+  constexpr uint32_t kResident = kScatterPerCu * kCus;
+  return (uint64_t)(K + kSortTile / 2 - 1) / (kSortTile / 2) + (uint64_t)B <= kResident;
 }
 
 // Point frame offset b clamped into [0, N].

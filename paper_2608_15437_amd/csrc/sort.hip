@@ -155,6 +155,7 @@ __device__ __forceinline__ void segments_body(const Config& c, uint32_t* s_tmp, 
   // and tile written by its own thread (its frame found by a search over
   // the first indices: the last frame whose first index is at most its own)
   const uint32_t mt = chunk_min_tiles(K, c.B);
+  const bool half = half_tile_chunks(K, c.B);
   const int per = (c.B + BLOCK - 1) / BLOCK;
   const int b0 = tid * per;
   unsigned long long most = 0ull;
@@ -163,7 +164,7 @@ __device__ __forceinline__ void segments_body(const Config& c, uint32_t* s_tmp, 
     const int b = b0 + j;
     if (b < c.B) {
       const uint32_t n = fstart[b + 1] - fstart[b];
-      mine += (n + frame_chunk_pairs(n, mt) - 1) / frame_chunk_pairs(n, mt);
+      mine += (n + frame_chunk_pairs(n, mt, half) - 1) / frame_chunk_pairs(n, mt, half);
       most = max(most, (unsigned long long)n << 32 | (uint32_t)~(uint32_t)b);
       mine_vt += (n + kVoxTile - 1) / kVoxTile;
     }
@@ -188,7 +189,7 @@ __device__ __forceinline__ void segments_body(const Config& c, uint32_t* s_tmp, 
       const uint32_t n = fstart[b + 1] - fstart[b];
       sfirst[b] = min(run, cap);
       tfirst[b] = min(run_vt, cap_vt);
-      run += (n + frame_chunk_pairs(n, mt) - 1) / frame_chunk_pairs(n, mt);
+      run += (n + frame_chunk_pairs(n, mt, half) - 1) / frame_chunk_pairs(n, mt, half);
       run_vt += (n + kVoxTile - 1) / kVoxTile;
     }
   }
@@ -208,7 +209,7 @@ __device__ __forceinline__ void segments_body(const Config& c, uint32_t* s_tmp, 
   for (uint32_t k = tid; k < nsc; k += BLOCK) {
     const int32_t b = frame_of(sfirst, k);
     const uint32_t f0 = fstart[b], f1 = fstart[b + 1];
-    const uint32_t CH = frame_chunk_pairs(f1 - f0, mt);
+    const uint32_t CH = frame_chunk_pairs(f1 - f0, mt, half);
     const uint32_t k0 = sfirst[b], k1 = sfirst[b + 1];
     const uint32_t lo = f0 + (k - k0) * CH;
     c.schunk[k] = make_uint4(lo, min(lo + CH, f1), (uint32_t)b, f0);
@@ -475,14 +476,178 @@ struct ScatterLds {
   uint32_t scan_tmp[2][kWaves];
 };
 
+// A tile's pairs in the order (wave, round, lane): wave w holds pairs
+// [base + w * 64 * NR, base + (w + 1) * 64 * NR), NR rounds of 64 (NR =
+// kSortItems, or half of it for a chunk of at most half a tile).
+template <int NR>
 __device__ __forceinline__ void load_sort_tile(const uint32_t* kin, const uint32_t* vin, uint32_t base, uint32_t hi,
                                                uint32_t* key, uint32_t* val) {
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
 #pragma unroll
   for (int r = 0; r < kSortItems; ++r) {
-    const uint32_t i = base + wave * (64 * kSortItems) + r * 64 + lane;
-    key[r] = i < hi ? kin[i] : 0u;
-    val[r] = i < hi ? (vin != nullptr ? vin[i] : i) : 0u;  // no values: each key's own position
+    const uint32_t i = base + wave * (64 * NR) + r * 64 + lane;
+    const bool in = r < NR && i < hi;
+    key[r] = in ? kin[i] : 0u;
+    val[r] = in ? (vin != nullptr ? vin[i] : i) : 0u;  // no values: each key's own position
+  }
+}
+
+// One pair chunk k of the scatter (entries ch, fc), its tiles in the order
+// (wave, round, lane) with NR rounds of 64 per wave: kSortItems, or half of
+// it for a chunk of at most half a tile (every wave busy, half the rounds).
+template <int NR>
+__device__ __forceinline__ void scatter_chunk(const Config& c, ScatterLds& L, int pass, uint32_t k, const uint4 ch,
+                                              const uint2 fc, uint32_t K, const uint32_t* kin, const uint32_t* vin,
+                                              uint32_t* kout, uint32_t* vout) {
+  constexpr int kRows = 8;  // count rows in flight together
+  const int tid = threadIdx.x;
+  const int lane = tid & 63, wave = tid >> 6;
+  WsHeader* h = c.hdr;
+  const int shift = pass * c.dbits;
+  const uint32_t nbins = 1u << c.dbits;
+  const uint32_t mask = nbins - 1u;
+  const uint32_t e0 = 2u * (uint32_t)tid;  // this thread's digits e0 and e0 + 1
+  const bool d0 = e0 < nbins, d1 = e0 + 1u < nbins;
+  const uint32_t lo = ch.x, hi = ch.y;
+  uint32_t key[kSortItems], val[kSortItems], nkey[kSortItems], nval[kSortItems];
+  if (lo < hi) load_sort_tile<NR>(kin, vin, lo, hi, key, val);
+  // the first kRows count rows of the frame's chunks (at most
+  // kMaxFrameChunks rows) go out now and are summed after the first
+  // tile is ranked: digit bases = frame start + the frame's smaller
+  // digits + this digit in the frame's earlier chunks
+  const uint32_t k0 = fc.x, k1 = max(fc.y, k0);
+  uint2 x[kRows];
+#pragma unroll
+  for (int u = 0; u < kRows; ++u)
+    x[u] = k0 + u < k1 ? *reinterpret_cast<const uint2*>(c.cnt + (int64_t)(k0 + u) * kSortBins + e0) : make_uint2(0u, 0u);
+  uint32_t run0 = 0, run1 = 0;  // output position of the next pair of digit e0, e0 + 1
+  for (uint32_t base = lo; base < hi; base += kSortTile) {
+    const bool first = base == lo;
+    const bool more = base + kSortTile < hi;
+    if (more) load_sort_tile<NR>(kin, vin, base + kSortTile, hi, nkey, nval);
+    for (uint32_t e = tid; e < kWaves * kSortBins; e += kBlock) (&L.wave_cnt[0][0])[e] = 0u;
+    __syncthreads();  // also: the previous tile's reads of pos and kv are done
+    uint32_t rank[kSortItems];
+    bool valid[kSortItems];
+#pragma unroll
+    for (int r = 0; r < kSortItems; ++r) valid[r] = r < NR && base + wave * (64 * NR) + r * 64 + lane < hi;
+    auto dig = [&](int r) -> uint32_t { return (key[r] >> shift) & mask; };  // recomputed: fewer live registers
+    // wave multi-split over the rounds (tile order: wave, round, lane): the
+    // first lane of each digit's group adds the group's size to the wave's
+    // count of that digit with an LDS atomic that returns the count before
+    // it.  A wave's LDS operations complete in issue order, so the rounds'
+    // atomics go out back to back; each lane then takes its group's count
+    // from the group's first lane (bpermute) and adds its place in the group.
+    {
+      uint32_t old[kSortItems];
+#pragma unroll
+      for (int r = NR; r < kSortItems; ++r) rank[r] = 0u;  // rounds a half-tile chunk does not use
+#pragma unroll
+      for (int r = 0; r < NR; ++r) {
+        const uint64_t mm = match_digit(dig(r), valid[r]);
+        const uint32_t below = count_below(mm);
+        rank[r] = (uint32_t)(mm != 0ull ? __builtin_ctzll(mm) : 0) << 8 | below;  // the group's first lane, the lane's place
+        old[r] = 0u;
+        if (valid[r] && below == 0) old[r] = atomicAdd(&L.wave_cnt[wave][dig(r)], (uint32_t)__popcll(mm));
+      }
+#pragma unroll
+      for (int r = 0; r < NR; ++r) {
+        const uint32_t prior = (uint32_t)__builtin_amdgcn_ds_bpermute((int)(rank[r] >> 8) << 2, (int)old[r]);
+        rank[r] = prior + (rank[r] & 0xffu);
+      }
+    }
+    uint32_t ft0 = 0, ft1 = 0, pre0 = 0, pre1 = 0;  // the frame's totals of e0, e1 and their count in earlier chunks
+    if (first) {  // uniform
+      for (uint32_t kk = k0;; kk += kRows) {
+#pragma unroll
+        for (int u = 0; u < kRows; ++u) {
+          const uint32_t a = d0 ? x[u].x : 0u, b = d1 ? x[u].y : 0u;
+          if (kk + u < k) {
+            pre0 += a;
+            pre1 += b;
+          }
+          ft0 += a;
+          ft1 += b;
+        }
+        if (kk + kRows >= k1) break;
+#pragma unroll
+        for (int u = 0; u < kRows; ++u) {  // the next rows' loads in flight together
+          const uint32_t kr = kk + kRows + u;
+          x[u] = kr < k1 ? *reinterpret_cast<const uint2*>(c.cnt + (int64_t)kr * kSortBins + e0) : make_uint2(0u, 0u);
+        }
+      }
+    }
+    __syncthreads();  // the wave counts are complete
+    // per digit: the tile's count, each wave's first place inside the
+    // tile's run of that digit; one scan over the digits for the tile
+    // and, on a chunk's first tile, one for the frame's totals
+    const uint2* wc = reinterpret_cast<const uint2*>(&L.wave_cnt[0][0]);
+    uint2 cw[kWaves];
+#pragma unroll
+    for (int w = 0; w < kWaves; ++w) cw[w] = wc[w * (kSortBins / 2) + tid];
+    uint32_t t0 = 0, t1 = 0;
+#pragma unroll
+    for (int w = 0; w < kWaves; ++w) {
+      t0 += cw[w].x;
+      t1 += cw[w].y;
+    }
+    const uint32_t xt = wave_inclusive_sum(t0 + t1);
+    const uint32_t xf = first ? wave_inclusive_sum(ft0 + ft1) : 0u;
+    if (lane == 63) {
+      L.scan_tmp[0][wave] = xt;
+      L.scan_tmp[1][wave] = xf;
+    }
+    __syncthreads();
+    uint32_t wt = 0, wf = 0;
+#pragma unroll
+    for (int w = 0; w < kWaves; ++w)
+      if (w < wave) {
+        wt += L.scan_tmp[0][w];
+        wf += L.scan_tmp[1][w];
+      }
+    const uint32_t lo0 = wt + xt - (t0 + t1), lo1 = lo0 + t0;  // the digits' first places in the reordered tile
+    if (first) {
+      const uint32_t fb0 = ch.w + wf + xf - (ft0 + ft1);  // frame start + the frame's smaller digits
+      run0 = fb0 + pre0;
+      run1 = fb0 + ft0 + pre1;
+    }
+    uint2* wo = reinterpret_cast<uint2*>(&L.wave_cnt[0][0]);
+    uint32_t a0 = lo0, a1 = lo1;
+#pragma unroll
+    for (int w = 0; w < kWaves; ++w) {
+      wo[w * (kSortBins / 2) + tid] = make_uint2(a0, a1);
+      a0 += cw[w].x;
+      a1 += cw[w].y;
+    }
+    *reinterpret_cast<uint2*>(&L.pos[e0]) = make_uint2(run0 - lo0, run1 - lo1);  // position of tile place i: pos + i
+    run0 += t0;
+    run1 += t1;
+    __syncthreads();
+#pragma unroll
+    for (int r = 0; r < kSortItems; ++r)
+      if (valid[r]) L.kv[L.wave_cnt[wave][dig(r)] + rank[r]] = make_uint2(key[r], val[r]);
+    __syncthreads();
+    const uint32_t n_in = min((uint32_t)kSortTile, hi - base);
+#pragma unroll
+    for (int r = 0; r < kSortItems; ++r) {  // unrolled: the LDS reads of all rounds in flight together
+      const uint32_t i = (uint32_t)(r * kBlock + tid);
+      if (i < n_in) {
+        const uint2 kv = L.kv[i];
+        const uint32_t gp = L.pos[(kv.x >> shift) & mask] + i;
+        if (gp < K) {  // always true when the counts match the pairs
+          kout[gp] = kv.x;
+          vout[gp] = kv.y;
+        } else {
+          raise_fault(h, MMBEV_FAULT_INTERNAL);
+        }
+      }
+    }
+    if (more)
+#pragma unroll
+      for (int r = 0; r < kSortItems; ++r) {
+        key[r] = nkey[r];
+        val[r] = nval[r];
+      }
   }
 }
 
@@ -495,16 +660,8 @@ __global__ __launch_bounds__(kBlock, kScatterPerCu) void scatter_kernel(Config c
   __shared__ ScatterLds L;
   static_assert(sizeof(ScatterLds) <= 160 * 1024 / kScatterPerCu, "workgroups per CU");
   static_assert(kSortBins == 2 * kBlock, "two digits per thread");
-  constexpr int kRows = 8;  // count rows in flight together
-  const int tid = threadIdx.x;
-  const int lane = tid & 63, wave = tid >> 6;
   WsHeader* h = c.hdr;
   const uint32_t nsc = h->schunks, K = h->kept;
-  const int shift = pass * c.dbits;
-  const uint32_t nbins = 1u << c.dbits;
-  const uint32_t mask = nbins - 1u;
-  const uint32_t e0 = 2u * (uint32_t)tid;  // this thread's digits e0 and e0 + 1
-  const bool d0 = e0 < nbins, d1 = e0 + 1u < nbins;
   // chunks dealt to the XCDs in contiguous blocks: a frame's chunks share
   // one L2, where their neighbouring digit runs merge into whole lines and
   // their count rows are read once; a grid of resident size walks them
@@ -513,145 +670,11 @@ __global__ __launch_bounds__(kBlock, kScatterPerCu) void scatter_kernel(Config c
     if (k >= nsc) break;  // uniform
     const uint4 ch = c.schunk[k];
     const uint2 fc = c.schunk_frame[k];
-    const uint32_t lo = ch.x, hi = ch.y;
-    uint32_t key[kSortItems], val[kSortItems], nkey[kSortItems], nval[kSortItems];
-    if (lo < hi) load_sort_tile(kin, vin, lo, hi, key, val);
-    // the first kRows count rows of the frame's chunks (at most
-    // kMaxFrameChunks rows) go out now and are summed after the first
-    // tile is ranked: digit bases = frame start + the frame's smaller
-    // digits + this digit in the frame's earlier chunks
-    const uint32_t k0 = fc.x, k1 = max(fc.y, k0);
-    uint2 x[kRows];
-#pragma unroll
-    for (int u = 0; u < kRows; ++u)
-      x[u] = k0 + u < k1 ? *reinterpret_cast<const uint2*>(c.cnt + (int64_t)(k0 + u) * kSortBins + e0) : make_uint2(0u, 0u);
-    uint32_t run0 = 0, run1 = 0;  // output position of the next pair of digit e0, e0 + 1
-    for (uint32_t base = lo; base < hi; base += kSortTile) {
-      const bool first = base == lo;
-      const bool more = base + kSortTile < hi;
-      if (more) load_sort_tile(kin, vin, base + kSortTile, hi, nkey, nval);
-      for (uint32_t e = tid; e < kWaves * kSortBins; e += kBlock) (&L.wave_cnt[0][0])[e] = 0u;
-      __syncthreads();  // also: the previous tile's reads of pos and kv are done
-      uint32_t rank[kSortItems];
-      bool valid[kSortItems];
-#pragma unroll
-      for (int r = 0; r < kSortItems; ++r) valid[r] = base + wave * (64 * kSortItems) + r * 64 + lane < hi;
-      auto dig = [&](int r) -> uint32_t { return (key[r] >> shift) & mask; };  // recomputed: fewer live registers
-      // wave multi-split over the rounds (tile order: wave, round, lane): the
-      // first lane of each digit's group adds the group's size to the wave's
-      // count of that digit with an LDS atomic that returns the count before
-      // it.  A wave's LDS operations complete in issue order, so the rounds'
-      // atomics go out back to back; each lane then takes its group's count
-      // from the group's first lane (bpermute) and adds its place in the group.
-      {
-        uint32_t old[kSortItems];
-#pragma unroll
-        for (int r = 0; r < kSortItems; ++r) {
-          const uint64_t mm = match_digit(dig(r), valid[r]);
-          const uint32_t below = count_below(mm);
-          rank[r] = (uint32_t)(mm != 0ull ? __builtin_ctzll(mm) : 0) << 8 | below;  // the group's first lane, the lane's place
-          old[r] = 0u;
-          if (valid[r] && below == 0) old[r] = atomicAdd(&L.wave_cnt[wave][dig(r)], (uint32_t)__popcll(mm));
-        }
-#pragma unroll
-        for (int r = 0; r < kSortItems; ++r) {
-          const uint32_t prior = (uint32_t)__builtin_amdgcn_ds_bpermute((int)(rank[r] >> 8) << 2, (int)old[r]);
-          rank[r] = prior + (rank[r] & 0xffu);
-        }
-      }
-      uint32_t ft0 = 0, ft1 = 0, pre0 = 0, pre1 = 0;  // the frame's totals of e0, e1 and their count in earlier chunks
-      if (first) {  // uniform
-        for (uint32_t kk = k0;; kk += kRows) {
-#pragma unroll
-          for (int u = 0; u < kRows; ++u) {
-            const uint32_t a = d0 ? x[u].x : 0u, b = d1 ? x[u].y : 0u;
-            if (kk + u < k) {
-              pre0 += a;
-              pre1 += b;
-            }
-            ft0 += a;
-            ft1 += b;
-          }
-          if (kk + kRows >= k1) break;
-#pragma unroll
-          for (int u = 0; u < kRows; ++u) {  // the next rows' loads in flight together
-            const uint32_t kr = kk + kRows + u;
-            x[u] = kr < k1 ? *reinterpret_cast<const uint2*>(c.cnt + (int64_t)kr * kSortBins + e0) : make_uint2(0u, 0u);
-          }
-        }
-      }
-      __syncthreads();  // the wave counts are complete
-      // per digit: the tile's count, each wave's first place inside the
-      // tile's run of that digit; one scan over the digits for the tile
-      // and, on a chunk's first tile, one for the frame's totals
-      const uint2* wc = reinterpret_cast<const uint2*>(&L.wave_cnt[0][0]);
-      uint2 cw[kWaves];
-#pragma unroll
-      for (int w = 0; w < kWaves; ++w) cw[w] = wc[w * (kSortBins / 2) + tid];
-      uint32_t t0 = 0, t1 = 0;
-#pragma unroll
-      for (int w = 0; w < kWaves; ++w) {
-        t0 += cw[w].x;
-        t1 += cw[w].y;
-      }
-      const uint32_t xt = wave_inclusive_sum(t0 + t1);
-      const uint32_t xf = first ? wave_inclusive_sum(ft0 + ft1) : 0u;
-      if (lane == 63) {
-        L.scan_tmp[0][wave] = xt;
-        L.scan_tmp[1][wave] = xf;
-      }
-      __syncthreads();
-      uint32_t wt = 0, wf = 0;
-#pragma unroll
-      for (int w = 0; w < kWaves; ++w)
-        if (w < wave) {
-          wt += L.scan_tmp[0][w];
-          wf += L.scan_tmp[1][w];
-        }
-      const uint32_t lo0 = wt + xt - (t0 + t1), lo1 = lo0 + t0;  // the digits' first places in the reordered tile
-      if (first) {
-        const uint32_t fb0 = ch.w + wf + xf - (ft0 + ft1);  // frame start + the frame's smaller digits
-        run0 = fb0 + pre0;
-        run1 = fb0 + ft0 + pre1;
-      }
-      uint2* wo = reinterpret_cast<uint2*>(&L.wave_cnt[0][0]);
-      uint32_t a0 = lo0, a1 = lo1;
-#pragma unroll
-      for (int w = 0; w < kWaves; ++w) {
-        wo[w * (kSortBins / 2) + tid] = make_uint2(a0, a1);
-        a0 += cw[w].x;
-        a1 += cw[w].y;
-      }
-      *reinterpret_cast<uint2*>(&L.pos[e0]) = make_uint2(run0 - lo0, run1 - lo1);  // position of tile place i: pos + i
-      run0 += t0;
-      run1 += t1;
-      __syncthreads();
-#pragma unroll
-      for (int r = 0; r < kSortItems; ++r)
-        if (valid[r]) L.kv[L.wave_cnt[wave][dig(r)] + rank[r]] = make_uint2(key[r], val[r]);
-      __syncthreads();
-      const uint32_t n_in = min((uint32_t)kSortTile, hi - base);
-#pragma unroll
-      for (int r = 0; r < kSortItems; ++r) {  // unrolled: the LDS reads of all rounds in flight together
-        const uint32_t i = (uint32_t)(r * kBlock + tid);
-        if (i < n_in) {
-          const uint2 kv = L.kv[i];
-          const uint32_t gp = L.pos[(kv.x >> shift) & mask] + i;
-          if (gp < K) {  // always true when the counts match the pairs
-            kout[gp] = kv.x;
-            vout[gp] = kv.y;
-          } else {
-            raise_fault(h, MMBEV_FAULT_INTERNAL);
-          }
-        }
-      }
-      if (more)
-#pragma unroll
-        for (int r = 0; r < kSortItems; ++r) {
-          key[r] = nkey[r];
-          val[r] = nval[r];
-        }
-    }
+    // a chunk of at most half a tile: half the rounds per wave
+    if (ch.y - ch.x <= (uint32_t)kSortTile / 2u)  // uniform
+      scatter_chunk<kSortItems / 2>(c, L, pass, k, ch, fc, K, kin, vin, kout, vout);
+    else
+      scatter_chunk<kSortItems>(c, L, pass, k, ch, fc, K, kin, vin, kout, vout);
   }
 }
 

@@ -432,9 +432,42 @@ __global__ __launch_bounds__(kCompactBlock) void compact_kernel(Config c, uint32
   }
 }
 
-__global__ __launch_bounds__(kBlock) void count_kernel(Config c, int pass, const uint32_t* kin) {
-  __shared__ uint32_t s_hist[kWaves][kSortBins];  // one histogram per wave, summed at the end
+// The digit counts of pair chunk k ([lo, hi)) into row k.  Q histogram
+// copies per wave (lane % Q; rows padded by a word, so that one digit's
+// copies lie in different LDS banks): for chunks of more than one tile,
+// where the atomics of lanes on one digit are the cost, four; else one (the
+// copies' clearing and summing cost more than they save).
+template <int Q>
+__device__ __forceinline__ void count_chunk(const Config& c, uint32_t* s_hist, uint32_t k, uint32_t lo, uint32_t hi,
+                                            const uint32_t* kin, int shift, uint32_t mask, uint32_t nbins) {
+  constexpr int kRow = kSortBins + 1;
   const int tid = threadIdx.x, wave = tid >> 6;
+  uint32_t* hw = s_hist + (wave * Q + tid % Q) * kRow;
+  for (uint32_t e = tid; e < (uint32_t)(kWaves * Q * kRow); e += kBlock) s_hist[e] = 0;
+  __syncthreads();
+  for (uint32_t base = lo; base < hi; base += kBlock * kCountItems) {
+    uint32_t key[kCountItems];
+#pragma unroll
+    for (int j = 0; j < kCountItems; ++j) {  // all loads of the batch in flight together
+      const uint32_t i = base + j * kBlock + tid;
+      key[j] = i < hi ? kin[i] : 0u;
+    }
+#pragma unroll
+    for (int j = 0; j < kCountItems; ++j)
+      if (base + j * kBlock + tid < hi) atomicAdd(&hw[(key[j] >> shift) & mask], 1u);
+  }
+  __syncthreads();
+  for (uint32_t e = tid; e < nbins; e += kBlock) {
+    uint32_t t = 0;
+#pragma unroll
+    for (int w = 0; w < kWaves * Q; ++w) t += s_hist[w * kRow + e];
+    c.cnt[(int64_t)k * kSortBins + e] = t;
+  }
+  __syncthreads();  // the next chunk clears the histograms
+}
+
+__global__ __launch_bounds__(kBlock) void count_kernel(Config c, int pass, const uint32_t* kin) {
+  __shared__ uint32_t s_hist[kWaves * 4 * (kSortBins + 1)];  // per wave up to four histogram copies
   // the first chunk's entry loads with the chunk count (in bounds: the grid is at most schunk_max)
   const uint32_t nsc = c.hdr->schunks;
   uint4 ch = c.schunk[blockIdx.x];
@@ -444,28 +477,10 @@ __global__ __launch_bounds__(kBlock) void count_kernel(Config c, int pass, const
   const uint32_t mask = nbins - 1u;
   for (uint32_t k = blockIdx.x; k < nsc; k += gridDim.x) {  // a grid of resident size walks the chunks
     if (k != blockIdx.x) ch = c.schunk[k];
-    for (uint32_t e = tid; e < kWaves * kSortBins; e += kBlock) (&s_hist[0][0])[e] = 0;
-    __syncthreads();
-    const uint32_t lo = ch.x, hi = ch.y;
-    for (uint32_t base = lo; base < hi; base += kBlock * kCountItems) {
-      uint32_t key[kCountItems];
-#pragma unroll
-      for (int j = 0; j < kCountItems; ++j) {  // all loads of the batch in flight together
-        const uint32_t i = base + j * kBlock + tid;
-        key[j] = i < hi ? kin[i] : 0u;
-      }
-#pragma unroll
-      for (int j = 0; j < kCountItems; ++j)
-        if (base + j * kBlock + tid < hi) atomicAdd(&s_hist[wave][(key[j] >> shift) & mask], 1u);
-    }
-    __syncthreads();
-    for (uint32_t e = tid; e < nbins; e += kBlock) {
-      uint32_t t = 0;
-#pragma unroll
-      for (int w = 0; w < kWaves; ++w) t += s_hist[w][e];
-      c.cnt[(int64_t)k * kSortBins + e] = t;
-    }
-    __syncthreads();  // the next chunk clears the histograms
+    if (ch.y - ch.x > (uint32_t)kSortTile)  // uniform
+      count_chunk<4>(c, s_hist, k, ch.x, ch.y, kin, shift, mask, nbins);
+    else
+      count_chunk<1>(c, s_hist, k, ch.x, ch.y, kin, shift, mask, nbins);
   }
 }
 

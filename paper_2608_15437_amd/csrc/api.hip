@@ -365,12 +365,17 @@ mmbev_status_t voxelize(const mmbev_points_t* points, const uint8_t* sweep_ids, 
   c.lds_roi = c.lds_pose_cap * 12;
   c.lds_bm = c.lds_roi + 6 * c.lds_roi_cap;
   c.lds_cell = c.lds_bm + c.lds_bm_cap;
-  c.lds_dyn_bytes = (int32_t)(((size_t)(c.lds_cell + c.lds_cell_cap) * 4 + 15) / 16 * 16);
-  // one ROI word per cell, every table of a frame in LDS and a thread per
-  // frame: each filter workgroup lays out the call and builds its frame's
-  // tables itself, and the staging kernel is not launched
-  c.fuse_stage = p.W == 1 && p.B <= kFuseFrames && c.lds_pose_cap == p.S && c.lds_bm_cap == p.S * p.W &&
-                 c.lds_cell_cap == p.ncells + 1 && c.lds_roi_cap >= p.max_rois && p.S <= kBlock;
+  // every table of a frame in LDS and a thread per frame: each filter
+  // workgroup lays out the call and builds its frame's tables itself, and the
+  // staging kernel is not launched; with several ROI words per cell only for
+  // a few frames whose cells' words fit in LDS too (they take a larger share
+  // of the filter's LDS, which a few frames' workgroups can afford)
+  const bool fits = p.B <= kFuseFrames && c.lds_pose_cap == p.S && c.lds_bm_cap == p.S * p.W &&
+                    c.lds_cell_cap == p.ncells + 1 && c.lds_roi_cap >= p.max_rois && p.S <= kBlock;
+  c.fuse_stage = fits && (p.W == 1 || (p.B <= kFuseWideFrames && (int64_t)p.ncells * p.W <= kFuseWordCap));
+  c.lds_wmask = c.fuse_stage && p.W > 1 ? c.lds_cell + c.lds_cell_cap : -1;
+  const int32_t lds_words = c.lds_wmask >= 0 ? c.lds_wmask + p.ncells * p.W : c.lds_cell + c.lds_cell_cap;
+  c.lds_dyn_bytes = (int32_t)(((size_t)lds_words * 4 + 15) / 16 * 16);
   c.small_call = p.fchunk_max <= kSmallChunks;
   c.schunk_max = (int32_t)p.schunk_max;
   c.vtile_max = (int32_t)p.vtile_max;

@@ -96,9 +96,10 @@ __device__ __forceinline__ void wave_lds_sync() {
 }
 
 // ST: everything the workgroup needs (ROI offsets, poses, budget masks, ROI
-// records) is staged in LDS, so every lookup below is a plain LDS read.
-// Without ST every lookup reads global memory.
-template <bool ST>
+// records) is staged in LDS, so every lookup below is a plain LDS read
+// (ST == 2: the cells' ROI words too, when a frame has several).  Without ST
+// (0) every lookup reads global memory.
+template <int ST>
 __device__ __forceinline__ void load_pose(const Config& c, const FilterLds& L, int32_t b, uint32_t s, float* P) {
   if (ST) {
     const float* src = lds_pose((b - L.f0) * c.S + s);
@@ -111,19 +112,19 @@ __device__ __forceinline__ void load_pose(const Config& c, const FilterLds& L, i
   }
 }
 
-template <bool ST>
+template <int ST>
 __device__ __forceinline__ uint32_t budget_word(const Config& c, const FilterLds& L, int32_t b, uint32_t s, int w) {
   if (ST) return lds_bm(c)[((b - L.f0) * c.S + s) * c.W + w];
   return c.budgetmask[((int64_t)b * c.S + s) * c.W + w];
 }
 
-template <bool ST>
+template <int ST>
 __device__ __forceinline__ int32_t frame_roi_base(const Config& c, const FilterLds& L, int32_t b) {
   if (ST) return L.roff[b - L.f0];
   return min(max(c.roi_off[b], 0), c.R);
 }
 
-template <bool ST>
+template <int ST>
 __device__ __forceinline__ bool roi_hit(const Config& c, const FilterLds& L, int32_t gj, float px, float py) {
   mmbev_roi_t r;
   if (ST) {
@@ -181,7 +182,7 @@ __device__ __forceinline__ bool quantize_fast(const Config& c, float px, float p
 // walking its own bits and stopping at its first hit.  (A loop shared by the
 // wave, one broadcast read per distinct ROI, measured slower: most lanes hit
 // their first ROI.)
-template <bool ST>
+template <int ST>
 __device__ __forceinline__ bool roi_test_one_word(const Config& c, const FilterLds& L, int32_t r0, uint32_t cand,
                                                   float px, float py) {
   bool hit = false;
@@ -196,12 +197,24 @@ __device__ __forceinline__ bool roi_test_one_word(const Config& c, const FilterL
 
 // Phase B, more than 32 ROIs per frame: the ROIs of the point's cell that
 // admit its sweep, word by word, tested lane by lane.
-template <bool ST>
+template <int ST>
 __device__ __forceinline__ bool roi_test_words(const Config& c, const FilterLds& L, int32_t b, uint32_t s,
                                                int32_t r0, int32_t ix, int32_t iy, float px, float py) {
   const int32_t cell = (iy >> c.cell_shift) * c.ncx + (ix >> c.cell_shift);
-  const uint32_t* cm = c.cellmask + ((int64_t)b * c.ncells + cell) * c.W;
   bool hit = false;
+  if (ST == 2) {  // the word masks the filter built in LDS
+    const uint32_t* cm = reinterpret_cast<const uint32_t*>(filter_dyn) + c.lds_wmask + cell * c.W;
+    for (int w = 0; w < c.W && !hit; ++w) {
+      uint32_t m = cm[w] & budget_word<ST>(c, L, b, s, w);
+      while (m && !hit) {
+        const int k = __builtin_ctz(m);
+        m &= m - 1;
+        hit = roi_hit<ST>(c, L, r0 + w * 32 + k, px, py);
+      }
+    }
+    return hit;
+  }
+  const uint32_t* cm = c.cellmask + ((int64_t)b * c.ncells + cell) * c.W;
   for (int w = 0; w < c.W && !hit; ++w) {
     uint32_t m = cm[w] & budget_word<ST>(c, L, b, s, w);
     while (m && !hit) {
@@ -368,7 +381,7 @@ struct CellConsts {
   int32_t fr;        // staged: b - f0
 };
 
-template <bool ST>
+template <int ST>
 __device__ __forceinline__ CellConsts cell_consts(const Config& c, const FilterLds& L, int32_t b) {
   const int32_t fr = ST ? b - L.f0 : 0;
   CellConsts k{c.inv_vs[0], c.inv_vs[1], c.nmin_v[0], c.nmin_v[1], c.cell_pad,
@@ -415,7 +428,7 @@ struct QuadState {
 // single wave-wide read when the wave holds one sweep).
 // BG: the out-of-ROI keep rate is nonzero (without it no draw is made and
 // the code below is the ROI-only path).
-template <bool ST, bool BG>
+template <int ST, bool BG>
 __device__ __forceinline__ void phase_a(const Config& c, const CellConsts& kc, const FilterLds& L, int32_t b,
                                         uint32_t i0, const Quad& d, QuadState& st) {
   const uint32_t S = (uint32_t)c.S;
@@ -492,7 +505,7 @@ struct WaveRun {
 // store inside the tile loop would make the compiler wait for it (and, since
 // vector memory operations complete in order, for every tile load before it)
 // once its source registers are reused.
-template <bool ST, bool BG>
+template <int ST, bool BG>
 __device__ __forceinline__ void decide_round(const Config& c, const FilterLds& L, WaveLds& Q, WaveRun& wr,
                                              uint32_t n) {
   const uint32_t lane = (uint32_t)(threadIdx.x & 63);
@@ -524,7 +537,7 @@ __device__ __forceinline__ void decide_round(const Config& c, const FilterLds& L
 // admits the sweep, or drawn for the out-of-ROI keep)
 // appended in point order (lane, then q) to the wave's ring, deciding full
 // rounds of 64 as they become available.
-template <bool ST, bool BG>
+template <int ST, bool BG>
 __device__ __forceinline__ void phase_b(const Config& c, const FilterLds& L, WaveLds& Q, uint32_t i0,
                                         QuadState& st, WaveRun& wr) {
   bool has[4];
@@ -567,7 +580,7 @@ __device__ __forceinline__ void phase_b(const Config& c, const FilterLds& L, Wav
 // issues the same loads in the same order, and the loop over the steps has a
 // fixed trip count and no early exit, so the compiler's wait before a tile's
 // data counts exactly the loads of the tiles after it.
-template <bool ST, bool BG, int J>
+template <int ST, bool BG, int J>
 __device__ __forceinline__ void pipeline_step(const Config& c, const CellConsts& kc, const FilterLds& L, WaveLds& Q,
                                               int32_t b, const TileRows& rows, const TileRows& spare,
                                               uint32_t a0, uint32_t ntiles, uint32_t k0, uint32_t lane4,
@@ -591,7 +604,7 @@ __device__ __forceinline__ void pipeline_step(const Config& c, const CellConsts&
 // pipeline of kFilterDepth buffers with 16-byte loads (when the rows allow
 // them; otherwise every tile is loaded point by point): the loads of the
 // next kFilterDepth - 1 tiles are in flight while a tile is handled.
-template <bool VEC, bool ST, bool BG>
+template <bool VEC, int ST, bool BG>
 __device__ __forceinline__ void run_wave(const Config& c, const FilterLds& L, WaveLds& Q, int32_t b, uint32_t lo,
                                          uint32_t hi, WaveRun& wr) {
   const uint32_t lane = (uint32_t)(threadIdx.x & 63), lane4 = 4u * lane;
@@ -641,9 +654,9 @@ __device__ __forceinline__ void run_wave(const Config& c, const FilterLds& L, Wa
 struct FuseLds {
   uint32_t first[kFuseFrames + 1];  // first filter chunk of frame b
   int32_t roff[kFuseFrames + 1];    // ROI offsets as given
-  int16_t rect[32][4];              // cell rectangles of the frame's ROIs
-  uint32_t area[33];                // their cells before ROI j (exclusive prefix), then the total
-  uint32_t bud[32];                 // their sweep budgets
+  int16_t rect[kMaxLdsRois][4];     // cell rectangles of the frame's ROIs
+  uint32_t area[kMaxLdsRois + 1];   // their cells before ROI j (exclusive prefix), then the total
+  uint32_t bud[kMaxLdsRois];        // their sweep budgets
   uint32_t tmp[2 * kWaves];
 };
 static_assert(sizeof(FuseLds) <= kWaves * sizeof(WaveLds), "fits the waves' queues");
@@ -718,16 +731,20 @@ __device__ __forceinline__ FuseLayout fuse_layout(const Config& c, FuseLds& F) {
   return g;
 }
 
-// The fused instance's tables of frame f (one ROI word: at most 32 ROIs,
-// roi_n of them from roi_lo): poses, ROI records and budgets loaded
-// together; the budget word of every sweep and the frame's cell row (a zero
-// word, then per coarse cell the ROIs whose conservative rectangle covers
-// it) built in LDS from the records, as the staging kernel builds them.
+// The fused instance's tables of frame f (roi_n ROIs from roi_lo): poses,
+// ROI records and budgets loaded together; the budget words of every
+// (sweep, ROI word) and the frame's cell row (a zero word, then per coarse
+// cell the ROIs whose conservative rectangle covers it: with several ROI
+// words, their OR, and every word in the word masks at word lds_wmask of
+// the dynamic LDS) built in LDS from the records, as the staging kernel
+// builds them.
+template <bool WIDE>
 __device__ __forceinline__ void fuse_staging(const Config& c, FilterLds& L, FuseLds& F, int32_t f, int32_t roi_lo,
                                              int32_t roi_n, int32_t ro0, int32_t ro1) {
   constexpr int kPoseRegs = (kMaxPoseLds * 12 + kBlock - 1) / kBlock;
   const int tid = threadIdx.x;
   const int np = c.S * 12;
+  const int W = WIDE ? c.W : 1;
   float pv[kPoseRegs];
   const float* poses = c.poses + (int64_t)f * np;
 #pragma unroll
@@ -746,6 +763,8 @@ __device__ __forceinline__ void fuse_staging(const Config& c, FilterLds& L, Fuse
   for (int j = 0; j < kPoseRegs; ++j)
     if (tid + j * kBlock < np) dynf[tid + j * kBlock] = pv[j];  // pose rows from word 0
   for (int e = tid; e <= c.ncells; e += kBlock) dyn[c.lds_cell + e] = 0u;
+  if (WIDE)
+    for (int e = tid; e < c.ncells * W; e += kBlock) dyn[c.lds_wmask + e] = 0u;
   uint32_t area = 0;
   if (tid < roi_n) {
     dynf[c.lds_roi + 0 * c.lds_roi_cap + tid] = r.cx;
@@ -759,19 +778,30 @@ __device__ __forceinline__ void fuse_staging(const Config& c, FilterLds& L, Fuse
     area = rc[1] >= rc[0] && rc[3] >= rc[2] ? (uint32_t)(rc[1] - rc[0] + 1) * (uint32_t)(rc[3] - rc[2] + 1) : 0u;
     F.bud[tid] = bud;
   }
-  if (tid < 64) {  // wave 0: the rectangles' cell counts scanned (at most 32 ROIs)
-    const uint32_t x = wave_inclusive_sum(area);
-    if (tid < 32) F.area[tid] = x - area;
-    if (tid == 31) F.area[32] = x;
+  // the rectangles' cell counts scanned: one wave for at most 64 ROIs
+  // (always so with one ROI word), the workgroup otherwise
+  if (!WIDE || roi_n <= 64) {  // uniform
+    if (tid < 64) {
+      const uint32_t x = wave_inclusive_sum(area);
+      F.area[tid] = x - area;
+      if (tid == 63) F.area[kMaxLdsRois] = x;
+    }
+  } else {
+    uint32_t total;
+    const uint32_t ex = block_exclusive_scan(area, F.tmp, total);
+    F.area[tid] = ex;
+    if (tid == 0) F.area[kMaxLdsRois] = total;
   }
   __syncthreads();
-  if (tid < c.S) {  // sweep s: the ROIs whose budget admits it
-    uint32_t w = 0;
-    for (int j = 0; j < roi_n; ++j) w |= F.bud[j] > (uint32_t)tid ? 1u << j : 0u;
-    dyn[c.lds_bm + tid] = w;
+  if (tid < c.S * W) {  // (sweep s, ROI word w): the word's ROIs whose budget admits s
+    const int s = tid / W, w = tid % W;
+    uint32_t m = 0;
+    for (int j = 32 * w; j < min(32 * w + 32, roi_n); ++j) m |= F.bud[j] > (uint32_t)s ? 1u << (j & 31) : 0u;
+    dyn[c.lds_bm + tid] = m;
   }
   // every (ROI, covered cell) pair: the ROI's bit ORed into the cell's word
-  const uint32_t cells = F.area[32];
+  // (and, with several ROI words, into the cell's word of that ROI)
+  const uint32_t cells = F.area[kMaxLdsRois];
   for (uint32_t i = tid; i < cells; i += kBlock) {
     int32_t lo = 0, hi = roi_n - 1;  // the ROI: the last one whose first pair is at most i
     while (lo < hi) {
@@ -780,15 +810,16 @@ __device__ __forceinline__ void fuse_staging(const Config& c, FilterLds& L, Fuse
     }
     const int16_t* rc = F.rect[lo];
     const uint32_t q = i - F.area[lo], wx = (uint32_t)(rc[1] - rc[0] + 1);
-    const uint32_t cx = (uint32_t)rc[0] + q % wx, cy = (uint32_t)rc[2] + q / wx;
-    atomicOr(&dyn[c.lds_cell + 1 + cy * (uint32_t)c.ncx + cx], 1u << lo);
+    const uint32_t cell = ((uint32_t)rc[2] + q / wx) * (uint32_t)c.ncx + (uint32_t)rc[0] + q % wx;
+    atomicOr(&dyn[c.lds_cell + 1 + cell], 1u << (lo & 31));
+    if (WIDE) atomicOr(&dyn[c.lds_wmask + cell * (uint32_t)W + (uint32_t)(lo >> 5)], 1u << (lo & 31));
   }
 }
 
 // Workgroup w: its waves over filter chunks kWaves*w .. kWaves*w + 3.  Per
 // chunk it leaves the bitmap of its kept points, their number, its first
 // point and its frame.  BG: the out-of-ROI keep rate is nonzero.
-template <bool VEC, bool BG, bool FS>
+template <bool VEC, bool BG, int FS>
 __global__ __launch_bounds__(kBlock, 5) void filter_kernel(Config c) {
   __shared__ FilterLds L;
   __shared__ WaveLds Qs[kWaves];
@@ -871,7 +902,7 @@ __global__ __launch_bounds__(kBlock, 5) void filter_kernel(Config c) {
   }
   const bool staged = pl.staged;
   if (FS) {
-    if (pl.staged) fuse_staging(c, L, F, pl.f0, pl.roi_lo, pl.roi_n, ro0, ro1);
+    if (pl.staged) fuse_staging<FS == 2>(c, L, F, pl.f0, pl.roi_lo, pl.roi_n, ro0, ro1);
   } else if (staged) {
     do_staging(c, L, pl);
   }
@@ -880,9 +911,9 @@ __global__ __launch_bounds__(kBlock, 5) void filter_kernel(Config c) {
   if (k >= nchunks || (FS && !pl.staged)) return;
   WaveRun wr{0u, 0u, 0u, lo, b, k};
   if (staged)
-    run_wave<VEC, true, BG>(c, L, Q, b, lo, hi, wr);
+    run_wave<VEC, FS == 2 ? 2 : 1, BG>(c, L, Q, b, lo, hi, wr);
   else
-    run_wave<VEC, false, BG>(c, L, Q, b, lo, hi, wr);
+    run_wave<VEC, 0, BG>(c, L, Q, b, lo, hi, wr);
   if (lane == 0) {
     c.fcount[k] = wr.kept;
     c.fchunk_lo[k] = lo;
@@ -896,23 +927,35 @@ hipError_t launch_filter(const Config& c, hipStream_t st) {
   // one instance per load form and per rate (none, or a nonzero one)
   const dim3 grid(c.filter_grid), block(kBlock);
   const size_t dyn = (size_t)c.lds_dyn_bytes;
-  if (c.fuse_stage) {  // the filter lays out the call and builds its frame's tables itself
+  // FS: 0 the staging kernel's tables, 1 the filter's own (one ROI word
+  // per cell), 2 the filter's own with the cells' ROI words in LDS
+  const int fs = c.fuse_stage ? (c.lds_wmask >= 0 ? 2 : 1) : 0;
+  if (fs == 1) {
     if (c.vec && c.bg_thr == 0u)
-      hipLaunchKernelGGL((filter_kernel<true, false, true>), grid, block, dyn, st, c);
+      hipLaunchKernelGGL((filter_kernel<true, false, 1>), grid, block, dyn, st, c);
     else if (c.vec)
-      hipLaunchKernelGGL((filter_kernel<true, true, true>), grid, block, dyn, st, c);
+      hipLaunchKernelGGL((filter_kernel<true, true, 1>), grid, block, dyn, st, c);
     else if (c.bg_thr == 0u)
-      hipLaunchKernelGGL((filter_kernel<false, false, true>), grid, block, dyn, st, c);
+      hipLaunchKernelGGL((filter_kernel<false, false, 1>), grid, block, dyn, st, c);
     else
-      hipLaunchKernelGGL((filter_kernel<false, true, true>), grid, block, dyn, st, c);
+      hipLaunchKernelGGL((filter_kernel<false, true, 1>), grid, block, dyn, st, c);
+  } else if (fs == 2) {
+    if (c.vec && c.bg_thr == 0u)
+      hipLaunchKernelGGL((filter_kernel<true, false, 2>), grid, block, dyn, st, c);
+    else if (c.vec)
+      hipLaunchKernelGGL((filter_kernel<true, true, 2>), grid, block, dyn, st, c);
+    else if (c.bg_thr == 0u)
+      hipLaunchKernelGGL((filter_kernel<false, false, 2>), grid, block, dyn, st, c);
+    else
+      hipLaunchKernelGGL((filter_kernel<false, true, 2>), grid, block, dyn, st, c);
   } else if (c.vec && c.bg_thr == 0u) {
-    hipLaunchKernelGGL((filter_kernel<true, false, false>), grid, block, dyn, st, c);
+    hipLaunchKernelGGL((filter_kernel<true, false, 0>), grid, block, dyn, st, c);
   } else if (c.vec) {
-    hipLaunchKernelGGL((filter_kernel<true, true, false>), grid, block, dyn, st, c);
+    hipLaunchKernelGGL((filter_kernel<true, true, 0>), grid, block, dyn, st, c);
   } else if (c.bg_thr == 0u) {
-    hipLaunchKernelGGL((filter_kernel<false, false, false>), grid, block, dyn, st, c);
+    hipLaunchKernelGGL((filter_kernel<false, false, 0>), grid, block, dyn, st, c);
   } else {
-    hipLaunchKernelGGL((filter_kernel<false, true, false>), grid, block, dyn, st, c);
+    hipLaunchKernelGGL((filter_kernel<false, true, 0>), grid, block, dyn, st, c);
   }
   return hipGetLastError();
 }

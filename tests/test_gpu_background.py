@@ -17,7 +17,7 @@ pytestmark = pytest.mark.gpu
 SEED_HI = 0xF00DFACE12345678
 
 
-@pytest.mark.parametrize("name", ["c1", "c2", "c5"])
+@pytest.mark.parametrize("name", ["c1", "c2", "c4", "c5"])
 @pytest.mark.parametrize("rho,seed", [(0.05, 7), (0.5, SEED_HI), (1.0, 0)])
 def test_configs_with_background(gpu_lib, name, rho, seed):
     wl = synth.CONFIGS[name]()

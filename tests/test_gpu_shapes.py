@@ -109,12 +109,14 @@ def test_full_32_bit_keys(gpu_lib):
 
 
 @pytest.mark.parametrize("rho", [0.3, 1.0])
-def test_strided_rows_with_background(gpu_lib, rho):
+@pytest.mark.parametrize("rois", [6, 40])
+def test_strided_rows_with_background(gpu_lib, rho, rois):
     """A row stride that forbids 16-byte loads (point-by-point loads) with a
-    nonzero out-of-ROI keep rate."""
+    nonzero out-of-ROI keep rate, with one ROI word per cell (6 ROIs) and
+    with two (40 ROIs, whose cell words the filter keeps in LDS)."""
     import torch
 
-    wl = synth.small(160, frames=3, beams=7, azimuths=61, sweeps=3)
+    wl = synth.small(160, frames=3, beams=7, azimuths=61, sweeps=3, rois=rois)
     case = case_from_workload(wl)
     N = case.feat.shape[1]
     wide = np.zeros((case.feat.shape[0], N + 1), dtype=np.float32)

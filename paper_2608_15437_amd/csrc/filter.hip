@@ -22,7 +22,10 @@
 //
 // Wave k of the grid owns filter chunk k: a contiguous run of at most
 // fchunk_points points inside one frame (the chunk table and the frame of
-// every workgroup are laid out by the staging kernel).  The waves of a
+// every workgroup are laid out by the staging kernel, or, when the call's
+// frames and tables are small enough, by every workgroup for itself before
+// it stages its frame's tables into LDS from the poses, ROIs and budgets
+// directly, so that no staging kernel runs).  The waves of a
 // workgroup share the LDS copy of their frame's poses, budget masks, ROI
 // records, ROI offsets and cell map (staged once, behind the only workgroup
 // barrier) and are otherwise independent: a wave marks its kept points in

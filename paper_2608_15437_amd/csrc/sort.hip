@@ -13,25 +13,30 @@
 //
 // segments -- one workgroup: the kept-pair prefix of the filter chunks, the
 //             first pair of every frame (the prefix at its first filter
-//             chunk), and the pair chunks (at most
-//             kMaxFrameChunks per frame, whole scatter tiles, the last of a
+//             chunk), and the pair chunks (at most kMaxFrameChunks per frame,
+//             whole scatter tiles, or half tiles for frames of at most
+//             kHalfTileFramePairs pairs when the call allows; the last of a
 //             frame shorter) and the voxel tiles of the later kernels
-//             (kVoxTile pairs, the last of a frame shorter).
+//             (kVoxTile pairs, the last of a frame shorter).  For calls of
+//             at most kSmallChunks filter chunks this work is done by one
+//             more workgroup of the compaction launch instead.
 // compact  -- one workgroup per filter chunk: its kept pairs (at the start of the
 //             chunk's point range) copied to their compact place, and the
 //             kept points' records (index, x', y', z', features) written
 //             there, so the mean reads compact records instead of points.
 // Then per pass:
 // count    -- workgroup k counts the digits of pair chunk k (row k of the
-//             [chunk][digit] count matrix);
+//             [chunk][digit] count matrix; per-wave LDS histograms, four
+//             copies each for chunks of more than one tile);
 // scatter  -- the workgroup of chunk k (chunks dealt to the XCDs in
 //             contiguous blocks) sums the count rows of its frame's chunks (the
 //             frame's digit totals, and its digits in the earlier chunks:
 //             where each of its digits starts), then walks its chunk tile by
 //             tile (the next tile's
 //             pairs loading while the current one is handled): ranks each
-//             pair inside the tile (wave multi-split), reorders the tile by
-//             digit in LDS, and writes every digit's run to its place.
+//             pair inside the tile (wave multi-split; half the rounds for a
+//             chunk of at most half a tile), reorders the tile by digit in
+//             LDS, and writes every digit's run to its place.
 #include "launch.hpp"
 
 namespace mmbev {

@@ -27,9 +27,9 @@ constexpr int kMaxLdsRois = 256;      // ROI records of one filter workgroup sta
 constexpr int kMaxLdsBudgetWords = 256;
 constexpr int kMaxPoseLds = 64;       // (frame, sweep) poses of one filter workgroup staged in LDS
 constexpr int kSmallChunks = 2048;  // calls of at most this many filter chunks need no segments launch
-constexpr int kFuseFrames = kBlock - 1;
+constexpr int kFuseFrames = kBlock - 1;  // frames of a call whose point filter lays out the call itself (one per thread)
 constexpr int kFuseWideFrames = 16;    // ... and with several ROI words per cell, at most this many frames
-constexpr int kFuseWordCap = 8192;     // ... whose cells' ROI words (cells x words) fit this many LDS words  // frames of a call whose point filter lays out the call itself (one per thread)
+constexpr int kFuseWordCap = 8192;     // ... whose cells' ROI words (cells x words) fit this many LDS words
 constexpr int kMaxCellSide = 64;      // coarse BEV cells per grid side (at most 64 x 64 per frame)
 constexpr int kMaxLdsCells = 4096;    // cell words of one filter workgroup staged in LDS (16 KB)
 // radix passes (segmented by frame) and the voxel head scan

@@ -8,7 +8,9 @@ paths of the HIP library:
   them): the filter's instance that reads its tables from global memory;
 * keys of the full 32 bits (a grid of exactly 2^32 voxels: four radix
   passes of 8 bits);
-* strided rows (point-by-point loads) together with an out-of-ROI keep rate.
+* strided rows (point-by-point loads) together with an out-of-ROI keep rate;
+* the limits up to which the point filter builds its frames' tables itself
+  with several ROI words per cell (frames per call, cell words per frame).
 
 The steps are those of Alg. 1 (keep loop, Voxelize, feature encoder) and
 Eq. 6/7; structure bit for bit, features within 1e-5.
@@ -85,6 +87,26 @@ def test_many_rois_on_the_full_frame(gpu_lib):
     case.budgets = rng.integers(1, 11, 1024).astype(np.uint8)
     print("[shapes] c2 with 1024 ROIs", flush=True)
     check(gpu_lib, case, label="c2 1024 rois", desc=desc)
+
+
+@pytest.mark.parametrize("frames,nroi", [(16, 128), (17, 128), (16, 129)])
+def test_frame_tables_built_by_the_filter_at_their_limits(gpu_lib, frames, nroi):
+    """A 1440 x 1440 grid (45 x 45 coarse cells) with several ROI words per
+    cell: at 16 frames and 128 ROIs (four words, 8,100 cell words) the point
+    filter builds every frame's tables in LDS itself; one frame more, or one
+    ROI word more (10,125 cell words), and the staging kernel builds them."""
+    import oracle
+
+    wl = synth.small(170 + frames + nroi, frames=frames, beams=6, azimuths=48, sweeps=3, dims=(1440, 1440, 16),
+                     max_voxels=600, max_points=5)
+    rng = np.random.default_rng(frames * 1000 + nroi)
+    counts = [nroi] + list(rng.integers(0, nroi + 1, frames - 1))
+    desc = _random_rois(rng, sum(counts), 13.0)
+    case = case_from_workload(wl, rois=oracle.make_rois(desc))
+    case.roi_offsets = np.concatenate([[0], np.cumsum(counts)]).astype(np.int32)
+    case.budgets = rng.integers(1, 4, sum(counts)).astype(np.uint8)
+    vz, exp = check(gpu_lib, case, label=f"{frames} frames x {nroi} rois", desc=desc)
+    assert int(exp["voxel_offsets"][-1]) > 0
 
 
 @pytest.mark.parametrize("S", [80, 255])

@@ -75,9 +75,6 @@ __device__ __forceinline__ float* lds_roi(const Config& c, int k) {
 __device__ __forceinline__ uint32_t* lds_bm(const Config& c) {
   return reinterpret_cast<uint32_t*>(filter_dyn) + c.lds_bm;
 }
-__device__ __forceinline__ uint32_t* lds_cell(const Config& c) {
-  return reinterpret_cast<uint32_t*>(filter_dyn) + c.lds_cell;
-}
 
 // Per-wave state in LDS: the candidate queue (a ring) and the kept bitmap
 // of the wave's chunk.

@@ -8,7 +8,6 @@ double in the same order, so in practice they agree exactly).
 import numpy as np
 import pytest
 
-import oracle
 import synth
 from common import Case, assert_same_voxels, case_from_workload, load_golden, records
 

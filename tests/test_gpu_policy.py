@@ -2,10 +2,8 @@
 mmbev_build_rois output drives the HIP path, the oracle's selector output
 drives the oracle path, and the voxels must match bit for bit (features
 within the path's stated tolerance)."""
-import numpy as np
 import pytest
 
-import oracle
 import synth
 from common import Case, assert_same_voxels, case_from_workload
 from oracle import policy as P

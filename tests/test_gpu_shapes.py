@@ -19,7 +19,7 @@ import numpy as np
 import pytest
 
 import synth
-from common import Case, assert_same_voxels, case_from_workload
+from common import assert_same_voxels, case_from_workload
 from test_gpu_parity import FEAT_TOL, check
 
 pytestmark = pytest.mark.gpu

@@ -7,7 +7,7 @@ import numpy as np
 import pytest
 
 import synth
-from common import assert_same_voxels, case_from_workload
+from common import assert_same_voxels
 
 pytestmark = pytest.mark.gpu
 FEAT_TOL = 1e-5
